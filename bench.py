@@ -1,0 +1,231 @@
+#!/usr/bin/env python3
+"""Benchmark of the CNN forward contraction on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+                    [--out-dtype fp32|bf16] [--eager] [--no-cpu-baseline] [--all]
+
+A step is one forward convolution Out = conv(In, Ker) of the workload
+(default: the 3x3 layer Nb=32, Nc=Nk=64, 56x56 outputs, stride 1, bf16 In
+and Ker, fp32 accumulation and fp32 Out) through the C ABI (cnn_fwd), on
+inputs already resident in device memory.  The K timed steps are captured
+into one HIP graph and replayed, so host launch cost does not pace a
+kernel of a few microseconds (--eager launches each step from the host
+instead).  The timed region is bracketed by torch.cuda.synchronize().
+
+Prints ONE JSON line: the metric (conv TFLOP/s = 2 Nb Nk Nc Nr Ns Nw Nh /
+seconds per step), the roofline of the convolution kernel (HIP events on
+the stream it runs on, algorithmic bytes or flops per launch), and the fp64
+CPU oracle timed on this host as a baseline.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_TFLOPS = {"bf16": 2516.6, "f32": 157.3}   # dense MFMA, MI355X datasheet
+PEAK_HBM_GBS = 8000.0                           # HBM3E, MI355X datasheet
+DEFAULT_WORKLOAD = "conv3x3_b32"
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2105_13480_amd", "csrc")
+    for f in sorted(os.listdir(csrc)):
+        with open(os.path.join(csrc, f), "rb") as fh:
+            h.update(f.encode() + b"\0" + fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(workload: str, mode: str):
+    """HBM bytes per launch from the committed rocprofv3 counter summary,
+    if it was taken on the current kernel sources (else None)."""
+    path = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+    try:
+        with open(path) as fh:
+            data = json.load(fh)
+    except (OSError, ValueError):
+        return None
+    rec = data.get(f"{workload}/{mode}")
+    if not rec or rec.get("source_hash") != kernel_source_hash():
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def time_workload(w, mode: str, steps: int, warmup: int, eager: bool):
+    import numpy as np
+    import torch
+
+    from paper_2105_13480_amd import cnn, inputs
+
+    In, Ker = inputs.make_inputs(w)
+    if In.dtype == np.uint16:
+        dIn = torch.from_numpy(In.view(np.int16)).view(torch.bfloat16).cuda()
+        dKer = torch.from_numpy(Ker.view(np.int16)).view(torch.bfloat16).cuda()
+    else:
+        dIn, dKer = torch.from_numpy(In).cuda(), torch.from_numpy(Ker).cuda()
+    out_dt = torch.bfloat16 if mode == "bf16_obf16" else torch.float32
+    dOut = torch.empty((w.Nb, w.Nk, w.Nw, w.Nh), dtype=out_dt, device="cuda")
+    plan = cnn.plan(cnn.problem(*w.dims()), cnn.DTYPES[mode])
+
+    def step():
+        cnn.fwd(dIn, dKer, dOut, w.sw, w.sh)
+
+    for _ in range(max(warmup, 1)):
+        step()
+    torch.cuda.synchronize()
+
+    graph = None
+    if not eager:
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            for _ in range(steps):
+                step()
+        graph.replay()  # one untimed replay
+        torch.cuda.synchronize()
+
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev0.record()
+    if graph is not None:
+        graph.replay()
+    else:
+        for _ in range(steps):
+            step()
+    ev1.record()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms_per_step = (t1 - t0) * 1e3 / steps
+    kernel_ms = ev0.elapsed_time(ev1) / steps
+    del graph
+    return ms_per_step, kernel_ms, plan
+
+
+def cpu_baseline(w, budget_s: float = 10.0):
+    """fp64 oracle on this host's cores: whole workload (or a prefix of the
+    batch for large ones), repeated until about `budget_s` seconds."""
+    import oracle
+    from paper_2105_13480_amd import inputs
+
+    In, Ker = inputs.make_inputs(w)
+    per_image = w.flops / w.Nb
+    nb = w.Nb
+    # keep one pass under ~1/3 of the budget at ~10 GFLOP/s
+    while nb > 1 and per_image * nb > budget_s / 3 * 10e9:
+        nb //= 2
+    sub = In[:nb]
+    oracle.conv(sub, Ker[:1], w.sw, w.sh)  # load + warm
+    passes, t0 = 0, time.perf_counter()
+    while True:
+        oracle.conv(sub, Ker, w.sw, w.sh)
+        passes += 1
+        el = time.perf_counter() - t0
+        if el >= budget_s or passes >= 50:
+            break
+    flops = per_image * nb * passes
+    return {"value": round(flops / el / 1e12, 6), "unit": "TFLOP/s", "cores": oracle.threads(),
+            "kind": "oracle",
+            "sample": f"{nb} of {w.Nb} images of {w.name}, full Nk/Nc/spatial extent, "
+                      f"{passes} passes in {el:.1f} s (fp64 seven-loop direct convolution)"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--out-dtype", choices=["fp32", "bf16"], default="fp32")
+    ap.add_argument("--eager", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--all", action="store_true",
+                    help="also time every workload and output dtype (table on stderr)")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py: this build runs on one GPU only; the contraction shards along the "
+              "batch with no exchange, but no multi-GPU path is implemented (use --gpus 1)",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2105_13480_amd import cnn, inputs
+
+    if not torch.cuda.is_available():
+        print("bench.py: no GPU visible", file=sys.stderr)
+        sys.exit(1)
+    cnn.lib()  # fail loudly if the HIP library is missing
+
+    w = inputs.BY_NAME[args.workload]
+    mode = "f32" if w.dtype == "f32" else ("bf16" if args.out_dtype == "fp32" else "bf16_obf16")
+    ms, kms, plan = time_workload(w, mode, args.steps, args.warmup, args.eager)
+
+    prec = "f32" if mode == "f32" else "bf16"
+    tflops = w.flops / (ms * 1e-3) / 1e12
+    k_tflops = w.flops / (kms * 1e-3) / 1e12
+    alg_bytes = plan.compulsory_bytes
+    ai = w.flops / alg_bytes
+    ridge = PEAK_TFLOPS[prec] * 1e12 / (PEAK_HBM_GBS * 1e9)
+    if ai < ridge:
+        achieved = alg_bytes / (kms * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
+                "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4)}
+    else:
+        roof = {"bound": "mfma", "achieved": round(k_tflops, 2), "peak": PEAK_TFLOPS[prec],
+                "unit": "TFLOP/s", "frac": round(k_tflops / PEAK_TFLOPS[prec], 4)}
+    roof["traffic"] = measured_traffic(w.name, mode)
+    roof["algorithmic_bytes_per_launch"] = alg_bytes
+    roof["kernel_ms"] = round(kms, 5)
+
+    line = {
+        "metric": "conv TFLOP/s (2*Nb*Nk*Nc*Nr*Ns*Nw*Nh/s) + % MFMA peak, 1 MI355X",
+        "value": round(tflops, 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": prec,
+        "data": "synthetic (seeded uniform In, He-normal Ker)",
+        "config": {"workload": w.name, "Nb": w.Nb, "Nc": w.Nc, "Nk": w.Nk, "Nw": w.Nw,
+                   "Nh": w.Nh, "Nr": w.Nr, "Ns": w.Ns, "sw": w.sw, "sh": w.sh,
+                   "in_dtype": w.dtype, "acc_dtype": "f32",
+                   "out_dtype": "bf16" if mode == "bf16_obf16" else "f32",
+                   "launch": "eager" if args.eager else "hipgraph",
+                   "plan": {k: v for k, v in plan.as_dict().items()
+                            if k in ("kernel", "variant", "tk", "tp", "tc", "grid")}},
+        "pct_mfma_peak": round(100.0 * tflops / PEAK_TFLOPS[prec], 2),
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(w)
+
+    if args.all:
+        for ww in inputs.WORKLOADS:
+            for md in (["f32"] if ww.dtype == "f32" else ["bf16", "bf16_obf16"]):
+                m2, k2, p2 = time_workload(ww, md, min(args.steps, 100), 5, args.eager)
+                pr = "f32" if md == "f32" else "bf16"
+                print(f"{ww.name:18s} {md:10s} kernel {k2 * 1e3:9.2f} us  "
+                      f"{ww.flops / (k2 * 1e-3) / 1e12:8.1f} TF/s  "
+                      f"{100 * ww.flops / (k2 * 1e-3) / 1e12 / PEAK_TFLOPS[pr]:5.1f}% peak  "
+                      f"{p2.compulsory_bytes / (k2 * 1e-3) / 1e9:7.0f} GB/s  "
+                      f"plan {p2.as_dict()['kernel']} v{p2.variant} tk{p2.tk} tp{p2.tp} tc{p2.tc}",
+                      file=sys.stderr, flush=True)
+
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

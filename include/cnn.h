@@ -1,0 +1,200 @@
+/*
+ * cnn.h -- C ABI of the MI355X (gfx950) CNN forward contraction library
+ * (libcnn_mi355x.so).
+ *
+ * The operation (paper Sec. 1, the CNN equation; Listing 1 with strides):
+ *
+ *   Out[b][k][w][h] = sum_{c<Nc} sum_{r<Nr} sum_{s<Ns}
+ *                       In[b][c][sw*w + r][sh*h + s] * Ker[k][c][r][s]
+ *
+ * b < Nb batch, k < Nk output feature, c < Nc input feature, w < Nw and
+ * h < Nh output pixel, r < Nr and s < Ns stencil tap, sw / sh the strides
+ * sigma_w / sigma_h.  It is a cross-correlation (no kernel flip) with no
+ * padding ("valid"): In has exactly Nx = sw*(Nw-1)+Nr rows and
+ * Ny = sh*(Nh-1)+Ns columns per channel.
+ *
+ * Layout: every tensor is dense and row-major in the index order above
+ * (last index fastest): In[Nb][Nc][Nx][Ny], Ker[Nk][Nc][Nr][Ns],
+ * Out[Nb][Nk][Nw][Nh].  No strides, no padding arguments.
+ *
+ * Ownership: the caller owns all three buffers, which are device pointers
+ * on the current HIP device.  The library keeps no pointer after a call,
+ * never writes In or Ker, and fully overwrites Out (Out is never read, so
+ * its prior contents do not matter).  Out must not overlap In or Ker.
+ *
+ * Streams: every compute call is asynchronous on `stream` (a hipStream_t
+ * passed as void*; NULL is the null stream).  There is no implicit
+ * synchronisation; a kernel fault surfaces at the caller's next
+ * synchronisation on that stream.
+ *
+ * Errors: every function returns a cnn_status (0 = success, negative =
+ * error).  Arguments are validated before any HIP call, so an error return
+ * guarantees nothing was launched.  cnn_last_error() returns a per-thread
+ * message describing the most recent failure.  No C++ exception crosses
+ * this interface.
+ *
+ * Thread safety: all functions are reentrant; calls may be made from several
+ * host threads at once.
+ */
+#ifndef CNN_MI355X_H
+#define CNN_MI355X_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define CNN_ABI_VERSION 1
+
+/* Element types of (In, Ker) -> Out.  Accumulation is always fp32. */
+typedef enum cnn_dtype {
+  CNN_F32 = 0,        /* In, Ker, Out float32                              */
+  CNN_BF16 = 1,       /* In, Ker bfloat16; Out float32                     */
+  CNN_BF16_OBF16 = 2  /* In, Ker bfloat16; Out bfloat16 (round to nearest even) */
+} cnn_dtype;
+
+typedef enum cnn_status {
+  CNN_OK = 0,
+  CNN_E_NULL = -1,         /* a required pointer argument is NULL                  */
+  CNN_E_SHAPE = -2,        /* a size < 1 or a stride < 1                           */
+  CNN_E_DTYPE = -3,        /* unknown dtype                                        */
+  CNN_E_OVERFLOW = -4,     /* an element count does not fit the kernels' indexing  */
+  CNN_E_ALIAS = -5,        /* Out overlaps In or Ker                               */
+  CNN_E_UNSUPPORTED = -6,  /* requested kernel / tiling does not exist or does not fit */
+  CNN_E_HIP = -7,          /* a HIP runtime call failed (see cnn_last_error)       */
+  CNN_E_PLAN = -8          /* plan does not belong to this problem / dtype         */
+} cnn_status;
+
+/* Problem sizes in the paper's notation (Sec. 1). */
+typedef struct cnn_problem {
+  int64_t Nb, Nc, Nk, Nw, Nh, Nr, Ns, sw, sh;
+} cnn_problem;
+
+/* A box tiling (Listing 2): tile sizes of the b, k, c, w, h loops. */
+typedef struct cnn_tiles {
+  int64_t Tb, Tk, Tc, Tw, Th;
+} cnn_tiles;
+
+/* Kernel families. */
+typedef enum cnn_kernel {
+  CNN_K_AUTO = 0,     /* let cnn_plan choose                                          */
+  CNN_K_DIRECT = 1,   /* one thread per output, fp32 FMA; any shape (correctness path)  */
+  CNN_K_IGEMM = 2,    /* implicit GEMM on MFMA, LDS-staged halo'd In slab + Ker tile    */
+  CNN_K_POINTWISE = 3,/* 1x1 kernels (any stride): strided gather, no halo              */
+  CNN_K_SMALLC = 4    /* few input channels, wide stencils: K = (c, r, s) flattened     */
+} cnn_kernel;
+
+/*
+ * Machine budget the tile selector works against: the per-processor fast
+ * memory M of Eq. (1), split into the two stores a CU really has.
+ */
+typedef struct cnn_budget {
+  int64_t cus;          /* compute units (the paper's P processors)                 */
+  int64_t lds_bytes;    /* LDS per CU (holds the In and Ker tiles)                  */
+  int64_t acc_regs;     /* fp32 accumulator registers per lane for the Out tile     */
+  int64_t wg_per_cu;    /* workgroups the selector plans to keep resident per CU    */
+} cnn_budget;
+
+/*
+ * An execution plan.  Produced by cnn_plan (automatic choice) or
+ * cnn_plan_tiles (a requested tiling); consumed by cnn_fwd_plan.
+ *
+ * Tiles: a workgroup computes tk output features for tp consecutive outputs
+ * of the flattened (b, w, h) index (the paper's composite T_bhw), looping
+ * over all Nc input features tc at a time (Listing 3 with W_c = N_c).
+ */
+typedef struct cnn_plan_t {
+  cnn_problem prob;     /* problem the plan was made for                            */
+  int32_t dtype;        /* cnn_dtype                                                */
+  int32_t kernel;       /* cnn_kernel (never CNN_K_AUTO in a finished plan)         */
+  int32_t variant;      /* internal kernel instantiation id                         */
+  int32_t reserved;
+  int64_t tk;           /* output features per workgroup (T_k)                      */
+  int64_t tp;           /* outputs of the flattened (b,w,h) index per workgroup     */
+  int64_t tc;           /* input features per LDS stage (T_c)                       */
+  int64_t grid;         /* workgroups launched                                      */
+  int64_t lds_bytes;    /* LDS per workgroup                                        */
+  int64_t slab_rows;    /* max input rows a workgroup stages (halo included)        */
+  double eq1_elems[3];  /* Eq. (1) terms Out, Ker, In for this tiling (elements)    */
+  double eq1_bytes;     /* the same, weighted by element size, summed               */
+  double compulsory_bytes; /* |In read| + |Ker| + |Out|, each once                  */
+  double flops;         /* 2 Nb Nk Nc Nr Ns Nw Nh                                   */
+} cnn_plan_t;
+
+/*
+ * Out = conv(In, Ker) on `stream`.  Chooses (and caches) a plan with
+ * cnn_plan for the current device.  See the file header for layouts.
+ * Errors: CNN_E_NULL, CNN_E_SHAPE, CNN_E_DTYPE, CNN_E_OVERFLOW,
+ * CNN_E_ALIAS, CNN_E_HIP.
+ */
+int cnn_fwd(const void* In, const void* Ker, void* Out,
+            int64_t Nb, int64_t Nc, int64_t Nk, int64_t Nw, int64_t Nh,
+            int64_t Nr, int64_t Ns, int64_t sw, int64_t sh,
+            int dtype, void* stream);
+
+/*
+ * Tile-size selection (Sec. 2, Eq. (1)).  Evaluates the Eq. (1) data
+ * movement of every tiling the kernels implement whose footprint fits the
+ * budget, and returns the cheapest (ties and grid-fill rules are documented
+ * with the implementation).  budget == NULL queries the current HIP device.
+ * Writes *plan.  Errors: CNN_E_NULL, CNN_E_SHAPE, CNN_E_DTYPE,
+ * CNN_E_OVERFLOW, CNN_E_HIP (device query failed).
+ */
+int cnn_plan(const cnn_problem* prob, int dtype, const cnn_budget* budget,
+             cnn_plan_t* plan);
+
+/*
+ * Build the plan for a requested kernel family and tiling (tests, tuning).
+ * kernel = CNN_K_DIRECT ignores tk/tp/tc.  Returns CNN_E_UNSUPPORTED when
+ * no instantiation implements (kernel, tk, tp, tc) for this dtype or its
+ * LDS footprint exceeds the budget.  budget == NULL queries the device.
+ */
+int cnn_plan_tiles(const cnn_problem* prob, int dtype, int kernel,
+                   int64_t tk, int64_t tp, int64_t tc,
+                   const cnn_budget* budget, cnn_plan_t* plan);
+
+/*
+ * Out = conv(In, Ker) with an explicit plan.  The plan's problem and dtype
+ * must equal (*prob, dtype), else CNN_E_PLAN.  Other errors as cnn_fwd.
+ */
+int cnn_fwd_plan(const void* In, const void* Ker, void* Out,
+                 const cnn_problem* prob, int dtype, const cnn_plan_t* plan,
+                 void* stream);
+
+/*
+ * Eq. (1) of the paper for a box tiling, in elements: terms[0] = Out
+ * written once, terms[1] = Ker re-read per (b, w, h) tile, terms[2] = In
+ * (with halo) re-read per k tile.  halo_mode 0 = the formula as printed
+ * (real division, halo sigma*T + R - 1); 1 = exact (tile counts rounded up,
+ * edge tiles clipped, halo sigma*(T-1) + R).  *footprint (may be NULL)
+ * receives the left side of the Eq. (1) capacity constraint in elements,
+ * in the same halo mode.  Errors: CNN_E_NULL, CNN_E_SHAPE.
+ */
+int cnn_eq1_cost(const cnn_problem* prob, const cnn_tiles* tiles, int halo_mode,
+                 double terms[3], double* footprint);
+
+/*
+ * Eq. (1) terms (elements) of the composite tiling a plan uses: tp
+ * consecutive outputs of the flattened (b, w, h) index by tk features, each
+ * tile staging whole input rows.  Errors: CNN_E_NULL, CNN_E_SHAPE.
+ */
+int cnn_slab_cost(const cnn_problem* prob, int64_t tk, int64_t tp, double terms[3]);
+
+/* Budget of HIP device `device` (CU count, LDS per CU, accumulator regs). */
+int cnn_device_budget(int device, cnn_budget* budget);
+
+/* Static description of a status code. */
+const char* cnn_strerror(int status);
+
+/* Per-thread message of the most recent failing call ("" if none). */
+const char* cnn_last_error(void);
+
+/* CNN_ABI_VERSION of the loaded library. */
+int cnn_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CNN_MI355X_H */

@@ -1,0 +1,213 @@
+"""ctypes binding of the C ABI in include/cnn.h (libcnn_mi355x.so).
+
+Argument marshalling only: every step of the convolution runs in the HIP
+kernels of the library.  If the library has not been built this module
+raises on first use -- there is no fallback implementation.
+
+Tensor arguments are torch tensors on the GPU (device memory and the
+current stream are all torch is used for); raw device pointers can be
+passed to the ``*_ptr`` variants instead.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libcnn_mi355x.so")
+
+CNN_F32, CNN_BF16, CNN_BF16_OBF16 = 0, 1, 2
+DTYPES = {"f32": CNN_F32, "bf16": CNN_BF16, "bf16_obf16": CNN_BF16_OBF16}
+
+K_AUTO, K_DIRECT, K_IGEMM, K_POINTWISE, K_SMALLC = 0, 1, 2, 3, 4
+KERNEL_NAMES = {K_DIRECT: "direct", K_IGEMM: "igemm", K_POINTWISE: "pointwise", K_SMALLC: "smallc"}
+
+STATUS = {0: "CNN_OK", -1: "CNN_E_NULL", -2: "CNN_E_SHAPE", -3: "CNN_E_DTYPE",
+          -4: "CNN_E_OVERFLOW", -5: "CNN_E_ALIAS", -6: "CNN_E_UNSUPPORTED",
+          -7: "CNN_E_HIP", -8: "CNN_E_PLAN"}
+
+# Every symbol include/cnn.h declares.
+EXPORTS = ["cnn_fwd", "cnn_plan", "cnn_plan_tiles", "cnn_fwd_plan", "cnn_eq1_cost",
+           "cnn_slab_cost", "cnn_device_budget", "cnn_strerror", "cnn_last_error",
+           "cnn_abi_version"]
+
+i64 = ctypes.c_int64
+
+
+class Problem(ctypes.Structure):
+    _fields_ = [(n, i64) for n in ("Nb", "Nc", "Nk", "Nw", "Nh", "Nr", "Ns", "sw", "sh")]
+
+
+class Tiles(ctypes.Structure):
+    _fields_ = [(n, i64) for n in ("Tb", "Tk", "Tc", "Tw", "Th")]
+
+
+class Budget(ctypes.Structure):
+    _fields_ = [(n, i64) for n in ("cus", "lds_bytes", "acc_regs", "wg_per_cu")]
+
+
+class Plan(ctypes.Structure):
+    _fields_ = [("prob", Problem), ("dtype", ctypes.c_int32), ("kernel", ctypes.c_int32),
+                ("variant", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("tk", i64), ("tp", i64), ("tc", i64), ("grid", i64), ("lds_bytes", i64),
+                ("slab_rows", i64), ("eq1_elems", ctypes.c_double * 3),
+                ("eq1_bytes", ctypes.c_double), ("compulsory_bytes", ctypes.c_double),
+                ("flops", ctypes.c_double)]
+
+    def as_dict(self) -> dict:
+        return {"kernel": KERNEL_NAMES.get(self.kernel, str(self.kernel)), "variant": self.variant,
+                "tk": self.tk, "tp": self.tp, "tc": self.tc, "grid": self.grid,
+                "lds_bytes": self.lds_bytes, "slab_rows": self.slab_rows,
+                "eq1_elems": list(self.eq1_elems), "eq1_bytes": self.eq1_bytes,
+                "compulsory_bytes": self.compulsory_bytes, "flops": self.flops}
+
+
+class CnnError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{STATUS.get(status, status)}: {message}")
+        self.status = status
+
+
+_lib = None
+
+
+def lib():
+    """The loaded library (raises if it was not built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"HIP library missing: {LIB_PATH} "
+                           "(build it with: python -m paper_2105_13480_amd.build)")
+    L = ctypes.CDLL(LIB_PATH)
+    vp = ctypes.c_void_p
+    P, T, B, PL = (ctypes.POINTER(x) for x in (Problem, Tiles, Budget, Plan))
+    L.cnn_fwd.argtypes = [vp, vp, vp] + [i64] * 9 + [ctypes.c_int, vp]
+    L.cnn_plan.argtypes = [P, ctypes.c_int, B, PL]
+    L.cnn_plan_tiles.argtypes = [P, ctypes.c_int, ctypes.c_int, i64, i64, i64, B, PL]
+    L.cnn_fwd_plan.argtypes = [vp, vp, vp, P, ctypes.c_int, PL, vp]
+    L.cnn_eq1_cost.argtypes = [P, T, ctypes.c_int, ctypes.POINTER(ctypes.c_double),
+                               ctypes.POINTER(ctypes.c_double)]
+    L.cnn_slab_cost.argtypes = [P, i64, i64, ctypes.POINTER(ctypes.c_double)]
+    L.cnn_device_budget.argtypes = [ctypes.c_int, B]
+    L.cnn_strerror.argtypes = [ctypes.c_int]
+    L.cnn_strerror.restype = ctypes.c_char_p
+    L.cnn_last_error.argtypes = []
+    L.cnn_last_error.restype = ctypes.c_char_p
+    L.cnn_abi_version.argtypes = []
+    for f in ("cnn_fwd", "cnn_plan", "cnn_plan_tiles", "cnn_fwd_plan", "cnn_eq1_cost",
+              "cnn_slab_cost", "cnn_device_budget", "cnn_abi_version"):
+        getattr(L, f).restype = ctypes.c_int
+    _lib = L
+    return L
+
+
+def _check(status: int):
+    if status != 0:
+        raise CnnError(status, lib().cnn_last_error().decode())
+
+
+def problem(Nb, Nc, Nk, Nw, Nh, Nr, Ns, sw=1, sh=1) -> Problem:
+    return Problem(Nb, Nc, Nk, Nw, Nh, Nr, Ns, sw, sh)
+
+
+def budget(cus=256, lds_bytes=160 * 1024, acc_regs=128, wg_per_cu=2) -> Budget:
+    return Budget(cus, lds_bytes, acc_regs, wg_per_cu)
+
+
+def device_budget(device: int = 0) -> Budget:
+    b = Budget()
+    _check(lib().cnn_device_budget(device, ctypes.byref(b)))
+    return b
+
+
+def plan(prob: Problem, dtype: int, bud: Budget | None = None) -> Plan:
+    pl = Plan()
+    _check(lib().cnn_plan(ctypes.byref(prob), dtype, ctypes.byref(bud) if bud else None,
+                          ctypes.byref(pl)))
+    return pl
+
+
+def plan_tiles(prob: Problem, dtype: int, kernel: int, tk=0, tp=0, tc=0,
+               bud: Budget | None = None) -> Plan:
+    pl = Plan()
+    _check(lib().cnn_plan_tiles(ctypes.byref(prob), dtype, kernel, tk, tp, tc,
+                                ctypes.byref(bud) if bud else None, ctypes.byref(pl)))
+    return pl
+
+
+def eq1_cost(prob: Problem, tiles: Tiles, halo: int = 0):
+    """(terms[Out, Ker, In], footprint) of Eq. (1); halo 0 = printed, 1 = exact."""
+    terms = (ctypes.c_double * 3)()
+    fp = ctypes.c_double()
+    _check(lib().cnn_eq1_cost(ctypes.byref(prob), ctypes.byref(tiles), halo, terms,
+                              ctypes.byref(fp)))
+    return tuple(terms), fp.value
+
+
+def slab_cost(prob: Problem, tk: int, tp: int):
+    terms = (ctypes.c_double * 3)()
+    _check(lib().cnn_slab_cost(ctypes.byref(prob), tk, tp, terms))
+    return tuple(terms)
+
+
+# ---- compute entry points ------------------------------------------------
+
+def fwd_ptr(In: int, Ker: int, Out: int, dims, dtype: int, stream: int = 0):
+    """cnn_fwd on raw device pointers; dims = (Nb,Nc,Nk,Nw,Nh,Nr,Ns,sw,sh)."""
+    _check(lib().cnn_fwd(In, Ker, Out, *dims, dtype, stream))
+
+
+def fwd_plan_ptr(In: int, Ker: int, Out: int, prob: Problem, dtype: int, pl: Plan,
+                 stream: int = 0):
+    _check(lib().cnn_fwd_plan(In, Ker, Out, ctypes.byref(prob), dtype, ctypes.byref(pl), stream))
+
+
+def _tensor_dims(In, Ker, Out, sw, sh):
+    import torch
+    for name, t in (("In", In), ("Ker", Ker), ("Out", Out)):
+        if not t.is_cuda or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous GPU tensor")
+        if t.dim() != 4:
+            raise ValueError(f"{name} must be 4-d")
+    Nb, Nc, Nx, Ny = In.shape
+    Nk, Nc2, Nr, Ns = Ker.shape
+    if Nc2 != Nc or (Nx - Nr) % sw or (Ny - Ns) % sh or Nx < Nr or Ny < Ns:
+        raise ValueError("In extent must be sigma*(N-1)+R and channels must agree")
+    Nw, Nh = (Nx - Nr) // sw + 1, (Ny - Ns) // sh + 1
+    if tuple(Out.shape) != (Nb, Nk, Nw, Nh):
+        raise ValueError(f"Out must have shape {(Nb, Nk, Nw, Nh)}")
+    if In.dtype == torch.float32 and Ker.dtype == torch.float32 and Out.dtype == torch.float32:
+        dt = CNN_F32
+    elif In.dtype == torch.bfloat16 and Ker.dtype == torch.bfloat16:
+        if Out.dtype == torch.float32:
+            dt = CNN_BF16
+        elif Out.dtype == torch.bfloat16:
+            dt = CNN_BF16_OBF16
+        else:
+            raise ValueError("Out must be float32 or bfloat16")
+    else:
+        raise ValueError("In/Ker must both be float32 or both bfloat16")
+    return (Nb, Nc, Nk, Nw, Nh, Nr, Ns, sw, sh), dt
+
+
+def _stream(stream):
+    import torch
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    return getattr(stream, "cuda_stream", stream)
+
+
+def fwd(In, Ker, Out, sw: int = 1, sh: int = 1, stream=None):
+    """Out = conv(In, Ker) on the GPU via cnn_fwd (asynchronous on the
+    current torch stream unless ``stream`` is given)."""
+    dims, dt = _tensor_dims(In, Ker, Out, sw, sh)
+    fwd_ptr(In.data_ptr(), Ker.data_ptr(), Out.data_ptr(), dims, dt, _stream(stream))
+    return Out
+
+
+def fwd_plan(In, Ker, Out, pl: Plan, sw: int = 1, sh: int = 1, stream=None):
+    dims, dt = _tensor_dims(In, Ker, Out, sw, sh)
+    fwd_plan_ptr(In.data_ptr(), Ker.data_ptr(), Out.data_ptr(), problem(*dims), dt, pl,
+                 _stream(stream))
+    return Out

@@ -1,0 +1,288 @@
+// C ABI entry points (include/cnn.h): argument validation, plan cache,
+// dispatch to the kernels.  Every argument check happens before the first
+// HIP call, so error returns never leave work queued.
+#include <hip/hip_runtime.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <map>
+#include <mutex>
+#include <string>
+#include <tuple>
+
+#include "internal.h"
+
+namespace cnnlib {
+int select_plan(const cnn_problem& p, int dtype, const cnn_budget& bud, int kernel,
+                int64_t tk, int64_t tp, int64_t tc, cnn_plan_t* out);
+void eq1_terms(const cnn_problem& p, const cnn_tiles& t, int exact, double terms[3],
+               double* footprint);
+void slab_terms(const cnn_problem& p, int64_t tk, int64_t tp, double terms[3]);
+}  // namespace cnnlib
+
+using namespace cnnlib;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+int fail(int status, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+int fail(int status, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return status;
+}
+
+bool mul_ok(int64_t a, int64_t b, int64_t* r) { return !__builtin_mul_overflow(a, b, r); }
+
+// Shape validation and the element counts the kernels index with.
+int check_problem(const cnn_problem& p) {
+  const int64_t v[9] = {p.Nb, p.Nc, p.Nk, p.Nw, p.Nh, p.Nr, p.Ns, p.sw, p.sh};
+  static const char* names[9] = {"Nb", "Nc", "Nk", "Nw", "Nh", "Nr", "Ns", "sw", "sh"};
+  for (int i = 0; i < 9; ++i)
+    if (v[i] < 1) return fail(CNN_E_SHAPE, "%s = %lld must be >= 1", names[i], (long long)v[i]);
+  for (int i = 0; i < 9; ++i)
+    if (v[i] > 0x7fffffffLL) return fail(CNN_E_OVERFLOW, "%s = %lld exceeds 2^31-1", names[i], (long long)v[i]);
+  int64_t Nx, Ny, t;
+  if (!mul_ok(p.sw, p.Nw - 1, &t) || (Nx = t + p.Nr) > 0x7fffffffLL ||
+      !mul_ok(p.sh, p.Nh - 1, &t) || (Ny = t + p.Ns) > 0x7fffffffLL)
+    return fail(CNN_E_OVERFLOW, "input extent exceeds 2^31-1");
+  // Counts the kernels keep in 32-bit: outputs per image plane, flattened
+  // (b, w, h) outputs, input plane, flattened (b, x, y) input positions,
+  // Ker elements per feature.
+  int64_t hw = 0, npix = 0, nxny = 0, bxy = 0, kel = 0;
+  if (!mul_ok(p.Nw, p.Nh, &hw) || !mul_ok(hw, p.Nb, &npix) || npix > 0x7fffffffLL ||
+      !mul_ok(Nx, Ny, &nxny) || !mul_ok(nxny, p.Nb, &bxy) || bxy > 0x7fffffffLL ||
+      !mul_ok(p.Nc, p.Nr * p.Ns, &kel) || kel > 0x7fffffffLL || p.Nr * p.Ns > 0x7fffffffLL)
+    return fail(CNN_E_OVERFLOW, "problem exceeds 32-bit kernel indexing (outputs %lld, positions %lld)",
+                (long long)npix, (long long)bxy);
+  // Whole-tensor element counts below 2^62.
+  int64_t in_n, ker_n, out_n;
+  if (!mul_ok(bxy, p.Nc, &in_n) || in_n >= (1LL << 62) || !mul_ok(kel, p.Nk, &ker_n) ||
+      ker_n >= (1LL << 62) || !mul_ok(npix, p.Nk, &out_n) || out_n >= (1LL << 62))
+    return fail(CNN_E_OVERFLOW, "tensor element count exceeds 2^62");
+  return CNN_OK;
+}
+
+int check_dtype(int dtype) {
+  if (dtype != CNN_F32 && dtype != CNN_BF16 && dtype != CNN_BF16_OBF16)
+    return fail(CNN_E_DTYPE, "unknown dtype %d", dtype);
+  return CNN_OK;
+}
+
+void tensor_bytes(const cnn_problem& p, int dtype, int64_t* in_b, int64_t* ker_b, int64_t* out_b) {
+  const int64_t Nx = p.sw * (p.Nw - 1) + p.Nr, Ny = p.sh * (p.Nh - 1) + p.Ns;
+  *in_b = p.Nb * p.Nc * Nx * Ny * in_bytes(dtype);
+  *ker_b = p.Nk * p.Nc * p.Nr * p.Ns * in_bytes(dtype);
+  *out_b = p.Nb * p.Nk * p.Nw * p.Nh * out_bytes(dtype);
+}
+
+bool overlap(const void* a, int64_t na, const void* b, int64_t nb) {
+  const uintptr_t x = (uintptr_t)a, y = (uintptr_t)b;
+  return x < y + (uintptr_t)nb && y < x + (uintptr_t)na;
+}
+
+int check_buffers(const void* In, const void* Ker, const void* Out, const cnn_problem& p, int dtype) {
+  if (!In || !Ker || !Out) return fail(CNN_E_NULL, "In, Ker and Out must be non-NULL");
+  int64_t ib, kb, ob;
+  tensor_bytes(p, dtype, &ib, &kb, &ob);
+  if (overlap(Out, ob, In, ib) || overlap(Out, ob, Ker, kb))
+    return fail(CNN_E_ALIAS, "Out overlaps In or Ker");
+  return CNN_OK;
+}
+
+ConvArgs make_args(const cnn_plan_t& pl) {
+  const cnn_problem& p = pl.prob;
+  ConvArgs a;
+  memset(&a, 0, sizeof(a));
+  a.Nb = (int32_t)p.Nb; a.Nc = (int32_t)p.Nc; a.Nk = (int32_t)p.Nk;
+  a.Nw = (int32_t)p.Nw; a.Nh = (int32_t)p.Nh; a.Nr = (int32_t)p.Nr; a.Ns = (int32_t)p.Ns;
+  a.sw = (int32_t)p.sw; a.sh = (int32_t)p.sh;
+  a.Nx = (int32_t)(p.sw * (p.Nw - 1) + p.Nr);
+  a.Ny = (int32_t)(p.sh * (p.Nh - 1) + p.Ns);
+  a.hw = (int32_t)(p.Nw * p.Nh);
+  a.npix = (int32_t)(p.Nb * p.Nw * p.Nh);
+  a.nxny = a.Nx * a.Ny;
+  a.in_img = (int64_t)p.Nc * a.nxny;
+  a.out_total = (int64_t)a.npix * p.Nk;
+  a.tp = (int32_t)pl.tp;
+  a.tk = (int32_t)pl.tk;
+  a.tc = (int32_t)pl.tc;
+  a.n_ptiles = (int32_t)((a.npix + pl.tp - 1) / pl.tp);
+  a.n_ktiles = (int32_t)((p.Nk + pl.tk - 1) / pl.tk);
+  a.slab_max = (int32_t)pl.slab_rows;
+  a.grid = (int32_t)pl.grid;
+  return a;
+}
+
+bool same_problem(const cnn_problem& a, const cnn_problem& b) {
+  return a.Nb == b.Nb && a.Nc == b.Nc && a.Nk == b.Nk && a.Nw == b.Nw && a.Nh == b.Nh &&
+         a.Nr == b.Nr && a.Ns == b.Ns && a.sw == b.sw && a.sh == b.sh;
+}
+
+const Variant* find_variant(int id) {
+  int n = 0;
+  const Variant* vs = variants(&n);
+  for (int i = 0; i < n; ++i)
+    if (vs[i].id == id) return &vs[i];
+  return nullptr;
+}
+
+int run_plan(const void* In, const void* Ker, void* Out, const cnn_plan_t& pl, hipStream_t st) {
+  const ConvArgs a = make_args(pl);
+  hipError_t e;
+  if (pl.kernel == CNN_K_DIRECT) {
+    e = launch_direct(In, Ker, Out, a, pl.dtype, st);
+  } else {
+    const Variant* v = find_variant(pl.variant);
+    if (!v || v->kernel != pl.kernel || v->dtype != pl.dtype || v->tk != pl.tk ||
+        v->tp != pl.tp || v->tc != pl.tc)
+      return fail(CNN_E_PLAN, "plan names no matching kernel instantiation (variant %d)", pl.variant);
+    e = launch_igemm(*v, In, Ker, Out, a, pl.lds_bytes, st);
+  }
+  if (e != hipSuccess) return fail(CNN_E_HIP, "kernel launch failed: %s", hipGetErrorString(e));
+  return CNN_OK;
+}
+
+// Plan cache keyed by (problem, dtype, device).
+typedef std::tuple<int64_t, int64_t, int64_t, int64_t, int64_t, int64_t, int64_t, int64_t, int64_t, int, int> Key;
+std::mutex g_cache_mu;
+std::map<Key, cnn_plan_t> g_cache;
+
+}  // namespace
+
+extern "C" {
+
+int cnn_abi_version(void) { return CNN_ABI_VERSION; }
+
+const char* cnn_last_error(void) { return g_last_error.c_str(); }
+
+const char* cnn_strerror(int status) {
+  switch (status) {
+    case CNN_OK: return "success";
+    case CNN_E_NULL: return "NULL pointer argument";
+    case CNN_E_SHAPE: return "size or stride below 1";
+    case CNN_E_DTYPE: return "unknown dtype";
+    case CNN_E_OVERFLOW: return "problem too large for the kernels' indexing";
+    case CNN_E_ALIAS: return "Out overlaps In or Ker";
+    case CNN_E_UNSUPPORTED: return "kernel or tiling not available for this problem";
+    case CNN_E_HIP: return "HIP runtime error";
+    case CNN_E_PLAN: return "plan does not match the problem";
+    default: return "unknown status";
+  }
+}
+
+int cnn_device_budget(int device, cnn_budget* budget) {
+  if (!budget) return fail(CNN_E_NULL, "budget must be non-NULL");
+  hipDeviceProp_t prop;
+  hipError_t e = hipGetDeviceProperties(&prop, device);
+  if (e != hipSuccess) return fail(CNN_E_HIP, "hipGetDeviceProperties: %s", hipGetErrorString(e));
+  budget->cus = prop.multiProcessorCount;
+  budget->lds_bytes = (int64_t)prop.maxSharedMemoryPerMultiProcessor;
+  if (budget->lds_bytes <= 0) budget->lds_bytes = (int64_t)prop.sharedMemPerBlock;
+  budget->acc_regs = 128;
+  budget->wg_per_cu = 2;
+  return CNN_OK;
+}
+
+static int resolve_budget(const cnn_budget* in, cnn_budget* out) {
+  if (in) {
+    if (in->cus < 1 || in->lds_bytes < 1 || in->acc_regs < 1 || in->wg_per_cu < 1)
+      return fail(CNN_E_SHAPE, "budget fields must be >= 1");
+    *out = *in;
+    return CNN_OK;
+  }
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(CNN_E_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+  return cnn_device_budget(dev, out);
+}
+
+int cnn_plan_tiles(const cnn_problem* prob, int dtype, int kernel, int64_t tk, int64_t tp,
+                   int64_t tc, const cnn_budget* budget, cnn_plan_t* plan) {
+  if (!prob || !plan) return fail(CNN_E_NULL, "prob and plan must be non-NULL");
+  int st;
+  if ((st = check_problem(*prob)) || (st = check_dtype(dtype))) return st;
+  if (kernel < CNN_K_AUTO || kernel > CNN_K_SMALLC) return fail(CNN_E_UNSUPPORTED, "unknown kernel %d", kernel);
+  cnn_budget bud;
+  if ((st = resolve_budget(budget, &bud))) return st;
+  st = select_plan(*prob, dtype, bud, kernel, tk, tp, tc, plan);
+  if (st) return fail(st, "no kernel instantiation for kernel %d tk %lld tp %lld tc %lld dtype %d",
+                      kernel, (long long)tk, (long long)tp, (long long)tc, dtype);
+  return CNN_OK;
+}
+
+int cnn_plan(const cnn_problem* prob, int dtype, const cnn_budget* budget, cnn_plan_t* plan) {
+  return cnn_plan_tiles(prob, dtype, CNN_K_AUTO, 0, 0, 0, budget, plan);
+}
+
+int cnn_fwd_plan(const void* In, const void* Ker, void* Out, const cnn_problem* prob, int dtype,
+                 const cnn_plan_t* plan, void* stream) {
+  if (!prob || !plan) return fail(CNN_E_NULL, "prob and plan must be non-NULL");
+  int st;
+  if ((st = check_problem(*prob)) || (st = check_dtype(dtype))) return st;
+  if ((st = check_buffers(In, Ker, Out, *prob, dtype))) return st;
+  if (!same_problem(plan->prob, *prob) || plan->dtype != dtype)
+    return fail(CNN_E_PLAN, "plan was made for another problem or dtype");
+  return run_plan(In, Ker, Out, *plan, (hipStream_t)stream);
+}
+
+int cnn_fwd(const void* In, const void* Ker, void* Out, int64_t Nb, int64_t Nc, int64_t Nk,
+            int64_t Nw, int64_t Nh, int64_t Nr, int64_t Ns, int64_t sw, int64_t sh, int dtype,
+            void* stream) {
+  const cnn_problem p = {Nb, Nc, Nk, Nw, Nh, Nr, Ns, sw, sh};
+  int st;
+  if ((st = check_problem(p)) || (st = check_dtype(dtype))) return st;
+  if ((st = check_buffers(In, Ker, Out, p, dtype))) return st;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(CNN_E_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+  const Key key(Nb, Nc, Nk, Nw, Nh, Nr, Ns, sw, sh, dtype, dev);
+  cnn_plan_t plan;
+  bool hit = false;
+  {
+    std::lock_guard<std::mutex> g(g_cache_mu);
+    auto it = g_cache.find(key);
+    if (it != g_cache.end()) {
+      plan = it->second;
+      hit = true;
+    }
+  }
+  if (!hit) {
+    cnn_budget bud;
+    if ((st = cnn_device_budget(dev, &bud))) return st;
+    if ((st = select_plan(p, dtype, bud, CNN_K_AUTO, 0, 0, 0, &plan)))
+      return fail(st, "tile selection failed");
+    std::lock_guard<std::mutex> g(g_cache_mu);
+    g_cache[key] = plan;
+  }
+  return run_plan(In, Ker, Out, plan, (hipStream_t)stream);
+}
+
+int cnn_eq1_cost(const cnn_problem* prob, const cnn_tiles* tiles, int halo_mode, double terms[3],
+                 double* footprint) {
+  if (!prob || !tiles || !terms) return fail(CNN_E_NULL, "prob, tiles and terms must be non-NULL");
+  int st;
+  if ((st = check_problem(*prob))) return st;
+  if (tiles->Tb < 1 || tiles->Tk < 1 || tiles->Tc < 1 || tiles->Tw < 1 || tiles->Th < 1)
+    return fail(CNN_E_SHAPE, "tile sizes must be >= 1");
+  if (halo_mode != 0 && halo_mode != 1) return fail(CNN_E_SHAPE, "halo_mode must be 0 or 1");
+  eq1_terms(*prob, *tiles, halo_mode, terms, footprint);
+  return CNN_OK;
+}
+
+int cnn_slab_cost(const cnn_problem* prob, int64_t tk, int64_t tp, double terms[3]) {
+  if (!prob || !terms) return fail(CNN_E_NULL, "prob and terms must be non-NULL");
+  int st;
+  if ((st = check_problem(*prob))) return st;
+  if (tk < 1 || tp < 1) return fail(CNN_E_SHAPE, "tk and tp must be >= 1");
+  slab_terms(*prob, tk, tp, terms);
+  return CNN_OK;
+}
+
+}  // extern "C"

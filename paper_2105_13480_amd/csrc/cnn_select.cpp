@@ -1,0 +1,210 @@
+// Tile-size selection from the paper's data-movement model (Sec. 2, Eq. (1)).
+//
+// For every kernel instantiation of the requested dtype the selector
+//   1. computes the tile footprint -- the halo'd In slab and the Ker tile in
+//      LDS, the Out tile in accumulator registers (the two halves of the
+//      paper's fast memory M) -- and drops tilings that exceed the budget;
+//   2. evaluates Eq. (1) for that tiling: Out written once, Ker re-read once
+//      per (b,w,h) tile, the halo'd In slab re-read once per k tile (exact
+//      halo, edge tiles clipped), in bytes;
+//   3. turns it into a time: a CU processes ceil(tiles / slots) rounds of
+//      `slots / cus` tiles, each tile bound by its MFMA work (padded to
+//      whole MFMA blocks) or its share of the Eq. (1) traffic, whichever is
+//      larger.  This accounts for the P processors of Eq. (2) that the
+//      sequential Eq. (1) leaves out: a tiling with fewer tiles than
+//      workgroup slots leaves CUs idle however little data it moves.
+// The smallest time wins; ties go to the larger tk, then the larger tp,
+// then the larger tc, then the lower instantiation id.
+#include <math.h>
+#include <string.h>
+
+#include <algorithm>
+
+#include "internal.h"
+
+namespace cnnlib {
+
+static int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// Walk the composite tiles of tp outputs; return the largest slab and
+// (optionally) the total number of slab rows over all tiles.
+static int64_t walk_slabs(const cnn_problem& p, int64_t tp, int64_t* total_rows) {
+  const int64_t hw = p.Nw * p.Nh;
+  const int64_t npix = p.Nb * hw;
+  const int64_t Nx = p.sw * (p.Nw - 1) + p.Nr;
+  int64_t mx = 0, tot = 0;
+  for (int64_t f = 0; f < npix; f += tp) {
+    const int64_t last = std::min(f + tp, npix) - 1;
+    const int64_t b0 = f / hw, w0 = (f % hw) / p.Nh;
+    const int64_t b1 = last / hw, w1 = (last % hw) / p.Nh;
+    const int64_t S = (b1 * Nx + p.sw * w1 + p.Nr) - (b0 * Nx + p.sw * w0);
+    mx = std::max(mx, S);
+    tot += S;
+  }
+  if (total_rows) *total_rows = tot;
+  return mx;
+}
+
+int64_t slab_rows_max(const cnn_problem& p, int64_t tp) { return walk_slabs(p, tp, nullptr); }
+
+void slab_terms(const cnn_problem& p, int64_t tk, int64_t tp, double terms[3]) {
+  const int64_t npix = p.Nb * p.Nw * p.Nh;
+  const int64_t Ny = p.sh * (p.Nh - 1) + p.Ns;
+  int64_t rows = 0;
+  walk_slabs(p, tp, &rows);
+  terms[0] = (double)(npix * p.Nk);
+  terms[1] = (double)(ceil_div(npix, tp) * p.Nk * p.Nc * p.Nr * p.Ns);
+  terms[2] = (double)ceil_div(p.Nk, tk) * (double)(p.Nc * Ny) * (double)rows;
+}
+
+void eq1_terms(const cnn_problem& p, const cnn_tiles& t, int exact, double terms[3],
+               double* footprint) {
+  const double Nb = (double)p.Nb, Nc = (double)p.Nc, Nk = (double)p.Nk, Nw = (double)p.Nw,
+               Nh = (double)p.Nh, Nr = (double)p.Nr, Ns = (double)p.Ns, sw = (double)p.sw,
+               sh = (double)p.sh;
+  terms[0] = Nb * Nk * Nw * Nh;
+  if (!exact) {
+    terms[1] = Nk * Nc * Nr * Ns * Nw * Nh * Nb / ((double)t.Tw * t.Th * t.Tb);
+    terms[2] = Nb * Nc * (sw * t.Tw + Nr - 1) * (sh * t.Th + Ns - 1) * Nw * Nh * Nk /
+               ((double)t.Tw * t.Th * t.Tk);
+    if (footprint)
+      *footprint = (sw * t.Tw + Nr - 1) * (sh * t.Th + Ns - 1) * t.Tb * t.Tc +
+                   (double)t.Tw * t.Th * t.Tb * t.Tk + Nr * Ns * t.Tk * t.Tc;
+    return;
+  }
+  // Exact: ceil tile counts, clipped edge tiles, halo sigma*(T-1) + R.
+  const int64_t nb = ceil_div(p.Nb, t.Tb), nw = ceil_div(p.Nw, t.Tw), nh = ceil_div(p.Nh, t.Th);
+  terms[1] = (double)(nb * nw * nh) * (double)(p.Nk * p.Nc * p.Nr * p.Ns);
+  int64_t xs = 0, ys = 0;
+  for (int64_t i = 0; i < p.Nw; i += t.Tw) xs += p.sw * (std::min(t.Tw, p.Nw - i) - 1) + p.Nr;
+  for (int64_t i = 0; i < p.Nh; i += t.Th) ys += p.sh * (std::min(t.Th, p.Nh - i) - 1) + p.Ns;
+  terms[2] = (double)ceil_div(p.Nk, t.Tk) * (double)(p.Nc * p.Nb) * (double)xs * (double)ys;
+  if (footprint)
+    *footprint = (double)(p.sw * (t.Tw - 1) + p.Nr) * (double)(p.sh * (t.Th - 1) + p.Ns) *
+                     (double)(t.Tb * t.Tc) +
+                 (double)(t.Tw * t.Th * t.Tb * t.Tk) + (double)(p.Nr * p.Ns * t.Tk * t.Tc);
+}
+
+// MFMA throughput per CU per clock for the dtype's operand type.
+static double mfma_rate(int dtype) { return dtype == CNN_F32 ? 256.0 : 4096.0; }
+// CU <- L2 bytes per CU per clock assumed by the time model.
+static const double kL2BytesPerClk = 64.0;
+
+// Fill *plan for one implicit-GEMM variant; false if it does not fit.
+static bool eval_variant(const cnn_problem& p, int dtype, const Variant& v,
+                         const cnn_budget& bud, cnn_plan_t* plan, double* time_clk) {
+  const int64_t RS = p.Nr * p.Ns;
+  const int64_t Ny = p.sh * (p.Nh - 1) + p.Ns;
+  const int64_t npix = p.Nb * p.Nw * p.Nh;
+  const int64_t S = slab_rows_max(p, v.tp);
+  const int64_t lds = igemm_lds_bytes(v, S, Ny, RS);
+  if (lds > bud.lds_bytes || v.acc > bud.acc_regs) return false;
+  const int64_t n_p = ceil_div(npix, v.tp), n_k = ceil_div(p.Nk, v.tk);
+  const int64_t grid = n_p * n_k;
+  if (grid > 0x7fffffffLL) return false;
+  int64_t occ = bud.lds_bytes / lds;
+  occ = std::max<int64_t>(1, std::min<int64_t>(occ, bud.wg_per_cu));
+  const int64_t slots = bud.cus * occ;
+  const int64_t rounds = ceil_div(grid, slots);
+
+  double terms[3];
+  slab_terms(p, v.tk, v.tp, terms);
+  const double e_in = in_bytes(dtype), e_out = out_bytes(dtype);
+  const double bytes = e_out * terms[0] + e_in * (terms[1] + terms[2]);
+  const double tile_flops =
+      2.0 * v.tk * v.tp * (double)(ceil_div(p.Nc, v.tc) * v.tc) * (double)RS;
+  const double tile_clk =
+      std::max(tile_flops / mfma_rate(dtype), (bytes / (double)grid) / kL2BytesPerClk);
+  *time_clk = (double)rounds * (double)slots / (double)bud.cus * tile_clk;
+
+  memset(plan, 0, sizeof(*plan));
+  plan->prob = p;
+  plan->dtype = dtype;
+  plan->kernel = CNN_K_IGEMM;
+  plan->variant = v.id;
+  plan->tk = v.tk;
+  plan->tp = v.tp;
+  plan->tc = v.tc;
+  plan->grid = grid;
+  plan->lds_bytes = lds;
+  plan->slab_rows = S;
+  for (int i = 0; i < 3; ++i) plan->eq1_elems[i] = terms[i];
+  plan->eq1_bytes = bytes;
+  return true;
+}
+
+static void fill_common(const cnn_problem& p, int dtype, cnn_plan_t* plan) {
+  const int64_t Nx = p.sw * (p.Nw - 1) + p.Nr, Ny = p.sh * (p.Nh - 1) + p.Ns;
+  const double e_in = in_bytes(dtype), e_out = out_bytes(dtype);
+  // Compulsory traffic: In elements that some output reads, Ker, Out once.
+  const double rows_read = (p.sw >= p.Nr) ? (double)(p.Nw * p.Nr) : (double)Nx;
+  const double cols_read = (p.sh >= p.Ns) ? (double)(p.Nh * p.Ns) : (double)Ny;
+  plan->compulsory_bytes = e_in * ((double)(p.Nb * p.Nc) * rows_read * cols_read +
+                                   (double)(p.Nk * p.Nc * p.Nr * p.Ns)) +
+                           e_out * (double)(p.Nb * p.Nk * p.Nw * p.Nh);
+  plan->flops = 2.0 * (double)p.Nb * p.Nk * p.Nc * p.Nr * p.Ns * p.Nw * p.Nh;
+}
+
+void direct_plan(const cnn_problem& p, int dtype, cnn_plan_t* plan) {
+  memset(plan, 0, sizeof(*plan));
+  plan->prob = p;
+  plan->dtype = dtype;
+  plan->kernel = CNN_K_DIRECT;
+  plan->variant = 1;
+  plan->tk = 1;
+  plan->tp = 1;
+  plan->tc = p.Nc;
+  const int64_t out = p.Nb * p.Nk * p.Nw * p.Nh;
+  plan->grid = std::min<int64_t>((out + 255) / 256, 65536);
+  // Each thread reads its own In window and Ker row: Eq. (1) with unit tiles.
+  cnn_tiles t = {1, 1, p.Nc, 1, 1};
+  double terms[3];
+  eq1_terms(p, t, 1, terms, nullptr);
+  for (int i = 0; i < 3; ++i) plan->eq1_elems[i] = terms[i];
+  plan->eq1_bytes = out_bytes(dtype) * terms[0] + in_bytes(dtype) * (terms[1] + terms[2]);
+  fill_common(p, dtype, plan);
+}
+
+int select_plan(const cnn_problem& p, int dtype, const cnn_budget& bud, int kernel,
+                int64_t tk, int64_t tp, int64_t tc, cnn_plan_t* out) {
+  if (kernel == CNN_K_DIRECT) {
+    direct_plan(p, dtype, out);
+    return CNN_OK;
+  }
+  if (kernel != CNN_K_AUTO && kernel != CNN_K_IGEMM) return CNN_E_UNSUPPORTED;
+  int n = 0;
+  const Variant* vs = variants(&n);
+  bool found = false;
+  double best_t = 0;
+  cnn_plan_t best;
+  for (int i = 0; i < n; ++i) {
+    const Variant& v = vs[i];
+    if (v.dtype != dtype || v.kernel != CNN_K_IGEMM) continue;
+    if (kernel == CNN_K_IGEMM && (v.tk != tk || v.tp != tp || v.tc != tc)) continue;
+    cnn_plan_t cand;
+    double t;
+    if (!eval_variant(p, dtype, v, bud, &cand, &t)) continue;
+    bool better = !found || t < best_t;
+    if (found && t == best_t) {
+      if (cand.tk != best.tk) better = cand.tk > best.tk;
+      else if (cand.tp != best.tp) better = cand.tp > best.tp;
+      else if (cand.tc != best.tc) better = cand.tc > best.tc;
+      else better = cand.variant < best.variant;
+    }
+    if (better) {
+      best = cand;
+      best_t = t;
+      found = true;
+    }
+  }
+  if (!found) {
+    if (kernel != CNN_K_AUTO) return CNN_E_UNSUPPORTED;
+    direct_plan(p, dtype, out);  // no slab fits LDS: the direct kernel takes it
+    return CNN_OK;
+  }
+  fill_common(p, dtype, &best);
+  *out = best;
+  return CNN_OK;
+}
+
+}  // namespace cnnlib

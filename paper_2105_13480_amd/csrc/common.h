@@ -1,0 +1,39 @@
+// Device helpers shared by the library's kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace cnnlib {
+
+typedef uint16_t bf16_t;  // bfloat16 bit pattern (top half of an IEEE float32)
+
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ float to_f32(float x) { return x; }
+__device__ __forceinline__ float to_f32(bf16_t x) { return __uint_as_float((uint32_t)x << 16); }
+
+template <typename T> __device__ __forceinline__ T from_f32(float x);
+template <> __device__ __forceinline__ float from_f32<float>(float x) { return x; }
+// float32 -> bfloat16, round to nearest, ties to even; NaN stays a quiet NaN.
+template <> __device__ __forceinline__ bf16_t from_f32<bf16_t>(float x) {
+  uint32_t u = __float_as_uint(x);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (bf16_t)0x7fc0;
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (bf16_t)(u >> 16);
+}
+
+// The hardware hands consecutive workgroup ids to the 8 XCDs round-robin
+// (id % 8).  Renumber so that each XCD receives one contiguous run of
+// logical tiles: tiles that share input data (the k-tiles of one pixel tile)
+// then meet in the same XCD's L2.  A bijection on [0, grid).
+__device__ __forceinline__ int xcd_remap(int bid, int grid) {
+  const int q = grid >> 3, rem = grid & 7;
+  const int x = bid & 7, i = bid >> 3;
+  return x * q + (x < rem ? x : rem) + i;
+}
+
+}  // namespace cnnlib

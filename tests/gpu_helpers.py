@@ -1,0 +1,77 @@
+"""Shared helpers of the GPU tests: host<->device marshalling of the seeded
+inputs and the error metrics.  No convolution arithmetic lives here."""
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+
+from paper_2105_13480_amd import cnn, inputs
+
+TOL = {"f32": 1e-5, "bf16": 2e-2, "bf16_obf16": 2e-2}
+
+
+def say(msg: str):
+    """Name the case before each GPU step (flushed, so it survives a crash)."""
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def to_gpu(arr: np.ndarray):
+    import torch
+    if arr.dtype == np.uint16:
+        return torch.from_numpy(np.ascontiguousarray(arr).view(np.int16)).view(torch.bfloat16).cuda()
+    return torch.from_numpy(np.ascontiguousarray(arr, dtype=np.float32)).cuda()
+
+
+def out_tensor(Nb, Nk, Nw, Nh, mode: str, fill=float("nan")):
+    import torch
+    dt = torch.bfloat16 if mode == "bf16_obf16" else torch.float32
+    return torch.full((Nb, Nk, Nw, Nh), fill, dtype=dt, device="cuda")
+
+
+def to_host64(t) -> np.ndarray:
+    """Exact float64 values of a float32 or bfloat16 GPU tensor."""
+    import torch
+    if t.dtype == torch.bfloat16:
+        bits = t.view(torch.int16).cpu().numpy().view(np.uint16)
+        return inputs.bf16_bits_to_f32(bits).astype(np.float64)
+    return t.float().cpu().numpy().astype(np.float64)
+
+
+def run(In: np.ndarray, Ker: np.ndarray, sw: int, sh: int, mode: str, plan=None,
+        stream=None, fill=float("nan")):
+    """Upload, run cnn_fwd (or cnn_fwd_plan), synchronise, return float64 Out."""
+    import torch
+    Nb, Nc, Nx, Ny = In.shape
+    Nk, _, Nr, Ns = Ker.shape
+    Nw, Nh = (Nx - Nr) // sw + 1, (Ny - Ns) // sh + 1
+    dIn, dKer = to_gpu(In), to_gpu(Ker)
+    dOut = out_tensor(Nb, Nk, Nw, Nh, mode, fill)
+    if plan is None:
+        cnn.fwd(dIn, dKer, dOut, sw, sh, stream=stream)
+    else:
+        cnn.fwd_plan(dIn, dKer, dOut, plan, sw, sh, stream=stream)
+    torch.cuda.synchronize()
+    return to_host64(dOut)
+
+
+def errors(got: np.ndarray, want: np.ndarray, absv: np.ndarray):
+    """(normwise, componentwise-conditioned, pointwise) max relative errors.
+
+    normwise      max|g - o| / max|o|
+    conditioned   max|g - o| / A, A = sum |In * Ker| (rounding-error scale of
+                  any fp32 summation order); where A == 0 the error must be 0
+    pointwise     max|g - o| / |o| over |o| > 0 (reported, not gated: the
+                  zero-mean kernel makes outputs cross zero)
+    """
+    d = np.abs(got - want)
+    scale = np.abs(want).max() if want.size else 0.0
+    normwise = float(d.max() / scale) if scale > 0 else float(d.max() if d.size else 0.0)
+    pos = absv > 0
+    cond = float((d[pos] / absv[pos]).max()) if pos.any() else 0.0
+    if (~pos).any() and d[~pos].max() > 0:
+        cond = float("inf")
+    nz = np.abs(want) > 0
+    point = float((d[nz] / np.abs(want[nz])).max()) if nz.any() else 0.0
+    return normwise, cond, point

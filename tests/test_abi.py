@@ -1,0 +1,156 @@
+"""C ABI checks that need no GPU: the library loads, exports every symbol
+include/cnn.h declares, rejects bad arguments before any HIP call, and its
+host-side model (Eq. (1), composite-tile costs, tile selection) equals the
+oracle's."""
+import ctypes
+import itertools
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import eq1 as oeq1
+from oracle import select as osel
+from paper_2105_13480_amd import cnn, inputs
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared_functions():
+    text = open(os.path.join(ROOT, "include", "cnn.h")).read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\*?\s+\*?(cnn_\w+)\(", text, re.M)))
+
+
+def test_header_and_binding_agree():
+    assert _declared_functions() == sorted(cnn.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol():
+    L = cnn.lib()
+    for name in _declared_functions():
+        assert hasattr(L, name), name
+    assert L.cnn_abi_version() == 1
+
+
+def test_strerror_covers_all_codes():
+    L = cnn.lib()
+    for code in cnn.STATUS:
+        assert L.cnn_strerror(code)
+    assert L.cnn_strerror(12345) == b"unknown status"
+
+
+DIMS = (2, 3, 4, 5, 6, 3, 3, 1, 1)
+
+
+def _fwd(ptrs=(0x1000, 0x100000, 0x200000), dims=DIMS, dtype=cnn.CNN_F32):
+    return cnn.lib().cnn_fwd(*ptrs, *dims, dtype, None)
+
+
+def test_null_pointers_rejected():
+    assert _fwd(ptrs=(0, 0x100000, 0x200000)) == -1
+    assert _fwd(ptrs=(0x1000, 0, 0x200000)) == -1
+    assert _fwd(ptrs=(0x1000, 0x100000, 0)) == -1
+    assert b"non-NULL" in cnn.lib().cnn_last_error()
+
+
+@pytest.mark.parametrize("i", range(9))
+def test_sizes_below_one_rejected(i):
+    dims = list(DIMS)
+    dims[i] = 0
+    assert _fwd(dims=tuple(dims)) == -2
+    dims[i] = -3
+    assert _fwd(dims=tuple(dims)) == -2
+
+
+def test_bad_dtype_rejected():
+    assert _fwd(dtype=7) == -3
+    assert _fwd(dtype=-1) == -3
+
+
+def test_overflow_rejected():
+    assert _fwd(dims=(1 << 20, 1, 1, 1 << 10, 1 << 10, 1, 1, 1, 1)) == -4
+    assert _fwd(dims=(1, 1, 1, 1, 1, 1 << 31, 1, 1, 1)) == -4
+    assert _fwd(dims=(1, 1, 1, 1 << 20, 1, 1, 1, 1 << 12, 1)) == -4
+
+
+def test_alias_rejected():
+    # Out = [0x200000, +2*4*5*6*4 bytes); In covers 2*3*7*8*4 bytes from its base
+    assert _fwd(ptrs=(0x200000 - 8, 0x100000, 0x200000)) == -5
+    assert _fwd(ptrs=(0x1000, 0x200000 + 16, 0x200000)) == -5
+    assert b"overlaps" in cnn.lib().cnn_last_error()
+
+
+def test_fwd_plan_rejects_foreign_plan():
+    p = cnn.problem(*DIMS)
+    pl = cnn.plan(p, cnn.CNN_F32, cnn.budget())
+    q = cnn.problem(2, 3, 4, 5, 6, 3, 3, 1, 2)
+    st = cnn.lib().cnn_fwd_plan(0x1000, 0x100000, 0x200000, ctypes.byref(q), cnn.CNN_F32,
+                                ctypes.byref(pl), None)
+    assert st == -8
+    st = cnn.lib().cnn_fwd_plan(0x1000, 0x100000, 0x200000, ctypes.byref(p), cnn.CNN_BF16,
+                                ctypes.byref(pl), None)
+    assert st == -8
+
+
+def test_plan_tiles_unknown_tiling_unsupported():
+    p = cnn.problem(*DIMS)
+    with pytest.raises(cnn.CnnError) as e:
+        cnn.plan_tiles(p, cnn.CNN_F32, cnn.K_IGEMM, 64, 96, 8, cnn.budget())
+    assert e.value.status == -6
+
+
+def _problems():
+    rng = np.random.default_rng(21)
+    out = [oeq1.Problem(*w.dims()) for w in inputs.WORKLOADS]
+    for _ in range(25):
+        Nr, Ns = rng.integers(1, 6, size=2)
+        out.append(oeq1.Problem(int(rng.integers(1, 5)), int(rng.integers(1, 40)),
+                                int(rng.integers(1, 300)), int(rng.integers(1, 30)),
+                                int(rng.integers(1, 30)), int(Nr), int(Ns),
+                                int(rng.integers(1, 4)), int(rng.integers(1, 4))))
+    return out
+
+
+@pytest.mark.parametrize("halo", [0, 1])
+def test_eq1_matches_oracle(halo):
+    rng = np.random.default_rng(5)
+    for p in _problems():
+        for _ in range(4):
+            t = oeq1.Tiles(*(int(rng.integers(1, n + 1)) for n in (p.Nb, p.Nk, p.Nc, p.Nw, p.Nh)))
+            terms, fp = cnn.eq1_cost(cnn.problem(*p.__dict__.values()), cnn.Tiles(*t.__dict__.values()), halo)
+            want = oeq1.eq1_terms(p, t, "exact" if halo else "paper")
+            wfp = oeq1.eq1_footprint(p, t, "exact" if halo else "paper")
+            if halo:
+                assert terms == tuple(float(x) for x in want) and fp == wfp
+            else:
+                np.testing.assert_allclose(terms, want, rtol=1e-13)
+                np.testing.assert_allclose(fp, wfp, rtol=1e-13)
+
+
+def test_slab_cost_matches_oracle():
+    for p in _problems():
+        for tk, tp in [(32, 32), (64, 256), (256, 128), (7, 50)]:
+            got = cnn.slab_cost(cnn.problem(*p.__dict__.values()), tk, tp)
+            assert got == tuple(float(x) for x in oeq1.slab_terms(p, tk, tp))
+
+
+@pytest.mark.parametrize("dtype", [0, 1, 2])
+def test_selector_matches_oracle(dtype):
+    for p in _problems():
+        for bud in [(256, 160 * 1024, 128, 2), (64, 64 * 1024, 64, 1), (8, 160 * 1024, 128, 2)]:
+            pl = cnn.plan(cnn.problem(*p.__dict__.values()), dtype, cnn.budget(*bud))
+            want = osel.choose(p, dtype, *bud)
+            assert (pl.kernel, pl.variant, pl.tk, pl.tp, pl.tc) == want, (p, bud)
+
+
+def test_plan_reports_eq1_and_compulsory_bytes():
+    w = inputs.BY_NAME["conv3x3_b32"]
+    p = oeq1.Problem(*w.dims())
+    pl = cnn.plan(cnn.problem(*w.dims()), cnn.CNN_BF16, cnn.budget())
+    o, k, i = oeq1.slab_terms(p, pl.tk, pl.tp)
+    assert tuple(pl.eq1_elems) == (o, k, i)
+    assert pl.eq1_bytes == 4 * o + 2 * (k + i)
+    comp = 2 * (w.Nb * w.Nc * w.Nx * w.Ny + w.Nk * w.Nc * 9) + 4 * w.Nb * w.Nk * w.Nw * w.Nh
+    assert pl.compulsory_bytes == comp
+    assert pl.flops == w.flops

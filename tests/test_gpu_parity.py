@@ -1,0 +1,158 @@
+"""GPU parity: the HIP path (through the C ABI) against the fp64 oracle.
+
+Bars: fp32 max relative error 1e-5, bf16 inputs with fp32 accumulation 2e-2,
+both normwise and componentwise-conditioned (see gpu_helpers.errors).
+Integer inputs make every fp32 partial sum exact, so those cases must match
+the oracle bit for bit; a delta kernel must reproduce a strided copy of In
+bit for bit.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from oracle import select as osel
+from paper_2105_13480_amd import cnn, inputs
+
+from gpu_helpers import TOL, errors, run, say, to_gpu, out_tensor, to_host64
+
+pytestmark = pytest.mark.gpu
+
+MODES = {"f32": cnn.CNN_F32, "bf16": cnn.CNN_BF16, "bf16_obf16": cnn.CNN_BF16_OBF16}
+
+
+def _arrays(dims, mode, seed, dist=("uniform", -1.0, 1.0), kdist=("he",)):
+    return inputs.make_arrays(*dims, "f32" if mode == "f32" else "bf16",
+                              seed_in=seed, seed_ker=seed + 1, in_dist=dist, ker_dist=kdist)
+
+
+# ---- mid-size problems: whole output compared element by element ---------
+MID = [
+    (3, 40, 70, 13, 11, 3, 3, 1, 1),     # ragged everywhere
+    (2, 37, 33, 9, 14, 3, 2, 2, 1),      # Nr != Ns, sw != sh
+    (1, 64, 96, 20, 20, 3, 3, 2, 2),
+    (4, 17, 5, 7, 7, 5, 5, 1, 1),
+    (3, 70, 130, 10, 10, 1, 1, 1, 1),    # 1x1
+    (2, 48, 40, 9, 8, 1, 1, 2, 2),       # 1x1 stride 2
+    (2, 3, 64, 30, 30, 7, 7, 2, 2),      # stem-like, few channels
+    (1, 1, 1, 1, 1, 1, 1, 1, 1),         # degenerate
+    (1, 1, 1, 5, 3, 4, 2, 3, 1),
+    (5, 2, 3, 1, 9, 1, 3, 1, 2),
+]
+
+
+@pytest.mark.parametrize("mode", list(MODES))
+@pytest.mark.parametrize("dims", MID)
+def test_mid_size_auto_plan(dims, mode):
+    say(f"[parity] auto plan dims={dims} mode={mode}")
+    In, Ker = _arrays(dims, mode, seed=sum(dims))
+    sw, sh = dims[7], dims[8]
+    got = run(In, Ker, sw, sh, mode)
+    want, absv = oracle.conv(In, Ker, sw, sh, with_abs=True)
+    nw, cond, _ = errors(got, want, absv)
+    assert nw <= TOL[mode] and cond <= TOL[mode], (nw, cond)
+
+
+def _variant_rows(dtype):
+    return [r for r in osel.IGEMM if r[1] == dtype]
+
+
+@pytest.mark.parametrize("row", _variant_rows(0) + _variant_rows(1) + _variant_rows(2),
+                         ids=lambda r: f"v{r[0]}")
+def test_every_igemm_variant_exact_integers(row):
+    vid, dt, wm, wn, mb, nb, tc = row
+    tk, tp = 32 * wm * mb, 32 * wn * nb
+    mode = {0: "f32", 1: "bf16", 2: "bf16_obf16"}[dt]
+    # spans several tiles with ragged pixel, feature and channel tails
+    dims = (3, tc + 5, tk + 7, 9, 13, 3, 3, 1, 2)
+    In, Ker = _arrays(dims, mode, seed=vid, dist=("int", -2, 2), kdist=("int", -2, 2))
+    pl = cnn.plan_tiles(cnn.problem(*dims), dt, cnn.K_IGEMM, tk, tp, tc)
+    say(f"[parity] variant {vid} tk={tk} tp={tp} tc={tc} dims={dims} grid={pl.grid}")
+    got = run(In, Ker, dims[7], dims[8], mode, plan=pl)
+    want = oracle.conv(In, Ker, dims[7], dims[8])
+    if mode == "bf16_obf16":
+        want = inputs.bf16_bits_to_f32(inputs.f32_to_bf16_bits(want.astype(np.float32))).astype(np.float64)
+    assert np.array_equal(got, want)
+
+
+@pytest.mark.parametrize("mode", list(MODES))
+def test_direct_kernel_exact_integers(mode):
+    dims = (2, 7, 9, 11, 6, 3, 2, 2, 1)
+    In, Ker = _arrays(dims, mode, seed=3, dist=("int", -2, 2), kdist=("int", -2, 2))
+    pl = cnn.plan_tiles(cnn.problem(*dims), MODES[mode], cnn.K_DIRECT)
+    say(f"[parity] direct kernel dims={dims} mode={mode}")
+    got = run(In, Ker, dims[7], dims[8], mode, plan=pl)
+    want = oracle.conv(In, Ker, dims[7], dims[8])
+    if mode == "bf16_obf16":
+        want = inputs.bf16_bits_to_f32(inputs.f32_to_bf16_bits(want.astype(np.float32))).astype(np.float64)
+    assert np.array_equal(got, want)
+
+
+@pytest.mark.parametrize("kernel", ["auto", "direct"])
+@pytest.mark.parametrize("mode", ["f32", "bf16"])
+@pytest.mark.parametrize("geom", [(3, 3, 1, 1), (3, 2, 2, 1), (1, 1, 2, 2), (7, 7, 2, 2)])
+def test_delta_kernel_is_strided_copy(geom, mode, kernel):
+    """Ker[k,c,r,s] = [c == k mod Nc][r == r0][s == s0] copies In exactly."""
+    Nr, Ns, sw, sh = geom
+    Nb, Nc, Nk, Nw, Nh = 2, 5, 11, 9, 7
+    dims = (Nb, Nc, Nk, Nw, Nh, Nr, Ns, sw, sh)
+    In, _ = _arrays(dims, mode, seed=31)
+    for r0, s0 in [(0, 0), (Nr - 1, Ns - 1), (Nr // 2, 0)]:
+        Ker32 = np.zeros((Nk, Nc, Nr, Ns), dtype=np.float32)
+        for k in range(Nk):
+            Ker32[k, k % Nc, r0, s0] = 1.0
+        Ker = Ker32 if mode == "f32" else inputs.f32_to_bf16_bits(Ker32)
+        pl = None
+        if kernel == "direct":
+            pl = cnn.plan_tiles(cnn.problem(*dims), MODES[mode], cnn.K_DIRECT)
+        say(f"[parity] delta kernel geom={geom} r0={r0} s0={s0} mode={mode} kernel={kernel}")
+        got = run(In, Ker, sw, sh, mode, plan=pl)
+        In64 = oracle.widen(In)
+        for k in range(Nk):
+            want = In64[:, k % Nc, r0::sw, s0::sh][:, :Nw, :Nh]
+            assert np.array_equal(got[:, k], want)
+
+
+def test_out_is_overwritten_not_read():
+    dims = (2, 9, 33, 6, 7, 3, 3, 1, 1)
+    In, Ker = _arrays(dims, "bf16", seed=41)
+    say("[parity] Out prefilled with NaN and with 1e30")
+    a = run(In, Ker, 1, 1, "bf16", fill=float("nan"))
+    b = run(In, Ker, 1, 1, "bf16", fill=1e30)
+    assert np.isfinite(a).all() and np.array_equal(a, b)
+
+
+def test_repeatable_bitwise():
+    w = inputs.BY_NAME["conv3x3_b32"]
+    dims = (4,) + w.dims()[1:]
+    In, Ker = _arrays(dims, "bf16", seed=43)
+    say(f"[parity] run twice dims={dims}")
+    a = run(In, Ker, 1, 1, "bf16")
+    b = run(In, Ker, 1, 1, "bf16")
+    assert np.array_equal(a, b)
+
+
+def test_nondefault_stream():
+    import torch
+    dims = (2, 16, 40, 12, 12, 3, 3, 1, 1)
+    In, Ker = _arrays(dims, "bf16", seed=47)
+    s = torch.cuda.Stream()
+    say("[parity] launch on a side stream")
+    with torch.cuda.stream(s):
+        got = run(In, Ker, 1, 1, "bf16", stream=s)
+    want, absv = oracle.conv(In, Ker, 1, 1, with_abs=True)
+    nw, cond, _ = errors(got, want, absv)
+    assert nw <= TOL["bf16"] and cond <= TOL["bf16"]
+
+
+def test_bad_arguments_raise_before_launch():
+    import torch
+    dims = (1, 2, 3, 4, 4, 3, 3, 1, 1)
+    In, Ker = _arrays(dims, "f32", seed=1)
+    dIn, dKer = to_gpu(In), to_gpu(Ker)
+    out = out_tensor(1, 3, 4, 4, "f32")
+    with pytest.raises(cnn.CnnError) as e:
+        cnn.fwd_ptr(dIn.data_ptr(), dKer.data_ptr(), dIn.data_ptr(), dims, cnn.CNN_F32)
+    assert e.value.status == -5
+    with pytest.raises(cnn.CnnError):
+        cnn.fwd_ptr(dIn.data_ptr(), dKer.data_ptr(), out.data_ptr(), dims, 9)
+    torch.cuda.synchronize()
