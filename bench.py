@@ -3,6 +3,7 @@
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
                     [--out-dtype fp32|bf16] [--eager] [--no-cpu-baseline] [--all]
+                    [--plan KERNEL:TK:TP:TC] [--copy-bytes N]
 
 A step is one forward convolution Out = conv(In, Ker) of the workload
 (default: the 3x3 layer Nb=32, Nc=Nk=64, 56x56 outputs, stride 1, bf16 In
@@ -58,7 +59,42 @@ def measured_traffic(workload: str, mode: str):
     return rec.get("hbm_bytes_per_launch")
 
 
-def time_workload(w, mode: str, steps: int, warmup: int, eager: bool):
+KERNELS = {"direct": 1, "igemm": 2, "igemm_pipe": 5, "igemm_dma": 6, "igemm_wide": 7}
+
+
+def forced_plan(spec: str, w, mode: str):
+    """Plan for --plan KERNEL[:TK:TP:TC] (e.g. igemm_pipe:64:256:16)."""
+    from paper_2105_13480_amd import cnn
+    parts = spec.split(":")
+    kern = KERNELS[parts[0]]
+    tk, tp, tc = (int(x) for x in parts[1:4]) if len(parts) == 4 else (0, 0, 0)
+    return cnn.plan_tiles(cnn.problem(*w.dims()), cnn.DTYPES[mode], kern, tk, tp, tc)
+
+
+def copy_calibration(nbytes: int, steps: int):
+    """Device-to-device copy of a known size (torch), for scaling the HBM
+    byte counters of rocprofv3 (FETCH_SIZE / WRITE_SIZE)."""
+    import torch
+    n = nbytes // 4
+    a = torch.ones(n, dtype=torch.float32, device="cuda")
+    b = torch.empty_like(a)
+    for _ in range(3):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    ev0.record()
+    for _ in range(steps):
+        b.copy_(a)
+    ev1.record()
+    torch.cuda.synchronize()
+    ms = ev0.elapsed_time(ev1) / steps
+    print(json.dumps({"copy_bytes": n * 4, "ms_per_copy": round(ms, 5),
+                      "GB_per_s_read_plus_write": round(2 * n * 4 / (ms * 1e-3) / 1e9, 1)}),
+          flush=True)
+
+
+def time_workload(w, mode: str, steps: int, warmup: int, eager: bool, plan_spec: str = ""):
     import numpy as np
     import torch
 
@@ -72,11 +108,23 @@ def time_workload(w, mode: str, steps: int, warmup: int, eager: bool):
         dIn, dKer = torch.from_numpy(In).cuda(), torch.from_numpy(Ker).cuda()
     out_dt = torch.bfloat16 if mode == "bf16_obf16" else torch.float32
     dOut = torch.empty((w.Nb, w.Nk, w.Nw, w.Nh), dtype=out_dt, device="cuda")
-    plan = cnn.plan(cnn.problem(*w.dims()), cnn.DTYPES[mode])
+    if plan_spec:
+        plan = forced_plan(plan_spec, w, mode)
 
-    def step():
-        cnn.fwd(dIn, dKer, dOut, w.sw, w.sh)
+        def step():
+            cnn.fwd_plan(dIn, dKer, dOut, plan, w.sw, w.sh)
+    else:
+        plan = cnn.plan(cnn.problem(*w.dims()), cnn.DTYPES[mode])
 
+        def step():
+            cnn.fwd(dIn, dKer, dOut, w.sw, w.sh)
+
+    # Warm up on the stream that is then captured: the library keeps its
+    # workspace per stream and cannot allocate during capture.
+    cap_stream = torch.cuda.Stream()
+    with torch.cuda.stream(cap_stream):
+        for _ in range(max(warmup, 1)):
+            step()
     for _ in range(max(warmup, 1)):
         step()
     torch.cuda.synchronize()
@@ -84,7 +132,7 @@ def time_workload(w, mode: str, steps: int, warmup: int, eager: bool):
     graph = None
     if not eager:
         graph = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(graph):
+        with torch.cuda.graph(graph, stream=cap_stream):
             for _ in range(steps):
                 step()
         graph.replay()  # one untimed replay
@@ -148,6 +196,10 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--all", action="store_true",
                     help="also time every workload and output dtype (table on stderr)")
+    ap.add_argument("--plan", default="",
+                    help="force a tiling, KERNEL[:TK:TP:TC] with KERNEL in direct/igemm/igemm_pipe")
+    ap.add_argument("--copy-bytes", type=int, default=0,
+                    help="only time a device copy of this many bytes (counter calibration)")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -164,10 +216,13 @@ def main():
         print("bench.py: no GPU visible", file=sys.stderr)
         sys.exit(1)
     cnn.lib()  # fail loudly if the HIP library is missing
+    if args.copy_bytes:
+        copy_calibration(args.copy_bytes, args.steps)
+        return
 
     w = inputs.BY_NAME[args.workload]
     mode = "f32" if w.dtype == "f32" else ("bf16" if args.out_dtype == "fp32" else "bf16_obf16")
-    ms, kms, plan = time_workload(w, mode, args.steps, args.warmup, args.eager)
+    ms, kms, plan = time_workload(w, mode, args.steps, args.warmup, args.eager, args.plan)
 
     prec = "f32" if mode == "f32" else "bf16"
     tflops = w.flops / (ms * 1e-3) / 1e12

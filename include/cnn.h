@@ -80,9 +80,17 @@ typedef struct cnn_tiles {
 typedef enum cnn_kernel {
   CNN_K_AUTO = 0,     /* let cnn_plan choose                                          */
   CNN_K_DIRECT = 1,   /* one thread per output, fp32 FMA; any shape (correctness path)  */
-  CNN_K_IGEMM = 2,    /* implicit GEMM on MFMA, LDS-staged halo'd In slab + Ker tile    */
+  CNN_K_IGEMM = 2,    /* implicit GEMM on MFMA, LDS-staged halo'd In slab + Ker tile,
+                         element-wise staging (any dtype; fallback of CNN_K_IGEMM_PIPE) */
   CNN_K_POINTWISE = 3,/* 1x1 kernels (any stride): strided gather, no halo              */
-  CNN_K_SMALLC = 4    /* few input channels, wide stencils: K = (c, r, s) flattened     */
+  CNN_K_SMALLC = 4,   /* few input channels, wide stencils: K = (c, r, s) flattened     */
+  CNN_K_IGEMM_PIPE = 5,/* implicit GEMM, bf16: repacked Ker streamed by DMA, In staged
+                         through registers, both double-buffered in LDS               */
+  CNN_K_IGEMM_DMA = 6,/* implicit GEMM, bf16: Ker and the natural In rows both copied
+                         by 16-byte DMA into a ring of LDS buffers, In transposed in LDS */
+  CNN_K_IGEMM_WIDE = 7/* implicit GEMM, bf16: In staged as 8x8 (position x channel)
+                         blocks of 16-byte loads transposed in registers, swizzled LDS,
+                         MFMA operands prefetched one K-step ahead                  */
 } cnn_kernel;
 
 /*
@@ -116,6 +124,8 @@ typedef struct cnn_plan_t {
   int64_t grid;         /* workgroups launched                                      */
   int64_t lds_bytes;    /* LDS per workgroup                                        */
   int64_t slab_rows;    /* max input rows a workgroup stages (halo included)        */
+  int64_t ws_bytes;     /* device workspace the plan needs (repacked Ker); the
+                           library allocates it per (device, stream) on first use */
   double eq1_elems[3];  /* Eq. (1) terms Out, Ker, In for this tiling (elements)    */
   double eq1_bytes;     /* the same, weighted by element size, summed               */
   double compulsory_bytes; /* |In read| + |Ker| + |Out|, each once                  */
@@ -161,6 +171,24 @@ int cnn_plan_tiles(const cnn_problem* prob, int dtype, int kernel,
 int cnn_fwd_plan(const void* In, const void* Ker, void* Out,
                  const cnn_problem* prob, int dtype, const cnn_plan_t* plan,
                  void* stream);
+
+/*
+ * As cnn_fwd_plan, with a caller-provided device workspace of ws_bytes
+ * bytes (at least plan->ws_bytes, 16-byte aligned; NULL allowed when
+ * plan->ws_bytes is 0).  The library then allocates nothing, so this form
+ * may be used while the stream is being captured into a HIP graph.  The
+ * workspace must not be used by another call that may run concurrently.
+ * Errors: as cnn_fwd_plan, and CNN_E_SHAPE if the workspace is too small or
+ * misaligned.
+ *
+ * cnn_fwd and cnn_fwd_plan keep one workspace per (device, stream),
+ * allocated on the first call that needs it (or a larger one); during
+ * stream capture they cannot allocate and return CNN_E_UNSUPPORTED if the
+ * stream has no large enough workspace yet.
+ */
+int cnn_fwd_plan_ws(const void* In, const void* Ker, void* Out,
+                    const cnn_problem* prob, int dtype, const cnn_plan_t* plan,
+                    void* workspace, int64_t ws_bytes, void* stream);
 
 /*
  * Eq. (1) of the paper for a box tiling, in elements: terms[0] = Out

@@ -21,6 +21,22 @@ with slots = cus * min(wg_per_cu, floor(lds / footprint)), tile_flops the
 MFMA work of one tile padded to whole blocks, mfma_rate 4096 (bf16) or
 256 (fp32) flops per CU per clock, 64 bytes per CU per clock from L2.
 Lowest time wins; ties go to larger tk, then tp, then tc, then lower id.
+
+Two implicit-GEMM families are ranked in tiers.  Tier 1 (the pipelined
+bf16 kernel) double-buffers both LDS tiles: footprint
+2 * 16 * (tc/8 * even(S*Ny) + blk), blk = RS * tc/8 * tk vectors rounded up
+to a multiple of 256; it also needs its stencil to match a compile-time
+one (or be generic), ceil(S*Ny/2) <= 256 * maxp slab position pairs, and
+(tp // (Nw*Nh) + 2) images to span < 2^31 bytes of In and of Out.
+Tier 0 holds the wide-staging bf16 kernel -- footprint
+2 * 16 * (tc/8 * ceil8(S*Ny) + blk), tc/8 * ceil(S*Ny/8) <= 256*maxi items,
+the same 2^31-byte span rule as below -- and the DMA-staged bf16 kernel:
+footprint
+16 * (tc/8 * S*Ny + nbuf * 256 * (ndi + ndk)); it needs tc*S*nbr <= 256*ndi
+natural-copy blocks (nbr = (Ny + 14) // 8 per row), RS*tc/8*tk <= 256*ndk Ker
+vectors, S*Ny <= 256*mpos positions, and (imgs*Nc + tc) input planes and imgs
+output images to span < 2^31 bytes.  Each later tier is ranked only if no
+candidate of the earlier tiers fits; tier 2 (the plain staging kernel) last.
 If nothing fits, the direct kernel is used.
 """
 from __future__ import annotations
@@ -46,21 +62,137 @@ IGEMM = [
 ]
 
 
+# (id, dtype, wm, wn, mb, nb, tc, nr, ns, maxp) of the pipelined kernel.
+IGEMM2 = [
+    (400, BF16, 1, 4, 2, 2, 16, 3, 3, 3), (401, BF16, 2, 2, 2, 2, 16, 3, 3, 3),
+    (402, BF16, 2, 2, 2, 4, 16, 3, 3, 3), (404, BF16, 1, 4, 2, 2, 32, 3, 3, 2),
+    (410, BF16, 1, 4, 2, 2, 16, 0, 0, 4), (411, BF16, 2, 2, 2, 4, 16, 0, 0, 4),
+    (412, BF16, 4, 1, 2, 4, 16, 0, 0, 4),
+    (500, BF16_OBF16, 1, 4, 2, 2, 16, 3, 3, 3), (501, BF16_OBF16, 2, 2, 2, 2, 16, 3, 3, 3),
+    (502, BF16_OBF16, 2, 2, 2, 4, 16, 3, 3, 3), (504, BF16_OBF16, 1, 4, 2, 2, 32, 3, 3, 2),
+    (510, BF16_OBF16, 1, 4, 2, 2, 16, 0, 0, 4), (511, BF16_OBF16, 2, 2, 2, 4, 16, 0, 0, 4),
+    (512, BF16_OBF16, 4, 1, 2, 4, 16, 0, 0, 4),
+]
+
+
+# (id, dtype, wm, wn, mb, nb, tc, nr, ns, nbuf, ndi, ndk, mpos) of the
+# DMA-staged kernel.
+IGEMM3 = [
+    (600, BF16, 1, 4, 2, 2, 16, 3, 3, 3, 6, 5, 3),
+    (602, BF16, 2, 2, 2, 2, 16, 3, 3, 2, 7, 9, 3), (603, BF16, 2, 2, 2, 4, 16, 3, 3, 2, 6, 9, 3),
+    (610, BF16, 1, 4, 2, 2, 16, 0, 0, 3, 4, 1, 2), (611, BF16, 2, 2, 2, 4, 16, 0, 0, 3, 4, 2, 2),
+    (612, BF16, 4, 1, 2, 4, 16, 0, 0, 3, 4, 2, 2), (613, BF16, 1, 4, 2, 1, 16, 0, 0, 2, 6, 13, 4),
+    (700, BF16_OBF16, 1, 4, 2, 2, 16, 3, 3, 3, 6, 5, 3),
+    (702, BF16_OBF16, 2, 2, 2, 2, 16, 3, 3, 2, 7, 9, 3),
+    (703, BF16_OBF16, 2, 2, 2, 4, 16, 3, 3, 2, 6, 9, 3),
+    (710, BF16_OBF16, 1, 4, 2, 2, 16, 0, 0, 3, 4, 1, 2),
+    (711, BF16_OBF16, 2, 2, 2, 4, 16, 0, 0, 3, 4, 2, 2),
+    (712, BF16_OBF16, 4, 1, 2, 4, 16, 0, 0, 3, 4, 2, 2),
+    (713, BF16_OBF16, 1, 4, 2, 1, 16, 0, 0, 2, 6, 13, 4),
+]
+
+
+# (id, dtype, wm, wn, mb, nb, tc, nr, ns, maxi) of the wide-staging kernel.
+IGEMM4 = [
+    (800, BF16, 1, 4, 2, 2, 16, 3, 3, 1), (801, BF16, 1, 4, 2, 2, 32, 3, 3, 2),
+    (802, BF16, 2, 2, 2, 4, 16, 3, 3, 2), (803, BF16, 2, 2, 2, 2, 16, 3, 3, 1),
+    (810, BF16, 4, 1, 2, 4, 32, 1, 1, 1), (811, BF16, 2, 2, 2, 4, 32, 1, 1, 1),
+    (812, BF16, 4, 1, 2, 4, 64, 1, 1, 1), (820, BF16, 1, 4, 2, 2, 16, 0, 0, 2),
+    (900, BF16_OBF16, 1, 4, 2, 2, 16, 3, 3, 1), (901, BF16_OBF16, 1, 4, 2, 2, 32, 3, 3, 2),
+    (902, BF16_OBF16, 2, 2, 2, 4, 16, 3, 3, 2), (903, BF16_OBF16, 2, 2, 2, 2, 16, 3, 3, 1),
+    (910, BF16_OBF16, 4, 1, 2, 4, 32, 1, 1, 1), (911, BF16_OBF16, 2, 2, 2, 4, 32, 1, 1, 1),
+    (912, BF16_OBF16, 4, 1, 2, 4, 64, 1, 1, 1), (920, BF16_OBF16, 1, 4, 2, 2, 16, 0, 0, 2),
+]
+
+
 def _max_slab(p: eq1.Problem, tp: int) -> int:
     n = p.Nb * p.Nw * p.Nh
     return max(eq1.slab_rows(p, f, min(f + tp, n) - 1) for f in range(0, n, tp))
 
 
-def candidates(p: eq1.Problem, dtype: int, cus: int, lds_bytes: int, acc_regs: int,
-               wg_per_cu: int):
-    """Yield (time, tk, tp, tc, id, info) for every feasible candidate."""
+def _cost(p, dtype, tk, tp, tc, lds, cus, lds_bytes, wg_per_cu):
     e_in = 4 if dtype == F32 else 2
     e_out = 2 if dtype == BF16_OBF16 else 4
-    kv = 1 if dtype == F32 else 8
-    vec = 4 if dtype == F32 else 16
     rate = 256.0 if dtype == F32 else 4096.0
     RS = p.Nr * p.Ns
     npix = p.Nb * p.Nw * p.Nh
+    tiles = math.ceil(npix / tp) * math.ceil(p.Nk / tk)
+    occ = max(1, min(lds_bytes // lds, wg_per_cu))
+    slots = cus * occ
+    rounds = math.ceil(tiles / slots)
+    o, k, i = eq1.slab_terms(p, tk, tp)
+    nbytes = e_out * o + e_in * (k + i)
+    tile_flops = 2.0 * tk * tp * (math.ceil(p.Nc / tc) * tc) * RS
+    tile_clk = max(tile_flops / rate, (nbytes / tiles) / 64.0)
+    return rounds * slots / cus * tile_clk, {"grid": tiles, "lds": lds, "bytes": nbytes,
+                                             "terms": (o, k, i)}
+
+
+def candidates(p: eq1.Problem, dtype: int, cus: int, lds_bytes: int, acc_regs: int,
+               wg_per_cu: int, tier: int = 2):
+    """Yield (time, tk, tp, tc, id, info) for every feasible candidate of a tier."""
+    RS = p.Nr * p.Ns
+    e_out = 2 if dtype == BF16_OBF16 else 4
+    if tier == 0:
+        for vid, dt, wm, wn, mb, nb, tc, nr, ns, maxi in IGEMM4:
+            if dt != dtype or (nr > 0 and (nr, ns) != (p.Nr, p.Ns)):
+                continue
+            tk, tp, acc = 32 * wm * mb, 32 * wn * nb, 16 * mb * nb
+            S = _max_slab(p, tp)
+            if (tc // 8) * math.ceil(S * p.Ny / 8) > 256 * maxi:
+                continue
+            imgs = tp // (p.Nw * p.Nh) + 2
+            if ((imgs * p.Nc + tc) * p.Nx * p.Ny * 2 >= 2 ** 31
+                    or imgs * p.Nk * p.Nw * p.Nh * e_out >= 2 ** 31):
+                continue
+            blk = math.ceil(RS * (tc // 8) * tk / 256) * 256
+            sn8 = math.ceil(S * p.Ny / 8) * 8
+            lds = 2 * ((tc // 8) * sn8 + blk) * 16
+            if lds > lds_bytes or acc > acc_regs:
+                continue
+            t, info = _cost(p, dtype, tk, tp, tc, lds, cus, lds_bytes, wg_per_cu)
+            yield t, tk, tp, tc, vid, info
+        nbr = (p.Ny + 14) // 8
+        for vid, dt, wm, wn, mb, nb, tc, nr, ns, nbuf, ndi, ndk, mpos in IGEMM3:
+            if dt != dtype or (nr > 0 and (nr, ns) != (p.Nr, p.Ns)):
+                continue
+            tk, tp, acc = 32 * wm * mb, 32 * wn * nb, 16 * mb * nb
+            S = _max_slab(p, tp)
+            if (tc * S * nbr > 256 * ndi or RS * (tc // 8) * tk > 256 * ndk
+                    or S * p.Ny > 256 * mpos):
+                continue
+            imgs = tp // (p.Nw * p.Nh) + 2
+            if ((imgs * p.Nc + tc) * p.Nx * p.Ny * 2 >= 2 ** 31
+                    or imgs * p.Nk * p.Nw * p.Nh * e_out >= 2 ** 31):
+                continue
+            lds = ((tc // 8) * S * p.Ny + nbuf * 256 * (ndi + ndk)) * 16
+            if lds > lds_bytes or acc > acc_regs:
+                continue
+            t, info = _cost(p, dtype, tk, tp, tc, lds, cus, lds_bytes, wg_per_cu)
+            yield t, tk, tp, tc, vid, info
+        return
+    if tier == 1:
+        for vid, dt, wm, wn, mb, nb, tc, nr, ns, maxp in IGEMM2:
+            if dt != dtype or (nr > 0 and (nr, ns) != (p.Nr, p.Ns)):
+                continue
+            tk, tp, acc = 32 * wm * mb, 32 * wn * nb, 16 * mb * nb
+            S = _max_slab(p, tp)
+            if math.ceil(S * p.Ny / 2) > 256 * maxp:
+                continue
+            imgs = tp // (p.Nw * p.Nh) + 2
+            if (imgs * p.Nc * p.Nx * p.Ny * 2 >= 2 ** 31
+                    or imgs * p.Nk * p.Nw * p.Nh * e_out >= 2 ** 31):
+                continue
+            blk = math.ceil(RS * (tc // 8) * tk / 256) * 256
+            sn = (S * p.Ny + 1) // 2 * 2
+            lds = 2 * ((tc // 8) * sn + blk) * 16
+            if lds > lds_bytes or acc > acc_regs:
+                continue
+            t, info = _cost(p, dtype, tk, tp, tc, lds, cus, lds_bytes, wg_per_cu)
+            yield t, tk, tp, tc, vid, info
+        return
+    kv = 1 if dtype == F32 else 8
+    vec = 4 if dtype == F32 else 16
     for vid, dt, wm, wn, mb, nb, tc in IGEMM:
         if dt != dtype:
             continue
@@ -70,27 +202,25 @@ def candidates(p: eq1.Problem, dtype: int, cus: int, lds_bytes: int, acc_regs: i
         lds = (groups * S * p.Ny + RS * groups * tk) * vec
         if lds > lds_bytes or acc > acc_regs:
             continue
-        tiles = math.ceil(npix / tp) * math.ceil(p.Nk / tk)
-        occ = max(1, min(lds_bytes // lds, wg_per_cu))
-        slots = cus * occ
-        rounds = math.ceil(tiles / slots)
-        o, k, i = eq1.slab_terms(p, tk, tp)
-        nbytes = e_out * o + e_in * (k + i)
-        tile_flops = 2.0 * tk * tp * (math.ceil(p.Nc / tc) * tc) * RS
-        tile_clk = max(tile_flops / rate, (nbytes / tiles) / 64.0)
-        t = rounds * slots / cus * tile_clk
-        yield t, tk, tp, tc, vid, {"grid": tiles, "lds": lds, "slab": S, "bytes": nbytes,
-                                   "terms": (o, k, i)}
+        t, info = _cost(p, dtype, tk, tp, tc, lds, cus, lds_bytes, wg_per_cu)
+        yield t, tk, tp, tc, vid, info
 
 
 def choose(p: eq1.Problem, dtype: int, cus=256, lds_bytes=160 * 1024, acc_regs=128,
            wg_per_cu=2):
-    """(kernel, variant id, tk, tp, tc) the rule above selects."""
+    """(kernel, variant id, tk, tp, tc) the rule above selects; kernel 6 is
+    the DMA-staged family, 5 the register-staged pipelined one, 2 the plain
+    staging one, 1 the direct kernel."""
     best = None
-    for t, tk, tp, tc, vid, info in candidates(p, dtype, cus, lds_bytes, acc_regs, wg_per_cu):
-        key = (t, -tk, -tp, -tc, vid)
-        if best is None or key < best[0]:
-            best = (key, (2, vid, tk, tp, tc))
+    for tier in (0, 1, 2):
+        for t, tk, tp, tc, vid, info in candidates(p, dtype, cus, lds_bytes, acc_regs,
+                                                   wg_per_cu, tier):
+            key = (t, -tk, -tp, -tc, vid)
+            if best is None or key < best[0]:
+                kern = (7 if vid >= 800 else 6) if tier == 0 else (5 if tier == 1 else 2)
+                best = (key, (kern, vid, tk, tp, tc))
+        if best is not None:
+            break
     if best is None:
         return (1, 1, 1, 1, p.Nc)
     return best[1]

@@ -19,15 +19,16 @@ LIB_PATH = os.path.join(_HERE, "libcnn_mi355x.so")
 CNN_F32, CNN_BF16, CNN_BF16_OBF16 = 0, 1, 2
 DTYPES = {"f32": CNN_F32, "bf16": CNN_BF16, "bf16_obf16": CNN_BF16_OBF16}
 
-K_AUTO, K_DIRECT, K_IGEMM, K_POINTWISE, K_SMALLC = 0, 1, 2, 3, 4
-KERNEL_NAMES = {K_DIRECT: "direct", K_IGEMM: "igemm", K_POINTWISE: "pointwise", K_SMALLC: "smallc"}
+K_AUTO, K_DIRECT, K_IGEMM, K_POINTWISE, K_SMALLC, K_IGEMM_PIPE, K_IGEMM_DMA, K_IGEMM_WIDE = range(8)
+KERNEL_NAMES = {K_DIRECT: "direct", K_IGEMM: "igemm", K_POINTWISE: "pointwise", K_SMALLC: "smallc",
+                K_IGEMM_PIPE: "igemm_pipe", K_IGEMM_DMA: "igemm_dma", K_IGEMM_WIDE: "igemm_wide"}
 
 STATUS = {0: "CNN_OK", -1: "CNN_E_NULL", -2: "CNN_E_SHAPE", -3: "CNN_E_DTYPE",
           -4: "CNN_E_OVERFLOW", -5: "CNN_E_ALIAS", -6: "CNN_E_UNSUPPORTED",
           -7: "CNN_E_HIP", -8: "CNN_E_PLAN"}
 
 # Every symbol include/cnn.h declares.
-EXPORTS = ["cnn_fwd", "cnn_plan", "cnn_plan_tiles", "cnn_fwd_plan", "cnn_eq1_cost",
+EXPORTS = ["cnn_fwd", "cnn_plan", "cnn_plan_tiles", "cnn_fwd_plan", "cnn_fwd_plan_ws", "cnn_eq1_cost",
            "cnn_slab_cost", "cnn_device_budget", "cnn_strerror", "cnn_last_error",
            "cnn_abi_version"]
 
@@ -50,14 +51,14 @@ class Plan(ctypes.Structure):
     _fields_ = [("prob", Problem), ("dtype", ctypes.c_int32), ("kernel", ctypes.c_int32),
                 ("variant", ctypes.c_int32), ("reserved", ctypes.c_int32),
                 ("tk", i64), ("tp", i64), ("tc", i64), ("grid", i64), ("lds_bytes", i64),
-                ("slab_rows", i64), ("eq1_elems", ctypes.c_double * 3),
+                ("slab_rows", i64), ("ws_bytes", i64), ("eq1_elems", ctypes.c_double * 3),
                 ("eq1_bytes", ctypes.c_double), ("compulsory_bytes", ctypes.c_double),
                 ("flops", ctypes.c_double)]
 
     def as_dict(self) -> dict:
         return {"kernel": KERNEL_NAMES.get(self.kernel, str(self.kernel)), "variant": self.variant,
                 "tk": self.tk, "tp": self.tp, "tc": self.tc, "grid": self.grid,
-                "lds_bytes": self.lds_bytes, "slab_rows": self.slab_rows,
+                "lds_bytes": self.lds_bytes, "slab_rows": self.slab_rows, "ws_bytes": self.ws_bytes,
                 "eq1_elems": list(self.eq1_elems), "eq1_bytes": self.eq1_bytes,
                 "compulsory_bytes": self.compulsory_bytes, "flops": self.flops}
 
@@ -86,6 +87,7 @@ def lib():
     L.cnn_plan.argtypes = [P, ctypes.c_int, B, PL]
     L.cnn_plan_tiles.argtypes = [P, ctypes.c_int, ctypes.c_int, i64, i64, i64, B, PL]
     L.cnn_fwd_plan.argtypes = [vp, vp, vp, P, ctypes.c_int, PL, vp]
+    L.cnn_fwd_plan_ws.argtypes = [vp, vp, vp, P, ctypes.c_int, PL, vp, i64, vp]
     L.cnn_eq1_cost.argtypes = [P, T, ctypes.c_int, ctypes.POINTER(ctypes.c_double),
                                ctypes.POINTER(ctypes.c_double)]
     L.cnn_slab_cost.argtypes = [P, i64, i64, ctypes.POINTER(ctypes.c_double)]
@@ -95,7 +97,7 @@ def lib():
     L.cnn_last_error.argtypes = []
     L.cnn_last_error.restype = ctypes.c_char_p
     L.cnn_abi_version.argtypes = []
-    for f in ("cnn_fwd", "cnn_plan", "cnn_plan_tiles", "cnn_fwd_plan", "cnn_eq1_cost",
+    for f in ("cnn_fwd", "cnn_plan", "cnn_plan_tiles", "cnn_fwd_plan", "cnn_fwd_plan_ws", "cnn_eq1_cost",
               "cnn_slab_cost", "cnn_device_budget", "cnn_abi_version"):
         getattr(L, f).restype = ctypes.c_int
     _lib = L
@@ -163,6 +165,12 @@ def fwd_plan_ptr(In: int, Ker: int, Out: int, prob: Problem, dtype: int, pl: Pla
     _check(lib().cnn_fwd_plan(In, Ker, Out, ctypes.byref(prob), dtype, ctypes.byref(pl), stream))
 
 
+def fwd_plan_ws_ptr(In: int, Ker: int, Out: int, prob: Problem, dtype: int, pl: Plan,
+                    ws: int, ws_bytes: int, stream: int = 0):
+    _check(lib().cnn_fwd_plan_ws(In, Ker, Out, ctypes.byref(prob), dtype, ctypes.byref(pl),
+                                 ws, ws_bytes, stream))
+
+
 def _tensor_dims(In, Ker, Out, sw, sh):
     import torch
     for name, t in (("In", In), ("Ker", Ker), ("Out", Out)):
@@ -210,4 +218,14 @@ def fwd_plan(In, Ker, Out, pl: Plan, sw: int = 1, sh: int = 1, stream=None):
     dims, dt = _tensor_dims(In, Ker, Out, sw, sh)
     fwd_plan_ptr(In.data_ptr(), Ker.data_ptr(), Out.data_ptr(), problem(*dims), dt, pl,
                  _stream(stream))
+    return Out
+
+
+def fwd_plan_ws(In, Ker, Out, pl: Plan, workspace, sw: int = 1, sh: int = 1, stream=None):
+    """cnn_fwd_plan_ws with a caller-owned workspace tensor (any dtype, on the GPU)."""
+    dims, dt = _tensor_dims(In, Ker, Out, sw, sh)
+    ws_ptr = workspace.data_ptr() if workspace is not None else 0
+    ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    fwd_plan_ws_ptr(In.data_ptr(), Ker.data_ptr(), Out.data_ptr(), problem(*dims), dt, pl,
+                    ws_ptr, ws_bytes, _stream(stream))
     return Out

@@ -109,6 +109,7 @@ ConvArgs make_args(const cnn_plan_t& pl) {
   a.npix = (int32_t)(p.Nb * p.Nw * p.Nh);
   a.nxny = a.Nx * a.Ny;
   a.in_img = (int64_t)p.Nc * a.nxny;
+  a.in_total = a.in_img * p.Nb;
   a.out_total = (int64_t)a.npix * p.Nk;
   a.tp = (int32_t)pl.tp;
   a.tk = (int32_t)pl.tk;
@@ -125,6 +126,68 @@ bool same_problem(const cnn_problem& a, const cnn_problem& b) {
          a.Nr == b.Nr && a.Ns == b.Ns && a.sw == b.sw && a.sh == b.sh;
 }
 
+// Device workspace per (device, stream): holds the repacked Ker.  Kernels on
+// one stream run in order, so consecutive calls on a stream may share it.
+std::mutex g_ws_mu;
+std::map<std::pair<int, uintptr_t>, std::pair<void*, int64_t>> g_ws;
+
+int get_workspace(hipStream_t st, int64_t bytes, void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(CNN_E_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+  std::lock_guard<std::mutex> g(g_ws_mu);
+  auto& ent = g_ws[std::make_pair(dev, (uintptr_t)st)];
+  if (ent.second < bytes) {
+    hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+    e = hipStreamIsCapturing(st, &cap);
+    if (e != hipSuccess) return fail(CNN_E_HIP, "hipStreamIsCapturing: %s", hipGetErrorString(e));
+    if (cap != hipStreamCaptureStatusNone)
+      return fail(CNN_E_UNSUPPORTED,
+                  "stream is capturing and has no %lld-byte workspace yet: call once on this "
+                  "stream before capture, or use cnn_fwd_plan_ws", (long long)bytes);
+    if (ent.first) {
+      e = hipStreamSynchronize(st);
+      if (e == hipSuccess) e = hipFree(ent.first);
+      if (e != hipSuccess) return fail(CNN_E_HIP, "workspace release: %s", hipGetErrorString(e));
+      ent.first = nullptr;
+      ent.second = 0;
+    }
+    e = hipMalloc(&ent.first, (size_t)bytes);
+    if (e != hipSuccess) {
+      ent.first = nullptr;
+      return fail(CNN_E_HIP, "workspace allocation of %lld bytes: %s", (long long)bytes,
+                  hipGetErrorString(e));
+    }
+    ent.second = bytes;
+  }
+  *out = ent.first;
+  return CNN_OK;
+}
+
+const Variant4* find_variant4(int id) {
+  int n = 0;
+  const Variant4* vs = variants4(&n);
+  for (int i = 0; i < n; ++i)
+    if (vs[i].id == id) return &vs[i];
+  return nullptr;
+}
+
+const Variant3* find_variant3(int id) {
+  int n = 0;
+  const Variant3* vs = variants3(&n);
+  for (int i = 0; i < n; ++i)
+    if (vs[i].id == id) return &vs[i];
+  return nullptr;
+}
+
+const Variant2* find_variant2(int id) {
+  int n = 0;
+  const Variant2* vs = variants2(&n);
+  for (int i = 0; i < n; ++i)
+    if (vs[i].id == id) return &vs[i];
+  return nullptr;
+}
+
 const Variant* find_variant(int id) {
   int n = 0;
   const Variant* vs = variants(&n);
@@ -133,11 +196,44 @@ const Variant* find_variant(int id) {
   return nullptr;
 }
 
-int run_plan(const void* In, const void* Ker, void* Out, const cnn_plan_t& pl, hipStream_t st) {
+// ws == nullptr: use the library's per-(device, stream) workspace.
+int run_plan(const void* In, const void* Ker, void* Out, const cnn_plan_t& pl, hipStream_t st,
+             void* user_ws = nullptr) {
   const ConvArgs a = make_args(pl);
   hipError_t e;
   if (pl.kernel == CNN_K_DIRECT) {
     e = launch_direct(In, Ker, Out, a, pl.dtype, st);
+  } else if (const Variant4* v4 = find_variant4(pl.variant)) {
+    if (pl.kernel != CNN_K_IGEMM_WIDE || v4->dtype != pl.dtype || v4->tk != pl.tk ||
+        v4->tp != pl.tp || v4->tc != pl.tc || pl.ws_bytes != igemm4_ws_bytes(*v4, pl.prob))
+      return fail(CNN_E_PLAN, "plan names no matching kernel instantiation (variant %d)", pl.variant);
+    void* ws = user_ws;
+    if (!ws) {
+      int st2 = get_workspace(st, pl.ws_bytes, &ws);
+      if (st2) return st2;
+    }
+    e = launch_igemm4(*v4, In, Ker, Out, ws, a, pl.lds_bytes, st);
+  } else if (const Variant3* v3 = find_variant3(pl.variant)) {
+    if (pl.kernel != CNN_K_IGEMM_DMA || v3->dtype != pl.dtype || v3->tk != pl.tk ||
+        v3->tp != pl.tp || v3->tc != pl.tc || pl.ws_bytes != igemm3_ws_bytes(*v3, pl.prob))
+      return fail(CNN_E_PLAN, "plan names no matching kernel instantiation (variant %d)", pl.variant);
+    void* ws = user_ws;
+    if (!ws) {
+      int st2 = get_workspace(st, pl.ws_bytes, &ws);
+      if (st2) return st2;
+    }
+    e = launch_igemm3(*v3, In, Ker, Out, ws, a, pl.lds_bytes, st);
+  } else if (const Variant2* v2 = find_variant2(pl.variant)) {
+    if (pl.kernel != CNN_K_IGEMM_PIPE || v2->dtype != pl.dtype || v2->tk != pl.tk ||
+        v2->tp != pl.tp || v2->tc != pl.tc ||
+        pl.ws_bytes != igemm2_ws_bytes(*v2, pl.prob))
+      return fail(CNN_E_PLAN, "plan names no matching kernel instantiation (variant %d)", pl.variant);
+    void* ws = user_ws;
+    if (!ws) {
+      int st2 = get_workspace(st, pl.ws_bytes, &ws);
+      if (st2) return st2;
+    }
+    e = launch_igemm2(*v2, In, Ker, Out, ws, a, pl.lds_bytes, st);
   } else {
     const Variant* v = find_variant(pl.variant);
     if (!v || v->kernel != pl.kernel || v->dtype != pl.dtype || v->tk != pl.tk ||
@@ -208,7 +304,8 @@ int cnn_plan_tiles(const cnn_problem* prob, int dtype, int kernel, int64_t tk, i
   if (!prob || !plan) return fail(CNN_E_NULL, "prob and plan must be non-NULL");
   int st;
   if ((st = check_problem(*prob)) || (st = check_dtype(dtype))) return st;
-  if (kernel < CNN_K_AUTO || kernel > CNN_K_SMALLC) return fail(CNN_E_UNSUPPORTED, "unknown kernel %d", kernel);
+  if (kernel < CNN_K_AUTO || kernel > CNN_K_IGEMM_WIDE)
+    return fail(CNN_E_UNSUPPORTED, "unknown kernel %d", kernel);
   cnn_budget bud;
   if ((st = resolve_budget(budget, &bud))) return st;
   st = select_plan(*prob, dtype, bud, kernel, tk, tp, tc, plan);
@@ -230,6 +327,24 @@ int cnn_fwd_plan(const void* In, const void* Ker, void* Out, const cnn_problem* 
   if (!same_problem(plan->prob, *prob) || plan->dtype != dtype)
     return fail(CNN_E_PLAN, "plan was made for another problem or dtype");
   return run_plan(In, Ker, Out, *plan, (hipStream_t)stream);
+}
+
+int cnn_fwd_plan_ws(const void* In, const void* Ker, void* Out, const cnn_problem* prob,
+                    int dtype, const cnn_plan_t* plan, void* workspace, int64_t ws_bytes,
+                    void* stream) {
+  if (!prob || !plan) return fail(CNN_E_NULL, "prob and plan must be non-NULL");
+  int st;
+  if ((st = check_problem(*prob)) || (st = check_dtype(dtype))) return st;
+  if ((st = check_buffers(In, Ker, Out, *prob, dtype))) return st;
+  if (!same_problem(plan->prob, *prob) || plan->dtype != dtype)
+    return fail(CNN_E_PLAN, "plan was made for another problem or dtype");
+  if (plan->ws_bytes > 0) {
+    if (!workspace) return fail(CNN_E_NULL, "plan needs a %lld-byte workspace", (long long)plan->ws_bytes);
+    if (ws_bytes < plan->ws_bytes || ((uintptr_t)workspace & 15))
+      return fail(CNN_E_SHAPE, "workspace must be >= %lld bytes and 16-byte aligned",
+                  (long long)plan->ws_bytes);
+  }
+  return run_plan(In, Ker, Out, *plan, (hipStream_t)stream, workspace);
 }
 
 int cnn_fwd(const void* In, const void* Ker, void* Out, int64_t Nb, int64_t Nc, int64_t Nk,

@@ -14,7 +14,10 @@
 //      sequential Eq. (1) leaves out: a tiling with fewer tiles than
 //      workgroup slots leaves CUs idle however little data it moves.
 // The smallest time wins; ties go to the larger tk, then the larger tp,
-// then the larger tc, then the lower instantiation id.
+// then the larger tc, then the lower instantiation id.  The pipelined bf16
+// kernel (conv_igemm2) is tier 1; the plain staging kernel (conv_igemm) is
+// considered only when no tier-1 instantiation fits; the direct kernel
+// takes problems no implicit-GEMM tiling fits.
 #include <math.h>
 #include <string.h>
 
@@ -90,16 +93,14 @@ static double mfma_rate(int dtype) { return dtype == CNN_F32 ? 256.0 : 4096.0; }
 // CU <- L2 bytes per CU per clock assumed by the time model.
 static const double kL2BytesPerClk = 64.0;
 
-// Fill *plan for one implicit-GEMM variant; false if it does not fit.
-static bool eval_variant(const cnn_problem& p, int dtype, const Variant& v,
-                         const cnn_budget& bud, cnn_plan_t* plan, double* time_clk) {
+// Time model and plan fields shared by the implicit-GEMM families.
+static bool eval_tiling(const cnn_problem& p, int dtype, int id, int64_t tk, int64_t tp,
+                        int64_t tc, int64_t acc, int64_t S, int64_t lds, int64_t ws,
+                        const cnn_budget& bud, cnn_plan_t* plan, double* time_clk) {
   const int64_t RS = p.Nr * p.Ns;
-  const int64_t Ny = p.sh * (p.Nh - 1) + p.Ns;
   const int64_t npix = p.Nb * p.Nw * p.Nh;
-  const int64_t S = slab_rows_max(p, v.tp);
-  const int64_t lds = igemm_lds_bytes(v, S, Ny, RS);
-  if (lds > bud.lds_bytes || v.acc > bud.acc_regs) return false;
-  const int64_t n_p = ceil_div(npix, v.tp), n_k = ceil_div(p.Nk, v.tk);
+  if (lds > bud.lds_bytes || acc > bud.acc_regs) return false;
+  const int64_t n_p = ceil_div(npix, tp), n_k = ceil_div(p.Nk, tk);
   const int64_t grid = n_p * n_k;
   if (grid > 0x7fffffffLL) return false;
   int64_t occ = bud.lds_bytes / lds;
@@ -108,11 +109,11 @@ static bool eval_variant(const cnn_problem& p, int dtype, const Variant& v,
   const int64_t rounds = ceil_div(grid, slots);
 
   double terms[3];
-  slab_terms(p, v.tk, v.tp, terms);
+  slab_terms(p, tk, tp, terms);
   const double e_in = in_bytes(dtype), e_out = out_bytes(dtype);
   const double bytes = e_out * terms[0] + e_in * (terms[1] + terms[2]);
   const double tile_flops =
-      2.0 * v.tk * v.tp * (double)(ceil_div(p.Nc, v.tc) * v.tc) * (double)RS;
+      2.0 * tk * tp * (double)(ceil_div(p.Nc, tc) * tc) * (double)RS;
   const double tile_clk =
       std::max(tile_flops / mfma_rate(dtype), (bytes / (double)grid) / kL2BytesPerClk);
   *time_clk = (double)rounds * (double)slots / (double)bud.cus * tile_clk;
@@ -121,16 +122,79 @@ static bool eval_variant(const cnn_problem& p, int dtype, const Variant& v,
   plan->prob = p;
   plan->dtype = dtype;
   plan->kernel = CNN_K_IGEMM;
-  plan->variant = v.id;
-  plan->tk = v.tk;
-  plan->tp = v.tp;
-  plan->tc = v.tc;
+  plan->variant = id;
+  plan->tk = tk;
+  plan->tp = tp;
+  plan->tc = tc;
   plan->grid = grid;
   plan->lds_bytes = lds;
   plan->slab_rows = S;
+  plan->ws_bytes = ws;
   for (int i = 0; i < 3; ++i) plan->eq1_elems[i] = terms[i];
   plan->eq1_bytes = bytes;
   return true;
+}
+
+// Plain staging kernel (conv_igemm).
+static bool eval_variant(const cnn_problem& p, int dtype, const Variant& v,
+                         const cnn_budget& bud, cnn_plan_t* plan, double* time_clk) {
+  const int64_t Ny = p.sh * (p.Nh - 1) + p.Ns;
+  const int64_t S = slab_rows_max(p, v.tp);
+  const int64_t lds = igemm_lds_bytes(v, S, Ny, p.Nr * p.Ns);
+  return eval_tiling(p, dtype, v.id, v.tk, v.tp, v.tc, v.acc, S, lds, 0, bud, plan, time_clk);
+}
+
+// Wide-staging pipelined kernel (conv_igemm4).
+static bool eval_variant4(const cnn_problem& p, int dtype, const Variant4& v,
+                          const cnn_budget& bud, cnn_plan_t* plan, double* time_clk) {
+  const int64_t Ny = p.sh * (p.Nh - 1) + p.Ns;
+  const int64_t S = slab_rows_max(p, v.tp);
+  if (!igemm4_fits(v, p, S)) return false;
+  const int64_t Nx = p.sw * (p.Nw - 1) + p.Nr;
+  const int64_t imgs = v.tp / (p.Nw * p.Nh) + 2;
+  if ((imgs * p.Nc + v.tc) * Nx * Ny * 2 >= (1LL << 31) ||
+      imgs * p.Nk * p.Nw * p.Nh * out_bytes(dtype) >= (1LL << 31))
+    return false;
+  const int64_t lds = igemm4_lds_bytes(v, S, Ny, p.Nr * p.Ns);
+  return eval_tiling(p, dtype, v.id, v.tk, v.tp, v.tc, v.acc, S, lds, igemm4_ws_bytes(v, p),
+                     bud, plan, time_clk);
+}
+
+// DMA-staged kernel (conv_igemm3).
+static bool eval_variant3(const cnn_problem& p, int dtype, const Variant3& v,
+                          const cnn_budget& bud, cnn_plan_t* plan, double* time_clk) {
+  const int64_t Ny = p.sh * (p.Nh - 1) + p.Ns;
+  const int64_t S = slab_rows_max(p, v.tp);
+  if (!igemm3_fits(v, p, S)) return false;
+  const int64_t Nx = p.sw * (p.Nw - 1) + p.Nr;
+  const int64_t imgs = v.tp / (p.Nw * p.Nh) + 2;
+  if ((imgs * p.Nc + v.tc) * Nx * Ny * 2 >= (1LL << 31) ||
+      imgs * p.Nk * p.Nw * p.Nh * out_bytes(dtype) >= (1LL << 31))
+    return false;
+  const int64_t lds = igemm3_lds_bytes(v, S, Ny);
+  return eval_tiling(p, dtype, v.id, v.tk, v.tp, v.tc, v.acc, S, lds, igemm3_ws_bytes(v, p),
+                     bud, plan, time_clk);
+}
+
+// Pipelined kernel (conv_igemm2): its stencil must match a compile-time one
+// (or be generic) and its slab must fit the per-thread staging registers.
+static bool eval_variant2(const cnn_problem& p, int dtype, const Variant2& v,
+                          const cnn_budget& bud, cnn_plan_t* plan, double* time_clk) {
+  if (v.nr > 0 && (v.nr != p.Nr || v.ns != p.Ns)) return false;
+  const int64_t Ny = p.sh * (p.Nh - 1) + p.Ns;
+  const int64_t S = slab_rows_max(p, v.tp);
+  const int64_t pairs = (S * Ny + 1) / 2;
+  if (pairs > 256 * (int64_t)v.maxp) return false;
+  // per-tile buffer offsets are 32-bit: the images a tile touches must span
+  // less than 2 GiB of In and of Out
+  const int64_t Nx = p.sw * (p.Nw - 1) + p.Nr;
+  const int64_t imgs = v.tp / (p.Nw * p.Nh) + 2;
+  if (imgs * p.Nc * Nx * Ny * 2 >= (1LL << 31) ||
+      imgs * p.Nk * p.Nw * p.Nh * out_bytes(dtype) >= (1LL << 31))
+    return false;
+  const int64_t lds = igemm2_lds_bytes(v, S, Ny, p.Nr * p.Ns);
+  return eval_tiling(p, dtype, v.id, v.tk, v.tp, v.tc, v.acc, S, lds, igemm2_ws_bytes(v, p),
+                     bud, plan, time_clk);
 }
 
 static void fill_common(const cnn_problem& p, int dtype, cnn_plan_t* plan) {
@@ -171,19 +235,13 @@ int select_plan(const cnn_problem& p, int dtype, const cnn_budget& bud, int kern
     direct_plan(p, dtype, out);
     return CNN_OK;
   }
-  if (kernel != CNN_K_AUTO && kernel != CNN_K_IGEMM) return CNN_E_UNSUPPORTED;
-  int n = 0;
-  const Variant* vs = variants(&n);
+  if (kernel != CNN_K_AUTO && kernel != CNN_K_IGEMM && kernel != CNN_K_IGEMM_PIPE &&
+      kernel != CNN_K_IGEMM_DMA && kernel != CNN_K_IGEMM_WIDE)
+    return CNN_E_UNSUPPORTED;
   bool found = false;
   double best_t = 0;
   cnn_plan_t best;
-  for (int i = 0; i < n; ++i) {
-    const Variant& v = vs[i];
-    if (v.dtype != dtype || v.kernel != CNN_K_IGEMM) continue;
-    if (kernel == CNN_K_IGEMM && (v.tk != tk || v.tp != tp || v.tc != tc)) continue;
-    cnn_plan_t cand;
-    double t;
-    if (!eval_variant(p, dtype, v, bud, &cand, &t)) continue;
+  auto consider = [&](const cnn_plan_t& cand, double t) {
     bool better = !found || t < best_t;
     if (found && t == best_t) {
       if (cand.tk != best.tk) better = cand.tk > best.tk;
@@ -195,6 +253,62 @@ int select_plan(const cnn_problem& p, int dtype, const cnn_budget& bud, int kern
       best = cand;
       best_t = t;
       found = true;
+    }
+  };
+  // Tier 1: the DMA-staged kernel, tier 2: the register-staged pipelined
+  // kernel (both bf16), tier 3: the plain staging kernel.  The wide-staging
+// kernel competes within tier 1.
+  int n4 = 0;
+  const Variant4* vs4 = variants4(&n4);
+  for (int i = 0; i < n4; ++i) {
+    const Variant4& v = vs4[i];
+    if (v.dtype != dtype || (kernel != CNN_K_AUTO && kernel != CNN_K_IGEMM_WIDE)) continue;
+    if (kernel == CNN_K_IGEMM_WIDE && (v.tk != tk || v.tp != tp || v.tc != tc)) continue;
+    cnn_plan_t cand;
+    double t;
+    if (eval_variant4(p, dtype, v, bud, &cand, &t)) {
+      cand.kernel = CNN_K_IGEMM_WIDE;
+      consider(cand, t);
+    }
+  }
+  int n3 = 0;
+  const Variant3* vs3 = variants3(&n3);
+  for (int i = 0; i < n3; ++i) {
+    const Variant3& v = vs3[i];
+    if (v.dtype != dtype || (kernel != CNN_K_AUTO && kernel != CNN_K_IGEMM_DMA)) continue;
+    if (kernel == CNN_K_IGEMM_DMA && (v.tk != tk || v.tp != tp || v.tc != tc)) continue;
+    cnn_plan_t cand;
+    double t;
+    if (eval_variant3(p, dtype, v, bud, &cand, &t)) {
+      cand.kernel = CNN_K_IGEMM_DMA;
+      consider(cand, t);
+    }
+  }
+  const bool tier1_found = found;
+  int n2 = 0;
+  const Variant2* vs2 = variants2(&n2);
+  for (int i = 0; i < n2; ++i) {
+    const Variant2& v = vs2[i];
+    if (tier1_found || v.dtype != dtype || (kernel != CNN_K_AUTO && kernel != CNN_K_IGEMM_PIPE))
+      continue;
+    if (kernel == CNN_K_IGEMM_PIPE && (v.tk != tk || v.tp != tp || v.tc != tc)) continue;
+    cnn_plan_t cand;
+    double t;
+    if (eval_variant2(p, dtype, v, bud, &cand, &t)) {
+      cand.kernel = CNN_K_IGEMM_PIPE;
+      consider(cand, t);
+    }
+  }
+  if (!found && (kernel == CNN_K_AUTO || kernel == CNN_K_IGEMM)) {
+    int n = 0;
+    const Variant* vs = variants(&n);
+    for (int i = 0; i < n; ++i) {
+      const Variant& v = vs[i];
+      if (v.dtype != dtype || v.kernel != CNN_K_IGEMM) continue;
+      if (kernel == CNN_K_IGEMM && (v.tk != tk || v.tp != tp || v.tc != tc)) continue;
+      cnn_plan_t cand;
+      double t;
+      if (eval_variant(p, dtype, v, bud, &cand, &t)) consider(cand, t);
     }
   }
   if (!found) {

@@ -5,7 +5,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
-#include "../../include/cnn.h"
+#include "cnn.h"
 
 namespace cnnlib {
 
@@ -21,6 +21,7 @@ struct ConvArgs {
   int32_t npix;        // Nb*Nw*Nh outputs of the flattened (b, w, h) index
   int32_t nxny;        // Nx*Ny input elements per (b, c) plane
   int64_t in_img;      // Nc*Nx*Ny input elements per image
+  int64_t in_total;    // Nb*Nc*Nx*Ny
   int64_t out_total;   // Nb*Nk*Nw*Nh
   // tiling (implicit-GEMM kernels)
   int32_t tp, tk, tc;  // outputs, features, channels per workgroup tile / stage
@@ -43,16 +44,71 @@ struct Variant {
 // Variant table (defined next to the kernels) and its size.
 const Variant* variants(int* count);
 
+// A pipelined implicit-GEMM instantiation (bf16 In/Ker, packed Ker).
+struct Variant2 {
+  int32_t id;
+  int32_t dtype;    // CNN_BF16 or CNN_BF16_OBF16
+  int32_t tk, tp, tc;
+  int32_t acc;      // fp32 accumulators per lane
+  int32_t nr, ns;   // compile-time stencil (0 = any)
+  int32_t maxp;     // slab position pairs per thread: ceil(S*Ny/2) <= 256*maxp
+};
+const Variant2* variants2(int* count);
+int64_t igemm2_blk_vecs(const Variant2& v, int64_t RS);
+int64_t igemm2_lds_bytes(const Variant2& v, int64_t slab_rows, int64_t Ny, int64_t RS);
+int64_t igemm2_ws_bytes(const Variant2& v, const cnn_problem& p);
+
 // LDS bytes an implicit-GEMM variant needs for a given slab height.
 int64_t igemm_lds_bytes(const Variant& v, int64_t slab_rows, int64_t Ny, int64_t RS);
 
 // Max input rows any composite tile of `tp` outputs stages.
 int64_t slab_rows_max(const cnn_problem& p, int64_t tp);
 
+// A DMA-staged implicit-GEMM instantiation (bf16 In/Ker, packed Ker).
+struct Variant3 {
+  int32_t id;
+  int32_t dtype;
+  int32_t tk, tp, tc;
+  int32_t acc;
+  int32_t nr, ns;   // compile-time stencil (0 = any)
+  int32_t nbuf;     // copy buffers in the DMA ring (2 or 3)
+  int32_t ndi, ndk; // DMA instructions per thread per stage (In copy, Ker)
+  int32_t mpos;     // transposed positions per thread (slab positions <= 256*mpos)
+};
+const Variant3* variants3(int* count);
+int64_t igemm3_lds_bytes(const Variant3& v, int64_t slab_rows, int64_t Ny);
+int64_t igemm3_ws_bytes(const Variant3& v, const cnn_problem& p);
+bool igemm3_fits(const Variant3& v, const cnn_problem& p, int64_t slab_rows);
+
+// A wide-staging, software-pipelined instantiation (bf16, packed Ker).
+struct Variant4 {
+  int32_t id;
+  int32_t dtype;
+  int32_t tk, tp, tc;
+  int32_t acc;
+  int32_t nr, ns;   // compile-time stencil (0 = any)
+  int32_t maxi;     // In items per thread: tc/8 * ceil(S*Ny/8) <= 256*maxi
+};
+const Variant4* variants4(int* count);
+int64_t igemm4_lds_bytes(const Variant4& v, int64_t slab_rows, int64_t Ny, int64_t RS);
+int64_t igemm4_ws_bytes(const Variant4& v, const cnn_problem& p);
+bool igemm4_fits(const Variant4& v, const cnn_problem& p, int64_t slab_rows);
+hipError_t launch_igemm4(const Variant4& v, const void* In, const void* Ker, void* Out,
+                         void* ws, const ConvArgs& a, int64_t lds_bytes, hipStream_t stream);
+
+// Ker repack for the pipelined kernels (defined with conv_igemm2).
+__global__ void pack_ker_bf16(const uint16_t* __restrict__ Ker, uint32_t __attribute__((ext_vector_type(4)))* __restrict__ P,
+                              ConvArgs a, int TK, int TC, int blk_vecs, int64_t total_vecs);
+
 // Launchers (asynchronous; return hipGetLastError()).
 hipError_t launch_direct(const void* In, const void* Ker, void* Out, const ConvArgs& a,
                          int dtype, hipStream_t stream);
 hipError_t launch_igemm(const Variant& v, const void* In, const void* Ker, void* Out,
                         const ConvArgs& a, int64_t lds_bytes, hipStream_t stream);
+hipError_t launch_igemm3(const Variant3& v, const void* In, const void* Ker, void* Out,
+                         void* ws, const ConvArgs& a, int64_t lds_bytes, hipStream_t stream);
+// Packs Ker into `ws` (igemm2_ws_bytes) and runs the pipelined kernel.
+hipError_t launch_igemm2(const Variant2& v, const void* In, const void* Ker, void* Out,
+                         void* ws, const ConvArgs& a, int64_t lds_bytes, hipStream_t stream);
 
 }  // namespace cnnlib

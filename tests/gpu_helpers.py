@@ -75,3 +75,42 @@ def errors(got: np.ndarray, want: np.ndarray, absv: np.ndarray):
     nz = np.abs(want) > 0
     point = float((d[nz] / np.abs(want[nz])).max()) if nz.any() else 0.0
     return normwise, cond, point
+
+
+def variant_dims(kernel, vid, dt, tk, tp, tc, stencil):
+    """Problem sizes on which instantiation `vid` is what cnn_plan_tiles
+    picks for (kernel, tk, tp, tc): ragged channel, feature and output
+    tails, several tiles.  None if no candidate fits."""
+    Nr, Ns = stencil
+    cands = [(3, tc + 5, tk + 7, 9, 13, Nr, Ns, 1, 2), (2, tc + 5, tk + 7, 7, 13, Nr, Ns, 1, 1),
+             (2, tc + 3, max(1, tk - 5), 5, 9, Nr, Ns, 1, 1), (1, tc + 5, tk + 3, 6, 7, Nr, Ns, 1, 1),
+             (2, tc + 5, tk + 7, 4, 5, Nr, Ns, 2, 1), (1, tc + 5, tk + 7, 3, 4, Nr, Ns, 1, 1)]
+    for dims in cands:
+        try:
+            pl = cnn.plan_tiles(cnn.problem(*dims), dt, kernel, tk, tp, tc, cnn.budget())
+        except cnn.CnnError:
+            continue
+        if pl.variant == vid:
+            return dims
+    return None
+
+
+def variant_cases():
+    """(kernel, vid, dtype, tk, tp, tc, stencil) of every implicit-GEMM
+    instantiation, from the oracle's independent tables."""
+    from oracle import select as osel
+    out = []
+    for vid, dt, wm, wn, mb, nb, tc in osel.IGEMM:
+        out.append((cnn.K_IGEMM, vid, dt, 32 * wm * mb, 32 * wn * nb, tc, (3, 3)))
+    for vid, dt, wm, wn, mb, nb, tc, nr, ns, _ in osel.IGEMM4:
+        out.append((cnn.K_IGEMM_WIDE, vid, dt, 32 * wm * mb, 32 * wn * nb, tc,
+                    (nr, ns) if nr else (5, 2)))
+    for vid, dt, wm, wn, mb, nb, tc, nr, ns, *_ in osel.IGEMM3:
+        tk = 32 * wm * mb
+        out.append((cnn.K_IGEMM_DMA, vid, dt, tk, 32 * wn * nb, tc,
+                    (nr, ns) if nr else ((1, 1) if vid % 100 in (10, 11, 12) else (5, 2))))
+    for vid, dt, wm, wn, mb, nb, tc, nr, ns, _ in osel.IGEMM2:
+        tk = 32 * wm * mb
+        out.append((cnn.K_IGEMM_PIPE, vid, dt, tk, 32 * wn * nb, tc,
+                    (nr, ns) if nr else ((1, 1) if tk >= 256 else (5, 2))))
+    return out

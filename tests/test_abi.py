@@ -154,3 +154,14 @@ def test_plan_reports_eq1_and_compulsory_bytes():
     comp = 2 * (w.Nb * w.Nc * w.Nx * w.Ny + w.Nk * w.Nc * 9) + 4 * w.Nb * w.Nk * w.Nw * w.Nh
     assert pl.compulsory_bytes == comp
     assert pl.flops == w.flops
+
+
+def test_every_instantiation_has_a_fitting_test_shape():
+    """The GPU variant test needs, for each instantiation, a problem it fits;
+    check on the CPU that one exists."""
+    import sys
+    sys.path.insert(0, os.path.join(ROOT, "tests"))
+    from gpu_helpers import variant_cases, variant_dims
+    for case in variant_cases():
+        kernel, vid, dt, tk, tp, tc, stencil = case
+        assert variant_dims(kernel, vid, dt, tk, tp, tc, stencil) is not None, vid

@@ -13,7 +13,8 @@ import oracle
 from oracle import select as osel
 from paper_2105_13480_amd import cnn, inputs
 
-from gpu_helpers import TOL, errors, run, say, to_gpu, out_tensor, to_host64
+from gpu_helpers import (TOL, errors, out_tensor, run, say, to_gpu, to_host64, variant_cases,
+                         variant_dims)
 
 pytestmark = pytest.mark.gpu
 
@@ -52,20 +53,15 @@ def test_mid_size_auto_plan(dims, mode):
     assert nw <= TOL[mode] and cond <= TOL[mode], (nw, cond)
 
 
-def _variant_rows(dtype):
-    return [r for r in osel.IGEMM if r[1] == dtype]
-
-
-@pytest.mark.parametrize("row", _variant_rows(0) + _variant_rows(1) + _variant_rows(2),
-                         ids=lambda r: f"v{r[0]}")
-def test_every_igemm_variant_exact_integers(row):
-    vid, dt, wm, wn, mb, nb, tc = row
-    tk, tp = 32 * wm * mb, 32 * wn * nb
+@pytest.mark.parametrize("case", variant_cases(), ids=lambda c: f"v{c[1]}")
+def test_every_igemm_variant_exact_integers(case):
+    kernel, vid, dt, tk, tp, tc, stencil = case
     mode = {0: "f32", 1: "bf16", 2: "bf16_obf16"}[dt]
-    # spans several tiles with ragged pixel, feature and channel tails
-    dims = (3, tc + 5, tk + 7, 9, 13, 3, 3, 1, 2)
+    dims = variant_dims(kernel, vid, dt, tk, tp, tc, stencil)
+    assert dims is not None, f"no test shape fits instantiation {vid}"
     In, Ker = _arrays(dims, mode, seed=vid, dist=("int", -2, 2), kdist=("int", -2, 2))
-    pl = cnn.plan_tiles(cnn.problem(*dims), dt, cnn.K_IGEMM, tk, tp, tc)
+    pl = cnn.plan_tiles(cnn.problem(*dims), dt, kernel, tk, tp, tc)
+    assert pl.variant == vid
     say(f"[parity] variant {vid} tk={tk} tp={tp} tc={tc} dims={dims} grid={pl.grid}")
     got = run(In, Ker, dims[7], dims[8], mode, plan=pl)
     want = oracle.conv(In, Ker, dims[7], dims[8])
