@@ -67,8 +67,11 @@ def forced_plan(spec: str, w, mode: str):
     from paper_2105_13480_amd import cnn
     parts = spec.split(":")
     kern = KERNELS[parts[0]]
-    tk, tp, tc = (int(x) for x in parts[1:4]) if len(parts) == 4 else (0, 0, 0)
-    return cnn.plan_tiles(cnn.problem(*w.dims()), cnn.DTYPES[mode], kern, tk, tp, tc)
+    tk, tp, tc = (int(x) for x in parts[1:4]) if len(parts) >= 4 else (0, 0, 0)
+    pl = cnn.plan_tiles(cnn.problem(*w.dims()), cnn.DTYPES[mode], kern, tk, tp, tc)
+    if len(parts) == 5 and pl.variant != int(parts[4]):
+        raise SystemExit(f"--plan {spec}: the tiling resolves to variant {pl.variant}")
+    return pl
 
 
 def copy_calibration(nbytes: int, steps: int):
@@ -94,7 +97,60 @@ def copy_calibration(nbytes: int, steps: int):
           flush=True)
 
 
-def time_workload(w, mode: str, steps: int, warmup: int, eager: bool, plan_spec: str = ""):
+def _counter_medians(csv_dir: str, counter: str):
+    """{kernel name: (dispatches, median value in KiB)} of one rocprofv3
+    --pmc pass (its *counter_collection.csv)."""
+    import csv
+    import glob
+    import statistics
+    vals = {}
+    for path in glob.glob(os.path.join(csv_dir, "**", "*counter_collection.csv"), recursive=True):
+        with open(path) as fh:
+            for r in csv.DictReader(fh):
+                if r["Counter_Name"] == counter:
+                    vals.setdefault(r["Kernel_Name"], []).append(float(r["Counter_Value"]))
+    return {k: (len(v), statistics.median(v)) for k, v in vals.items()}
+
+
+def summarize_counters(pmc_dir: str, workload: str, mode: str, copy_bytes: int, commands):
+    """Write profiles/hbm_traffic.json from four rocprofv3 --pmc passes under
+    pmc_dir: conv_fetch / conv_write (FETCH_SIZE / WRITE_SIZE of this bench
+    with a forced plan) and copy_fetch / copy_write (the same counters on a
+    device copy of copy_bytes, whose true traffic is known).  Counter KiB are
+    scaled by true / counted bytes of the copy."""
+    cf = _counter_medians(os.path.join(pmc_dir, "copy_fetch"), "FETCH_SIZE")
+    cw = _counter_medians(os.path.join(pmc_dir, "copy_write"), "WRITE_SIZE")
+    kf = _counter_medians(os.path.join(pmc_dir, "conv_fetch"), "FETCH_SIZE")
+    kw = _counter_medians(os.path.join(pmc_dir, "conv_write"), "WRITE_SIZE")
+    copy_f = max((v for k, v in cf.items() if "copyBuffer" in k), key=lambda x: x[0])[1]
+    copy_w = max((v for k, v in cw.items() if "copyBuffer" in k), key=lambda x: x[0])[1]
+    f_scale = copy_bytes / (copy_f * 1024.0)
+    w_scale = copy_bytes / (copy_w * 1024.0)
+    conv = [k for k in kf if "cnnlib::conv_" in k]
+    name = max(conv, key=lambda k: kf[k][0])
+    fetch = kf[name][1] * 1024.0 * f_scale
+    write = kw[name][1] * 1024.0 * w_scale
+    path = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+    try:
+        with open(path) as fh:
+            data = json.load(fh)
+    except (OSError, ValueError):
+        data = {}
+    data[f"{workload}/{mode}"] = {
+        "kernel": name, "dispatches": kf[name][0],
+        "fetch_kib_median": kf[name][1], "write_kib_median": kw[name][1],
+        "copy_bytes": copy_bytes, "copy_fetch_kib": copy_f, "copy_write_kib": copy_w,
+        "fetch_scale": round(f_scale, 4), "write_scale": round(w_scale, 4),
+        "hbm_fetch_bytes": round(fetch), "hbm_write_bytes": round(write),
+        "hbm_bytes_per_launch": round(fetch + write),
+        "source_hash": kernel_source_hash(), "commands": commands}
+    with open(path, "w") as fh:
+        json.dump(data, fh, indent=1, sort_keys=True)
+    print(json.dumps(data[f"{workload}/{mode}"]))
+
+
+def time_workload(w, mode: str, steps: int, warmup: int, eager: bool, plan_spec: str = "",
+                  find: bool = True):
     import numpy as np
     import torch
 
@@ -108,20 +164,25 @@ def time_workload(w, mode: str, steps: int, warmup: int, eager: bool, plan_spec:
         dIn, dKer = torch.from_numpy(In).cuda(), torch.from_numpy(Ker).cuda()
     out_dt = torch.bfloat16 if mode == "bf16_obf16" else torch.float32
     dOut = torch.empty((w.Nb, w.Nk, w.Nw, w.Nh), dtype=out_dt, device="cuda")
+    # Warm up on the stream that is then captured: the library keeps its
+    # workspace per stream and cannot allocate during capture.
+    cap_stream = torch.cuda.Stream()
     if plan_spec:
         plan = forced_plan(plan_spec, w, mode)
+        selection = "forced"
 
         def step():
             cnn.fwd_plan(dIn, dKer, dOut, plan, w.sw, w.sh)
     else:
-        plan = cnn.plan(cnn.problem(*w.dims()), cnn.DTYPES[mode])
+        if find:  # time every feasible tiling once, before the timed region
+            cnn.plan_find(dIn, dKer, dOut, w.sw, w.sh, stream=cap_stream)
+            torch.cuda.synchronize()
+        plan = cnn.plan_lookup(cnn.problem(*w.dims()), cnn.DTYPES[mode])
+        selection = "find" if find else "model"
 
         def step():
             cnn.fwd(dIn, dKer, dOut, w.sw, w.sh)
 
-    # Warm up on the stream that is then captured: the library keeps its
-    # workspace per stream and cannot allocate during capture.
-    cap_stream = torch.cuda.Stream()
     with torch.cuda.stream(cap_stream):
         for _ in range(max(warmup, 1)):
             step()
@@ -154,6 +215,7 @@ def time_workload(w, mode: str, steps: int, warmup: int, eager: bool, plan_spec:
     ms_per_step = (t1 - t0) * 1e3 / steps
     kernel_ms = ev0.elapsed_time(ev1) / steps
     del graph
+    plan.selection = selection
     return ms_per_step, kernel_ms, plan
 
 
@@ -193,14 +255,30 @@ def main():
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--out-dtype", choices=["fp32", "bf16"], default="fp32")
     ap.add_argument("--eager", action="store_true")
+    ap.add_argument("--model-plan", action="store_true",
+                    help="use the Eq. (1) model's plan instead of timing the feasible tilings")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--all", action="store_true",
                     help="also time every workload and output dtype (table on stderr)")
     ap.add_argument("--plan", default="",
-                    help="force a tiling, KERNEL[:TK:TP:TC] with KERNEL in direct/igemm/igemm_pipe")
+                    help="force a tiling, KERNEL[:TK:TP:TC[:VARIANT]], KERNEL one of "
+                         + "/".join(KERNELS))
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="only time a device copy of this many bytes (counter calibration)")
+    ap.add_argument("--summarize-counters", default="",
+                    help="write profiles/hbm_traffic.json from rocprofv3 --pmc passes in this "
+                         "directory (conv_fetch, conv_write, copy_fetch, copy_write); no GPU")
+    ap.add_argument("--commands", default="",
+                    help="with --summarize-counters: the commands that made the passes")
     args = ap.parse_args()
+
+    if args.summarize_counters:
+        from paper_2105_13480_amd import inputs as _inputs
+        w = _inputs.BY_NAME[args.workload]
+        mode = "f32" if w.dtype == "f32" else ("bf16" if args.out_dtype == "fp32" else "bf16_obf16")
+        summarize_counters(args.summarize_counters, w.name, mode, args.copy_bytes,
+                           [c for c in args.commands.split(";;") if c])
+        return
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -222,7 +300,9 @@ def main():
 
     w = inputs.BY_NAME[args.workload]
     mode = "f32" if w.dtype == "f32" else ("bf16" if args.out_dtype == "fp32" else "bf16_obf16")
-    ms, kms, plan = time_workload(w, mode, args.steps, args.warmup, args.eager, args.plan)
+    ms, kms, plan = time_workload(w, mode, args.steps, args.warmup, args.eager, args.plan,
+                                  find=not args.model_plan)
+    model = cnn.plan(cnn.problem(*w.dims()), cnn.DTYPES[mode])
 
     prec = "f32" if mode == "f32" else "bf16"
     tflops = w.flops / (ms * 1e-3) / 1e12
@@ -260,7 +340,10 @@ def main():
                    "out_dtype": "bf16" if mode == "bf16_obf16" else "f32",
                    "launch": "eager" if args.eager else "hipgraph",
                    "plan": {k: v for k, v in plan.as_dict().items()
-                            if k in ("kernel", "variant", "tk", "tp", "tc", "grid")}},
+                            if k in ("kernel", "variant", "tk", "tp", "tc", "grid")},
+                   "plan_selection": plan.selection,
+                   "model_plan": {k: v for k, v in model.as_dict().items()
+                                  if k in ("kernel", "variant", "tk", "tp", "tc")}},
         "pct_mfma_peak": round(100.0 * tflops / PEAK_TFLOPS[prec], 2),
         "roofline": roof,
     }
@@ -270,7 +353,8 @@ def main():
     if args.all:
         for ww in inputs.WORKLOADS:
             for md in (["f32"] if ww.dtype == "f32" else ["bf16", "bf16_obf16"]):
-                m2, k2, p2 = time_workload(ww, md, min(args.steps, 100), 5, args.eager)
+                m2, k2, p2 = time_workload(ww, md, min(args.steps, 100), 5, args.eager,
+                                           find=not args.model_plan)
                 pr = "f32" if md == "f32" else "bf16"
                 print(f"{ww.name:18s} {md:10s} kernel {k2 * 1e3:9.2f} us  "
                       f"{ww.flops / (k2 * 1e-3) / 1e12:8.1f} TF/s  "

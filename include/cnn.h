@@ -133,9 +133,11 @@ typedef struct cnn_plan_t {
 } cnn_plan_t;
 
 /*
- * Out = conv(In, Ker) on `stream`.  Chooses (and caches) a plan with
- * cnn_plan for the current device.  See the file header for layouts.
- * Errors: CNN_E_NULL, CNN_E_SHAPE, CNN_E_DTYPE, CNN_E_OVERFLOW,
+ * Out = conv(In, Ker) on `stream` (the CNN equation of Sec. 1, scheduled as
+ * Listing 3 of Sec. 2).  Uses the plan cached for (problem, dtype, current
+ * device): the winner of an earlier cnn_plan_find, else cnn_plan's choice
+ * (computed on the first call and cached).  See the file header for
+ * layouts.  Errors: CNN_E_NULL, CNN_E_SHAPE, CNN_E_DTYPE, CNN_E_OVERFLOW,
  * CNN_E_ALIAS, CNN_E_HIP.
  */
 int cnn_fwd(const void* In, const void* Ker, void* Out,
@@ -153,6 +155,29 @@ int cnn_fwd(const void* In, const void* Ker, void* Out,
  */
 int cnn_plan(const cnn_problem* prob, int dtype, const cnn_budget* budget,
              cnn_plan_t* plan);
+
+/*
+ * Empirical selection among the tilings cnn_plan considers (every
+ * instantiation whose Eq. (1) footprint fits the current device's budget):
+ * runs each on the caller's buffers on `stream`, times it with HIP events
+ * (one untimed run, then 3-20 timed runs), and returns the fastest in
+ * *plan (its mean time in *best_ms when best_ms is not NULL).  The winner
+ * is cached for (problem, dtype, device), so later cnn_fwd calls use it.
+ * In and Ker are only read; Out is overwritten and on success holds the
+ * result of the winning plan.  Blocks until the timing runs finish; cannot
+ * be called while `stream` is being captured (CNN_E_UNSUPPORTED).  Other
+ * errors as cnn_fwd.
+ */
+int cnn_plan_find(const void* In, const void* Ker, void* Out,
+                  const cnn_problem* prob, int dtype, void* stream,
+                  cnn_plan_t* plan, double* best_ms);
+
+/*
+ * The plan cnn_fwd would use for (prob, dtype) on the current device
+ * (cached winner of cnn_plan_find, else cnn_plan's choice).  Errors:
+ * CNN_E_NULL, CNN_E_SHAPE, CNN_E_DTYPE, CNN_E_OVERFLOW, CNN_E_HIP.
+ */
+int cnn_plan_lookup(const cnn_problem* prob, int dtype, cnn_plan_t* plan);
 
 /*
  * Build the plan for a requested kernel family and tiling (tests, tuning).

@@ -28,8 +28,8 @@ STATUS = {0: "CNN_OK", -1: "CNN_E_NULL", -2: "CNN_E_SHAPE", -3: "CNN_E_DTYPE",
           -7: "CNN_E_HIP", -8: "CNN_E_PLAN"}
 
 # Every symbol include/cnn.h declares.
-EXPORTS = ["cnn_fwd", "cnn_plan", "cnn_plan_tiles", "cnn_fwd_plan", "cnn_fwd_plan_ws", "cnn_eq1_cost",
-           "cnn_slab_cost", "cnn_device_budget", "cnn_strerror", "cnn_last_error",
+EXPORTS = ["cnn_fwd", "cnn_plan", "cnn_plan_find", "cnn_plan_lookup", "cnn_plan_tiles",
+           "cnn_fwd_plan", "cnn_fwd_plan_ws", "cnn_eq1_cost", "cnn_slab_cost", "cnn_device_budget", "cnn_strerror", "cnn_last_error",
            "cnn_abi_version"]
 
 i64 = ctypes.c_int64
@@ -85,6 +85,8 @@ def lib():
     P, T, B, PL = (ctypes.POINTER(x) for x in (Problem, Tiles, Budget, Plan))
     L.cnn_fwd.argtypes = [vp, vp, vp] + [i64] * 9 + [ctypes.c_int, vp]
     L.cnn_plan.argtypes = [P, ctypes.c_int, B, PL]
+    L.cnn_plan_find.argtypes = [vp, vp, vp, P, ctypes.c_int, vp, PL, ctypes.POINTER(ctypes.c_double)]
+    L.cnn_plan_lookup.argtypes = [P, ctypes.c_int, PL]
     L.cnn_plan_tiles.argtypes = [P, ctypes.c_int, ctypes.c_int, i64, i64, i64, B, PL]
     L.cnn_fwd_plan.argtypes = [vp, vp, vp, P, ctypes.c_int, PL, vp]
     L.cnn_fwd_plan_ws.argtypes = [vp, vp, vp, P, ctypes.c_int, PL, vp, i64, vp]
@@ -97,7 +99,7 @@ def lib():
     L.cnn_last_error.argtypes = []
     L.cnn_last_error.restype = ctypes.c_char_p
     L.cnn_abi_version.argtypes = []
-    for f in ("cnn_fwd", "cnn_plan", "cnn_plan_tiles", "cnn_fwd_plan", "cnn_fwd_plan_ws", "cnn_eq1_cost",
+    for f in ("cnn_fwd", "cnn_plan", "cnn_plan_find", "cnn_plan_lookup", "cnn_plan_tiles", "cnn_fwd_plan", "cnn_fwd_plan_ws", "cnn_eq1_cost",
               "cnn_slab_cost", "cnn_device_budget", "cnn_abi_version"):
         getattr(L, f).restype = ctypes.c_int
     _lib = L
@@ -127,6 +129,13 @@ def plan(prob: Problem, dtype: int, bud: Budget | None = None) -> Plan:
     pl = Plan()
     _check(lib().cnn_plan(ctypes.byref(prob), dtype, ctypes.byref(bud) if bud else None,
                           ctypes.byref(pl)))
+    return pl
+
+
+def plan_lookup(prob: Problem, dtype: int) -> Plan:
+    """The plan cnn_fwd uses for (prob, dtype) on the current device."""
+    pl = Plan()
+    _check(lib().cnn_plan_lookup(ctypes.byref(prob), dtype, ctypes.byref(pl)))
     return pl
 
 
@@ -212,6 +221,18 @@ def fwd(In, Ker, Out, sw: int = 1, sh: int = 1, stream=None):
     dims, dt = _tensor_dims(In, Ker, Out, sw, sh)
     fwd_ptr(In.data_ptr(), Ker.data_ptr(), Out.data_ptr(), dims, dt, _stream(stream))
     return Out
+
+
+def plan_find(In, Ker, Out, sw: int = 1, sh: int = 1, stream=None):
+    """cnn_plan_find: time every feasible tiling on these buffers, cache and
+    return (plan, mean ms) of the fastest.  Synchronises the stream."""
+    dims, dt = _tensor_dims(In, Ker, Out, sw, sh)
+    pl = Plan()
+    ms = ctypes.c_double()
+    _check(lib().cnn_plan_find(In.data_ptr(), Ker.data_ptr(), Out.data_ptr(),
+                               ctypes.byref(problem(*dims)), dt, _stream(stream),
+                               ctypes.byref(pl), ctypes.byref(ms)))
+    return pl, ms.value
 
 
 def fwd_plan(In, Ker, Out, pl: Plan, sw: int = 1, sh: int = 1, stream=None):

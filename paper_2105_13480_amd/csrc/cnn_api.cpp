@@ -6,6 +6,7 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <algorithm>
 #include <map>
 #include <mutex>
 #include <string>
@@ -19,6 +20,8 @@ int select_plan(const cnn_problem& p, int dtype, const cnn_budget& bud, int kern
 void eq1_terms(const cnn_problem& p, const cnn_tiles& t, int exact, double terms[3],
                double* footprint);
 void slab_terms(const cnn_problem& p, int64_t tk, int64_t tp, double terms[3]);
+int enumerate_plans(const cnn_problem& p, int dtype, const cnn_budget& bud, cnn_plan_t* out,
+                    int cap);
 }  // namespace cnnlib
 
 using namespace cnnlib;
@@ -347,6 +350,107 @@ int cnn_fwd_plan_ws(const void* In, const void* Ker, void* Out, const cnn_proble
   return run_plan(In, Ker, Out, *plan, (hipStream_t)stream, workspace);
 }
 
+// The plan cnn_fwd uses on the current device: the cached one (the model's
+// choice, or the winner of cnn_plan_find), else the model's choice, cached.
+static int current_plan(const cnn_problem& p, int dtype, cnn_plan_t* plan) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(CNN_E_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+  const Key key(p.Nb, p.Nc, p.Nk, p.Nw, p.Nh, p.Nr, p.Ns, p.sw, p.sh, dtype, dev);
+  {
+    std::lock_guard<std::mutex> g(g_cache_mu);
+    auto it = g_cache.find(key);
+    if (it != g_cache.end()) {
+      *plan = it->second;
+      return CNN_OK;
+    }
+  }
+  cnn_budget bud;
+  int st;
+  if ((st = cnn_device_budget(dev, &bud))) return st;
+  if ((st = select_plan(p, dtype, bud, CNN_K_AUTO, 0, 0, 0, plan)))
+    return fail(st, "tile selection failed");
+  std::lock_guard<std::mutex> g(g_cache_mu);
+  g_cache.emplace(key, *plan);  // keeps a plan another thread stored first
+  *plan = g_cache[key];
+  return CNN_OK;
+}
+
+int cnn_plan_lookup(const cnn_problem* prob, int dtype, cnn_plan_t* plan) {
+  if (!prob || !plan) return fail(CNN_E_NULL, "prob and plan must be non-NULL");
+  int st;
+  if ((st = check_problem(*prob)) || (st = check_dtype(dtype))) return st;
+  return current_plan(*prob, dtype, plan);
+}
+
+int cnn_plan_find(const void* In, const void* Ker, void* Out, const cnn_problem* prob, int dtype,
+                  void* stream, cnn_plan_t* plan, double* best_ms) {
+  if (!prob || !plan) return fail(CNN_E_NULL, "prob and plan must be non-NULL");
+  int st;
+  if ((st = check_problem(*prob)) || (st = check_dtype(dtype))) return st;
+  if ((st = check_buffers(In, Ker, Out, *prob, dtype))) return st;
+  hipStream_t hs = (hipStream_t)stream;
+  hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+  hipError_t e = hipStreamIsCapturing(hs, &cap);
+  if (e != hipSuccess) return fail(CNN_E_HIP, "hipStreamIsCapturing: %s", hipGetErrorString(e));
+  if (cap != hipStreamCaptureStatusNone)
+    return fail(CNN_E_UNSUPPORTED, "cnn_plan_find times kernels and cannot run under capture");
+  int dev = 0;
+  if ((e = hipGetDevice(&dev)) != hipSuccess)
+    return fail(CNN_E_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+  cnn_budget bud;
+  if ((st = cnn_device_budget(dev, &bud))) return st;
+  static const int kCap = 128;
+  cnn_plan_t* cands = new cnn_plan_t[kCap];
+  const int n = enumerate_plans(*prob, dtype, bud, cands, kCap);
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  if ((e = hipEventCreate(&e0)) != hipSuccess || (e = hipEventCreate(&e1)) != hipSuccess) {
+    if (e0) (void)hipEventDestroy(e0);
+    delete[] cands;
+    return fail(CNN_E_HIP, "hipEventCreate: %s", hipGetErrorString(e));
+  }
+  int best = -1;
+  float best_t = 0.f;
+  // Times `reps` back-to-back runs of candidate i; -1 on a launch error.
+  auto time_it = [&](int i, int reps, float* ms) -> int {
+    int s2;
+    if ((e = hipEventRecord(e0, hs)) != hipSuccess) return fail(CNN_E_HIP, "hipEventRecord: %s", hipGetErrorString(e));
+    for (int r = 0; r < reps; ++r)
+      if ((s2 = run_plan(In, Ker, Out, cands[i], hs))) return s2;
+    if ((e = hipEventRecord(e1, hs)) != hipSuccess || (e = hipEventSynchronize(e1)) != hipSuccess ||
+        (e = hipEventElapsedTime(ms, e0, e1)) != hipSuccess)
+      return fail(CNN_E_HIP, "timing: %s", hipGetErrorString(e));
+    *ms /= (float)reps;
+    return CNN_OK;
+  };
+  st = CNN_OK;
+  for (int i = 0; i < n && st == CNN_OK; ++i) {
+    float t1 = 0.f, t = 0.f;
+    if ((st = time_it(i, 1, &t1))) break;  // first run: workspace, caches
+    const int reps = t1 <= 0.f ? 20 : std::max(3, std::min(20, (int)(2.0f / t1)));
+    if ((st = time_it(i, reps, &t))) break;
+    if (best < 0 || t < best_t) {
+      best = i;
+      best_t = t;
+    }
+  }
+  (void)hipEventDestroy(e0);
+  (void)hipEventDestroy(e1);
+  if (st == CNN_OK) {
+    // Leave Out holding the winner's result, like a cnn_fwd call would.
+    st = run_plan(In, Ker, Out, cands[best], hs);
+  }
+  if (st == CNN_OK) {
+    *plan = cands[best];
+    if (best_ms) *best_ms = best_t;
+    const cnn_problem& p = *prob;
+    std::lock_guard<std::mutex> g(g_cache_mu);
+    g_cache[Key(p.Nb, p.Nc, p.Nk, p.Nw, p.Nh, p.Nr, p.Ns, p.sw, p.sh, dtype, dev)] = cands[best];
+  }
+  delete[] cands;
+  return st;
+}
+
 int cnn_fwd(const void* In, const void* Ker, void* Out, int64_t Nb, int64_t Nc, int64_t Nk,
             int64_t Nw, int64_t Nh, int64_t Nr, int64_t Ns, int64_t sw, int64_t sh, int dtype,
             void* stream) {
@@ -354,28 +458,8 @@ int cnn_fwd(const void* In, const void* Ker, void* Out, int64_t Nb, int64_t Nc, 
   int st;
   if ((st = check_problem(p)) || (st = check_dtype(dtype))) return st;
   if ((st = check_buffers(In, Ker, Out, p, dtype))) return st;
-  int dev = 0;
-  hipError_t e = hipGetDevice(&dev);
-  if (e != hipSuccess) return fail(CNN_E_HIP, "hipGetDevice: %s", hipGetErrorString(e));
-  const Key key(Nb, Nc, Nk, Nw, Nh, Nr, Ns, sw, sh, dtype, dev);
   cnn_plan_t plan;
-  bool hit = false;
-  {
-    std::lock_guard<std::mutex> g(g_cache_mu);
-    auto it = g_cache.find(key);
-    if (it != g_cache.end()) {
-      plan = it->second;
-      hit = true;
-    }
-  }
-  if (!hit) {
-    cnn_budget bud;
-    if ((st = cnn_device_budget(dev, &bud))) return st;
-    if ((st = select_plan(p, dtype, bud, CNN_K_AUTO, 0, 0, 0, &plan)))
-      return fail(st, "tile selection failed");
-    std::lock_guard<std::mutex> g(g_cache_mu);
-    g_cache[key] = plan;
-  }
+  if ((st = current_plan(p, dtype, &plan))) return st;
   return run_plan(In, Ker, Out, plan, (hipStream_t)stream);
 }
 

@@ -321,4 +321,37 @@ int select_plan(const cnn_problem& p, int dtype, const cnn_budget& bud, int kern
   return CNN_OK;
 }
 
+int enumerate_plans(const cnn_problem& p, int dtype, const cnn_budget& bud, cnn_plan_t* out,
+                    int cap) {
+  int n = 0;
+  auto add = [&](cnn_plan_t& cand, int kernel) {
+    if (n >= cap) return;
+    cand.kernel = kernel;
+    fill_common(p, dtype, &cand);
+    out[n++] = cand;
+  };
+  double t;
+  cnn_plan_t cand;
+  int n4 = 0, n3 = 0, n2 = 0, n1 = 0;
+  const Variant4* vs4 = variants4(&n4);
+  for (int i = 0; i < n4; ++i)
+    if (vs4[i].dtype == dtype && eval_variant4(p, dtype, vs4[i], bud, &cand, &t))
+      add(cand, CNN_K_IGEMM_WIDE);
+  const Variant3* vs3 = variants3(&n3);
+  for (int i = 0; i < n3; ++i)
+    if (vs3[i].dtype == dtype && eval_variant3(p, dtype, vs3[i], bud, &cand, &t))
+      add(cand, CNN_K_IGEMM_DMA);
+  const Variant2* vs2 = variants2(&n2);
+  for (int i = 0; i < n2; ++i)
+    if (vs2[i].dtype == dtype && eval_variant2(p, dtype, vs2[i], bud, &cand, &t))
+      add(cand, CNN_K_IGEMM_PIPE);
+  const Variant* vs = variants(&n1);
+  for (int i = 0; i < n1; ++i)
+    if (vs[i].dtype == dtype && vs[i].kernel == CNN_K_IGEMM &&
+        eval_variant(p, dtype, vs[i], bud, &cand, &t))
+      add(cand, CNN_K_IGEMM);
+  if (n == 0 && cap > 0) direct_plan(p, dtype, &out[n++]);
+  return n;
+}
+
 }  // namespace cnnlib

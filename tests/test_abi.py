@@ -165,3 +165,23 @@ def test_every_instantiation_has_a_fitting_test_shape():
     for case in variant_cases():
         kernel, vid, dt, tk, tp, tc, stencil = case
         assert variant_dims(kernel, vid, dt, tk, tp, tc, stencil) is not None, vid
+
+
+def test_plan_find_and_lookup_validate_before_hip():
+    L = cnn.lib()
+    p = cnn.problem(*DIMS)
+    pl = cnn.Plan()
+    assert L.cnn_plan_find(0x1000, 0x100000, 0x200000, None, cnn.CNN_F32, None,
+                           ctypes.byref(pl), None) == -1
+    assert L.cnn_plan_find(0, 0x100000, 0x200000, ctypes.byref(p), cnn.CNN_F32, None,
+                           ctypes.byref(pl), None) == -1
+    assert L.cnn_plan_find(0x1000, 0x100000, 0x200000, ctypes.byref(p), 9, None,
+                           ctypes.byref(pl), None) == -3
+    q = cnn.problem(2, 3, 4, 0, 6, 3, 3, 1, 1)
+    assert L.cnn_plan_find(0x1000, 0x100000, 0x200000, ctypes.byref(q), cnn.CNN_F32, None,
+                           ctypes.byref(pl), None) == -2
+    assert L.cnn_plan_find(0x200000 - 8, 0x100000, 0x200000, ctypes.byref(p), cnn.CNN_F32,
+                           None, ctypes.byref(pl), None) == -5
+    assert L.cnn_plan_lookup(None, cnn.CNN_F32, ctypes.byref(pl)) == -1
+    assert L.cnn_plan_lookup(ctypes.byref(p), 5, ctypes.byref(pl)) == -3
+    assert L.cnn_plan_lookup(ctypes.byref(q), cnn.CNN_F32, ctypes.byref(pl)) == -2

@@ -152,3 +152,34 @@ def test_bad_arguments_raise_before_launch():
     with pytest.raises(cnn.CnnError):
         cnn.fwd_ptr(dIn.data_ptr(), dKer.data_ptr(), out.data_ptr(), dims, 9)
     torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("mode", ["bf16", "f32"])
+def test_plan_find_exact_and_cached(mode):
+    """cnn_plan_find times every feasible tiling, leaves the winner's result
+    in Out, and cnn_fwd then uses the winner."""
+    import torch
+    dims = (3, 40, 70, 13, 11, 3, 3, 1, 1)
+    Nb, Nc, Nk, Nw, Nh, Nr, Ns, sw, sh = dims
+    rng = np.random.default_rng(77)
+    Nx, Ny = sw * (Nw - 1) + Nr, sh * (Nh - 1) + Ns
+    In = rng.integers(-2, 3, size=(Nb, Nc, Nx, Ny)).astype(np.float32)
+    Ker = rng.integers(-2, 3, size=(Nk, Nc, Nr, Ns)).astype(np.float32)
+    if mode == "bf16":
+        In, Ker = inputs.f32_to_bf16_bits(In), inputs.f32_to_bf16_bits(Ker)
+    want = oracle.conv(In, Ker, sw, sh)
+    dIn, dKer = to_gpu(In), to_gpu(Ker)
+    dOut = out_tensor(Nb, Nk, Nw, Nh, mode)
+    say(f"[parity] plan_find dims={dims} mode={mode}")
+    pl, ms = cnn.plan_find(dIn, dKer, dOut, sw, sh)
+    torch.cuda.synchronize()
+    assert ms > 0
+    assert np.array_equal(to_host64(dOut), want)
+    cached = cnn.plan_lookup(cnn.problem(*dims), MODES[mode])
+    assert (cached.kernel, cached.variant, cached.tk, cached.tp, cached.tc) == \
+        (pl.kernel, pl.variant, pl.tk, pl.tp, pl.tc)
+    dOut.fill_(float("nan"))
+    say(f"[parity] cnn_fwd after plan_find dims={dims} mode={mode}")
+    cnn.fwd(dIn, dKer, dOut, sw, sh)
+    torch.cuda.synchronize()
+    assert np.array_equal(to_host64(dOut), want)
