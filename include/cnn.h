@@ -88,9 +88,12 @@ typedef enum cnn_kernel {
                          through registers, both double-buffered in LDS               */
   CNN_K_IGEMM_DMA = 6,/* implicit GEMM, bf16: Ker and the natural In rows both copied
                          by 16-byte DMA into a ring of LDS buffers, In transposed in LDS */
-  CNN_K_IGEMM_WIDE = 7/* implicit GEMM, bf16: In staged as 8x8 (position x channel)
+  CNN_K_IGEMM_WIDE = 7,/* implicit GEMM, bf16: In staged as 8x8 (position x channel)
                          blocks of 16-byte loads transposed in registers, swizzled LDS,
                          MFMA operands prefetched one K-step ahead                  */
+  CNN_K_IGEMM_RAWK = 8 /* as CNN_K_IGEMM_PIPE for fixed 3x3 / 1x1 stencils, Nc % 8 == 0:
+                         raw Ker rows copied by DMA, MFMA operands built in registers,
+                         no repack and no workspace                                 */
 } cnn_kernel;
 
 /*

@@ -62,16 +62,26 @@ IGEMM = [
 ]
 
 
-# (id, dtype, wm, wn, mb, nb, tc, nr, ns, maxp) of the pipelined kernel.
+# (id, dtype, wm, wn, mb, nb, tc, nr, ns, maxp, rawk) of the pipelined
+# kernel; rawk = 1: Ker staged from its raw rows (Nc must be a multiple of 8),
+# LDS rows of (taps*tc/8 rounded up to odd) 16-byte chunks per feature.
 IGEMM2 = [
-    (400, BF16, 1, 4, 2, 2, 16, 3, 3, 3), (401, BF16, 2, 2, 2, 2, 16, 3, 3, 3),
-    (402, BF16, 2, 2, 2, 4, 16, 3, 3, 3), (404, BF16, 1, 4, 2, 2, 32, 3, 3, 2),
-    (410, BF16, 1, 4, 2, 2, 16, 0, 0, 4), (411, BF16, 2, 2, 2, 4, 16, 0, 0, 4),
-    (412, BF16, 4, 1, 2, 4, 16, 0, 0, 4),
-    (500, BF16_OBF16, 1, 4, 2, 2, 16, 3, 3, 3), (501, BF16_OBF16, 2, 2, 2, 2, 16, 3, 3, 3),
-    (502, BF16_OBF16, 2, 2, 2, 4, 16, 3, 3, 3), (504, BF16_OBF16, 1, 4, 2, 2, 32, 3, 3, 2),
-    (510, BF16_OBF16, 1, 4, 2, 2, 16, 0, 0, 4), (511, BF16_OBF16, 2, 2, 2, 4, 16, 0, 0, 4),
-    (512, BF16_OBF16, 4, 1, 2, 4, 16, 0, 0, 4),
+    (400, BF16, 1, 4, 2, 2, 16, 3, 3, 3, 0), (401, BF16, 2, 2, 2, 2, 16, 3, 3, 3, 0),
+    (402, BF16, 2, 2, 2, 4, 16, 3, 3, 3, 0), (404, BF16, 1, 4, 2, 2, 32, 3, 3, 2, 0),
+    (410, BF16, 1, 4, 2, 2, 16, 0, 0, 4, 0), (411, BF16, 2, 2, 2, 4, 16, 0, 0, 4, 0),
+    (412, BF16, 4, 1, 2, 4, 16, 0, 0, 4, 0),
+    (420, BF16, 1, 4, 2, 2, 16, 3, 3, 3, 1), (421, BF16, 2, 2, 2, 2, 16, 3, 3, 3, 1),
+    (422, BF16, 2, 2, 2, 4, 16, 3, 3, 3, 1), (424, BF16, 1, 4, 2, 2, 32, 3, 3, 2, 1),
+    (430, BF16, 1, 4, 2, 2, 16, 1, 1, 4, 1), (431, BF16, 2, 2, 2, 4, 16, 1, 1, 4, 1),
+    (432, BF16, 4, 1, 2, 4, 16, 1, 1, 4, 1),
+    (500, BF16_OBF16, 1, 4, 2, 2, 16, 3, 3, 3, 0), (501, BF16_OBF16, 2, 2, 2, 2, 16, 3, 3, 3, 0),
+    (502, BF16_OBF16, 2, 2, 2, 4, 16, 3, 3, 3, 0), (504, BF16_OBF16, 1, 4, 2, 2, 32, 3, 3, 2, 0),
+    (510, BF16_OBF16, 1, 4, 2, 2, 16, 0, 0, 4, 0), (511, BF16_OBF16, 2, 2, 2, 4, 16, 0, 0, 4, 0),
+    (512, BF16_OBF16, 4, 1, 2, 4, 16, 0, 0, 4, 0),
+    (520, BF16_OBF16, 1, 4, 2, 2, 16, 3, 3, 3, 1), (521, BF16_OBF16, 2, 2, 2, 2, 16, 3, 3, 3, 1),
+    (522, BF16_OBF16, 2, 2, 2, 4, 16, 3, 3, 3, 1), (524, BF16_OBF16, 1, 4, 2, 2, 32, 3, 3, 2, 1),
+    (530, BF16_OBF16, 1, 4, 2, 2, 16, 1, 1, 4, 1), (531, BF16_OBF16, 2, 2, 2, 4, 16, 1, 1, 4, 1),
+    (532, BF16_OBF16, 4, 1, 2, 4, 16, 1, 1, 4, 1),
 ]
 
 
@@ -103,6 +113,17 @@ IGEMM4 = [
     (910, BF16_OBF16, 4, 1, 2, 4, 32, 1, 1, 1), (911, BF16_OBF16, 2, 2, 2, 4, 32, 1, 1, 1),
     (912, BF16_OBF16, 4, 1, 2, 4, 64, 1, 1, 1), (920, BF16_OBF16, 1, 4, 2, 2, 16, 0, 0, 2),
 ]
+
+
+def balanced_tp(p: eq1.Problem, tp_max: int, tk: int, slots: int) -> int:
+    """Outputs per tile: as many rounds of `slots` workgroups as tiles of
+    tp_max outputs need, and within them the most (hence smallest, equal)
+    tiles -- each processor's share N/P of Eq. (2).  Never below 32."""
+    npix = p.Nb * p.Nw * p.Nh
+    nk = -(-p.Nk // tk)
+    rounds = -(-(-(-npix // tp_max) * nk) // slots)
+    ptiles = max(1, (rounds * slots) // nk)
+    return min(tp_max, max(-(-npix // ptiles), min(tp_max, 32)))
 
 
 def _max_slab(p: eq1.Problem, tp: int) -> int:
@@ -172,20 +193,32 @@ def candidates(p: eq1.Problem, dtype: int, cus: int, lds_bytes: int, acc_regs: i
             yield t, tk, tp, tc, vid, info
         return
     if tier == 1:
-        for vid, dt, wm, wn, mb, nb, tc, nr, ns, maxp in IGEMM2:
+        for vid, dt, wm, wn, mb, nb, tc, nr, ns, maxp, rawk in IGEMM2:
             if dt != dtype or (nr > 0 and (nr, ns) != (p.Nr, p.Ns)):
                 continue
-            tk, tp, acc = 32 * wm * mb, 32 * wn * nb, 16 * mb * nb
+            if rawk and (p.Nc % 8 or (p.Nk + 512) * p.Nc * RS * 2 >= 2 ** 31):
+                continue
+            tk, tp_max, acc = 32 * wm * mb, 32 * wn * nb, 16 * mb * nb
+            if rawk:
+                row = RS * tc // 8
+                row += 1 - row % 2
+                blk = math.ceil(tk * row / 64) * 64
+            else:
+                blk = math.ceil(RS * (tc // 8) * tk / 256) * 256
+
+            def lds_of(S):
+                return 2 * ((tc // 8) * ((S * p.Ny + 1) // 2 * 2) + blk) * 16
+
+            wgs = max(1, min(wg_per_cu, lds_bytes // lds_of(_max_slab(p, tp_max))))
+            tp = balanced_tp(p, tp_max, tk, cus * wgs)
             S = _max_slab(p, tp)
             if math.ceil(S * p.Ny / 2) > 256 * maxp:
                 continue
-            imgs = tp // (p.Nw * p.Nh) + 2
+            imgs = tp_max // (p.Nw * p.Nh) + 2
             if (imgs * p.Nc * p.Nx * p.Ny * 2 >= 2 ** 31
                     or imgs * p.Nk * p.Nw * p.Nh * e_out >= 2 ** 31):
                 continue
-            blk = math.ceil(RS * (tc // 8) * tk / 256) * 256
-            sn = (S * p.Ny + 1) // 2 * 2
-            lds = 2 * ((tc // 8) * sn + blk) * 16
+            lds = lds_of(S)
             if lds > lds_bytes or acc > acc_regs:
                 continue
             t, info = _cost(p, dtype, tk, tp, tc, lds, cus, lds_bytes, wg_per_cu)
@@ -208,16 +241,23 @@ def candidates(p: eq1.Problem, dtype: int, cus: int, lds_bytes: int, acc_regs: i
 
 def choose(p: eq1.Problem, dtype: int, cus=256, lds_bytes=160 * 1024, acc_regs=128,
            wg_per_cu=2):
-    """(kernel, variant id, tk, tp, tc) the rule above selects; kernel 6 is
-    the DMA-staged family, 5 the register-staged pipelined one, 2 the plain
-    staging one, 1 the direct kernel."""
+    """(kernel, variant id, tk, tp, tc) the rule above selects; kernel 7 is
+    the wide-staging family, 6 the DMA-staged one, 5 the register-staged
+    pipelined one (8 when it stages raw Ker rows), 2 the plain staging one,
+    1 the direct kernel."""
+    rawk_ids = {row[0] for row in IGEMM2 if row[10]}
     best = None
     for tier in (0, 1, 2):
         for t, tk, tp, tc, vid, info in candidates(p, dtype, cus, lds_bytes, acc_regs,
                                                    wg_per_cu, tier):
             key = (t, -tk, -tp, -tc, vid)
             if best is None or key < best[0]:
-                kern = (7 if vid >= 800 else 6) if tier == 0 else (5 if tier == 1 else 2)
+                if tier == 0:
+                    kern = 7 if vid >= 800 else 6
+                elif tier == 1:
+                    kern = 8 if vid in rawk_ids else 5
+                else:
+                    kern = 2
                 best = (key, (kern, vid, tk, tp, tc))
         if best is not None:
             break

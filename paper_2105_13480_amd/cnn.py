@@ -19,9 +19,11 @@ LIB_PATH = os.path.join(_HERE, "libcnn_mi355x.so")
 CNN_F32, CNN_BF16, CNN_BF16_OBF16 = 0, 1, 2
 DTYPES = {"f32": CNN_F32, "bf16": CNN_BF16, "bf16_obf16": CNN_BF16_OBF16}
 
-K_AUTO, K_DIRECT, K_IGEMM, K_POINTWISE, K_SMALLC, K_IGEMM_PIPE, K_IGEMM_DMA, K_IGEMM_WIDE = range(8)
+(K_AUTO, K_DIRECT, K_IGEMM, K_POINTWISE, K_SMALLC, K_IGEMM_PIPE, K_IGEMM_DMA, K_IGEMM_WIDE,
+ K_IGEMM_RAWK) = range(9)
 KERNEL_NAMES = {K_DIRECT: "direct", K_IGEMM: "igemm", K_POINTWISE: "pointwise", K_SMALLC: "smallc",
-                K_IGEMM_PIPE: "igemm_pipe", K_IGEMM_DMA: "igemm_dma", K_IGEMM_WIDE: "igemm_wide"}
+                K_IGEMM_PIPE: "igemm_pipe", K_IGEMM_DMA: "igemm_dma", K_IGEMM_WIDE: "igemm_wide",
+                K_IGEMM_RAWK: "igemm_rawk"}
 
 STATUS = {0: "CNN_OK", -1: "CNN_E_NULL", -2: "CNN_E_SHAPE", -3: "CNN_E_DTYPE",
           -4: "CNN_E_OVERFLOW", -5: "CNN_E_ALIAS", -6: "CNN_E_UNSUPPORTED",

@@ -52,6 +52,7 @@ struct Variant2 {
   int32_t acc;      // fp32 accumulators per lane
   int32_t nr, ns;   // compile-time stencil (0 = any)
   int32_t maxp;     // slab position pairs per thread: ceil(S*Ny/2) <= 256*maxp
+  int32_t rawk;     // 1: stages raw Ker rows (needs Nc % 8 == 0), no repack / workspace
 };
 const Variant2* variants2(int* count);
 int64_t igemm2_blk_vecs(const Variant2& v, int64_t RS);
@@ -107,7 +108,8 @@ hipError_t launch_igemm(const Variant& v, const void* In, const void* Ker, void*
                         const ConvArgs& a, int64_t lds_bytes, hipStream_t stream);
 hipError_t launch_igemm3(const Variant3& v, const void* In, const void* Ker, void* Out,
                          void* ws, const ConvArgs& a, int64_t lds_bytes, hipStream_t stream);
-// Packs Ker into `ws` (igemm2_ws_bytes) and runs the pipelined kernel.
+// Runs the pipelined kernel; non-raw-Ker variants first pack Ker into `ws`
+// (igemm2_ws_bytes).
 hipError_t launch_igemm2(const Variant2& v, const void* In, const void* Ker, void* Out,
                          void* ws, const ConvArgs& a, int64_t lds_bytes, hipStream_t stream);
 

@@ -5,11 +5,16 @@
 // the input features tc at a time), with the data movement rebuilt for the
 // CDNA4 memory system:
 //
-// * Ker is repacked once per call by pack_ker into the exact LDS image of
-//   every (k tile, c stage) block: [tap][c/8][k][8].  A workgroup then
-//   streams its Ker blocks with 16-byte global->LDS DMA loads
-//   (global_load_lds_dwordx4): no registers, fully coalesced.  Without the
-//   repack every workgroup would transpose the whole Ker tile itself.
+// * Ker, fixed stencils (RAWK) with Nc a multiple of 8: the stage's raw Ker
+//   rows -- for each feature, its TC channels times all taps, one
+//   contiguous run of memory -- are copied with 16-byte buffer->LDS DMA,
+//   one padding chunk per row so the A-operand reads of 8 consecutive
+//   features hit distinct LDS banks.  A lane reads its feature's 8
+//   channels x RS taps (16*RS contiguous bytes) and builds each tap's
+//   MFMA operand with four v_perm: no repack kernel, no workspace.
+// * Ker, other problems: repacked once per call by pack_ker into the exact
+//   LDS image of every (k tile, c stage) block, [tap][c/8][k][8], which a
+//   workgroup streams with 16-byte global->LDS DMA loads.
 // * The halo'd In slab (whole input rows, see conv_igemm) is loaded as
 //   dwords -- two consecutive positions of one channel per lane, so each
 //   wave-wide load is a 256-byte contiguous run -- eight channels per work
@@ -19,6 +24,9 @@
 //   with a funnel shift; pairs that straddle an image use two 16-bit loads.
 // * Two LDS buffers per operand: the loads of stage i+1 are in flight while
 //   stage i runs on the MFMA units; one barrier per stage.
+// * The tile size a.tp is a run-time value up to TP (the lanes' capacity):
+//   the selector shrinks it so the tiles fill the machine's workgroup slots
+//   evenly (the P processors of Eq. (2) each get the same share).
 #include <type_traits>
 
 #include "internal.h"
@@ -94,13 +102,28 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, in
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, n, 0x00020000);
 }
 
-template <typename TO, int WM, int WN, int MB, int NB, int TC, int NR, int NS, int MAXP>
+// 16-byte buffer -> LDS copy (lane i's 16 bytes land at lds + 16 i, lds
+// wave-uniform); out-of-range reads give zeros.  Device-only builtin.
+__device__ __forceinline__ void dma16b(__amdgpu_buffer_rsrc_t r, void* lds, uint32_t voff) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, LDS_PTR(void, lds), 16, voff, 0, 0, 0);
+#endif
+}
+
+// Raw-Ker LDS row: RS*TC/8 16-byte chunks of one feature, padded to an odd
+// count (row strides of 8 consecutive features then start in distinct
+// 4-bank groups).
+__host__ __device__ constexpr int rawk_row_chunks(int RS, int TC) {
+  return (RS * TC / 8) | 1;
+}
+
+template <typename TO, int WM, int WN, int MB, int NB, int TC, int NR, int NS, int MAXP,
+          bool RAWK>
 __global__ __launch_bounds__(256) void conv_igemm2(const bf16_t* __restrict__ In,
                                                    const u32x4_t* __restrict__ Kp,
                                                    TO* __restrict__ Out, ConvArgs a,
                                                    int blk_vecs) {
   constexpr int TK = 32 * WM * MB;
-  constexpr int TP = 32 * WN * NB;
   constexpr int G = TC / 8;
   constexpr int KSTEPS = G / 2;
   static_assert(WM * WN == 4, "four waves");
@@ -119,12 +142,13 @@ __global__ __launch_bounds__(256) void conv_igemm2(const bf16_t* __restrict__ In
   const int wm = wave / WN, wn = wave % WN;
   const int l32 = lane & 31, half = lane >> 5;
 
+  static_assert(!RAWK || (NR > 0 && NS > 0), "raw Ker needs a compile-time stencil");
   const int tile = xcd_remap(blockIdx.x, gridDim.x);
   const int pt = tile / a.n_ktiles;
   const int kt = tile - pt * a.n_ktiles;
-  const int p0 = pt * TP;
+  const int p0 = pt * a.tp;
   const int k0 = kt * TK;
-  const int plast = min(p0 + TP, a.npix) - 1;
+  const int plast = min(p0 + a.tp, a.npix) - 1;
   const int b0 = p0 / a.hw, w0 = (p0 - b0 * a.hw) / a.Nh;
   const int b1 = plast / a.hw, w1 = (plast - b1 * a.hw) / a.Nh;
   const int G0 = b0 * a.Nx + a.sw * w0;
@@ -236,10 +260,37 @@ __global__ __launch_bounds__(256) void conv_igemm2(const bf16_t* __restrict__ In
     }
   };
   const int n_cc = (a.Nc + TC - 1) / TC;
+  // Raw Ker: LDS chunk slot v of a stage is feature k0 + v / RC chunk
+  // v % RC of that feature's run (chunks past RS*TC/8 are padding).
+  constexpr int RS_C = (NR > 0 ? NR : 1) * (NS > 0 ? NS : 1);
+  constexpr int RC = rawk_row_chunks(RS_C, TC);
+  constexpr int RAW_VECS = (TK * RC + 63) / 64 * 64;
+  constexpr int RAW_DMA = (RAW_VECS + 255) / 256;
+  const __amdgpu_buffer_rsrc_t ker_rsrc =
+      make_rsrc(reinterpret_cast<const bf16_t*>(Kp), (int64_t)a.Nk * a.Nc * RS_C * 2);
+  uint32_t raw_off[RAWK ? RAW_DMA : 1];
+  if constexpr (RAWK) {
+#pragma unroll
+    for (int j = 0; j < RAW_DMA; ++j) {
+      const int v = tid + 256 * j;
+      const int kk = v / RC;
+      const int part = v - kk * RC;
+      // padding chunks and rows past Nk read whatever is in range (or zeros)
+      raw_off[j] = (uint32_t)((((int64_t)(k0 + kk) * a.Nc) * RS_C) * 2 + 16 * part);
+    }
+  }
   auto dma_ker = [&](int cc, u32x4_t* dst) {
-    const u32x4_t* src = Kp + ((int64_t)kt * n_cc + cc) * blk_vecs;
-    for (int v0 = wave * 64; v0 < blk_vecs; v0 += 256)
-      __builtin_amdgcn_global_load_lds(src + v0 + lane, LDS_PTR(void, dst + v0), 16, 0, 0);
+    if constexpr (RAWK) {
+      const uint32_t so = (uint32_t)(cc * TC * RS_C * 2);
+#pragma unroll
+      for (int j = 0; j < RAW_DMA; ++j)
+        if (256 * j + wave * 64 < RAW_VECS)
+          dma16b(ker_rsrc, dst + 256 * j + wave * 64, raw_off[j] + so);
+    } else {
+      const u32x4_t* src = Kp + ((int64_t)kt * n_cc + cc) * blk_vecs;
+      for (int v0 = wave * 64; v0 < blk_vecs; v0 += 256)
+        __builtin_amdgcn_global_load_lds(src + v0 + lane, LDS_PTR(void, dst + v0), 16, 0, 0);
+    }
   };
 
   f32x16_t acc[MB][NB];
@@ -284,7 +335,56 @@ __global__ __launch_bounds__(256) void conv_igemm2(const bf16_t* __restrict__ In
                 acc[mb][nb], 0, 0, 0);
       }
     };
-    if constexpr (NR > 0 && NS > 0) {
+    if constexpr (RAWK) {
+      // Per K-step group: the lane's 8 channels x RS taps of each of its
+      // features (RS 16-byte LDS reads), then one operand per tap.
+      constexpr int RSD = RS_C * 4;  // dwords of a lane's run
+#pragma unroll
+      for (int j = 0; j < KSTEPS; ++j) {
+        const int grp = 2 * j + half;
+        const bool gv = cc * TC + 8 * grp < a.Nc;  // whole group in range (Nc % 8 == 0)
+        uint32_t raw[MB][RSD];
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) {
+          const u32x4_t* src = kb + ((wm * MB + mb) * 32 + l32) * RC + grp * RS_C;
+#pragma unroll
+          for (int q = 0; q < RS_C; ++q) {
+            const u32x4_t v = src[q];
+#pragma unroll
+            for (int d = 0; d < 4; ++d) raw[mb][4 * q + d] = gv ? v[d] : 0u;
+          }
+        }
+#pragma unroll
+        for (int r = 0; r < NR; ++r) {
+#pragma unroll
+          for (int s = 0; s < NS; ++s) {
+            const int tap = r * NS + s;
+            const int toff = r * a.Ny + s;
+            u32x4_t av[MB], bv[NB];
+#pragma unroll
+            for (int mb = 0; mb < MB; ++mb) {
+#pragma unroll
+              for (int i = 0; i < 4; ++i) {
+                // elements (channel 2i, tap) and (channel 2i+1, tap) of the run
+                const int e0 = (2 * i) * RS_C + tap, e1 = e0 + RS_C;
+                const uint32_t sel = ((e0 & 1) ? 0x0302u : 0x0100u) |
+                                     ((e1 & 1) ? 0x07060000u : 0x05040000u);
+                av[mb][i] = __builtin_amdgcn_perm(raw[mb][e1 >> 1], raw[mb][e0 >> 1], sel);
+              }
+            }
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb) bv[nb] = ib[grp * SN + pix[nb] + toff];
+#pragma unroll
+            for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+              for (int nb = 0; nb < NB; ++nb)
+                acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                    __builtin_bit_cast(bf16x8_t, av[mb]), __builtin_bit_cast(bf16x8_t, bv[nb]),
+                    acc[mb][nb], 0, 0, 0);
+          }
+        }
+      }
+    } else if constexpr (NR > 0 && NS > 0) {
 #pragma unroll
       for (int r = 0; r < NR; ++r)
 #pragma unroll
@@ -326,28 +426,43 @@ __global__ __launch_bounds__(256) void conv_igemm2(const bf16_t* __restrict__ In
 }
 
 // ---- instantiation table ----------------------------------------------------
-// (id, dtype, WM, WN, MB, NB, TC, NR, NS, MAXP): tk = 32*WM*MB, tp = 32*WN*NB;
+// (id, dtype, WM, WN, MB, NB, TC, NR, NS, MAXP, RAWK): tk = 32*WM*MB,
+// tp = 32*WN*NB (the largest tile; plans may use fewer outputs per tile);
 // NR = NS = 0 reads the stencil size at run time; MAXP position pairs per
-// thread bound the slab (ceil(S*Ny/2) <= 256*MAXP).
-#define CNN_IGEMM2_VARIANTS(X)                       \
-  X(400, CNN_BF16, 1, 4, 2, 2, 16, 3, 3, 3)          \
-  X(401, CNN_BF16, 2, 2, 2, 2, 16, 3, 3, 3)          \
-  X(402, CNN_BF16, 2, 2, 2, 4, 16, 3, 3, 3)          \
-  X(404, CNN_BF16, 1, 4, 2, 2, 32, 3, 3, 2)          \
-  X(410, CNN_BF16, 1, 4, 2, 2, 16, 0, 0, 4)          \
-  X(411, CNN_BF16, 2, 2, 2, 4, 16, 0, 0, 4)          \
-  X(412, CNN_BF16, 4, 1, 2, 4, 16, 0, 0, 4)          \
-  X(500, CNN_BF16_OBF16, 1, 4, 2, 2, 16, 3, 3, 3)    \
-  X(501, CNN_BF16_OBF16, 2, 2, 2, 2, 16, 3, 3, 3)    \
-  X(502, CNN_BF16_OBF16, 2, 2, 2, 4, 16, 3, 3, 3)    \
-  X(504, CNN_BF16_OBF16, 1, 4, 2, 2, 32, 3, 3, 2)    \
-  X(510, CNN_BF16_OBF16, 1, 4, 2, 2, 16, 0, 0, 4)    \
-  X(511, CNN_BF16_OBF16, 2, 2, 2, 4, 16, 0, 0, 4)    \
-  X(512, CNN_BF16_OBF16, 4, 1, 2, 4, 16, 0, 0, 4)
+// thread bound the slab (ceil(S*Ny/2) <= 256*MAXP); RAWK stages raw Ker.
+#define CNN_IGEMM2_VARIANTS(X)                          \
+  X(400, CNN_BF16, 1, 4, 2, 2, 16, 3, 3, 3, 0)          \
+  X(401, CNN_BF16, 2, 2, 2, 2, 16, 3, 3, 3, 0)          \
+  X(402, CNN_BF16, 2, 2, 2, 4, 16, 3, 3, 3, 0)          \
+  X(404, CNN_BF16, 1, 4, 2, 2, 32, 3, 3, 2, 0)          \
+  X(410, CNN_BF16, 1, 4, 2, 2, 16, 0, 0, 4, 0)          \
+  X(411, CNN_BF16, 2, 2, 2, 4, 16, 0, 0, 4, 0)          \
+  X(412, CNN_BF16, 4, 1, 2, 4, 16, 0, 0, 4, 0)          \
+  X(420, CNN_BF16, 1, 4, 2, 2, 16, 3, 3, 3, 1)          \
+  X(421, CNN_BF16, 2, 2, 2, 2, 16, 3, 3, 3, 1)          \
+  X(422, CNN_BF16, 2, 2, 2, 4, 16, 3, 3, 3, 1)          \
+  X(424, CNN_BF16, 1, 4, 2, 2, 32, 3, 3, 2, 1)          \
+  X(430, CNN_BF16, 1, 4, 2, 2, 16, 1, 1, 4, 1)          \
+  X(431, CNN_BF16, 2, 2, 2, 4, 16, 1, 1, 4, 1)          \
+  X(432, CNN_BF16, 4, 1, 2, 4, 16, 1, 1, 4, 1)          \
+  X(500, CNN_BF16_OBF16, 1, 4, 2, 2, 16, 3, 3, 3, 0)    \
+  X(501, CNN_BF16_OBF16, 2, 2, 2, 2, 16, 3, 3, 3, 0)    \
+  X(502, CNN_BF16_OBF16, 2, 2, 2, 4, 16, 3, 3, 3, 0)    \
+  X(504, CNN_BF16_OBF16, 1, 4, 2, 2, 32, 3, 3, 2, 0)    \
+  X(510, CNN_BF16_OBF16, 1, 4, 2, 2, 16, 0, 0, 4, 0)    \
+  X(511, CNN_BF16_OBF16, 2, 2, 2, 4, 16, 0, 0, 4, 0)    \
+  X(512, CNN_BF16_OBF16, 4, 1, 2, 4, 16, 0, 0, 4, 0)    \
+  X(520, CNN_BF16_OBF16, 1, 4, 2, 2, 16, 3, 3, 3, 1)    \
+  X(521, CNN_BF16_OBF16, 2, 2, 2, 2, 16, 3, 3, 3, 1)    \
+  X(522, CNN_BF16_OBF16, 2, 2, 2, 4, 16, 3, 3, 3, 1)    \
+  X(524, CNN_BF16_OBF16, 1, 4, 2, 2, 32, 3, 3, 2, 1)    \
+  X(530, CNN_BF16_OBF16, 1, 4, 2, 2, 16, 1, 1, 4, 1)    \
+  X(531, CNN_BF16_OBF16, 2, 2, 2, 4, 16, 1, 1, 4, 1)    \
+  X(532, CNN_BF16_OBF16, 4, 1, 2, 4, 16, 1, 1, 4, 1)
 
 static const Variant2 kVariants2[] = {
-#define CNN_ROW2(id, dt, wm, wn, mb, nb, tc, nr, ns, maxp) \
-  {id, dt, 32 * (wm) * (mb), 32 * (wn) * (nb), tc, 16 * (mb) * (nb), nr, ns, maxp},
+#define CNN_ROW2(id, dt, wm, wn, mb, nb, tc, nr, ns, maxp, rawk) \
+  {id, dt, 32 * (wm) * (mb), 32 * (wn) * (nb), tc, 16 * (mb) * (nb), nr, ns, maxp, rawk},
     CNN_IGEMM2_VARIANTS(CNN_ROW2)
 #undef CNN_ROW2
 };
@@ -358,6 +473,10 @@ const Variant2* variants2(int* count) {
 }
 
 int64_t igemm2_blk_vecs(const Variant2& v, int64_t RS) {
+  if (v.rawk) {
+    const int64_t n = v.tk * (int64_t)rawk_row_chunks((int)RS, v.tc);
+    return (n + 63) / 64 * 64;
+  }
   const int64_t n = RS * (v.tc / 8) * v.tk;
   return (n + 255) / 256 * 256;
 }
@@ -368,24 +487,32 @@ int64_t igemm2_lds_bytes(const Variant2& v, int64_t slab_rows, int64_t Ny, int64
 }
 
 int64_t igemm2_ws_bytes(const Variant2& v, const cnn_problem& p) {
+  if (v.rawk) return 0;
   const int64_t n_kt = (p.Nk + v.tk - 1) / v.tk, n_cc = (p.Nc + v.tc - 1) / v.tc;
   return n_kt * n_cc * igemm2_blk_vecs(v, p.Nr * p.Ns) * 16;
 }
 
-template <int DT, int WM, int WN, int MB, int NB, int TC, int NR, int NS, int MAXP>
+template <int DT, int WM, int WN, int MB, int NB, int TC, int NR, int NS, int MAXP, int RAWK>
 static hipError_t launch_one2(const void* In, const void* Ker, void* Out, void* ws,
                               const ConvArgs& a, int64_t lds, hipStream_t stream) {
   typedef typename std::conditional<DT == CNN_BF16, float, bf16_t>::type TO;
   constexpr int TK = 32 * WM * MB;
   const int64_t RS = (int64_t)a.Nr * a.Ns;
-  const int64_t blk = (RS * (TC / 8) * TK + 255) / 256 * 256;
-  const int64_t n_kt = (a.Nk + TK - 1) / TK, n_cc = (a.Nc + TC - 1) / TC;
-  const int64_t total = n_kt * n_cc * blk;
-  int64_t pgrid = (total + 255) / 256;
-  if (pgrid > 4096) pgrid = 4096;
-  hipLaunchKernelGGL(pack_ker_bf16, dim3((unsigned)pgrid), dim3(256), 0, stream,
-                     (const bf16_t*)Ker, (u32x4_t*)ws, a, TK, TC, (int)blk, total);
-  auto kern = conv_igemm2<TO, WM, WN, MB, NB, TC, NR, NS, MAXP>;
+  int64_t blk;
+  const void* kp = Ker;
+  if (RAWK) {
+    blk = (TK * (int64_t)rawk_row_chunks((int)RS, TC) + 63) / 64 * 64;
+  } else {
+    blk = (RS * (TC / 8) * TK + 255) / 256 * 256;
+    const int64_t n_kt = (a.Nk + TK - 1) / TK, n_cc = (a.Nc + TC - 1) / TC;
+    const int64_t total = n_kt * n_cc * blk;
+    int64_t pgrid = (total + 255) / 256;
+    if (pgrid > 4096) pgrid = 4096;
+    hipLaunchKernelGGL(pack_ker_bf16, dim3((unsigned)pgrid), dim3(256), 0, stream,
+                       (const bf16_t*)Ker, (u32x4_t*)ws, a, TK, TC, (int)blk, total);
+    kp = ws;
+  }
+  auto kern = conv_igemm2<TO, WM, WN, MB, NB, TC, NR, NS, MAXP, (RAWK != 0)>;
   static bool attr_set = false;
   if (!attr_set) {
     hipError_t e = hipFuncSetAttribute((const void*)kern,
@@ -394,16 +521,17 @@ static hipError_t launch_one2(const void* In, const void* Ker, void* Out, void* 
     attr_set = true;
   }
   hipLaunchKernelGGL(kern, dim3((unsigned)a.grid), dim3(256), (unsigned)lds, stream,
-                     (const bf16_t*)In, (const u32x4_t*)ws, (TO*)Out, a, (int)blk);
+                     (const bf16_t*)In, (const u32x4_t*)kp, (TO*)Out, a, (int)blk);
   return hipGetLastError();
 }
 
 hipError_t launch_igemm2(const Variant2& v, const void* In, const void* Ker, void* Out,
                          void* ws, const ConvArgs& a, int64_t lds_bytes, hipStream_t stream) {
   switch (v.id) {
-#define CNN_CASE2(id, dt, wm, wn, mb, nb, tc, nr, ns, maxp) \
-  case id:                                                  \
-    return launch_one2<dt, wm, wn, mb, nb, tc, nr, ns, maxp>(In, Ker, Out, ws, a, lds_bytes, stream);
+#define CNN_CASE2(id, dt, wm, wn, mb, nb, tc, nr, ns, maxp, rawk)                                  \
+  case id:                                                                                        \
+    return launch_one2<dt, wm, wn, mb, nb, tc, nr, ns, maxp, rawk>(In, Ker, Out, ws, a, lds_bytes, \
+                                                                   stream);
     CNN_IGEMM2_VARIANTS(CNN_CASE2)
 #undef CNN_CASE2
     default:
