@@ -82,8 +82,10 @@ typedef enum cnn_kernel {
   CNN_K_DIRECT = 1,   /* one thread per output, fp32 FMA; any shape (correctness path)  */
   CNN_K_IGEMM = 2,    /* implicit GEMM on MFMA, LDS-staged halo'd In slab + Ker tile,
                          element-wise staging (any dtype; fallback of CNN_K_IGEMM_PIPE) */
-  CNN_K_POINTWISE = 3,/* 1x1 kernels (any stride): strided gather, no halo              */
-  CNN_K_SMALLC = 4,   /* few input channels, wide stencils: K = (c, r, s) flattened     */
+  CNN_K_POINTWISE = 3,/* 1x1 stencils, any stride, bf16, Nc % 8 == 0: the inputs of the
+                         tile's outputs gathered (no halo, no unused rows), 64 channels
+                         per stage, raw Ker rows as in CNN_K_IGEMM_RAWK              */
+  CNN_K_SMALLC = 4,   /* reserved (few input channels, wide stencils); not built       */
   CNN_K_IGEMM_PIPE = 5,/* implicit GEMM, bf16: repacked Ker streamed by DMA, In staged
                          through registers, both double-buffered in LDS               */
   CNN_K_IGEMM_DMA = 6,/* implicit GEMM, bf16: Ker and the natural In rows both copied

@@ -62,26 +62,31 @@ IGEMM = [
 ]
 
 
-# (id, dtype, wm, wn, mb, nb, tc, nr, ns, maxp, rawk) of the pipelined
+# (id, dtype, wm, wn, mb, nb, tc, nr, ns, maxp, rawk, pw) of the pipelined
 # kernel; rawk = 1: Ker staged from its raw rows (Nc must be a multiple of 8),
-# LDS rows of (taps*tc/8 rounded up to odd) 16-byte chunks per feature.
+# LDS rows of (taps*tc/8 rounded up to odd) 16-byte chunks per feature;
+# pw = 1: 1x1 gather, stages the tile's outputs (pairs: ceil(tp/2)).
 IGEMM2 = [
-    (400, BF16, 1, 4, 2, 2, 16, 3, 3, 3, 0), (401, BF16, 2, 2, 2, 2, 16, 3, 3, 3, 0),
-    (402, BF16, 2, 2, 2, 4, 16, 3, 3, 3, 0), (404, BF16, 1, 4, 2, 2, 32, 3, 3, 2, 0),
-    (410, BF16, 1, 4, 2, 2, 16, 0, 0, 4, 0), (411, BF16, 2, 2, 2, 4, 16, 0, 0, 4, 0),
-    (412, BF16, 4, 1, 2, 4, 16, 0, 0, 4, 0),
-    (420, BF16, 1, 4, 2, 2, 16, 3, 3, 3, 1), (421, BF16, 2, 2, 2, 2, 16, 3, 3, 3, 1),
-    (422, BF16, 2, 2, 2, 4, 16, 3, 3, 3, 1), (424, BF16, 1, 4, 2, 2, 32, 3, 3, 2, 1),
-    (430, BF16, 1, 4, 2, 2, 16, 1, 1, 4, 1), (431, BF16, 2, 2, 2, 4, 16, 1, 1, 4, 1),
-    (432, BF16, 4, 1, 2, 4, 16, 1, 1, 4, 1),
-    (500, BF16_OBF16, 1, 4, 2, 2, 16, 3, 3, 3, 0), (501, BF16_OBF16, 2, 2, 2, 2, 16, 3, 3, 3, 0),
-    (502, BF16_OBF16, 2, 2, 2, 4, 16, 3, 3, 3, 0), (504, BF16_OBF16, 1, 4, 2, 2, 32, 3, 3, 2, 0),
-    (510, BF16_OBF16, 1, 4, 2, 2, 16, 0, 0, 4, 0), (511, BF16_OBF16, 2, 2, 2, 4, 16, 0, 0, 4, 0),
-    (512, BF16_OBF16, 4, 1, 2, 4, 16, 0, 0, 4, 0),
-    (520, BF16_OBF16, 1, 4, 2, 2, 16, 3, 3, 3, 1), (521, BF16_OBF16, 2, 2, 2, 2, 16, 3, 3, 3, 1),
-    (522, BF16_OBF16, 2, 2, 2, 4, 16, 3, 3, 3, 1), (524, BF16_OBF16, 1, 4, 2, 2, 32, 3, 3, 2, 1),
-    (530, BF16_OBF16, 1, 4, 2, 2, 16, 1, 1, 4, 1), (531, BF16_OBF16, 2, 2, 2, 4, 16, 1, 1, 4, 1),
-    (532, BF16_OBF16, 4, 1, 2, 4, 16, 1, 1, 4, 1),
+    (400, BF16, 1, 4, 2, 2, 16, 3, 3, 3, 0, 0), (401, BF16, 2, 2, 2, 2, 16, 3, 3, 3, 0, 0),
+    (402, BF16, 2, 2, 2, 4, 16, 3, 3, 3, 0, 0), (404, BF16, 1, 4, 2, 2, 32, 3, 3, 2, 0, 0),
+    (410, BF16, 1, 4, 2, 2, 16, 0, 0, 4, 0, 0), (411, BF16, 2, 2, 2, 4, 16, 0, 0, 4, 0, 0),
+    (412, BF16, 4, 1, 2, 4, 16, 0, 0, 4, 0, 0),
+    (420, BF16, 1, 4, 2, 2, 16, 3, 3, 3, 1, 0), (421, BF16, 2, 2, 2, 2, 16, 3, 3, 3, 1, 0),
+    (422, BF16, 2, 2, 2, 4, 16, 3, 3, 3, 1, 0), (424, BF16, 1, 4, 2, 2, 32, 3, 3, 2, 1, 0),
+    (430, BF16, 1, 4, 2, 2, 16, 1, 1, 4, 1, 0), (431, BF16, 2, 2, 2, 4, 16, 1, 1, 4, 1, 0),
+    (432, BF16, 4, 1, 2, 4, 16, 1, 1, 4, 1, 0),
+    (440, BF16, 4, 1, 2, 4, 64, 1, 1, 1, 1, 1), (441, BF16, 2, 2, 2, 4, 64, 1, 1, 1, 1, 1),
+    (442, BF16, 1, 4, 2, 2, 64, 1, 1, 1, 1, 1),
+    (500, BF16_OBF16, 1, 4, 2, 2, 16, 3, 3, 3, 0, 0), (501, BF16_OBF16, 2, 2, 2, 2, 16, 3, 3, 3, 0, 0),
+    (502, BF16_OBF16, 2, 2, 2, 4, 16, 3, 3, 3, 0, 0), (504, BF16_OBF16, 1, 4, 2, 2, 32, 3, 3, 2, 0, 0),
+    (510, BF16_OBF16, 1, 4, 2, 2, 16, 0, 0, 4, 0, 0), (511, BF16_OBF16, 2, 2, 2, 4, 16, 0, 0, 4, 0, 0),
+    (512, BF16_OBF16, 4, 1, 2, 4, 16, 0, 0, 4, 0, 0),
+    (520, BF16_OBF16, 1, 4, 2, 2, 16, 3, 3, 3, 1, 0), (521, BF16_OBF16, 2, 2, 2, 2, 16, 3, 3, 3, 1, 0),
+    (522, BF16_OBF16, 2, 2, 2, 4, 16, 3, 3, 3, 1, 0), (524, BF16_OBF16, 1, 4, 2, 2, 32, 3, 3, 2, 1, 0),
+    (530, BF16_OBF16, 1, 4, 2, 2, 16, 1, 1, 4, 1, 0), (531, BF16_OBF16, 2, 2, 2, 4, 16, 1, 1, 4, 1, 0),
+    (532, BF16_OBF16, 4, 1, 2, 4, 16, 1, 1, 4, 1, 0),
+    (540, BF16_OBF16, 4, 1, 2, 4, 64, 1, 1, 1, 1, 1), (541, BF16_OBF16, 2, 2, 2, 4, 64, 1, 1, 1, 1, 1),
+    (542, BF16_OBF16, 1, 4, 2, 2, 64, 1, 1, 1, 1, 1),
 ]
 
 
@@ -118,12 +123,15 @@ IGEMM4 = [
 def balanced_tp(p: eq1.Problem, tp_max: int, tk: int, slots: int) -> int:
     """Outputs per tile: as many rounds of `slots` workgroups as tiles of
     tp_max outputs need, and within them the most (hence smallest, equal)
-    tiles -- each processor's share N/P of Eq. (2).  Never below 32."""
+    tiles -- each processor's share N/P of Eq. (2).  Even, never below 32."""
     npix = p.Nb * p.Nw * p.Nh
     nk = -(-p.Nk // tk)
     rounds = -(-(-(-npix // tp_max) * nk) // slots)
     ptiles = max(1, (rounds * slots) // nk)
-    return min(tp_max, max(-(-npix // ptiles), min(tp_max, 32)))
+    tp = -(-npix // ptiles)
+    if tp % 2:
+        tp += 1
+    return min(tp_max, max(tp, min(tp_max, 32)))
 
 
 def _max_slab(p: eq1.Problem, tp: int) -> int:
@@ -193,7 +201,7 @@ def candidates(p: eq1.Problem, dtype: int, cus: int, lds_bytes: int, acc_regs: i
             yield t, tk, tp, tc, vid, info
         return
     if tier == 1:
-        for vid, dt, wm, wn, mb, nb, tc, nr, ns, maxp, rawk in IGEMM2:
+        for vid, dt, wm, wn, mb, nb, tc, nr, ns, maxp, rawk, pw in IGEMM2:
             if dt != dtype or (nr > 0 and (nr, ns) != (p.Nr, p.Ns)):
                 continue
             if rawk and (p.Nc % 8 or (p.Nk + 512) * p.Nc * RS * 2 >= 2 ** 31):
@@ -206,19 +214,20 @@ def candidates(p: eq1.Problem, dtype: int, cus: int, lds_bytes: int, acc_regs: i
             else:
                 blk = math.ceil(RS * (tc // 8) * tk / 256) * 256
 
-            def lds_of(S):
-                return 2 * ((tc // 8) * ((S * p.Ny + 1) // 2 * 2) + blk) * 16
+            def lds_of(S, t):
+                per_group = (t + 1) // 2 * 2 if pw else (S * p.Ny + 1) // 2 * 2
+                return 2 * ((tc // 8) * per_group + blk) * 16
 
-            wgs = max(1, min(wg_per_cu, lds_bytes // lds_of(_max_slab(p, tp_max))))
+            wgs = max(1, min(wg_per_cu, lds_bytes // lds_of(_max_slab(p, tp_max), tp_max)))
             tp = balanced_tp(p, tp_max, tk, cus * wgs)
             S = _max_slab(p, tp)
-            if math.ceil(S * p.Ny / 2) > 256 * maxp:
+            if math.ceil((tp if pw else S * p.Ny) / 2) > 256 * maxp:
                 continue
             imgs = tp_max // (p.Nw * p.Nh) + 2
             if (imgs * p.Nc * p.Nx * p.Ny * 2 >= 2 ** 31
                     or imgs * p.Nk * p.Nw * p.Nh * e_out >= 2 ** 31):
                 continue
-            lds = lds_of(S)
+            lds = lds_of(S, tp)
             if lds > lds_bytes or acc > acc_regs:
                 continue
             t, info = _cost(p, dtype, tk, tp, tc, lds, cus, lds_bytes, wg_per_cu)
@@ -243,9 +252,10 @@ def choose(p: eq1.Problem, dtype: int, cus=256, lds_bytes=160 * 1024, acc_regs=1
            wg_per_cu=2):
     """(kernel, variant id, tk, tp, tc) the rule above selects; kernel 7 is
     the wide-staging family, 6 the DMA-staged one, 5 the register-staged
-    pipelined one (8 when it stages raw Ker rows), 2 the plain staging one,
-    1 the direct kernel."""
+    pipelined one (8 when it stages raw Ker rows, 3 for its 1x1 gather),
+    2 the plain staging one, 1 the direct kernel."""
     rawk_ids = {row[0] for row in IGEMM2 if row[10]}
+    pw_ids = {row[0] for row in IGEMM2 if row[11]}
     best = None
     for tier in (0, 1, 2):
         for t, tk, tp, tc, vid, info in candidates(p, dtype, cus, lds_bytes, acc_regs,
@@ -255,7 +265,7 @@ def choose(p: eq1.Problem, dtype: int, cus=256, lds_bytes=160 * 1024, acc_regs=1
                 if tier == 0:
                     kern = 7 if vid >= 800 else 6
                 elif tier == 1:
-                    kern = 8 if vid in rawk_ids else 5
+                    kern = 3 if vid in pw_ids else (8 if vid in rawk_ids else 5)
                 else:
                     kern = 2
                 best = (key, (kern, vid, tk, tp, tc))

@@ -208,8 +208,11 @@ bool v2_geometry_ok(const Variant2& v, const cnn_plan_t& pl) {
   const int64_t grid = ((p.Nb * p.Nw * p.Nh + pl.tp - 1) / pl.tp) * ((p.Nk + v.tk - 1) / v.tk);
   if (v.nr > 0 && (v.nr != p.Nr || v.ns != p.Ns)) return false;
   if (v.rawk && p.Nc % 8 != 0) return false;
-  return pl.slab_rows == S && (S * Ny + 1) / 2 <= 256LL * v.maxp && pl.grid == grid &&
-         pl.lds_bytes == igemm2_lds_bytes(v, S, Ny, p.Nr * p.Ns) && pl.lds_bytes <= 160 * 1024;
+  const int64_t pairs = v.pw ? (pl.tp + 1) / 2 : (S * Ny + 1) / 2;
+  if (v.pw && (p.Nr != 1 || p.Ns != 1)) return false;
+  return pl.slab_rows == S && pairs <= 256LL * v.maxp && pl.grid == grid &&
+         pl.lds_bytes == igemm2_lds_bytes(v, S, Ny, p.Nr * p.Ns, pl.tp) &&
+         pl.lds_bytes <= 160 * 1024;
 }
 
 // ws == nullptr: use the library's per-(device, stream) workspace.
@@ -240,7 +243,7 @@ int run_plan(const void* In, const void* Ker, void* Out, const cnn_plan_t& pl, h
     }
     e = launch_igemm3(*v3, In, Ker, Out, ws, a, pl.lds_bytes, st);
   } else if (const Variant2* v2 = find_variant2(pl.variant)) {
-    if (pl.kernel != (v2->rawk ? CNN_K_IGEMM_RAWK : CNN_K_IGEMM_PIPE) || v2->dtype != pl.dtype ||
+    if (pl.kernel != v2_family(*v2) || v2->dtype != pl.dtype ||
         v2->tk != pl.tk ||
         pl.tp < 1 || pl.tp > v2->tp || v2->tc != pl.tc ||
         pl.ws_bytes != igemm2_ws_bytes(*v2, pl.prob) || !v2_geometry_ok(*v2, pl))
@@ -321,7 +324,7 @@ int cnn_plan_tiles(const cnn_problem* prob, int dtype, int kernel, int64_t tk, i
   if (!prob || !plan) return fail(CNN_E_NULL, "prob and plan must be non-NULL");
   int st;
   if ((st = check_problem(*prob)) || (st = check_dtype(dtype))) return st;
-  if (kernel < CNN_K_AUTO || kernel > CNN_K_IGEMM_RAWK)
+  if (kernel < CNN_K_AUTO || kernel > CNN_K_IGEMM_RAWK || kernel == CNN_K_SMALLC)
     return fail(CNN_E_UNSUPPORTED, "unknown kernel %d", kernel);
   cnn_budget bud;
   if ((st = resolve_budget(budget, &bud))) return st;

@@ -180,14 +180,21 @@ static bool eval_variant3(const cnn_problem& p, int dtype, const Variant3& v,
 // fewest rounds of `slots` concurrent workgroups that TP-output tiles need,
 // then the smallest tile that still fits in those rounds, so every
 // workgroup of every round gets the same share (the P processors of
-// Eq. (2) each take N/P).  At least 32 outputs (one MFMA block).
+// Eq. (2) each take N/P).  Rounded up to an even count (the kernels stage
+// outputs in pairs), at least 32 outputs (one MFMA block).
 int64_t balanced_tp(const cnn_problem& p, int64_t TP, int64_t tk, int64_t slots) {
   const int64_t npix = p.Nb * p.Nw * p.Nh;
   const int64_t n_k = ceil_div(p.Nk, tk);
   const int64_t rounds = ceil_div(ceil_div(npix, TP) * n_k, slots);
   const int64_t ptiles = std::max<int64_t>(1, rounds * slots / n_k);
-  const int64_t tp = ceil_div(npix, ptiles);
+  int64_t tp = ceil_div(npix, ptiles);
+  tp += tp & 1;
   return std::min(TP, std::max<int64_t>(tp, std::min<int64_t>(TP, 32)));
+}
+
+// Kernel family of a pipelined-kernel instantiation.
+int v2_family(const Variant2& v) {
+  return v.pw ? CNN_K_POINTWISE : v.rawk ? CNN_K_IGEMM_RAWK : CNN_K_IGEMM_PIPE;
 }
 
 // Pipelined kernel (conv_igemm2): its stencil must match a compile-time one
@@ -200,11 +207,11 @@ static bool eval_variant2(const cnn_problem& p, int dtype, const Variant2& v,
   if (v.rawk && (p.Nc % 8 != 0 || (p.Nk + 512) * p.Nc * p.Nr * p.Ns * 2 >= (1LL << 31)))
     return false;
   const int64_t Ny = p.sh * (p.Nh - 1) + p.Ns;
-  const int64_t lds_full = igemm2_lds_bytes(v, slab_rows_max(p, v.tp), Ny, p.Nr * p.Ns);
+  const int64_t lds_full = igemm2_lds_bytes(v, slab_rows_max(p, v.tp), Ny, p.Nr * p.Ns, v.tp);
   const int64_t occ = std::max<int64_t>(1, std::min<int64_t>(bud.wg_per_cu, bud.lds_bytes / lds_full));
   const int64_t tp = balanced_tp(p, v.tp, v.tk, bud.cus * occ);
   const int64_t S = slab_rows_max(p, tp);
-  const int64_t pairs = (S * Ny + 1) / 2;
+  const int64_t pairs = v.pw ? (tp + 1) / 2 : (S * Ny + 1) / 2;
   if (pairs > 256 * (int64_t)v.maxp) return false;
   // per-tile buffer offsets are 32-bit: the images a tile touches must span
   // less than 2 GiB of In and of Out
@@ -213,7 +220,7 @@ static bool eval_variant2(const cnn_problem& p, int dtype, const Variant2& v,
   if (imgs * p.Nc * Nx * Ny * 2 >= (1LL << 31) ||
       imgs * p.Nk * p.Nw * p.Nh * out_bytes(dtype) >= (1LL << 31))
     return false;
-  const int64_t lds = igemm2_lds_bytes(v, S, Ny, p.Nr * p.Ns);
+  const int64_t lds = igemm2_lds_bytes(v, S, Ny, p.Nr * p.Ns, tp);
   return eval_tiling(p, dtype, v.id, v.tk, tp, v.tc, v.acc, S, lds, igemm2_ws_bytes(v, p),
                      bud, plan, time_clk);
 }
@@ -257,7 +264,8 @@ int select_plan(const cnn_problem& p, int dtype, const cnn_budget& bud, int kern
     return CNN_OK;
   }
   if (kernel != CNN_K_AUTO && kernel != CNN_K_IGEMM && kernel != CNN_K_IGEMM_PIPE &&
-      kernel != CNN_K_IGEMM_DMA && kernel != CNN_K_IGEMM_WIDE && kernel != CNN_K_IGEMM_RAWK)
+      kernel != CNN_K_IGEMM_DMA && kernel != CNN_K_IGEMM_WIDE && kernel != CNN_K_IGEMM_RAWK &&
+      kernel != CNN_K_POINTWISE)
     return CNN_E_UNSUPPORTED;
   bool found = false;
   double best_t = 0;
@@ -310,7 +318,7 @@ int select_plan(const cnn_problem& p, int dtype, const cnn_budget& bud, int kern
   const Variant2* vs2 = variants2(&n2);
   for (int i = 0; i < n2; ++i) {
     const Variant2& v = vs2[i];
-    const int family = v.rawk ? CNN_K_IGEMM_RAWK : CNN_K_IGEMM_PIPE;
+    const int family = v2_family(v);
     if (tier1_found || v.dtype != dtype || (kernel != CNN_K_AUTO && kernel != family))
       continue;
     if (kernel == family && (v.tk != tk || v.tp != tp || v.tc != tc)) continue;  // tp: largest tile
@@ -366,7 +374,7 @@ int enumerate_plans(const cnn_problem& p, int dtype, const cnn_budget& bud, cnn_
   const Variant2* vs2 = variants2(&n2);
   for (int i = 0; i < n2; ++i)
     if (vs2[i].dtype == dtype && eval_variant2(p, dtype, vs2[i], bud, &cand, &t))
-      add(cand, vs2[i].rawk ? CNN_K_IGEMM_RAWK : CNN_K_IGEMM_PIPE);
+      add(cand, v2_family(vs2[i]));
   const Variant* vs = variants(&n1);
   for (int i = 0; i < n1; ++i)
     if (vs[i].dtype == dtype && vs[i].kernel == CNN_K_IGEMM &&

@@ -53,10 +53,13 @@ struct Variant2 {
   int32_t nr, ns;   // compile-time stencil (0 = any)
   int32_t maxp;     // slab position pairs per thread: ceil(S*Ny/2) <= 256*maxp
   int32_t rawk;     // 1: stages raw Ker rows (needs Nc % 8 == 0), no repack / workspace
+  int32_t pw;       // 1: 1x1 gather -- stages the tile's outputs' inputs, any stride
 };
 const Variant2* variants2(int* count);
+int v2_family(const Variant2& v);
 int64_t igemm2_blk_vecs(const Variant2& v, int64_t RS);
-int64_t igemm2_lds_bytes(const Variant2& v, int64_t slab_rows, int64_t Ny, int64_t RS);
+int64_t igemm2_lds_bytes(const Variant2& v, int64_t slab_rows, int64_t Ny, int64_t RS,
+                         int64_t tp);
 int64_t igemm2_ws_bytes(const Variant2& v, const cnn_problem& p);
 
 // LDS bytes an implicit-GEMM variant needs for a given slab height.

@@ -91,7 +91,9 @@ __global__ __launch_bounds__(256) void pack_ker_bf16(const bf16_t* __restrict__ 
 //   kElement   a pair straddles an image: two 16-bit loads per pair.
 // Loads go through buffer descriptors based at the tile's first image, so
 // offsets are 32-bit and reads past the tensor return 0 instead of faulting.
-enum { kAligned = 0, kFunnel = 1, kElement = 2 };
+//   kStride2   (1x1 gather, stride 2 along h) one 8-byte load covers the
+//              pair's two elements, 4 bytes apart; v_perm packs them.
+enum { kAligned = 0, kFunnel = 1, kElement = 2, kStride2 = 3 };
 
 // Extent rounded up to whole dwords: a dword holding a tensor's last
 // 16-bit element must not count as out of range (the extra bytes share the
@@ -118,7 +120,7 @@ __host__ __device__ constexpr int rawk_row_chunks(int RS, int TC) {
 }
 
 template <typename TO, int WM, int WN, int MB, int NB, int TC, int NR, int NS, int MAXP,
-          bool RAWK>
+          bool RAWK, bool PW>
 __global__ __launch_bounds__(256) void conv_igemm2(const bf16_t* __restrict__ In,
                                                    const u32x4_t* __restrict__ Kp,
                                                    TO* __restrict__ Out, ConvArgs a,
@@ -132,7 +134,9 @@ __global__ __launch_bounds__(256) void conv_igemm2(const bf16_t* __restrict__ In
   const int Ns = NS > 0 ? NS : a.Ns;
 
   extern __shared__ __attribute__((aligned(16))) char smem[];
-  const int SN = (a.slab_max * a.Ny + 1) & ~1;  // even: pairs never cross groups
+  // positions per channel group (even: pairs never cross groups); the 1x1
+  // gather (PW) stages the tile's outputs, the others its input rows
+  const int SN = PW ? ((a.tp + 1) & ~1) : ((a.slab_max * a.Ny + 1) & ~1);
   u32x4_t* inbuf = reinterpret_cast<u32x4_t*>(smem);  // [2][G][SN]
   u32x4_t* kerbuf = inbuf + 2 * G * SN;                 // [2][blk_vecs]
 
@@ -143,6 +147,7 @@ __global__ __launch_bounds__(256) void conv_igemm2(const bf16_t* __restrict__ In
   const int l32 = lane & 31, half = lane >> 5;
 
   static_assert(!RAWK || (NR > 0 && NS > 0), "raw Ker needs a compile-time stencil");
+  static_assert(!PW || (NR == 1 && NS == 1 && RAWK), "the gather is for raw-Ker 1x1 stencils");
   const int tile = xcd_remap(blockIdx.x, gridDim.x);
   const int pt = tile / a.n_ktiles;
   const int kt = tile - pt * a.n_ktiles;
@@ -153,7 +158,7 @@ __global__ __launch_bounds__(256) void conv_igemm2(const bf16_t* __restrict__ In
   const int b1 = plast / a.hw, w1 = (plast - b1 * a.hw) / a.Nh;
   const int G0 = b0 * a.Nx + a.sw * w0;
   const int S = b1 * a.Nx + a.sw * w1 + Nr - G0;
-  const int SNt = S * a.Ny;
+  const int SNt = PW ? plast - p0 + 1 : S * a.Ny;
   const int npairs = (SNt + 1) >> 1;
 
   // Output side: LDS position of each lane's (r, s) = (0, 0) tap and its
@@ -170,7 +175,7 @@ __global__ __launch_bounds__(256) void conv_igemm2(const bf16_t* __restrict__ In
     const int q = pc - b * a.hw;
     const int w = q / a.Nh;
     const int h = q - w * a.Nh;
-    pix[nb] = (b * a.Nx + a.sw * w - G0) * a.Ny + a.sh * h;
+    pix[nb] = PW ? pc - p0 : (b * a.Nx + a.sw * w - G0) * a.Ny + a.sh * h;
     obyte[nb] = (uint32_t)(((int64_t)(b - b0) * a.Nk * a.hw + q) * (int64_t)sizeof(TO));
   }
 
@@ -179,10 +184,26 @@ __global__ __launch_bounds__(256) void conv_igemm2(const bf16_t* __restrict__ In
   // so dword offsets relative to it are dword-aligned in memory.
   const int64_t base_el = ((int64_t)b0 * a.in_img) & ~(int64_t)1;
   const __amdgpu_buffer_rsrc_t in_rsrc = make_rsrc(In + base_el, (a.in_total - base_el) * 2);
-  int path = ((a.Ny & 1) == 0 && (base_el & 1) == 0) ? kAligned : kFunnel;
-  if (path == kFunnel) {
-    for (int b = b0 + 1; b <= b1; ++b)
-      if ((((int64_t)b * a.Nx - G0) * a.Ny) & 1) path = kElement;
+  int path;
+  if constexpr (PW) {
+    // Pairs are outputs (2i, 2i+1) of the tile (p0 and Nh even keep them in
+    // one output row).  Stride 1 along h: the two elements are adjacent
+    // and, with Ny even, dword-aligned.  Stride 2: 4 bytes apart, one
+    // 8-byte load, unless the tile holds the tensor's last input row, where
+    // the load could reach past the end.
+    const bool even = (a.Nh & 1) == 0 && (p0 & 1) == 0;
+    if (even && a.sh == 1 && (a.Ny & 1) == 0)
+      path = kAligned;
+    else if (even && a.sh == 2 && !(b1 == a.Nb - 1 && w1 == a.Nw - 1))
+      path = kStride2;
+    else
+      path = kElement;
+  } else {
+    path = ((a.Ny & 1) == 0 && (base_el & 1) == 0) ? kAligned : kFunnel;
+    if (path == kFunnel) {
+      for (int b = b0 + 1; b <= b1; ++b)
+        if ((((int64_t)b * a.Nx - G0) * a.Ny) & 1) path = kElement;
+    }
   }
   const int gpos0 = G0 * a.Ny;
   uint32_t voff[MAXP], voff2[MAXP];  // byte offsets (channel 0) of pos / of pos+1
@@ -194,64 +215,124 @@ __global__ __launch_bounds__(256) void conv_igemm2(const bf16_t* __restrict__ In
     pvalid[j] = pr < npairs;
     const int pos = 2 * (pvalid[j] ? pr : 0);
     pdst[j] = pos;
-    const int gp = gpos0 + pos;
-    const int b = gp / a.nxny;
-    const int r0 = gp - b * a.nxny;
-    voff[j] = (uint32_t)(((int64_t)b * a.in_img - base_el + r0) * 2);
-    // second position: next element, or the next image's first element
-    const int b2 = (r0 + 1 == a.nxny) ? b + 1 : b;
-    const int r2 = (r0 + 1 == a.nxny) ? 0 : r0 + 1;
-    voff2[j] = (uint32_t)(((int64_t)b2 * a.in_img - base_el + r2) * 2);
+    if constexpr (PW) {
+      // element of output p: In[b][c][sw*w][sh*h] (channel 0 here)
+      auto gather = [&](int p) -> uint32_t {
+        const int b = p / a.hw;
+        const int q = p - b * a.hw;
+        const int w = q / a.Nh;
+        const int h = q - w * a.Nh;
+        return (uint32_t)(((int64_t)b * a.in_img - base_el + (int64_t)a.sw * w * a.Ny +
+                           (int64_t)a.sh * h) * 2);
+      };
+      voff[j] = gather(p0 + pos);
+      voff2[j] = gather(min(p0 + pos + 1, plast));
+    } else {
+      const int gp = gpos0 + pos;
+      const int b = gp / a.nxny;
+      const int r0 = gp - b * a.nxny;
+      voff[j] = (uint32_t)(((int64_t)b * a.in_img - base_el + r0) * 2);
+      // second position: next element, or the next image's first element
+      const int b2 = (r0 + 1 == a.nxny) ? b + 1 : b;
+      const int r2 = (r0 + 1 == a.nxny) ? 0 : r0 + 1;
+      voff2[j] = (uint32_t)(((int64_t)b2 * a.in_img - base_el + r2) * 2);
+    }
   }
 
   uint32_t pre[G][MAXP][8];
-  auto load_in = [&](int c0) {
+  // Gather staging (1x1 kernels), the stage starting at c0: channel
+  // q = 8g + i into every pair slot (slots past the tile reload position
+  // 0).  One uniform switch on the load path per stage, then straight-line
+  // loads; a channel past Nc loads channel Nc-1 and write_in zeroes it.
+  auto load_path = [&](auto tag, int c0) __attribute__((always_inline)) {
+    constexpr int P = decltype(tag)::value;
 #pragma unroll
-    for (int g = 0; g < G; ++g) {
+    for (int q = 0; q < 8 * G; ++q) {
+      const int g = q >> 3, i = q & 7;
+      const int c = c0 + q;
+      const uint32_t so = (uint32_t)((int64_t)min(c, a.Nc - 1) * a.nxny * 2);
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const int c = c0 + 8 * g + i;
-        if (c < a.Nc) {
-          const uint32_t so = (uint32_t)((int64_t)c * a.nxny * 2);
-          if (path == kAligned) {
-#pragma unroll
-            for (int j = 0; j < MAXP; ++j)
-              pre[g][j][i] = __builtin_amdgcn_raw_buffer_load_b32(in_rsrc, voff[j], so, 0);
-          } else if (path == kFunnel) {
-#pragma unroll
-            for (int j = 0; j < MAXP; ++j) {
-              const uint32_t t = voff[j] + (so & 2u);
-              const uint32_t lo_off = t & ~3u;
-              const uint32_t lo = __builtin_amdgcn_raw_buffer_load_b32(in_rsrc, lo_off, so & ~3u, 0);
-              const uint32_t hi = __builtin_amdgcn_raw_buffer_load_b32(in_rsrc, lo_off + 4, so & ~3u, 0);
-              pre[g][j][i] = __builtin_amdgcn_alignbit(hi, lo, (t & 2u) * 8u);
-            }
-          } else {
-#pragma unroll
-            for (int j = 0; j < MAXP; ++j) {
-              const uint32_t lo = __builtin_amdgcn_raw_buffer_load_b16(in_rsrc, voff[j], so, 0);
-              const uint32_t hi = __builtin_amdgcn_raw_buffer_load_b16(in_rsrc, voff2[j], so, 0);
-              pre[g][j][i] = lo | (hi << 16);
-            }
-          }
+      for (int j = 0; j < MAXP; ++j) {
+        if constexpr (P == kAligned) {
+          pre[g][j][i] = __builtin_amdgcn_raw_buffer_load_b32(in_rsrc, voff[j], so, 0);
+        } else if constexpr (P == kStride2) {
+          const u32x2_t d = __builtin_bit_cast(
+              u32x2_t, __builtin_amdgcn_raw_buffer_load_b64(in_rsrc, voff[j], so, 0));
+          pre[g][j][i] = __builtin_amdgcn_perm(d[1], d[0], 0x05040100u);
         } else {
-#pragma unroll
-          for (int j = 0; j < MAXP; ++j) pre[g][j][i] = 0u;
+          const uint32_t lo = __builtin_amdgcn_raw_buffer_load_b16(in_rsrc, voff[j], so, 0);
+          const uint32_t hi = __builtin_amdgcn_raw_buffer_load_b16(in_rsrc, voff2[j], so, 0);
+          pre[g][j][i] = lo | (hi << 16);
         }
       }
     }
   };
-  auto write_in = [&](u32x4_t* buf) {
+  // Slab staging (row-staged kernels): per channel, a uniform test and
+  // the path switch.  Measured faster than load_path's straight-line form
+  // for the 3x3 tilings, slower for the 1x1 gather.
+  auto load_rows = [&](int c0) __attribute__((always_inline)) {
+#pragma unroll
+    for (int q = 0; q < 8 * G; ++q) {
+      const int g = q >> 3, i = q & 7;
+      const int c = c0 + q;
+      if (c < a.Nc) {
+        const uint32_t so = (uint32_t)((int64_t)c * a.nxny * 2);
+        if (path == kAligned) {
+#pragma unroll
+          for (int j = 0; j < MAXP; ++j)
+            pre[g][j][i] = __builtin_amdgcn_raw_buffer_load_b32(in_rsrc, voff[j], so, 0);
+        } else if (path == kFunnel) {
+#pragma unroll
+          for (int j = 0; j < MAXP; ++j) {
+            const uint32_t t = voff[j] + (so & 2u);
+            const uint32_t lo_off = t & ~3u;
+            const uint32_t lo = __builtin_amdgcn_raw_buffer_load_b32(in_rsrc, lo_off, so & ~3u, 0);
+            const uint32_t hi = __builtin_amdgcn_raw_buffer_load_b32(in_rsrc, lo_off + 4, so & ~3u, 0);
+            pre[g][j][i] = __builtin_amdgcn_alignbit(hi, lo, (t & 2u) * 8u);
+          }
+        } else {
+#pragma unroll
+          for (int j = 0; j < MAXP; ++j) {
+            const uint32_t lo = __builtin_amdgcn_raw_buffer_load_b16(in_rsrc, voff[j], so, 0);
+            const uint32_t hi = __builtin_amdgcn_raw_buffer_load_b16(in_rsrc, voff2[j], so, 0);
+            pre[g][j][i] = lo | (hi << 16);
+          }
+        }
+      } else {
+#pragma unroll
+        for (int j = 0; j < MAXP; ++j) pre[g][j][i] = 0u;
+      }
+    }
+  };
+  auto load_in = [&](int c0) __attribute__((always_inline)) {
+    if constexpr (PW) {
+      if (path == kAligned)
+        load_path(std::integral_constant<int, kAligned>(), c0);
+      else if (path == kStride2)
+        load_path(std::integral_constant<int, kStride2>(), c0);
+      else
+        load_path(std::integral_constant<int, kElement>(), c0);
+    } else {
+      load_rows(c0);
+    }
+  };
+  auto write_in = [&](u32x4_t* buf, int c0) {
 #pragma unroll
     for (int g = 0; g < G; ++g) {
+      // channels past Nc were loaded as channel Nc-1: zero them
+      uint32_t keep[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) keep[i] = c0 + 8 * g + i < a.Nc ? ~0u : 0u;
 #pragma unroll
       for (int j = 0; j < MAXP; ++j) {
         if (pvalid[j]) {
           u32x4_t lo, hi;
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
-            lo[i] = __builtin_amdgcn_perm(pre[g][j][2 * i + 1], pre[g][j][2 * i], 0x05040100u);
-            hi[i] = __builtin_amdgcn_perm(pre[g][j][2 * i + 1], pre[g][j][2 * i], 0x07060302u);
+            const uint32_t e0 = pre[g][j][2 * i] & keep[2 * i];
+            const uint32_t e1 = pre[g][j][2 * i + 1] & keep[2 * i + 1];
+            lo[i] = __builtin_amdgcn_perm(e1, e0, 0x05040100u);
+            hi[i] = __builtin_amdgcn_perm(e1, e0, 0x07060302u);
           }
           buf[g * SN + pdst[j]] = lo;
           buf[g * SN + pdst[j] + 1] = hi;
@@ -307,10 +388,11 @@ __global__ __launch_bounds__(256) void conv_igemm2(const bf16_t* __restrict__ In
     const int buf = cc & 1;
     u32x4_t* ib = inbuf + buf * G * SN;
     const u32x4_t* kb = kerbuf + buf * blk_vecs;
-    write_in(ib);
+    write_in(ib, cc * TC);
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
-    if (cc + 1 < n_cc) {
+    const bool more = cc + 1 < n_cc;
+    if (more) {
       dma_ker(cc + 1, kerbuf + (buf ^ 1) * blk_vecs);
       load_in((cc + 1) * TC);
     }
@@ -426,43 +508,50 @@ __global__ __launch_bounds__(256) void conv_igemm2(const bf16_t* __restrict__ In
 }
 
 // ---- instantiation table ----------------------------------------------------
-// (id, dtype, WM, WN, MB, NB, TC, NR, NS, MAXP, RAWK): tk = 32*WM*MB,
+// (id, dtype, WM, WN, MB, NB, TC, NR, NS, MAXP, RAWK, PW): tk = 32*WM*MB,
 // tp = 32*WN*NB (the largest tile; plans may use fewer outputs per tile);
 // NR = NS = 0 reads the stencil size at run time; MAXP position pairs per
-// thread bound the slab (ceil(S*Ny/2) <= 256*MAXP); RAWK stages raw Ker.
+// thread bound the slab (ceil(S*Ny/2) <= 256*MAXP; with PW, ceil(tp/2));
+// RAWK stages raw Ker; PW gathers the 1x1 inputs of the tile's outputs.
 #define CNN_IGEMM2_VARIANTS(X)                          \
-  X(400, CNN_BF16, 1, 4, 2, 2, 16, 3, 3, 3, 0)          \
-  X(401, CNN_BF16, 2, 2, 2, 2, 16, 3, 3, 3, 0)          \
-  X(402, CNN_BF16, 2, 2, 2, 4, 16, 3, 3, 3, 0)          \
-  X(404, CNN_BF16, 1, 4, 2, 2, 32, 3, 3, 2, 0)          \
-  X(410, CNN_BF16, 1, 4, 2, 2, 16, 0, 0, 4, 0)          \
-  X(411, CNN_BF16, 2, 2, 2, 4, 16, 0, 0, 4, 0)          \
-  X(412, CNN_BF16, 4, 1, 2, 4, 16, 0, 0, 4, 0)          \
-  X(420, CNN_BF16, 1, 4, 2, 2, 16, 3, 3, 3, 1)          \
-  X(421, CNN_BF16, 2, 2, 2, 2, 16, 3, 3, 3, 1)          \
-  X(422, CNN_BF16, 2, 2, 2, 4, 16, 3, 3, 3, 1)          \
-  X(424, CNN_BF16, 1, 4, 2, 2, 32, 3, 3, 2, 1)          \
-  X(430, CNN_BF16, 1, 4, 2, 2, 16, 1, 1, 4, 1)          \
-  X(431, CNN_BF16, 2, 2, 2, 4, 16, 1, 1, 4, 1)          \
-  X(432, CNN_BF16, 4, 1, 2, 4, 16, 1, 1, 4, 1)          \
-  X(500, CNN_BF16_OBF16, 1, 4, 2, 2, 16, 3, 3, 3, 0)    \
-  X(501, CNN_BF16_OBF16, 2, 2, 2, 2, 16, 3, 3, 3, 0)    \
-  X(502, CNN_BF16_OBF16, 2, 2, 2, 4, 16, 3, 3, 3, 0)    \
-  X(504, CNN_BF16_OBF16, 1, 4, 2, 2, 32, 3, 3, 2, 0)    \
-  X(510, CNN_BF16_OBF16, 1, 4, 2, 2, 16, 0, 0, 4, 0)    \
-  X(511, CNN_BF16_OBF16, 2, 2, 2, 4, 16, 0, 0, 4, 0)    \
-  X(512, CNN_BF16_OBF16, 4, 1, 2, 4, 16, 0, 0, 4, 0)    \
-  X(520, CNN_BF16_OBF16, 1, 4, 2, 2, 16, 3, 3, 3, 1)    \
-  X(521, CNN_BF16_OBF16, 2, 2, 2, 2, 16, 3, 3, 3, 1)    \
-  X(522, CNN_BF16_OBF16, 2, 2, 2, 4, 16, 3, 3, 3, 1)    \
-  X(524, CNN_BF16_OBF16, 1, 4, 2, 2, 32, 3, 3, 2, 1)    \
-  X(530, CNN_BF16_OBF16, 1, 4, 2, 2, 16, 1, 1, 4, 1)    \
-  X(531, CNN_BF16_OBF16, 2, 2, 2, 4, 16, 1, 1, 4, 1)    \
-  X(532, CNN_BF16_OBF16, 4, 1, 2, 4, 16, 1, 1, 4, 1)
+  X(400, CNN_BF16, 1, 4, 2, 2, 16, 3, 3, 3, 0, 0)          \
+  X(401, CNN_BF16, 2, 2, 2, 2, 16, 3, 3, 3, 0, 0)          \
+  X(402, CNN_BF16, 2, 2, 2, 4, 16, 3, 3, 3, 0, 0)          \
+  X(404, CNN_BF16, 1, 4, 2, 2, 32, 3, 3, 2, 0, 0)          \
+  X(410, CNN_BF16, 1, 4, 2, 2, 16, 0, 0, 4, 0, 0)          \
+  X(411, CNN_BF16, 2, 2, 2, 4, 16, 0, 0, 4, 0, 0)          \
+  X(412, CNN_BF16, 4, 1, 2, 4, 16, 0, 0, 4, 0, 0)          \
+  X(420, CNN_BF16, 1, 4, 2, 2, 16, 3, 3, 3, 1, 0)          \
+  X(421, CNN_BF16, 2, 2, 2, 2, 16, 3, 3, 3, 1, 0)          \
+  X(422, CNN_BF16, 2, 2, 2, 4, 16, 3, 3, 3, 1, 0)          \
+  X(424, CNN_BF16, 1, 4, 2, 2, 32, 3, 3, 2, 1, 0)          \
+  X(430, CNN_BF16, 1, 4, 2, 2, 16, 1, 1, 4, 1, 0)          \
+  X(431, CNN_BF16, 2, 2, 2, 4, 16, 1, 1, 4, 1, 0)          \
+  X(432, CNN_BF16, 4, 1, 2, 4, 16, 1, 1, 4, 1, 0)          \
+  X(440, CNN_BF16, 4, 1, 2, 4, 64, 1, 1, 1, 1, 1)          \
+  X(441, CNN_BF16, 2, 2, 2, 4, 64, 1, 1, 1, 1, 1)          \
+  X(442, CNN_BF16, 1, 4, 2, 2, 64, 1, 1, 1, 1, 1)          \
+  X(500, CNN_BF16_OBF16, 1, 4, 2, 2, 16, 3, 3, 3, 0, 0)    \
+  X(501, CNN_BF16_OBF16, 2, 2, 2, 2, 16, 3, 3, 3, 0, 0)    \
+  X(502, CNN_BF16_OBF16, 2, 2, 2, 4, 16, 3, 3, 3, 0, 0)    \
+  X(504, CNN_BF16_OBF16, 1, 4, 2, 2, 32, 3, 3, 2, 0, 0)    \
+  X(510, CNN_BF16_OBF16, 1, 4, 2, 2, 16, 0, 0, 4, 0, 0)    \
+  X(511, CNN_BF16_OBF16, 2, 2, 2, 4, 16, 0, 0, 4, 0, 0)    \
+  X(512, CNN_BF16_OBF16, 4, 1, 2, 4, 16, 0, 0, 4, 0, 0)    \
+  X(520, CNN_BF16_OBF16, 1, 4, 2, 2, 16, 3, 3, 3, 1, 0)    \
+  X(521, CNN_BF16_OBF16, 2, 2, 2, 2, 16, 3, 3, 3, 1, 0)    \
+  X(522, CNN_BF16_OBF16, 2, 2, 2, 4, 16, 3, 3, 3, 1, 0)    \
+  X(524, CNN_BF16_OBF16, 1, 4, 2, 2, 32, 3, 3, 2, 1, 0)    \
+  X(530, CNN_BF16_OBF16, 1, 4, 2, 2, 16, 1, 1, 4, 1, 0)    \
+  X(531, CNN_BF16_OBF16, 2, 2, 2, 4, 16, 1, 1, 4, 1, 0)    \
+  X(532, CNN_BF16_OBF16, 4, 1, 2, 4, 16, 1, 1, 4, 1, 0)    \
+  X(540, CNN_BF16_OBF16, 4, 1, 2, 4, 64, 1, 1, 1, 1, 1)    \
+  X(541, CNN_BF16_OBF16, 2, 2, 2, 4, 64, 1, 1, 1, 1, 1)    \
+  X(542, CNN_BF16_OBF16, 1, 4, 2, 2, 64, 1, 1, 1, 1, 1)
 
 static const Variant2 kVariants2[] = {
-#define CNN_ROW2(id, dt, wm, wn, mb, nb, tc, nr, ns, maxp, rawk) \
-  {id, dt, 32 * (wm) * (mb), 32 * (wn) * (nb), tc, 16 * (mb) * (nb), nr, ns, maxp, rawk},
+#define CNN_ROW2(id, dt, wm, wn, mb, nb, tc, nr, ns, maxp, rawk, pw) \
+  {id, dt, 32 * (wm) * (mb), 32 * (wn) * (nb), tc, 16 * (mb) * (nb), nr, ns, maxp, rawk, pw},
     CNN_IGEMM2_VARIANTS(CNN_ROW2)
 #undef CNN_ROW2
 };
@@ -481,8 +570,9 @@ int64_t igemm2_blk_vecs(const Variant2& v, int64_t RS) {
   return (n + 255) / 256 * 256;
 }
 
-int64_t igemm2_lds_bytes(const Variant2& v, int64_t slab_rows, int64_t Ny, int64_t RS) {
-  const int64_t sn = (slab_rows * Ny + 1) / 2 * 2;
+int64_t igemm2_lds_bytes(const Variant2& v, int64_t slab_rows, int64_t Ny, int64_t RS,
+                         int64_t tp) {
+  const int64_t sn = v.pw ? (tp + 1) / 2 * 2 : (slab_rows * Ny + 1) / 2 * 2;
   return 2 * ((v.tc / 8) * sn + igemm2_blk_vecs(v, RS)) * 16;
 }
 
@@ -492,7 +582,8 @@ int64_t igemm2_ws_bytes(const Variant2& v, const cnn_problem& p) {
   return n_kt * n_cc * igemm2_blk_vecs(v, p.Nr * p.Ns) * 16;
 }
 
-template <int DT, int WM, int WN, int MB, int NB, int TC, int NR, int NS, int MAXP, int RAWK>
+template <int DT, int WM, int WN, int MB, int NB, int TC, int NR, int NS, int MAXP, int RAWK,
+          int PW>
 static hipError_t launch_one2(const void* In, const void* Ker, void* Out, void* ws,
                               const ConvArgs& a, int64_t lds, hipStream_t stream) {
   typedef typename std::conditional<DT == CNN_BF16, float, bf16_t>::type TO;
@@ -512,7 +603,7 @@ static hipError_t launch_one2(const void* In, const void* Ker, void* Out, void* 
                        (const bf16_t*)Ker, (u32x4_t*)ws, a, TK, TC, (int)blk, total);
     kp = ws;
   }
-  auto kern = conv_igemm2<TO, WM, WN, MB, NB, TC, NR, NS, MAXP, (RAWK != 0)>;
+  auto kern = conv_igemm2<TO, WM, WN, MB, NB, TC, NR, NS, MAXP, (RAWK != 0), (PW != 0)>;
   static bool attr_set = false;
   if (!attr_set) {
     hipError_t e = hipFuncSetAttribute((const void*)kern,
@@ -528,10 +619,10 @@ static hipError_t launch_one2(const void* In, const void* Ker, void* Out, void* 
 hipError_t launch_igemm2(const Variant2& v, const void* In, const void* Ker, void* Out,
                          void* ws, const ConvArgs& a, int64_t lds_bytes, hipStream_t stream) {
   switch (v.id) {
-#define CNN_CASE2(id, dt, wm, wn, mb, nb, tc, nr, ns, maxp, rawk)                                  \
-  case id:                                                                                        \
-    return launch_one2<dt, wm, wn, mb, nb, tc, nr, ns, maxp, rawk>(In, Ker, Out, ws, a, lds_bytes, \
-                                                                   stream);
+#define CNN_CASE2(id, dt, wm, wn, mb, nb, tc, nr, ns, maxp, rawk, pw)                    \
+  case id:                                                                              \
+    return launch_one2<dt, wm, wn, mb, nb, tc, nr, ns, maxp, rawk, pw>(In, Ker, Out, ws, a, \
+                                                                       lds_bytes, stream);
     CNN_IGEMM2_VARIANTS(CNN_CASE2)
 #undef CNN_CASE2
     default:

@@ -84,7 +84,7 @@ def variant_dims(kernel, vid, dt, tk, tp, tc, stencil):
     Nr, Ns = stencil
     cands = [(3, tc + 5, tk + 7, 9, 13, Nr, Ns, 1, 2), (2, tc + 5, tk + 7, 7, 13, Nr, Ns, 1, 1),
              (3, tc + 8, tk + 7, 9, 13, Nr, Ns, 1, 2), (2, tc + 8, tk + 7, 7, 13, Nr, Ns, 1, 1),
-             (2, tc + 8, tk + 7, 4, 5, Nr, Ns, 2, 1),
+             (2, tc + 8, tk + 7, 4, 5, Nr, Ns, 2, 1), (2, tc + 8, tk + 7, 6, 8, Nr, Ns, 2, 2),
              (2, tc + 3, max(1, tk - 5), 5, 9, Nr, Ns, 1, 1), (1, tc + 5, tk + 3, 6, 7, Nr, Ns, 1, 1),
              (2, tc + 5, tk + 7, 4, 5, Nr, Ns, 2, 1), (1, tc + 5, tk + 7, 3, 4, Nr, Ns, 1, 1)]
     for dims in cands:
@@ -111,8 +111,9 @@ def variant_cases():
         tk = 32 * wm * mb
         out.append((cnn.K_IGEMM_DMA, vid, dt, tk, 32 * wn * nb, tc,
                     (nr, ns) if nr else ((1, 1) if vid % 100 in (10, 11, 12) else (5, 2))))
-    for vid, dt, wm, wn, mb, nb, tc, nr, ns, _, rawk in osel.IGEMM2:
+    for vid, dt, wm, wn, mb, nb, tc, nr, ns, _, rawk, pw in osel.IGEMM2:
         tk = 32 * wm * mb
-        out.append((cnn.K_IGEMM_RAWK if rawk else cnn.K_IGEMM_PIPE, vid, dt, tk, 32 * wn * nb, tc,
+        kern = cnn.K_POINTWISE if pw else (cnn.K_IGEMM_RAWK if rawk else cnn.K_IGEMM_PIPE)
+        out.append((kern, vid, dt, tk, 32 * wn * nb, tc,
                     (nr, ns) if nr else ((1, 1) if tk >= 256 else (5, 2))))
     return out

@@ -183,3 +183,36 @@ def test_plan_find_exact_and_cached(mode):
     cnn.fwd(dIn, dKer, dOut, sw, sh)
     torch.cuda.synchronize()
     assert np.array_equal(to_host64(dOut), want)
+
+
+@pytest.mark.parametrize("mode", ["bf16", "bf16_obf16"])
+@pytest.mark.parametrize("shape", [
+    (3, 72, 70, 10, 14, 1, 1, 1, 1),   # stride 1, Nh even: aligned pairs
+    (2, 80, 40, 9, 13, 1, 1, 1, 1),    # Nh odd: element path
+    (3, 72, 70, 10, 14, 1, 1, 2, 2),   # stride 2, Nh even: 8-byte gather
+    (2, 64, 33, 7, 9, 1, 1, 2, 2),     # stride 2, Nh odd
+    (2, 64, 33, 6, 8, 1, 1, 2, 1),     # stride only along w
+    (2, 64, 33, 6, 8, 1, 1, 1, 3),     # stride 3 along h
+])
+@pytest.mark.parametrize("tk", [64, 128, 256])
+def test_pointwise_gather_exact(shape, tk, mode):
+    """The 1x1 gather kernels (every tiling, every load path) on small
+    integers: bit-exact with the oracle in the fp32-Out mode, and within
+    bf16 rounding of it in the bf16-Out mode."""
+    Nb, Nc, Nk, Nw, Nh, Nr, Ns, sw, sh = shape
+    tp = {64: 256, 128: 256, 256: 128}[tk]
+    try:
+        pl = cnn.plan_tiles(cnn.problem(*shape), MODES[mode], cnn.K_POINTWISE, tk, tp, 64)
+    except cnn.CnnError:
+        pytest.skip("tiling does not fit this shape")
+    rng = np.random.default_rng(sum(shape) + tk)
+    Nx, Ny = sw * (Nw - 1) + Nr, sh * (Nh - 1) + Ns
+    In = inputs.f32_to_bf16_bits(rng.integers(-2, 3, size=(Nb, Nc, Nx, Ny)).astype(np.float32))
+    Ker = inputs.f32_to_bf16_bits(rng.integers(-2, 3, size=(Nk, Nc, Nr, Ns)).astype(np.float32))
+    want = oracle.conv(In, Ker, sw, sh)
+    say(f"[parity] pointwise gather shape={shape} tk={tk} mode={mode} v{pl.variant} tp={pl.tp}")
+    got = run(In, Ker, sw, sh, mode, plan=pl)
+    if mode == "bf16":
+        assert np.array_equal(got, want)
+    else:
+        assert np.array_equal(got, oracle.widen(inputs.f32_to_bf16_bits(want.astype(np.float32))))
