@@ -59,8 +59,8 @@ def measured_traffic(workload: str, mode: str):
     return rec.get("hbm_bytes_per_launch")
 
 
-KERNELS = {"direct": 1, "igemm": 2, "igemm_pipe": 5, "igemm_dma": 6, "igemm_wide": 7,
-           "igemm_rawk": 8}
+KERNELS = {"direct": 1, "igemm": 2, "pointwise": 3, "smallc": 4, "igemm_pipe": 5,
+           "igemm_dma": 6, "igemm_wide": 7, "igemm_rawk": 8}
 
 
 def forced_plan(spec: str, w, mode: str):

@@ -85,7 +85,9 @@ typedef enum cnn_kernel {
   CNN_K_POINTWISE = 3,/* 1x1 stencils, any stride, bf16, Nc % 8 == 0: the inputs of the
                          tile's outputs gathered (no halo, no unused rows), 64 channels
                          per stage, raw Ker rows as in CNN_K_IGEMM_RAWK              */
-  CNN_K_SMALLC = 4,   /* reserved (few input channels, wide stencils); not built       */
+  CNN_K_SMALLC = 4,   /* few input channels, wide stencils (Ns <= 8, ceil(Nc*Nr/2) <= 24),
+                         bf16: K = flattened (c, r, s), Ker in registers, the whole
+                         halo'd slab in LDS; tc of its plans is Nc                    */
   CNN_K_IGEMM_PIPE = 5,/* implicit GEMM, bf16: repacked Ker streamed by DMA, In staged
                          through registers, both double-buffered in LDS               */
   CNN_K_IGEMM_DMA = 6,/* implicit GEMM, bf16: Ker and the natural In rows both copied

@@ -120,6 +120,14 @@ IGEMM4 = [
 ]
 
 
+# (id, dtype, nb, ks) of the few-channel kernel: tk = 64, tp = 128*nb,
+# K = flattened (c, r, s padded to 8), ceil(Nc*Nr/2) <= ks K-steps, Ns <= 8.
+SMALLC = [
+    (1000, BF16, 2, 12), (1001, BF16, 1, 12), (1002, BF16, 2, 24),
+    (1100, BF16_OBF16, 2, 12), (1101, BF16_OBF16, 1, 12), (1102, BF16_OBF16, 2, 24),
+]
+
+
 def balanced_tp(p: eq1.Problem, tp_max: int, tk: int, slots: int) -> int:
     """Outputs per tile: as many rounds of `slots` workgroups as tiles of
     tp_max outputs need, and within them the most (hence smallest, equal)
@@ -232,6 +240,25 @@ def candidates(p: eq1.Problem, dtype: int, cus: int, lds_bytes: int, acc_regs: i
                 continue
             t, info = _cost(p, dtype, tk, tp, tc, lds, cus, lds_bytes, wg_per_cu)
             yield t, tk, tp, tc, vid, info
+        for vid, dt, nb, ks in SMALLC:
+            if dt != dtype or p.Ns > 8 or -(-(p.Nc * p.Nr) // 2) > ks:
+                continue
+            if (p.Nb * p.Nc * p.Nx * p.Ny * 2 >= 2 ** 31 or p.Nk * p.Nc * RS * 2 >= 2 ** 31):
+                continue
+            tk, tp_max, acc = 64, 128 * nb, 32 * nb
+            if (tp_max // (p.Nw * p.Nh) + 2) * p.Nk * p.Nw * p.Nh * e_out >= 2 ** 31:
+                continue
+
+            def lds_s(S):
+                return ks * 2 * 64 * 16 + p.Nc * S * (p.Ny + 8) * 2
+
+            wgs = max(1, min(wg_per_cu, lds_bytes // lds_s(_max_slab(p, tp_max))))
+            tp = balanced_tp(p, tp_max, tk, cus * wgs)
+            lds = lds_s(_max_slab(p, tp))
+            if lds > lds_bytes or acc > acc_regs:
+                continue
+            t, info = _cost(p, dtype, tk, tp, p.Nc, lds, cus, lds_bytes, wg_per_cu)
+            yield t, tk, tp, p.Nc, vid, info
         return
     kv = 1 if dtype == F32 else 8
     vec = 4 if dtype == F32 else 16
@@ -253,7 +280,7 @@ def choose(p: eq1.Problem, dtype: int, cus=256, lds_bytes=160 * 1024, acc_regs=1
     """(kernel, variant id, tk, tp, tc) the rule above selects; kernel 7 is
     the wide-staging family, 6 the DMA-staged one, 5 the register-staged
     pipelined one (8 when it stages raw Ker rows, 3 for its 1x1 gather),
-    2 the plain staging one, 1 the direct kernel."""
+    4 the few-channel one, 2 the plain staging one, 1 the direct kernel."""
     rawk_ids = {row[0] for row in IGEMM2 if row[10]}
     pw_ids = {row[0] for row in IGEMM2 if row[11]}
     best = None
@@ -265,7 +292,10 @@ def choose(p: eq1.Problem, dtype: int, cus=256, lds_bytes=160 * 1024, acc_regs=1
                 if tier == 0:
                     kern = 7 if vid >= 800 else 6
                 elif tier == 1:
-                    kern = 3 if vid in pw_ids else (8 if vid in rawk_ids else 5)
+                    if vid >= 1000:
+                        kern = 4
+                    else:
+                        kern = 3 if vid in pw_ids else (8 if vid in rawk_ids else 5)
                 else:
                     kern = 2
                 best = (key, (kern, vid, tk, tp, tc))

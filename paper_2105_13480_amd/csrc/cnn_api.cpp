@@ -167,6 +167,24 @@ int get_workspace(hipStream_t st, int64_t bytes, void** out) {
   return CNN_OK;
 }
 
+const VariantS* find_variant_s(int id) {
+  int n = 0;
+  const VariantS* vs = variants_smallc(&n);
+  for (int i = 0; i < n; ++i)
+    if (vs[i].id == id) return &vs[i];
+  return nullptr;
+}
+
+// Geometry a few-channel plan must carry (the kernel sizes LDS from it).
+bool smallc_geometry_ok(const VariantS& v, const cnn_plan_t& pl) {
+  const cnn_problem& p = pl.prob;
+  if (p.Ns > 8 || (p.Nc * p.Nr + 1) / 2 > v.ks || pl.tp < 1 || pl.tp > v.tp) return false;
+  const int64_t S = slab_rows_max(p, pl.tp);
+  const int64_t grid = ((p.Nb * p.Nw * p.Nh + pl.tp - 1) / pl.tp) * ((p.Nk + v.tk - 1) / v.tk);
+  return pl.slab_rows == S && pl.grid == grid && pl.lds_bytes == smallc_lds_bytes(v, p, S) &&
+         pl.lds_bytes <= 160 * 1024;
+}
+
 const Variant4* find_variant4(int id) {
   int n = 0;
   const Variant4* vs = variants4(&n);
@@ -222,6 +240,11 @@ int run_plan(const void* In, const void* Ker, void* Out, const cnn_plan_t& pl, h
   hipError_t e;
   if (pl.kernel == CNN_K_DIRECT) {
     e = launch_direct(In, Ker, Out, a, pl.dtype, st);
+  } else if (pl.kernel == CNN_K_SMALLC) {
+    const VariantS* vs = find_variant_s(pl.variant);
+    if (!vs || vs->dtype != pl.dtype || vs->tk != pl.tk || !smallc_geometry_ok(*vs, pl))
+      return fail(CNN_E_PLAN, "plan names no matching kernel instantiation (variant %d)", pl.variant);
+    e = launch_smallc(*vs, In, Ker, Out, a, pl.lds_bytes, st);
   } else if (const Variant4* v4 = find_variant4(pl.variant)) {
     if (pl.kernel != CNN_K_IGEMM_WIDE || v4->dtype != pl.dtype || v4->tk != pl.tk ||
         v4->tp != pl.tp || v4->tc != pl.tc || pl.ws_bytes != igemm4_ws_bytes(*v4, pl.prob))
@@ -324,7 +347,7 @@ int cnn_plan_tiles(const cnn_problem* prob, int dtype, int kernel, int64_t tk, i
   if (!prob || !plan) return fail(CNN_E_NULL, "prob and plan must be non-NULL");
   int st;
   if ((st = check_problem(*prob)) || (st = check_dtype(dtype))) return st;
-  if (kernel < CNN_K_AUTO || kernel > CNN_K_IGEMM_RAWK || kernel == CNN_K_SMALLC)
+  if (kernel < CNN_K_AUTO || kernel > CNN_K_IGEMM_RAWK)
     return fail(CNN_E_UNSUPPORTED, "unknown kernel %d", kernel);
   cnn_budget bud;
   if ((st = resolve_budget(budget, &bud))) return st;

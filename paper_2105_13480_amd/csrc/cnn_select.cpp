@@ -225,6 +225,26 @@ static bool eval_variant2(const cnn_problem& p, int dtype, const Variant2& v,
                      bud, plan, time_clk);
 }
 
+// Few-channel kernel (conv_smallc): the flattened (c, r) rows must fit the
+// registers' K-steps, the stencil at most 8 wide, the slab in LDS, and the
+// tensors the 32-bit offsets.
+static bool eval_smallc(const cnn_problem& p, int dtype, const VariantS& v, const cnn_budget& bud,
+                        cnn_plan_t* plan, double* time_clk) {
+  if (p.Ns > 8 || (p.Nc * p.Nr + 1) / 2 > v.ks) return false;
+  const int64_t Nx = p.sw * (p.Nw - 1) + p.Nr, Ny = p.sh * (p.Nh - 1) + p.Ns;
+  if (p.Nb * p.Nc * Nx * Ny * 2 >= (1LL << 31) || p.Nk * p.Nc * p.Nr * p.Ns * 2 >= (1LL << 31))
+    return false;
+  const int64_t imgs = v.tp / (p.Nw * p.Nh) + 2;
+  if (imgs * p.Nk * p.Nw * p.Nh * out_bytes(dtype) >= (1LL << 31)) return false;
+  const int64_t lds_full = smallc_lds_bytes(v, p, slab_rows_max(p, v.tp));
+  const int64_t occ = std::max<int64_t>(1, std::min<int64_t>(bud.wg_per_cu, bud.lds_bytes / lds_full));
+  const int64_t tp = balanced_tp(p, v.tp, v.tk, bud.cus * occ);
+  const int64_t S = slab_rows_max(p, tp);
+  const int64_t lds = smallc_lds_bytes(v, p, S);
+  // one stage holds every channel (tc = Nc)
+  return eval_tiling(p, dtype, v.id, v.tk, tp, p.Nc, v.acc, S, lds, 0, bud, plan, time_clk);
+}
+
 static void fill_common(const cnn_problem& p, int dtype, cnn_plan_t* plan) {
   const int64_t Nx = p.sw * (p.Nw - 1) + p.Nr, Ny = p.sh * (p.Nh - 1) + p.Ns;
   const double e_in = in_bytes(dtype), e_out = out_bytes(dtype);
@@ -265,7 +285,7 @@ int select_plan(const cnn_problem& p, int dtype, const cnn_budget& bud, int kern
   }
   if (kernel != CNN_K_AUTO && kernel != CNN_K_IGEMM && kernel != CNN_K_IGEMM_PIPE &&
       kernel != CNN_K_IGEMM_DMA && kernel != CNN_K_IGEMM_WIDE && kernel != CNN_K_IGEMM_RAWK &&
-      kernel != CNN_K_POINTWISE)
+      kernel != CNN_K_POINTWISE && kernel != CNN_K_SMALLC)
     return CNN_E_UNSUPPORTED;
   bool found = false;
   double best_t = 0;
@@ -314,6 +334,20 @@ int select_plan(const cnn_problem& p, int dtype, const cnn_budget& bud, int kern
     }
   }
   const bool tier1_found = found;
+  int ns = 0;
+  const VariantS* vss = variants_smallc(&ns);
+  for (int i = 0; i < ns; ++i) {
+    const VariantS& v = vss[i];
+    if (tier1_found || v.dtype != dtype || (kernel != CNN_K_AUTO && kernel != CNN_K_SMALLC))
+      continue;
+    if (kernel == CNN_K_SMALLC && (v.tk != tk || v.tp != tp)) continue;  // tc: always Nc
+    cnn_plan_t cand;
+    double t;
+    if (eval_smallc(p, dtype, v, bud, &cand, &t)) {
+      cand.kernel = CNN_K_SMALLC;
+      consider(cand, t);
+    }
+  }
   int n2 = 0;
   const Variant2* vs2 = variants2(&n2);
   for (int i = 0; i < n2; ++i) {
@@ -375,6 +409,11 @@ int enumerate_plans(const cnn_problem& p, int dtype, const cnn_budget& bud, cnn_
   for (int i = 0; i < n2; ++i)
     if (vs2[i].dtype == dtype && eval_variant2(p, dtype, vs2[i], bud, &cand, &t))
       add(cand, v2_family(vs2[i]));
+  int nsc = 0;
+  const VariantS* vss = variants_smallc(&nsc);
+  for (int i = 0; i < nsc; ++i)
+    if (vss[i].dtype == dtype && eval_smallc(p, dtype, vss[i], bud, &cand, &t))
+      add(cand, CNN_K_SMALLC);
   const Variant* vs = variants(&n1);
   for (int i = 0; i < n1; ++i)
     if (vs[i].dtype == dtype && vs[i].kernel == CNN_K_IGEMM &&

@@ -100,6 +100,19 @@ bool igemm4_fits(const Variant4& v, const cnn_problem& p, int64_t slab_rows);
 hipError_t launch_igemm4(const Variant4& v, const void* In, const void* Ker, void* Out,
                          void* ws, const ConvArgs& a, int64_t lds_bytes, hipStream_t stream);
 
+// A few-channel, wide-stencil instantiation (bf16): K = flattened (c, r, s8).
+struct VariantS {
+  int32_t id;
+  int32_t dtype;
+  int32_t tk, tp;   // tk = 64; tp = largest tile
+  int32_t ks;       // K-steps held in registers: ceil(Nc*Nr/2) <= ks
+  int32_t acc;
+};
+const VariantS* variants_smallc(int* count);
+int64_t smallc_lds_bytes(const VariantS& v, const cnn_problem& p, int64_t slab_rows);
+hipError_t launch_smallc(const VariantS& v, const void* In, const void* Ker, void* Out,
+                         const ConvArgs& a, int64_t lds_bytes, hipStream_t stream);
+
 // Ker repack for the pipelined kernels (defined with conv_igemm2).
 __global__ void pack_ker_bf16(const uint16_t* __restrict__ Ker, uint32_t __attribute__((ext_vector_type(4)))* __restrict__ P,
                               ConvArgs a, int TK, int TC, int blk_vecs, int64_t total_vecs);

@@ -1,0 +1,267 @@
+// Implicit-GEMM convolution for few input channels and wide stencils
+// (bf16 MFMA, gfx950), e.g. a 3-channel 7x7 input layer.
+//
+// Same tile schedule as the other implicit-GEMM kernels (paper Sec. 2.1,
+// Listing 3 with W_c = N_c; tiles of tp consecutive outputs of the
+// flattened (b, w, h) index by 64 features), but with Nc*Nr*Ns small the
+// whole contraction fits one stage, so the K dimension of the MFMA is the
+// flattened (c, r, s) index instead of channels:
+//
+// * K order: q = c*Nr + r, then s padded to 8, so each 8-element K-group of
+//   a lane is one (c, r) row of the stencil -- 8 consecutive input columns.
+//   ceil(Nc*Nr/2) MFMA K-steps of 16; padded taps carry zero weights.
+// * Ker (A operand): packed once per workgroup into an LDS image
+//   [K-step][lane half][feature][8] -- one 16-byte read per operand.
+// * In (B operand): the tile's halo'd slab -- every input row the tile's
+//   outputs touch, all Nc channels -- staged once in its natural layout
+//   (row stride Ny + 8, zero padding), and each operand gathered with eight
+//   16-bit LDS reads at the lane's output position plus the (c, r) offset.
+// * One tile per workgroup and several workgroups per CU: a workgroup's
+//   Out stores (the dominant HBM traffic of such layers) overlap other
+//   workgroups' staging and MFMA work.
+#include <type_traits>
+
+#include "internal.h"
+#include "common.h"
+
+namespace cnnlib {
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc_s(const void* base, int64_t bytes) {
+  bytes = (bytes + 3) & ~(int64_t)3;
+  const int32_t n = bytes > 0x7ffffffcLL ? 0x7ffffffc : (int32_t)bytes;
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, n, 0x00020000);
+}
+
+// KS: largest number of K-steps (ceil(Nc*Nr/2)) the registers hold.
+template <typename TO, int NB, int KS>
+__global__ __launch_bounds__(256) void conv_smallc(const bf16_t* __restrict__ In,
+                                                   const bf16_t* __restrict__ Ker,
+                                                   TO* __restrict__ Out, ConvArgs a) {
+  constexpr int MB = 2;         // 64 features per tile, shared by the 4 waves
+  constexpr int TK = 32 * MB;
+  constexpr int KVEC = KS * 2 * TK;  // Ker image vectors
+  static_assert(KVEC % 256 == 0, "whole Ker image vectors per thread");
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  u32x4_t* kimg = reinterpret_cast<u32x4_t*>(smem);           // [KS][2][TK]
+  bf16_t* slab = reinterpret_cast<bf16_t*>(kimg + KVEC);      // [Nc][S][RSTR]
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int l32 = lane & 31, half = lane >> 5;
+
+  const int tile = xcd_remap(blockIdx.x, gridDim.x);
+  const int pt = tile / a.n_ktiles;
+  const int kt = tile - pt * a.n_ktiles;
+  const int p0 = pt * a.tp;
+  const int k0 = kt * TK;
+  const int plast = min(p0 + a.tp, a.npix) - 1;
+  const int b0 = p0 / a.hw, w0 = (p0 - b0 * a.hw) / a.Nh;
+  const int b1 = plast / a.hw, w1 = (plast - b1 * a.hw) / a.Nh;
+  const int G0 = b0 * a.Nx + a.sw * w0;                    // first slab row (flattened b, x)
+  const int S = b1 * a.Nx + a.sw * w1 + a.Nr - G0;         // slab rows
+  const int RSTR = a.Ny + 8;                               // LDS row stride (elements)
+  const int nq = a.Nc * a.Nr;                              // (c, r) rows of the stencil
+  const int nks = (nq + 1) >> 1;                           // K-steps
+
+  // Ker image: vector (j, h, kk) holds Ker[k0+kk][c][r][0..7] for the
+  // (c, r) row q = 2j + h, zero past Ns, nq or Nk.  All of a thread's
+  // loads are issued before any is used.
+  {
+    const __amdgpu_buffer_rsrc_t kr = rsrc_s(Ker, (int64_t)a.Nk * a.Nc * a.Nr * a.Ns * 2);
+    constexpr int PER = KVEC / 256;
+    uint32_t e[PER][8];
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int v = tid + 256 * u;
+      const int kk = v % TK;
+      const int jh = v / TK;  // 2j + h == q
+      const int k = k0 + kk;
+      const bool qv = k < a.Nk && jh < nq;
+      const int q = qv ? jh : 0;
+      const int c = q / a.Nr, r = q - (q / a.Nr) * a.Nr;
+      const uint32_t base =
+          (uint32_t)((((int64_t)(qv ? k : 0) * a.Nc + c) * a.Nr + r) * a.Ns * 2);
+#pragma unroll
+      for (int s = 0; s < 8; ++s)
+        e[u][s] = (qv && s < a.Ns) ? __builtin_amdgcn_raw_buffer_load_b16(kr, base + 2 * s, 0, 0)
+                                   : 0u;
+    }
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      u32x4_t vv;
+#pragma unroll
+      for (int d = 0; d < 4; ++d) vv[d] = e[u][2 * d] | (e[u][2 * d + 1] << 16);
+      kimg[tid + 256 * u] = vv;
+    }
+  }
+
+  // Stage the slab: element (c, row, col) of the LDS image is
+  // In[b][c][x][col] for flattened input row G0 + row = b*Nx + x; the 8
+  // padding columns are zero.  Batches of 16 independent loads per thread.
+  {
+    const __amdgpu_buffer_rsrc_t ir = rsrc_s(In, a.in_total * 2);
+    const int n = a.Nc * S * RSTR;
+    constexpr int U = 16;
+    for (int e0 = 0; e0 < n; e0 += 256 * U) {
+      uint32_t v[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int e = e0 + tid + 256 * u;
+        const int c = e / (S * RSTR);
+        const int rem = e - c * (S * RSTR);
+        const int row = rem / RSTR;
+        const int col = rem - row * RSTR;
+        const int gr = G0 + row;
+        const int b = gr / a.Nx;
+        const int x = gr - b * a.Nx;
+        const int64_t off =
+            (int64_t)b * a.in_img + (int64_t)c * a.nxny + (int64_t)x * a.Ny + col;
+        const bool ok = e < n && col < a.Ny;
+        v[u] = ok ? __builtin_amdgcn_raw_buffer_load_b16(ir, (uint32_t)(off * 2), 0, 0) : 0u;
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int e = e0 + tid + 256 * u;
+        if (e < n) slab[e] = (bf16_t)v[u];
+      }
+    }
+  }
+  __syncthreads();
+
+  // Output side: each lane's slab position and Out offset; lanes past the
+  // tile's last output recompute and rewrite it (no store masks).
+  int pbase[NB];
+  uint32_t obyte[NB];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
+    const int p = p0 + (wave * NB + nb) * 32 + l32;
+    const int pc = p <= plast ? p : plast;
+    const int b = pc / a.hw;
+    const int q = pc - b * a.hw;
+    const int w = q / a.Nh;
+    const int h = q - w * a.Nh;
+    pbase[nb] = (b * a.Nx + a.sw * w - G0) * RSTR + a.sh * h;
+    obyte[nb] = (uint32_t)(((int64_t)(b - b0) * a.Nk * a.hw + q) * (int64_t)sizeof(TO));
+  }
+
+  f32x16_t acc[MB][NB];
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+      for (int j = 0; j < 16; ++j) acc[mb][nb][j] = 0.f;
+
+#pragma unroll
+  for (int j = 0; j < KS; ++j) {
+    if (j < nks) {
+      const int q = min(2 * j + half, nq - 1);  // past nq: weights are zero
+      const int c = q / a.Nr, r = q - (q / a.Nr) * a.Nr;
+      const int qoff = (c * S + r) * RSTR;
+      u32x4_t bv[NB];
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) {
+        const bf16_t* src = slab + qoff + pbase[nb];
+#pragma unroll
+        for (int d = 0; d < 4; ++d)
+          bv[nb][d] = (uint32_t)src[2 * d] | ((uint32_t)src[2 * d + 1] << 16);
+      }
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) {
+        const u32x4_t av = kimg[(2 * j + half) * TK + mb * 32 + l32];
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb)
+          acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+              __builtin_bit_cast(bf16x8_t, av), __builtin_bit_cast(bf16x8_t, bv[nb]),
+              acc[mb][nb], 0, 0, 0);
+      }
+    }
+  }
+
+  // Epilogue: register j of a 32x32 accumulator holds feature
+  // 8*(j/4) + 4*half + j%4 of output l32.
+  const __amdgpu_buffer_rsrc_t out_rsrc =
+      rsrc_s(Out + (int64_t)b0 * a.Nk * a.hw,
+             (a.out_total - (int64_t)b0 * a.Nk * a.hw) * (int64_t)sizeof(TO));
+  const uint32_t half_off = (uint32_t)(4 * half * a.hw * (int)sizeof(TO));
+  const bool k_full = k0 + TK <= a.Nk;
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) {
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      const int kw = k0 + mb * 32 + 8 * (j >> 2) + (j & 3);
+      const uint32_t so = (uint32_t)kw * (uint32_t)a.hw * (uint32_t)sizeof(TO);
+      if (k_full || kw + 4 * half < a.Nk) {
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) {
+          if constexpr (sizeof(TO) == 4) {
+            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc[mb][nb][j]), out_rsrc,
+                                                  obyte[nb] + half_off, so, 0);
+          } else {
+            __builtin_amdgcn_raw_buffer_store_b16(from_f32<bf16_t>(acc[mb][nb][j]), out_rsrc,
+                                                  obyte[nb] + half_off, so, 0);
+          }
+        }
+      }
+    }
+  }
+}
+
+// ---- instantiation table ----------------------------------------------------
+// (id, dtype, NB, KS): tk = 64, tp = 128*NB (largest tile); KS = most
+// K-steps, ceil(Nc*Nr/2) <= KS; any Ns <= 8, any stride.
+#define CNN_SMALLC_VARIANTS(X)             \
+  X(1000, CNN_BF16, 2, 12)                 \
+  X(1001, CNN_BF16, 1, 12)                 \
+  X(1002, CNN_BF16, 2, 24)                 \
+  X(1100, CNN_BF16_OBF16, 2, 12)           \
+  X(1101, CNN_BF16_OBF16, 1, 12)           \
+  X(1102, CNN_BF16_OBF16, 2, 24)
+
+static const VariantS kVariantsS[] = {
+#define CNN_ROWS(id, dt, nb, ks) {id, dt, 64, 128 * (nb), ks, 16 * 2 * (nb)},
+    CNN_SMALLC_VARIANTS(CNN_ROWS)
+#undef CNN_ROWS
+};
+
+const VariantS* variants_smallc(int* count) {
+  *count = (int)(sizeof(kVariantsS) / sizeof(kVariantsS[0]));
+  return kVariantsS;
+}
+
+int64_t smallc_lds_bytes(const VariantS& v, const cnn_problem& p, int64_t slab_rows) {
+  return (int64_t)v.ks * 2 * v.tk * 16 + p.Nc * slab_rows * (p.sh * (p.Nh - 1) + p.Ns + 8) * 2;
+}
+
+template <int DT, int NB, int KS>
+static hipError_t launch_s(const void* In, const void* Ker, void* Out, const ConvArgs& a,
+                           int64_t lds, hipStream_t stream) {
+  typedef typename std::conditional<DT == CNN_BF16, float, bf16_t>::type TO;
+  auto kern = conv_smallc<TO, NB, KS>;
+  static bool attr_set = false;
+  if (!attr_set) {
+    hipError_t e = hipFuncSetAttribute((const void*)kern,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+    if (e != hipSuccess) return e;
+    attr_set = true;
+  }
+  hipLaunchKernelGGL(kern, dim3((unsigned)a.grid), dim3(256), (unsigned)lds, stream,
+                     (const bf16_t*)In, (const bf16_t*)Ker, (TO*)Out, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_smallc(const VariantS& v, const void* In, const void* Ker, void* Out,
+                         const ConvArgs& a, int64_t lds_bytes, hipStream_t stream) {
+  switch (v.id) {
+#define CNN_CASES(id, dt, nb, ks) \
+  case id:                        \
+    return launch_s<dt, nb, ks>(In, Ker, Out, a, lds_bytes, stream);
+    CNN_SMALLC_VARIANTS(CNN_CASES)
+#undef CNN_CASES
+    default:
+      return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace cnnlib
