@@ -95,9 +95,13 @@ typedef enum cnn_kernel {
   CNN_K_IGEMM_WIDE = 7,/* implicit GEMM, bf16: In staged as 8x8 (position x channel)
                          blocks of 16-byte loads transposed in registers, swizzled LDS,
                          MFMA operands prefetched one K-step ahead                  */
-  CNN_K_IGEMM_RAWK = 8 /* as CNN_K_IGEMM_PIPE for fixed 3x3 / 1x1 stencils, Nc % 8 == 0:
+  CNN_K_IGEMM_RAWK = 8,/* as CNN_K_IGEMM_PIPE for fixed 3x3 / 1x1 stencils, Nc % 8 == 0:
                          raw Ker rows copied by DMA, MFMA operands built in registers,
                          no repack and no workspace                                 */
+  CNN_K_STREAM = 9    /* persistent workgroups (grid = workgroup slots) walking tile
+                         ranges as one pipeline: next tile's loads during the last
+                         stage, Out stores drain under the next tile; raw Ker, kept
+                         resident in LDS when it fits; fixed 3x3, Nc % 8 == 0     */
 } cnn_kernel;
 
 /*

@@ -128,13 +128,30 @@ SMALLC = [
 ]
 
 
-def balanced_tp(p: eq1.Problem, tp_max: int, tk: int, slots: int) -> int:
+# (id, dtype, wm, wn, mb, nb, tc, nr, ns, kres) of the persistent streaming
+# kernel: tk = 32*wm*mb, tp = 32*wn*nb, 64*wm*wn threads (one input pair
+# each); kres keeps all of Ker in LDS (Nk <= tk); grid = workgroup slots.
+STREAM = [
+    (1300, BF16, 1, 8, 2, 1, 16, 3, 3, 1), (1310, BF16, 2, 4, 2, 1, 16, 3, 3, 0),
+    (1400, BF16_OBF16, 1, 8, 2, 1, 16, 3, 3, 1), (1410, BF16_OBF16, 2, 4, 2, 1, 16, 3, 3, 0),
+]
+
+
+def stream_grid(p: eq1.Problem, tk: int, tp: int, threads: int, lds: int, cus: int,
+                lds_bytes: int, wg_per_cu: int) -> int:
+    """Workgroups a streaming plan launches: its slots, at most its tiles."""
+    slots = cus * max(1, min(wg_per_cu * 256 // threads, lds_bytes // lds))
+    return min(slots, -(-(p.Nb * p.Nw * p.Nh) // tp) * -(-p.Nk // tk))
+
+
+def balanced_tp(p: eq1.Problem, tp_max: int, tk: int, slots: int, min_rounds: int = 1) -> int:
     """Outputs per tile: as many rounds of `slots` workgroups as tiles of
     tp_max outputs need, and within them the most (hence smallest, equal)
-    tiles -- each processor's share N/P of Eq. (2).  Even, never below 32."""
+    tiles -- each processor's share N/P of Eq. (2).  Even, never below 32;
+    min_rounds > 1 asks for that many tiles per slot (persistent kernels)."""
     npix = p.Nb * p.Nw * p.Nh
     nk = -(-p.Nk // tk)
-    rounds = -(-(-(-npix // tp_max) * nk) // slots)
+    rounds = max(min_rounds, -(-(-(-npix // tp_max) * nk) // slots))
     ptiles = max(1, (rounds * slots) // nk)
     tp = -(-npix // ptiles)
     if tp % 2:
@@ -240,6 +257,34 @@ def candidates(p: eq1.Problem, dtype: int, cus: int, lds_bytes: int, acc_regs: i
                 continue
             t, info = _cost(p, dtype, tk, tp, tc, lds, cus, lds_bytes, wg_per_cu)
             yield t, tk, tp, tc, vid, info
+        for vid, dt, wm, wn, mb, nb, tc, nr, ns, kres in STREAM:
+            if dt != dtype or (nr, ns) != (p.Nr, p.Ns) or p.Nc % 8:
+                continue
+            tk, tp_max, acc, threads = 32 * wm * mb, 32 * wn * nb, 16 * mb * nb, 64 * wm * wn
+            if kres and p.Nk > tk:
+                continue
+            if ((p.Nk + 512) * p.Nc * RS * 2 >= 2 ** 31 or p.Nb * p.Nc * p.Nx * p.Ny * 2 >= 2 ** 31
+                    or p.Nb * p.Nk * p.Nw * p.Nh * e_out >= 2 ** 31):
+                continue
+            rc = (RS * tc // 8) | 1
+            kvecs = -(-(tk * rc) // 64) * 64
+            n_cc = -(-p.Nc // tc)
+
+            def lds_t(S):
+                sn = (S * p.Ny + 1) // 2 * 2 + 2
+                return (2 * (tc // 8) * sn + (n_cc if kres else 2) * kvecs) * 16
+
+            lds_full = lds_t(_max_slab(p, tp_max))
+            slots = cus * max(1, min(wg_per_cu * 256 // threads, lds_bytes // lds_full))
+            tp = balanced_tp(p, tp_max, tk, slots, 2)
+            S = _max_slab(p, tp)
+            if -(-(S * p.Ny) // 2) > threads:
+                continue
+            lds = lds_t(S)
+            if lds > lds_bytes or acc > acc_regs:
+                continue
+            t, info = _cost(p, dtype, tk, tp, tc, lds, cus, lds_bytes, wg_per_cu)
+            yield t, tk, tp, tc, vid, info
         for vid, dt, nb, ks in SMALLC:
             if dt != dtype or p.Ns > 8 or -(-(p.Nc * p.Nr) // 2) > ks:
                 continue
@@ -280,7 +325,8 @@ def choose(p: eq1.Problem, dtype: int, cus=256, lds_bytes=160 * 1024, acc_regs=1
     """(kernel, variant id, tk, tp, tc) the rule above selects; kernel 7 is
     the wide-staging family, 6 the DMA-staged one, 5 the register-staged
     pipelined one (8 when it stages raw Ker rows, 3 for its 1x1 gather),
-    4 the few-channel one, 2 the plain staging one, 1 the direct kernel."""
+    4 the few-channel one, 9 the persistent streaming one, 2 the plain
+    staging one, 1 the direct kernel."""
     rawk_ids = {row[0] for row in IGEMM2 if row[10]}
     pw_ids = {row[0] for row in IGEMM2 if row[11]}
     best = None
@@ -292,7 +338,9 @@ def choose(p: eq1.Problem, dtype: int, cus=256, lds_bytes=160 * 1024, acc_regs=1
                 if tier == 0:
                     kern = 7 if vid >= 800 else 6
                 elif tier == 1:
-                    if vid >= 1000:
+                    if vid >= 1300:
+                        kern = 9
+                    elif vid >= 1000:
                         kern = 4
                     else:
                         kern = 3 if vid in pw_ids else (8 if vid in rawk_ids else 5)

@@ -20,10 +20,10 @@ CNN_F32, CNN_BF16, CNN_BF16_OBF16 = 0, 1, 2
 DTYPES = {"f32": CNN_F32, "bf16": CNN_BF16, "bf16_obf16": CNN_BF16_OBF16}
 
 (K_AUTO, K_DIRECT, K_IGEMM, K_POINTWISE, K_SMALLC, K_IGEMM_PIPE, K_IGEMM_DMA, K_IGEMM_WIDE,
- K_IGEMM_RAWK) = range(9)
+ K_IGEMM_RAWK, K_STREAM) = range(10)
 KERNEL_NAMES = {K_DIRECT: "direct", K_IGEMM: "igemm", K_POINTWISE: "pointwise", K_SMALLC: "smallc",
                 K_IGEMM_PIPE: "igemm_pipe", K_IGEMM_DMA: "igemm_dma", K_IGEMM_WIDE: "igemm_wide",
-                K_IGEMM_RAWK: "igemm_rawk"}
+                K_IGEMM_RAWK: "igemm_rawk", K_STREAM: "stream"}
 
 STATUS = {0: "CNN_OK", -1: "CNN_E_NULL", -2: "CNN_E_SHAPE", -3: "CNN_E_DTYPE",
           -4: "CNN_E_OVERFLOW", -5: "CNN_E_ALIAS", -6: "CNN_E_UNSUPPORTED",
@@ -82,6 +82,10 @@ def lib():
     if not os.path.exists(LIB_PATH):
         raise RuntimeError(f"HIP library missing: {LIB_PATH} "
                            "(build it with: python -m paper_2105_13480_amd.build)")
+    # The library and torch both need libamdhip64.so.7, and the loader keeps
+    # the first one loaded.  Load torch's first: a process whose torch ran
+    # on another copy of the HIP runtime finds no GPU.
+    import torch  # noqa: F401
     L = ctypes.CDLL(LIB_PATH)
     vp = ctypes.c_void_p
     P, T, B, PL = (ctypes.POINTER(x) for x in (Problem, Tiles, Budget, Plan))

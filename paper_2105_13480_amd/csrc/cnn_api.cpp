@@ -185,6 +185,27 @@ bool smallc_geometry_ok(const VariantS& v, const cnn_plan_t& pl) {
          pl.lds_bytes <= 160 * 1024;
 }
 
+const VariantT* find_variant_t(int id) {
+  int n = 0;
+  const VariantT* vs = variants_stream(&n);
+  for (int i = 0; i < n; ++i)
+    if (vs[i].id == id) return &vs[i];
+  return nullptr;
+}
+
+// Geometry a streaming plan must carry: the kernel sizes LDS, its pair
+// slots and its tile ranges from it.
+bool stream_geometry_ok(const VariantT& v, const cnn_plan_t& pl) {
+  const cnn_problem& p = pl.prob;
+  if (v.nr != p.Nr || v.ns != p.Ns || p.Nc % 8 != 0 || (v.kres && p.Nk > v.tk)) return false;
+  if (pl.tp < 1 || pl.tp > v.tp) return false;
+  const int64_t Ny = p.sh * (p.Nh - 1) + p.Ns;
+  const int64_t S = slab_rows_max(p, pl.tp);
+  const int64_t tiles = ((p.Nb * p.Nw * p.Nh + pl.tp - 1) / pl.tp) * ((p.Nk + v.tk - 1) / v.tk);
+  return pl.slab_rows == S && (S * Ny + 1) / 2 <= v.threads && pl.grid >= 1 && pl.grid <= tiles &&
+         pl.lds_bytes == stream_lds_bytes(v, p, S) && pl.lds_bytes <= 160 * 1024;
+}
+
 const Variant4* find_variant4(int id) {
   int n = 0;
   const Variant4* vs = variants4(&n);
@@ -240,6 +261,12 @@ int run_plan(const void* In, const void* Ker, void* Out, const cnn_plan_t& pl, h
   hipError_t e;
   if (pl.kernel == CNN_K_DIRECT) {
     e = launch_direct(In, Ker, Out, a, pl.dtype, st);
+  } else if (pl.kernel == CNN_K_STREAM) {
+    const VariantT* vt = find_variant_t(pl.variant);
+    if (!vt || vt->dtype != pl.dtype || vt->tk != pl.tk || vt->tc != pl.tc ||
+        !stream_geometry_ok(*vt, pl))
+      return fail(CNN_E_PLAN, "plan names no matching kernel instantiation (variant %d)", pl.variant);
+    e = launch_stream(*vt, In, Ker, Out, a, pl.lds_bytes, st);
   } else if (pl.kernel == CNN_K_SMALLC) {
     const VariantS* vs = find_variant_s(pl.variant);
     if (!vs || vs->dtype != pl.dtype || vs->tk != pl.tk || !smallc_geometry_ok(*vs, pl))
@@ -347,7 +374,7 @@ int cnn_plan_tiles(const cnn_problem* prob, int dtype, int kernel, int64_t tk, i
   if (!prob || !plan) return fail(CNN_E_NULL, "prob and plan must be non-NULL");
   int st;
   if ((st = check_problem(*prob)) || (st = check_dtype(dtype))) return st;
-  if (kernel < CNN_K_AUTO || kernel > CNN_K_IGEMM_RAWK)
+  if (kernel < CNN_K_AUTO || kernel > CNN_K_STREAM)
     return fail(CNN_E_UNSUPPORTED, "unknown kernel %d", kernel);
   cnn_budget bud;
   if ((st = resolve_budget(budget, &bud))) return st;

@@ -181,11 +181,13 @@ static bool eval_variant3(const cnn_problem& p, int dtype, const Variant3& v,
 // then the smallest tile that still fits in those rounds, so every
 // workgroup of every round gets the same share (the P processors of
 // Eq. (2) each take N/P).  Rounded up to an even count (the kernels stage
-// outputs in pairs), at least 32 outputs (one MFMA block).
-int64_t balanced_tp(const cnn_problem& p, int64_t TP, int64_t tk, int64_t slots) {
+// outputs in pairs), at least 32 outputs (one MFMA block).  min_rounds > 1
+// asks for at least that many tiles per slot (persistent kernels).
+int64_t balanced_tp(const cnn_problem& p, int64_t TP, int64_t tk, int64_t slots,
+                    int64_t min_rounds) {
   const int64_t npix = p.Nb * p.Nw * p.Nh;
   const int64_t n_k = ceil_div(p.Nk, tk);
-  const int64_t rounds = ceil_div(ceil_div(npix, TP) * n_k, slots);
+  const int64_t rounds = std::max(min_rounds, ceil_div(ceil_div(npix, TP) * n_k, slots));
   const int64_t ptiles = std::max<int64_t>(1, rounds * slots / n_k);
   int64_t tp = ceil_div(npix, ptiles);
   tp += tp & 1;
@@ -209,7 +211,7 @@ static bool eval_variant2(const cnn_problem& p, int dtype, const Variant2& v,
   const int64_t Ny = p.sh * (p.Nh - 1) + p.Ns;
   const int64_t lds_full = igemm2_lds_bytes(v, slab_rows_max(p, v.tp), Ny, p.Nr * p.Ns, v.tp);
   const int64_t occ = std::max<int64_t>(1, std::min<int64_t>(bud.wg_per_cu, bud.lds_bytes / lds_full));
-  const int64_t tp = balanced_tp(p, v.tp, v.tk, bud.cus * occ);
+  const int64_t tp = balanced_tp(p, v.tp, v.tk, bud.cus * occ, 1);
   const int64_t S = slab_rows_max(p, tp);
   const int64_t pairs = v.pw ? (tp + 1) / 2 : (S * Ny + 1) / 2;
   if (pairs > 256 * (int64_t)v.maxp) return false;
@@ -238,11 +240,37 @@ static bool eval_smallc(const cnn_problem& p, int dtype, const VariantS& v, cons
   if (imgs * p.Nk * p.Nw * p.Nh * out_bytes(dtype) >= (1LL << 31)) return false;
   const int64_t lds_full = smallc_lds_bytes(v, p, slab_rows_max(p, v.tp));
   const int64_t occ = std::max<int64_t>(1, std::min<int64_t>(bud.wg_per_cu, bud.lds_bytes / lds_full));
-  const int64_t tp = balanced_tp(p, v.tp, v.tk, bud.cus * occ);
+  const int64_t tp = balanced_tp(p, v.tp, v.tk, bud.cus * occ, 1);
   const int64_t S = slab_rows_max(p, tp);
   const int64_t lds = smallc_lds_bytes(v, p, S);
   // one stage holds every channel (tc = Nc)
   return eval_tiling(p, dtype, v.id, v.tk, tp, p.Nc, v.acc, S, lds, 0, bud, plan, time_clk);
+}
+
+// Persistent streaming kernel (conv_stream): fixed stencil, Nc % 8 == 0,
+// one input pair per thread, KRES needs one k tile; the grid is the
+// workgroup slots (each walks a range of tiles).
+static bool eval_stream(const cnn_problem& p, int dtype, const VariantT& v, const cnn_budget& bud,
+                        cnn_plan_t* plan, double* time_clk) {
+  if (v.nr != p.Nr || v.ns != p.Ns || p.Nc % 8 != 0) return false;
+  if (v.kres && p.Nk > v.tk) return false;
+  const int64_t Nx = p.sw * (p.Nw - 1) + p.Nr, Ny = p.sh * (p.Nh - 1) + p.Ns;
+  if ((p.Nk + 512) * p.Nc * p.Nr * p.Ns * 2 >= (1LL << 31) ||
+      p.Nb * p.Nc * Nx * Ny * 2 >= (1LL << 31) ||
+      p.Nb * p.Nk * p.Nw * p.Nh * out_bytes(dtype) >= (1LL << 31))
+    return false;
+  const int64_t lds_full = stream_lds_bytes(v, p, slab_rows_max(p, v.tp));
+  const int64_t occ = std::max<int64_t>(
+      1, std::min<int64_t>(bud.wg_per_cu * 256 / v.threads, bud.lds_bytes / lds_full));
+  const int64_t slots = bud.cus * occ;
+  const int64_t tp = balanced_tp(p, v.tp, v.tk, slots, 2);
+  const int64_t S = slab_rows_max(p, tp);
+  if ((S * Ny + 1) / 2 > v.threads) return false;
+  const int64_t lds = stream_lds_bytes(v, p, S);
+  if (!eval_tiling(p, dtype, v.id, v.tk, tp, v.tc, v.acc, S, lds, 0, bud, plan, time_clk))
+    return false;
+  plan->grid = std::min<int64_t>(plan->grid, slots);
+  return true;
 }
 
 static void fill_common(const cnn_problem& p, int dtype, cnn_plan_t* plan) {
@@ -285,7 +313,7 @@ int select_plan(const cnn_problem& p, int dtype, const cnn_budget& bud, int kern
   }
   if (kernel != CNN_K_AUTO && kernel != CNN_K_IGEMM && kernel != CNN_K_IGEMM_PIPE &&
       kernel != CNN_K_IGEMM_DMA && kernel != CNN_K_IGEMM_WIDE && kernel != CNN_K_IGEMM_RAWK &&
-      kernel != CNN_K_POINTWISE && kernel != CNN_K_SMALLC)
+      kernel != CNN_K_POINTWISE && kernel != CNN_K_SMALLC && kernel != CNN_K_STREAM)
     return CNN_E_UNSUPPORTED;
   bool found = false;
   double best_t = 0;
@@ -334,6 +362,20 @@ int select_plan(const cnn_problem& p, int dtype, const cnn_budget& bud, int kern
     }
   }
   const bool tier1_found = found;
+  int nt = 0;
+  const VariantT* vst = variants_stream(&nt);
+  for (int i = 0; i < nt; ++i) {
+    const VariantT& v = vst[i];
+    if (tier1_found || v.dtype != dtype || (kernel != CNN_K_AUTO && kernel != CNN_K_STREAM))
+      continue;
+    if (kernel == CNN_K_STREAM && (v.tk != tk || v.tp != tp || v.tc != tc)) continue;
+    cnn_plan_t cand;
+    double t;
+    if (eval_stream(p, dtype, v, bud, &cand, &t)) {
+      cand.kernel = CNN_K_STREAM;
+      consider(cand, t);
+    }
+  }
   int ns = 0;
   const VariantS* vss = variants_smallc(&ns);
   for (int i = 0; i < ns; ++i) {
@@ -409,6 +451,11 @@ int enumerate_plans(const cnn_problem& p, int dtype, const cnn_budget& bud, cnn_
   for (int i = 0; i < n2; ++i)
     if (vs2[i].dtype == dtype && eval_variant2(p, dtype, vs2[i], bud, &cand, &t))
       add(cand, v2_family(vs2[i]));
+  int ntt = 0;
+  const VariantT* vst = variants_stream(&ntt);
+  for (int i = 0; i < ntt; ++i)
+    if (vst[i].dtype == dtype && eval_stream(p, dtype, vst[i], bud, &cand, &t))
+      add(cand, CNN_K_STREAM);
   int nsc = 0;
   const VariantS* vss = variants_smallc(&nsc);
   for (int i = 0; i < nsc; ++i)

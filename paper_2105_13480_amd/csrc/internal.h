@@ -113,6 +113,21 @@ int64_t smallc_lds_bytes(const VariantS& v, const cnn_problem& p, int64_t slab_r
 hipError_t launch_smallc(const VariantS& v, const void* In, const void* Ker, void* Out,
                          const ConvArgs& a, int64_t lds_bytes, hipStream_t stream);
 
+// A persistent streaming instantiation (bf16, fixed stencil, raw Ker).
+struct VariantT {
+  int32_t id;
+  int32_t dtype;
+  int32_t tk, tp, tc;  // tp = largest tile
+  int32_t acc;
+  int32_t nr, ns;      // compile-time stencil
+  int32_t threads;     // workgroup size
+  int32_t kres;        // 1: the whole Ker stays in LDS (Nk <= tk)
+};
+const VariantT* variants_stream(int* count);
+int64_t stream_lds_bytes(const VariantT& v, const cnn_problem& p, int64_t slab_rows);
+hipError_t launch_stream(const VariantT& v, const void* In, const void* Ker, void* Out,
+                         const ConvArgs& a, int64_t lds_bytes, hipStream_t stream);
+
 // Ker repack for the pipelined kernels (defined with conv_igemm2).
 __global__ void pack_ker_bf16(const uint16_t* __restrict__ Ker, uint32_t __attribute__((ext_vector_type(4)))* __restrict__ P,
                               ConvArgs a, int TK, int TC, int blk_vecs, int64_t total_vecs);

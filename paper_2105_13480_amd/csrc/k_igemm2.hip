@@ -119,8 +119,11 @@ __host__ __device__ constexpr int rawk_row_chunks(int RS, int TC) {
   return (RS * TC / 8) | 1;
 }
 
+// ODDY: the input rows have odd length, so pairs need the funnel or the
+// element path (and two words per pair in flight); with Ny even every pair
+// is one aligned dword.  The launcher picks the instantiation from Ny.
 template <typename TO, int WM, int WN, int MB, int NB, int TC, int NR, int NS, int MAXP,
-          bool RAWK, bool PW>
+          bool RAWK, bool PW, bool ODDY>
 __global__ __launch_bounds__(256) void conv_igemm2(const bf16_t* __restrict__ In,
                                                    const u32x4_t* __restrict__ Kp,
                                                    TO* __restrict__ Out, ConvArgs a,
@@ -198,12 +201,12 @@ __global__ __launch_bounds__(256) void conv_igemm2(const bf16_t* __restrict__ In
       path = kStride2;
     else
       path = kElement;
+  } else if constexpr (!ODDY) {
+    path = kAligned;  // Ny even: pairs are aligned and never straddle an image
   } else {
-    path = ((a.Ny & 1) == 0 && (base_el & 1) == 0) ? kAligned : kFunnel;
-    if (path == kFunnel) {
-      for (int b = b0 + 1; b <= b1; ++b)
-        if ((((int64_t)b * a.Nx - G0) * a.Ny) & 1) path = kElement;
-    }
+    path = kFunnel;
+    for (int b = b0 + 1; b <= b1; ++b)
+      if ((((int64_t)b * a.Nx - G0) * a.Ny) & 1) path = kElement;
   }
   const int gpos0 = G0 * a.Ny;
   uint32_t voff[MAXP], voff2[MAXP];  // byte offsets (channel 0) of pos / of pos+1
@@ -240,6 +243,7 @@ __global__ __launch_bounds__(256) void conv_igemm2(const bf16_t* __restrict__ In
   }
 
   uint32_t pre[G][MAXP][8];
+  uint32_t pre2[G][MAXP][8];  // second word of a pair (row paths; unused by the gather)
   // Gather staging (1x1 kernels), the stage starting at c0: channel
   // q = 8g + i into every pair slot (slots past the tile reload position
   // 0).  One uniform switch on the load path per stage, then straight-line
@@ -267,42 +271,40 @@ __global__ __launch_bounds__(256) void conv_igemm2(const bf16_t* __restrict__ In
       }
     }
   };
-  // Slab staging (row-staged kernels): per channel, a uniform test and
-  // the path switch.  Measured faster than load_path's straight-line form
-  // for the 3x3 tilings, slower for the 1x1 gather.
-  auto load_rows = [&](int c0) __attribute__((always_inline)) {
+  // Slab staging (row-staged kernels): one uniform switch on the load path
+  // per stage, then straight-line loads of every channel (a channel past Nc
+  // loads channel Nc-1; write_in zeroes it).  The words of a pair are
+  // combined only in write_in, so no load waits for another.
+  auto load_rows_p = [&](auto tag, int c0) __attribute__((always_inline)) {
+    constexpr int P = decltype(tag)::value;
 #pragma unroll
     for (int q = 0; q < 8 * G; ++q) {
       const int g = q >> 3, i = q & 7;
-      const int c = c0 + q;
-      if (c < a.Nc) {
-        const uint32_t so = (uint32_t)((int64_t)c * a.nxny * 2);
-        if (path == kAligned) {
+      const uint32_t so = (uint32_t)((int64_t)min(c0 + q, a.Nc - 1) * a.nxny * 2);
 #pragma unroll
-          for (int j = 0; j < MAXP; ++j)
-            pre[g][j][i] = __builtin_amdgcn_raw_buffer_load_b32(in_rsrc, voff[j], so, 0);
-        } else if (path == kFunnel) {
-#pragma unroll
-          for (int j = 0; j < MAXP; ++j) {
-            const uint32_t t = voff[j] + (so & 2u);
-            const uint32_t lo_off = t & ~3u;
-            const uint32_t lo = __builtin_amdgcn_raw_buffer_load_b32(in_rsrc, lo_off, so & ~3u, 0);
-            const uint32_t hi = __builtin_amdgcn_raw_buffer_load_b32(in_rsrc, lo_off + 4, so & ~3u, 0);
-            pre[g][j][i] = __builtin_amdgcn_alignbit(hi, lo, (t & 2u) * 8u);
-          }
+      for (int j = 0; j < MAXP; ++j) {
+        if constexpr (P == kAligned) {
+          pre[g][j][i] = __builtin_amdgcn_raw_buffer_load_b32(in_rsrc, voff[j], so, 0);
+        } else if constexpr (P == kFunnel) {
+          // the two aligned dwords around the pair
+          const uint32_t lo_off = (voff[j] + (so & 2u)) & ~3u;
+          pre[g][j][i] = __builtin_amdgcn_raw_buffer_load_b32(in_rsrc, lo_off, so & ~3u, 0);
+          pre2[g][j][i] = __builtin_amdgcn_raw_buffer_load_b32(in_rsrc, lo_off + 4, so & ~3u, 0);
         } else {
-#pragma unroll
-          for (int j = 0; j < MAXP; ++j) {
-            const uint32_t lo = __builtin_amdgcn_raw_buffer_load_b16(in_rsrc, voff[j], so, 0);
-            const uint32_t hi = __builtin_amdgcn_raw_buffer_load_b16(in_rsrc, voff2[j], so, 0);
-            pre[g][j][i] = lo | (hi << 16);
-          }
+          // the pair's two elements
+          pre[g][j][i] = __builtin_amdgcn_raw_buffer_load_b16(in_rsrc, voff[j], so, 0);
+          pre2[g][j][i] = __builtin_amdgcn_raw_buffer_load_b16(in_rsrc, voff2[j], so, 0);
         }
-      } else {
-#pragma unroll
-        for (int j = 0; j < MAXP; ++j) pre[g][j][i] = 0u;
       }
     }
+  };
+  auto load_rows = [&](int c0) __attribute__((always_inline)) {
+    if constexpr (!ODDY)
+      load_rows_p(std::integral_constant<int, kAligned>(), c0);
+    else if (path == kFunnel)
+      load_rows_p(std::integral_constant<int, kFunnel>(), c0);
+    else
+      load_rows_p(std::integral_constant<int, kElement>(), c0);
   };
   auto load_in = [&](int c0) __attribute__((always_inline)) {
     if constexpr (PW) {
@@ -316,21 +318,39 @@ __global__ __launch_bounds__(256) void conv_igemm2(const bf16_t* __restrict__ In
       load_rows(c0);
     }
   };
-  auto write_in = [&](u32x4_t* buf, int c0) {
+  // Each pair as one dword (funnel shift or packing per load path), then
+  // 8 channels transposed into the two 16-byte vectors of the pair.
+  auto write_path = [&](auto tag, u32x4_t* buf, int c0) __attribute__((always_inline)) {
+    constexpr int P = decltype(tag)::value;
 #pragma unroll
     for (int g = 0; g < G; ++g) {
       // channels past Nc were loaded as channel Nc-1: zero them
-      uint32_t keep[8];
+      uint32_t keep[8], par[8];
 #pragma unroll
-      for (int i = 0; i < 8; ++i) keep[i] = c0 + 8 * g + i < a.Nc ? ~0u : 0u;
+      for (int i = 0; i < 8; ++i) {
+        keep[i] = c0 + 8 * g + i < a.Nc ? ~0u : 0u;
+        par[i] = (uint32_t)(((int64_t)(c0 + 8 * g + i) * a.nxny) & 1);
+      }
 #pragma unroll
       for (int j = 0; j < MAXP; ++j) {
         if (pvalid[j]) {
+          uint32_t wd[8];
+#pragma unroll
+          for (int i = 0; i < 8; ++i) {
+            if constexpr (P == kFunnel && !PW) {
+              const uint32_t sh = (((voff[j] >> 1) + par[i]) & 1u) * 16u;
+              wd[i] = __builtin_amdgcn_alignbit(pre2[g][j][i], pre[g][j][i], sh);
+            } else if constexpr (P == kElement && !PW) {
+              wd[i] = pre[g][j][i] | (pre2[g][j][i] << 16);
+            } else {
+              wd[i] = pre[g][j][i];
+            }
+          }
           u32x4_t lo, hi;
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
-            const uint32_t e0 = pre[g][j][2 * i] & keep[2 * i];
-            const uint32_t e1 = pre[g][j][2 * i + 1] & keep[2 * i + 1];
+            const uint32_t e0 = wd[2 * i] & keep[2 * i];
+            const uint32_t e1 = wd[2 * i + 1] & keep[2 * i + 1];
             lo[i] = __builtin_amdgcn_perm(e1, e0, 0x05040100u);
             hi[i] = __builtin_amdgcn_perm(e1, e0, 0x07060302u);
           }
@@ -339,6 +359,14 @@ __global__ __launch_bounds__(256) void conv_igemm2(const bf16_t* __restrict__ In
         }
       }
     }
+  };
+  auto write_in = [&](u32x4_t* buf, int c0) __attribute__((always_inline)) {
+    if (PW || !ODDY)
+      write_path(std::integral_constant<int, kAligned>(), buf, c0);
+    else if (path == kFunnel)
+      write_path(std::integral_constant<int, kFunnel>(), buf, c0);
+    else
+      write_path(std::integral_constant<int, kElement>(), buf, c0);
   };
   const int n_cc = (a.Nc + TC - 1) / TC;
   // Raw Ker: LDS chunk slot v of a stage is feature k0 + v / RC chunk
@@ -424,7 +452,8 @@ __global__ __launch_bounds__(256) void conv_igemm2(const bf16_t* __restrict__ In
 #pragma unroll
       for (int j = 0; j < KSTEPS; ++j) {
         const int grp = 2 * j + half;
-        const bool gv = cc * TC + 8 * grp < a.Nc;  // whole group in range (Nc % 8 == 0)
+        // whole group in range (Nc % 8 == 0); masked, not branched on
+        const uint32_t gmask = cc * TC + 8 * grp < a.Nc ? ~0u : 0u;
         uint32_t raw[MB][RSD];
 #pragma unroll
         for (int mb = 0; mb < MB; ++mb) {
@@ -433,7 +462,7 @@ __global__ __launch_bounds__(256) void conv_igemm2(const bf16_t* __restrict__ In
           for (int q = 0; q < RS_C; ++q) {
             const u32x4_t v = src[q];
 #pragma unroll
-            for (int d = 0; d < 4; ++d) raw[mb][4 * q + d] = gv ? v[d] : 0u;
+            for (int d = 0; d < 4; ++d) raw[mb][4 * q + d] = v[d] & gmask;
           }
         }
 #pragma unroll
@@ -603,13 +632,15 @@ static hipError_t launch_one2(const void* In, const void* Ker, void* Out, void* 
                        (const bf16_t*)Ker, (u32x4_t*)ws, a, TK, TC, (int)blk, total);
     kp = ws;
   }
-  auto kern = conv_igemm2<TO, WM, WN, MB, NB, TC, NR, NS, MAXP, (RAWK != 0), (PW != 0)>;
-  static bool attr_set = false;
-  if (!attr_set) {
+  auto kern = (!PW && (a.Ny & 1))
+                  ? conv_igemm2<TO, WM, WN, MB, NB, TC, NR, NS, MAXP, (RAWK != 0), (PW != 0), true>
+                  : conv_igemm2<TO, WM, WN, MB, NB, TC, NR, NS, MAXP, (RAWK != 0), (PW != 0), false>;
+  static bool attr_set[2] = {false, false};
+  if (!attr_set[a.Ny & 1]) {
     hipError_t e = hipFuncSetAttribute((const void*)kern,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
     if (e != hipSuccess) return e;
-    attr_set = true;
+    attr_set[a.Ny & 1] = true;
   }
   hipLaunchKernelGGL(kern, dim3((unsigned)a.grid), dim3(256), (unsigned)lds, stream,
                      (const bf16_t*)In, (const u32x4_t*)kp, (TO*)Out, a, (int)blk);

@@ -166,31 +166,36 @@ __global__ __launch_bounds__(256) void conv_igemm3(const bf16_t* __restrict__ In
     for (int j = 0; j < NDK; ++j)
       dma16(ker_rsrc, kb + 256 * j + 64 * wave, (uint32_t)(256 * j + tid) * 16u, so_k);
   };
-  auto transpose = [&](int cc, int slot) {
+  // All of a thread's reads first (unconditional, straight-line), then its
+  // writes: reads and writes share the LDS array, so interleaving them -- or
+  // branching per element -- would serialize every read.  Channels past Nc
+  // are read anyway (in-range LDS) and masked to zero.
+  auto transpose = [&](int cc, int slot) __attribute__((always_inline)) {
     const uint16_t* nat = reinterpret_cast<const uint16_t*>(natbuf + slot * NAT);
     const int c0 = cc * TC;
+    uint32_t e[G][MPOS][8];
 #pragma unroll
     for (int g = 0; g < G; ++g) {
-      uint32_t cm[8];
-      bool cv[8];
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
         const int cl = 8 * g + i;  // channel within the stage (the DMA offsets' channel)
-        cv[i] = c0 + cl < a.Nc;
-        cm[i] = (uint32_t)(((int64_t)cl * a.nxny) & 7);
+        const uint32_t keep = c0 + cl < a.Nc ? 0xffffu : 0u;
+        const uint32_t cm = (uint32_t)(((int64_t)cl * a.nxny) & 7);
+#pragma unroll
+        for (int m = 0; m < MPOS; ++m) {
+          const int idx = cl * rb * 8 + t_base[m] + (int)((t_rs[m] + cm) & 7u);
+          e[g][m][i] = (uint32_t)nat[idx] & keep;
+        }
       }
+    }
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
 #pragma unroll
       for (int m = 0; m < MPOS; ++m) {
         if (t_ok[m]) {
-          uint32_t e[8];
-#pragma unroll
-          for (int i = 0; i < 8; ++i) {
-            const int idx = (8 * g + i) * rb * 8 + t_base[m] + (int)((t_rs[m] + cm[i]) & 7u);
-            e[i] = cv[i] ? (uint32_t)nat[idx] : 0u;
-          }
           u32x4_t v;
 #pragma unroll
-          for (int i = 0; i < 4; ++i) v[i] = e[2 * i] | (e[2 * i + 1] << 16);
+          for (int i = 0; i < 4; ++i) v[i] = e[g][m][2 * i] | (e[g][m][2 * i + 1] << 16);
           tbuf[g * SN + tid + 256 * m] = v;
         }
       }

@@ -90,6 +90,7 @@ def variant_dims(kernel, vid, dt, tk, tp, tc, stencil):
         cands = []
     cands += [(3, tc + 5, tk + 7, 9, 13, Nr, Ns, 1, 2), (2, tc + 5, tk + 7, 7, 13, Nr, Ns, 1, 1),
              (3, tc + 8, tk + 7, 9, 13, Nr, Ns, 1, 2), (2, tc + 8, tk + 7, 7, 13, Nr, Ns, 1, 1),
+             (3, tc + 8, max(1, tk - 5), 9, 13, Nr, Ns, 1, 2),
              (2, tc + 8, tk + 7, 4, 5, Nr, Ns, 2, 1), (2, tc + 8, tk + 7, 6, 8, Nr, Ns, 2, 2),
              (2, tc + 3, max(1, tk - 5), 5, 9, Nr, Ns, 1, 1), (1, tc + 5, tk + 3, 6, 7, Nr, Ns, 1, 1),
              (2, tc + 5, tk + 7, 4, 5, Nr, Ns, 2, 1), (1, tc + 5, tk + 7, 3, 4, Nr, Ns, 1, 1)]
@@ -117,6 +118,8 @@ def variant_cases():
         tk = 32 * wm * mb
         out.append((cnn.K_IGEMM_DMA, vid, dt, tk, 32 * wn * nb, tc,
                     (nr, ns) if nr else ((1, 1) if vid % 100 in (10, 11, 12) else (5, 2))))
+    for vid, dt, wm, wn, mb, nb, tc, nr, ns, kres in osel.STREAM:
+        out.append((cnn.K_STREAM, vid, dt, 32 * wm * mb, 32 * wn * nb, tc, (nr, ns)))
     for vid, dt, nb, ks in osel.SMALLC:
         out.append((cnn.K_SMALLC, vid, dt, 64, 128 * nb, 0, (7, 7) if ks <= 12 else (5, 5)))
     for vid, dt, wm, wn, mb, nb, tc, nr, ns, _, rawk, pw in osel.IGEMM2:

@@ -216,3 +216,34 @@ def test_pointwise_gather_exact(shape, tk, mode):
         assert np.array_equal(got, want)
     else:
         assert np.array_equal(got, oracle.widen(inputs.f32_to_bf16_bits(want.astype(np.float32))))
+
+
+@pytest.mark.parametrize("mode", ["bf16", "bf16_obf16"])
+@pytest.mark.parametrize("shape,tk,tp", [
+    ((4, 24, 60, 12, 14, 3, 3, 1, 1), 64, 256),    # resident Ker (Nk <= tk), even rows
+    ((3, 32, 50, 11, 9, 3, 3, 1, 1), 64, 256),     # resident Ker, odd rows (funnel / element)
+    ((4, 24, 150, 12, 14, 3, 3, 1, 1), 128, 128),  # streamed Ker, ragged k tiles
+    ((2, 40, 130, 9, 10, 3, 3, 2, 2), 128, 128),   # stride 2
+])
+@pytest.mark.parametrize("cus", [3, 7])
+def test_stream_multi_tile_exact(shape, tk, tp, cus, mode):
+    """The persistent kernel with few workgroup slots, so every workgroup
+    walks several tiles (next-tile prefetch, stores draining under the next
+    tile): bit-exact with the oracle on integer inputs."""
+    Nb, Nc, Nk, Nw, Nh, Nr, Ns, sw, sh = shape
+    pl = cnn.plan_tiles(cnn.problem(*shape), MODES[mode], cnn.K_STREAM, tk, tp, 16,
+                        cnn.budget(cus, 160 * 1024, 128, 2))
+    tiles = -(-(Nb * Nw * Nh) // pl.tp) * -(-Nk // pl.tk)
+    assert pl.grid < tiles  # several tiles per workgroup
+    rng = np.random.default_rng(sum(shape) + cus)
+    Nx, Ny = sw * (Nw - 1) + Nr, sh * (Nh - 1) + Ns
+    In = inputs.f32_to_bf16_bits(rng.integers(-2, 3, size=(Nb, Nc, Nx, Ny)).astype(np.float32))
+    Ker = inputs.f32_to_bf16_bits(rng.integers(-2, 3, size=(Nk, Nc, Nr, Ns)).astype(np.float32))
+    want = oracle.conv(In, Ker, sw, sh)
+    say(f"[parity] stream multi-tile shape={shape} v{pl.variant} tp={pl.tp} grid={pl.grid} "
+        f"tiles={tiles} mode={mode}")
+    got = run(In, Ker, sw, sh, mode, plan=pl)
+    if mode == "bf16":
+        assert np.array_equal(got, want)
+    else:
+        assert np.array_equal(got, oracle.widen(inputs.f32_to_bf16_bits(want.astype(np.float32))))
