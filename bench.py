@@ -69,10 +69,20 @@ def forced_plan(spec: str, w, mode: str):
     parts = spec.split(":")
     kern = KERNELS[parts[0]]
     tk, tp, tc = (int(x) for x in parts[1:4]) if len(parts) >= 4 else (0, 0, 0)
-    pl = cnn.plan_tiles(cnn.problem(*w.dims()), cnn.DTYPES[mode], kern, tk, tp, tc)
-    if len(parts) == 5 and pl.variant != int(parts[4]):
-        raise SystemExit(f"--plan {spec}: the tiling resolves to variant {pl.variant}")
-    return pl
+    prob = cnn.problem(*w.dims())
+    if len(parts) < 5:
+        return cnn.plan_tiles(prob, cnn.DTYPES[mode], kern, tk, tp, tc)
+    # with a variant, TP may be the plan's (balanced) tile: find the variant's
+    # largest tile among the instantiated sizes
+    want = int(parts[4])
+    for tp_max in [tp] + [32 * m for m in range(1, 17)]:
+        try:
+            pl = cnn.plan_tiles(prob, cnn.DTYPES[mode], kern, tk, tp_max, tc)
+        except cnn.CnnError:
+            continue
+        if pl.variant == want:
+            return pl
+    raise SystemExit(f"--plan {spec}: no tiling resolves to variant {want}")
 
 
 def copy_calibration(nbytes: int, steps: int):
