@@ -128,12 +128,17 @@ SMALLC = [
 ]
 
 
-# (id, dtype, wm, wn, mb, nb, tc, nr, ns, kres) of the persistent streaming
-# kernel: tk = 32*wm*mb, tp = 32*wn*nb, 64*wm*wn threads (one input pair
-# each); kres keeps all of Ker in LDS (Nk <= tk); grid = workgroup slots.
+# (id, dtype, wm, wn, mb, nb, tc, nr, ns, kres, mpos, ndma) of the persistent
+# streaming kernel: tk = 32*wm*mb, tp = 32*wn*nb, 64*wm*wn threads; kres
+# keeps all of Ker in LDS (Nk <= tk), packed as MFMA operands (tc/8 vectors
+# per tap and feature per stage), else two raw-row stages; the slab must fit mpos transposed
+# positions and ndma 16-byte natural-copy blocks per thread (rows copied as
+# ceil((Ny+14)/8) blocks); grid = workgroup slots.
 STREAM = [
-    (1300, BF16, 1, 8, 2, 1, 16, 3, 3, 1), (1310, BF16, 2, 4, 2, 1, 16, 3, 3, 0),
-    (1400, BF16_OBF16, 1, 8, 2, 1, 16, 3, 3, 1), (1410, BF16_OBF16, 2, 4, 2, 1, 16, 3, 3, 0),
+    (1300, BF16, 2, 4, 1, 2, 16, 3, 3, 1, 1, 2),
+    (1310, BF16, 2, 4, 2, 1, 16, 3, 3, 0, 2, 3),
+    (1400, BF16_OBF16, 2, 4, 1, 2, 16, 3, 3, 1, 1, 2),
+    (1410, BF16_OBF16, 2, 4, 2, 1, 16, 3, 3, 0, 2, 3),
 ]
 
 
@@ -257,7 +262,7 @@ def candidates(p: eq1.Problem, dtype: int, cus: int, lds_bytes: int, acc_regs: i
                 continue
             t, info = _cost(p, dtype, tk, tp, tc, lds, cus, lds_bytes, wg_per_cu)
             yield t, tk, tp, tc, vid, info
-        for vid, dt, wm, wn, mb, nb, tc, nr, ns, kres in STREAM:
+        for vid, dt, wm, wn, mb, nb, tc, nr, ns, kres, mpos, ndma in STREAM:
             if dt != dtype or (nr, ns) != (p.Nr, p.Ns) or p.Nc % 8:
                 continue
             tk, tp_max, acc, threads = 32 * wm * mb, 32 * wn * nb, 16 * mb * nb, 64 * wm * wn
@@ -270,15 +275,18 @@ def candidates(p: eq1.Problem, dtype: int, cus: int, lds_bytes: int, acc_regs: i
             kvecs = -(-(tk * rc) // 64) * 64
             n_cc = -(-p.Nc // tc)
 
+            nbr = (p.Ny + 14) // 8
+
+            ker_vecs = n_cc * RS * (tc // 8) * tk if kres else 2 * kvecs
+
             def lds_t(S):
-                sn = (S * p.Ny + 1) // 2 * 2 + 2
-                return (2 * (tc // 8) * sn + (n_cc if kres else 2) * kvecs) * 16
+                return (2 * threads * ndma + (tc // 8) * S * p.Ny + ker_vecs) * 16
 
             lds_full = lds_t(_max_slab(p, tp_max))
             slots = cus * max(1, min(wg_per_cu * 256 // threads, lds_bytes // lds_full))
             tp = balanced_tp(p, tp_max, tk, slots, 2)
             S = _max_slab(p, tp)
-            if -(-(S * p.Ny) // 2) > threads:
+            if S * p.Ny > threads * mpos or tc * S * nbr > threads * ndma:
                 continue
             lds = lds_t(S)
             if lds > lds_bytes or acc > acc_regs:

@@ -199,10 +199,9 @@ bool stream_geometry_ok(const VariantT& v, const cnn_plan_t& pl) {
   const cnn_problem& p = pl.prob;
   if (v.nr != p.Nr || v.ns != p.Ns || p.Nc % 8 != 0 || (v.kres && p.Nk > v.tk)) return false;
   if (pl.tp < 1 || pl.tp > v.tp) return false;
-  const int64_t Ny = p.sh * (p.Nh - 1) + p.Ns;
   const int64_t S = slab_rows_max(p, pl.tp);
   const int64_t tiles = ((p.Nb * p.Nw * p.Nh + pl.tp - 1) / pl.tp) * ((p.Nk + v.tk - 1) / v.tk);
-  return pl.slab_rows == S && (S * Ny + 1) / 2 <= v.threads && pl.grid >= 1 && pl.grid <= tiles &&
+  return pl.slab_rows == S && stream_fits(v, p, S) && pl.grid >= 1 && pl.grid <= tiles &&
          pl.lds_bytes == stream_lds_bytes(v, p, S) && pl.lds_bytes <= 160 * 1024;
 }
 

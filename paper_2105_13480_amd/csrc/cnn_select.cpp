@@ -248,8 +248,8 @@ static bool eval_smallc(const cnn_problem& p, int dtype, const VariantS& v, cons
 }
 
 // Persistent streaming kernel (conv_stream): fixed stencil, Nc % 8 == 0,
-// one input pair per thread, KRES needs one k tile; the grid is the
-// workgroup slots (each walks a range of tiles).
+// the slab within the per-thread copy and transpose counts, KRES needs one
+// k tile; the grid is the workgroup slots (each walks a range of tiles).
 static bool eval_stream(const cnn_problem& p, int dtype, const VariantT& v, const cnn_budget& bud,
                         cnn_plan_t* plan, double* time_clk) {
   if (v.nr != p.Nr || v.ns != p.Ns || p.Nc % 8 != 0) return false;
@@ -265,7 +265,7 @@ static bool eval_stream(const cnn_problem& p, int dtype, const VariantT& v, cons
   const int64_t slots = bud.cus * occ;
   const int64_t tp = balanced_tp(p, v.tp, v.tk, slots, 2);
   const int64_t S = slab_rows_max(p, tp);
-  if ((S * Ny + 1) / 2 > v.threads) return false;
+  if (!stream_fits(v, p, S)) return false;
   const int64_t lds = stream_lds_bytes(v, p, S);
   if (!eval_tiling(p, dtype, v.id, v.tk, tp, v.tc, v.acc, S, lds, 0, bud, plan, time_clk))
     return false;

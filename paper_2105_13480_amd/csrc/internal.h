@@ -122,9 +122,12 @@ struct VariantT {
   int32_t nr, ns;      // compile-time stencil
   int32_t threads;     // workgroup size
   int32_t kres;        // 1: the whole Ker stays in LDS (Nk <= tk)
+  int32_t mpos;        // transposed positions per thread: S*Ny <= threads*mpos
+  int32_t ndma;        // natural-copy blocks per thread: tc*S*ceil((Ny+14)/8) <= threads*ndma
 };
 const VariantT* variants_stream(int* count);
 int64_t stream_lds_bytes(const VariantT& v, const cnn_problem& p, int64_t slab_rows);
+bool stream_fits(const VariantT& v, const cnn_problem& p, int64_t slab_rows);
 hipError_t launch_stream(const VariantT& v, const void* In, const void* Ker, void* Out,
                          const ConvArgs& a, int64_t lds_bytes, hipStream_t stream);
 

@@ -118,7 +118,7 @@ def variant_cases():
         tk = 32 * wm * mb
         out.append((cnn.K_IGEMM_DMA, vid, dt, tk, 32 * wn * nb, tc,
                     (nr, ns) if nr else ((1, 1) if vid % 100 in (10, 11, 12) else (5, 2))))
-    for vid, dt, wm, wn, mb, nb, tc, nr, ns, kres in osel.STREAM:
+    for vid, dt, wm, wn, mb, nb, tc, nr, ns, kres, _, _ in osel.STREAM:
         out.append((cnn.K_STREAM, vid, dt, 32 * wm * mb, 32 * wn * nb, tc, (nr, ns)))
     for vid, dt, nb, ks in osel.SMALLC:
         out.append((cnn.K_SMALLC, vid, dt, 64, 128 * nb, 0, (7, 7) if ks <= 12 else (5, 5)))
