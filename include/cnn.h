@@ -98,10 +98,16 @@ typedef enum cnn_kernel {
   CNN_K_IGEMM_RAWK = 8,/* as CNN_K_IGEMM_PIPE for fixed 3x3 / 1x1 stencils, Nc % 8 == 0:
                          raw Ker rows copied by DMA, MFMA operands built in registers,
                          no repack and no workspace                                 */
-  CNN_K_STREAM = 9    /* persistent workgroups (grid = workgroup slots) walking tile
+  CNN_K_STREAM = 9,   /* persistent workgroups (grid = workgroup slots) walking tile
                          ranges as one pipeline: next tile's loads during the last
                          stage, Out stores drain under the next tile; raw Ker, kept
                          resident in LDS when it fits; fixed 3x3, Nc % 8 == 0     */
+  CNN_K_ROWS = 10     /* stride-1 row streaming, bf16: tiles are whole output rows
+                         of one image (tp = L*Nh, L dividing Nw) by 64 features;
+                         the Ker tile resident in LDS, input rows streamed through
+                         a ring of row buffers and read with transposing LDS
+                         reads; fixed 3x3 or 1x1, Nc % 8 == 0, Ny <= 64; tc of
+                         its plans is Nc                                          */
 } cnn_kernel;
 
 /*

@@ -142,6 +142,21 @@ STREAM = [
 ]
 
 
+# (id, dtype, nr, ns, mb, ncg) of the row-streaming kernel: tk = 64, stride
+# 1, input rows of at most 32*mb positions, Nc rounded up to 16 equal to
+# 16*ncg; a tile is L whole output rows of one image (tp = L*Nh, L | Nw).
+# (Its wave layout -- rows per wave -- does not enter the selection.)
+# Taken only when requested (not ranked by `choose`); where several fit,
+# the lowest id.
+ROWS = [
+    (1500, BF16, 3, 3, 1, 4), (1501, BF16, 3, 3, 1, 2), (1502, BF16, 3, 3, 2, 4),
+    (1503, BF16, 3, 3, 2, 2), (1504, BF16, 1, 1, 2, 4),
+    (1600, BF16_OBF16, 3, 3, 1, 4), (1601, BF16_OBF16, 3, 3, 1, 2),
+    (1602, BF16_OBF16, 3, 3, 2, 4), (1603, BF16_OBF16, 3, 3, 2, 2),
+    (1604, BF16_OBF16, 1, 1, 2, 4),
+]
+
+
 def stream_grid(p: eq1.Problem, tk: int, tp: int, threads: int, lds: int, cus: int,
                 lds_bytes: int, wg_per_cu: int) -> int:
     """Workgroups a streaming plan launches: its slots, at most its tiles."""

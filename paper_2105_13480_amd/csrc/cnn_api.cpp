@@ -205,6 +205,26 @@ bool stream_geometry_ok(const VariantT& v, const cnn_plan_t& pl) {
          pl.lds_bytes == stream_lds_bytes(v, p, S) && pl.lds_bytes <= 160 * 1024;
 }
 
+const VariantR* find_variant_r(int id) {
+  int n = 0;
+  const VariantR* vs = variants_rows(&n);
+  for (int i = 0; i < n; ++i)
+    if (vs[i].id == id) return &vs[i];
+  return nullptr;
+}
+
+// Geometry a row-streaming plan must carry: whole output rows of one image
+// per tile (the kernel derives its band from tp), its LDS size and grid.
+bool rows_geometry_ok(const VariantR& v, const cnn_plan_t& pl) {
+  const cnn_problem& p = pl.prob;
+  if (!rows_fits(v, p) || pl.tc != p.Nc || pl.tp < p.Nh || pl.tp % p.Nh) return false;
+  const int64_t L = pl.tp / p.Nh;
+  if (p.Nw % L) return false;
+  const int64_t grid = p.Nb * (p.Nw / L) * ((p.Nk + v.tk - 1) / v.tk);
+  return pl.slab_rows == L + p.Nr - 1 && pl.grid == grid &&
+         pl.lds_bytes == rows_lds_bytes(v, p) && pl.lds_bytes <= 160 * 1024;
+}
+
 const Variant4* find_variant4(int id) {
   int n = 0;
   const Variant4* vs = variants4(&n);
@@ -266,6 +286,11 @@ int run_plan(const void* In, const void* Ker, void* Out, const cnn_plan_t& pl, h
         !stream_geometry_ok(*vt, pl))
       return fail(CNN_E_PLAN, "plan names no matching kernel instantiation (variant %d)", pl.variant);
     e = launch_stream(*vt, In, Ker, Out, a, pl.lds_bytes, st);
+  } else if (pl.kernel == CNN_K_ROWS) {
+    const VariantR* vr = find_variant_r(pl.variant);
+    if (!vr || vr->dtype != pl.dtype || vr->tk != pl.tk || !rows_geometry_ok(*vr, pl))
+      return fail(CNN_E_PLAN, "plan names no matching kernel instantiation (variant %d)", pl.variant);
+    e = launch_rows(*vr, In, Ker, Out, a, pl.lds_bytes, st);
   } else if (pl.kernel == CNN_K_SMALLC) {
     const VariantS* vs = find_variant_s(pl.variant);
     if (!vs || vs->dtype != pl.dtype || vs->tk != pl.tk || !smallc_geometry_ok(*vs, pl))
@@ -373,7 +398,7 @@ int cnn_plan_tiles(const cnn_problem* prob, int dtype, int kernel, int64_t tk, i
   if (!prob || !plan) return fail(CNN_E_NULL, "prob and plan must be non-NULL");
   int st;
   if ((st = check_problem(*prob)) || (st = check_dtype(dtype))) return st;
-  if (kernel < CNN_K_AUTO || kernel > CNN_K_STREAM)
+  if (kernel < CNN_K_AUTO || kernel > CNN_K_ROWS)
     return fail(CNN_E_UNSUPPORTED, "unknown kernel %d", kernel);
   cnn_budget bud;
   if ((st = resolve_budget(budget, &bud))) return st;

@@ -273,6 +273,42 @@ static bool eval_stream(const cnn_problem& p, int dtype, const VariantT& v, cons
   return true;
 }
 
+// Row-streaming kernel (conv_rows): stride 1, fixed stencil, Nc % 8 == 0,
+// input rows of at most 32*mb positions; a tile is L whole output rows of
+// one image (L divides Nw, tp = L*Nh) by 64 features, all Nc channels.
+// L = 0 picks the band: the fewest rounds of groups of wr rows per
+// workgroup (one workgroup per CU), then the largest L (least halo).
+static bool eval_rows(const cnn_problem& p, int dtype, const VariantR& v, const cnn_budget& bud,
+                      int64_t L, cnn_plan_t* plan, double* time_clk) {
+  if (!rows_fits(v, p)) return false;
+  const int64_t Nx = p.Nw + p.Nr - 1, Ny = p.Nh + p.Ns - 1;
+  if (p.Nb * p.Nc * Nx * Ny * 2 >= (1LL << 31) || p.Nk * p.Nc * p.Nr * p.Ns * 2 >= (1LL << 31) ||
+      p.Nb * p.Nk * p.Nw * p.Nh * out_bytes(dtype) >= (1LL << 31))
+    return false;
+  const int64_t lds = rows_lds_bytes(v, p);
+  if (lds > std::min<int64_t>(bud.lds_bytes, 160 * 1024)) return false;
+  const int64_t nk = ceil_div(p.Nk, v.tk);
+  if (L == 0) {
+    int64_t best = -1;
+    for (int64_t l = 1; l <= p.Nw; ++l) {
+      if (p.Nw % l) continue;
+      const int64_t cost = ceil_div(p.Nb * (p.Nw / l) * nk, bud.cus) * ceil_div(l, v.wr);
+      if (best < 0 || cost <= best) {
+        best = cost;
+        L = l;
+      }
+    }
+  }
+  if (L < 1 || p.Nw % L) return false;
+  const int64_t tp = L * p.Nh;
+  // the accumulator budget is per lane at two waves per SIMD (8 per
+  // workgroup); a 4-wave workgroup (one wave per SIMD) has twice the registers
+  cnn_budget b2 = bud;
+  b2.acc_regs = bud.acc_regs * 8 / v.waves;
+  return eval_tiling(p, dtype, v.id, v.tk, tp, p.Nc, v.acc, L + p.Nr - 1, lds, 0, b2, plan,
+                     time_clk);
+}
+
 static void fill_common(const cnn_problem& p, int dtype, cnn_plan_t* plan) {
   const int64_t Nx = p.sw * (p.Nw - 1) + p.Nr, Ny = p.sh * (p.Nh - 1) + p.Ns;
   const double e_in = in_bytes(dtype), e_out = out_bytes(dtype);
@@ -313,7 +349,8 @@ int select_plan(const cnn_problem& p, int dtype, const cnn_budget& bud, int kern
   }
   if (kernel != CNN_K_AUTO && kernel != CNN_K_IGEMM && kernel != CNN_K_IGEMM_PIPE &&
       kernel != CNN_K_IGEMM_DMA && kernel != CNN_K_IGEMM_WIDE && kernel != CNN_K_IGEMM_RAWK &&
-      kernel != CNN_K_POINTWISE && kernel != CNN_K_SMALLC && kernel != CNN_K_STREAM)
+      kernel != CNN_K_POINTWISE && kernel != CNN_K_SMALLC && kernel != CNN_K_STREAM &&
+      kernel != CNN_K_ROWS)
     return CNN_E_UNSUPPORTED;
   bool found = false;
   double best_t = 0;
@@ -332,6 +369,22 @@ int select_plan(const cnn_problem& p, int dtype, const cnn_budget& bud, int kern
       found = true;
     }
   };
+  // The row-streaming kernel is taken only when asked for (a requested
+  // tiling or the plan search): tp = L*Nh whole rows, tc always Nc.
+  if (kernel == CNN_K_ROWS) {
+    int nr = 0;
+    const VariantR* vr = variants_rows(&nr);
+    for (int i = 0; i < nr; ++i) {
+      const VariantR& v = vr[i];
+      if (v.dtype != dtype || v.tk != tk || p.Nh < 1 || tp % p.Nh) continue;
+      cnn_plan_t cand;
+      double t;
+      if (eval_rows(p, dtype, v, bud, tp / p.Nh, &cand, &t)) {
+        cand.kernel = CNN_K_ROWS;
+        consider(cand, t);
+      }
+    }
+  }
   // Tier 1: the DMA-staged kernel, tier 2: the register-staged pipelined
   // kernel (both bf16), tier 3: the plain staging kernel.  The wide-staging
 // kernel competes within tier 1.
@@ -461,6 +514,15 @@ int enumerate_plans(const cnn_problem& p, int dtype, const cnn_budget& bud, cnn_
   for (int i = 0; i < nsc; ++i)
     if (vss[i].dtype == dtype && eval_smallc(p, dtype, vss[i], bud, &cand, &t))
       add(cand, CNN_K_SMALLC);
+  // row streaming: every band length L (dividing Nw) of 2 .. 4 groups' rows
+  int nrw = 0;
+  const VariantR* vrw = variants_rows(&nrw);
+  for (int i = 0; i < nrw; ++i) {
+    if (vrw[i].dtype != dtype) continue;
+    for (int64_t L = 2; L <= std::min<int64_t>(p.Nw, 4 * vrw[i].wr); ++L)
+      if (p.Nw % L == 0 && eval_rows(p, dtype, vrw[i], bud, L, &cand, &t))
+        add(cand, CNN_K_ROWS);
+  }
   const Variant* vs = variants(&n1);
   for (int i = 0; i < n1; ++i)
     if (vs[i].dtype == dtype && vs[i].kernel == CNN_K_IGEMM &&

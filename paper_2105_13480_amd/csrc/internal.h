@@ -131,6 +131,25 @@ bool stream_fits(const VariantT& v, const cnn_problem& p, int64_t slab_rows);
 hipError_t launch_stream(const VariantT& v, const void* In, const void* Ker, void* Out,
                          const ConvArgs& a, int64_t lds_bytes, hipStream_t stream);
 
+// A row-streaming instantiation (bf16, stride 1, fixed stencil): tk = 64,
+// tiles of whole output rows, Ker resident.
+struct VariantR {
+  int32_t id;
+  int32_t dtype;
+  int32_t tk;
+  int32_t nr, ns;  // compile-time stencil
+  int32_t wr;      // output rows per group
+  int32_t mb;      // 32-position blocks per input row: Ny <= 32*mb
+  int32_t waves;   // waves per workgroup (two per group of rows)
+  int32_t ncg;     // 16-channel groups: Nc rounded up to 16 is 16*ncg
+  int32_t acc;
+};
+const VariantR* variants_rows(int* count);
+int64_t rows_lds_bytes(const VariantR& v, const cnn_problem& p);
+bool rows_fits(const VariantR& v, const cnn_problem& p);
+hipError_t launch_rows(const VariantR& v, const void* In, const void* Ker, void* Out,
+                       const ConvArgs& a, int64_t lds_bytes, hipStream_t stream);
+
 // Ker repack for the pipelined kernels (defined with conv_igemm2).
 __global__ void pack_ker_bf16(const uint16_t* __restrict__ Ker, uint32_t __attribute__((ext_vector_type(4)))* __restrict__ P,
                               ConvArgs a, int TK, int TC, int blk_vecs, int64_t total_vecs);

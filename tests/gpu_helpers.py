@@ -82,6 +82,8 @@ def variant_dims(kernel, vid, dt, tk, tp, tc, stencil):
     picks for (kernel, tk, tp, tc): ragged channel, feature and output
     tails, several tiles.  None if no candidate fits."""
     Nr, Ns = stencil
+    if kernel == cnn.K_ROWS:
+        return rows_dims(vid, dt, stencil)
     if kernel == cnn.K_SMALLC:  # few channels: Nc*Nr rows must fit the K-steps
         nc = 3 if Nr == 7 else 9
         cands = [(3, nc, tk + 7, 9, 13, Nr, Ns, 2, 2), (2, nc, tk + 7, 7, 13, Nr, Ns, 1, 1),
@@ -104,6 +106,29 @@ def variant_dims(kernel, vid, dt, tk, tp, tc, stencil):
     return None
 
 
+def rows_dims(vid, dt, stencil):
+    """A stride-1 problem the row-streaming instantiation `vid` is chosen
+    for: two k tiles (ragged), a ragged channel tail, a band of several
+    row groups; the (tp = L*Nh) is returned as dims[-1] of the tuple."""
+    from oracle import select as osel
+    row = next(r for r in osel.ROWS if r[0] == vid)
+    _, _, nr, ns, mb, ncg = row
+    nc = 16 * ncg - 8                      # Nc % 8 == 0, last group half empty
+    nh = (29 if mb == 1 else 45) - (ns - 1) if ns > 1 else (30 if mb == 1 else 50)
+    for dims in [(2, nc, 71, 10, nh, nr, ns, 1, 1), (3, nc, 64, 6, nh + 1, nr, ns, 1, 1)]:
+        for L in (dims[3], 5, 2, 1):
+            if dims[3] % L:
+                continue
+            try:
+                pl = cnn.plan_tiles(cnn.problem(*dims), dt, cnn.K_ROWS, 64, L * dims[4], 0,
+                                    cnn.budget())
+            except cnn.CnnError:
+                continue
+            if pl.variant == vid:
+                return dims
+    return None
+
+
 def variant_cases():
     """(kernel, vid, dtype, tk, tp, tc, stencil) of every implicit-GEMM
     instantiation, from the oracle's independent tables."""
@@ -120,6 +145,8 @@ def variant_cases():
                     (nr, ns) if nr else ((1, 1) if vid % 100 in (10, 11, 12) else (5, 2))))
     for vid, dt, wm, wn, mb, nb, tc, nr, ns, kres, _, _ in osel.STREAM:
         out.append((cnn.K_STREAM, vid, dt, 32 * wm * mb, 32 * wn * nb, tc, (nr, ns)))
+    for vid, dt, nr, ns, mb, ncg in osel.ROWS:
+        out.append((cnn.K_ROWS, vid, dt, 64, 0, 0, (nr, ns)))
     for vid, dt, nb, ks in osel.SMALLC:
         out.append((cnn.K_SMALLC, vid, dt, 64, 128 * nb, 0, (7, 7) if ks <= 12 else (5, 5)))
     for vid, dt, wm, wn, mb, nb, tc, nr, ns, _, rawk, pw in osel.IGEMM2:

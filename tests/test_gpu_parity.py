@@ -247,3 +247,54 @@ def test_stream_multi_tile_exact(shape, tk, tp, cus, mode):
         assert np.array_equal(got, want)
     else:
         assert np.array_equal(got, oracle.widen(inputs.f32_to_bf16_bits(want.astype(np.float32))))
+
+
+# ---- row-streaming kernel: bands, row groups, store paths -----------------
+ROWS_SHAPES = [
+    (2, 56, 71, 10, 56, 3, 3, 1, 1),   # Ny = 58 (two 32-position blocks), 16-byte stores
+    (3, 64, 64, 9, 30, 3, 3, 1, 1),    # Ny = 32 exactly, Nh % 4 != 0: element stores
+    (2, 24, 40, 8, 62, 3, 3, 1, 1),    # Ny = 64 exactly, two channel groups, one k tile
+    (1, 32, 130, 12, 13, 3, 3, 1, 1),  # three k tiles, ragged
+    (2, 56, 70, 6, 50, 1, 1, 1, 1),    # 1x1
+]
+
+
+@pytest.mark.parametrize("mode", ["bf16", "bf16_obf16"])
+@pytest.mark.parametrize("shape", ROWS_SHAPES)
+def test_rows_bands_exact(shape, mode):
+    """Every band length L (dividing Nw): single partial group, several full
+    groups, a partial last group; bit-exact with the oracle on integers."""
+    Nb, Nc, Nk, Nw, Nh, Nr, Ns, sw, sh = shape
+    rng = np.random.default_rng(sum(shape))
+    Nx, Ny = Nw + Nr - 1, Nh + Ns - 1
+    In = inputs.f32_to_bf16_bits(rng.integers(-2, 3, size=(Nb, Nc, Nx, Ny)).astype(np.float32))
+    Ker = inputs.f32_to_bf16_bits(rng.integers(-2, 3, size=(Nk, Nc, Nr, Ns)).astype(np.float32))
+    want = oracle.conv(In, Ker, sw, sh)
+    if mode == "bf16_obf16":
+        want = oracle.widen(inputs.f32_to_bf16_bits(want.astype(np.float32)))
+    bands = [L for L in range(1, Nw + 1) if Nw % L == 0]
+    for L in bands:
+        pl = cnn.plan_tiles(cnn.problem(*shape), MODES[mode], cnn.K_ROWS, 64, L * Nh, 0)
+        say(f"[parity] rows shape={shape} L={L} v{pl.variant} grid={pl.grid} mode={mode}")
+        got = run(In, Ker, sw, sh, mode, plan=pl)
+        assert np.array_equal(got, want), f"band length {L}"
+
+
+def test_rows_float_headline_shape():
+    """The 56x56 3x3 layer on uniform inputs through the row kernel: sampled
+    outputs within the bf16 tolerance of the fp64 oracle."""
+    w = inputs.BY_NAME["conv3x3_b32"]
+    In, Ker = inputs.make_inputs(w)
+    pl = cnn.plan_tiles(cnn.problem(*w.dims()), cnn.CNN_BF16, cnn.K_ROWS, 64, 0, 0)
+    say(f"[parity] rows headline v{pl.variant} tp={pl.tp} grid={pl.grid}")
+    got = run(In, Ker, 1, 1, "bf16", plan=pl)
+    rng = np.random.default_rng(5)
+    idx = np.stack([rng.integers(0, m, size=4000) for m in (w.Nb, w.Nk, w.Nw, w.Nh)], axis=1)
+    # every band's first and last output row, first and last column
+    edge = [(b, k, y, h) for b in (0, w.Nb - 1) for k in (0, 31, 32, 63)
+            for y in range(w.Nw) for h in (0, w.Nh - 1)]
+    idx = np.unique(np.concatenate([idx, np.array(edge)]), axis=0)
+    want, absv = oracle.conv_points(In, Ker, idx, 1, 1, with_abs=True)
+    g = got[idx[:, 0], idx[:, 1], idx[:, 2], idx[:, 3]]
+    nw, cond, _ = errors(g, want, absv)
+    assert nw <= TOL["bf16"] and cond <= TOL["bf16"], (nw, cond)

@@ -1,5 +1,6 @@
-"""GPU parity at the full benchmark sizes, in the launch configuration the
-benchmark times (cnn_fwd with the automatic plan).
+"""GPU parity at the full benchmark sizes, in both launch configurations:
+cnn_fwd with the automatic plan, and the plan cnn_plan_find measures to be
+fastest (the one the benchmark times).
 
 The tiny workload is compared element by element.  For the large ones the
 oracle computes a sample of outputs one by one -- random points plus the
@@ -13,7 +14,7 @@ import pytest
 import oracle
 from paper_2105_13480_amd import cnn, inputs
 
-from gpu_helpers import TOL, errors, run, say
+from gpu_helpers import TOL, errors, out_tensor, run, say, to_gpu
 
 pytestmark = pytest.mark.gpu
 
@@ -46,18 +47,25 @@ def _checksum(In64, Ker64, w):
     return tot, tot_abs
 
 
+@pytest.mark.parametrize("plan_src", ["auto", "find"])
 @pytest.mark.parametrize("mode_out", ["fp32_out", "bf16_out"])
 @pytest.mark.parametrize("name", [w.name for w in inputs.WORKLOADS])
-def test_workload(name, mode_out):
+def test_workload(name, mode_out, plan_src):
     w = inputs.BY_NAME[name]
     if w.dtype == "f32" and mode_out == "bf16_out":
         pytest.skip("fp32 workload has fp32 output only")
     mode = "f32" if w.dtype == "f32" else ("bf16" if mode_out == "fp32_out" else "bf16_obf16")
     In, Ker = inputs.make_inputs(w)
-    plan = cnn.plan(cnn.problem(*w.dims()), cnn.DTYPES[mode])
-    say(f"[workload] {name} mode={mode} plan={plan.as_dict()['kernel']} v{plan.variant} "
-        f"tk={plan.tk} tp={plan.tp} tc={plan.tc} grid={plan.grid}")
-    got = run(In, Ker, w.sw, w.sh, mode)
+    if plan_src == "auto":
+        plan = cnn.plan(cnn.problem(*w.dims()), cnn.DTYPES[mode])
+    else:
+        dIn, dKer = to_gpu(In), to_gpu(Ker)
+        dOut = out_tensor(w.Nb, w.Nk, w.Nw, w.Nh, mode, 0.0)
+        plan, _ = cnn.plan_find(dIn, dKer, dOut, w.sw, w.sh)
+        del dIn, dKer, dOut
+    say(f"[workload] {name} mode={mode} {plan_src} plan={plan.as_dict()['kernel']} "
+        f"v{plan.variant} tk={plan.tk} tp={plan.tp} tc={plan.tc} grid={plan.grid}")
+    got = run(In, Ker, w.sw, w.sh, mode, plan=None if plan_src == "auto" else plan)
     assert got.shape == (w.Nb, w.Nk, w.Nw, w.Nh)
     assert np.isfinite(got).all()
     tol = TOL[mode]
