@@ -66,8 +66,10 @@ __device__ __forceinline__ void lds_barrier_r() {
 // pairs; the two waves of a pair take 32 features each and the same RPW
 // output rows, so a group is WR = RPW * WAVES/2 output rows.  MB:
 // 32-position blocks per row (Ny <= 32*MB).  NCG: 16-channel groups (Nc
-// rounded up to 16 is 16*NCG, the tail zero).
-template <typename TO, int NR, int NS, int WAVES, int RPW, int MB, int NCG>
+// rounded up to 16 is 16*NCG, the tail zero).  VEC (Nh % 4 == 0): a group's
+// Out rows are written as 16-byte (8-byte) chunks spread over the next
+// group's products; otherwise element by element at the end of the group.
+template <typename TO, int NR, int NS, int WAVES, int RPW, int MB, int NCG, bool VEC>
 __global__ __launch_bounds__(64 * WAVES) void conv_rows(const bf16_t* __restrict__ In,
                                                        const bf16_t* __restrict__ Ker,
                                                        TO* __restrict__ Out, ConvArgs a, int L,
@@ -234,16 +236,43 @@ __global__ __launch_bounds__(64 * WAVES) void conv_rows(const bf16_t* __restrict
 
   const int n = k0 + wk * 32 + l32;  // this lane's output feature
   const bool nv = n < a.Nk;
-  const bool vec_store = (a.Nh & 3) == 0;
 
   f32x16_t acc[RPW][NS][MB];
+
+  // VEC: the previous group's Out rows, pending: chunk c of row j holds
+  // positions 32*(c/4) + 8*(c%4) + 4*half .. +3 of feature n.  Every chunk is
+  // always issued (invalid ones at an offset past the range check, which
+  // drops them), so each group issues the same stores on every path.
+  constexpr int NCHUNK = 4 * MB;
+  constexpr int SOW = sizeof(TO) == 4 ? 16 : 8;  // pending words per block (fp32 or packed bf16)
+  uint32_t so[RPW][MB][SOW];
+  uint32_t s_orow[RPW];
+  bool s_on[RPW];
+#pragma unroll
+  for (int j = 0; j < RPW; ++j) s_on[j] = false;
+  auto store_chunk = [&](int j, int c) __attribute__((always_inline)) {
+    const int mb = c / 4, g = c % 4;
+    const int p0 = 32 * mb + 8 * g + 4 * half;
+    const uint32_t vo =
+        (s_on[j] && p0 < a.Nh) ? (s_orow[j] + p0) * (uint32_t)sizeof(TO) : 0x80000000u;
+    if constexpr (sizeof(TO) == 4) {
+      const u32x4_t v = {so[j][mb][4 * g], so[j][mb][4 * g + 1], so[j][mb][4 * g + 2],
+                         so[j][mb][4 * g + 3]};
+      __builtin_amdgcn_raw_buffer_store_b128(v, out_rsrc, vo, 0, 0);
+    } else {
+      const u32x2_t v = {so[j][mb][2 * g], so[j][mb][2 * g + 1]};
+      __builtin_amdgcn_raw_buffer_store_b64(v, out_rsrc, vo, 0, 0);
+    }
+  };
 
   for (int gi = 0; gi < n_groups; ++gi) {
 
     // this wave's first output row, relative to y0; rows past the band are
-    // computed from stale ring rows (in bounds) and not stored
+    // computed too (from stale ring rows, in bounds) and not stored: every
+    // wave runs the same straight-line code, so the waits count exactly (a
+    // wave without a row shares its SIMD with one that has a row)
     const int yrel = gi * WR + wp * RPW;
-    if (yrel < Lb) {  // wave-uniform
+    {
 #pragma unroll
       for (int j = 0; j < RPW; ++j)
 #pragma unroll
@@ -297,6 +326,8 @@ __global__ __launch_bounds__(64 * WAVES) void conv_rows(const bf16_t* __restrict
                   acc[j][s][mb], 0, 0, 0);
         }
       };
+      // (VEC: the previous group's chunks go out a few per step)
+      constexpr int CPS = (RPW * NCHUNK + NSTEP - 1) / NSTEP;
       u32x4_t A[2][MB], B[2][NR][NS];
       read_step(0, A[0], B[0]);
 #pragma unroll
@@ -304,6 +335,13 @@ __global__ __launch_bounds__(64 * WAVES) void conv_rows(const bf16_t* __restrict
         if (t + 1 < NSTEP) read_step(t + 1, A[(t + 1) & 1], B[(t + 1) & 1]);
         __builtin_amdgcn_sched_barrier(0);
         multiply_step(t, A[t & 1], B[t & 1]);
+        if constexpr (VEC) {
+#pragma unroll
+          for (int k = 0; k < CPS; ++k) {
+            const int c = t * CPS + k;
+            if (c < RPW * NCHUNK) store_chunk(c / NCHUNK, c % NCHUNK);
+          }
+        }
         __builtin_amdgcn_sched_barrier(0);
       }
     }
@@ -329,6 +367,7 @@ __global__ __launch_bounds__(64 * WAVES) void conv_rows(const bf16_t* __restrict
 
 #pragma unroll
     for (int j = 0; j < RPW; ++j) {
+      if constexpr (VEC) s_on[j] = false;
       if (yrel + j >= Lb) continue;  // wave-uniform
       // Out[h] = sum_s acc_s[h + s]; register 4g + i of block mb holds
       // position 32mb + 8g + 4*half + i.
@@ -347,17 +386,19 @@ __global__ __launch_bounds__(64 * WAVES) void conv_rows(const bf16_t* __restrict
             for (int i = 0; i + s < 4; ++i) o[mb][4 * g + i] += acc[j][s][mb][4 * g + i + s];
             // i + s >= 4: position 32mb + 8g + 4*half + i + s lies in the
             // partner half: half 0 takes register (mb, g, i') of lane l+32,
-            // half 1 takes register (next 8-group, i') of lane l-32.
+            // half 1 takes register (next 8-group, i') of lane l-32.  One
+            // v_permlane32_swap of (mine, next) moves mine's upper half to
+            // the lower lanes of its second result and next's lower half to
+            // the upper lanes of its first.
 #pragma unroll
             for (int ip = 0; ip < s; ++ip) {
               const int ng = g + 1 < 4 ? g + 1 : 0;
               const int nmb = g + 1 < 4 ? mb : mb + 1;
               const float mine = acc[j][s][mb][4 * g + ip];
               const float next = nmb < MB ? acc[j][s][nmb < MB ? nmb : 0][4 * ng + ip] : 0.f;
-              const float z = half ? mine : next;
-              const float w = __int_as_float(
-                  __builtin_amdgcn_ds_bpermute((lane ^ 32) << 2, __float_as_int(z)));
-              o[mb][4 * g + ip + 4 - s] += w;
+              const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mine),
+                                                               __float_as_uint(next), false, false);
+              o[mb][4 * g + ip + 4 - s] += __uint_as_float(half ? sw[0] : sw[1]);
             }
           }
         }
@@ -366,29 +407,28 @@ __global__ __launch_bounds__(64 * WAVES) void conv_rows(const bf16_t* __restrict
       const int y = y0 + yrel + j;
       const uint32_t orow =
           (uint32_t)((((int64_t)b * a.Nk + (nv ? n : 0)) * a.Nw + y) * a.Nh);  // elements
+      if constexpr (VEC) {
+        s_on[j] = nv;
+        s_orow[j] = orow;
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+          for (int w = 0; w < SOW; ++w) {
+            if constexpr (sizeof(TO) == 4)
+              so[j][mb][w] = __float_as_uint(o[mb][w]);
+            else
+              so[j][mb][w] = (uint32_t)from_f32<bf16_t>(o[mb][2 * w]) |
+                             ((uint32_t)from_f32<bf16_t>(o[mb][2 * w + 1]) << 16);
+          }
+        continue;  // written during the next group (or after the last)
+      }
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb) {
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
           if (32 * mb + 8 * g >= a.Nh) continue;  // wave-uniform
           const int p0 = 32 * mb + 8 * g + 4 * half;
-          if (vec_store) {
-            const uint32_t vo =
-                (nv && p0 < a.Nh) ? (orow + p0) * (uint32_t)sizeof(TO) : 0x80000000u;
-            if constexpr (sizeof(TO) == 4) {
-              const u32x4_t v = {__float_as_uint(o[mb][4 * g]), __float_as_uint(o[mb][4 * g + 1]),
-                                 __float_as_uint(o[mb][4 * g + 2]),
-                                 __float_as_uint(o[mb][4 * g + 3])};
-              __builtin_amdgcn_raw_buffer_store_b128(v, out_rsrc, vo, 0, 0);
-            } else {
-              const u32x2_t v = {
-                  (uint32_t)from_f32<bf16_t>(o[mb][4 * g]) |
-                      ((uint32_t)from_f32<bf16_t>(o[mb][4 * g + 1]) << 16),
-                  (uint32_t)from_f32<bf16_t>(o[mb][4 * g + 2]) |
-                      ((uint32_t)from_f32<bf16_t>(o[mb][4 * g + 3]) << 16)};
-              __builtin_amdgcn_raw_buffer_store_b64(v, out_rsrc, vo, 0, 0);
-            }
-          } else {
+          {
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
               const uint32_t vo =
@@ -405,6 +445,10 @@ __global__ __launch_bounds__(64 * WAVES) void conv_rows(const bf16_t* __restrict
       }
     }
     lds_barrier_r();  // next group's rows written; every wave done with this group's
+  }
+  if constexpr (VEC) {
+#pragma unroll
+    for (int c = 0; c < RPW * NCHUNK; ++c) store_chunk(c / NCHUNK, c % NCHUNK);
   }
 }
 
@@ -455,12 +499,17 @@ template <int DT, int NR, int NS, int WAVES, int RPW, int MB, int NCG>
 static hipError_t launch_r(const void* In, const void* Ker, void* Out, const ConvArgs& a,
                            int64_t lds, hipStream_t stream) {
   typedef typename std::conditional<DT == CNN_BF16, float, bf16_t>::type TO;
-  auto kern = conv_rows<TO, NR, NS, WAVES, RPW, MB, NCG>;
+  // 16-byte Out chunks need rows of a multiple of 4 outputs
+  auto kern = (a.Nh & 3) == 0 ? conv_rows<TO, NR, NS, WAVES, RPW, MB, NCG, true>
+                              : conv_rows<TO, NR, NS, WAVES, RPW, MB, NCG, false>;
   static bool attr_set = false;
   if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute((const void*)kern,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
-    if (e != hipSuccess) return e;
+    for (auto k : {conv_rows<TO, NR, NS, WAVES, RPW, MB, NCG, true>,
+                   conv_rows<TO, NR, NS, WAVES, RPW, MB, NCG, false>}) {
+      hipError_t e = hipFuncSetAttribute((const void*)k,
+                                         hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+      if (e != hipSuccess) return e;
+    }
     attr_set = true;
   }
   const int L = a.tp / a.Nh;

@@ -253,9 +253,13 @@ def test_stream_multi_tile_exact(shape, tk, tp, cus, mode):
 ROWS_SHAPES = [
     (2, 56, 71, 10, 56, 3, 3, 1, 1),   # Ny = 58 (two 32-position blocks), 16-byte stores
     (3, 64, 64, 9, 30, 3, 3, 1, 1),    # Ny = 32 exactly, Nh % 4 != 0: element stores
+    (3, 64, 64, 9, 28, 3, 3, 1, 1),    # one 32-position block, 16-byte stores
     (2, 24, 40, 8, 62, 3, 3, 1, 1),    # Ny = 64 exactly, two channel groups, one k tile
+    (2, 24, 40, 12, 44, 3, 3, 1, 1),   # two channel groups, 16-byte stores
     (1, 32, 130, 12, 13, 3, 3, 1, 1),  # three k tiles, ragged
+    (1, 32, 130, 12, 12, 3, 3, 1, 1),  # three k tiles, 16-byte stores
     (2, 56, 70, 6, 50, 1, 1, 1, 1),    # 1x1
+    (2, 56, 70, 6, 48, 1, 1, 1, 1),    # 1x1, 16-byte stores
 ]
 
 
