@@ -141,17 +141,28 @@ __global__ __launch_bounds__(64 * WAVES) void conv_rows(const bf16_t* __restrict
     return __builtin_bit_cast(
         u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(in_rsrc, (uint32_t)(e * 2), 0, 0));
   };
-  auto store_block = [&](int xa, int f, u32x4_t v, int fix) __attribute__((always_inline)) {
+  // Write a block to its ring slot: zeroing a channel past Nc is a mask;
+  // the last-element patch is rare (one block of the whole tensor), so it
+  // rewrites the block behind a branch.
+  auto put_block = [&](u32x4_t* dst, u32x4_t v, int fix) __attribute__((always_inline)) {
+    const uint32_t keep = fix == -2 ? 0u : ~0u;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const uint32_t lo = fix == 2 * i ? ((v[i] & 0xffff0000u) | in_last) : v[i];
-      const uint32_t w = fix == 2 * i + 1 ? ((lo & 0xffffu) | (in_last << 16)) : lo;
-      v[i] = fix == -2 ? 0u : w;
+    for (int i = 0; i < 4; ++i) v[i] &= keep;
+    *dst = v;
+    if (fix >= 0) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const uint32_t lo = fix == 2 * i ? ((v[i] & 0xffff0000u) | in_last) : v[i];
+        v[i] = fix == 2 * i + 1 ? ((lo & 0xffffu) | (in_last << 16)) : lo;
+      }
+      *dst = v;
     }
+  };
+  auto store_block = [&](int xa, int f, u32x4_t v, int fix) __attribute__((always_inline)) {
     const int rr = f / row_blocks;
     const int rem = f - rr * row_blocks;
     const int slot = (xa + rr - y0) % NRING;
-    reinterpret_cast<u32x4_t*>(rows + slot * row_elems)[rem] = v;
+    put_block(reinterpret_cast<u32x4_t*>(rows + slot * row_elems) + rem, v, fix);
   };
 
   // Rows group gi adds beyond group gi-1's: [new_lo(gi), new_lo(gi) + new_n(gi)).
