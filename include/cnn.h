@@ -102,12 +102,16 @@ typedef enum cnn_kernel {
                          ranges as one pipeline: next tile's loads during the last
                          stage, Out stores drain under the next tile; raw Ker, kept
                          resident in LDS when it fits; fixed 3x3, Nc % 8 == 0     */
-  CNN_K_ROWS = 10     /* stride-1 row streaming, bf16: tiles are whole output rows
+  CNN_K_ROWS = 10,    /* stride-1 row streaming, bf16: tiles are whole output rows
                          of one image (tp = L*Nh, L dividing Nw) by 64 features;
                          the Ker tile resident in LDS, input rows streamed through
                          a ring of row buffers and read with transposing LDS
                          reads; fixed 3x3 or 1x1, Nc % 8 == 0, Ny <= 64; tc of
                          its plans is Nc                                          */
+  CNN_K_GEMM1 = 11    /* 1x1 stride-1 layers as a per-pixel GEMM, bf16: In channel
+                         rows read by transposing LDS reads, Ker rows as they lie,
+                         both double-buffered in LDS; Nc % 8 == 0, Nw*Nh and tp
+                         multiples of 4                                           */
 } cnn_kernel;
 
 /*

@@ -157,6 +157,15 @@ ROWS = [
 ]
 
 
+# (id, dtype, wp, wk, mbp, nbk, tc) of the 1x1 stride-1 GEMM kernel: tk =
+# 32*wk*nbk, tp <= 32*wp*mbp (a multiple of 4, as are Nw*Nh), Nc % 8 == 0.
+# Taken only when requested (not ranked by `choose`).
+GEMM1 = [
+    (1700, BF16, 2, 4, 4, 2, 64), (1701, BF16, 4, 2, 2, 2, 64),
+    (1800, BF16_OBF16, 2, 4, 4, 2, 64), (1801, BF16_OBF16, 4, 2, 2, 2, 64),
+]
+
+
 def stream_grid(p: eq1.Problem, tk: int, tp: int, threads: int, lds: int, cus: int,
                 lds_bytes: int, wg_per_cu: int) -> int:
     """Workgroups a streaming plan launches: its slots, at most its tiles."""

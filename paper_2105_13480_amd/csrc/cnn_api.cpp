@@ -225,6 +225,23 @@ bool rows_geometry_ok(const VariantR& v, const cnn_plan_t& pl) {
          pl.lds_bytes == rows_lds_bytes(v, p) && pl.lds_bytes <= 160 * 1024;
 }
 
+const VariantG* find_variant_g(int id) {
+  int n = 0;
+  const VariantG* vs = variants_gemm1(&n);
+  for (int i = 0; i < n; ++i)
+    if (vs[i].id == id) return &vs[i];
+  return nullptr;
+}
+
+// Geometry a 1x1 GEMM plan must carry: its tile within the instantiation's,
+// the grid its tiles imply, its LDS size.
+bool gemm1_geometry_ok(const VariantG& v, const cnn_plan_t& pl) {
+  const cnn_problem& p = pl.prob;
+  if (pl.tp < 1 || pl.tp > v.tp || !gemm1_fits(v, p, pl.tp)) return false;
+  const int64_t grid = ((p.Nb * p.Nw * p.Nh + pl.tp - 1) / pl.tp) * ((p.Nk + v.tk - 1) / v.tk);
+  return pl.grid == grid && pl.lds_bytes == gemm1_lds_bytes(v) && pl.lds_bytes <= 160 * 1024;
+}
+
 const Variant4* find_variant4(int id) {
   int n = 0;
   const Variant4* vs = variants4(&n);
@@ -286,6 +303,12 @@ int run_plan(const void* In, const void* Ker, void* Out, const cnn_plan_t& pl, h
         !stream_geometry_ok(*vt, pl))
       return fail(CNN_E_PLAN, "plan names no matching kernel instantiation (variant %d)", pl.variant);
     e = launch_stream(*vt, In, Ker, Out, a, pl.lds_bytes, st);
+  } else if (pl.kernel == CNN_K_GEMM1) {
+    const VariantG* vg = find_variant_g(pl.variant);
+    if (!vg || vg->dtype != pl.dtype || vg->tk != pl.tk || vg->tc != pl.tc ||
+        !gemm1_geometry_ok(*vg, pl))
+      return fail(CNN_E_PLAN, "plan names no matching kernel instantiation (variant %d)", pl.variant);
+    e = launch_gemm1(*vg, In, Ker, Out, a, pl.lds_bytes, st);
   } else if (pl.kernel == CNN_K_ROWS) {
     const VariantR* vr = find_variant_r(pl.variant);
     if (!vr || vr->dtype != pl.dtype || vr->tk != pl.tk || !rows_geometry_ok(*vr, pl))
@@ -398,7 +421,7 @@ int cnn_plan_tiles(const cnn_problem* prob, int dtype, int kernel, int64_t tk, i
   if (!prob || !plan) return fail(CNN_E_NULL, "prob and plan must be non-NULL");
   int st;
   if ((st = check_problem(*prob)) || (st = check_dtype(dtype))) return st;
-  if (kernel < CNN_K_AUTO || kernel > CNN_K_ROWS)
+  if (kernel < CNN_K_AUTO || kernel > CNN_K_GEMM1)
     return fail(CNN_E_UNSUPPORTED, "unknown kernel %d", kernel);
   cnn_budget bud;
   if ((st = resolve_budget(budget, &bud))) return st;

@@ -309,6 +309,22 @@ static bool eval_rows(const cnn_problem& p, int dtype, const VariantR& v, const 
                      time_clk);
 }
 
+// 1x1 stride-1 GEMM kernel (conv_gemm1): tiles of tp consecutive pixels
+// (a multiple of 4, balanced over the CUs) by tk features.
+static bool eval_gemm1(const cnn_problem& p, int dtype, const VariantG& v, const cnn_budget& bud,
+                       cnn_plan_t* plan, double* time_clk) {
+  const int64_t lds = gemm1_lds_bytes(v);
+  if (lds > std::min<int64_t>(bud.lds_bytes, 160 * 1024)) return false;
+  if (p.Nb * p.Nc * p.Nw * p.Nh * 2 >= (1LL << 30) || p.Nk * p.Nc * 2 >= (1LL << 30) ||
+      p.Nb * p.Nk * p.Nw * p.Nh * out_bytes(dtype) >= (1LL << 31))
+    return false;
+  const int64_t occ = std::max<int64_t>(1, std::min<int64_t>(bud.wg_per_cu, bud.lds_bytes / lds));
+  int64_t tp = balanced_tp(p, v.tp, v.tk, bud.cus * occ, 1);
+  tp = std::min<int64_t>(v.tp, (tp + 3) / 4 * 4);
+  if (!gemm1_fits(v, p, tp)) return false;
+  return eval_tiling(p, dtype, v.id, v.tk, tp, v.tc, v.acc, 1, lds, 0, bud, plan, time_clk);
+}
+
 static void fill_common(const cnn_problem& p, int dtype, cnn_plan_t* plan) {
   const int64_t Nx = p.sw * (p.Nw - 1) + p.Nr, Ny = p.sh * (p.Nh - 1) + p.Ns;
   const double e_in = in_bytes(dtype), e_out = out_bytes(dtype);
@@ -350,7 +366,7 @@ int select_plan(const cnn_problem& p, int dtype, const cnn_budget& bud, int kern
   if (kernel != CNN_K_AUTO && kernel != CNN_K_IGEMM && kernel != CNN_K_IGEMM_PIPE &&
       kernel != CNN_K_IGEMM_DMA && kernel != CNN_K_IGEMM_WIDE && kernel != CNN_K_IGEMM_RAWK &&
       kernel != CNN_K_POINTWISE && kernel != CNN_K_SMALLC && kernel != CNN_K_STREAM &&
-      kernel != CNN_K_ROWS)
+      kernel != CNN_K_ROWS && kernel != CNN_K_GEMM1)
     return CNN_E_UNSUPPORTED;
   bool found = false;
   double best_t = 0;
@@ -381,6 +397,21 @@ int select_plan(const cnn_problem& p, int dtype, const cnn_budget& bud, int kern
       double t;
       if (eval_rows(p, dtype, v, bud, tp / p.Nh, &cand, &t)) {
         cand.kernel = CNN_K_ROWS;
+        consider(cand, t);
+      }
+    }
+  }
+  // The 1x1 GEMM kernel likewise: only when asked for (tp: its largest tile).
+  if (kernel == CNN_K_GEMM1) {
+    int ng = 0;
+    const VariantG* vg = variants_gemm1(&ng);
+    for (int i = 0; i < ng; ++i) {
+      const VariantG& v = vg[i];
+      if (v.dtype != dtype || v.tk != tk || v.tp != tp || v.tc != tc) continue;
+      cnn_plan_t cand;
+      double t;
+      if (eval_gemm1(p, dtype, v, bud, &cand, &t)) {
+        cand.kernel = CNN_K_GEMM1;
         consider(cand, t);
       }
     }
@@ -514,6 +545,11 @@ int enumerate_plans(const cnn_problem& p, int dtype, const cnn_budget& bud, cnn_
   for (int i = 0; i < nsc; ++i)
     if (vss[i].dtype == dtype && eval_smallc(p, dtype, vss[i], bud, &cand, &t))
       add(cand, CNN_K_SMALLC);
+  int ngm = 0;
+  const VariantG* vgm = variants_gemm1(&ngm);
+  for (int i = 0; i < ngm; ++i)
+    if (vgm[i].dtype == dtype && eval_gemm1(p, dtype, vgm[i], bud, &cand, &t))
+      add(cand, CNN_K_GEMM1);
   // row streaming: every band length L (dividing Nw) of 2 .. 4 groups' rows
   int nrw = 0;
   const VariantR* vrw = variants_rows(&nrw);

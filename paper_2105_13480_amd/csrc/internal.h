@@ -150,6 +150,21 @@ bool rows_fits(const VariantR& v, const cnn_problem& p);
 hipError_t launch_rows(const VariantR& v, const void* In, const void* Ker, void* Out,
                        const ConvArgs& a, int64_t lds_bytes, hipStream_t stream);
 
+// A 1x1 stride-1 GEMM instantiation (bf16): tk features x up to tp pixels,
+// tc channels per stage.
+struct VariantG {
+  int32_t id;
+  int32_t dtype;
+  int32_t tk, tp, tc;  // tp = largest tile
+  int32_t threads;
+  int32_t acc;
+};
+const VariantG* variants_gemm1(int* count);
+int64_t gemm1_lds_bytes(const VariantG& v);
+bool gemm1_fits(const VariantG& v, const cnn_problem& p, int64_t tp);
+hipError_t launch_gemm1(const VariantG& v, const void* In, const void* Ker, void* Out,
+                        const ConvArgs& a, int64_t lds_bytes, hipStream_t stream);
+
 // Ker repack for the pipelined kernels (defined with conv_igemm2).
 __global__ void pack_ker_bf16(const uint16_t* __restrict__ Ker, uint32_t __attribute__((ext_vector_type(4)))* __restrict__ P,
                               ConvArgs a, int TK, int TC, int blk_vecs, int64_t total_vecs);

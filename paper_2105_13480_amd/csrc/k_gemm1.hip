@@ -1,0 +1,323 @@
+// 1x1, stride-1 convolution as a per-pixel GEMM (bf16 MFMA, gfx950).
+//
+// With Nr = Ns = 1 and unit strides, In[b][c][w][h] and Out[b][k][w][h]
+// share the flattened pixel index p = (b, w, h): Out[k][p] = sum_c Ker[k][c]
+// * In[c][p] (Eq. (1) with Nr = Ns = 1: no halo).  A workgroup owns a tile of
+// tp consecutive pixels by tk output features and walks the input features
+// tc at a time (Listing 3 with W_c = N_c):
+//
+// * In: per stage, the tile's tc channel rows [c][p] in their natural layout,
+//   4 pixels (8 bytes) per load, so a load never crosses an image (Nh*Nw and
+//   the tile start are multiples of 4).  The MFMA A operand (pixels x 8
+//   channels) is read straight from those rows by the transposing LDS read
+//   (ds_read_b64_tr_b16): no transpose pass.
+// * Ker: per stage, the tk rows [k][c] of tc channels, 16-byte loads; a row
+//   segment is the MFMA B operand as it lies (8 consecutive channels).
+// * Both are double-buffered in LDS: the next stage's loads are in flight
+//   (in registers) while the current stage is multiplied.
+// * D[pixel][feature]: each lane ends with 4 consecutive pixels of one
+//   feature, written as one 16-byte (fp32) or 8-byte (bf16) store.
+#include <type_traits>
+
+#include "internal.h"
+#include "common.h"
+
+namespace cnnlib {
+
+namespace {
+
+typedef short s16x4_g __attribute__((ext_vector_type(4)));
+#define LDS_PTR_G(T, p) ((__attribute__((address_space(3))) T*)(p))
+
+__device__ __forceinline__ u32x2_t read_tr16_g(const bf16_t* p) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  return __builtin_bit_cast(
+      u32x2_t, __builtin_amdgcn_ds_read_tr16_b64_v4i16(LDS_PTR_G(s16x4_g, const_cast<bf16_t*>(p))));
+#else
+  (void)p;
+  return u32x2_t{0u, 0u};
+#endif
+}
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc_g(const void* base, int64_t bytes) {
+  bytes = (bytes + 3) & ~(int64_t)3;
+  const int32_t n = bytes > 0x7ffffffcLL ? 0x7ffffffc : (int32_t)bytes;
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, n, 0x00020000);
+}
+
+// Wait for this wave's LDS operations, then s_barrier; outstanding global
+// loads and stores are not waited for.
+__device__ __forceinline__ void lds_barrier_g() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+}  // namespace
+
+// TO: Out element type.  WP x WK waves: WP pixel groups of MBP 32-pixel
+// blocks, WK feature groups of NBK 32-feature blocks.  TC: channels per stage.
+template <typename TO, int WP, int WK, int MBP, int NBK, int TC>
+__global__ __launch_bounds__(64 * WP * WK) void conv_gemm1(const bf16_t* __restrict__ In,
+                                                          const bf16_t* __restrict__ Ker,
+                                                          TO* __restrict__ Out, ConvArgs a) {
+  constexpr int NT = 64 * WP * WK;
+  constexpr int TPMAX = 32 * WP * MBP;   // pixels per tile (at most)
+  constexpr int TK = 32 * WK * NBK;      // features per tile
+  constexpr int RSI = TPMAX + 16;        // LDS In row (pixels): +32 bytes, distinct banks per channel
+  constexpr int RSK = TC + 8;            // LDS Ker row (channels): +16 bytes, conflict-free B reads
+  constexpr int IN_ELEMS = TC * RSI;
+  constexpr int KER_ELEMS = TK * RSK;
+  constexpr int NQ = TPMAX / 4;          // 4-pixel chunks per channel row
+  constexpr int NIN = (TC * NQ + NT - 1) / NT;          // In chunks per thread per stage
+  constexpr int NKER = (TK * (TC / 8) + NT - 1) / NT;   // Ker blocks per thread per stage
+  constexpr int KSTEPS = TC / 16;
+  static_assert(TC % 16 == 0, "whole K-steps");
+
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  bf16_t* in_lds = reinterpret_cast<bf16_t*>(smem);            // [2][TC][RSI]
+  bf16_t* ker_lds = in_lds + 2 * IN_ELEMS;                      // [2][TK][RSK]
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int wp = wave / WK, wk = wave % WK;
+  const int l32 = lane & 31, half = lane >> 5;
+
+  const int tile = xcd_remap(blockIdx.x, gridDim.x);
+  const int pt = tile / a.n_ktiles;
+  const int kt = tile - pt * a.n_ktiles;
+  const int p0 = pt * a.tp;
+  const int tp = min(a.tp, a.npix - p0);  // pixels of this tile (a multiple of 4)
+  const int k0 = kt * TK;
+  const int n_st = (a.Nc + TC - 1) / TC;
+
+  const __amdgpu_buffer_rsrc_t in_rsrc = rsrc_g(In, a.in_total * 2);
+  const __amdgpu_buffer_rsrc_t ker_rsrc = rsrc_g(Ker, (int64_t)a.Nk * a.Nc * 2);
+  const __amdgpu_buffer_rsrc_t out_rsrc = rsrc_g(Out, a.out_total * (int64_t)sizeof(TO));
+
+  // Per-thread load slots (fixed over the stages): In chunk f = (channel
+  // f / NQ, pixels 4*(f % NQ) .. +3); Ker block g = (feature g / (TC/8),
+  // channels 8*(g % (TC/8)) .. +7).  Invalid slots load nothing useful and
+  // write zeros (a mask), so every load is issued and every wait is exact.
+  int in_off[NIN];        // element offset of the chunk's pixel, channel 0
+  int in_c[NIN];          // channel within the stage
+  uint32_t in_ok[NIN];    // ~0 if the chunk's pixels are in the tile
+  int in_dst[NIN];
+#pragma unroll
+  for (int j = 0; j < NIN; ++j) {
+    const int f = min(tid + NT * j, TC * NQ - 1);
+    const int c = f / NQ, q = f % NQ;
+    const int p = p0 + 4 * q;
+    const bool ok = tid + NT * j < TC * NQ && 4 * q < tp;
+    const int pc = ok ? p : p0;
+    const int b = pc / a.hw;
+    in_off[j] = b * (int)a.in_img + (pc - b * a.hw);  // < in_total < 2^30
+    in_c[j] = c;
+    in_ok[j] = ok ? ~0u : 0u;
+    in_dst[j] = c * RSI + 4 * q;
+  }
+  int ker_off[NKER];
+  int ker_c[NKER];
+  bool ker_ok[NKER];
+  int ker_dst[NKER];
+#pragma unroll
+  for (int j = 0; j < NKER; ++j) {
+    const int g = min(tid + NT * j, TK * (TC / 8) - 1);
+    const int n = g / (TC / 8), cb = g % (TC / 8);
+    ker_ok[j] = tid + NT * j < TK * (TC / 8) && k0 + n < a.Nk;
+    ker_off[j] = (k0 + n) * a.Nc + 8 * cb;  // (features past Nk masked)
+    ker_c[j] = 8 * cb;
+    ker_dst[j] = n * RSK + 8 * cb;
+  }
+
+  u32x2_t vin[NIN];
+  u32x4_t vker[NKER];
+  auto load_stage = [&](int s) __attribute__((always_inline)) {
+    const int c0 = s * TC;
+#pragma unroll
+    for (int j = 0; j < NIN; ++j) {
+      const int c = min(c0 + in_c[j], a.Nc - 1);
+      vin[j] = __builtin_bit_cast(
+          u32x2_t, __builtin_amdgcn_raw_buffer_load_b64(
+                       in_rsrc, (uint32_t)((in_off[j] + c * a.hw) * 2), 0, 0));
+    }
+#pragma unroll
+    for (int j = 0; j < NKER; ++j) {
+      const int c = min(c0 + ker_c[j], a.Nc - 8);
+      vker[j] = __builtin_bit_cast(
+          u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(
+                       ker_rsrc, (uint32_t)((ker_off[j] - ker_c[j] + c) * 2), 0, 0));
+    }
+  };
+  auto write_stage = [&](int s, int buf) __attribute__((always_inline)) {
+    const int c0 = s * TC;
+    bf16_t* ib = in_lds + buf * IN_ELEMS;
+    bf16_t* kb = ker_lds + buf * KER_ELEMS;
+#pragma unroll
+    for (int j = 0; j < NIN; ++j) {
+      const uint32_t keep = (c0 + in_c[j] < a.Nc) ? in_ok[j] : 0u;
+      if (tid + NT * j < TC * NQ)
+        *reinterpret_cast<u32x2_t*>(ib + in_dst[j]) = u32x2_t{vin[j][0] & keep, vin[j][1] & keep};
+    }
+#pragma unroll
+    for (int j = 0; j < NKER; ++j) {
+      const uint32_t keep = (ker_ok[j] && c0 + ker_c[j] < a.Nc) ? ~0u : 0u;
+      if (tid + NT * j < TK * (TC / 8))
+        *reinterpret_cast<u32x4_t*>(kb + ker_dst[j]) =
+            u32x4_t{vker[j][0] & keep, vker[j][1] & keep, vker[j][2] & keep, vker[j][3] & keep};
+    }
+  };
+
+  // A operand lane offsets (transposing read, as in the row kernel): lane i
+  // of 16-lane group G supplies channel 8*(G/2) + i/4 (+4 for the second
+  // read), pixels 16*(G%2) + 4*(i%4) of the 32-pixel block.
+  const int G = lane >> 4, li = lane & 15;
+  const int aoff0 = (8 * (G >> 1) + (li >> 2)) * RSI + 16 * (G & 1) + 4 * (li & 3) +
+                    32 * (wp * MBP);
+  const int aoff1 = aoff0 + 4 * RSI;
+  const int boff = (wk * NBK * 32 + l32) * RSK + 8 * half;
+
+  f32x16_t acc[MBP][NBK];
+#pragma unroll
+  for (int mb = 0; mb < MBP; ++mb)
+#pragma unroll
+    for (int nb = 0; nb < NBK; ++nb)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[mb][nb][e] = 0.f;
+
+  load_stage(0);
+  write_stage(0, 0);
+  lds_barrier_g();
+  for (int s = 0; s < n_st; ++s) {
+    const int buf = s & 1;
+    if (s + 1 < n_st) load_stage(s + 1);
+    const bf16_t* ib = in_lds + buf * IN_ELEMS;
+    const bf16_t* kb = ker_lds + buf * KER_ELEMS;
+    // K-steps of 16 channels, operands one step ahead
+    auto read_ops = [&](int ks, u32x4_t (&A)[MBP], u32x4_t (&B)[NBK])
+                        __attribute__((always_inline)) {
+#pragma unroll
+      for (int mb = 0; mb < MBP; ++mb) {
+        const u32x2_t lo = read_tr16_g(ib + ks * 16 * RSI + aoff0 + 32 * mb);
+        const u32x2_t hi = read_tr16_g(ib + ks * 16 * RSI + aoff1 + 32 * mb);
+        A[mb] = u32x4_t{lo[0], lo[1], hi[0], hi[1]};
+      }
+#pragma unroll
+      for (int nb = 0; nb < NBK; ++nb)
+        B[nb] = *reinterpret_cast<const u32x4_t*>(kb + boff + nb * 32 * RSK + ks * 16);
+    };
+    u32x4_t A[2][MBP], B[2][NBK];
+    read_ops(0, A[0], B[0]);
+#pragma unroll
+    for (int ks = 0; ks < KSTEPS; ++ks) {
+      if (ks + 1 < KSTEPS) read_ops(ks + 1, A[(ks + 1) & 1], B[(ks + 1) & 1]);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int mb = 0; mb < MBP; ++mb)
+#pragma unroll
+        for (int nb = 0; nb < NBK; ++nb)
+          acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+              __builtin_bit_cast(bf16x8_t, A[ks & 1][mb]), __builtin_bit_cast(bf16x8_t, B[ks & 1][nb]),
+              acc[mb][nb], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    if (s + 1 < n_st) write_stage(s + 1, buf ^ 1);
+    lds_barrier_g();
+  }
+
+  // Epilogue: register 4g + i of block (mb, nb) holds pixel
+  // 32*(wp*MBP + mb) + 8g + 4*half + i of the tile, feature
+  // k0 + 32*(wk*NBK + nb) + l32.
+#pragma unroll
+  for (int nb = 0; nb < NBK; ++nb) {
+    const int n = k0 + 32 * (wk * NBK + nb) + l32;
+    const bool nv = n < a.Nk;
+#pragma unroll
+    for (int mb = 0; mb < MBP; ++mb) {
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int q = 32 * (wp * MBP + mb) + 8 * g + 4 * half;  // pixel within the tile
+        const int p = p0 + (q < tp ? q : 0);
+        const int b = p / a.hw;
+        const uint32_t vo = (nv && q < tp)
+                                ? (uint32_t)((((int64_t)b * a.Nk + n) * a.hw + (p - b * a.hw)) *
+                                             (int64_t)sizeof(TO))
+                                : 0x80000000u;
+        if constexpr (sizeof(TO) == 4) {
+          const u32x4_t v = {__float_as_uint(acc[mb][nb][4 * g]), __float_as_uint(acc[mb][nb][4 * g + 1]),
+                             __float_as_uint(acc[mb][nb][4 * g + 2]),
+                             __float_as_uint(acc[mb][nb][4 * g + 3])};
+          __builtin_amdgcn_raw_buffer_store_b128(v, out_rsrc, vo, 0, 0);
+        } else {
+          const u32x2_t v = {(uint32_t)from_f32<bf16_t>(acc[mb][nb][4 * g]) |
+                                 ((uint32_t)from_f32<bf16_t>(acc[mb][nb][4 * g + 1]) << 16),
+                             (uint32_t)from_f32<bf16_t>(acc[mb][nb][4 * g + 2]) |
+                                 ((uint32_t)from_f32<bf16_t>(acc[mb][nb][4 * g + 3]) << 16)};
+          __builtin_amdgcn_raw_buffer_store_b64(v, out_rsrc, vo, 0, 0);
+        }
+      }
+    }
+  }
+}
+
+// ---- instantiation table ----------------------------------------------------
+// (id, dtype, WP, WK, MBP, NBK, TC): tk = 32*WK*NBK, tp <= 32*WP*MBP,
+// 64*WP*WK threads.
+#define CNN_GEMM1_VARIANTS(X)                  \
+  X(1700, CNN_BF16, 2, 4, 4, 2, 64)            \
+  X(1701, CNN_BF16, 4, 2, 2, 2, 64)            \
+  X(1800, CNN_BF16_OBF16, 2, 4, 4, 2, 64)      \
+  X(1801, CNN_BF16_OBF16, 4, 2, 2, 2, 64)
+
+static const VariantG kVariantsG[] = {
+#define CNN_GV(id, dt, wp, wk, mbp, nbk, tc) \
+  {id, dt, 32 * wk * nbk, 32 * wp * mbp, tc, 64 * wp * wk, 16 * mbp * nbk},
+    CNN_GEMM1_VARIANTS(CNN_GV)
+#undef CNN_GV
+};
+
+const VariantG* variants_gemm1(int* count) {
+  *count = (int)(sizeof(kVariantsG) / sizeof(kVariantsG[0]));
+  return kVariantsG;
+}
+
+int64_t gemm1_lds_bytes(const VariantG& v) {
+  return 2 * ((int64_t)v.tc * (v.tp + 16) + (int64_t)v.tk * (v.tc + 8)) * 2;
+}
+
+bool gemm1_fits(const VariantG& v, const cnn_problem& p, int64_t tp) {
+  (void)v;
+  return p.Nr == 1 && p.Ns == 1 && p.sw == 1 && p.sh == 1 && p.Nc % 8 == 0 &&
+         (p.Nw * p.Nh) % 4 == 0 && tp % 4 == 0 && tp >= 4;
+}
+
+template <int DT, int WP, int WK, int MBP, int NBK, int TC>
+static hipError_t launch_g(const void* In, const void* Ker, void* Out, const ConvArgs& a,
+                           int64_t lds, hipStream_t stream) {
+  typedef typename std::conditional<DT == CNN_BF16, float, bf16_t>::type TO;
+  auto kern = conv_gemm1<TO, WP, WK, MBP, NBK, TC>;
+  static bool attr_set = false;
+  if (!attr_set) {
+    hipError_t e = hipFuncSetAttribute((const void*)kern,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+    if (e != hipSuccess) return e;
+    attr_set = true;
+  }
+  hipLaunchKernelGGL(kern, dim3((unsigned)a.grid), dim3(64 * WP * WK), (unsigned)lds, stream,
+                     (const bf16_t*)In, (const bf16_t*)Ker, (TO*)Out, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_gemm1(const VariantG& v, const void* In, const void* Ker, void* Out,
+                        const ConvArgs& a, int64_t lds_bytes, hipStream_t stream) {
+  switch (v.id) {
+#define CNN_CASEG(id, dt, wp, wk, mbp, nbk, tc) \
+  case id:                                     \
+    return launch_g<dt, wp, wk, mbp, nbk, tc>(In, Ker, Out, a, lds_bytes, stream);
+    CNN_GEMM1_VARIANTS(CNN_CASEG)
+#undef CNN_CASEG
+    default:
+      return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace cnnlib

@@ -84,6 +84,17 @@ def variant_dims(kernel, vid, dt, tk, tp, tc, stencil):
     Nr, Ns = stencil
     if kernel == cnn.K_ROWS:
         return rows_dims(vid, dt, stencil)
+    if kernel == cnn.K_GEMM1:  # 1x1 stride 1, Nw*Nh % 4 == 0, Nc % 8 == 0
+        cands = [(3, tc + 8, tk + 7, 6, 10, 1, 1, 1, 1), (2, 2 * tc + 16, tk - 5, 8, 14, 1, 1, 1, 1),
+                 (1, 24, tk + 7, 4, 5, 1, 1, 1, 1)]
+        for dims in cands:
+            try:
+                pl = cnn.plan_tiles(cnn.problem(*dims), dt, kernel, tk, tp, tc, cnn.budget())
+            except cnn.CnnError:
+                continue
+            if pl.variant == vid:
+                return dims
+        return None
     if kernel == cnn.K_SMALLC:  # few channels: Nc*Nr rows must fit the K-steps
         nc = 3 if Nr == 7 else 9
         cands = [(3, nc, tk + 7, 9, 13, Nr, Ns, 2, 2), (2, nc, tk + 7, 7, 13, Nr, Ns, 1, 1),
@@ -145,6 +156,8 @@ def variant_cases():
                     (nr, ns) if nr else ((1, 1) if vid % 100 in (10, 11, 12) else (5, 2))))
     for vid, dt, wm, wn, mb, nb, tc, nr, ns, kres, _, _ in osel.STREAM:
         out.append((cnn.K_STREAM, vid, dt, 32 * wm * mb, 32 * wn * nb, tc, (nr, ns)))
+    for vid, dt, wp, wk, mbp, nbk, tc in osel.GEMM1:
+        out.append((cnn.K_GEMM1, vid, dt, 32 * wk * nbk, 32 * wp * mbp, tc, (1, 1)))
     for vid, dt, nr, ns, mb, ncg in osel.ROWS:
         out.append((cnn.K_ROWS, vid, dt, 64, 0, 0, (nr, ns)))
     for vid, dt, nb, ks in osel.SMALLC:

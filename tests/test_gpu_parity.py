@@ -302,3 +302,39 @@ def test_rows_float_headline_shape():
     g = got[idx[:, 0], idx[:, 1], idx[:, 2], idx[:, 3]]
     nw, cond, _ = errors(g, want, absv)
     assert nw <= TOL["bf16"] and cond <= TOL["bf16"], (nw, cond)
+
+
+# ---- 1x1 stride-1 GEMM kernel: stages, k tiles, tiles across images --------
+GEMM1_SHAPES = [
+    (3, 72, 71, 6, 10, 1, 1, 1, 1),     # Nc = 72: a second stage of 8 channels
+    (2, 64, 300, 4, 5, 1, 1, 1, 1),     # two k tiles of 256, 20-pixel images
+    (5, 40, 130, 7, 12, 1, 1, 1, 1),    # 84-pixel images, tiles span images
+    (1, 128, 64, 14, 14, 1, 1, 1, 1),   # one 196-pixel image
+]
+
+
+@pytest.mark.parametrize("mode", ["bf16", "bf16_obf16"])
+@pytest.mark.parametrize("shape", GEMM1_SHAPES)
+def test_gemm1_exact(shape, mode):
+    """Every 1x1 GEMM instantiation of the mode, its balanced tile and a
+    small tile (several tiles per image or images per tile): bit-exact with
+    the oracle on integer inputs."""
+    Nb, Nc, Nk, Nw, Nh, Nr, Ns, sw, sh = shape
+    rng = np.random.default_rng(sum(shape) + 11)
+    In = inputs.f32_to_bf16_bits(rng.integers(-2, 3, size=(Nb, Nc, Nw, Nh)).astype(np.float32))
+    Ker = inputs.f32_to_bf16_bits(rng.integers(-2, 3, size=(Nk, Nc, 1, 1)).astype(np.float32))
+    want = oracle.conv(In, Ker, 1, 1)
+    if mode == "bf16_obf16":
+        want = oracle.widen(inputs.f32_to_bf16_bits(want.astype(np.float32)))
+    dt = MODES[mode]
+    for vid, vdt, wp, wk, mbp, nbk, tc in osel.GEMM1:
+        if vdt != dt:
+            continue
+        tk, tpmax = 32 * wk * nbk, 32 * wp * mbp
+        for cus in (256, 3):  # balanced tile; few slots -> the largest tile
+            pl = cnn.plan_tiles(cnn.problem(*shape), dt, cnn.K_GEMM1, tk, tpmax, tc,
+                                cnn.budget(cus, 160 * 1024, 128, 2))
+            assert pl.variant == vid and pl.tp % 4 == 0
+            say(f"[parity] gemm1 shape={shape} v{vid} tp={pl.tp} grid={pl.grid} mode={mode}")
+            got = run(In, Ker, 1, 1, mode, plan=pl)
+            assert np.array_equal(got, want), (vid, pl.tp)
