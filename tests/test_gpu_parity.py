@@ -310,6 +310,8 @@ GEMM1_SHAPES = [
     (2, 64, 300, 4, 5, 1, 1, 1, 1),     # two k tiles of 256, 20-pixel images
     (5, 40, 130, 7, 12, 1, 1, 1, 1),    # 84-pixel images, tiles span images
     (1, 128, 64, 14, 14, 1, 1, 1, 1),   # one 196-pixel image
+    (2, 24, 40, 6, 6, 1, 1, 1, 1),      # Nc < one stage: Ker blocks past Nc
+    (3, 8, 33, 4, 4, 1, 1, 1, 1),       # a single 8-channel block
 ]
 
 
