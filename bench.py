@@ -60,7 +60,8 @@ def measured_traffic(workload: str, mode: str):
 
 
 KERNELS = {"direct": 1, "igemm": 2, "pointwise": 3, "smallc": 4, "igemm_pipe": 5,
-           "igemm_dma": 6, "igemm_wide": 7, "igemm_rawk": 8, "stream": 9, "rows": 10, "gemm1": 11}
+           "igemm_dma": 6, "igemm_wide": 7, "igemm_rawk": 8, "stream": 9, "rows": 10, "gemm1": 11,
+           "srows": 12}
 
 
 def forced_plan(spec: str, w, mode: str):

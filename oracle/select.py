@@ -166,6 +166,16 @@ GEMM1 = [
 ]
 
 
+# (id, dtype, nr, ns, L) of the stride-2 row-band kernel: tk = 256, tc = 16,
+# strides 2 and 2, Nc % 16 == 0, Nh % 4 == 0, Nh <= 32, Ny <= 64; a tile is
+# L whole output rows of one image (tp = L*Nh, L | Nw).  Taken only when
+# requested (not ranked by `choose`).
+SROWS = [
+    (1900, BF16, 3, 3, 7), (1901, BF16, 3, 3, 4),
+    (2000, BF16_OBF16, 3, 3, 7), (2001, BF16_OBF16, 3, 3, 4),
+]
+
+
 def stream_grid(p: eq1.Problem, tk: int, tp: int, threads: int, lds: int, cus: int,
                 lds_bytes: int, wg_per_cu: int) -> int:
     """Workgroups a streaming plan launches: its slots, at most its tiles."""

@@ -20,11 +20,11 @@ CNN_F32, CNN_BF16, CNN_BF16_OBF16 = 0, 1, 2
 DTYPES = {"f32": CNN_F32, "bf16": CNN_BF16, "bf16_obf16": CNN_BF16_OBF16}
 
 (K_AUTO, K_DIRECT, K_IGEMM, K_POINTWISE, K_SMALLC, K_IGEMM_PIPE, K_IGEMM_DMA, K_IGEMM_WIDE,
- K_IGEMM_RAWK, K_STREAM, K_ROWS, K_GEMM1) = range(12)
+ K_IGEMM_RAWK, K_STREAM, K_ROWS, K_GEMM1, K_SROWS) = range(13)
 KERNEL_NAMES = {K_DIRECT: "direct", K_IGEMM: "igemm", K_POINTWISE: "pointwise", K_SMALLC: "smallc",
                 K_IGEMM_PIPE: "igemm_pipe", K_IGEMM_DMA: "igemm_dma", K_IGEMM_WIDE: "igemm_wide",
                 K_IGEMM_RAWK: "igemm_rawk", K_STREAM: "stream", K_ROWS: "rows",
-                K_GEMM1: "gemm1"}
+                K_GEMM1: "gemm1", K_SROWS: "srows"}
 
 STATUS = {0: "CNN_OK", -1: "CNN_E_NULL", -2: "CNN_E_SHAPE", -3: "CNN_E_DTYPE",
           -4: "CNN_E_OVERFLOW", -5: "CNN_E_ALIAS", -6: "CNN_E_UNSUPPORTED",

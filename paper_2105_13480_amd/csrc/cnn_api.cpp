@@ -242,6 +242,26 @@ bool gemm1_geometry_ok(const VariantG& v, const cnn_plan_t& pl) {
   return pl.grid == grid && pl.lds_bytes == gemm1_lds_bytes(v) && pl.lds_bytes <= 160 * 1024;
 }
 
+const VariantQ* find_variant_q(int id) {
+  int n = 0;
+  const VariantQ* vs = variants_srows(&n);
+  for (int i = 0; i < n; ++i)
+    if (vs[i].id == id) return &vs[i];
+  return nullptr;
+}
+
+// Geometry a stride-2 row-band plan must carry: bands of the instantiation's
+// L whole rows of one image, 16 channels per chunk, its grid, LDS and
+// workspace sizes.
+bool srows_geometry_ok(const VariantQ& v, const cnn_plan_t& pl) {
+  const cnn_problem& p = pl.prob;
+  if (!srows_fits(v, p) || pl.tc != 16 || pl.tp != v.L * p.Nh) return false;
+  const int64_t grid = p.Nb * (p.Nw / v.L) * ((p.Nk + v.tk - 1) / v.tk);
+  return pl.slab_rows == srows_slab_rows(v) && pl.grid == grid &&
+         pl.lds_bytes == srows_lds_bytes(v) && pl.lds_bytes <= 160 * 1024 &&
+         pl.ws_bytes == srows_ws_bytes(v, p);
+}
+
 const Variant4* find_variant4(int id) {
   int n = 0;
   const Variant4* vs = variants4(&n);
@@ -314,6 +334,16 @@ int run_plan(const void* In, const void* Ker, void* Out, const cnn_plan_t& pl, h
     if (!vr || vr->dtype != pl.dtype || vr->tk != pl.tk || !rows_geometry_ok(*vr, pl))
       return fail(CNN_E_PLAN, "plan names no matching kernel instantiation (variant %d)", pl.variant);
     e = launch_rows(*vr, In, Ker, Out, a, pl.lds_bytes, st);
+  } else if (pl.kernel == CNN_K_SROWS) {
+    const VariantQ* vq = find_variant_q(pl.variant);
+    if (!vq || vq->dtype != pl.dtype || vq->tk != pl.tk || !srows_geometry_ok(*vq, pl))
+      return fail(CNN_E_PLAN, "plan names no matching kernel instantiation (variant %d)", pl.variant);
+    void* ws = user_ws;
+    if (!ws) {
+      int st2 = get_workspace(st, pl.ws_bytes, &ws);
+      if (st2) return st2;
+    }
+    e = launch_srows(*vq, In, Ker, Out, ws, a, pl.lds_bytes, st);
   } else if (pl.kernel == CNN_K_SMALLC) {
     const VariantS* vs = find_variant_s(pl.variant);
     if (!vs || vs->dtype != pl.dtype || vs->tk != pl.tk || !smallc_geometry_ok(*vs, pl))
@@ -421,7 +451,7 @@ int cnn_plan_tiles(const cnn_problem* prob, int dtype, int kernel, int64_t tk, i
   if (!prob || !plan) return fail(CNN_E_NULL, "prob and plan must be non-NULL");
   int st;
   if ((st = check_problem(*prob)) || (st = check_dtype(dtype))) return st;
-  if (kernel < CNN_K_AUTO || kernel > CNN_K_GEMM1)
+  if (kernel < CNN_K_AUTO || kernel > CNN_K_SROWS)
     return fail(CNN_E_UNSUPPORTED, "unknown kernel %d", kernel);
   cnn_budget bud;
   if ((st = resolve_budget(budget, &bud))) return st;

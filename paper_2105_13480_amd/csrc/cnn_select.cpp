@@ -325,6 +325,23 @@ static bool eval_gemm1(const cnn_problem& p, int dtype, const VariantG& v, const
   return eval_tiling(p, dtype, v.id, v.tk, tp, v.tc, v.acc, 1, lds, 0, bud, plan, time_clk);
 }
 
+// Stride-2 row-band kernel (conv_srows): fixed stencil, tiles of the
+// instantiation's L whole output rows of one image by 256 features, 16
+// channels per chunk, Ker repacked into the workspace.
+static bool eval_srows(const cnn_problem& p, int dtype, const VariantQ& v, const cnn_budget& bud,
+                       cnn_plan_t* plan, double* time_clk) {
+  if (!srows_fits(v, p)) return false;
+  const int64_t Nx = 2 * (p.Nw - 1) + p.Nr, Ny = 2 * (p.Nh - 1) + p.Ns;
+  const int64_t ws = srows_ws_bytes(v, p);
+  if (p.Nb * p.Nc * Nx * Ny * 2 >= (1LL << 31) || ws >= (1LL << 31) ||
+      p.Nb * p.Nk * p.Nw * p.Nh * out_bytes(dtype) >= (1LL << 31))
+    return false;
+  const int64_t lds = srows_lds_bytes(v);
+  if (lds > std::min<int64_t>(bud.lds_bytes, 160 * 1024)) return false;
+  return eval_tiling(p, dtype, v.id, v.tk, v.L * p.Nh, 16, v.acc, srows_slab_rows(v), lds, ws,
+                     bud, plan, time_clk);
+}
+
 static void fill_common(const cnn_problem& p, int dtype, cnn_plan_t* plan) {
   const int64_t Nx = p.sw * (p.Nw - 1) + p.Nr, Ny = p.sh * (p.Nh - 1) + p.Ns;
   const double e_in = in_bytes(dtype), e_out = out_bytes(dtype);
@@ -366,7 +383,7 @@ int select_plan(const cnn_problem& p, int dtype, const cnn_budget& bud, int kern
   if (kernel != CNN_K_AUTO && kernel != CNN_K_IGEMM && kernel != CNN_K_IGEMM_PIPE &&
       kernel != CNN_K_IGEMM_DMA && kernel != CNN_K_IGEMM_WIDE && kernel != CNN_K_IGEMM_RAWK &&
       kernel != CNN_K_POINTWISE && kernel != CNN_K_SMALLC && kernel != CNN_K_STREAM &&
-      kernel != CNN_K_ROWS && kernel != CNN_K_GEMM1)
+      kernel != CNN_K_ROWS && kernel != CNN_K_GEMM1 && kernel != CNN_K_SROWS)
     return CNN_E_UNSUPPORTED;
   bool found = false;
   double best_t = 0;
@@ -412,6 +429,22 @@ int select_plan(const cnn_problem& p, int dtype, const cnn_budget& bud, int kern
       double t;
       if (eval_gemm1(p, dtype, v, bud, &cand, &t)) {
         cand.kernel = CNN_K_GEMM1;
+        consider(cand, t);
+      }
+    }
+  }
+  // The stride-2 row-band kernel likewise (tp = L*Nh names the band; 0: any).
+  if (kernel == CNN_K_SROWS) {
+    int nq = 0;
+    const VariantQ* vq = variants_srows(&nq);
+    for (int i = 0; i < nq; ++i) {
+      const VariantQ& v = vq[i];
+      if (v.dtype != dtype || v.tk != tk || (tp != 0 && tp != v.L * p.Nh) || (tc != 0 && tc != 16))
+        continue;
+      cnn_plan_t cand;
+      double t;
+      if (eval_srows(p, dtype, v, bud, &cand, &t)) {
+        cand.kernel = CNN_K_SROWS;
         consider(cand, t);
       }
     }
@@ -550,6 +583,11 @@ int enumerate_plans(const cnn_problem& p, int dtype, const cnn_budget& bud, cnn_
   for (int i = 0; i < ngm; ++i)
     if (vgm[i].dtype == dtype && eval_gemm1(p, dtype, vgm[i], bud, &cand, &t))
       add(cand, CNN_K_GEMM1);
+  int nsq = 0;
+  const VariantQ* vsq = variants_srows(&nsq);
+  for (int i = 0; i < nsq; ++i)
+    if (vsq[i].dtype == dtype && eval_srows(p, dtype, vsq[i], bud, &cand, &t))
+      add(cand, CNN_K_SROWS);
   // row streaming: every band length L (dividing Nw) of 2 .. 4 groups' rows
   int nrw = 0;
   const VariantR* vrw = variants_rows(&nrw);

@@ -165,6 +165,24 @@ bool gemm1_fits(const VariantG& v, const cnn_problem& p, int64_t tp);
 hipError_t launch_gemm1(const VariantG& v, const void* In, const void* Ker, void* Out,
                         const ConvArgs& a, int64_t lds_bytes, hipStream_t stream);
 
+// A stride-2 row-band instantiation (bf16, fixed stencil): tk = 256, bands
+// of L whole output rows (Nh <= 32), 16 channels per chunk, packed Ker.
+struct VariantQ {
+  int32_t id;
+  int32_t dtype;
+  int32_t tk;
+  int32_t nr, ns;  // compile-time stencil
+  int32_t L;       // output rows per band
+  int32_t acc;     // fp32 accumulators per lane
+};
+const VariantQ* variants_srows(int* count);
+int64_t srows_slab_rows(const VariantQ& v);
+int64_t srows_lds_bytes(const VariantQ& v);
+int64_t srows_ws_bytes(const VariantQ& v, const cnn_problem& p);
+bool srows_fits(const VariantQ& v, const cnn_problem& p);
+hipError_t launch_srows(const VariantQ& v, const void* In, const void* Ker, void* Out, void* ws,
+                        const ConvArgs& a, int64_t lds_bytes, hipStream_t stream);
+
 // Ker repack for the pipelined kernels (defined with conv_igemm2).
 __global__ void pack_ker_bf16(const uint16_t* __restrict__ Ker, uint32_t __attribute__((ext_vector_type(4)))* __restrict__ P,
                               ConvArgs a, int TK, int TC, int blk_vecs, int64_t total_vecs);

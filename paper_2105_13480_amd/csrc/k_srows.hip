@@ -1,0 +1,478 @@
+// Stride-2 convolution over bands of whole output rows (bf16 MFMA, gfx950).
+//
+// Out[b][k][w][h] = sum_{c,r,s} In[b][c][2w+r][2h+s] * Ker[k][c][r][s]
+// (Eq. (1)'s problem with sigma_w = sigma_h = 2).  A workgroup owns a band of
+// L whole output rows of one image by TK = 256 output features and walks the
+// input features 16 at a time (Listing 3 with W_c = N_c); each 16-channel
+// chunk is taken in Nr stages, one stencil row r per stage.
+//
+// * In: per chunk, the band's 2(L-1)+Nr input rows, 16-byte loads of 8
+//   columns of one channel (rows start at any element; the loads are
+//   unaligned).  Registers transpose four channels x eight columns into
+//   MFMA-ready units of channels, split by column parity: unit (g, row, i)
+//   holds the 8 channels of group g at column 2i, unit (g, row, 32 + i) at
+//   column 2i+1.  Tap s of output position h reads unit s/2 + h (s even)
+//   or 32 + (s-1)/2 + h (s odd): for every tap the 32 positions of a row are
+//   32 consecutive 16-byte units, read with ds_read_b128.
+// * Ker: repacked once per call into the B-operand image of every (k tile,
+//   chunk, stencil row) slice, [s][g][k][8 channels]; a stage copies the
+//   next stage's slice (24 KB for 3x3) straight into LDS with 16-byte
+//   buffer->LDS loads, one contiguous kilobyte per wave instruction.
+// * Buffers: Ker slices four deep (the copy for stage t + 3 is issued in
+//   stage t; stage t's last K-step already reads stage t + 1's operands), In
+//   two deep by chunk (the next chunk's loads are issued in a chunk's first
+//   stage and written after its second); copies, loads and operand reads
+//   are issued between the K-steps' products; one barrier per stage.
+// * Waves: waves w and w+4 (one SIMD) take features 64*(w%4) .. +63 (two
+//   32-feature blocks) x the band's L rows, half of the (row, block) pairs
+//   each, with the same straight-line code for odd L too.  A 32-position
+//   MFMA block is one output row (Nh <= 32).
+// * D[position][feature]: a lane ends with 4 consecutive positions of one
+//   feature, written as one 16-byte (fp32) or 8-byte (bf16) store.
+#include <type_traits>
+
+#include "internal.h"
+#include "common.h"
+
+namespace cnnlib {
+
+namespace {
+
+#define LDS_PTR_Q(T, p) ((__attribute__((address_space(3))) T*)(p))
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc_q(const void* base, int64_t bytes) {
+  bytes = (bytes + 3) & ~(int64_t)3;
+  const int32_t n = bytes > 0x7ffffffcLL ? 0x7ffffffc : (int32_t)bytes;
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, n, 0x00020000);
+}
+
+// 16-byte buffer -> LDS copy: lane i's 16 bytes land at lds + 16 i (lds
+// wave-uniform).
+__device__ __forceinline__ void dma16_q(__amdgpu_buffer_rsrc_t r, void* lds, uint32_t voff) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, LDS_PTR_Q(void, lds), 16, voff, 0, 0, 0);
+#else
+  (void)r;
+  (void)lds;
+  (void)voff;
+#endif
+}
+
+// f(integral_constant<int, I>) for I = B .. E-1, in order.
+template <int B, int E, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (B < E) {
+    f(std::integral_constant<int, B>());
+    static_for<B + 1, E>(f);
+  }
+}
+
+}  // namespace
+
+// TO: Out element type.  NR x NS stencil, stride 2 both ways; L output rows
+// per band.
+template <typename TO, int NR, int NS, int L>
+__global__ __launch_bounds__(512) void conv_srows(const bf16_t* __restrict__ In,
+                                                  const u32x4_t* __restrict__ Kp,
+                                                  TO* __restrict__ Out, ConvArgs a,
+                                                  int blk_vecs) {
+  constexpr int NT = 512;
+  constexpr int TK = 256;
+  constexpr int SR = NR >= 2 ? 2 * (L - 1) + NR : L;  // slab rows held per chunk
+  constexpr int SX = NR >= 2 ? 1 : 2;                 // input rows per slab row
+  constexpr int RW = (L + 1) / 2;                     // rows per wave
+  constexpr int NI = 2 * SR * 8 * 2;                  // In items per chunk
+  constexpr int NIPT = (NI + NT - 1) / NT;            // items per thread
+  constexpr int IN_UNITS = 2 * SR * 64;               // 16-byte units per In buffer
+  constexpr int KER_UNITS = NS * 2 * TK;              // per Ker buffer (one stencil row)
+  constexpr int NDK = KER_UNITS / NT;                 // copies per thread per stage
+  static_assert(L >= 2 && RW <= 4, "two row groups of at most four rows");
+  static_assert(NR >= 2, "In loads one stage ahead of their LDS writes");
+  static_assert(NS <= 3 && NR <= 3, "taps within one 64-unit row");
+  static_assert(KER_UNITS % NT == 0, "whole copies");
+
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  u32x4_t* kbuf = reinterpret_cast<u32x4_t*>(smem);  // [4][NS][2][TK]
+  u32x4_t* ibuf = kbuf + 4 * KER_UNITS;              // [2][2][SR][64]
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int fp = wave & 3;   // feature pair
+  const int rg = wave >> 2;  // row group
+  const int l32 = lane & 31, half = lane >> 5;
+
+  const int n_bands = a.Nw / L;
+  const int tile = xcd_remap(blockIdx.x, gridDim.x);
+  const int band = tile / a.n_ktiles;
+  const int kt = tile - band * a.n_ktiles;
+  const int b = band / n_bands;
+  const int w0 = (band - b * n_bands) * L;
+  const int k0 = kt * TK;
+  const int n_cc = a.Nc / 16;
+
+  const __amdgpu_buffer_rsrc_t in_rsrc = rsrc_q(In, a.in_total * 2);
+  const __amdgpu_buffer_rsrc_t kp_rsrc =
+      rsrc_q(Kp, (int64_t)a.n_ktiles * n_cc * blk_vecs * 16);
+  const __amdgpu_buffer_rsrc_t out_rsrc = rsrc_q(Out, a.out_total * (int64_t)sizeof(TO));
+
+  // ---- In items: (g, slab row j, 8-column block b8, channel half hc); an
+  // item is four 16-byte loads (channels 8g + 4hc + 0..3 of the chunk).
+  // The range check drops a whole dword that straddles the end of In; the
+  // only element such a dword can hold is In's last, loaded once and
+  // patched in when the item is written.
+  const uint32_t in_last =
+      __builtin_amdgcn_raw_buffer_load_b16(in_rsrc, (uint32_t)((a.in_total - 1) * 2), 0, 0);
+  int in_e[NIPT];    // element offset of the item's channel 8g + 4hc of chunk 0
+  int in_dst[NIPT];  // unit of its first even column (+ 8 bytes for hc = 1)
+  int in_hc[NIPT];
+  bool in_ok[NIPT];
+#pragma unroll
+  for (int j = 0; j < NIPT; ++j) {
+    const int t = tid + NT * j;
+    const int tt = t < NI ? t : NI - 1;
+    const int hc = tt & 1, b8 = (tt >> 1) & 7, gj = tt >> 4;
+    const int g = gj / SR, jr = gj - g * SR;
+    const int x = 2 * w0 + jr * SX;
+    in_e[j] = (int)((int64_t)b * a.in_img) + (8 * g + 4 * hc) * a.nxny + x * a.Ny + 8 * b8;
+    in_dst[j] = (g * SR + jr) * 64 + 4 * b8;
+    in_hc[j] = hc;
+    in_ok[j] = t < NI;
+  }
+  u32x4_t vin[NIPT][4];
+  auto load_in_part = [&](int cc, int k0_, int k1_) __attribute__((always_inline)) {
+#pragma unroll
+    for (int j = 0; j < NIPT; ++j)
+#pragma unroll
+      for (int k = k0_; k < k1_; ++k)
+        vin[j][k] = __builtin_bit_cast(
+            u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(
+                         in_rsrc, (uint32_t)((in_e[j] + (16 * cc + k) * a.nxny) * 2), 0, 0));
+  };
+  auto write_in = [&](int cc, u32x4_t* dstb) __attribute__((always_inline)) {
+    char* base = reinterpret_cast<char*>(dstb);
+#pragma unroll
+    for (int j = 0; j < NIPT; ++j) {
+      if (!in_ok[j]) continue;
+      u32x4_t v[4] = {vin[j][0], vin[j][1], vin[j][2], vin[j][3]};
+      // the last-element patch (one item of the whole tensor)
+      const int d0 = (int)(a.in_total - 1) - (in_e[j] + 16 * cc * a.nxny);
+      if (d0 >= 0 && d0 < 3 * a.nxny + 8) {
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const int d = d0 - k * a.nxny;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const uint32_t lo = d == 2 * i ? ((v[k][i] & 0xffff0000u) | in_last) : v[k][i];
+            v[k][i] = d == 2 * i + 1 ? ((lo & 0xffffu) | (in_last << 16)) : lo;
+          }
+        }
+      }
+      char* p = base + in_dst[j] * 16 + 8 * in_hc[j];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const u32x2_t ev = {__builtin_amdgcn_perm(v[1][i], v[0][i], 0x05040100u),
+                            __builtin_amdgcn_perm(v[3][i], v[2][i], 0x05040100u)};
+        *reinterpret_cast<u32x2_t*>(p + 16 * i) = ev;
+        if (NS > 1) {
+          const u32x2_t od = {__builtin_amdgcn_perm(v[1][i], v[0][i], 0x07060302u),
+                              __builtin_amdgcn_perm(v[3][i], v[2][i], 0x07060302u)};
+          *reinterpret_cast<u32x2_t*>(p + 16 * (32 + i)) = od;
+        }
+      }
+    }
+  };
+  // Ker slice (chunk cc, stencil row r) -> a Ker buffer, in NDK pieces of
+  // one 16-byte copy per thread
+  auto copy_ker_piece = [&](int cc, int r, u32x4_t* dst, int j) __attribute__((always_inline)) {
+    const uint32_t base = (uint32_t)((kt * n_cc + cc) * blk_vecs + r * KER_UNITS);
+    dma16_q(kp_rsrc, dst + NT * j + 64 * wave, (base + NT * j + tid) * 16u);
+  };
+  auto copy_ker = [&](int cc, int r, u32x4_t* dst) __attribute__((always_inline)) {
+#pragma unroll
+    for (int j = 0; j < NDK; ++j) copy_ker_piece(cc, r, dst, j);
+  };
+
+  // Rows and feature blocks of a wave (the two waves of a SIMD, w and w+4,
+  // together cover the band's L rows x the feature pair's two blocks):
+  //   even L: wave w+4*q takes rows q*L/2 + i, both blocks;
+  //   odd L = 2m+1: wave w takes rows i = 0..m with block 0 and rows 0..m-1
+  //   with block 1; wave w+4 takes rows L-1-i with block 1 and rows L-1-i,
+  //   i < m, with block 0.  Row m is split between them by block, so both
+  //   run the same 2*RW - 1 products per K-step, straight-line.
+  constexpr bool ODD = (L & 1) != 0;
+  const int row0 = rg == 0 ? 0 : (ODD ? L - 1 : L / 2);  // band row of i = 0
+  const int rdir = (rg == 1 && ODD) ? -1 : 1;
+  const int nbf = (rg == 1 && ODD) ? 1 : 0;               // block of the first B operand
+  auto has_second = [](int i) { return !ODD || i < RW - 1; };
+  // Operand offsets (units): A = In unit (half, slab row, position l32);
+  // B = Ker unit (s, half, feature 64 fp + 32 nb + l32).
+  const int a_off = half * SR * 64 + l32;
+  const int b_first = half * TK + 64 * fp + 32 * nbf + l32;
+  const int b_second = half * TK + 64 * fp + 32 * (1 - nbf) + l32;
+
+  f32x16_t acc[RW][2];
+#pragma unroll
+  for (int i = 0; i < RW; ++i)
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][nb][e] = 0.f;
+
+  // Operand registers of two consecutive K-steps (parity p): A[p][i] = In
+  // unit of row i, B[p][q] = Ker unit of the wave's first / second block.
+  u32x4_t A[2][RW], B[2][2];
+  auto read_a = [&](const u32x4_t* ib, int r, int s, int i) __attribute__((always_inline)) {
+    const int col = (s & 1) ? 32 + (s >> 1) : (s >> 1);
+    const int jr = (2 * (row0 + rdir * i) + r) / SX;
+    return ib[a_off + jr * 64 + col];
+  };
+  auto read_b = [&](const u32x4_t* kb, int s, int q) __attribute__((always_inline)) {
+    return kb[s * 2 * TK + (q ? b_second : b_first)];
+  };
+
+  // One stage (stencil row r of the chunk in ib, Ker slice kb): the
+  // products of NS K-steps from operand parity P, whose step-0 operands are
+  // already in registers.  Each next step's operands -- in the last step,
+  // those of the next stage's first step (nib, nkb, nr), whose data landed
+  // before the previous barrier -- are read between the products, one row
+  // ahead of their use, so no stage starts on a cold LDS read.  mem(slot)
+  // issues this stage's share of the copies and loads for later stages
+  // (slot 0 first, slot s + 1 after K-step s's products).
+  auto stage = [&](auto PC, const u32x4_t* ib, const u32x4_t* kb, int r, const u32x4_t* nib,
+                   const u32x4_t* nkb, int nr, auto mem) __attribute__((always_inline)) {
+    constexpr int P = decltype(PC)::value;
+    mem(0);
+    __builtin_amdgcn_sched_barrier(0);
+    static_for<0, NS>([&](auto SC) {
+      constexpr int st = decltype(SC)::value;
+      constexpr int cu = (P + st) & 1, nx = cu ^ 1;
+#pragma unroll
+      for (int i = 0; i < RW; ++i) {
+#pragma unroll
+        for (int q = 0; q < 2; ++q)
+          if (q == 0 || has_second(i))
+            acc[i][q] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                __builtin_bit_cast(bf16x8_t, A[cu][i]), __builtin_bit_cast(bf16x8_t, B[cu][q]),
+                acc[i][q], 0, 0, 0);
+        if (i == 0) {
+          B[nx][0] = st + 1 < NS ? read_b(kb, st + 1, 0) : read_b(nkb, 0, 0);
+          B[nx][1] = st + 1 < NS ? read_b(kb, st + 1, 1) : read_b(nkb, 0, 1);
+        }
+        A[nx][i] = st + 1 < NS ? read_a(ib, r, st + 1, i) : read_a(nib, nr, 0, i);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      mem(st + 1);
+      __builtin_amdgcn_sched_barrier(0);
+    });
+  };
+
+  // ---- prologue: chunk 0's rows and the first three Ker slices.  Ker is
+  // four slices deep: stage t reads buffer t % 4 and, in its last K-step,
+  // buffer (t + 1) % 4; the copy for stage t + 3 is issued during stage t
+  // and waited for at the end of stage t + 1.
+  copy_ker(0, 0, kbuf);
+#pragma unroll
+  for (int t = 1; t < 3; ++t) copy_ker(min(t / NR, n_cc - 1), t % NR, kbuf + t * KER_UNITS);
+  load_in_part(0, 0, 4);
+  write_in(0, ibuf);
+  asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  B[0][0] = read_b(kbuf, 0, 0);
+  B[0][1] = read_b(kbuf, 0, 1);
+#pragma unroll
+  for (int i = 0; i < RW; ++i) A[0][i] = read_a(ibuf, 0, 0, i);
+
+  int kcur = 0;  // Ker buffer of the current stage
+  for (int cc = 0; cc < n_cc; ++cc) {
+    const int cn = cc + 1 < n_cc ? cc + 1 : cc;  // (the last chunk reloads itself)
+    const u32x4_t* ib = ibuf + (cc & 1) * IN_UNITS;
+    static_for<0, NR>([&](auto RC) {
+      constexpr int r = decltype(RC)::value;
+      const u32x4_t* kb = kbuf + kcur * KER_UNITS;
+      const int k1 = (kcur + 1) & 3, k3 = (kcur + 3) & 3;
+      // stage + 3: (cc3, r3), clamped to the last chunk (a redundant copy)
+      const int cc3 = min(cc + (r + 3) / NR, n_cc - 1), r3 = (r + 3) % NR;
+      auto mem = [&](int slot) __attribute__((always_inline)) {
+        if (r == 0 && slot == 0) load_in_part(cn, 0, 2);
+        if (r == 0 && slot == 1) load_in_part(cn, 2, 4);
+#pragma unroll
+        for (int j = 0; j < NDK; ++j)
+          if (slot == 1 + (j * NS) / NDK) copy_ker_piece(cc3, r3, kbuf + k3 * KER_UNITS, j);
+      };
+      // the next stage: (cc, r + 1), or (cc + 1, 0) from the other In buffer
+      const u32x4_t* nib = r + 1 < NR ? ib : ibuf + ((cc + 1) & 1) * IN_UNITS;
+      stage(std::integral_constant<int, (r * NS) & 1>(), ib, kb, r, nib, kbuf + k1 * KER_UNITS,
+            (r + 1) % NR, mem);
+      __builtin_amdgcn_sched_barrier(0);
+      if (r == NR - 2) write_in(cn, ibuf + ((cc + 1) & 1) * IN_UNITS);
+      // the copy issued a stage ago (for stage + 2) has landed; this stage's
+      // copies and loads may stay in flight
+      if (r == 0)
+        asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(NDK + 4 * NIPT) : "memory");
+      else
+        asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(NDK) : "memory");
+      kcur = k1;
+    });
+    if constexpr (((NR * NS) & 1) != 0) {
+      // a chunk has an odd number of K-steps: the next chunk's first
+      // operands were read into parity 1
+#pragma unroll
+      for (int i = 0; i < RW; ++i) A[0][i] = A[1][i];
+      B[0][0] = B[1][0];
+      B[0][1] = B[1][1];
+    }
+  }
+
+  // ---- epilogue: register 4g + e of block (i, q) holds position
+  // 8g + 4*half + e of output row w0 + row0 + rdir*i, feature
+  // k0 + 64 fp + 32 (q ? 1 - nbf : nbf) + l32.
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    const int n = k0 + 64 * fp + 32 * (q ? 1 - nbf : nbf) + l32;
+    const bool nv = n < a.Nk;
+#pragma unroll
+    for (int i = 0; i < RW; ++i) {
+      if (q == 1 && !has_second(i)) continue;
+      const int w = w0 + row0 + rdir * i;
+      const int64_t rbase = (((int64_t)b * a.Nk + n) * a.Nw + w) * a.Nh;
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int h0 = 8 * g + 4 * half;
+        const uint32_t vo = (nv && h0 < a.Nh) ? (uint32_t)((rbase + h0) * (int64_t)sizeof(TO))
+                                              : 0x80000000u;
+        if constexpr (sizeof(TO) == 4) {
+          const u32x4_t v = {__float_as_uint(acc[i][q][4 * g]), __float_as_uint(acc[i][q][4 * g + 1]),
+                             __float_as_uint(acc[i][q][4 * g + 2]),
+                             __float_as_uint(acc[i][q][4 * g + 3])};
+          __builtin_amdgcn_raw_buffer_store_b128(v, out_rsrc, vo, 0, 0);
+        } else {
+          const u32x2_t v = {(uint32_t)from_f32<bf16_t>(acc[i][q][4 * g]) |
+                                 ((uint32_t)from_f32<bf16_t>(acc[i][q][4 * g + 1]) << 16),
+                             (uint32_t)from_f32<bf16_t>(acc[i][q][4 * g + 2]) |
+                                 ((uint32_t)from_f32<bf16_t>(acc[i][q][4 * g + 3]) << 16)};
+          __builtin_amdgcn_raw_buffer_store_b64(v, out_rsrc, vo, 0, 0);
+        }
+      }
+    }
+  }
+}
+
+// ---- Ker repack --------------------------------------------------------------
+// Slice image of every (k tile, 16-channel chunk): unit
+// ((kt*n_cc + cc)*blk_vecs + (tap*2 + g)*TK + kk) holds channels
+// 16cc + 8g .. +7 of feature kt*TK + kk at tap (zero for features past Nk),
+// so the stage of stencil row r copies units r*NS*2*TK .. +NS*2*TK of its
+// block.  One thread per (k tile, chunk, g, kk): its feature's 8 channels x
+// RS taps are one 16-byte-aligned run of RS 16-byte blocks, transposed in
+// registers (v_perm) into RS units.
+template <int RS>
+__global__ __launch_bounds__(256) void pack_ker_srows(const bf16_t* __restrict__ Ker,
+                                                      u32x4_t* __restrict__ P, ConvArgs a,
+                                                      int blk_vecs) {
+  constexpr int TK = 256;
+  const int n_cc = a.Nc / 16;
+  const int t = blockIdx.x * 256 + threadIdx.x;
+  if (t >= a.n_ktiles * n_cc * 2 * TK) return;
+  const int kk = t % TK, g = (t / TK) & 1, blk = t / (2 * TK);
+  const int kt = blk / n_cc, cc = blk - kt * n_cc;
+  const int k = kt * TK + kk;
+  const bool ok = k < a.Nk;
+  u32x4_t run[RS];
+  const u32x4_t* src =
+      reinterpret_cast<const u32x4_t*>(Ker + ((int64_t)(ok ? k : 0) * a.Nc + 16 * cc + 8 * g) * RS);
+#pragma unroll
+  for (int q = 0; q < RS; ++q) run[q] = src[q];
+  u32x4_t* dst = P + (int64_t)blk * blk_vecs + g * TK + kk;
+#pragma unroll
+  for (int tap = 0; tap < RS; ++tap) {
+    u32x4_t v;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int e0 = (2 * i) * RS + tap, e1 = e0 + RS;
+      const uint32_t sel =
+          ((e0 & 1) ? 0x0302u : 0x0100u) | ((e1 & 1) ? 0x07060000u : 0x05040000u);
+      const uint32_t w1 = run[(e1 >> 1) >> 2][(e1 >> 1) & 3];
+      const uint32_t w0 = run[(e0 >> 1) >> 2][(e0 >> 1) & 3];
+      v[i] = ok ? __builtin_amdgcn_perm(w1, w0, sel) : 0u;
+    }
+    dst[tap * 2 * TK] = v;
+  }
+}
+
+// ---- instantiation table ----------------------------------------------------
+// (id, dtype, NR, NS, L): tk = 256, tc = 16, bands of L output rows.
+#define CNN_SROWS_VARIANTS(X)       \
+  X(1900, CNN_BF16, 3, 3, 7)        \
+  X(1901, CNN_BF16, 3, 3, 4)        \
+  X(2000, CNN_BF16_OBF16, 3, 3, 7)  \
+  X(2001, CNN_BF16_OBF16, 3, 3, 4)
+
+static const VariantQ kVariantsQ[] = {
+#define CNN_QV(id, dt, nr, ns, l) {id, dt, 256, nr, ns, l, 32 * ((l + 1) / 2) - 16 * (l & 1)},
+    CNN_SROWS_VARIANTS(CNN_QV)
+#undef CNN_QV
+};
+
+const VariantQ* variants_srows(int* count) {
+  *count = (int)(sizeof(kVariantsQ) / sizeof(kVariantsQ[0]));
+  return kVariantsQ;
+}
+
+int64_t srows_slab_rows(const VariantQ& v) {
+  return v.nr >= 2 ? 2 * (v.L - 1) + v.nr : v.L;
+}
+
+int64_t srows_lds_bytes(const VariantQ& v) {
+  return (4 * (int64_t)v.ns * 2 * v.tk + 2 * 2 * srows_slab_rows(v) * 64) * 16;
+}
+
+int64_t srows_blk_vecs(const VariantQ& v) {
+  const int64_t n = (int64_t)v.nr * v.ns * 2 * v.tk;
+  return (n + 255) / 256 * 256;
+}
+
+int64_t srows_ws_bytes(const VariantQ& v, const cnn_problem& p) {
+  return ((p.Nk + v.tk - 1) / v.tk) * (p.Nc / 16) * srows_blk_vecs(v) * 16;
+}
+
+bool srows_fits(const VariantQ& v, const cnn_problem& p) {
+  const int64_t Ny = 2 * (p.Nh - 1) + p.Ns;
+  return p.sw == 2 && p.sh == 2 && p.Nr == v.nr && p.Ns == v.ns && p.Nc % 16 == 0 &&
+         p.Nh % 4 == 0 && p.Nh <= 32 && Ny <= 64 && p.Nw % v.L == 0;
+}
+
+template <int DT, int NR, int NS, int L>
+static hipError_t launch_q(const void* In, const void* Ker, void* Out, void* ws, const ConvArgs& a,
+                           int64_t lds, hipStream_t stream, const VariantQ& v) {
+  typedef typename std::conditional<DT == CNN_BF16, float, bf16_t>::type TO;
+  const int blk = (int)srows_blk_vecs(v);
+  const int64_t threads = (int64_t)a.n_ktiles * (a.Nc / 16) * 2 * 256;
+  hipLaunchKernelGGL(pack_ker_srows<NR * NS>, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0,
+                     stream, (const bf16_t*)Ker, (u32x4_t*)ws, a, blk);
+  auto kern = conv_srows<TO, NR, NS, L>;
+  static bool attr_set = false;
+  if (!attr_set) {
+    hipError_t e = hipFuncSetAttribute((const void*)kern,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+    if (e != hipSuccess) return e;
+    attr_set = true;
+  }
+  hipLaunchKernelGGL(kern, dim3((unsigned)a.grid), dim3(512), (unsigned)lds, stream,
+                     (const bf16_t*)In, (const u32x4_t*)ws, (TO*)Out, a, blk);
+  return hipGetLastError();
+}
+
+hipError_t launch_srows(const VariantQ& v, const void* In, const void* Ker, void* Out, void* ws,
+                        const ConvArgs& a, int64_t lds_bytes, hipStream_t stream) {
+  switch (v.id) {
+#define CNN_CASEQ(id, dt, nr, ns, l) \
+  case id:                          \
+    return launch_q<dt, nr, ns, l>(In, Ker, Out, ws, a, lds_bytes, stream, v);
+    CNN_SROWS_VARIANTS(CNN_CASEQ)
+#undef CNN_CASEQ
+    default:
+      return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace cnnlib

@@ -84,6 +84,15 @@ def variant_dims(kernel, vid, dt, tk, tp, tc, stencil):
     Nr, Ns = stencil
     if kernel == cnn.K_ROWS:
         return rows_dims(vid, dt, stencil)
+    if kernel == cnn.K_SROWS:  # stride 2, Nc % 16 == 0, Nh % 4 == 0, L | Nw
+        from oracle import select as osel
+        L = next(r[4] for r in osel.SROWS if r[0] == vid)
+        dims = {7: (2, 32, 300, 7, 28, Nr, Ns, 2, 2), 4: (3, 16, 64, 8, 12, Nr, Ns, 2, 2)}[L]
+        try:
+            pl = cnn.plan_tiles(cnn.problem(*dims), dt, kernel, tk, 0, tc, cnn.budget())
+        except cnn.CnnError:
+            return None
+        return dims if pl.variant == vid else None
     if kernel == cnn.K_GEMM1:  # 1x1 stride 1, Nw*Nh % 4 == 0, Nc % 8 == 0
         cands = [(3, tc + 8, tk + 7, 6, 10, 1, 1, 1, 1), (2, 2 * tc + 16, tk - 5, 8, 14, 1, 1, 1, 1),
                  (1, 24, tk + 7, 4, 5, 1, 1, 1, 1)]
@@ -158,6 +167,8 @@ def variant_cases():
         out.append((cnn.K_STREAM, vid, dt, 32 * wm * mb, 32 * wn * nb, tc, (nr, ns)))
     for vid, dt, wp, wk, mbp, nbk, tc in osel.GEMM1:
         out.append((cnn.K_GEMM1, vid, dt, 32 * wk * nbk, 32 * wp * mbp, tc, (1, 1)))
+    for vid, dt, nr, ns, L in osel.SROWS:
+        out.append((cnn.K_SROWS, vid, dt, 256, 0, 16, (nr, ns)))
     for vid, dt, nr, ns, mb, ncg in osel.ROWS:
         out.append((cnn.K_ROWS, vid, dt, 64, 0, 0, (nr, ns)))
     for vid, dt, nb, ks in osel.SMALLC:

@@ -340,3 +340,62 @@ def test_gemm1_exact(shape, mode):
             say(f"[parity] gemm1 shape={shape} v{vid} tp={pl.tp} grid={pl.grid} mode={mode}")
             got = run(In, Ker, 1, 1, mode, plan=pl)
             assert np.array_equal(got, want), (vid, pl.tp)
+
+
+# ---- stride-2 row-band kernel: chunks, k tiles, bands, the last element -----
+SROWS_SHAPES = [
+    (2, 32, 300, 7, 28, 3, 3, 2, 2),    # Ny = 57: two k tiles (the second ragged), one band
+    (3, 16, 64, 8, 12, 3, 3, 2, 2),     # one chunk, features past Nk, two bands of 4
+    (1, 48, 256, 14, 28, 3, 3, 2, 2),   # three chunks, two bands of 7
+    (2, 16, 40, 28, 4, 3, 3, 2, 2),     # Nh = 4: rows of one 16-byte store, 4 or 7 bands
+]
+
+
+@pytest.mark.parametrize("mode", ["bf16", "bf16_obf16"])
+@pytest.mark.parametrize("shape", SROWS_SHAPES)
+def test_srows_exact(shape, mode):
+    """Every stride-2 row-band instantiation of the mode whose band divides
+    Nw: bit-exact with the oracle on integer inputs.  In's element count is
+    even and its last row's final load starts 2 bytes into a dword, so the
+    last-element patch runs."""
+    Nb, Nc, Nk, Nw, Nh, Nr, Ns, sw, sh = shape
+    rng = np.random.default_rng(sum(shape) + 29)
+    Nx, Ny = 2 * (Nw - 1) + Nr, 2 * (Nh - 1) + Ns
+    In = inputs.f32_to_bf16_bits(rng.integers(-2, 3, size=(Nb, Nc, Nx, Ny)).astype(np.float32))
+    Ker = inputs.f32_to_bf16_bits(rng.integers(-2, 3, size=(Nk, Nc, Nr, Ns)).astype(np.float32))
+    want = oracle.conv(In, Ker, 2, 2)
+    if mode == "bf16_obf16":
+        want = oracle.widen(inputs.f32_to_bf16_bits(want.astype(np.float32)))
+    dt = MODES[mode]
+    ran = 0
+    for vid, vdt, nr, ns, L in osel.SROWS:
+        if vdt != dt or (nr, ns) != (Nr, Ns) or Nw % L:
+            continue
+        pl = cnn.plan_tiles(cnn.problem(*shape), dt, cnn.K_SROWS, 256, L * Nh, 16)
+        assert pl.variant == vid and pl.grid == Nb * (Nw // L) * -(-Nk // 256)
+        say(f"[parity] srows shape={shape} v{vid} L={L} grid={pl.grid} mode={mode}")
+        got = run(In, Ker, 2, 2, mode, plan=pl)
+        assert np.array_equal(got, want), (vid, L)
+        ran += 1
+    assert ran > 0
+
+
+def test_srows_float_strided_shape():
+    """The strided 3x3 layer (64 images, 128 -> 256 channels, 28x28 outputs)
+    on uniform inputs through the row-band kernel: sampled outputs within
+    the bf16 tolerance of the fp64 oracle."""
+    w = inputs.BY_NAME["conv3x3_s2_b64"]
+    In, Ker = inputs.make_inputs(w)
+    pl = cnn.plan_tiles(cnn.problem(*w.dims()), cnn.CNN_BF16, cnn.K_SROWS, 256, 7 * w.Nh, 16)
+    say(f"[parity] srows strided v{pl.variant} tp={pl.tp} grid={pl.grid}")
+    got = run(In, Ker, 2, 2, "bf16", plan=pl)
+    rng = np.random.default_rng(6)
+    idx = np.stack([rng.integers(0, m, size=4000) for m in (w.Nb, w.Nk, w.Nw, w.Nh)], axis=1)
+    # every band's rows at both ends of a row, the feature blocks' edges
+    edge = [(b, k, y, h) for b in (0, w.Nb - 1) for k in (0, 31, 32, 63, 64, 255)
+            for y in range(w.Nw) for h in (0, 3, 4, w.Nh - 1)]
+    idx = np.unique(np.concatenate([idx, np.array(edge)]), axis=0)
+    want, absv = oracle.conv_points(In, Ker, idx, 2, 2, with_abs=True)
+    g = got[idx[:, 0], idx[:, 1], idx[:, 2], idx[:, 3]]
+    nw, cond, _ = errors(g, want, absv)
+    assert nw <= TOL["bf16"] and cond <= TOL["bf16"], (nw, cond)
