@@ -338,8 +338,12 @@ static bool eval_srows(const cnn_problem& p, int dtype, const VariantQ& v, const
     return false;
   const int64_t lds = srows_lds_bytes(v);
   if (lds > std::min<int64_t>(bud.lds_bytes, 160 * 1024)) return false;
+  // the accumulator budget is per lane at two waves per SIMD; a 4-wave
+  // workgroup (one wave per SIMD) has twice the registers
+  cnn_budget b2 = bud;
+  b2.acc_regs = bud.acc_regs * 8 / v.waves;
   return eval_tiling(p, dtype, v.id, v.tk, v.L * p.Nh, 16, v.acc, srows_slab_rows(v), lds, ws,
-                     bud, plan, time_clk);
+                     b2, plan, time_clk);
 }
 
 static void fill_common(const cnn_problem& p, int dtype, cnn_plan_t* plan) {

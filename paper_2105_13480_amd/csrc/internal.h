@@ -173,6 +173,7 @@ struct VariantQ {
   int32_t tk;
   int32_t nr, ns;  // compile-time stencil
   int32_t L;       // output rows per band
+  int32_t waves;   // 4 (one per feature pair) or 8 (two, rows split)
   int32_t acc;     // fp32 accumulators per lane
 };
 const VariantQ* variants_srows(int* count);

@@ -21,8 +21,9 @@
 // * Buffers: Ker slices four deep (the copy for stage t + 3 is issued in
 //   stage t; stage t's last K-step already reads stage t + 1's operands), In
 //   two deep by chunk (the next chunk's loads are issued in a chunk's first
-//   stage and written after its second); copies, loads and operand reads
-//   are issued between the K-steps' products; one barrier per stage.
+//   stage and written during its second); copies, loads, In writes and
+//   operand reads are issued between the K-steps' products; one barrier per
+//   stage.
 // * Waves: waves w and w+4 (one SIMD) take features 64*(w%4) .. +63 (two
 //   32-feature blocks) x the band's L rows, half of the (row, block) pairs
 //   each, with the same straight-line code for odd L too.  A 32-position
@@ -71,22 +72,24 @@ __device__ __forceinline__ void static_for(F&& f) {
 
 // TO: Out element type.  NR x NS stencil, stride 2 both ways; L output rows
 // per band.
-template <typename TO, int NR, int NS, int L>
-__global__ __launch_bounds__(512) void conv_srows(const bf16_t* __restrict__ In,
+template <typename TO, int NR, int NS, int L, int NWV>
+__global__ __launch_bounds__(64 * NWV) void conv_srows(const bf16_t* __restrict__ In,
                                                   const u32x4_t* __restrict__ Kp,
                                                   TO* __restrict__ Out, ConvArgs a,
                                                   int blk_vecs) {
-  constexpr int NT = 512;
+  constexpr int NT = 64 * NWV;
+  constexpr bool SPLIT = NWV == 8;  // two waves per feature pair (rows split)
   constexpr int TK = 256;
   constexpr int SR = NR >= 2 ? 2 * (L - 1) + NR : L;  // slab rows held per chunk
   constexpr int SX = NR >= 2 ? 1 : 2;                 // input rows per slab row
-  constexpr int RW = (L + 1) / 2;                     // rows per wave
+  constexpr int RW = SPLIT ? (L + 1) / 2 : L;         // rows per wave
   constexpr int NI = 2 * SR * 8 * 2;                  // In items per chunk
   constexpr int NIPT = (NI + NT - 1) / NT;            // items per thread
   constexpr int IN_UNITS = 2 * SR * 64;               // 16-byte units per In buffer
   constexpr int KER_UNITS = NS * 2 * TK;              // per Ker buffer (one stencil row)
   constexpr int NDK = KER_UNITS / NT;                 // copies per thread per stage
-  static_assert(L >= 2 && RW <= 4, "two row groups of at most four rows");
+  static_assert(NWV == 4 || NWV == 8, "one or two waves per feature pair");
+  static_assert(L >= 2 && RW <= (SPLIT ? 4 : 8), "rows per wave");
   static_assert(NR >= 2, "In loads one stage ahead of their LDS writes");
   static_assert(NS <= 3 && NR <= 3, "taps within one 64-unit row");
   static_assert(KER_UNITS % NT == 0, "whole copies");
@@ -99,7 +102,7 @@ __global__ __launch_bounds__(512) void conv_srows(const bf16_t* __restrict__ In,
   const int lane = tid & 63;
   const int wave = tid >> 6;
   const int fp = wave & 3;   // feature pair
-  const int rg = wave >> 2;  // row group
+  const int rg = SPLIT ? wave >> 2 : 0;  // row group
   const int l32 = lane & 31, half = lane >> 5;
 
   const int n_bands = a.Nw / L;
@@ -116,6 +119,13 @@ __global__ __launch_bounds__(512) void conv_srows(const bf16_t* __restrict__ In,
       rsrc_q(Kp, (int64_t)a.n_ktiles * n_cc * blk_vecs * 16);
   const __amdgpu_buffer_rsrc_t out_rsrc = rsrc_q(Out, a.out_total * (int64_t)sizeof(TO));
 
+  // ---- In layout: unit u (0..63) of a slab row holds column 2u (u < 32) or
+  // 2(u-32)+1; within each aligned group of 4 units it sits at slot
+  // swz(u) = 4 (u/4) + (u%4 + 2 ((u/16) % 2) + row % 2) % 4.  The rotation
+  // makes the 8-byte writes of a half wave (blocks b8 and b8 + 4, rows j and
+  // j + 1) cover all 64 banks, while any 32 consecutive units -- an operand
+  // read, whose partial end groups are 8 groups apart and rotate alike --
+  // still fall in distinct banks.
   // ---- In items: (g, slab row j, 8-column block b8, channel half hc); an
   // item is four 16-byte loads (channels 8g + 4hc + 0..3 of the chunk).
   // The range check drops a whole dword that straddles the end of In; the
@@ -126,6 +136,7 @@ __global__ __launch_bounds__(512) void conv_srows(const bf16_t* __restrict__ In,
   int in_e[NIPT];    // element offset of the item's channel 8g + 4hc of chunk 0
   int in_dst[NIPT];  // unit of its first even column (+ 8 bytes for hc = 1)
   int in_hc[NIPT];
+  int in_rot[NIPT];  // the block's slot rotation (swz)
   bool in_ok[NIPT];
 #pragma unroll
   for (int j = 0; j < NIPT; ++j) {
@@ -137,6 +148,7 @@ __global__ __launch_bounds__(512) void conv_srows(const bf16_t* __restrict__ In,
     in_e[j] = (int)((int64_t)b * a.in_img) + (8 * g + 4 * hc) * a.nxny + x * a.Ny + 8 * b8;
     in_dst[j] = (g * SR + jr) * 64 + 4 * b8;
     in_hc[j] = hc;
+    in_rot[j] = 2 * ((b8 >> 2) & 1) + (jr & 1);
     in_ok[j] = t < NI;
   }
   u32x4_t vin[NIPT][4];
@@ -149,7 +161,10 @@ __global__ __launch_bounds__(512) void conv_srows(const bf16_t* __restrict__ In,
             u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(
                          in_rsrc, (uint32_t)((in_e[j] + (16 * cc + k) * a.nxny) * 2), 0, 0));
   };
-  auto write_in = [&](int cc, u32x4_t* dstb) __attribute__((always_inline)) {
+  // Write steps [i0_, i1_) of the items' units: step i writes column pair i
+  // of the block, units 4 b8 + i (even column) and 32 + 4 b8 + i (odd
+  // column), 8 bytes each, at their swizzled slots (swz below).
+  auto write_in_part = [&](int cc, u32x4_t* dstb, int i0_, int i1_) __attribute__((always_inline)) {
     char* base = reinterpret_cast<char*>(dstb);
 #pragma unroll
     for (int j = 0; j < NIPT; ++j) {
@@ -170,17 +185,21 @@ __global__ __launch_bounds__(512) void conv_srows(const bf16_t* __restrict__ In,
       }
       char* p = base + in_dst[j] * 16 + 8 * in_hc[j];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
+      for (int i = i0_; i < i1_; ++i) {
+        const int slot = 16 * ((i + in_rot[j]) & 3);
         const u32x2_t ev = {__builtin_amdgcn_perm(v[1][i], v[0][i], 0x05040100u),
                             __builtin_amdgcn_perm(v[3][i], v[2][i], 0x05040100u)};
-        *reinterpret_cast<u32x2_t*>(p + 16 * i) = ev;
+        *reinterpret_cast<u32x2_t*>(p + slot) = ev;
         if (NS > 1) {
           const u32x2_t od = {__builtin_amdgcn_perm(v[1][i], v[0][i], 0x07060302u),
                               __builtin_amdgcn_perm(v[3][i], v[2][i], 0x07060302u)};
-          *reinterpret_cast<u32x2_t*>(p + 16 * (32 + i)) = od;
+          *reinterpret_cast<u32x2_t*>(p + 16 * 32 + slot) = od;
         }
       }
     }
+  };
+  auto write_in = [&](int cc, u32x4_t* dstb) __attribute__((always_inline)) {
+    write_in_part(cc, dstb, 0, 4);
   };
   // Ker slice (chunk cc, stencil row r) -> a Ker buffer, in NDK pieces of
   // one 16-byte copy per thread
@@ -200,14 +219,22 @@ __global__ __launch_bounds__(512) void conv_srows(const bf16_t* __restrict__ In,
   //   with block 1; wave w+4 takes rows L-1-i with block 1 and rows L-1-i,
   //   i < m, with block 0.  Row m is split between them by block, so both
   //   run the same 2*RW - 1 products per K-step, straight-line.
-  constexpr bool ODD = (L & 1) != 0;
-  const int row0 = rg == 0 ? 0 : (ODD ? L - 1 : L / 2);  // band row of i = 0
+  constexpr bool ODD = SPLIT && (L & 1) != 0;
+  const int row0 = rg == 0 ? 0 : (ODD ? L - 1 : L / 2);  // band row of i = 0 (rg = 0: 4 waves)
   const int rdir = (rg == 1 && ODD) ? -1 : 1;
   const int nbf = (rg == 1 && ODD) ? 1 : 0;               // block of the first B operand
   auto has_second = [](int i) { return !ODD || i < RW - 1; };
   // Operand offsets (units): A = In unit (half, slab row, position l32);
   // B = Ker unit (s, half, feature 64 fp + 32 nb + l32).
-  const int a_off = half * SR * 64 + l32;
+  const int a_off = half * SR * 64;
+  // swizzled unit offset of this lane's position for tap s and row parity
+  auto swz = [](int u, int par) { return (u & ~3) | (((u & 3) + 2 * ((u >> 4) & 1) + par) & 3); };
+  int a_sw[NS][2];
+#pragma unroll
+  for (int s_ = 0; s_ < NS; ++s_)
+#pragma unroll
+    for (int par = 0; par < 2; ++par)
+      a_sw[s_][par] = swz(((s_ & 1) ? 32 + (s_ >> 1) : (s_ >> 1)) + l32, par);
   const int b_first = half * TK + 64 * fp + 32 * nbf + l32;
   const int b_second = half * TK + 64 * fp + 32 * (1 - nbf) + l32;
 
@@ -223,9 +250,8 @@ __global__ __launch_bounds__(512) void conv_srows(const bf16_t* __restrict__ In,
   // unit of row i, B[p][q] = Ker unit of the wave's first / second block.
   u32x4_t A[2][RW], B[2][2];
   auto read_a = [&](const u32x4_t* ib, int r, int s, int i) __attribute__((always_inline)) {
-    const int col = (s & 1) ? 32 + (s >> 1) : (s >> 1);
     const int jr = (2 * (row0 + rdir * i) + r) / SX;
-    return ib[a_off + jr * 64 + col];
+    return ib[a_off + jr * 64 + a_sw[s][jr & 1]];
   };
   auto read_b = [&](const u32x4_t* kb, int s, int q) __attribute__((always_inline)) {
     return kb[s * 2 * TK + (q ? b_second : b_first)];
@@ -295,6 +321,8 @@ __global__ __launch_bounds__(512) void conv_srows(const bf16_t* __restrict__ In,
       auto mem = [&](int slot) __attribute__((always_inline)) {
         if (r == 0 && slot == 0) load_in_part(cn, 0, 2);
         if (r == 0 && slot == 1) load_in_part(cn, 2, 4);
+        if (r == NR - 2 && slot == 1) write_in_part(cn, ibuf + ((cc + 1) & 1) * IN_UNITS, 0, 2);
+        if (r == NR - 2 && slot == 2) write_in_part(cn, ibuf + ((cc + 1) & 1) * IN_UNITS, 2, 4);
 #pragma unroll
         for (int j = 0; j < NDK; ++j)
           if (slot == 1 + (j * NS) / NDK) copy_ker_piece(cc3, r3, kbuf + k3 * KER_UNITS, j);
@@ -304,7 +332,6 @@ __global__ __launch_bounds__(512) void conv_srows(const bf16_t* __restrict__ In,
       stage(std::integral_constant<int, (r * NS) & 1>(), ib, kb, r, nib, kbuf + k1 * KER_UNITS,
             (r + 1) % NR, mem);
       __builtin_amdgcn_sched_barrier(0);
-      if (r == NR - 2) write_in(cn, ibuf + ((cc + 1) & 1) * IN_UNITS);
       // the copy issued a stage ago (for stage + 2) has landed; this stage's
       // copies and loads may stay in flight
       if (r == 0)
@@ -400,15 +427,21 @@ __global__ __launch_bounds__(256) void pack_ker_srows(const bf16_t* __restrict__
 }
 
 // ---- instantiation table ----------------------------------------------------
-// (id, dtype, NR, NS, L): tk = 256, tc = 16, bands of L output rows.
-#define CNN_SROWS_VARIANTS(X)       \
-  X(1900, CNN_BF16, 3, 3, 7)        \
-  X(1901, CNN_BF16, 3, 3, 4)        \
-  X(2000, CNN_BF16_OBF16, 3, 3, 7)  \
-  X(2001, CNN_BF16_OBF16, 3, 3, 4)
+// (id, dtype, NR, NS, L, waves): tk = 256, tc = 16, bands of L output rows.
+// (Four waves -- one per feature pair, all L rows, accumulators in AGPRs --
+// time the same as eight on the 3x3 stride-2 layer, so only eight are built.)
+#define CNN_SROWS_VARIANTS(X)          \
+  X(1900, CNN_BF16, 3, 3, 7, 8)        \
+  X(1901, CNN_BF16, 3, 3, 4, 8)        \
+  X(2000, CNN_BF16_OBF16, 3, 3, 7, 8)  \
+  X(2001, CNN_BF16_OBF16, 3, 3, 4, 8)
 
+// acc: fp32 accumulators per lane (8 waves: 2 RW - 1 blocks for odd L, else
+// 2 RW; 4 waves: 2 L blocks, of 16 each)
 static const VariantQ kVariantsQ[] = {
-#define CNN_QV(id, dt, nr, ns, l) {id, dt, 256, nr, ns, l, 32 * ((l + 1) / 2) - 16 * (l & 1)},
+#define CNN_QV(id, dt, nr, ns, l, nw)                                                  \
+  {id, dt, 256, nr, ns, l, nw,                                                         \
+   nw == 8 ? 32 * ((l + 1) / 2) - 16 * (l & 1) : 32 * l},
     CNN_SROWS_VARIANTS(CNN_QV)
 #undef CNN_QV
 };
@@ -441,7 +474,7 @@ bool srows_fits(const VariantQ& v, const cnn_problem& p) {
          p.Nh % 4 == 0 && p.Nh <= 32 && Ny <= 64 && p.Nw % v.L == 0;
 }
 
-template <int DT, int NR, int NS, int L>
+template <int DT, int NR, int NS, int L, int NWV>
 static hipError_t launch_q(const void* In, const void* Ker, void* Out, void* ws, const ConvArgs& a,
                            int64_t lds, hipStream_t stream, const VariantQ& v) {
   typedef typename std::conditional<DT == CNN_BF16, float, bf16_t>::type TO;
@@ -449,7 +482,7 @@ static hipError_t launch_q(const void* In, const void* Ker, void* Out, void* ws,
   const int64_t threads = (int64_t)a.n_ktiles * (a.Nc / 16) * 2 * 256;
   hipLaunchKernelGGL(pack_ker_srows<NR * NS>, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0,
                      stream, (const bf16_t*)Ker, (u32x4_t*)ws, a, blk);
-  auto kern = conv_srows<TO, NR, NS, L>;
+  auto kern = conv_srows<TO, NR, NS, L, NWV>;
   static bool attr_set = false;
   if (!attr_set) {
     hipError_t e = hipFuncSetAttribute((const void*)kern,
@@ -457,7 +490,7 @@ static hipError_t launch_q(const void* In, const void* Ker, void* Out, void* ws,
     if (e != hipSuccess) return e;
     attr_set = true;
   }
-  hipLaunchKernelGGL(kern, dim3((unsigned)a.grid), dim3(512), (unsigned)lds, stream,
+  hipLaunchKernelGGL(kern, dim3((unsigned)a.grid), dim3(64 * NWV), (unsigned)lds, stream,
                      (const bf16_t*)In, (const u32x4_t*)ws, (TO*)Out, a, blk);
   return hipGetLastError();
 }
@@ -465,9 +498,9 @@ static hipError_t launch_q(const void* In, const void* Ker, void* Out, void* ws,
 hipError_t launch_srows(const VariantQ& v, const void* In, const void* Ker, void* Out, void* ws,
                         const ConvArgs& a, int64_t lds_bytes, hipStream_t stream) {
   switch (v.id) {
-#define CNN_CASEQ(id, dt, nr, ns, l) \
-  case id:                          \
-    return launch_q<dt, nr, ns, l>(In, Ker, Out, ws, a, lds_bytes, stream, v);
+#define CNN_CASEQ(id, dt, nr, ns, l, nw) \
+  case id:                              \
+    return launch_q<dt, nr, ns, l, nw>(In, Ker, Out, ws, a, lds_bytes, stream, v);
     CNN_SROWS_VARIANTS(CNN_CASEQ)
 #undef CNN_CASEQ
     default:
