@@ -54,6 +54,18 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc_r(const void* base, int64
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, n, 0x00020000);
 }
 
+// 16-byte buffer -> LDS copy: lane i's 16 bytes land at lds + 16 i (lds
+// wave-uniform); out-of-range reads give zeros.
+__device__ __forceinline__ void dma16_r(__amdgpu_buffer_rsrc_t r, void* lds, uint32_t voff) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, LDS_PTR_R(void, lds), 16, voff, 0, 0, 0);
+#else
+  (void)r;
+  (void)lds;
+  (void)voff;
+#endif
+}
+
 // Wait for this wave's LDS operations, then s_barrier; outstanding global
 // loads and stores are not waited for.
 __device__ __forceinline__ void lds_barrier_r() {
@@ -89,12 +101,19 @@ __global__ __launch_bounds__(64 * WAVES) void conv_rows(const bf16_t* __restrict
   constexpr int NTRIP = NCG * 2 * TK;                               // Ker (group, half, feature)
   constexpr int KPT = (NTRIP + NT - 1) / NT;
   constexpr int NQ = RPW + NR - 1;     // input rows a wave reads per group
+  // RAWST: the ring holds the raw Ker tile (all copies of whole 16-byte
+  // chunks), so the set-up copies it there with buffer->LDS DMA and repacks
+  // it from LDS; B-operand planes then get 2 units of padding (PST) so the
+  // repack's writes spread over the banks.
+  constexpr int KCH = (TK * ncp * RS / 8 + NT - 1) / NT;  // DMA copies per thread (at most)
+  constexpr bool RAWST = NRING * row_elems * 2 >= KCH * NT * 16;
+  constexpr int PST = RAWST ? TK + 2 : TK;  // B-operand plane stride (units)
   static_assert(NS <= 4, "a tap shift crosses at most into the partner lane");
   static_assert(WAVES % 2 == 0, "waves come in feature pairs");
 
   extern __shared__ __attribute__((aligned(16))) char smem[];
-  u32x4_t* kbuf = reinterpret_cast<u32x4_t*>(smem);  // [NCG][RS][2][TK] B operands
-  bf16_t* rows = reinterpret_cast<bf16_t*>(kbuf + NCG * RS * 2 * TK);  // [NRING][ncp][RSTR]
+  u32x4_t* kbuf = reinterpret_cast<u32x4_t*>(smem);  // [NCG][RS][2][PST] B operands
+  bf16_t* rows = reinterpret_cast<bf16_t*>(kbuf + NCG * RS * 2 * PST);  // [NRING][ncp][RSTR]
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -177,7 +196,72 @@ __global__ __launch_bounds__(64 * WAVES) void conv_rows(const bf16_t* __restrict
   // ((cg*RS + tap)*2 + g)*TK + kk holds channels 16cg + 8g .. +7 of feature
   // k0 + kk at tap (a feature's 8 channels x all taps are one 16-byte-aligned
   // run of RS 16-byte blocks).
-  {
+  if constexpr (RAWST) {
+    // The tile's raw rows Ker[k0 .. k0+63][Nc][RS] are one contiguous run
+    // of 16-byte chunks: copied into the ring by DMA, one kilobyte per wave
+    // instruction (features past Nk read as zeros).  The first group's rows
+    // and the next group's are loaded into registers meanwhile.
+    {
+      char* raw = reinterpret_cast<char*>(rows);
+      const int nch = TK * a.Nc * RS / 8;
+      const uint32_t kbase = (uint32_t)(k0 * a.Nc * RS * 2);
+      for (int q = 0; q * NT < nch; ++q)
+        dma16_r(ker_rsrc, raw + (NT * q + 64 * wave) * 16, kbase + (uint32_t)(NT * q + tid) * 16u);
+    }
+    const int nb0 = (min(WR, Lb) + NR - 1) * row_blocks;
+    u32x4_t v0[NINIT];
+    int fix0[NINIT];
+#pragma unroll
+    for (int j = 0; j < NINIT; ++j) v0[j] = load_block(y0, min(tid + NT * j, nb0 - 1), fix0[j]);
+#pragma unroll
+    for (int j = 0; j < NLD; ++j)
+      pre[j] = load_block(new_lo(1), max(0, min(tid + NT * j, new_n(1) * row_blocks - 1)), fixp[j]);
+    // the copies (issued first) have landed in every wave
+    asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(NINIT + NLD) : "memory");
+    // Repack: item (octet j, feature kk), j fastest, so a 16-lane group
+    // reads 8 octets of 2 features (runs 144 bytes / a feature apart: distinct
+    // banks) and writes 8 consecutive planes at 2 features (plane stride PST
+    // = TK + 2: distinct banks).
+    {
+      const char* raw = reinterpret_cast<const char*>(rows);
+      constexpr int NJ = 2 * NCG;  // 8-channel octets per feature
+#pragma unroll
+      for (int u = 0; u < KPT; ++u) {
+        const int tr = tid + NT * u;
+        if (tr >= NTRIP) continue;
+        const int j = tr % NJ, kk = tr / NJ;
+        const int c = 8 * j;
+        const bool ok = c < a.Nc && k0 + kk < a.Nk;
+        const u32x4_t* rp =
+            reinterpret_cast<const u32x4_t*>(raw + (ok ? (kk * a.Nc + c) * RS * 2 : 0));
+        u32x4_t run[RS];
+#pragma unroll
+        for (int q = 0; q < RS; ++q) run[q] = rp[q];
+        const int dst = ((j >> 1) * RS * 2 + (j & 1)) * PST + kk;
+#pragma unroll
+        for (int tap = 0; tap < RS; ++tap) {
+          u32x4_t v;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int e0 = (2 * i) * RS + tap, e1 = e0 + RS;
+            const uint32_t sel = ((e0 & 1) ? 0x0302u : 0x0100u) |
+                                 ((e1 & 1) ? 0x07060000u : 0x05040000u);
+            const uint32_t w1 = run[(e1 >> 1) >> 2][(e1 >> 1) & 3];
+            const uint32_t w0 = run[(e0 >> 1) >> 2][(e0 >> 1) & 3];
+            v[i] = ok ? __builtin_amdgcn_perm(w1, w0, sel) : 0u;
+          }
+          kbuf[dst + tap * 2 * PST] = v;
+        }
+      }
+    }
+    // every wave is done with the raw tile before rows overwrite it
+    lds_barrier_r();
+#pragma unroll
+    for (int j = 0; j < NINIT; ++j) {
+      const int f = tid + NT * j;
+      if (f < nb0) store_block(y0, f, v0[j], fix0[j]);
+    }
+  } else   {
     u32x4_t run[KPT][RS];
     bool ok[KPT];
 #pragma unroll
@@ -243,7 +327,7 @@ __global__ __launch_bounds__(64 * WAVES) void conv_rows(const bf16_t* __restrict
   const int G = lane >> 4, li = lane & 15;
   const int aoff0 = (8 * (G >> 1) + (li >> 2)) * RSTR + 16 * (G & 1) + 4 * (li & 3);
   const int aoff1 = aoff0 + 4 * RSTR;
-  const u32x4_t* kwave = kbuf + half * TK + wk * 32 + l32;
+  const u32x4_t* kwave = kbuf + half * PST + wk * 32 + l32;
 
   const int n = k0 + wk * 32 + l32;  // this lane's output feature
   const bool nv = n < a.Nk;
@@ -310,7 +394,7 @@ __global__ __launch_bounds__(64 * WAVES) void conv_rows(const bf16_t* __restrict
           const u32x2_t hi = read_tr16(rp + aoff1 + 32 * mb);
           A[mb] = u32x4_t{lo[0], lo[1], hi[0], hi[1]};
         }
-        const u32x4_t* kp = kwave + cg * RS * 2 * TK;
+        const u32x4_t* kp = kwave + cg * RS * 2 * PST;
 #pragma unroll
         for (int r = 0; r < NR; ++r) {
           bool used = false;
@@ -318,7 +402,7 @@ __global__ __launch_bounds__(64 * WAVES) void conv_rows(const bf16_t* __restrict
           for (int j = 0; j < RPW; ++j) used |= (q - j == r);
           if (!used) continue;  // compile-time
 #pragma unroll
-          for (int s = 0; s < NS; ++s) B[r][s] = kp[(r * NS + s) * 2 * TK];
+          for (int s = 0; s < NS; ++s) B[r][s] = kp[(r * NS + s) * 2 * PST];
         }
       };
       auto multiply_step = [&](int t, const u32x4_t (&A)[MB], const u32x4_t (&B)[NR][NS])
@@ -494,9 +578,12 @@ const VariantR* variants_rows(int* count) {
 int64_t rows_ncp(const cnn_problem& p) { return (p.Nc + 15) / 16 * 16; }
 
 int64_t rows_lds_bytes(const VariantR& v, const cnn_problem& p) {
-  const int64_t ncp = rows_ncp(p);
-  const int64_t ker = (ncp / 16) * v.nr * v.ns * 2 * v.tk * 16;
+  // (the kernel's NCG fixes ncp; RAWST and PST as in conv_rows)
+  const int64_t ncp = 16 * v.ncg, nt = 64 * v.waves, rs = v.nr * v.ns;
   const int64_t ring = (2 * v.wr + v.nr - 1) * ncp * 32 * v.mb * 2;
+  const int64_t kch = (v.tk * ncp * rs / 8 + nt - 1) / nt;
+  const int64_t pst = ring >= kch * nt * 16 ? v.tk + 2 : v.tk;
+  const int64_t ker = (ncp / 16) * rs * 2 * pst * 16;
   return ker + ring;
 }
 
