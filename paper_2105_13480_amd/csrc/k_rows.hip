@@ -423,6 +423,9 @@ __global__ __launch_bounds__(64 * WAVES) void conv_rows(const bf16_t* __restrict
       };
       // (VEC: the previous group's chunks go out a few per step)
       constexpr int CPS = (RPW * NCHUNK + NSTEP - 1) / NSTEP;
+      // The next group's rows (loaded a group ago) go to ring slots no wave
+      // reads in this group, one block per step between the products.
+      const int nb_next = new_n(gi + 1) * row_blocks;
       u32x4_t A[2][MB], B[2][NR][NS];
       read_step(0, A[0], B[0]);
 #pragma unroll
@@ -437,24 +440,20 @@ __global__ __launch_bounds__(64 * WAVES) void conv_rows(const bf16_t* __restrict
             if (c < RPW * NCHUNK) store_chunk(c / NCHUNK, c % NCHUNK);
           }
         }
+#pragma unroll
+        for (int j = 0; j < NLD; ++j) {
+          if ((j * NSTEP) / NLD != t) continue;  // compile-time
+          const int f = tid + NT * j;
+          if (f < nb_next) store_block(new_lo(gi + 1), f, pre[j], fixp[j]);
+        }
         __builtin_amdgcn_sched_barrier(0);
       }
     }
 
-    // The next group's rows (loaded a group ago) go to ring slots no wave
-    // reads in this group; then the loads of the group after it are issued,
-    // before this group's stores.  Every batch is issued and consumed
-    // whole, past the last group too (clamped, in-range loads whose blocks
-    // are not written), so the code is straight-line and each wait counts
-    // exactly the loads it needs.
-    {
-      const int nb = new_n(gi + 1) * row_blocks;
-#pragma unroll
-      for (int j = 0; j < NLD; ++j) {
-        const int f = tid + NT * j;
-        if (f < nb) store_block(new_lo(gi + 1), f, pre[j], fixp[j]);
-      }
-    }
+    // Then the loads of the group after it are issued, before this group's
+    // stores.  Every batch is issued and consumed whole, past the last group
+    // too (clamped, in-range loads whose blocks are not written), so the
+    // code is straight-line and each wait counts exactly the loads it needs.
 #pragma unroll
     for (int j = 0; j < NLD; ++j)
       pre[j] = load_block(new_lo(gi + 2),
