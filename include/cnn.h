@@ -108,10 +108,11 @@ typedef enum cnn_kernel {
                          a ring of row buffers and read with transposing LDS
                          reads; fixed 3x3 or 1x1, Nc % 8 == 0, Ny <= 64; tc of
                          its plans is Nc                                          */
-  CNN_K_GEMM1 = 11,   /* 1x1 stride-1 layers as a per-pixel GEMM, bf16: In channel
-                         rows read by transposing LDS reads, Ker rows as they lie,
-                         both double-buffered in LDS; Nc % 8 == 0, Nw*Nh and tp
-                         multiples of 4                                           */
+  CNN_K_GEMM1 = 11,   /* 1x1 layers as a per-pixel GEMM, bf16: In channel rows
+                         read by transposing LDS reads, Ker rows as they lie,
+                         both double-buffered in LDS; Nc % 8 == 0, tp a multiple
+                         of 4; strides 1 (Nw*Nh % 4 == 0) or 2 and 2 (Nh % 4 ==
+                         0: 4 output pixels = the even half of 8 input columns) */
   CNN_K_SROWS = 12    /* stride-2 layers over bands of whole output rows, bf16:
                          256 features x L rows per workgroup, In rows split by
                          column parity into MFMA-ready LDS units, Ker repacked

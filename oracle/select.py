@@ -157,12 +157,15 @@ ROWS = [
 ]
 
 
-# (id, dtype, wp, wk, mbp, nbk, tc) of the 1x1 stride-1 GEMM kernel: tk =
-# 32*wk*nbk, tp <= 32*wp*mbp (a multiple of 4, as are Nw*Nh), Nc % 8 == 0.
-# Taken only when requested (not ranked by `choose`).
+# (id, dtype, wp, wk, mbp, nbk, tc, s2) of the 1x1 GEMM kernel: tk =
+# 32*wk*nbk, tp <= 32*wp*mbp (a multiple of 4), Nc % 8 == 0; s2 = 0: strides
+# 1 and Nw*Nh % 4 == 0; s2 = 1: strides 2 and 2, Nh % 4 == 0.  Taken only
+# when requested (not ranked by `choose`).
 GEMM1 = [
-    (1700, BF16, 2, 4, 4, 2, 64), (1701, BF16, 4, 2, 2, 2, 64),
-    (1800, BF16_OBF16, 2, 4, 4, 2, 64), (1801, BF16_OBF16, 4, 2, 2, 2, 64),
+    (1700, BF16, 2, 4, 4, 2, 64, 0), (1701, BF16, 4, 2, 2, 2, 64, 0),
+    (1702, BF16, 2, 4, 4, 2, 32, 1),
+    (1800, BF16_OBF16, 2, 4, 4, 2, 64, 0), (1801, BF16_OBF16, 4, 2, 2, 2, 64, 0),
+    (1802, BF16_OBF16, 2, 4, 4, 2, 32, 1),
 ]
 
 

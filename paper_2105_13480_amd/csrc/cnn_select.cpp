@@ -315,7 +315,8 @@ static bool eval_gemm1(const cnn_problem& p, int dtype, const VariantG& v, const
                        cnn_plan_t* plan, double* time_clk) {
   const int64_t lds = gemm1_lds_bytes(v);
   if (lds > std::min<int64_t>(bud.lds_bytes, 160 * 1024)) return false;
-  if (p.Nb * p.Nc * p.Nw * p.Nh * 2 >= (1LL << 30) || p.Nk * p.Nc * 2 >= (1LL << 30) ||
+  const int64_t Nx = p.sw * (p.Nw - 1) + 1, Ny = p.sh * (p.Nh - 1) + 1;
+  if (p.Nb * p.Nc * Nx * Ny * 2 >= (1LL << 30) || p.Nk * p.Nc * 2 >= (1LL << 30) ||
       p.Nb * p.Nk * p.Nw * p.Nh * out_bytes(dtype) >= (1LL << 31))
     return false;
   const int64_t occ = std::max<int64_t>(1, std::min<int64_t>(bud.wg_per_cu, bud.lds_bytes / lds));

@@ -158,6 +158,7 @@ struct VariantG {
   int32_t tk, tp, tc;  // tp = largest tile
   int32_t threads;
   int32_t acc;
+  int32_t s2;          // 1: strides 2 and 2 (gathers the even input rows and columns)
 };
 const VariantG* variants_gemm1(int* count);
 int64_t gemm1_lds_bytes(const VariantG& v);

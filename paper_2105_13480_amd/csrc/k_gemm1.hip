@@ -55,7 +55,11 @@ __device__ __forceinline__ void lds_barrier_g() {
 
 // TO: Out element type.  WP x WK waves: WP pixel groups of MBP 32-pixel
 // blocks, WK feature groups of NBK 32-feature blocks.  TC: channels per stage.
-template <typename TO, int WP, int WK, int MBP, int NBK, int TC>
+// S2: strides 2 and 2 (Out pixel (w, h) reads In (2w, 2h)): a 4-pixel chunk
+// is the even elements of one unaligned 16-byte load (8 input columns),
+// picked with v_perm when the chunk is written to LDS; chunks never cross
+// an output row (Nh % 4 == 0).
+template <typename TO, int WP, int WK, int MBP, int NBK, int TC, bool S2>
 __global__ __launch_bounds__(64 * WP * WK) void conv_gemm1(const bf16_t* __restrict__ In,
                                                           const bf16_t* __restrict__ Ker,
                                                           TO* __restrict__ Out, ConvArgs a) {
@@ -110,7 +114,12 @@ __global__ __launch_bounds__(64 * WP * WK) void conv_gemm1(const bf16_t* __restr
     const bool ok = tid + NT * j < TC * NQ && 4 * q < tp;
     const int pc = ok ? p : p0;
     const int b = pc / a.hw;
-    in_off[j] = b * (int)a.in_img + (pc - b * a.hw);  // < in_total < 2^30
+    if constexpr (S2) {
+      const int rem = pc - b * a.hw, w = rem / a.Nh;
+      in_off[j] = b * (int)a.in_img + 2 * w * a.Ny + 2 * (rem - w * a.Nh);
+    } else {
+      in_off[j] = b * (int)a.in_img + (pc - b * a.hw);  // < in_total < 2^30
+    }
     in_c[j] = c;
     in_ok[j] = ok ? ~0u : 0u;
     in_dst[j] = c * RSI + 4 * q;
@@ -129,16 +138,27 @@ __global__ __launch_bounds__(64 * WP * WK) void conv_gemm1(const bf16_t* __restr
     ker_dst[j] = n * RSK + 8 * cb;
   }
 
-  u32x2_t vin[NIN];
+  typedef typename std::conditional<S2, u32x4_t, u32x2_t>::type vin_t;
+  vin_t vin[NIN];
   u32x4_t vker[NKER];
+  // S2: the range check drops a whole dword that straddles the end of In;
+  // the only needed element such a dword can hold is In's last, loaded once
+  // and patched in when its chunk is written.
+  const uint32_t in_last =
+      S2 ? __builtin_amdgcn_raw_buffer_load_b16(in_rsrc, (uint32_t)((a.in_total - 1) * 2), 0, 0) : 0u;
   auto load_stage = [&](int s) __attribute__((always_inline)) {
     const int c0 = s * TC;
 #pragma unroll
     for (int j = 0; j < NIN; ++j) {
       const int c = min(c0 + in_c[j], a.Nc - 1);
-      vin[j] = __builtin_bit_cast(
-          u32x2_t, __builtin_amdgcn_raw_buffer_load_b64(
-                       in_rsrc, (uint32_t)((in_off[j] + c * a.hw) * 2), 0, 0));
+      if constexpr (S2)
+        vin[j] = __builtin_bit_cast(
+            u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(
+                         in_rsrc, (uint32_t)((in_off[j] + c * a.nxny) * 2), 0, 0));
+      else
+        vin[j] = __builtin_bit_cast(
+            u32x2_t, __builtin_amdgcn_raw_buffer_load_b64(
+                         in_rsrc, (uint32_t)((in_off[j] + c * a.hw) * 2), 0, 0));
     }
 #pragma unroll
     for (int j = 0; j < NKER; ++j) {
@@ -155,8 +175,21 @@ __global__ __launch_bounds__(64 * WP * WK) void conv_gemm1(const bf16_t* __restr
 #pragma unroll
     for (int j = 0; j < NIN; ++j) {
       const uint32_t keep = (c0 + in_c[j] < a.Nc) ? in_ok[j] : 0u;
+      u32x2_t v;
+      if constexpr (S2) {
+        v = u32x2_t{__builtin_amdgcn_perm(vin[j][1], vin[j][0], 0x05040100u),
+                    __builtin_amdgcn_perm(vin[j][3], vin[j][2], 0x05040100u)};
+        const int d = (int)(a.in_total - 1) - (in_off[j] + min(c0 + in_c[j], a.Nc - 1) * a.nxny);
+        if (d >= 0 && d < 8 && (d & 1) == 0) {  // rare: In's last element, kept element d/2
+          const int kq = d >> 1;
+          const uint32_t w = v[kq >> 1];
+          v[kq >> 1] = (kq & 1) ? ((w & 0xffffu) | (in_last << 16)) : ((w & 0xffff0000u) | in_last);
+        }
+      } else {
+        v = vin[j];
+      }
       if (tid + NT * j < TC * NQ)
-        *reinterpret_cast<u32x2_t*>(ib + in_dst[j]) = u32x2_t{vin[j][0] & keep, vin[j][1] & keep};
+        *reinterpret_cast<u32x2_t*>(ib + in_dst[j]) = u32x2_t{v[0] & keep, v[1] & keep};
     }
 #pragma unroll
     for (int j = 0; j < NKER; ++j) {
@@ -263,14 +296,16 @@ __global__ __launch_bounds__(64 * WP * WK) void conv_gemm1(const bf16_t* __restr
 // (id, dtype, WP, WK, MBP, NBK, TC): tk = 32*WK*NBK, tp <= 32*WP*MBP,
 // 64*WP*WK threads.
 #define CNN_GEMM1_VARIANTS(X)                  \
-  X(1700, CNN_BF16, 2, 4, 4, 2, 64)            \
-  X(1701, CNN_BF16, 4, 2, 2, 2, 64)            \
-  X(1800, CNN_BF16_OBF16, 2, 4, 4, 2, 64)      \
-  X(1801, CNN_BF16_OBF16, 4, 2, 2, 2, 64)
+  X(1700, CNN_BF16, 2, 4, 4, 2, 64, 0)         \
+  X(1701, CNN_BF16, 4, 2, 2, 2, 64, 0)         \
+  X(1702, CNN_BF16, 2, 4, 4, 2, 32, 1)         \
+  X(1800, CNN_BF16_OBF16, 2, 4, 4, 2, 64, 0)   \
+  X(1801, CNN_BF16_OBF16, 4, 2, 2, 2, 64, 0)   \
+  X(1802, CNN_BF16_OBF16, 2, 4, 4, 2, 32, 1)
 
 static const VariantG kVariantsG[] = {
-#define CNN_GV(id, dt, wp, wk, mbp, nbk, tc) \
-  {id, dt, 32 * wk * nbk, 32 * wp * mbp, tc, 64 * wp * wk, 16 * mbp * nbk},
+#define CNN_GV(id, dt, wp, wk, mbp, nbk, tc, s2) \
+  {id, dt, 32 * wk * nbk, 32 * wp * mbp, tc, 64 * wp * wk, 16 * mbp * nbk, s2},
     CNN_GEMM1_VARIANTS(CNN_GV)
 #undef CNN_GV
 };
@@ -285,16 +320,18 @@ int64_t gemm1_lds_bytes(const VariantG& v) {
 }
 
 bool gemm1_fits(const VariantG& v, const cnn_problem& p, int64_t tp) {
-  (void)v;
+  if (v.s2)
+    return p.Nr == 1 && p.Ns == 1 && p.sw == 2 && p.sh == 2 && p.Nc % 8 == 0 && p.Nh % 4 == 0 &&
+           tp % 4 == 0 && tp >= 4;
   return p.Nr == 1 && p.Ns == 1 && p.sw == 1 && p.sh == 1 && p.Nc % 8 == 0 &&
          (p.Nw * p.Nh) % 4 == 0 && tp % 4 == 0 && tp >= 4;
 }
 
-template <int DT, int WP, int WK, int MBP, int NBK, int TC>
+template <int DT, int WP, int WK, int MBP, int NBK, int TC, int S2>
 static hipError_t launch_g(const void* In, const void* Ker, void* Out, const ConvArgs& a,
                            int64_t lds, hipStream_t stream) {
   typedef typename std::conditional<DT == CNN_BF16, float, bf16_t>::type TO;
-  auto kern = conv_gemm1<TO, WP, WK, MBP, NBK, TC>;
+  auto kern = conv_gemm1<TO, WP, WK, MBP, NBK, TC, S2 != 0>;
   static bool attr_set = false;
   if (!attr_set) {
     hipError_t e = hipFuncSetAttribute((const void*)kern,
@@ -310,9 +347,9 @@ static hipError_t launch_g(const void* In, const void* Ker, void* Out, const Con
 hipError_t launch_gemm1(const VariantG& v, const void* In, const void* Ker, void* Out,
                         const ConvArgs& a, int64_t lds_bytes, hipStream_t stream) {
   switch (v.id) {
-#define CNN_CASEG(id, dt, wp, wk, mbp, nbk, tc) \
-  case id:                                     \
-    return launch_g<dt, wp, wk, mbp, nbk, tc>(In, Ker, Out, a, lds_bytes, stream);
+#define CNN_CASEG(id, dt, wp, wk, mbp, nbk, tc, s2) \
+  case id:                                         \
+    return launch_g<dt, wp, wk, mbp, nbk, tc, s2>(In, Ker, Out, a, lds_bytes, stream);
     CNN_GEMM1_VARIANTS(CNN_CASEG)
 #undef CNN_CASEG
     default:

@@ -93,9 +93,10 @@ def variant_dims(kernel, vid, dt, tk, tp, tc, stencil):
         except cnn.CnnError:
             return None
         return dims if pl.variant == vid else None
-    if kernel == cnn.K_GEMM1:  # 1x1 stride 1, Nw*Nh % 4 == 0, Nc % 8 == 0
+    if kernel == cnn.K_GEMM1:  # 1x1, Nc % 8 == 0; stride 1 (Nw*Nh % 4 == 0) or 2 (Nh % 4 == 0)
         cands = [(3, tc + 8, tk + 7, 6, 10, 1, 1, 1, 1), (2, 2 * tc + 16, tk - 5, 8, 14, 1, 1, 1, 1),
-                 (1, 24, tk + 7, 4, 5, 1, 1, 1, 1)]
+                 (1, 24, tk + 7, 4, 5, 1, 1, 1, 1), (3, tc + 8, tk + 7, 6, 8, 1, 1, 2, 2),
+                 (2, 2 * tc + 16, tk - 5, 7, 12, 1, 1, 2, 2)]
         for dims in cands:
             try:
                 pl = cnn.plan_tiles(cnn.problem(*dims), dt, kernel, tk, tp, tc, cnn.budget())
@@ -165,7 +166,7 @@ def variant_cases():
                     (nr, ns) if nr else ((1, 1) if vid % 100 in (10, 11, 12) else (5, 2))))
     for vid, dt, wm, wn, mb, nb, tc, nr, ns, kres, _, _ in osel.STREAM:
         out.append((cnn.K_STREAM, vid, dt, 32 * wm * mb, 32 * wn * nb, tc, (nr, ns)))
-    for vid, dt, wp, wk, mbp, nbk, tc in osel.GEMM1:
+    for vid, dt, wp, wk, mbp, nbk, tc, _ in osel.GEMM1:
         out.append((cnn.K_GEMM1, vid, dt, 32 * wk * nbk, 32 * wp * mbp, tc, (1, 1)))
     for vid, dt, nr, ns, L in osel.SROWS:
         out.append((cnn.K_SROWS, vid, dt, 256, 0, 16, (nr, ns)))

@@ -329,8 +329,8 @@ def test_gemm1_exact(shape, mode):
     if mode == "bf16_obf16":
         want = oracle.widen(inputs.f32_to_bf16_bits(want.astype(np.float32)))
     dt = MODES[mode]
-    for vid, vdt, wp, wk, mbp, nbk, tc in osel.GEMM1:
-        if vdt != dt:
+    for vid, vdt, wp, wk, mbp, nbk, tc, s2 in osel.GEMM1:
+        if vdt != dt or s2:
             continue
         tk, tpmax = 32 * wk * nbk, 32 * wp * mbp
         for cus in (256, 3):  # balanced tile; few slots -> the largest tile
@@ -399,3 +399,45 @@ def test_srows_float_strided_shape():
     g = got[idx[:, 0], idx[:, 1], idx[:, 2], idx[:, 3]]
     nw, cond, _ = errors(g, want, absv)
     assert nw <= TOL["bf16"] and cond <= TOL["bf16"], (nw, cond)
+
+
+# ---- 1x1 GEMM kernel, strides 2 and 2: the even input rows and columns -----
+GEMM1_S2_SHAPES = [
+    (3, 72, 71, 6, 8, 1, 1, 2, 2),      # In 11x15 (odd rows: unaligned loads), two stages
+    (2, 64, 300, 4, 4, 1, 1, 2, 2),     # two k tiles of 256, 16-pixel images
+    (5, 40, 130, 7, 12, 1, 1, 2, 2),    # 84-pixel images, tiles span images
+    (1, 256, 64, 28, 28, 1, 1, 2, 2),   # one 784-pixel image, In 55x55
+    (2, 24, 40, 6, 4, 1, 1, 2, 2),      # Nc < one stage
+]
+
+
+@pytest.mark.parametrize("mode", ["bf16", "bf16_obf16"])
+@pytest.mark.parametrize("shape", GEMM1_S2_SHAPES)
+def test_gemm1_stride2_exact(shape, mode):
+    """Every stride-2 1x1 GEMM instantiation of the mode, at its balanced
+    tile and at the largest: bit-exact with the oracle on integer inputs
+    (In's element count is even and its last element sits in the second
+    half of a straddling dword in the last-row cases, so the patch runs)."""
+    Nb, Nc, Nk, Nw, Nh, Nr, Ns, sw, sh = shape
+    rng = np.random.default_rng(sum(shape) + 13)
+    Nx, Ny = 2 * Nw - 1, 2 * Nh - 1
+    In = inputs.f32_to_bf16_bits(rng.integers(-2, 3, size=(Nb, Nc, Nx, Ny)).astype(np.float32))
+    Ker = inputs.f32_to_bf16_bits(rng.integers(-2, 3, size=(Nk, Nc, 1, 1)).astype(np.float32))
+    want = oracle.conv(In, Ker, 2, 2)
+    if mode == "bf16_obf16":
+        want = oracle.widen(inputs.f32_to_bf16_bits(want.astype(np.float32)))
+    dt = MODES[mode]
+    ran = 0
+    for vid, vdt, wp, wk, mbp, nbk, tc, s2 in osel.GEMM1:
+        if vdt != dt or not s2:
+            continue
+        tk, tpmax = 32 * wk * nbk, 32 * wp * mbp
+        for cus in (256, 3):
+            pl = cnn.plan_tiles(cnn.problem(*shape), dt, cnn.K_GEMM1, tk, tpmax, tc,
+                                cnn.budget(cus, 160 * 1024, 128, 2))
+            assert pl.variant == vid and pl.tp % 4 == 0
+            say(f"[parity] gemm1 s2 shape={shape} v{vid} tp={pl.tp} grid={pl.grid} mode={mode}")
+            got = run(In, Ker, 2, 2, mode, plan=pl)
+            assert np.array_equal(got, want), (vid, pl.tp)
+            ran += 1
+    assert ran > 0
