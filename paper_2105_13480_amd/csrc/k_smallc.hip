@@ -14,8 +14,15 @@
 //   [K-step][lane half][feature][8] -- one 16-byte read per operand.
 // * In (B operand): the tile's halo'd slab -- every input row the tile's
 //   outputs touch, all Nc channels -- staged once in its natural layout
-//   (row stride Ny + 8, zero padding), and each operand gathered with eight
-//   16-bit LDS reads at the lane's output position plus the (c, r) offset.
+//   (row stride Ny + 8 rounded up to 8, columns past Ny zero) by unaligned
+//   16-byte loads of 8 columns, and each operand gathered at the lane's
+//   output position plus the (c, r) offset: eight 16-bit LDS reads, or four
+//   32-bit reads when the h stride is 2 (the position is then even).
+// * Ker runs (Ns <= 8 taps of one (k, c, r)) are one unaligned 16-byte load
+//   each, the taps past Ns masked to zero.
+// * A 16-byte load whose last dword straddles the end of its tensor loses
+//   that dword to the range check; the only element that matters there is
+//   the tensor's last, loaded once and patched in.
 // * One tile per workgroup and several workgroups per CU: a workgroup's
 //   Out stores (the dominant HBM traffic of such layers) overlap other
 //   workgroups' staging and MFMA work.
@@ -32,8 +39,9 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc_s(const void* base, int64
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, n, 0x00020000);
 }
 
-// KS: largest number of K-steps (ceil(Nc*Nr/2)) the registers hold.
-template <typename TO, int NB, int KS>
+// KS: largest number of K-steps (ceil(Nc*Nr/2)) the registers hold.  SH2:
+// sh == 2 (operands gathered with 32-bit LDS reads).
+template <typename TO, int NB, int KS, bool SH2>
 __global__ __launch_bounds__(256) void conv_smallc(const bf16_t* __restrict__ In,
                                                    const bf16_t* __restrict__ Ker,
                                                    TO* __restrict__ Out, ConvArgs a) {
@@ -60,7 +68,7 @@ __global__ __launch_bounds__(256) void conv_smallc(const bf16_t* __restrict__ In
   const int b1 = plast / a.hw, w1 = (plast - b1 * a.hw) / a.Nh;
   const int G0 = b0 * a.Nx + a.sw * w0;                    // first slab row (flattened b, x)
   const int S = b1 * a.Nx + a.sw * w1 + a.Nr - G0;         // slab rows
-  const int RSTR = a.Ny + 8;                               // LDS row stride (elements)
+  const int RSTR = (a.Ny + 15) & ~7;                       // LDS row stride (elements)
   const int nq = a.Nc * a.Nr;                              // (c, r) rows of the stencil
   const int nks = (nq + 1) >> 1;                           // K-steps
 
@@ -68,62 +76,92 @@ __global__ __launch_bounds__(256) void conv_smallc(const bf16_t* __restrict__ In
   // (c, r) row q = 2j + h, zero past Ns, nq or Nk.  All of a thread's
   // loads are issued before any is used.
   {
-    const __amdgpu_buffer_rsrc_t kr = rsrc_s(Ker, (int64_t)a.Nk * a.Nc * a.Nr * a.Ns * 2);
+    const int64_t ker_total = (int64_t)a.Nk * a.Nc * a.Nr * a.Ns;
+    const __amdgpu_buffer_rsrc_t kr = rsrc_s(Ker, ker_total * 2);
+    const uint32_t ker_last =
+        __builtin_amdgcn_raw_buffer_load_b16(kr, (uint32_t)((ker_total - 1) * 2), 0, 0);
     constexpr int PER = KVEC / 256;
-    uint32_t e[PER][8];
+    u32x4_t e[PER];
+    int ebase[PER];
+    bool eok[PER];
 #pragma unroll
     for (int u = 0; u < PER; ++u) {
       const int v = tid + 256 * u;
       const int kk = v % TK;
       const int jh = v / TK;  // 2j + h == q
       const int k = k0 + kk;
-      const bool qv = k < a.Nk && jh < nq;
-      const int q = qv ? jh : 0;
+      eok[u] = k < a.Nk && jh < nq;
+      const int q = eok[u] ? jh : 0;
       const int c = q / a.Nr, r = q - (q / a.Nr) * a.Nr;
-      const uint32_t base =
-          (uint32_t)((((int64_t)(qv ? k : 0) * a.Nc + c) * a.Nr + r) * a.Ns * 2);
-#pragma unroll
-      for (int s = 0; s < 8; ++s)
-        e[u][s] = (qv && s < a.Ns) ? __builtin_amdgcn_raw_buffer_load_b16(kr, base + 2 * s, 0, 0)
-                                   : 0u;
+      ebase[u] = (((eok[u] ? k : 0) * a.Nc + c) * a.Nr + r) * a.Ns;
+      e[u] = __builtin_bit_cast(
+          u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(kr, (uint32_t)(ebase[u] * 2), 0, 0));
     }
 #pragma unroll
     for (int u = 0; u < PER; ++u) {
-      u32x4_t vv;
+      u32x4_t vv = e[u];
+      const int d = (int)(ker_total - 1) - ebase[u];
 #pragma unroll
-      for (int d = 0; d < 4; ++d) vv[d] = e[u][2 * d] | (e[u][2 * d + 1] << 16);
+      for (int t = 0; t < 8; t += 2) {
+        // taps t, t+1 of the run: zero past Ns (and for invalid vectors);
+        // the tensor's last element patched in
+        uint32_t w = vv[t >> 1];
+        if (d == t) w = (w & 0xffff0000u) | ker_last;
+        if (d == t + 1) w = (w & 0xffffu) | (ker_last << 16);
+        const uint32_t keep = (eok[u] ? (t < a.Ns ? 0xffffu : 0u) | (t + 1 < a.Ns ? 0xffff0000u : 0u)
+                                      : 0u);
+        vv[t >> 1] = w & keep;
+      }
       kimg[tid + 256 * u] = vv;
     }
   }
 
   // Stage the slab: element (c, row, col) of the LDS image is
-  // In[b][c][x][col] for flattened input row G0 + row = b*Nx + x; the 8
-  // padding columns are zero.  Batches of 16 independent loads per thread.
+  // In[b][c][x][col] for flattened input row G0 + row = b*Nx + x, zero for
+  // col >= Ny.  Chunk (c, row, k8) = columns 8 k8 .. +7, one unaligned
+  // 16-byte load; batches of U independent loads per thread.
   {
     const __amdgpu_buffer_rsrc_t ir = rsrc_s(In, a.in_total * 2);
-    const int n = a.Nc * S * RSTR;
-    constexpr int U = 16;
+    const uint32_t in_last =
+        __builtin_amdgcn_raw_buffer_load_b16(ir, (uint32_t)((a.in_total - 1) * 2), 0, 0);
+    const int cpr = RSTR / 8;  // chunks per slab row
+    const int n = a.Nc * S * cpr;
+    constexpr int U = 4;
     for (int e0 = 0; e0 < n; e0 += 256 * U) {
-      uint32_t v[U];
+      u32x4_t v[U];
+      int off[U];
 #pragma unroll
       for (int u = 0; u < U; ++u) {
-        const int e = e0 + tid + 256 * u;
-        const int c = e / (S * RSTR);
-        const int rem = e - c * (S * RSTR);
-        const int row = rem / RSTR;
-        const int col = rem - row * RSTR;
+        const int e = min(e0 + tid + 256 * u, n - 1);
+        const int crow = e / cpr;
+        const int k8 = e - crow * cpr;
+        const int c = crow / S;
+        const int row = crow - c * S;
         const int gr = G0 + row;
         const int b = gr / a.Nx;
         const int x = gr - b * a.Nx;
-        const int64_t off =
-            (int64_t)b * a.in_img + (int64_t)c * a.nxny + (int64_t)x * a.Ny + col;
-        const bool ok = e < n && col < a.Ny;
-        v[u] = ok ? __builtin_amdgcn_raw_buffer_load_b16(ir, (uint32_t)(off * 2), 0, 0) : 0u;
+        off[u] = (int)((int64_t)b * a.in_img + (int64_t)c * a.nxny + (int64_t)x * a.Ny) + 8 * k8;
+        v[u] = __builtin_bit_cast(
+            u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(ir, (uint32_t)(off[u] * 2), 0, 0));
       }
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int e = e0 + tid + 256 * u;
-        if (e < n) slab[e] = (bf16_t)v[u];
+        if (e >= n) continue;
+        const int crow = e / cpr;
+        const int k8 = e - crow * cpr;
+        const int d = (int)(a.in_total - 1) - off[u];
+        u32x4_t vv = v[u];
+#pragma unroll
+        for (int t = 0; t < 8; t += 2) {
+          uint32_t w = vv[t >> 1];
+          if (d == t) w = (w & 0xffff0000u) | in_last;
+          if (d == t + 1) w = (w & 0xffffu) | (in_last << 16);
+          const int col = 8 * k8 + t;
+          const uint32_t keep = (col < a.Ny ? 0xffffu : 0u) | (col + 1 < a.Ny ? 0xffff0000u : 0u);
+          vv[t >> 1] = w & keep;
+        }
+        *reinterpret_cast<u32x4_t*>(slab + crow * RSTR + 8 * k8) = vv;
       }
     }
   }
@@ -163,9 +201,15 @@ __global__ __launch_bounds__(256) void conv_smallc(const bf16_t* __restrict__ In
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) {
         const bf16_t* src = slab + qoff + pbase[nb];
+        if constexpr (SH2) {
+          // the position's first column is even: 4-byte-aligned words
 #pragma unroll
-        for (int d = 0; d < 4; ++d)
-          bv[nb][d] = (uint32_t)src[2 * d] | ((uint32_t)src[2 * d + 1] << 16);
+          for (int d = 0; d < 4; ++d) bv[nb][d] = reinterpret_cast<const uint32_t*>(src)[d];
+        } else {
+#pragma unroll
+          for (int d = 0; d < 4; ++d)
+            bv[nb][d] = (uint32_t)src[2 * d] | ((uint32_t)src[2 * d + 1] << 16);
+        }
       }
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb) {
@@ -231,20 +275,21 @@ const VariantS* variants_smallc(int* count) {
 }
 
 int64_t smallc_lds_bytes(const VariantS& v, const cnn_problem& p, int64_t slab_rows) {
-  return (int64_t)v.ks * 2 * v.tk * 16 + p.Nc * slab_rows * (p.sh * (p.Nh - 1) + p.Ns + 8) * 2;
+  const int64_t Ny = p.sh * (p.Nh - 1) + p.Ns;
+  return (int64_t)v.ks * 2 * v.tk * 16 + p.Nc * slab_rows * ((Ny + 15) & ~(int64_t)7) * 2;
 }
 
 template <int DT, int NB, int KS>
 static hipError_t launch_s(const void* In, const void* Ker, void* Out, const ConvArgs& a,
                            int64_t lds, hipStream_t stream) {
   typedef typename std::conditional<DT == CNN_BF16, float, bf16_t>::type TO;
-  auto kern = conv_smallc<TO, NB, KS>;
-  static bool attr_set = false;
-  if (!attr_set) {
+  auto kern = a.sh == 2 ? conv_smallc<TO, NB, KS, true> : conv_smallc<TO, NB, KS, false>;
+  static bool attr_set[2] = {false, false};
+  if (!attr_set[a.sh == 2]) {
     hipError_t e = hipFuncSetAttribute((const void*)kern,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
     if (e != hipSuccess) return e;
-    attr_set = true;
+    attr_set[a.sh == 2] = true;
   }
   hipLaunchKernelGGL(kern, dim3((unsigned)a.grid), dim3(256), (unsigned)lds, stream,
                      (const bf16_t*)In, (const bf16_t*)Ker, (TO*)Out, a);
