@@ -117,7 +117,7 @@ typedef enum cnn_kernel {
                          256 features x L rows per workgroup, In rows split by
                          column parity into MFMA-ready LDS units, Ker repacked
                          per call (workspace) and copied by DMA one stencil row
-                         per stage; fixed 3x3, Nc % 16 == 0, Nh % 4 == 0,
+                         per stage; fixed 3x3, Nc % 16 == 0,
                          Nh <= 32, Ny <= 64, L | Nw; tp of its plans is L*Nh
                          (cnn_plan_tiles: tp = L*Nh, or 0 for any L)           */
 } cnn_kernel;

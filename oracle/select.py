@@ -170,7 +170,7 @@ GEMM1 = [
 
 
 # (id, dtype, nr, ns, L) of the stride-2 row-band kernel: tk = 256, tc = 16,
-# strides 2 and 2, Nc % 16 == 0, Nh % 4 == 0, Nh <= 32, Ny <= 64; a tile is
+# strides 2 and 2, Nc % 16 == 0, Nh <= 32, Ny <= 64; a tile is
 # L whole output rows of one image (tp = L*Nh, L | Nw).  Taken only when
 # requested (not ranked by `choose`).
 SROWS = [

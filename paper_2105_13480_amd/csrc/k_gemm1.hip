@@ -15,8 +15,10 @@
 //   segment is the MFMA B operand as it lies (8 consecutive channels).
 // * Both are double-buffered in LDS: the next stage's loads are in flight
 //   (in registers) while the current stage is multiplied.
-// * D[pixel][feature]: each lane ends with 4 consecutive pixels of one
-//   feature, written as one 16-byte (fp32) or 8-byte (bf16) store.
+// * D[feature][pixel] (Ker as the A operand): a lane ends with one pixel of
+//   16 features; each 4-byte store instruction writes 32 consecutive pixels
+//   of two features (whole 128-byte rows: faster than 16-byte stores of
+//   32-byte pieces of 32 feature rows).
 #include <type_traits>
 
 #include "internal.h"
@@ -249,7 +251,7 @@ __global__ __launch_bounds__(64 * WP * WK) void conv_gemm1(const bf16_t* __restr
 #pragma unroll
         for (int nb = 0; nb < NBK; ++nb)
           acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-              __builtin_bit_cast(bf16x8_t, A[ks & 1][mb]), __builtin_bit_cast(bf16x8_t, B[ks & 1][nb]),
+              __builtin_bit_cast(bf16x8_t, B[ks & 1][nb]), __builtin_bit_cast(bf16x8_t, A[ks & 1][mb]),
               acc[mb][nb], 0, 0, 0);
       __builtin_amdgcn_sched_barrier(0);
     }
@@ -257,36 +259,29 @@ __global__ __launch_bounds__(64 * WP * WK) void conv_gemm1(const bf16_t* __restr
     lds_barrier_g();
   }
 
-  // Epilogue: register 4g + i of block (mb, nb) holds pixel
-  // 32*(wp*MBP + mb) + 8g + 4*half + i of the tile, feature
-  // k0 + 32*(wk*NBK + nb) + l32.
+  // Epilogue: D[feature][pixel] (Ker is the A operand) -- register j of
+  // block (mb, nb) holds pixel 32*(wp*MBP + mb) + l32 of the tile, feature
+  // k0 + 32*(wk*NBK + nb) + 8(j/4) + 4*half + j%4.  Each 4-byte store
+  // instruction writes 32 consecutive pixels of two features.
 #pragma unroll
-  for (int nb = 0; nb < NBK; ++nb) {
-    const int n = k0 + 32 * (wk * NBK + nb) + l32;
-    const bool nv = n < a.Nk;
+  for (int mb = 0; mb < MBP; ++mb) {
+    const int q = 32 * (wp * MBP + mb) + l32;  // pixel within the tile
+    const int p = p0 + (q < tp ? q : 0);
+    const int b = p / a.hw;
+    const int64_t pix = (int64_t)b * a.Nk * a.hw + (p - b * a.hw);
 #pragma unroll
-    for (int mb = 0; mb < MBP; ++mb) {
+    for (int nb = 0; nb < NBK; ++nb) {
+      const int nblk = k0 + 32 * (wk * NBK + nb) + 4 * half;
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int q = 32 * (wp * MBP + mb) + 8 * g + 4 * half;  // pixel within the tile
-        const int p = p0 + (q < tp ? q : 0);
-        const int b = p / a.hw;
-        const uint32_t vo = (nv && q < tp)
-                                ? (uint32_t)((((int64_t)b * a.Nk + n) * a.hw + (p - b * a.hw)) *
-                                             (int64_t)sizeof(TO))
+      for (int j = 0; j < 16; ++j) {
+        const int n = nblk + 8 * (j >> 2) + (j & 3);
+        const uint32_t vo = (n < a.Nk && q < tp)
+                                ? (uint32_t)((pix + (int64_t)n * a.hw) * (int64_t)sizeof(TO))
                                 : 0x80000000u;
-        if constexpr (sizeof(TO) == 4) {
-          const u32x4_t v = {__float_as_uint(acc[mb][nb][4 * g]), __float_as_uint(acc[mb][nb][4 * g + 1]),
-                             __float_as_uint(acc[mb][nb][4 * g + 2]),
-                             __float_as_uint(acc[mb][nb][4 * g + 3])};
-          __builtin_amdgcn_raw_buffer_store_b128(v, out_rsrc, vo, 0, 0);
-        } else {
-          const u32x2_t v = {(uint32_t)from_f32<bf16_t>(acc[mb][nb][4 * g]) |
-                                 ((uint32_t)from_f32<bf16_t>(acc[mb][nb][4 * g + 1]) << 16),
-                             (uint32_t)from_f32<bf16_t>(acc[mb][nb][4 * g + 2]) |
-                                 ((uint32_t)from_f32<bf16_t>(acc[mb][nb][4 * g + 3]) << 16)};
-          __builtin_amdgcn_raw_buffer_store_b64(v, out_rsrc, vo, 0, 0);
-        }
+        if constexpr (sizeof(TO) == 4)
+          __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc[mb][nb][j]), out_rsrc, vo, 0, 0);
+        else
+          __builtin_amdgcn_raw_buffer_store_b16(from_f32<bf16_t>(acc[mb][nb][j]), out_rsrc, vo, 0, 0);
       }
     }
   }

@@ -28,8 +28,10 @@
 //   32-feature blocks) x the band's L rows, half of the (row, block) pairs
 //   each, with the same straight-line code for odd L too.  A 32-position
 //   MFMA block is one output row (Nh <= 32).
-// * D[position][feature]: a lane ends with 4 consecutive positions of one
-//   feature, written as one 16-byte (fp32) or 8-byte (bf16) store.
+// * D[feature][position] (Ker is the A operand): a lane ends with one
+//   position of 16 features, written as 4-byte (2-byte) stores; each store
+//   instruction writes whole rows (Nh positions) of two features, which
+//   measured faster than 16-byte stores of 32-byte pieces of 32 rows.
 #include <type_traits>
 
 #include "internal.h"
@@ -279,7 +281,7 @@ __global__ __launch_bounds__(64 * NWV) void conv_srows(const bf16_t* __restrict_
         for (int q = 0; q < 2; ++q)
           if (q == 0 || has_second(i))
             acc[i][q] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                __builtin_bit_cast(bf16x8_t, A[cu][i]), __builtin_bit_cast(bf16x8_t, B[cu][q]),
+                __builtin_bit_cast(bf16x8_t, B[cu][q]), __builtin_bit_cast(bf16x8_t, A[cu][i]),
                 acc[i][q], 0, 0, 0);
         if (i == 0) {
           B[nx][0] = st + 1 < NS ? read_b(kb, st + 1, 0) : read_b(nkb, 0, 0);
@@ -350,35 +352,27 @@ __global__ __launch_bounds__(64 * NWV) void conv_srows(const bf16_t* __restrict_
     }
   }
 
-  // ---- epilogue: register 4g + e of block (i, q) holds position
-  // 8g + 4*half + e of output row w0 + row0 + rdir*i, feature
-  // k0 + 64 fp + 32 (q ? 1 - nbf : nbf) + l32.
+  // ---- epilogue: register j of block (i, q) holds position l32 of output
+  // row w0 + row0 + rdir*i, feature k0 + 64 fp + 32 (q ? 1 - nbf : nbf) +
+  // 8 (j/4) + 4 half + j%4.
 #pragma unroll
   for (int q = 0; q < 2; ++q) {
-    const int n = k0 + 64 * fp + 32 * (q ? 1 - nbf : nbf) + l32;
-    const bool nv = n < a.Nk;
+    const int nblk = k0 + 64 * fp + 32 * (q ? 1 - nbf : nbf) + 4 * half;
 #pragma unroll
     for (int i = 0; i < RW; ++i) {
       if (q == 1 && !has_second(i)) continue;
       const int w = w0 + row0 + rdir * i;
-      const int64_t rbase = (((int64_t)b * a.Nk + n) * a.Nw + w) * a.Nh;
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int h0 = 8 * g + 4 * half;
-        const uint32_t vo = (nv && h0 < a.Nh) ? (uint32_t)((rbase + h0) * (int64_t)sizeof(TO))
-                                              : 0x80000000u;
-        if constexpr (sizeof(TO) == 4) {
-          const u32x4_t v = {__float_as_uint(acc[i][q][4 * g]), __float_as_uint(acc[i][q][4 * g + 1]),
-                             __float_as_uint(acc[i][q][4 * g + 2]),
-                             __float_as_uint(acc[i][q][4 * g + 3])};
-          __builtin_amdgcn_raw_buffer_store_b128(v, out_rsrc, vo, 0, 0);
-        } else {
-          const u32x2_t v = {(uint32_t)from_f32<bf16_t>(acc[i][q][4 * g]) |
-                                 ((uint32_t)from_f32<bf16_t>(acc[i][q][4 * g + 1]) << 16),
-                             (uint32_t)from_f32<bf16_t>(acc[i][q][4 * g + 2]) |
-                                 ((uint32_t)from_f32<bf16_t>(acc[i][q][4 * g + 3]) << 16)};
-          __builtin_amdgcn_raw_buffer_store_b64(v, out_rsrc, vo, 0, 0);
-        }
+      for (int j = 0; j < 16; ++j) {
+        const int n = nblk + 8 * (j >> 2) + (j & 3);
+        const uint32_t vo =
+            (n < a.Nk && l32 < a.Nh)
+                ? (uint32_t)(((((int64_t)b * a.Nk + n) * a.Nw + w) * a.Nh + l32) * (int64_t)sizeof(TO))
+                : 0x80000000u;
+        if constexpr (sizeof(TO) == 4)
+          __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc[i][q][j]), out_rsrc, vo, 0, 0);
+        else
+          __builtin_amdgcn_raw_buffer_store_b16(from_f32<bf16_t>(acc[i][q][j]), out_rsrc, vo, 0, 0);
       }
     }
   }
@@ -471,7 +465,7 @@ int64_t srows_ws_bytes(const VariantQ& v, const cnn_problem& p) {
 bool srows_fits(const VariantQ& v, const cnn_problem& p) {
   const int64_t Ny = 2 * (p.Nh - 1) + p.Ns;
   return p.sw == 2 && p.sh == 2 && p.Nr == v.nr && p.Ns == v.ns && p.Nc % 16 == 0 &&
-         p.Nh % 4 == 0 && p.Nh <= 32 && Ny <= 64 && p.Nw % v.L == 0;
+         p.Nh <= 32 && Ny <= 64 && p.Nw % v.L == 0;
 }
 
 template <int DT, int NR, int NS, int L, int NWV>

@@ -347,7 +347,9 @@ SROWS_SHAPES = [
     (2, 32, 300, 7, 28, 3, 3, 2, 2),    # Ny = 57: two k tiles (the second ragged), one band
     (3, 16, 64, 8, 12, 3, 3, 2, 2),     # one chunk, features past Nk, two bands of 4
     (1, 48, 256, 14, 28, 3, 3, 2, 2),   # three chunks, two bands of 7
-    (2, 16, 40, 28, 4, 3, 3, 2, 2),     # Nh = 4: rows of one 16-byte store, 4 or 7 bands
+    (2, 16, 40, 28, 4, 3, 3, 2, 2),     # Nh = 4: short rows, 4 or 7 bands
+    (2, 16, 40, 7, 27, 3, 3, 2, 2),     # Nh = 27 (Ny = 55): a ragged row end
+    (1, 32, 70, 8, 13, 3, 3, 2, 2),     # Nh = 13, two bands of 4, features past Nk
 ]
 
 
