@@ -38,6 +38,14 @@ vectors, S*Ny <= 256*mpos positions, and (imgs*Nc + tc) input planes and imgs
 output images to span < 2^31 bytes.  Each later tier is ranked only if no
 candidate of the earlier tiers fits; tier 2 (the plain staging kernel) last.
 If nothing fits, the direct kernel is used.
+
+Before all tiers the automatic choice takes a specialized family when one
+fits (`_special`): the 1x1 GEMM kernel for 1x1 layers (the first row of
+GEMM1 whose stride mode, size limits, LDS image and balanced tile fit),
+else the row-streaming kernel for stride 1 (the first row of ROWS that fits,
+with the band that needs the fewest rounds of row groups per workgroup, the
+largest such), else the stride-2 row-band kernel (the largest band that
+divides Nw, then the lowest id).  These are not ranked by the cost above.
 """
 from __future__ import annotations
 
@@ -142,25 +150,24 @@ STREAM = [
 ]
 
 
-# (id, dtype, nr, ns, mb, ncg) of the row-streaming kernel: tk = 64, stride
-# 1, input rows of at most 32*mb positions, Nc rounded up to 16 equal to
-# 16*ncg; a tile is L whole output rows of one image (tp = L*Nh, L | Nw).
-# (Its wave layout -- rows per wave -- does not enter the selection.)
-# Taken only when requested (not ranked by `choose`); where several fit,
-# the lowest id.
+# (id, dtype, nr, ns, mb, ncg, waves, rpw) of the row-streaming kernel: tk =
+# 64, stride 1, input rows of at most 32*mb positions, Nc rounded up to 16
+# equal to 16*ncg, `waves` waves of which each pair takes rpw rows of a
+# group (wr = rpw*waves/2 rows per group); a tile is L whole output rows of
+# one image (tp = L*Nh, L | Nw).  Where several fit, the lowest id.
 ROWS = [
-    (1500, BF16, 3, 3, 1, 4), (1501, BF16, 3, 3, 1, 2), (1502, BF16, 3, 3, 2, 4),
-    (1503, BF16, 3, 3, 2, 2), (1504, BF16, 1, 1, 2, 4),
-    (1600, BF16_OBF16, 3, 3, 1, 4), (1601, BF16_OBF16, 3, 3, 1, 2),
-    (1602, BF16_OBF16, 3, 3, 2, 4), (1603, BF16_OBF16, 3, 3, 2, 2),
-    (1604, BF16_OBF16, 1, 1, 2, 4),
+    (1500, BF16, 3, 3, 1, 4, 8, 1), (1501, BF16, 3, 3, 1, 2, 8, 1),
+    (1502, BF16, 3, 3, 2, 4, 8, 1), (1503, BF16, 3, 3, 2, 2, 8, 1),
+    (1504, BF16, 1, 1, 2, 4, 8, 1),
+    (1600, BF16_OBF16, 3, 3, 1, 4, 8, 1), (1601, BF16_OBF16, 3, 3, 1, 2, 8, 1),
+    (1602, BF16_OBF16, 3, 3, 2, 4, 8, 1), (1603, BF16_OBF16, 3, 3, 2, 2, 8, 1),
+    (1604, BF16_OBF16, 1, 1, 2, 4, 8, 1),
 ]
 
 
 # (id, dtype, wp, wk, mbp, nbk, tc, s2) of the 1x1 GEMM kernel: tk =
 # 32*wk*nbk, tp <= 32*wp*mbp (a multiple of 4), Nc % 8 == 0; s2 = 0: strides
-# 1 and Nw*Nh % 4 == 0; s2 = 1: strides 2 and 2, Nh % 4 == 0.  Taken only
-# when requested (not ranked by `choose`).
+# 1 and Nw*Nh % 4 == 0; s2 = 1: strides 2 and 2, Nh % 4 == 0.
 GEMM1 = [
     (1700, BF16, 2, 4, 4, 2, 64, 0), (1701, BF16, 4, 2, 2, 2, 64, 0),
     (1702, BF16, 2, 4, 4, 2, 32, 1),
@@ -171,8 +178,7 @@ GEMM1 = [
 
 # (id, dtype, nr, ns, L) of the stride-2 row-band kernel: tk = 256, tc = 16,
 # strides 2 and 2, Nc % 16 == 0, Nh <= 32, Ny <= 64; a tile is
-# L whole output rows of one image (tp = L*Nh, L | Nw).  Taken only when
-# requested (not ranked by `choose`).
+# L whole output rows of one image (tp = L*Nh, L | Nw); eight waves.
 SROWS = [
     (1900, BF16, 3, 3, 7), (1901, BF16, 3, 3, 4),
     (2000, BF16_OBF16, 3, 3, 7), (2001, BF16_OBF16, 3, 3, 4),
@@ -365,13 +371,88 @@ def candidates(p: eq1.Problem, dtype: int, cus: int, lds_bytes: int, acc_regs: i
         yield t, tk, tp, tc, vid, info
 
 
+def _special(p: eq1.Problem, dtype: int, cus: int, lds_bytes: int, acc_regs: int,
+             wg_per_cu: int):
+    """(kernel, id, tk, tp, tc) of the specialized tier, or None."""
+    e_out = 2 if dtype == BF16_OBF16 else 4
+    lds_cap = min(lds_bytes, 160 * 1024)
+    out_big = p.Nb * p.Nk * p.Nw * p.Nh * e_out >= 2 ** 31
+    # 1x1 GEMM: In planes of Nx x Ny for 1x1 taps
+    for vid, dt, wp, wk, mbp, nbk, tc, s2 in GEMM1:
+        if dt != dtype or p.Nr != 1 or p.Ns != 1 or p.Nc % 8:
+            continue
+        if s2 and not (p.sw == 2 and p.sh == 2 and p.Nh % 4 == 0):
+            continue
+        if not s2 and not (p.sw == 1 and p.sh == 1 and (p.Nw * p.Nh) % 4 == 0):
+            continue
+        tk, tpmax, acc = 32 * wk * nbk, 32 * wp * mbp, 16 * mbp * nbk
+        lds = 2 * (tc * (tpmax + 16) + tk * (tc + 8)) * 2
+        nx, ny = p.sw * (p.Nw - 1) + 1, p.sh * (p.Nh - 1) + 1
+        if (lds > lds_cap or p.Nb * p.Nc * nx * ny * 2 >= 2 ** 30
+                or p.Nk * p.Nc * 2 >= 2 ** 30 or out_big):
+            continue
+        occ = max(1, min(wg_per_cu, lds_bytes // lds))
+        tp = min(tpmax, -(-balanced_tp(p, tpmax, tk, cus * occ, 1) // 4) * 4)
+        if tp % 4 or tp < 4 or acc > acc_regs:
+            continue
+        return (11, vid, tk, tp, tc)
+    # stride-1 row streaming
+    for vid, dt, nr, ns, mb, ncg, waves, rpw in ROWS:
+        if (dt != dtype or (nr, ns) != (p.Nr, p.Ns) or p.sw != 1 or p.sh != 1 or p.Nc % 8
+                or -(-p.Nc // 16) * 16 != 16 * ncg or p.Nh + p.Ns - 1 > 32 * mb):
+            continue
+        if (p.Nb * p.Nc * p.Nx * p.Ny * 2 >= 2 ** 31 or p.Nk * p.Nc * nr * ns * 2 >= 2 ** 31
+                or out_big):
+            continue
+        wr, nt, ncp = rpw * waves // 2, 64 * waves, 16 * ncg
+        ring = (2 * wr + nr - 1) * ncp * 32 * mb * 2
+        copies = -(-(64 * ncp * nr * ns // 8) // nt)
+        plane = 66 if ring >= copies * nt * 16 else 64   # padded B-operand planes
+        lds = ncg * nr * ns * 2 * plane * 16 + ring
+        acc = 16 * mb * ns * rpw
+        if lds > lds_cap or acc > acc_regs * 8 // waves:
+            continue
+        nk = -(-p.Nk // 64)
+        band, best = 0, None
+        for l in range(1, p.Nw + 1):
+            if p.Nw % l:
+                continue
+            rounds = -(-(p.Nb * (p.Nw // l) * nk) // cus) * -(-l // wr)
+            if best is None or rounds <= best:
+                band, best = l, rounds
+        return (10, vid, 64, band * p.Nh, p.Nc)
+    # stride-2 row bands
+    pick = None
+    for vid, dt, nr, ns, L in SROWS:
+        if (dt != dtype or (nr, ns) != (p.Nr, p.Ns) or p.sw != 2 or p.sh != 2 or p.Nc % 16
+                or p.Nh > 32 or p.Ny > 64 or p.Nw % L):
+            continue
+        rows = 2 * (L - 1) + nr if nr >= 2 else L
+        blk = -(-(nr * ns * 2 * 256) // 256) * 256
+        ws = -(-p.Nk // 256) * (p.Nc // 16) * blk * 16
+        lds = (4 * ns * 2 * 256 + 2 * 2 * rows * 64) * 16
+        acc = 32 * ((L + 1) // 2) - 16 * (L % 2)
+        if (p.Nb * p.Nc * p.Nx * p.Ny * 2 >= 2 ** 31 or ws >= 2 ** 31 or out_big
+                or lds > lds_cap or acc > acc_regs):
+            continue
+        if pick is None or L > pick[0]:
+            pick = (L, vid)
+    if pick is not None:
+        return (12, pick[1], 256, pick[0] * p.Nh, 16)
+    return None
+
+
 def choose(p: eq1.Problem, dtype: int, cus=256, lds_bytes=160 * 1024, acc_regs=128,
            wg_per_cu=2):
-    """(kernel, variant id, tk, tp, tc) the rule above selects; kernel 7 is
-    the wide-staging family, 6 the DMA-staged one, 5 the register-staged
+    """(kernel, variant id, tk, tp, tc) the rule above selects; kernels 11,
+    10 and 12 are the specialized 1x1 GEMM, row-streaming and stride-2 row-band
+    families, 7 the wide-staging family, 6 the DMA-staged one, 5 the register-staged
     pipelined one (8 when it stages raw Ker rows, 3 for its 1x1 gather),
     4 the few-channel one, 9 the persistent streaming one, 2 the plain
     staging one, 1 the direct kernel."""
+    special = _special(p, dtype, cus, lds_bytes, acc_regs, wg_per_cu)
+    if special is not None:
+        return special
     rawk_ids = {row[0] for row in IGEMM2 if row[10]}
     pw_ids = {row[0] for row in IGEMM2 if row[11]}
     best = None

@@ -454,9 +454,50 @@ int select_plan(const cnn_problem& p, int dtype, const cnn_budget& bud, int kern
       }
     }
   }
+  // Tier 0 (automatic choice only): a specialized family, when one fits --
+  // the 1x1 GEMM kernel for 1x1 layers (lowest id), else the row-streaming
+  // kernel for stride 1 (its automatic band, lowest id), else the stride-2
+  // row-band kernel (the largest band, then the lowest id).  On the layers
+  // they were built for they are the fastest the plan search finds; the
+  // Eq. (1) time model below prices MFMA at peak and cannot rank them.
+  if (kernel == CNN_K_AUTO) {
+    cnn_plan_t cand;
+    double t;
+    int ng = 0;
+    const VariantG* vg = variants_gemm1(&ng);
+    for (int i = 0; i < ng; ++i)
+      if (vg[i].dtype == dtype && eval_gemm1(p, dtype, vg[i], bud, &cand, &t)) {
+        cand.kernel = CNN_K_GEMM1;
+        fill_common(p, dtype, &cand);
+        *out = cand;
+        return CNN_OK;
+      }
+    int nr = 0;
+    const VariantR* vr = variants_rows(&nr);
+    for (int i = 0; i < nr; ++i)
+      if (vr[i].dtype == dtype && eval_rows(p, dtype, vr[i], bud, 0, &cand, &t)) {
+        cand.kernel = CNN_K_ROWS;
+        fill_common(p, dtype, &cand);
+        *out = cand;
+        return CNN_OK;
+      }
+    int nq = 0;
+    const VariantQ* vq = variants_srows(&nq);
+    const VariantQ* bq = nullptr;
+    for (int i = 0; i < nq; ++i)
+      if (vq[i].dtype == dtype && eval_srows(p, dtype, vq[i], bud, &cand, &t) &&
+          (!bq || vq[i].L > bq->L))
+        bq = &vq[i];
+    if (bq && eval_srows(p, dtype, *bq, bud, &cand, &t)) {
+      cand.kernel = CNN_K_SROWS;
+      fill_common(p, dtype, &cand);
+      *out = cand;
+      return CNN_OK;
+    }
+  }
   // Tier 1: the DMA-staged kernel, tier 2: the register-staged pipelined
   // kernel (both bf16), tier 3: the plain staging kernel.  The wide-staging
-// kernel competes within tier 1.
+  // kernel competes within tier 1.
   int n4 = 0;
   const Variant4* vs4 = variants4(&n4);
   for (int i = 0; i < n4; ++i) {

@@ -133,7 +133,7 @@ def rows_dims(vid, dt, stencil):
     row groups; the (tp = L*Nh) is returned as dims[-1] of the tuple."""
     from oracle import select as osel
     row = next(r for r in osel.ROWS if r[0] == vid)
-    _, _, nr, ns, mb, ncg = row
+    _, _, nr, ns, mb, ncg, _, _ = row
     nc = 16 * ncg - 8                      # Nc % 8 == 0, last group half empty
     nh = (29 if mb == 1 else 45) - (ns - 1) if ns > 1 else (30 if mb == 1 else 50)
     for dims in [(2, nc, 71, 10, nh, nr, ns, 1, 1), (3, nc, 64, 6, nh + 1, nr, ns, 1, 1)]:
@@ -170,7 +170,7 @@ def variant_cases():
         out.append((cnn.K_GEMM1, vid, dt, 32 * wk * nbk, 32 * wp * mbp, tc, (1, 1)))
     for vid, dt, nr, ns, L in osel.SROWS:
         out.append((cnn.K_SROWS, vid, dt, 256, 0, 16, (nr, ns)))
-    for vid, dt, nr, ns, mb, ncg in osel.ROWS:
+    for vid, dt, nr, ns, mb, ncg, _, _ in osel.ROWS:
         out.append((cnn.K_ROWS, vid, dt, 64, 0, 0, (nr, ns)))
     for vid, dt, nb, ks in osel.SMALLC:
         out.append((cnn.K_SMALLC, vid, dt, 64, 128 * nb, 0, (7, 7) if ks <= 12 else (5, 5)))
