@@ -200,7 +200,7 @@ __global__ __launch_bounds__(64 * WAVES) void conv_rows(const bf16_t* __restrict
     // The tile's raw rows Ker[k0 .. k0+63][Nc][RS] are one contiguous run
     // of 16-byte chunks: copied into the ring by DMA, one kilobyte per wave
     // instruction (features past Nk read as zeros).  The first group's rows
-    // and the next group's are loaded into registers meanwhile.
+    // are loaded into registers meanwhile.
     {
       char* raw = reinterpret_cast<char*>(rows);
       const int nch = TK * a.Nc * RS / 8;
@@ -213,11 +213,8 @@ __global__ __launch_bounds__(64 * WAVES) void conv_rows(const bf16_t* __restrict
     int fix0[NINIT];
 #pragma unroll
     for (int j = 0; j < NINIT; ++j) v0[j] = load_block(y0, min(tid + NT * j, nb0 - 1), fix0[j]);
-#pragma unroll
-    for (int j = 0; j < NLD; ++j)
-      pre[j] = load_block(new_lo(1), max(0, min(tid + NT * j, new_n(1) * row_blocks - 1)), fixp[j]);
     // the copies (issued first) have landed in every wave
-    asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(NINIT + NLD) : "memory");
+    asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(NINIT) : "memory");
     // Repack: item (octet j, feature kk), j fastest, so a 16-lane group
     // reads 8 octets of 2 features (runs 144 bytes / a feature apart: distinct
     // banks) and writes 8 consecutive planes at 2 features (plane stride PST
@@ -287,9 +284,6 @@ __global__ __launch_bounds__(64 * WAVES) void conv_rows(const bf16_t* __restrict
 #pragma unroll
     for (int j = 0; j < NINIT; ++j) v0[j] = load_block(y0, min(tid + NT * j, nb0 - 1), fix0[j]);
 #pragma unroll
-    for (int j = 0; j < NLD; ++j)
-      pre[j] = load_block(new_lo(1), max(0, min(tid + NT * j, new_n(1) * row_blocks - 1)), fixp[j]);
-#pragma unroll
     for (int u = 0; u < KPT; ++u) {
       const int tr = tid + NT * u;
       if (tr < NTRIP) {
@@ -320,6 +314,12 @@ __global__ __launch_bounds__(64 * WAVES) void conv_rows(const bf16_t* __restrict
     }
   }
   __syncthreads();
+  // The second group's rows are requested only now, so that they do not
+  // compete with the first group's for HBM; they are written to the ring in
+  // the second half of the first group's steps.
+#pragma unroll
+  for (int j = 0; j < NLD; ++j)
+    pre[j] = load_block(new_lo(1), max(0, min(tid + NT * j, new_n(1) * row_blocks - 1)), fixp[j]);
 
   // In operand lane offsets (elements within a 16-channel group of a row):
   // lane i of 16-lane group G supplies channel 8*(G/2) + i/4 (+4 for the
@@ -360,6 +360,11 @@ __global__ __launch_bounds__(64 * WAVES) void conv_rows(const bf16_t* __restrict
     }
   };
 
+  // A SIMD issues the MFMAs of its older wave first, so the second half of
+  // the workgroup would finish each group's products last and alone; it
+  // takes the higher issue priority during the products instead (measured
+  // faster than equal priority and than alternating it step by step).
+  const bool hiw = __builtin_amdgcn_readfirstlane(threadIdx.x) >= NT / 2;
   for (int gi = 0; gi < n_groups; ++gi) {
 
     // this wave's first output row, relative to y0; rows past the band are
@@ -424,10 +429,12 @@ __global__ __launch_bounds__(64 * WAVES) void conv_rows(const bf16_t* __restrict
       // (VEC: the previous group's chunks go out a few per step)
       constexpr int CPS = (RPW * NCHUNK + NSTEP - 1) / NSTEP;
       // The next group's rows (loaded a group ago) go to ring slots no wave
-      // reads in this group, one block per step between the products.
+      // reads in this group, one block per step between the products of the
+      // group's second half.
       const int nb_next = new_n(gi + 1) * row_blocks;
       u32x4_t A[2][MB], B[2][NR][NS];
       read_step(0, A[0], B[0]);
+      if (hiw) __builtin_amdgcn_s_setprio(1);
 #pragma unroll
       for (int t = 0; t < NSTEP; ++t) {
         if (t + 1 < NSTEP) read_step(t + 1, A[(t + 1) & 1], B[(t + 1) & 1]);
@@ -442,12 +449,13 @@ __global__ __launch_bounds__(64 * WAVES) void conv_rows(const bf16_t* __restrict
         }
 #pragma unroll
         for (int j = 0; j < NLD; ++j) {
-          if ((j * NSTEP) / NLD != t) continue;  // compile-time
+          if (NSTEP / 2 + (j * (NSTEP - NSTEP / 2)) / NLD != t) continue;  // compile-time
           const int f = tid + NT * j;
           if (f < nb_next) store_block(new_lo(gi + 1), f, pre[j], fixp[j]);
         }
         __builtin_amdgcn_sched_barrier(0);
       }
+      __builtin_amdgcn_s_setprio(0);
     }
 
     // Then the loads of the group after it are issued, before this group's
