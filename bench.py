@@ -73,7 +73,7 @@ def measured_traffic(workload: str, mode: str):
 
 KERNELS = {"direct": 1, "igemm": 2, "pointwise": 3, "smallc": 4, "igemm_pipe": 5,
            "igemm_dma": 6, "igemm_wide": 7, "igemm_rawk": 8, "stream": 9, "rows": 10, "gemm1": 11,
-           "srows": 12}
+           "srows": 12, "splitc": 13}
 
 
 def forced_plan(spec: str, w, mode: str):
@@ -384,7 +384,8 @@ def main():
                       f"{ww.flops / (k2 * 1e-3) / 1e12:8.1f} TF/s  "
                       f"{100 * ww.flops / (k2 * 1e-3) / 1e12 / PEAK_TFLOPS[pr]:5.1f}% peak  "
                       f"{p2.compulsory_bytes / (k2 * 1e-3) / 1e9:7.0f} GB/s  "
-                      f"plan {p2.as_dict()['kernel']} v{p2.variant} tk{p2.tk} tp{p2.tp} tc{p2.tc}",
+                      f"plan {p2.as_dict()['kernel']} v{p2.variant} tk{p2.tk} tp{p2.tp} tc{p2.tc}"
+                      + (f" kc{p2.kc}" if p2.kernel == cnn.K_SPLITC else ""),
                       file=sys.stderr, flush=True)
 
     print(json.dumps(line), flush=True)

@@ -113,13 +113,21 @@ typedef enum cnn_kernel {
                          both double-buffered in LDS; Nc % 8 == 0, tp a multiple
                          of 4; strides 1 (Nw*Nh % 4 == 0) or 2 and 2 (Nh % 4 ==
                          0: 4 output pixels = the even half of 8 input columns) */
-  CNN_K_SROWS = 12    /* stride-2 layers over bands of whole output rows, bf16:
+  CNN_K_SROWS = 12,   /* stride-2 layers over bands of whole output rows, bf16:
                          256 features x L rows per workgroup, In rows split by
                          column parity into MFMA-ready LDS units, Ker repacked
                          per call (workspace) and copied by DMA one stencil row
                          per stage; fixed 3x3, Nc % 16 == 0,
                          Nh <= 32, Ny <= 64, L | Nw; tp of its plans is L*Nh
                          (cnn_plan_tiles: tp = L*Nh, or 0 for any L)           */
+  CNN_K_SPLITC = 13   /* the paper's Case 2 (Sec. 2.1, W_c < N_c; the partial Outs
+                         reduced at the end, Sec. 2.3) on one GPU: the
+                         CNN_K_IGEMM tiles (same tk/tp/tc and instantiations)
+                         with the channel loop split over kc workgroup slices
+                         (plan.kc); each slice writes fp32 partial sums to the
+                         workspace, a second kernel adds the kc slices in slice
+                         order and writes Out.  For shapes with few output
+                         tiles and many channels; any dtype and stencil       */
 } cnn_kernel;
 
 /*
@@ -146,15 +154,22 @@ typedef struct cnn_plan_t {
   int32_t dtype;        /* cnn_dtype                                                */
   int32_t kernel;       /* cnn_kernel (never CNN_K_AUTO in a finished plan)         */
   int32_t variant;      /* internal kernel instantiation id                         */
-  int32_t reserved;
+  int32_t kc;           /* CNN_K_SPLITC: channel slices (the paper's P_c), 1 ..
+                           ceil(Nc/tc); slice z takes channels [z*cs, z*cs + cs),
+                           cs = ceil(ceil(Nc/tc)/kc)*tc; a caller may change it
+                           and must then set ws_bytes = 4*kc*Nb*Nk*Nw*Nh.
+                           cnn_plan_tiles picks the smallest kc with no empty
+                           slice that gives at least two workgroups per CU,
+                           else ceil(Nc/tc).  0 for the other kernels.        */
   int64_t tk;           /* output features per workgroup (T_k)                      */
   int64_t tp;           /* outputs of the flattened (b,w,h) index per workgroup     */
   int64_t tc;           /* input features per LDS stage (T_c)                       */
   int64_t grid;         /* workgroups launched                                      */
   int64_t lds_bytes;    /* LDS per workgroup                                        */
   int64_t slab_rows;    /* max input rows a workgroup stages (halo included)        */
-  int64_t ws_bytes;     /* device workspace the plan needs (repacked Ker); the
-                           library allocates it per (device, stream) on first use */
+  int64_t ws_bytes;     /* device workspace the plan needs (repacked Ker, or the
+                           fp32 partial Outs of CNN_K_SPLITC); the library
+                           allocates it per (device, stream) on first use      */
   double eq1_elems[3];  /* Eq. (1) terms Out, Ker, In for this tiling (elements)    */
   double eq1_bytes;     /* the same, weighted by element size, summed               */
   double compulsory_bytes; /* |In read| + |Ker| + |Out|, each once                  */

@@ -20,11 +20,11 @@ CNN_F32, CNN_BF16, CNN_BF16_OBF16 = 0, 1, 2
 DTYPES = {"f32": CNN_F32, "bf16": CNN_BF16, "bf16_obf16": CNN_BF16_OBF16}
 
 (K_AUTO, K_DIRECT, K_IGEMM, K_POINTWISE, K_SMALLC, K_IGEMM_PIPE, K_IGEMM_DMA, K_IGEMM_WIDE,
- K_IGEMM_RAWK, K_STREAM, K_ROWS, K_GEMM1, K_SROWS) = range(13)
+ K_IGEMM_RAWK, K_STREAM, K_ROWS, K_GEMM1, K_SROWS, K_SPLITC) = range(14)
 KERNEL_NAMES = {K_DIRECT: "direct", K_IGEMM: "igemm", K_POINTWISE: "pointwise", K_SMALLC: "smallc",
                 K_IGEMM_PIPE: "igemm_pipe", K_IGEMM_DMA: "igemm_dma", K_IGEMM_WIDE: "igemm_wide",
                 K_IGEMM_RAWK: "igemm_rawk", K_STREAM: "stream", K_ROWS: "rows",
-                K_GEMM1: "gemm1", K_SROWS: "srows"}
+                K_GEMM1: "gemm1", K_SROWS: "srows", K_SPLITC: "splitc"}
 
 STATUS = {0: "CNN_OK", -1: "CNN_E_NULL", -2: "CNN_E_SHAPE", -3: "CNN_E_DTYPE",
           -4: "CNN_E_OVERFLOW", -5: "CNN_E_ALIAS", -6: "CNN_E_UNSUPPORTED",
@@ -52,7 +52,7 @@ class Budget(ctypes.Structure):
 
 class Plan(ctypes.Structure):
     _fields_ = [("prob", Problem), ("dtype", ctypes.c_int32), ("kernel", ctypes.c_int32),
-                ("variant", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("variant", ctypes.c_int32), ("kc", ctypes.c_int32),
                 ("tk", i64), ("tp", i64), ("tc", i64), ("grid", i64), ("lds_bytes", i64),
                 ("slab_rows", i64), ("ws_bytes", i64), ("eq1_elems", ctypes.c_double * 3),
                 ("eq1_bytes", ctypes.c_double), ("compulsory_bytes", ctypes.c_double),
@@ -60,7 +60,7 @@ class Plan(ctypes.Structure):
 
     def as_dict(self) -> dict:
         return {"kernel": KERNEL_NAMES.get(self.kernel, str(self.kernel)), "variant": self.variant,
-                "tk": self.tk, "tp": self.tp, "tc": self.tc, "grid": self.grid,
+                "tk": self.tk, "tp": self.tp, "tc": self.tc, "grid": self.grid, "kc": self.kc,
                 "lds_bytes": self.lds_bytes, "slab_rows": self.slab_rows, "ws_bytes": self.ws_bytes,
                 "eq1_elems": list(self.eq1_elems), "eq1_bytes": self.eq1_bytes,
                 "compulsory_bytes": self.compulsory_bytes, "flops": self.flops}

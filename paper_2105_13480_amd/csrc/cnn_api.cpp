@@ -294,6 +294,17 @@ const Variant* find_variant(int id) {
   return nullptr;
 }
 
+// Geometry a plain staging plan (and its split form) must carry: the slab,
+// grid and LDS size its tile implies.
+bool igemm_geometry_ok(const Variant& v, const cnn_plan_t& pl) {
+  const cnn_problem& p = pl.prob;
+  const int64_t Ny = p.sh * (p.Nh - 1) + p.Ns;
+  const int64_t S = slab_rows_max(p, pl.tp);
+  const int64_t grid = ((p.Nb * p.Nw * p.Nh + pl.tp - 1) / pl.tp) * ((p.Nk + v.tk - 1) / v.tk);
+  return pl.slab_rows == S && pl.grid == grid &&
+         pl.lds_bytes == igemm_lds_bytes(v, S, Ny, p.Nr * p.Ns) && pl.lds_bytes <= 160 * 1024;
+}
+
 // The launch geometry a pipelined-kernel plan carries must be the one its
 // tile size implies: the kernel sizes LDS and its tile loop from it.
 bool v2_geometry_ok(const Variant2& v, const cnn_plan_t& pl) {
@@ -344,6 +355,23 @@ int run_plan(const void* In, const void* Ker, void* Out, const cnn_plan_t& pl, h
       if (st2) return st2;
     }
     e = launch_srows(*vq, In, Ker, Out, ws, a, pl.lds_bytes, st);
+  } else if (pl.kernel == CNN_K_SPLITC) {
+    const Variant* v = find_variant(pl.variant);
+    const cnn_problem& p = pl.prob;
+    const int64_t stages = (p.Nc + pl.tc - 1) / (pl.tc > 0 ? pl.tc : 1);
+    if (!v || v->kernel != CNN_K_IGEMM || v->dtype != pl.dtype || v->tk != pl.tk ||
+        v->tp != pl.tp || v->tc != pl.tc || !igemm_geometry_ok(*v, pl))
+      return fail(CNN_E_PLAN, "plan names no matching kernel instantiation (variant %d)", pl.variant);
+    if (pl.kc < 1 || pl.kc > stages || pl.kc > 65535 ||
+        pl.ws_bytes != 4LL * pl.kc * p.Nb * p.Nk * p.Nw * p.Nh)
+      return fail(CNN_E_PLAN, "split plan needs 1 <= kc <= %lld and ws_bytes = 4*kc*|Out|",
+                  (long long)stages);
+    void* ws = user_ws;
+    if (!ws) {
+      int st2 = get_workspace(st, pl.ws_bytes, &ws);
+      if (st2) return st2;
+    }
+    e = launch_splitc(*v, In, Ker, Out, ws, a, pl.lds_bytes, pl.kc, pl.dtype, st);
   } else if (pl.kernel == CNN_K_SMALLC) {
     const VariantS* vs = find_variant_s(pl.variant);
     if (!vs || vs->dtype != pl.dtype || vs->tk != pl.tk || !smallc_geometry_ok(*vs, pl))
@@ -384,7 +412,7 @@ int run_plan(const void* In, const void* Ker, void* Out, const cnn_plan_t& pl, h
   } else {
     const Variant* v = find_variant(pl.variant);
     if (!v || v->kernel != pl.kernel || v->dtype != pl.dtype || v->tk != pl.tk ||
-        v->tp != pl.tp || v->tc != pl.tc)
+        v->tp != pl.tp || v->tc != pl.tc || !igemm_geometry_ok(*v, pl))
       return fail(CNN_E_PLAN, "plan names no matching kernel instantiation (variant %d)", pl.variant);
     e = launch_igemm(*v, In, Ker, Out, a, pl.lds_bytes, st);
   }
@@ -451,7 +479,7 @@ int cnn_plan_tiles(const cnn_problem* prob, int dtype, int kernel, int64_t tk, i
   if (!prob || !plan) return fail(CNN_E_NULL, "prob and plan must be non-NULL");
   int st;
   if ((st = check_problem(*prob)) || (st = check_dtype(dtype))) return st;
-  if (kernel < CNN_K_AUTO || kernel > CNN_K_SROWS)
+  if (kernel < CNN_K_AUTO || kernel > CNN_K_SPLITC)
     return fail(CNN_E_UNSUPPORTED, "unknown kernel %d", kernel);
   cnn_budget bud;
   if ((st = resolve_budget(budget, &bud))) return st;

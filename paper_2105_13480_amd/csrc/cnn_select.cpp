@@ -379,11 +379,40 @@ void direct_plan(const cnn_problem& p, int dtype, cnn_plan_t* plan) {
   fill_common(p, dtype, plan);
 }
 
+// Case 2 of Sec. 2.1 (W_c < N_c) on one GPU: the plain staging plan with its
+// channel loop split over kc workgroup slices of ceil(stages/kc) stages.  kc
+// is the smallest count with no empty slice that gives at least two
+// workgroups per CU, else one slice per stage.  The workspace holds kc fp32
+// partial Outs.
+static void splitc_finish(const cnn_problem& p, const cnn_budget& bud, cnn_plan_t* plan) {
+  const int64_t stages = ceil_div(p.Nc, plan->tc);
+  int64_t kc = std::min<int64_t>(stages, std::max<int64_t>(1, ceil_div(2 * bud.cus, plan->grid)));
+  while (ceil_div(stages, ceil_div(stages, kc)) != kc) ++kc;  // ends at kc = stages
+  plan->kernel = CNN_K_SPLITC;
+  plan->kc = (int32_t)kc;
+  plan->ws_bytes = 4 * kc * p.Nb * p.Nk * p.Nw * p.Nh;
+}
+
 int select_plan(const cnn_problem& p, int dtype, const cnn_budget& bud, int kernel,
                 int64_t tk, int64_t tp, int64_t tc, cnn_plan_t* out) {
   if (kernel == CNN_K_DIRECT) {
     direct_plan(p, dtype, out);
     return CNN_OK;
+  }
+  if (kernel == CNN_K_SPLITC) {
+    int n = 0;
+    const Variant* vs = variants(&n);
+    for (int i = 0; i < n; ++i) {
+      const Variant& v = vs[i];
+      if (v.dtype != dtype || v.kernel != CNN_K_IGEMM || v.tk != tk || v.tp != tp || v.tc != tc)
+        continue;
+      double t;
+      if (!eval_variant(p, dtype, v, bud, out, &t)) continue;
+      splitc_finish(p, bud, out);
+      fill_common(p, dtype, out);
+      return CNN_OK;
+    }
+    return CNN_E_UNSUPPORTED;
   }
   if (kernel != CNN_K_AUTO && kernel != CNN_K_IGEMM && kernel != CNN_K_IGEMM_PIPE &&
       kernel != CNN_K_IGEMM_DMA && kernel != CNN_K_IGEMM_WIDE && kernel != CNN_K_IGEMM_RAWK &&
@@ -646,8 +675,14 @@ int enumerate_plans(const cnn_problem& p, int dtype, const cnn_budget& bud, cnn_
   const Variant* vs = variants(&n1);
   for (int i = 0; i < n1; ++i)
     if (vs[i].dtype == dtype && vs[i].kernel == CNN_K_IGEMM &&
-        eval_variant(p, dtype, vs[i], bud, &cand, &t))
+        eval_variant(p, dtype, vs[i], bud, &cand, &t)) {
       add(cand, CNN_K_IGEMM);
+      // too few tiles for the chip and more than one stage: the split form
+      if (cand.grid < bud.cus && ceil_div(p.Nc, cand.tc) > 1 && n < cap) {
+        splitc_finish(p, bud, &cand);
+        add(cand, CNN_K_SPLITC);
+      }
+    }
   if (n == 0 && cap > 0) direct_plan(p, dtype, &out[n++]);
   return n;
 }

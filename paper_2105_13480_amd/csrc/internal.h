@@ -194,6 +194,13 @@ hipError_t launch_direct(const void* In, const void* Ker, void* Out, const ConvA
                          int dtype, hipStream_t stream);
 hipError_t launch_igemm(const Variant& v, const void* In, const void* Ker, void* Out,
                         const ConvArgs& a, int64_t lds_bytes, hipStream_t stream);
+// Split channels: conv_igemm over kc channel slices of
+// splitc_slice_channels(Nc, tc, kc) channels each, fp32 partials in `ws`
+// (kc * out_total floats), then their sum in slice order into Out.
+int64_t splitc_slice_channels(int64_t Nc, int64_t tc, int64_t kc);
+hipError_t launch_splitc(const Variant& v, const void* In, const void* Ker, void* Out,
+                         void* ws, const ConvArgs& a, int64_t lds_bytes, int kc, int dtype,
+                         hipStream_t stream);
 hipError_t launch_igemm3(const Variant3& v, const void* In, const void* Ker, void* Out,
                          void* ws, const ConvArgs& a, int64_t lds_bytes, hipStream_t stream);
 // Runs the pipelined kernel; non-raw-Ker variants first pack Ker into `ws`

@@ -23,6 +23,14 @@
 // channels per 16-byte vector for bf16: lane reads of one tap are then
 // 16-byte vectors at consecutive positions.
 // Ker tile: staged [tap][c/KV][k][KV], so A reads are consecutive vectors.
+//
+// Split channels (the paper's Case 2, P_c > 1): launched with gridDim.y = kc,
+// workgroup (tile, z) walks only the channels [z*cs, z*cs + cs) (cs a
+// multiple of TC, so no stage straddles two slices) and writes its fp32
+// partial tile to slice z of a workspace laid out as Out; splitc_reduce then
+// adds the kc slices in slice order (a fixed order: the result does not
+// depend on which workgroup finishes first) and writes Out.  Unsplit
+// launches have gridDim.y = 1 and cs >= Nc.
 #include "internal.h"
 #include "common.h"
 
@@ -65,7 +73,7 @@ __device__ __forceinline__ u32x4_t gather(const bf16_t* __restrict__ p, int64_t 
 template <typename TI, typename TO, int WM, int WN, int MB, int NB, int TC>
 __global__ __launch_bounds__(256) void conv_igemm(const TI* __restrict__ In,
                                                   const TI* __restrict__ Ker,
-                                                  TO* __restrict__ Out, ConvArgs a) {
+                                                  TO* __restrict__ Out, ConvArgs a, int cs) {
   constexpr int KV = Pack<TI>::KV;
   typedef typename Pack<TI>::V V;
   constexpr int TK = 32 * WM * MB;
@@ -129,7 +137,10 @@ __global__ __launch_bounds__(256) void conv_igemm(const TI* __restrict__ In,
       for (int j = 0; j < 16; ++j) acc[mb][nb][j] = 0.f;
 
   const int gpos0 = G0 * a.Ny;  // flattened (b, x, y) index of the slab start
-  for (int c0 = 0; c0 < a.Nc; c0 += TC) {
+  const int c_begin = (int)blockIdx.y * cs;
+  const int c_end = min(a.Nc, c_begin + cs);
+  Out += (int64_t)blockIdx.y * a.out_total;  // this slice's partial Out
+  for (int c0 = c_begin; c0 < c_end; c0 += TC) {
     __syncthreads();  // previous stage fully consumed
     // In slab: positions are consecutive in y, then x, then b.
     for (int pos = tid; pos < SNt; pos += 256) {
@@ -244,9 +255,14 @@ int64_t igemm_lds_bytes(const Variant& v, int64_t slab_rows, int64_t Ny, int64_t
 
 template <int DT, int WM, int WN, int MB, int NB, int TC>
 static hipError_t launch_one(const void* In, const void* Ker, void* Out, const ConvArgs& a,
-                             int64_t lds, hipStream_t stream) {
+                             int64_t lds, hipStream_t stream, int kc, int cs, bool split) {
   typedef typename DtypeTypes<DT>::TI TI;
   typedef typename DtypeTypes<DT>::TO TO;
+  // split launches write fp32 partial sums whatever the Out type: the bf16
+  // instantiation with fp32 Out
+  if constexpr (DT == CNN_BF16_OBF16)
+    if (split)
+      return launch_one<CNN_BF16, WM, WN, MB, NB, TC>(In, Ker, Out, a, lds, stream, kc, cs, true);
   auto kern = conv_igemm<TI, TO, WM, WN, MB, NB, TC>;
   static bool attr_set = false;  // benign race: every caller sets the same value
   if (!attr_set) {
@@ -255,22 +271,62 @@ static hipError_t launch_one(const void* In, const void* Ker, void* Out, const C
     if (e != hipSuccess) return e;
     attr_set = true;
   }
-  hipLaunchKernelGGL(kern, dim3((unsigned)a.grid), dim3(256), (unsigned)lds, stream,
-                     (const TI*)In, (const TI*)Ker, (TO*)Out, a);
+  hipLaunchKernelGGL(kern, dim3((unsigned)a.grid, (unsigned)kc), dim3(256), (unsigned)lds, stream,
+                     (const TI*)In, (const TI*)Ker, (TO*)Out, a, cs);
   return hipGetLastError();
 }
 
-hipError_t launch_igemm(const Variant& v, const void* In, const void* Ker, void* Out,
-                        const ConvArgs& a, int64_t lds_bytes, hipStream_t stream) {
+// Out[o] = sum over z = 0 .. kc-1, in that order, of Part[z][o].
+template <typename TO>
+__global__ __launch_bounds__(256) void splitc_reduce(const float* __restrict__ Part,
+                                                     TO* __restrict__ Out, int kc, int64_t n) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t o = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; o < n; o += stride) {
+    float s = Part[o];
+    for (int z = 1; z < kc; ++z) s += Part[(int64_t)z * n + o];
+    Out[o] = from_f32<TO>(s);
+  }
+}
+
+static hipError_t launch_igemm_kc(const Variant& v, const void* In, const void* Ker, void* Out,
+                                  const ConvArgs& a, int64_t lds_bytes, hipStream_t stream,
+                                  int kc, int cs, bool split) {
   switch (v.id) {
 #define CNN_CASE(id, dt, wm, wn, mb, nb, tc) \
   case id:                                   \
-    return launch_one<dt, wm, wn, mb, nb, tc>(In, Ker, Out, a, lds_bytes, stream);
+    return launch_one<dt, wm, wn, mb, nb, tc>(In, Ker, Out, a, lds_bytes, stream, kc, cs, split);
     CNN_IGEMM_VARIANTS(CNN_CASE)
 #undef CNN_CASE
     default:
       return hipErrorInvalidValue;
   }
+}
+
+hipError_t launch_igemm(const Variant& v, const void* In, const void* Ker, void* Out,
+                        const ConvArgs& a, int64_t lds_bytes, hipStream_t stream) {
+  return launch_igemm_kc(v, In, Ker, Out, a, lds_bytes, stream, 1, a.Nc, false);
+}
+
+int64_t splitc_slice_channels(int64_t Nc, int64_t tc, int64_t kc) {
+  const int64_t stages = (Nc + tc - 1) / tc;
+  return (stages + kc - 1) / kc * tc;
+}
+
+hipError_t launch_splitc(const Variant& v, const void* In, const void* Ker, void* Out,
+                         void* ws, const ConvArgs& a, int64_t lds_bytes, int kc, int dtype,
+                         hipStream_t stream) {
+  const int cs = (int)splitc_slice_channels(a.Nc, v.tc, kc);
+  hipError_t e = launch_igemm_kc(v, In, Ker, ws, a, lds_bytes, stream, kc, cs, true);
+  if (e != hipSuccess) return e;
+  int64_t blocks = (a.out_total + 255) / 256;
+  if (blocks > 2048) blocks = 2048;  // grid-stride loop covers the rest
+  if (dtype == CNN_BF16_OBF16)
+    hipLaunchKernelGGL(splitc_reduce<bf16_t>, dim3((unsigned)blocks), dim3(256), 0, stream,
+                       (const float*)ws, (bf16_t*)Out, kc, a.out_total);
+  else
+    hipLaunchKernelGGL(splitc_reduce<float>, dim3((unsigned)blocks), dim3(256), 0, stream,
+                       (const float*)ws, (float*)Out, kc, a.out_total);
+  return hipGetLastError();
 }
 
 }  // namespace cnnlib

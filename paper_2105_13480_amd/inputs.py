@@ -79,6 +79,10 @@ WORKLOADS = [
     Workload("pointwise_s2_b64", 6, 64, 256, 512, 28, 28, 1, 1, 2, 2, "bf16",
              ("uniform", 0.0, 1.0), ("he",),
              "supplementary strided pointwise: Nb=64 Nc=256 Nk=512, 28x28 out, 1x1, stride 2"),
+    Workload("late3x3_b1", 7, 1, 512, 512, 7, 7, 3, 3, 1, 1, "bf16",
+             ("uniform", 0.0, 1.0), ("he",),
+             "supplementary deep layer at batch 1: Nb=1 Nc=Nk=512, 7x7 out, 3x3, stride 1 "
+             "(few output tiles, many channels: the channel-split plans)"),
 ]
 
 BY_NAME = {w.name: w for w in WORKLOADS}

@@ -185,3 +185,53 @@ def test_plan_find_and_lookup_validate_before_hip():
     assert L.cnn_plan_lookup(None, cnn.CNN_F32, ctypes.byref(pl)) == -1
     assert L.cnn_plan_lookup(ctypes.byref(p), 5, ctypes.byref(pl)) == -3
     assert L.cnn_plan_lookup(ctypes.byref(q), cnn.CNN_F32, ctypes.byref(pl)) == -2
+
+
+SPLITC_PLANS = [((1, 16, 16, 16, 16, 3, 3, 1, 1), cnn.CNN_F32, 64, 64, 8),
+                ((1, 224, 64, 64, 110, 1, 1, 1, 1), cnn.CNN_BF16, 64, 64, 32),  # 7 stages, grid 110
+                ((1, 512, 512, 7, 7, 3, 3, 1, 1), cnn.CNN_BF16, 64, 64, 32),
+                ((1, 512, 512, 7, 7, 3, 3, 1, 1), cnn.CNN_BF16_OBF16, 128, 128, 32),
+                ((2, 200, 48, 6, 5, 3, 2, 2, 1), cnn.CNN_BF16, 64, 64, 32),
+                ((64, 24, 16, 28, 28, 3, 3, 1, 1), cnn.CNN_F32, 64, 64, 8)]
+
+
+@pytest.mark.parametrize("case", SPLITC_PLANS)
+def test_splitc_plan_is_the_staging_tiling_split_over_channels(case):
+    """CNN_K_SPLITC (Case 2 of Sec. 2.1, W_c < N_c): the CNN_K_IGEMM tiling
+    with kc channel slices of ceil(stages/kc) stages, none empty; enough
+    slices for two workgroups per CU unless every stage is its own slice,
+    and no more; a workspace of kc fp32 partial Outs."""
+    dims, dt, tk, tp, tc = case
+    bud = cnn.budget()
+    p = cnn.problem(*dims)
+    base = cnn.plan_tiles(p, dt, cnn.K_IGEMM, tk, tp, tc, bud)
+    sp = cnn.plan_tiles(p, dt, cnn.K_SPLITC, tk, tp, tc, bud)
+    same = ("variant", "tk", "tp", "tc", "grid", "lds_bytes", "slab_rows")
+    assert [getattr(sp, f) for f in same] == [getattr(base, f) for f in same]
+    assert sp.kernel == cnn.K_SPLITC and base.kc == 0 and base.ws_bytes == 0
+    Nb, Nc, Nk, Nw, Nh = dims[:5]
+    stages = -(-Nc // tc)
+
+    def nonempty(k):  # k slices of ceil(stages/k) stages: none empty
+        return (k - 1) * -(-stages // k) < stages
+
+    kc = sp.kc
+    assert 1 <= kc <= stages and nonempty(kc)
+    assert base.grid * kc >= 2 * bud.cus or kc == stages
+    for k in range(1, kc):  # no smaller valid count is enough
+        assert not (nonempty(k) and base.grid * k >= 2 * bud.cus), k
+    assert sp.ws_bytes == 4 * kc * Nb * Nk * Nw * Nh
+
+
+def test_splitc_bad_slice_count_rejected_before_hip():
+    dims = (1, 16, 16, 16, 16, 3, 3, 1, 1)
+    p = cnn.problem(*dims)
+    pl = cnn.plan_tiles(p, cnn.CNN_F32, cnn.K_SPLITC, 64, 64, 8, cnn.budget())
+    L = cnn.lib()
+    nout = 16 * 16 * 16
+    for kc, ws in [(0, 0), (3, 4 * 3 * nout), (2, 4 * 2 * nout - 4), (-1, 4 * nout)]:
+        q = cnn.Plan.from_buffer_copy(pl)
+        q.kc, q.ws_bytes = kc, ws
+        st = L.cnn_fwd_plan(0x1000, 0x100000, 0x200000, ctypes.byref(p), cnn.CNN_F32,
+                            ctypes.byref(q), None)
+        assert st == -8, (kc, ws)

@@ -443,3 +443,86 @@ def test_gemm1_stride2_exact(shape, mode):
             assert np.array_equal(got, want), (vid, pl.tp)
             ran += 1
     assert ran > 0
+
+
+# ---- channel slices (CNN_K_SPLITC, Case 2 of Sec. 2.1) --------------------
+SPLITC_CASES = [
+    ((1, 16, 16, 16, 16, 3, 3, 1, 1), "f32", 64, 64, 8),         # the tiny workload: 2 stages
+    ((1, 70, 40, 7, 7, 3, 3, 1, 1), "bf16", 64, 64, 32),         # 3 stages, the last ragged
+    ((2, 200, 48, 6, 5, 3, 2, 2, 1), "bf16_obf16", 64, 64, 32),  # 7 stages, strides (2, 1)
+    ((1, 37, 20, 9, 4, 1, 1, 1, 1), "f32", 64, 64, 8),           # 1x1, ragged channel tail
+    ((3, 45, 150, 5, 6, 3, 3, 1, 1), "bf16", 128, 256, 16),      # two k tiles, the second ragged
+]
+
+
+def _splitc_kcs(Nc, tc, kc_plan):
+    stages = -(-Nc // tc)
+    return sorted({1, 2, stages - 1, stages, kc_plan} & set(range(1, stages + 1)))
+
+
+@pytest.mark.parametrize("case", SPLITC_CASES)
+def test_splitc_exact(case):
+    """Channel slices: bit-exact with the oracle on integer inputs for kc =
+    1, 2, stages - 1 (some slices empty), stages and the plan's own kc.
+    Integer partial sums are exact in fp32, so the slice order cannot show."""
+    dims, mode, tk, tp, tc = case
+    Nb, Nc, Nk, Nw, Nh, Nr, Ns, sw, sh = dims
+    In, Ker = _arrays(dims, mode, seed=sum(dims) + 31, dist=("int", -3, 3), kdist=("int", -3, 3))
+    want = oracle.conv(In, Ker, sw, sh)
+    if mode == "bf16_obf16":
+        want = inputs.bf16_bits_to_f32(inputs.f32_to_bf16_bits(want.astype(np.float32))).astype(np.float64)
+    pl = cnn.plan_tiles(cnn.problem(*dims), MODES[mode], cnn.K_SPLITC, tk, tp, tc)
+    assert pl.kernel == cnn.K_SPLITC
+    for kc in _splitc_kcs(Nc, tc, pl.kc):
+        pl.kc, pl.ws_bytes = kc, 4 * kc * Nb * Nk * Nw * Nh
+        say(f"[parity] splitc dims={dims} mode={mode} v{pl.variant} grid={pl.grid} kc={kc}")
+        got = run(In, Ker, sw, sh, mode, plan=pl)
+        assert np.array_equal(got, want), kc
+
+
+@pytest.mark.parametrize("mode", ["bf16", "bf16_obf16"])
+def test_splitc_float_late_layer(mode):
+    """The batch-1 deep layer (512 -> 512 channels, 7x7 outputs) on uniform
+    inputs with its split plan (16 slices): every output within the bf16
+    tolerance of the fp64 oracle."""
+    w = inputs.BY_NAME["late3x3_b1"]
+    In, Ker = inputs.make_inputs(w)
+    pl = cnn.plan_tiles(cnn.problem(*w.dims()), MODES[mode], cnn.K_SPLITC, 64, 64, 32)
+    assert pl.kc > 1
+    say(f"[parity] splitc late3x3_b1 mode={mode} v{pl.variant} grid={pl.grid} kc={pl.kc}")
+    got = run(In, Ker, 1, 1, mode, plan=pl)
+    want, absv = oracle.conv(In, Ker, 1, 1, with_abs=True)
+    nw, cond, _ = errors(got, want, absv)
+    assert nw < TOL[mode] and cond < TOL[mode], (nw, cond)
+
+
+def test_splitc_caller_workspace_in_graph():
+    """cnn_fwd_plan_ws with a caller workspace, captured into a HIP graph and
+    replayed several times with eager work in between: every replay equals
+    the eager result bit for bit (the reduction order is fixed)."""
+    import torch
+    dims = (1, 70, 40, 7, 7, 3, 3, 1, 1)
+    In, Ker = _arrays(dims, "bf16", seed=77)
+    pl = cnn.plan_tiles(cnn.problem(*dims), cnn.CNN_BF16, cnn.K_SPLITC, 64, 64, 32)
+    dIn, dKer = to_gpu(In), to_gpu(Ker)
+    ws = torch.empty(pl.ws_bytes // 4, dtype=torch.float32, device="cuda")
+    ref = out_tensor(1, 40, 7, 7, "bf16")
+    say(f"[parity] splitc eager kc={pl.kc}")
+    cnn.fwd_plan_ws(dIn, dKer, ref, pl, ws)
+    torch.cuda.synchronize()
+    out = out_tensor(1, 40, 7, 7, "bf16")
+    s = torch.cuda.Stream()
+    g = torch.cuda.CUDAGraph()
+    say("[parity] splitc graph capture")
+    with torch.cuda.graph(g, stream=s):
+        cnn.fwd_plan_ws(dIn, dKer, out, pl, ws)
+    for i in range(4):
+        out.fill_(float("nan"))
+        ws.fill_(float("nan"))
+        torch.cuda.synchronize()
+        say(f"[parity] splitc graph replay {i}")
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(out, ref), i
+    want = oracle.conv(In, Ker, 1, 1)
+    assert np.abs(to_host64(ref) - want).max() <= TOL["bf16"] * np.abs(want).max()

@@ -43,6 +43,8 @@ def test_workload_extents():
     assert ext["conv3x3_s2_b64"] == (57, 57)
     assert ext["pointwise_b256"] == (14, 14)
     assert ext["stem7x7_s2_b64"] == (229, 229)
+    assert ext["pointwise_s2_b64"] == (55, 55)
+    assert ext["late3x3_b1"] == (9, 9)
 
 
 def test_he_normal_scale():
