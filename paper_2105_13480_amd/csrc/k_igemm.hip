@@ -276,14 +276,25 @@ static hipError_t launch_one(const void* In, const void* Ker, void* Out, const C
   return hipGetLastError();
 }
 
-// Out[o] = sum over z = 0 .. kc-1, in that order, of Part[z][o].
+// Out[o] = sum over z = 0 .. kc-1, in that order, of Part[z][o].  Eight
+// slices are loaded at a time (independent loads in flight together); the
+// additions stay in slice order.
 template <typename TO>
 __global__ __launch_bounds__(256) void splitc_reduce(const float* __restrict__ Part,
                                                      TO* __restrict__ Out, int kc, int64_t n) {
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   for (int64_t o = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; o < n; o += stride) {
-    float s = Part[o];
-    for (int z = 1; z < kc; ++z) s += Part[(int64_t)z * n + o];
+    const float* p = Part + o;
+    float s = p[0];
+    int z = 1;
+    for (; z + 8 <= kc; z += 8) {
+      float v[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) v[i] = p[(int64_t)(z + i) * n];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) s += v[i];
+    }
+    for (; z < kc; ++z) s += p[(int64_t)z * n];
     Out[o] = from_f32<TO>(s);
   }
 }

@@ -452,6 +452,7 @@ SPLITC_CASES = [
     ((2, 200, 48, 6, 5, 3, 2, 2, 1), "bf16_obf16", 64, 64, 32),  # 7 stages, strides (2, 1)
     ((1, 37, 20, 9, 4, 1, 1, 1, 1), "f32", 64, 64, 8),           # 1x1, ragged channel tail
     ((3, 45, 150, 5, 6, 3, 3, 1, 1), "bf16", 128, 256, 16),      # two k tiles, the second ragged
+    ((1, 300, 20, 4, 4, 3, 3, 1, 1), "f32", 64, 64, 8),          # 38 stages: kc 37 and 38
 ]
 
 
