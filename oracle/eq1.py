@@ -17,9 +17,10 @@ with sw, sh the strides sigma_w, sigma_h; a box tiling is
   T_bhw consecutive outputs of the flattened (b, w, h) index (Sec. 2 treats
   b, h, w as one composite index), each loading whole input rows.
 * :func:`eq4_cost`, :func:`case1a_tiles`, :func:`case1a_cost`,
-  :func:`relaxed_capacity`, :func:`table1_cost` -- Sec. 2.1: the relaxed
-  problem Eq. (4), its Case 1a optimum Eq. (6), the capacity M_L that makes
-  the relaxed optimum a valid tiling, and the Table 1 optima.
+  :func:`relaxed_capacity`, :func:`table1_cost`, :func:`table1_tiles` --
+  Sec. 2.1: the relaxed problem Eq. (4), its Case 1a optimum Eq. (6), the
+  capacity M_L that makes the relaxed optimum a valid tiling, the Table 1
+  optima and the tiles of each Table 1 row (Cases 1a, 2a, 2b).
 """
 from __future__ import annotations
 
@@ -189,3 +190,23 @@ def table1_cost(p: Problem, P: int, ML: float) -> float:
     if ML >= thr:
         return 3.0 * thr
     return ML + 2.0 * V / math.sqrt(ML) * math.sqrt(Q)
+
+
+def table1_tiles(p: Problem, P: int, ML: float):
+    """(row, Tk, Tbhw) of the Table 1 optimum.
+
+    Row 1 (Nk Nbhw / P >= ML): Case 1a, W_c = N_c, Tk and Tbhw of
+    :func:`case1a_tiles`.  Row 2 (ML >= V^(2/3) Q^(1/3), V = Nk Nc Nbhw / P,
+    Q = Nr Ns sw sh): Case 2a, W_c < N_c with T = W,
+    Tk = (V / (Nr Ns))^(1/3) (sw sh)^(2/3),
+    Tbhw = (V / (sw sh))^(1/3) (Nr Ns)^(2/3).  Row 3: Case 2b, the Case 1a
+    expressions (the capacity binds).
+    """
+    Nbhw = p.Nb * p.Nw * p.Nh
+    V = p.Nk * p.Nc * Nbhw / P
+    RS, ss = p.Nr * p.Ns, p.sw * p.sh
+    if p.Nk * Nbhw / P >= ML:
+        return (1,) + case1a_tiles(ML, p.Nr, p.Ns, p.sw, p.sh)
+    if ML >= V ** (2.0 / 3.0) * (RS * ss) ** (1.0 / 3.0):
+        return 2, (V / RS) ** (1.0 / 3.0) * ss ** (2.0 / 3.0), (V / ss) ** (1.0 / 3.0) * RS ** (2.0 / 3.0)
+    return (3,) + case1a_tiles(ML, p.Nr, p.Ns, p.sw, p.sh)

@@ -179,6 +179,40 @@ def test_table1_continuous_at_regime_boundaries():
     assert abs(eq1.case1a_cost(p, P, A / 2) - eq1.table1_cost(p, P, A / 2)) < 1e-9 * A
 
 
+@pytest.mark.parametrize("p,P", [(Problem(2, 64, 128, 14, 14, 3, 3, 2, 2), 16),
+                                 (Problem(1, 512, 512, 7, 7, 3, 3, 1, 1), 256),
+                                 (Problem(8, 3, 64, 56, 56, 7, 5, 2, 1), 64)])
+def test_table1_tiles_attain_the_row_cost_in_eq4(p, P):
+    """Each Table 1 row's tiles, put into the Eq. (4) objective with the
+    row's W (W_c = N_c in row 1; W = T, W_c < N_c in rows 2 and 3), give the
+    row's cost; rows 1 and 3 fill M_L; row 2's tiles are a stationary point
+    (no nearby tile pair costs less) and fit M_L."""
+    Nbhw = p.Nb * p.Nw * p.Nh
+    A = p.Nk * Nbhw / P
+    V = p.Nk * p.Nc * Nbhw / P
+    thr = V ** (2 / 3) * (p.Nr * p.Ns * p.sw * p.sh) ** (1 / 3)
+    rows = set()
+    for ML in [A / 3, 2 * max(A, thr)] + ([(A + thr) / 2] if A < thr else []):
+        row, tk, tb = eq1.table1_tiles(p, P, ML)
+        rows.add(row)
+        want = eq1.table1_cost(p, P, ML)
+        if row == 1:
+            assert ML <= A
+            got = eq1.eq4_cost(p, P, p.Nk, Nbhw / P, tk, tb)  # Wk Wbhw = Nk Nbhw / P
+            assert abs(tk * tb - ML) < 1e-9 * ML
+        else:
+            got = eq1.eq4_cost(p, P, tk, tb, tk, tb)
+            if row == 3:
+                assert abs(tk * tb - ML) < 1e-9 * ML and ML < thr
+            else:
+                assert tk * tb <= ML * (1 + 1e-12) and ML >= thr
+                for fk in (0.97, 1.0, 1.03):
+                    for fb in (0.97, 1.0, 1.03):
+                        assert eq1.eq4_cost(p, P, tk * fk, tb * fb, tk * fk, tb * fb) >= got * (1 - 1e-12)
+        assert abs(got - want) < 1e-9 * want, (row, got, want)
+    assert rows >= {1, 2}
+
+
 @pytest.mark.parametrize("p", [Problem(3, 2, 2, 5, 7, 3, 3, 1, 1), Problem(2, 2, 2, 4, 6, 3, 2, 2, 1),
                                Problem(4, 1, 1, 3, 3, 1, 1, 1, 1), Problem(2, 1, 1, 6, 5, 5, 3, 2, 2)])
 @pytest.mark.parametrize("T", [1, 4, 7, 12, 32])
