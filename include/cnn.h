@@ -278,6 +278,33 @@ int cnn_eq1_cost(const cnn_problem* prob, const cnn_tiles* tiles, int halo_mode,
  */
 int cnn_slab_cost(const cnn_problem* prob, int64_t tk, int64_t tp, double terms[3]);
 
+/*
+ * Closed-form optimum of the relaxed tiling problem, Eq. (4) of Sec. 2.1,
+ * for P processors with M elements of fast memory each (host only, no HIP
+ * call).  capacity_mode 0 takes M_L = M (the costs are then lower bounds for
+ * any valid tiles); 1 takes M_L = M - (1/2) 3K (sqrt(9K^2 + 4M) - 3K),
+ * K = sqrt(sw sh Nr Ns), for which the tiles are valid for Eq. (3).  With
+ * V = Nk Nc Nbhw / P and Q = Nr Ns sw sh (Nbhw = Nb Nw Nh), the Table 1 row:
+ *   1: Nk Nbhw / P >= M_L (Case 1a, W_c = N_c): Eq. (6),
+ *      Tk = sqrt(M_L sw sh / (Nr Ns)), Tbhw = sqrt(M_L Nr Ns / (sw sh));
+ *   2: M_L >= V^(2/3) Q^(1/3) (Case 2a, W_c < N_c): Eq. (8),
+ *      Tk = (V / (Nr Ns))^(1/3) (sw sh)^(2/3), Tbhw = (V / (sw sh))^(1/3) (Nr Ns)^(2/3);
+ *   3: otherwise (Case 2b, W_c < N_c): Eq. (9), the Case 1a tiles.
+ * Tiles are real-valued; costs are elements moved per processor.  Errors:
+ * CNN_E_NULL, CNN_E_SHAPE (a problem size below 1, P < 1, M <= 0 or a
+ * capacity_mode other than 0 and 1).
+ */
+typedef struct cnn_closed_form_t {
+  double M_L;           /* capacity of the relaxed problem                         */
+  double Tk, Tbhw;      /* the row's optimal tile sizes                            */
+  double cost;          /* the row's cost (Table 1)                                */
+  int32_t row;          /* Table 1 row, 1 .. 3                                     */
+  int32_t split_c;      /* 1 when the optimum has W_c < N_c (rows 2 and 3)         */
+} cnn_closed_form_t;
+
+int cnn_closed_form(const cnn_problem* prob, double P, double M, int capacity_mode,
+                    cnn_closed_form_t* out);
+
 /* Budget of HIP device `device` (CU count, LDS per CU, accumulator regs). */
 int cnn_device_budget(int device, cnn_budget* budget);
 

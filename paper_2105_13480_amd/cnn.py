@@ -32,8 +32,8 @@ STATUS = {0: "CNN_OK", -1: "CNN_E_NULL", -2: "CNN_E_SHAPE", -3: "CNN_E_DTYPE",
 
 # Every symbol include/cnn.h declares.
 EXPORTS = ["cnn_fwd", "cnn_plan", "cnn_plan_find", "cnn_plan_lookup", "cnn_plan_tiles",
-           "cnn_fwd_plan", "cnn_fwd_plan_ws", "cnn_eq1_cost", "cnn_slab_cost", "cnn_device_budget", "cnn_strerror", "cnn_last_error",
-           "cnn_abi_version"]
+           "cnn_fwd_plan", "cnn_fwd_plan_ws", "cnn_eq1_cost", "cnn_slab_cost", "cnn_closed_form",
+           "cnn_device_budget", "cnn_strerror", "cnn_last_error", "cnn_abi_version"]
 
 i64 = ctypes.c_int64
 
@@ -64,6 +64,11 @@ class Plan(ctypes.Structure):
                 "lds_bytes": self.lds_bytes, "slab_rows": self.slab_rows, "ws_bytes": self.ws_bytes,
                 "eq1_elems": list(self.eq1_elems), "eq1_bytes": self.eq1_bytes,
                 "compulsory_bytes": self.compulsory_bytes, "flops": self.flops}
+
+
+class ClosedForm(ctypes.Structure):
+    _fields_ = [("M_L", ctypes.c_double), ("Tk", ctypes.c_double), ("Tbhw", ctypes.c_double),
+                ("cost", ctypes.c_double), ("row", ctypes.c_int32), ("split_c", ctypes.c_int32)]
 
 
 class CnnError(RuntimeError):
@@ -100,6 +105,8 @@ def lib():
     L.cnn_eq1_cost.argtypes = [P, T, ctypes.c_int, ctypes.POINTER(ctypes.c_double),
                                ctypes.POINTER(ctypes.c_double)]
     L.cnn_slab_cost.argtypes = [P, i64, i64, ctypes.POINTER(ctypes.c_double)]
+    L.cnn_closed_form.argtypes = [P, ctypes.c_double, ctypes.c_double, ctypes.c_int,
+                                  ctypes.POINTER(ClosedForm)]
     L.cnn_device_budget.argtypes = [ctypes.c_int, B]
     L.cnn_strerror.argtypes = [ctypes.c_int]
     L.cnn_strerror.restype = ctypes.c_char_p
@@ -107,7 +114,7 @@ def lib():
     L.cnn_last_error.restype = ctypes.c_char_p
     L.cnn_abi_version.argtypes = []
     for f in ("cnn_fwd", "cnn_plan", "cnn_plan_find", "cnn_plan_lookup", "cnn_plan_tiles", "cnn_fwd_plan", "cnn_fwd_plan_ws", "cnn_eq1_cost",
-              "cnn_slab_cost", "cnn_device_budget", "cnn_abi_version"):
+              "cnn_slab_cost", "cnn_closed_form", "cnn_device_budget", "cnn_abi_version"):
         getattr(L, f).restype = ctypes.c_int
     _lib = L
     return L
@@ -167,6 +174,14 @@ def slab_cost(prob: Problem, tk: int, tp: int):
     terms = (ctypes.c_double * 3)()
     _check(lib().cnn_slab_cost(ctypes.byref(prob), tk, tp, terms))
     return tuple(terms)
+
+
+def closed_form(prob: Problem, P: float, M: float, capacity_mode: int = 0) -> ClosedForm:
+    """Table 1 optimum of Eq. (4): capacity_mode 0 = M_L = M (lower bound),
+    1 = the relaxed capacity valid for Eq. (3)."""
+    out = ClosedForm()
+    _check(lib().cnn_closed_form(ctypes.byref(prob), P, M, capacity_mode, ctypes.byref(out)))
+    return out
 
 
 # ---- compute entry points ------------------------------------------------

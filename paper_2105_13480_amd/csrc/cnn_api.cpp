@@ -647,6 +647,18 @@ int cnn_eq1_cost(const cnn_problem* prob, const cnn_tiles* tiles, int halo_mode,
   return CNN_OK;
 }
 
+int cnn_closed_form(const cnn_problem* prob, double P, double M, int capacity_mode,
+                    cnn_closed_form_t* out) {
+  if (!prob || !out) return fail(CNN_E_NULL, "prob and out must be non-NULL");
+  int st;
+  if ((st = check_problem(*prob))) return st;
+  if (!(P >= 1.0) || !(M > 0.0) || (capacity_mode != 0 && capacity_mode != 1))
+    return fail(CNN_E_SHAPE, "need P >= 1, M > 0 and capacity_mode 0 or 1");
+  closed_form(*prob, P, M, capacity_mode, out);
+  if (!(out->M_L > 0.0)) return fail(CNN_E_SHAPE, "M leaves no relaxed capacity");
+  return CNN_OK;
+}
+
 int cnn_slab_cost(const cnn_problem* prob, int64_t tk, int64_t tp, double terms[3]) {
   if (!prob || !terms) return fail(CNN_E_NULL, "prob and terms must be non-NULL");
   int st;

@@ -19,6 +19,7 @@
 // considered only when no tier-1 instantiation fits; the direct kernel
 // takes problems no implicit-GEMM tiling fits.
 #include <math.h>
+#include <cmath>
 #include <string.h>
 
 #include <algorithm>
@@ -377,6 +378,35 @@ void direct_plan(const cnn_problem& p, int dtype, cnn_plan_t* plan) {
   for (int i = 0; i < 3; ++i) plan->eq1_elems[i] = terms[i];
   plan->eq1_bytes = out_bytes(dtype) * terms[0] + in_bytes(dtype) * (terms[1] + terms[2]);
   fill_common(p, dtype, plan);
+}
+
+// Table 1 of Sec. 2.1: the closed-form optimum of Eq. (4).  The relaxed
+// capacity solves M_L + 3K sqrt(M_L) = M.
+void closed_form(const cnn_problem& p, double P, double M, int capacity_mode,
+                 cnn_closed_form_t* out) {
+  const double RS = (double)(p.Nr * p.Ns), ss = (double)(p.sw * p.sh), Q = RS * ss;
+  const double Nbhw = (double)p.Nb * (double)p.Nw * (double)p.Nh;
+  const double A = (double)p.Nk * Nbhw / P;   // Out per processor
+  const double V = A * (double)p.Nc;          // products per processor
+  double ML = M;
+  if (capacity_mode == 1) {
+    const double K = std::sqrt(Q);
+    ML = M - 0.5 * 3.0 * K * (std::sqrt(9.0 * K * K + 4.0 * M) - 3.0 * K);
+  }
+  const double ridge = std::cbrt(V * V) * std::cbrt(Q);  // V^(2/3) Q^(1/3)
+  out->M_L = ML;
+  if (A >= ML || ML < ridge) {  // the capacity binds: Cases 1a and 2b
+    out->row = A >= ML ? 1 : 3;
+    out->Tk = std::sqrt(ML * ss / RS);
+    out->Tbhw = std::sqrt(ML * RS / ss);
+    out->cost = (A >= ML ? A : ML) + 2.0 * V * std::sqrt(Q / ML);
+  } else {                      // Case 2a: the unconstrained optimum fits
+    out->row = 2;
+    out->Tk = std::cbrt(V / RS) * std::cbrt(ss * ss);
+    out->Tbhw = std::cbrt(V / ss) * std::cbrt(RS * RS);
+    out->cost = 3.0 * ridge;
+  }
+  out->split_c = out->row != 1;
 }
 
 // Case 2 of Sec. 2.1 (W_c < N_c) on one GPU: the plain staging plan with its

@@ -194,6 +194,10 @@ hipError_t launch_direct(const void* In, const void* Ker, void* Out, const ConvA
                          int dtype, hipStream_t stream);
 hipError_t launch_igemm(const Variant& v, const void* In, const void* Ker, void* Out,
                         const ConvArgs& a, int64_t lds_bytes, hipStream_t stream);
+// Table 1 optimum of Eq. (4) (host).
+void closed_form(const cnn_problem& p, double P, double M, int capacity_mode,
+                 cnn_closed_form_t* out);
+
 // Split channels: conv_igemm over kc channel slices of
 // splitc_slice_channels(Nc, tc, kc) channels each, fp32 partials in `ws`
 // (kc * out_total floats), then their sum in slice order into Out.

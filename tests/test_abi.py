@@ -235,3 +235,42 @@ def test_splitc_bad_slice_count_rejected_before_hip():
         st = L.cnn_fwd_plan(0x1000, 0x100000, 0x200000, ctypes.byref(p), cnn.CNN_F32,
                             ctypes.byref(q), None)
         assert st == -8, (kc, ws)
+
+
+def test_closed_form_matches_oracle():
+    """cnn_closed_form (Table 1 of Sec. 2.1) against the oracle's Table 1
+    row, tiles, cost and relaxed capacity, on random problems, processor
+    counts and capacities spanning all three rows, in both capacity modes."""
+    rng = np.random.default_rng(7)
+    rows = set()
+    for _ in range(300):
+        Nr, Ns = (int(x) for x in rng.integers(1, 8, size=2))
+        dims = (int(rng.integers(1, 65)), int(rng.integers(1, 1025)), int(rng.integers(1, 1025)),
+                int(rng.integers(1, 113)), int(rng.integers(1, 113)), Nr, Ns,
+                int(rng.integers(1, 3)), int(rng.integers(1, 3)))
+        P = float(2 ** int(rng.integers(0, 11)))
+        M = float(10 ** rng.uniform(2, 8))
+        p = oeq1.Problem(*dims)
+        for mode in (0, 1):
+            cf = cnn.closed_form(cnn.problem(*dims), P, M, mode)
+            ML = M if mode == 0 else oeq1.relaxed_capacity(M, Nr, Ns, dims[7], dims[8])
+            row, tk, tb = oeq1.table1_tiles(p, P, ML)
+            cost = oeq1.table1_cost(p, P, ML)
+            assert abs(cf.M_L - ML) <= 1e-12 * M
+            assert cf.row == row and cf.split_c == (row != 1)
+            for got, want in ((cf.Tk, tk), (cf.Tbhw, tb), (cf.cost, cost)):
+                assert abs(got - want) <= 1e-9 * abs(want), (dims, P, M, mode, got, want)
+            rows.add(row)
+    assert rows == {1, 2, 3}
+
+
+def test_closed_form_rejects_bad_arguments():
+    L = cnn.lib()
+    p = cnn.problem(1, 2, 3, 4, 5, 3, 3, 1, 1)
+    out = cnn.ClosedForm()
+    assert L.cnn_closed_form(None, 4.0, 100.0, 0, ctypes.byref(out)) == -1
+    assert L.cnn_closed_form(ctypes.byref(p), 4.0, 100.0, 0, None) == -1
+    for P, M, mode in [(0.5, 100.0, 0), (4.0, 0.0, 0), (4.0, -1.0, 1), (4.0, 100.0, 2)]:
+        assert L.cnn_closed_form(ctypes.byref(p), P, M, mode, ctypes.byref(out)) == -2
+    q = cnn.problem(1, 0, 3, 4, 5, 3, 3, 1, 1)
+    assert L.cnn_closed_form(ctypes.byref(q), 4.0, 100.0, 0, ctypes.byref(out)) == -2
