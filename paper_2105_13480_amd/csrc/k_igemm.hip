@@ -143,6 +143,8 @@ __global__ __launch_bounds__(256) void conv_igemm(const TI* __restrict__ In,
   for (int c0 = c_begin; c0 < c_end; c0 += TC) {
     __syncthreads();  // previous stage fully consumed
     // In slab: positions are consecutive in y, then x, then b.
+    // (unrolled so that several positions' loads are in flight together)
+#pragma unroll 2
     for (int pos = tid; pos < SNt; pos += 256) {
       const int gp = gpos0 + pos;
       const int b = gp / a.nxny;
@@ -151,6 +153,7 @@ __global__ __launch_bounds__(256) void conv_igemm(const TI* __restrict__ In,
       for (int g = 0; g < G; ++g) lds_in[g * SN + pos] = gather(src, a.nxny, c0 + g * KV, a.Nc);
     }
     // Ker tile, [tap][group][k].
+#pragma unroll 4
     for (int idx = tid; idx < RS * G * TK; idx += 256) {
       const int kk = idx % TK;
       const int rest = idx / TK;
@@ -276,23 +279,42 @@ static hipError_t launch_one(const void* In, const void* Ker, void* Out, const C
   return hipGetLastError();
 }
 
-// Out[o] = sum over z = 0 .. kc-1, in that order, of Part[z][o].  Eight
-// slices are loaded at a time (independent loads in flight together); the
-// additions stay in slice order.
+// Out[o] = sum over z = 0 .. kc-1, in that order, of Part[z][o].  Slices
+// are loaded 16 (then 4) at a time, independent loads in flight together;
+// the additions stay in slice order.
 template <typename TO>
 __global__ __launch_bounds__(256) void splitc_reduce(const float* __restrict__ Part,
                                                      TO* __restrict__ Out, int kc, int64_t n) {
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   for (int64_t o = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; o < n; o += stride) {
     const float* p = Part + o;
-    float s = p[0];
-    int z = 1;
-    for (; z + 8 <= kc; z += 8) {
-      float v[8];
+    float s;
+    int z;
+    if (kc >= 16) {
+      float v[16];
 #pragma unroll
-      for (int i = 0; i < 8; ++i) v[i] = p[(int64_t)(z + i) * n];
+      for (int i = 0; i < 16; ++i) v[i] = p[(int64_t)i * n];
+      s = v[0];
 #pragma unroll
-      for (int i = 0; i < 8; ++i) s += v[i];
+      for (int i = 1; i < 16; ++i) s += v[i];
+      z = 16;
+    } else {
+      s = p[0];
+      z = 1;
+    }
+    for (; z + 16 <= kc; z += 16) {
+      float v[16];
+#pragma unroll
+      for (int i = 0; i < 16; ++i) v[i] = p[(int64_t)(z + i) * n];
+#pragma unroll
+      for (int i = 0; i < 16; ++i) s += v[i];
+    }
+    for (; z + 4 <= kc; z += 4) {
+      float v[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) v[i] = p[(int64_t)(z + i) * n];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) s += v[i];
     }
     for (; z < kc; ++z) s += p[(int64_t)z * n];
     Out[o] = from_f32<TO>(s);
