@@ -167,12 +167,14 @@ ROWS = [
 
 # (id, dtype, wp, wk, mbp, nbk, tc, s2) of the 1x1 GEMM kernel: tk =
 # 32*wk*nbk, tp <= 32*wp*mbp (a multiple of 4), Nc % 8 == 0; s2 = 0: strides
-# 1 and Nw*Nh % 4 == 0; s2 = 1: strides 2 and 2, Nh % 4 == 0.
+# 1 and Nw*Nh % 4 == 0; s2 = 1: strides 2 and 2, Nh % 4 == 0; s2 = 2: strides
+# 1, a tile is one image (tp = Nw*Nh <= 32*wp*mbp - 8, Nw*Nh % 4 == 0), LDS
+# a ring of 4 stages.
 GEMM1 = [
     (1700, BF16, 2, 4, 4, 2, 64, 0), (1701, BF16, 4, 2, 2, 2, 64, 0),
-    (1702, BF16, 2, 4, 4, 2, 32, 1),
+    (1702, BF16, 2, 4, 4, 2, 32, 1), (1709, BF16, 2, 4, 4, 2, 32, 2),
     (1800, BF16_OBF16, 2, 4, 4, 2, 64, 0), (1801, BF16_OBF16, 4, 2, 2, 2, 64, 0),
-    (1802, BF16_OBF16, 2, 4, 4, 2, 32, 1),
+    (1802, BF16_OBF16, 2, 4, 4, 2, 32, 1), (1809, BF16_OBF16, 2, 4, 4, 2, 32, 2),
 ]
 
 
@@ -381,18 +383,27 @@ def _special(p: eq1.Problem, dtype: int, cus: int, lds_bytes: int, acc_regs: int
     for vid, dt, wp, wk, mbp, nbk, tc, s2 in GEMM1:
         if dt != dtype or p.Nr != 1 or p.Ns != 1 or p.Nc % 8:
             continue
-        if s2 and not (p.sw == 2 and p.sh == 2 and p.Nh % 4 == 0):
+        if s2 == 1 and not (p.sw == 2 and p.sh == 2 and p.Nh % 4 == 0):
             continue
-        if not s2 and not (p.sw == 1 and p.sh == 1 and (p.Nw * p.Nh) % 4 == 0):
+        if s2 != 1 and not (p.sw == 1 and p.sh == 1 and (p.Nw * p.Nh) % 4 == 0):
             continue
         tk, tpmax, acc = 32 * wk * nbk, 32 * wp * mbp, 16 * mbp * nbk
-        lds = 2 * (tc * (tpmax + 16) + tk * (tc + 8)) * 2
+        if s2 == 2 and p.Nw * p.Nh > tpmax - 8:
+            continue
+        if s2 == 2:  # four stages of whole 512-unit copy rounds (16-byte units)
+            units = tk * 4 + tc * (((tpmax - 8) // 8) | 1)
+            nt = 64 * wp * wk
+            lds = 4 * -(-units // nt) * nt * 16
+        else:
+            lds = 2 * (tc * (tpmax + 16) + tk * (tc + 8)) * 2
         nx, ny = p.sw * (p.Nw - 1) + 1, p.sh * (p.Nh - 1) + 1
         if (lds > lds_cap or p.Nb * p.Nc * nx * ny * 2 >= 2 ** 30
                 or p.Nk * p.Nc * 2 >= 2 ** 30 or out_big):
             continue
         occ = max(1, min(wg_per_cu, lds_bytes // lds))
         tp = min(tpmax, -(-balanced_tp(p, tpmax, tk, cus * occ, 1) // 4) * 4)
+        if s2 == 2:
+            tp = p.Nw * p.Nh
         if tp % 4 or tp < 4 or acc > acc_regs:
             continue
         return (11, vid, tk, tp, tc)

@@ -323,6 +323,7 @@ static bool eval_gemm1(const cnn_problem& p, int dtype, const VariantG& v, const
   const int64_t occ = std::max<int64_t>(1, std::min<int64_t>(bud.wg_per_cu, bud.lds_bytes / lds));
   int64_t tp = balanced_tp(p, v.tp, v.tk, bud.cus * occ, 1);
   tp = std::min<int64_t>(v.tp, (tp + 3) / 4 * 4);
+  if (v.s2 == 2) tp = p.Nw * p.Nh;  // a tile is one image
   if (!gemm1_fits(v, p, tp)) return false;
   return eval_tiling(p, dtype, v.id, v.tk, tp, v.tc, v.acc, 1, lds, 0, bud, plan, time_clk);
 }

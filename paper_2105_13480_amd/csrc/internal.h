@@ -158,7 +158,10 @@ struct VariantG {
   int32_t tk, tp, tc;  // tp = largest tile
   int32_t threads;
   int32_t acc;
-  int32_t s2;          // 1: strides 2 and 2 (gathers the even input rows and columns)
+  int32_t s2;          // 0: stride 1; 1: strides 2 and 2 (gathers the even input rows
+                       // and columns); 2: stride 1, whole-image tiles (at most
+                       // tp - 8 pixels), operands copied by DMA into a ring of 4
+                       // stages
 };
 const VariantG* variants_gemm1(int* count);
 int64_t gemm1_lds_bytes(const VariantG& v);

@@ -287,16 +287,222 @@ __global__ __launch_bounds__(64 * WP * WK) void conv_gemm1(const bf16_t* __restr
   }
 }
 
+// 16-byte buffer -> LDS copy: lane i's 16 bytes land at lds + 16 i (lds
+// wave-uniform); out-of-range reads give zeros.
+__device__ __forceinline__ void dma16_g(__amdgpu_buffer_rsrc_t r, void* lds, uint32_t voff) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, LDS_PTR_G(void, lds), 16, voff, 0, 0, 0);
+#else
+  (void)r;
+  (void)lds;
+  (void)voff;
+#endif
+}
+
+// The eight transposing reads of a K-step's A operands (four 32-pixel
+// blocks, rows r0 and r1 = r0 + 4 channels) in one block that also waits for
+// them.  As inline assembly they carry no memory operands the compiler could
+// match against the buffer->LDS copies in flight, so it adds no wait for
+// those copies (it would wait for all of them before a transposing-read
+// builtin); the values are defined only once the block's own wait is done.
+__device__ __forceinline__ void read_a4_tr(const bf16_t* r0, const bf16_t* r1, u32x4_t (&A)[4]) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  const uint32_t p0 = (uint32_t)(uintptr_t)LDS_PTR_G(bf16_t, const_cast<bf16_t*>(r0));
+  const uint32_t p1 = (uint32_t)(uintptr_t)LDS_PTR_G(bf16_t, const_cast<bf16_t*>(r1));
+  u32x2_t l0, h0, l1, h1, l2, h2, l3, h3;
+  asm volatile(
+      "ds_read_b64_tr_b16 %0, %8\n\t"
+      "ds_read_b64_tr_b16 %1, %9\n\t"
+      "ds_read_b64_tr_b16 %2, %8 offset:64\n\t"
+      "ds_read_b64_tr_b16 %3, %9 offset:64\n\t"
+      "ds_read_b64_tr_b16 %4, %8 offset:128\n\t"
+      "ds_read_b64_tr_b16 %5, %9 offset:128\n\t"
+      "ds_read_b64_tr_b16 %6, %8 offset:192\n\t"
+      "ds_read_b64_tr_b16 %7, %9 offset:192\n\t"
+      "s_waitcnt lgkmcnt(0)"
+      : "=&v"(l0), "=&v"(h0), "=&v"(l1), "=&v"(h1), "=&v"(l2), "=&v"(h2), "=&v"(l3), "=&v"(h3)
+      : "v"(p0), "v"(p1)
+      : "memory");
+  A[0] = u32x4_t{l0[0], l0[1], h0[0], h0[1]};
+  A[1] = u32x4_t{l1[0], l1[1], h1[0], h1[1]};
+  A[2] = u32x4_t{l2[0], l2[1], h2[0], h2[1]};
+  A[3] = u32x4_t{l3[0], l3[1], h3[0], h3[1]};
+#else
+  (void)r0;
+  (void)r1;
+  for (int i = 0; i < 4; ++i) A[i] = u32x4_t{0u, 0u, 0u, 0u};
+#endif
+}
+
+// Stride 1 with tiles of whole images (tp = Nw*Nh <= 32*WP*MBP): both
+// operands are copied by 16-byte buffer->LDS DMA into a ring of DEPTH stages
+// of TC = 32 channels, DEPTH-1 stages ahead of the products, with no
+// register staging.  Stage layout in 16-byte units:
+// * Ker: TK features x 4 chunks of 8 channels; chunk j of feature k at unit
+//   4k + (j ^ ((k >> 2) & 3)), so the 16 lanes reading one chunk index of 16
+//   consecutive features hit 16 distinct bank groups;
+// * In: TC channel rows of RU units (8 pixels each, RU = ceil(hw/8) made
+//   odd, so consecutive rows start in different banks), read by the
+//   transposing LDS read as in conv_gemm1.
+// Every wave issues NDMA copies per stage (lanes past the data read out of
+// range and write zeros inside the stage), so each wait counts exactly.
+template <typename TO, int WP, int WK, int MBP, int NBK, int TC, int DEPTH>
+__global__ __launch_bounds__(64 * WP * WK) void conv_gemm1d(const bf16_t* __restrict__ In,
+                                                           const bf16_t* __restrict__ Ker,
+                                                           TO* __restrict__ Out, ConvArgs a) {
+  constexpr int NT = 64 * WP * WK;
+  constexpr int TPMAX = 32 * WP * MBP;
+  constexpr int TK = 32 * WK * NBK;
+  static_assert(TC == 32, "the Ker swizzle assumes 4 chunks per feature");
+  static_assert(MBP == 4, "read_a4_tr reads four pixel blocks");
+  constexpr int KER_UNITS = TK * 4;
+  static_assert(KER_UNITS % 64 == 0, "a wave's copy is all Ker or all In");
+  constexpr int RU_MAX = ((TPMAX - 8) / 8) | 1;  // whole images of at most TPMAX - 8 pixels
+  constexpr int NDMA = (KER_UNITS + TC * RU_MAX + NT - 1) / NT;  // copies per thread per stage
+  constexpr int STAGE = NDMA * NT;                                // units per stage
+  constexpr int KSTEPS = TC / 16;
+
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  u32x4_t* ring = reinterpret_cast<u32x4_t*>(smem);  // [DEPTH][STAGE]
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int wvu = __builtin_amdgcn_readfirstlane(wave);
+  const int wp = wave / WK, wk = wave % WK;
+  const int l32 = lane & 31, half = lane >> 5;
+
+  const int tile = xcd_remap(blockIdx.x, gridDim.x);
+  const int b = tile / a.n_ktiles;  // a tile is image b
+  const int kt = tile - b * a.n_ktiles;
+  const int k0 = kt * TK;
+  const int hw = a.hw;
+  const int RU = ((hw + 7) / 8) | 1;
+  const int RSI = 8 * RU;  // In row stride in LDS (elements)
+  const int n_st = (a.Nc + TC - 1) / TC;
+
+  const __amdgpu_buffer_rsrc_t in_rsrc = rsrc_g(In, a.in_total * 2);
+  const __amdgpu_buffer_rsrc_t ker_rsrc = rsrc_g(Ker, (int64_t)a.Nk * a.Nc * 2);
+  const __amdgpu_buffer_rsrc_t out_rsrc = rsrc_g(Out, a.out_total * (int64_t)sizeof(TO));
+
+  // Copy slot j of this thread: unit NT*j + tid of every stage.
+  int d_base[NDMA];  // element offset at channel offset 0 of the stage
+  int d_ch[NDMA];    // channel (within the stage) of the unit's first element
+  bool d_ok[NDMA];
+#pragma unroll
+  for (int j = 0; j < NDMA; ++j) {
+    const int u = NT * j + tid;
+    if (u < KER_UNITS) {
+      const int k = u >> 2, ch = (u & 3) ^ ((k >> 2) & 3);
+      d_ok[j] = k0 + k < a.Nk;
+      d_base[j] = (k0 + k) * a.Nc + 8 * ch;
+      d_ch[j] = 8 * ch;
+    } else {
+      const int v = u - KER_UNITS, c = v / RU, q = v - (v / RU) * RU;
+      d_ok[j] = c < TC && 8 * q < hw;
+      d_base[j] = (b * a.Nc + c) * hw + 8 * q;
+      d_ch[j] = c;
+    }
+  }
+  auto issue = [&](int s) __attribute__((always_inline)) {
+    u32x4_t* dst = ring + (s % DEPTH) * STAGE;
+    const int c0 = s * TC;
+#pragma unroll
+    for (int j = 0; j < NDMA; ++j) {
+      const bool ok = d_ok[j] && s < n_st && c0 + d_ch[j] < a.Nc;
+      if (NT * j + 64 * wvu < KER_UNITS)  // wave-uniform
+        dma16_g(ker_rsrc, dst + NT * j + 64 * wvu,
+                ok ? (uint32_t)((d_base[j] + c0) * 2) : 0x80000000u);
+      else
+        dma16_g(in_rsrc, dst + NT * j + 64 * wvu,
+                ok ? (uint32_t)((d_base[j] + c0 * hw) * 2) : 0x80000000u);
+    }
+  };
+
+  // A operand (In rows, transposing read) and B operand (Ker chunks) offsets.
+  const int G = lane >> 4, li = lane & 15;
+  const int aoff0 = (8 * (G >> 1) + (li >> 2)) * RSI + 16 * (G & 1) + 4 * (li & 3) +
+                    32 * (wp * MBP);
+  const int aoff1 = aoff0 + 4 * RSI;
+  int bunit[NBK][KSTEPS];
+#pragma unroll
+  for (int nb = 0; nb < NBK; ++nb)
+#pragma unroll
+    for (int ks = 0; ks < KSTEPS; ++ks) {
+      const int kf = 32 * (wk * NBK + nb) + l32;
+      bunit[nb][ks] = 4 * kf + ((2 * ks + half) ^ ((kf >> 2) & 3));
+    }
+
+  f32x16_t acc[MBP][NBK];
+#pragma unroll
+  for (int mb = 0; mb < MBP; ++mb)
+#pragma unroll
+    for (int nb = 0; nb < NBK; ++nb)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[mb][nb][e] = 0.f;
+
+#pragma unroll
+  for (int s = 0; s < DEPTH - 1; ++s) issue(s);
+  for (int s = 0; s < n_st; ++s) {
+    // this wave's copies of stage s have landed (the DEPTH-2 later stages'
+    // may be in flight), then every wave's have
+    asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(NDMA * (DEPTH - 2)) : "memory");
+    issue(s + DEPTH - 1);  // into the buffer every wave finished with in step s-1
+    const u32x4_t* kb = ring + (s % DEPTH) * STAGE;
+    const bf16_t* ib = reinterpret_cast<const bf16_t*>(kb + KER_UNITS);
+#pragma unroll
+    for (int ks = 0; ks < KSTEPS; ++ks) {
+      u32x4_t A[MBP], B[NBK];
+#pragma unroll
+      for (int nb = 0; nb < NBK; ++nb) B[nb] = kb[bunit[nb][ks]];
+      read_a4_tr(ib + ks * 16 * RSI + aoff0, ib + ks * 16 * RSI + aoff1, A);
+#pragma unroll
+      for (int mb = 0; mb < MBP; ++mb)
+#pragma unroll
+        for (int nb = 0; nb < NBK; ++nb)
+          acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+              __builtin_bit_cast(bf16x8_t, B[nb]), __builtin_bit_cast(bf16x8_t, A[mb]),
+              acc[mb][nb], 0, 0, 0);
+    }
+  }
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the trailing (empty) copies
+
+  // Epilogue as in conv_gemm1: a lane holds pixel q of 16 features.
+#pragma unroll
+  for (int mb = 0; mb < MBP; ++mb) {
+    const int q = 32 * (wp * MBP + mb) + l32;
+    const int64_t pix = (int64_t)b * a.Nk * hw + (q < hw ? q : 0);
+#pragma unroll
+    for (int nb = 0; nb < NBK; ++nb) {
+      const int nblk = k0 + 32 * (wk * NBK + nb) + 4 * half;
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        const int n = nblk + 8 * (j >> 2) + (j & 3);
+        const uint32_t vo = (n < a.Nk && q < hw)
+                                ? (uint32_t)((pix + (int64_t)n * hw) * (int64_t)sizeof(TO))
+                                : 0x80000000u;
+        if constexpr (sizeof(TO) == 4)
+          __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc[mb][nb][j]), out_rsrc, vo, 0, 0);
+        else
+          __builtin_amdgcn_raw_buffer_store_b16(from_f32<bf16_t>(acc[mb][nb][j]), out_rsrc, vo, 0, 0);
+      }
+    }
+  }
+}
+
 // ---- instantiation table ----------------------------------------------------
-// (id, dtype, WP, WK, MBP, NBK, TC): tk = 32*WK*NBK, tp <= 32*WP*MBP,
-// 64*WP*WK threads.
+// (id, dtype, WP, WK, MBP, NBK, TC, mode): tk = 32*WK*NBK, tp <= 32*WP*MBP,
+// 64*WP*WK threads; mode 0: stride 1, 1: strides 2 and 2, 2: stride 1 with
+// whole-image tiles through the DMA ring (conv_gemm1d, four stages).
 #define CNN_GEMM1_VARIANTS(X)                  \
   X(1700, CNN_BF16, 2, 4, 4, 2, 64, 0)         \
   X(1701, CNN_BF16, 4, 2, 2, 2, 64, 0)         \
   X(1702, CNN_BF16, 2, 4, 4, 2, 32, 1)         \
+  X(1709, CNN_BF16, 2, 4, 4, 2, 32, 2)         \
   X(1800, CNN_BF16_OBF16, 2, 4, 4, 2, 64, 0)   \
   X(1801, CNN_BF16_OBF16, 4, 2, 2, 2, 64, 0)   \
-  X(1802, CNN_BF16_OBF16, 2, 4, 4, 2, 32, 1)
+  X(1802, CNN_BF16_OBF16, 2, 4, 4, 2, 32, 1)   \
+  X(1809, CNN_BF16_OBF16, 2, 4, 4, 2, 32, 2)
 
 static const VariantG kVariantsG[] = {
 #define CNN_GV(id, dt, wp, wk, mbp, nbk, tc, s2) \
@@ -311,22 +517,39 @@ const VariantG* variants_gemm1(int* count) {
 }
 
 int64_t gemm1_lds_bytes(const VariantG& v) {
+  if (v.s2 == 2) {  // a ring of 4 stages of NDMA*threads units
+    const int64_t ndma =
+        (v.tk * 4 + (int64_t)v.tc * (((v.tp - 8) / 8) | 1) + v.threads - 1) / v.threads;
+    return 4 * ndma * v.threads * 16;
+  }
   return 2 * ((int64_t)v.tc * (v.tp + 16) + (int64_t)v.tk * (v.tc + 8)) * 2;
 }
 
 bool gemm1_fits(const VariantG& v, const cnn_problem& p, int64_t tp) {
-  if (v.s2)
+  if (v.s2 == 2)  // whole-image tiles
+    return p.Nr == 1 && p.Ns == 1 && p.sw == 1 && p.sh == 1 && p.Nc % 8 == 0 &&
+           (p.Nw * p.Nh) % 4 == 0 && p.Nw * p.Nh <= v.tp - 8 && tp == p.Nw * p.Nh;
+  if (v.s2 == 1)
     return p.Nr == 1 && p.Ns == 1 && p.sw == 2 && p.sh == 2 && p.Nc % 8 == 0 && p.Nh % 4 == 0 &&
            tp % 4 == 0 && tp >= 4;
   return p.Nr == 1 && p.Ns == 1 && p.sw == 1 && p.sh == 1 && p.Nc % 8 == 0 &&
          (p.Nw * p.Nh) % 4 == 0 && tp % 4 == 0 && tp >= 4;
 }
 
+template <typename TO, int WP, int WK, int MBP, int NBK, int TC, int S2>
+struct Gemm1Kernel {
+  static constexpr auto fn = conv_gemm1<TO, WP, WK, MBP, NBK, TC, S2 == 1>;
+};
+template <typename TO, int WP, int WK, int MBP, int NBK, int TC>
+struct Gemm1Kernel<TO, WP, WK, MBP, NBK, TC, 2> {
+  static constexpr auto fn = conv_gemm1d<TO, WP, WK, MBP, NBK, TC, 4>;
+};
+
 template <int DT, int WP, int WK, int MBP, int NBK, int TC, int S2>
 static hipError_t launch_g(const void* In, const void* Ker, void* Out, const ConvArgs& a,
                            int64_t lds, hipStream_t stream) {
   typedef typename std::conditional<DT == CNN_BF16, float, bf16_t>::type TO;
-  auto kern = conv_gemm1<TO, WP, WK, MBP, NBK, TC, S2 != 0>;
+  auto kern = Gemm1Kernel<TO, WP, WK, MBP, NBK, TC, S2>::fn;
   static bool attr_set = false;
   if (!attr_set) {
     hipError_t e = hipFuncSetAttribute((const void*)kern,

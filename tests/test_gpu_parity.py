@@ -342,6 +342,36 @@ def test_gemm1_exact(shape, mode):
             assert np.array_equal(got, want), (vid, pl.tp)
 
 
+@pytest.mark.parametrize("mode", ["bf16", "bf16_obf16"])
+@pytest.mark.parametrize("shape", GEMM1_SHAPES + [(1, 1000, 33, 12, 20, 1, 1, 1, 1),
+                                                  (4, 8, 256, 2, 2, 1, 1, 1, 1)])
+def test_gemm1_ring_exact(shape, mode):
+    """The 1x1 GEMM kernel with whole-image tiles and both operands copied
+    by DMA into a four-stage ring: bit-exact with the oracle on integer
+    inputs (ragged last stage, a 240-pixel image, k tiles past Nk, 4-pixel
+    images)."""
+    Nb, Nc, Nk, Nw, Nh, Nr, Ns, sw, sh = shape
+    rng = np.random.default_rng(sum(shape) + 13)
+    In = inputs.f32_to_bf16_bits(rng.integers(-3, 4, size=(Nb, Nc, Nw, Nh)).astype(np.float32))
+    Ker = inputs.f32_to_bf16_bits(rng.integers(-3, 4, size=(Nk, Nc, 1, 1)).astype(np.float32))
+    want = oracle.conv(In, Ker, 1, 1)
+    if mode == "bf16_obf16":
+        want = oracle.widen(inputs.f32_to_bf16_bits(want.astype(np.float32)))
+    dt = MODES[mode]
+    ran = 0
+    for vid, vdt, wp, wk, mbp, nbk, tc, s2 in osel.GEMM1:
+        if vdt != dt or s2 != 2:
+            continue
+        tk, tpmax = 32 * wk * nbk, 32 * wp * mbp
+        pl = cnn.plan_tiles(cnn.problem(*shape), dt, cnn.K_GEMM1, tk, tpmax, tc)
+        assert pl.variant == vid and pl.tp == Nw * Nh and pl.grid == Nb * -(-Nk // tk)
+        say(f"[parity] gemm1 ring shape={shape} v{vid} grid={pl.grid} mode={mode}")
+        got = run(In, Ker, 1, 1, mode, plan=pl)
+        assert np.array_equal(got, want), vid
+        ran += 1
+    assert ran == 1
+
+
 # ---- stride-2 row-band kernel: chunks, k tiles, bands, the last element -----
 SROWS_SHAPES = [
     (2, 32, 300, 7, 28, 3, 3, 2, 2),    # Ny = 57: two k tiles (the second ragged), one band
@@ -431,7 +461,7 @@ def test_gemm1_stride2_exact(shape, mode):
     dt = MODES[mode]
     ran = 0
     for vid, vdt, wp, wk, mbp, nbk, tc, s2 in osel.GEMM1:
-        if vdt != dt or not s2:
+        if vdt != dt or s2 != 1:
             continue
         tk, tpmax = 32 * wk * nbk, 32 * wp * mbp
         for cus in (256, 3):
