@@ -204,8 +204,10 @@ int cnn_plan(const cnn_problem* prob, int dtype, const cnn_budget* budget,
  * Empirical selection among the tilings cnn_plan considers (every
  * instantiation whose Eq. (1) footprint fits the current device's budget):
  * runs each on the caller's buffers on `stream`, times it with HIP events
- * (one untimed run, then 3-20 timed runs), and returns the fastest in
- * *plan (its mean time in *best_ms when best_ms is not NULL).  The winner
+ * (one untimed run, then 3-20 timed runs), times the candidates within 15 %
+ * of the fastest (at most four) again over three interleaved rounds of
+ * 10-100 runs, and returns the one with the fastest round in *plan (that
+ * round's mean time in *best_ms when best_ms is not NULL).  The winner
  * is cached for (problem, dtype, device), so later cnn_fwd calls use it.
  * In and Ker are only read; Out is overwritten and on success holds the
  * result of the winning plan.  Blocks until the timing runs finish; cannot
