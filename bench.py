@@ -11,7 +11,10 @@ and Ker, fp32 accumulation and fp32 Out) through the C ABI (cnn_fwd), on
 inputs already resident in device memory.  The K timed steps are captured
 into one HIP graph and replayed, so host launch cost does not pace a
 kernel of a few microseconds (--eager launches each step from the host
-instead).  The timed region is bracketed by torch.cuda.synchronize().
+instead).  Before them, untimed replays of the same graph run for at least
+one second (or W steps with --warmup W), so that the timed steps see the
+GPU's sustained clocks; "warmup" in the JSON line is the number of untimed
+steps that ran.  The timed region is bracketed by torch.cuda.synchronize().
 
 Prints ONE JSON line: the metric (conv TFLOP/s = 2 Nb Nk Nc Nr Ns Nw Nh /
 seconds per step), the roofline of the convolution kernel (HIP events on
@@ -188,8 +191,8 @@ def time_workload(w, mode: str, steps: int, warmup: int, eager: bool, plan_spec:
         dIn, dKer = torch.from_numpy(In).cuda(), torch.from_numpy(Ker).cuda()
     out_dt = torch.bfloat16 if mode == "bf16_obf16" else torch.float32
     dOut = torch.empty((w.Nb, w.Nk, w.Nw, w.Nh), dtype=out_dt, device="cuda")
-    # Warm up on the stream that is then captured: the library keeps its
-    # workspace per stream and cannot allocate during capture.
+    # The first steps run on the stream that is then captured: the library
+    # keeps its workspace per stream and cannot allocate during capture.
     cap_stream = torch.cuda.Stream()
     if plan_spec:
         plan = forced_plan(plan_spec, w, mode)
@@ -208,11 +211,11 @@ def time_workload(w, mode: str, steps: int, warmup: int, eager: bool, plan_spec:
             cnn.fwd(dIn, dKer, dOut, w.sw, w.sh)
 
     with torch.cuda.stream(cap_stream):
-        for _ in range(max(warmup, 1)):
+        for _ in range(2):
             step()
-    for _ in range(max(warmup, 1)):
-        step()
+    step()  # (the default stream's workspace, for --eager)
     torch.cuda.synchronize()
+    done = 3
 
     graph = None
     if not eager:
@@ -220,8 +223,20 @@ def time_workload(w, mode: str, steps: int, warmup: int, eager: bool, plan_spec:
         with torch.cuda.graph(graph, stream=cap_stream):
             for _ in range(steps):
                 step()
-        graph.replay()  # one untimed replay
-        torch.cuda.synchronize()
+    # Untimed warm-up: warmup steps in all (rounded up to whole replays of
+    # the timed graph); warmup < 0: at least one second of them, so that the
+    # GPU clocks have reached their sustained state before the timed region.
+    t_w = time.perf_counter()
+    while (warmup < 0 and time.perf_counter() - t_w < 1.0) or done < warmup:
+        if graph is not None:
+            graph.replay()
+            done += steps
+        else:
+            step()
+            done += 1
+        if done % (10 * steps) < (steps if graph is not None else 1):
+            torch.cuda.synchronize()  # keep the host within a few replays of the GPU
+    torch.cuda.synchronize()
 
     ev0 = torch.cuda.Event(enable_timing=True)
     ev1 = torch.cuda.Event(enable_timing=True)
@@ -240,6 +255,7 @@ def time_workload(w, mode: str, steps: int, warmup: int, eager: bool, plan_spec:
     kernel_ms = ev0.elapsed_time(ev1) / steps
     del graph
     plan.selection = selection
+    plan.warmup_steps = done
     return ms_per_step, kernel_ms, plan
 
 
@@ -275,7 +291,9 @@ def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
-    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=-1,
+                    help="untimed steps before the timed ones; -1: at least one second of "
+                         "them (sustained GPU clocks)")
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--out-dtype", choices=["fp32", "bf16"], default="fp32")
     ap.add_argument("--eager", action="store_true")
@@ -351,7 +369,7 @@ def main():
         "unit": "TFLOP/s",
         "n_gpus": 1,
         "steps": args.steps,
-        "warmup": args.warmup,
+        "warmup": plan.warmup_steps,
         "ms_per_step": round(ms, 5),
         "higher_is_better": True,
         "scaling": "weak",
@@ -377,7 +395,7 @@ def main():
     if args.all:
         for ww in inputs.WORKLOADS:
             for md in (["f32"] if ww.dtype == "f32" else ["bf16", "bf16_obf16"]):
-                m2, k2, p2 = time_workload(ww, md, min(args.steps, 100), 5, args.eager,
+                m2, k2, p2 = time_workload(ww, md, min(args.steps, 100), args.warmup, args.eager,
                                            find=not args.model_plan)
                 pr = "f32" if md == "f32" else "bf16"
                 print(f"{ww.name:18s} {md:10s} kernel {k2 * 1e3:9.2f} us  "
