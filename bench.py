@@ -3,7 +3,7 @@
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
                     [--out-dtype fp32|bf16] [--eager] [--no-cpu-baseline] [--all]
-                    [--plan KERNEL:TK:TP:TC] [--copy-bytes N]
+                    [--plan KERNEL:TK:TP:TC] [--copy-bytes N] [--cold]
 
 A step is one forward convolution Out = conv(In, Ker) of the workload
 (default: the 3x3 layer Nb=32, Nc=Nk=64, 56x56 outputs, stride 1, bf16 In
@@ -259,6 +259,45 @@ def time_workload(w, mode: str, steps: int, warmup: int, eager: bool, plan_spec:
     return ms_per_step, kernel_ms, plan
 
 
+def cold_time(w, mode: str, reps: int = 30):
+    """Median time of one cnn_fwd call (HIP events around it on its stream)
+    with cold caches: a 1 GiB scratch tensor is written before each call,
+    outside the timed region, which evicts In, Ker and Out from the L2s and
+    the 256 MB MALL.  Also the median of single calls without the flush
+    (same timing method), for comparison.  Returns (cold_ms, warm_ms)."""
+    import statistics
+
+    import numpy as np
+    import torch
+
+    from paper_2105_13480_amd import cnn, inputs
+
+    In, Ker = inputs.make_inputs(w)
+    if In.dtype == np.uint16:
+        dIn = torch.from_numpy(In.view(np.int16)).view(torch.bfloat16).cuda()
+        dKer = torch.from_numpy(Ker.view(np.int16)).view(torch.bfloat16).cuda()
+    else:
+        dIn, dKer = torch.from_numpy(In).cuda(), torch.from_numpy(Ker).cuda()
+    out_dt = torch.bfloat16 if mode == "bf16_obf16" else torch.float32
+    dOut = torch.empty((w.Nb, w.Nk, w.Nw, w.Nh), dtype=out_dt, device="cuda")
+    scratch = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    cnn.fwd(dIn, dKer, dOut, w.sw, w.sh)  # the plan cnn_plan_find cached
+    cold, warm = [], []
+    for flush, acc in ((True, cold), (False, warm)):
+        for _ in range(reps):
+            if flush:
+                scratch.fill_(1.0)
+            torch.cuda.synchronize()
+            e0.record()
+            cnn.fwd(dIn, dKer, dOut, w.sw, w.sh)
+            e1.record()
+            torch.cuda.synchronize()
+            acc.append(e0.elapsed_time(e1))
+    del scratch
+    return statistics.median(cold), statistics.median(warm)
+
+
 def cpu_baseline(w, budget_s: float = 10.0):
     """fp64 oracle on this host's cores: whole workload (or a prefix of the
     batch for large ones), repeated until about `budget_s` seconds."""
@@ -297,6 +336,8 @@ def main():
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--out-dtype", choices=["fp32", "bf16"], default="fp32")
     ap.add_argument("--eager", action="store_true")
+    ap.add_argument("--cold", action="store_true",
+                    help="also time single calls with cold caches (a 1 GiB write before each)")
     ap.add_argument("--model-plan", action="store_true",
                     help="use the Eq. (1) model's plan instead of timing the feasible tilings")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -389,6 +430,12 @@ def main():
         "pct_mfma_peak": round(100.0 * tflops / PEAK_TFLOPS[prec], 2),
         "roofline": roof,
     }
+    if args.cold:
+        c_ms, w_ms = cold_time(w, mode)
+        line["cold"] = {"ms_median": round(c_ms, 5), "ms_warm_single": round(w_ms, 5),
+                        "reps": 30, "flush_bytes": 1 << 30,
+                        "note": "one cnn_fwd call between HIP events; caches flushed by a "
+                                "1 GiB write before each call (warm: no flush)"}
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(w)
 
@@ -405,6 +452,10 @@ def main():
                       f"plan {p2.as_dict()['kernel']} v{p2.variant} tk{p2.tk} tp{p2.tp} tc{p2.tc}"
                       + (f" kc{p2.kc}" if p2.kernel == cnn.K_SPLITC else ""),
                       file=sys.stderr, flush=True)
+                if args.cold:
+                    c_ms, w_ms = cold_time(ww, md)
+                    print(f"{ww.name:18s} {md:10s} single call: cold {c_ms * 1e3:9.2f} us, "
+                          f"warm {w_ms * 1e3:9.2f} us", file=sys.stderr, flush=True)
 
     print(json.dumps(line), flush=True)
 
