@@ -307,6 +307,23 @@ typedef struct cnn_closed_form_t {
 int cnn_closed_form(const cnn_problem* prob, double P, double M, int capacity_mode,
                     cnn_closed_form_t* out);
 
+/*
+ * Eq. (3) of Sec. 2.1 one level up, for a plan: its workgroup tiles split
+ * over `xcds` processors (the XCDs, each with an L2 of l2_bytes) the way the
+ * kernels assign them -- XCD x runs the x-th of `xcds` contiguous runs of
+ * the tile index (tile = pixel tile * ceil(Nk/tk) + k tile).  Each XCD reads
+ * from HBM each input row its tiles read (all channels and columns) once,
+ * and each Ker
+ * tile its run meets once if those Ker tiles fit its L2 beside the largest
+ * slab, else once per tile; Out is written once.  terms[0] = Out bytes
+ * written (plus, for CNN_K_SPLITC, the fp32 partial Outs written and read
+ * once), terms[1] = Ker bytes read, terms[2] = In bytes read.  A model for
+ * the HBM counters, not a measurement; host only.  Errors: CNN_E_NULL,
+ * CNN_E_SHAPE (xcds or l2_bytes below 1, a bad problem), CNN_E_DTYPE,
+ * CNN_E_PLAN (the direct kernel's plan, or tk or tp below 1).
+ */
+int cnn_hbm_bytes(const cnn_plan_t* plan, int64_t xcds, int64_t l2_bytes, double terms[3]);
+
 /* Budget of HIP device `device` (CU count, LDS per CU, accumulator regs). */
 int cnn_device_budget(int device, cnn_budget* budget);
 

@@ -32,7 +32,7 @@ STATUS = {0: "CNN_OK", -1: "CNN_E_NULL", -2: "CNN_E_SHAPE", -3: "CNN_E_DTYPE",
 
 # Every symbol include/cnn.h declares.
 EXPORTS = ["cnn_fwd", "cnn_plan", "cnn_plan_find", "cnn_plan_lookup", "cnn_plan_tiles",
-           "cnn_fwd_plan", "cnn_fwd_plan_ws", "cnn_eq1_cost", "cnn_slab_cost", "cnn_closed_form",
+           "cnn_fwd_plan", "cnn_fwd_plan_ws", "cnn_eq1_cost", "cnn_slab_cost", "cnn_closed_form", "cnn_hbm_bytes",
            "cnn_device_budget", "cnn_strerror", "cnn_last_error", "cnn_abi_version"]
 
 i64 = ctypes.c_int64
@@ -107,6 +107,7 @@ def lib():
     L.cnn_slab_cost.argtypes = [P, i64, i64, ctypes.POINTER(ctypes.c_double)]
     L.cnn_closed_form.argtypes = [P, ctypes.c_double, ctypes.c_double, ctypes.c_int,
                                   ctypes.POINTER(ClosedForm)]
+    L.cnn_hbm_bytes.argtypes = [PL, i64, i64, ctypes.POINTER(ctypes.c_double)]
     L.cnn_device_budget.argtypes = [ctypes.c_int, B]
     L.cnn_strerror.argtypes = [ctypes.c_int]
     L.cnn_strerror.restype = ctypes.c_char_p
@@ -114,7 +115,8 @@ def lib():
     L.cnn_last_error.restype = ctypes.c_char_p
     L.cnn_abi_version.argtypes = []
     for f in ("cnn_fwd", "cnn_plan", "cnn_plan_find", "cnn_plan_lookup", "cnn_plan_tiles", "cnn_fwd_plan", "cnn_fwd_plan_ws", "cnn_eq1_cost",
-              "cnn_slab_cost", "cnn_closed_form", "cnn_device_budget", "cnn_abi_version"):
+              "cnn_slab_cost", "cnn_closed_form", "cnn_hbm_bytes", "cnn_device_budget",
+              "cnn_abi_version"):
         getattr(L, f).restype = ctypes.c_int
     _lib = L
     return L
@@ -182,6 +184,13 @@ def closed_form(prob: Problem, P: float, M: float, capacity_mode: int = 0) -> Cl
     out = ClosedForm()
     _check(lib().cnn_closed_form(ctypes.byref(prob), P, M, capacity_mode, ctypes.byref(out)))
     return out
+
+
+def hbm_bytes(pl: Plan, xcds: int = 8, l2_bytes: int = 4 << 20):
+    """(Out, Ker, In) HBM bytes of a plan at the XCD / L2 level (a model)."""
+    terms = (ctypes.c_double * 3)()
+    _check(lib().cnn_hbm_bytes(ctypes.byref(pl), xcds, l2_bytes, terms))
+    return tuple(terms)
 
 
 # ---- compute entry points ------------------------------------------------

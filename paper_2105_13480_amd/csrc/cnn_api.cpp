@@ -679,6 +679,18 @@ int cnn_eq1_cost(const cnn_problem* prob, const cnn_tiles* tiles, int halo_mode,
   return CNN_OK;
 }
 
+int cnn_hbm_bytes(const cnn_plan_t* plan, int64_t xcds, int64_t l2_bytes, double terms[3]) {
+  if (!plan || !terms) return fail(CNN_E_NULL, "plan and terms must be non-NULL");
+  int st;
+  if ((st = check_problem(plan->prob)) || (st = check_dtype(plan->dtype))) return st;
+  if (xcds < 1 || l2_bytes < 1) return fail(CNN_E_SHAPE, "xcds and l2_bytes must be >= 1");
+  if (plan->kernel == CNN_K_DIRECT || plan->kernel < CNN_K_AUTO || plan->kernel > CNN_K_SPLITC ||
+      plan->tk < 1 || plan->tp < 1)
+    return fail(CNN_E_PLAN, "needs a tiled plan (not the direct kernel)");
+  hbm_terms(*plan, xcds, l2_bytes, terms);
+  return CNN_OK;
+}
+
 int cnn_closed_form(const cnn_problem* prob, double P, double M, int capacity_mode,
                     cnn_closed_form_t* out) {
   if (!prob || !out) return fail(CNN_E_NULL, "prob and out must be non-NULL");

@@ -381,6 +381,64 @@ void direct_plan(const cnn_problem& p, int dtype, cnn_plan_t* plan) {
   fill_common(p, dtype, plan);
 }
 
+// Eq. (3) one level up: the plan's tiles split over `xcds` processors (the
+// XCDs, each with an L2 of l2 bytes) as the kernels assign them -- XCD x
+// runs the x-th of `xcds` contiguous runs of the tile index (tile = pixel
+// tile * n_ktiles + k tile) -- each XCD reading from HBM the union of the
+// input rows its tiles read,
+// and each Ker tile its run meets once if those Ker tiles fit its L2 beside
+// the largest slab, else once per tile.  terms: Out written (with the fp32
+// partial Outs of channel-split plans, written and read once), Ker read,
+// In read; bytes.
+void hbm_terms(const cnn_plan_t& pl, int64_t xcds, int64_t l2, double terms[3]) {
+  const cnn_problem& p = pl.prob;
+  const int64_t hw = p.Nw * p.Nh, npix = p.Nb * hw;
+  const int64_t Nx = p.sw * (p.Nw - 1) + p.Nr, Ny = p.sh * (p.Nh - 1) + p.Ns;
+  const int64_t tp = pl.tp, tk = pl.tk;
+  const int64_t n_p = ceil_div(npix, tp), n_k = ceil_div(p.Nk, tk), tiles = n_p * n_k;
+  const double e_in = in_bytes(pl.dtype), e_out = out_bytes(pl.dtype);
+  const double row_bytes = e_in * (double)p.Nc * (double)Ny;  // one (b, x) row, all channels
+  auto ker_bytes = [&](int64_t kt) {
+    return e_in * (double)(std::min(tk, p.Nk - kt * tk) * p.Nc * p.Nr * p.Ns);
+  };
+  double in_b = 0.0, ker_b = 0.0;
+  const int64_t q = tiles / xcds, rem = tiles % xcds;
+  for (int64_t x = 0; x < xcds; ++x) {
+    const int64_t cnt = q + (x < rem ? 1 : 0);
+    if (cnt == 0) continue;
+    const int64_t t0 = x * q + std::min(x, rem), t1 = t0 + cnt;
+    // input rows read: output row (b, w) reads rows b*Nx + sw*w .. + Nr - 1;
+    // the output rows are visited in increasing order, so a running end
+    // counts each row once (rows between strided reads are not counted)
+    int64_t rows = 0, end = -1, max_slab = 0;
+    for (int64_t pt = t0 / n_k; pt <= (t1 - 1) / n_k; ++pt) {
+      const int64_t f = pt * tp, last = std::min(f + tp, npix) - 1;
+      const int64_t r0 = f / p.Nh, r1 = last / p.Nh;  // flattened (b, w) output rows
+      max_slab = std::max(max_slab, (r1 / p.Nw) * Nx + p.sw * (r1 % p.Nw) + p.Nr -
+                                        ((r0 / p.Nw) * Nx + p.sw * (r0 % p.Nw)));
+      for (int64_t r = r0; r <= r1; ++r) {
+        const int64_t g0 = (r / p.Nw) * Nx + p.sw * (r % p.Nw), g1 = g0 + p.Nr;
+        const int64_t from = std::max(g0, end);
+        if (g1 > from) rows += g1 - from;
+        end = std::max(end, g1);
+      }
+    }
+    in_b += (double)rows * row_bytes;
+    double set = 0.0, per_tile = 0.0;
+    for (int64_t kt = 0; kt < n_k; ++kt) {  // k tiles the run meets
+      bool met = cnt >= n_k;
+      for (int64_t t = t0; !met && t < t1; ++t) met = t % n_k == kt;
+      if (met) set += ker_bytes(kt);
+    }
+    for (int64_t t = t0; t < t1; ++t) per_tile += ker_bytes(t % n_k);
+    ker_b += set + (double)max_slab * row_bytes <= (double)l2 ? set : per_tile;
+  }
+  const double out = (double)npix * (double)p.Nk;
+  terms[0] = e_out * out + (pl.kernel == CNN_K_SPLITC ? 8.0 * pl.kc * out : 0.0);
+  terms[1] = ker_b;
+  terms[2] = in_b;
+}
+
 // Table 1 of Sec. 2.1: the closed-form optimum of Eq. (4).  The relaxed
 // capacity solves M_L + 3K sqrt(M_L) = M.
 void closed_form(const cnn_problem& p, double P, double M, int capacity_mode,

@@ -197,6 +197,9 @@ hipError_t launch_direct(const void* In, const void* Ker, void* Out, const ConvA
                          int dtype, hipStream_t stream);
 hipError_t launch_igemm(const Variant& v, const void* In, const void* Ker, void* Out,
                         const ConvArgs& a, int64_t lds_bytes, hipStream_t stream);
+// Two-level (XCD, L2) HBM bytes of a plan (host).
+void hbm_terms(const cnn_plan_t& pl, int64_t xcds, int64_t l2, double terms[3]);
+
 // Table 1 optimum of Eq. (4) (host).
 void closed_form(const cnn_problem& p, double P, double M, int capacity_mode,
                  cnn_closed_form_t* out);

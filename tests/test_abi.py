@@ -274,3 +274,71 @@ def test_closed_form_rejects_bad_arguments():
         assert L.cnn_closed_form(ctypes.byref(p), P, M, mode, ctypes.byref(out)) == -2
     q = cnn.problem(1, 0, 3, 4, 5, 3, 3, 1, 1)
     assert L.cnn_closed_form(ctypes.byref(q), 4.0, 100.0, 0, ctypes.byref(out)) == -2
+
+
+def _hbm_brute(pl, xcds, l2):
+    """cnn_hbm_bytes by enumeration: XCD x runs the x-th contiguous run of
+    the tile index; its In traffic is every (b, x) input row that any output
+    of its tiles reads with any stencil row, each once (all channels and
+    columns); its Ker traffic is each k tile it meets once (l2 large) or once
+    per tile (l2 = 1)."""
+    p = pl.prob
+    hw, npix = p.Nw * p.Nh, p.Nb * p.Nw * p.Nh
+    Ny = p.sh * (p.Nh - 1) + p.Ns
+    e_in = 4 if pl.dtype == cnn.CNN_F32 else 2
+    e_out = 2 if pl.dtype == cnn.CNN_BF16_OBF16 else 4
+    n_k = -(-p.Nk // pl.tk)
+    tiles = -(-npix // pl.tp) * n_k
+    q, rem = divmod(tiles, xcds)
+    ker = lambda kt: e_in * min(pl.tk, p.Nk - kt * pl.tk) * p.Nc * p.Nr * p.Ns
+    in_b = ker_b = 0
+    for x in range(xcds):
+        cnt = q + (1 if x < rem else 0)
+        t0 = x * q + min(x, rem)
+        rows, kts, per_tile = set(), set(), 0
+        for t in range(t0, t0 + cnt):
+            pt, kt = divmod(t, n_k)
+            kts.add(kt)
+            per_tile += ker(kt)
+            for f in range(pt * pl.tp, min((pt + 1) * pl.tp, npix)):
+                b, w = f // hw, (f % hw) // p.Nh
+                rows.update((b, p.sw * w + r) for r in range(p.Nr))
+        in_b += len(rows) * p.Nc * Ny * e_in
+        ker_b += sum(ker(k) for k in kts) if l2 > 1 else per_tile
+    out = npix * p.Nk
+    extra = 8 * pl.kc * out if pl.kernel == cnn.K_SPLITC else 0
+    return e_out * out + extra, ker_b, in_b
+
+
+@pytest.mark.parametrize("dims,dt,kernel,tk,tp,tc", [
+    ((3, 40, 70, 13, 11, 3, 3, 1, 1), cnn.CNN_BF16, cnn.K_IGEMM, 64, 64, 32),
+    ((2, 37, 130, 9, 14, 3, 2, 1, 1), cnn.CNN_BF16_OBF16, cnn.K_IGEMM, 128, 128, 32),
+    ((2, 16, 33, 7, 9, 3, 3, 1, 1), cnn.CNN_F32, cnn.K_IGEMM, 64, 64, 8),
+    ((2, 64, 64, 8, 20, 3, 3, 1, 1), cnn.CNN_BF16, cnn.K_ROWS, 64, 160, 0),
+    ((3, 72, 300, 6, 10, 1, 1, 1, 1), cnn.CNN_BF16, cnn.K_GEMM1, 256, 256, 64),
+    ((1, 70, 40, 7, 7, 3, 3, 1, 1), cnn.CNN_BF16, cnn.K_SPLITC, 64, 64, 32),
+    ((3, 48, 300, 7, 12, 1, 1, 2, 2), cnn.CNN_BF16, cnn.K_GEMM1, 256, 256, 32),   # rows skipped
+    ((2, 32, 300, 7, 28, 3, 3, 2, 2), cnn.CNN_BF16, cnn.K_SROWS, 256, 196, 16),
+    ((2, 5, 9, 6, 7, 2, 3, 3, 1), cnn.CNN_F32, cnn.K_IGEMM, 64, 64, 8),           # sw > Nr
+])
+def test_hbm_bytes_matches_enumeration(dims, dt, kernel, tk, tp, tc):
+    pl = cnn.plan_tiles(cnn.problem(*dims), dt, kernel, tk, tp, tc, cnn.budget())
+    for xcds in (1, 3, 8):
+        for l2 in (1 << 40, 1):
+            got = cnn.hbm_bytes(pl, xcds, l2)
+            want = _hbm_brute(pl, xcds, l2)
+            assert all(abs(g - w) <= 1e-9 * max(1.0, w) for g, w in zip(got, want)), \
+                (xcds, l2, got, want)
+
+
+def test_hbm_bytes_rejects_bad_arguments():
+    L = cnn.lib()
+    pl = cnn.plan_tiles(cnn.problem(1, 16, 16, 16, 16, 3, 3, 1, 1), cnn.CNN_F32, cnn.K_IGEMM,
+                        64, 64, 8, cnn.budget())
+    terms = (ctypes.c_double * 3)()
+    assert L.cnn_hbm_bytes(None, 8, 1 << 22, terms) == -1
+    assert L.cnn_hbm_bytes(ctypes.byref(pl), 0, 1 << 22, terms) == -2
+    assert L.cnn_hbm_bytes(ctypes.byref(pl), 8, 0, terms) == -2
+    d = cnn.plan_tiles(cnn.problem(1, 16, 16, 16, 16, 3, 3, 1, 1), cnn.CNN_F32, cnn.K_DIRECT,
+                       bud=cnn.budget())
+    assert L.cnn_hbm_bytes(ctypes.byref(d), 8, 1 << 22, terms) == -8
