@@ -403,6 +403,10 @@ def main():
         roof = {"bound": "mfma", "achieved": round(k_tflops, 2), "peak": PEAK_TFLOPS[prec],
                 "unit": "TFLOP/s", "frac": round(k_tflops / PEAK_TFLOPS[prec], 4)}
     roof["traffic"] = measured_traffic(w.name, mode)
+    try:  # Eq. (3) at the XCD / L2 level for the timed plan (a prediction)
+        roof["model_hbm_bytes"] = round(sum(cnn.hbm_bytes(plan, 8, 4 << 20)))
+    except cnn.CnnError:
+        roof["model_hbm_bytes"] = None
     roof["algorithmic_bytes_per_launch"] = alg_bytes
     roof["kernel_ms"] = round(kms, 5)
 
