@@ -356,6 +356,8 @@ def main():
     ap.add_argument("--commands", default="",
                     help="with --summarize-counters: the commands that made the passes")
     args = ap.parse_args()
+    if args.steps < 1:
+        raise SystemExit("--steps must be at least 1")
 
     if args.summarize_counters:
         from paper_2105_13480_amd import inputs as _inputs
