@@ -369,7 +369,7 @@ def main():
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py: this build runs on one GPU only; the contraction shards along the "
+        print("bench.py: this library runs on one GPU only; the contraction shards along the "
               "batch with no exchange, but no multi-GPU path is implemented (use --gpus 1)",
               file=sys.stderr)
         sys.exit(2)
