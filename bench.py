@@ -2,24 +2,29 @@
 """Benchmark of the CNN forward contraction on one MI355X.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
-                    [--out-dtype fp32|bf16] [--eager] [--no-cpu-baseline] [--all]
+                    [--out-dtype fp32|bf16] [--eager] [--no-cpu-baseline] [--no-configs]
                     [--plan KERNEL:TK:TP:TC] [--copy-bytes N] [--cold]
 
 A step is one forward convolution Out = conv(In, Ker) of the workload
-(default: the 3x3 layer Nb=32, Nc=Nk=64, 56x56 outputs, stride 1, bf16 In
-and Ker, fp32 accumulation and fp32 Out) through the C ABI (cnn_fwd), on
-inputs already resident in device memory.  The K timed steps are captured
-into one HIP graph and replayed, so host launch cost does not pace a
-kernel of a few microseconds (--eager launches each step from the host
-instead).  Before them, untimed replays of the same graph run for at least
-one second (or W steps with --warmup W), so that the timed steps see the
-GPU's sustained clocks; "warmup" in the JSON line is the number of untimed
-steps that ran.  The timed region is bracketed by torch.cuda.synchronize().
+(default: the largest, the strided 3x3 layer Nb=64, Nc=128, Nk=256, 28x28
+outputs, stride 2, bf16 In and Ker, fp32 accumulation and fp32 Out) through
+the C ABI, on inputs already resident in device memory, with the plan
+cnn_plan_find measures to be fastest (cnn_fwd runs it; cnn_fwd_plan_ws with
+a workspace allocated beforehand if that plan needs one).  The K timed
+steps are captured into one HIP graph and replayed, so host launch cost
+does not pace a kernel of a few microseconds (--eager launches each step
+from the host instead).  Before them, W untimed steps run and then further
+untimed replays until at least one second has passed, so that the timed
+steps see the GPU's sustained clocks ("warmup" in the JSON line is W,
+"untimed_steps" all the untimed steps that ran).  The timed region is
+bracketed by torch.cuda.synchronize().
 
 Prints ONE JSON line: the metric (conv TFLOP/s = 2 Nb Nk Nc Nr Ns Nw Nh /
 seconds per step), the roofline of the convolution kernel (HIP events on
-the stream it runs on, algorithmic bytes or flops per launch), and the fp64
-CPU oracle timed on this host as a baseline.
+the stream it runs on, algorithmic bytes or flops per launch), the fp64
+CPU oracle timed on this host as a baseline, and under "configs" the same
+figures for every workload (each with its own oracle baseline on a bounded
+sample).
 """
 from __future__ import annotations
 
@@ -35,22 +40,25 @@ sys.path.insert(0, ROOT)
 
 PEAK_TFLOPS = {"bf16": 2516.6, "f32": 157.3}   # dense MFMA, MI355X datasheet
 PEAK_HBM_GBS = 8000.0                           # HBM3E, MI355X datasheet
-DEFAULT_WORKLOAD = "conv3x3_b32"
+DEFAULT_WORKLOAD = "conv3x3_s2_b64"
 
 
-# The HBM counters are taken on the headline kernel (conv_rows) with a fixed
-# plan; its code comes from its own source, the shared headers and the
-# launch path, not from the other kernel families' sources or the plan
-# selector.
-COUNTED_KERNEL_SOURCE = "k_rows.hip"
+# The HBM counters are taken per workload on the kernel of a fixed plan; its
+# code comes from its family's source, the shared headers and the launch
+# path, not from the other families' sources or the plan selector.
+FAMILY_SOURCE = {"rows": "k_rows.hip", "srows": "k_srows.hip", "gemm1": "k_gemm1.hip",
+                 "smallc": "k_smallc.hip", "igemm": "k_igemm.hip", "splitc": "k_igemm.hip",
+                 "pointwise": "k_igemm2.hip", "igemm_pipe": "k_igemm2.hip",
+                 "igemm_rawk": "k_igemm2.hip", "igemm_dma": "k_igemm3.hip",
+                 "igemm_wide": "k_igemm4.hip", "direct": "k_direct.hip"}
 NOT_COUNTED = ("cnn_select.cpp",)
 
 
-def kernel_source_hash() -> str:
+def kernel_source_hash(family: str) -> str:
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2105_13480_amd", "csrc")
     for f in sorted(os.listdir(csrc)):
-        if (f.startswith("k_") and f != COUNTED_KERNEL_SOURCE) or f in NOT_COUNTED:
+        if (f.startswith("k_") and f != FAMILY_SOURCE.get(family)) or f in NOT_COUNTED:
             continue
         with open(os.path.join(csrc, f), "rb") as fh:
             h.update(f.encode() + b"\0" + fh.read())
@@ -59,9 +67,9 @@ def kernel_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def measured_traffic(workload: str, mode: str):
+def measured_traffic(workload: str, mode: str, family: str):
     """HBM bytes per launch from the committed rocprofv3 counter summary,
-    if it was taken on the current kernel sources (else None)."""
+    if it was taken on the current sources of the plan's kernel (else None)."""
     path = os.path.join(ROOT, "profiles", "hbm_traffic.json")
     try:
         with open(path) as fh:
@@ -69,13 +77,13 @@ def measured_traffic(workload: str, mode: str):
     except (OSError, ValueError):
         return None
     rec = data.get(f"{workload}/{mode}")
-    if not rec or rec.get("source_hash") != kernel_source_hash():
+    if not rec or rec.get("source_hash") != kernel_source_hash(family):
         return None
     return rec.get("hbm_bytes_per_launch")
 
 
 KERNELS = {"direct": 1, "igemm": 2, "pointwise": 3, "smallc": 4, "igemm_pipe": 5,
-           "igemm_dma": 6, "igemm_wide": 7, "igemm_rawk": 8, "stream": 9, "rows": 10, "gemm1": 11,
+           "igemm_dma": 6, "igemm_wide": 7, "igemm_rawk": 8, "rows": 10, "gemm1": 11,
            "srows": 12, "splitc": 13}
 
 
@@ -141,7 +149,8 @@ def _counter_medians(csv_dir: str, counter: str):
     return {k: (len(v), statistics.median(v)) for k, v in vals.items()}
 
 
-def summarize_counters(pmc_dir: str, workload: str, mode: str, copy_bytes: int, commands):
+def summarize_counters(pmc_dir: str, workload: str, mode: str, copy_bytes: int, commands,
+                       family: str):
     """Write profiles/hbm_traffic.json from four rocprofv3 --pmc passes under
     pmc_dir: conv_fetch / conv_write (FETCH_SIZE / WRITE_SIZE of this bench
     with a forced plan) and copy_fetch / copy_write (the same counters on a
@@ -172,18 +181,17 @@ def summarize_counters(pmc_dir: str, workload: str, mode: str, copy_bytes: int, 
         "fetch_scale": round(f_scale, 4), "write_scale": round(w_scale, 4),
         "hbm_fetch_bytes": round(fetch), "hbm_write_bytes": round(write),
         "hbm_bytes_per_launch": round(fetch + write),
-        "source_hash": kernel_source_hash(), "commands": commands}
+        "family": family, "source_hash": kernel_source_hash(family), "commands": commands}
     with open(path, "w") as fh:
         json.dump(data, fh, indent=1, sort_keys=True)
     print(json.dumps(data[f"{workload}/{mode}"]))
 
 
-def time_workload(w, mode: str, steps: int, warmup: int, eager: bool, plan_spec: str = "",
-                  find: bool = True):
+def _device_inputs(w, mode):
     import numpy as np
     import torch
 
-    from paper_2105_13480_amd import cnn, inputs
+    from paper_2105_13480_amd import inputs
 
     In, Ker = inputs.make_inputs(w)
     if In.dtype == np.uint16:
@@ -193,21 +201,42 @@ def time_workload(w, mode: str, steps: int, warmup: int, eager: bool, plan_spec:
         dIn, dKer = torch.from_numpy(In).cuda(), torch.from_numpy(Ker).cuda()
     out_dt = torch.bfloat16 if mode == "bf16_obf16" else torch.float32
     dOut = torch.empty((w.Nb, w.Nk, w.Nw, w.Nh), dtype=out_dt, device="cuda")
-    # The first steps run on the stream that is then captured: the library
-    # keeps its workspace per stream and cannot allocate during capture.
+    return dIn, dKer, dOut
+
+
+def time_workload(w, mode: str, steps: int, warmup: int, eager: bool, plan_spec: str = "",
+                  find: bool = True):
+    """(ms per step by the host clock, kernel ms per step by HIP events on the
+    launching stream, the plan, untimed steps run)."""
+    import torch
+
+    from paper_2105_13480_amd import cnn
+
+    dIn, dKer, dOut = _device_inputs(w, mode)
     cap_stream = torch.cuda.Stream()
     if plan_spec:
         plan = forced_plan(plan_spec, w, mode)
         selection = "forced"
+    elif find:  # time every candidate once, before the timed region
+        plan, _ = cnn.plan_find(dIn, dKer, dOut, w.sw, w.sh, stream=cap_stream)
+        torch.cuda.synchronize()
+        selection = "find"
+    else:  # the selector's own choice
+        plan = cnn.plan(cnn.problem(*w.dims()), cnn.DTYPES[mode])
+        selection = "model"
+    ws = None
+    if plan.ws_bytes > 0:  # allocated here, before the timed region
+        ws = torch.empty(plan.ws_bytes, dtype=torch.uint8, device="cuda")
 
+        def step():
+            cnn.fwd_plan_ws(dIn, dKer, dOut, plan, ws, w.sw, w.sh)
+    elif selection != "find":
         def step():
             cnn.fwd_plan(dIn, dKer, dOut, plan, w.sw, w.sh)
     else:
-        if find:  # time every feasible tiling once, before the timed region
-            cnn.plan_find(dIn, dKer, dOut, w.sw, w.sh, stream=cap_stream)
-            torch.cuda.synchronize()
-        plan = cnn.plan_lookup(cnn.problem(*w.dims()), cnn.DTYPES[mode])
-        selection = "find" if find else "model"
+        # cnn_fwd runs the cached plan: the fastest workspace-free candidate
+        # of the search (the one returned here), or the model's choice
+        assert cnn.plan_lookup(cnn.problem(*w.dims()), cnn.DTYPES[mode]).variant == plan.variant
 
         def step():
             cnn.fwd(dIn, dKer, dOut, w.sw, w.sh)
@@ -215,9 +244,8 @@ def time_workload(w, mode: str, steps: int, warmup: int, eager: bool, plan_spec:
     with torch.cuda.stream(cap_stream):
         for _ in range(2):
             step()
-    step()  # (the default stream's workspace, for --eager)
     torch.cuda.synchronize()
-    done = 3
+    done = 2
 
     graph = None
     if not eager:
@@ -225,11 +253,11 @@ def time_workload(w, mode: str, steps: int, warmup: int, eager: bool, plan_spec:
         with torch.cuda.graph(graph, stream=cap_stream):
             for _ in range(steps):
                 step()
-    # Untimed warm-up: warmup steps in all (rounded up to whole replays of
-    # the timed graph); warmup < 0: at least one second of them, so that the
-    # GPU clocks have reached their sustained state before the timed region.
+    # Untimed: at least `warmup` steps (whole replays of the timed graph),
+    # and at least one second of them, so that the GPU clocks have reached
+    # their sustained state before the timed region.
     t_w = time.perf_counter()
-    while (warmup < 0 and time.perf_counter() - t_w < 1.0) or done < warmup:
+    while time.perf_counter() - t_w < 1.0 or done < warmup:
         if graph is not None:
             graph.replay()
             done += steps
@@ -257,8 +285,23 @@ def time_workload(w, mode: str, steps: int, warmup: int, eager: bool, plan_spec:
     kernel_ms = ev0.elapsed_time(ev1) / steps
     del graph
     plan.selection = selection
-    plan.warmup_steps = done
-    return ms_per_step, kernel_ms, plan
+    return ms_per_step, kernel_ms, plan, done
+
+
+def roofline(w, mode: str, plan, kms: float):
+    """Roofline of the step's kernels from their event time: HBM-bound below
+    the ridge (algorithmic bytes per launch over 8 TB/s), else MFMA-bound."""
+    prec = "f32" if mode == "f32" else "bf16"
+    alg_bytes = plan.compulsory_bytes
+    ai = w.flops / alg_bytes
+    ridge = PEAK_TFLOPS[prec] * 1e12 / (PEAK_HBM_GBS * 1e9)
+    k_tflops = w.flops / (kms * 1e-3) / 1e12
+    if ai < ridge:
+        achieved = alg_bytes / (kms * 1e-3) / 1e9
+        return {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
+                "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4)}
+    return {"bound": "mfma", "achieved": round(k_tflops, 2), "peak": PEAK_TFLOPS[prec],
+            "unit": "TFLOP/s", "frac": round(k_tflops / PEAK_TFLOPS[prec], 4)}
 
 
 def cold_time(w, mode: str, reps: int = 30):
@@ -300,29 +343,36 @@ def cold_time(w, mode: str, reps: int = 30):
     return statistics.median(cold), statistics.median(warm)
 
 
-def cpu_baseline(w, budget_s: float = 10.0):
-    """fp64 oracle on this host's cores: whole workload (or a prefix of the
-    batch for large ones), repeated until about `budget_s` seconds."""
+def cpu_baseline(w, budget_s: float = 10.0, threads: int = 0):
+    """fp64 oracle on this host's cores (or `threads` of them): the whole
+    workload, or a prefix of its batch for large ones, repeated until about
+    `budget_s` seconds."""
     import oracle
     from paper_2105_13480_amd import inputs
 
     In, Ker = inputs.make_inputs(w)
-    per_image = w.flops / w.Nb
-    nb = w.Nb
-    # keep one pass under ~1/3 of the budget at ~10 GFLOP/s
-    while nb > 1 and per_image * nb > budget_s / 3 * 10e9:
-        nb //= 2
-    sub = In[:nb]
-    oracle.conv(sub, Ker[:1], w.sw, w.sh)  # load + warm
-    passes, t0 = 0, time.perf_counter()
-    while True:
-        oracle.conv(sub, Ker, w.sw, w.sh)
-        passes += 1
-        el = time.perf_counter() - t0
-        if el >= budget_s or passes >= 50:
-            break
+    prev = oracle.set_threads(threads) if threads else None
+    try:
+        per_image = w.flops / w.Nb
+        cores = oracle.threads()
+        nb = w.Nb
+        # keep one pass under ~1/3 of the budget at ~4 GFLOP/s per thread
+        while nb > 1 and per_image * nb > budget_s / 3 * 4e9 * cores:
+            nb //= 2
+        sub = In[:nb]
+        oracle.conv(sub, Ker[:1], w.sw, w.sh)  # load + warm
+        passes, t0 = 0, time.perf_counter()
+        while True:
+            oracle.conv(sub, Ker, w.sw, w.sh)
+            passes += 1
+            el = time.perf_counter() - t0
+            if el >= budget_s or passes >= 50:
+                break
+    finally:
+        if prev:
+            oracle.set_threads(prev)
     flops = per_image * nb * passes
-    return {"value": round(flops / el / 1e12, 6), "unit": "TFLOP/s", "cores": oracle.threads(),
+    return {"value": round(flops / el / 1e12, 6), "unit": "TFLOP/s", "cores": cores,
             "kind": "oracle",
             "sample": f"{nb} of {w.Nb} images of {w.name}, full Nk/Nc/spatial extent, "
                       f"{passes} passes in {el:.1f} s (fp64 seven-loop direct convolution)"}
@@ -332,19 +382,21 @@ def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
-    ap.add_argument("--warmup", type=int, default=-1,
-                    help="untimed steps before the timed ones; -1: at least one second of "
-                         "them (sustained GPU clocks)")
+    ap.add_argument("--warmup", type=int, default=0,
+                    help="untimed steps before the timed ones (at least one second of untimed "
+                         "steps runs in any case, for sustained GPU clocks)")
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--out-dtype", choices=["fp32", "bf16"], default="fp32")
     ap.add_argument("--eager", action="store_true")
     ap.add_argument("--cold", action="store_true",
                     help="also time single calls with cold caches (a 1 GiB write before each)")
     ap.add_argument("--model-plan", action="store_true",
-                    help="use the Eq. (1) model's plan instead of timing the feasible tilings")
+                    help="use the selector's model plan instead of timing the candidates")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="time the headline workload only (no per-workload list)")
     ap.add_argument("--all", action="store_true",
-                    help="also time every workload and output dtype (table on stderr)")
+                    help="per-workload list with both output dtypes (table on stderr)")
     ap.add_argument("--plan", default="",
                     help="force a tiling, KERNEL[:TK:TP:TC[:VARIANT]], KERNEL one of "
                          + "/".join(KERNELS))
@@ -353,18 +405,22 @@ def main():
     ap.add_argument("--summarize-counters", default="",
                     help="write profiles/hbm_traffic.json from rocprofv3 --pmc passes in this "
                          "directory (conv_fetch, conv_write, copy_fetch, copy_write); no GPU")
+    ap.add_argument("--family", default="",
+                    help="with --summarize-counters: the kernel family the passes ran")
     ap.add_argument("--commands", default="",
                     help="with --summarize-counters: the commands that made the passes")
     args = ap.parse_args()
     if args.steps < 1:
         raise SystemExit("--steps must be at least 1")
+    if args.warmup < 0:
+        raise SystemExit("--warmup must be at least 0")
 
     if args.summarize_counters:
         from paper_2105_13480_amd import inputs as _inputs
         w = _inputs.BY_NAME[args.workload]
         mode = "f32" if w.dtype == "f32" else ("bf16" if args.out_dtype == "fp32" else "bf16_obf16")
         summarize_counters(args.summarize_counters, w.name, mode, args.copy_bytes,
-                           [c for c in args.commands.split(";;") if c])
+                           [c for c in args.commands.split(";;") if c], args.family)
         return
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -385,32 +441,38 @@ def main():
         copy_calibration(args.copy_bytes, args.steps)
         return
 
+    def mode_of(w, out_dtype):
+        return "f32" if w.dtype == "f32" else ("bf16" if out_dtype == "fp32" else "bf16_obf16")
+
+    def plan_fields(pl):
+        d = pl.as_dict()
+        out = {k: d[k] for k in ("kernel", "variant", "tk", "tp", "tc", "grid")}
+        if pl.kernel == cnn.K_SPLITC:
+            out["kc"] = pl.kc
+        out["workspace_bytes"] = pl.ws_bytes
+        out["model_us"] = round(pl.model_us, 2)
+        return out
+
     w = inputs.BY_NAME[args.workload]
-    mode = "f32" if w.dtype == "f32" else ("bf16" if args.out_dtype == "fp32" else "bf16_obf16")
-    ms, kms, plan = time_workload(w, mode, args.steps, args.warmup, args.eager, args.plan,
-                                  find=not args.model_plan)
+    mode = mode_of(w, args.out_dtype)
+    print(f"bench: {w.name} {mode}: plan search and {args.steps} timed steps", file=sys.stderr,
+          flush=True)
+    ms, kms, plan, untimed = time_workload(w, mode, args.steps, args.warmup, args.eager,
+                                           args.plan, find=not args.model_plan)
     model = cnn.plan(cnn.problem(*w.dims()), cnn.DTYPES[mode])
 
     prec = "f32" if mode == "f32" else "bf16"
     tflops = w.flops / (ms * 1e-3) / 1e12
-    k_tflops = w.flops / (kms * 1e-3) / 1e12
-    alg_bytes = plan.compulsory_bytes
-    ai = w.flops / alg_bytes
-    ridge = PEAK_TFLOPS[prec] * 1e12 / (PEAK_HBM_GBS * 1e9)
-    if ai < ridge:
-        achieved = alg_bytes / (kms * 1e-3) / 1e9
-        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
-                "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4)}
-    else:
-        roof = {"bound": "mfma", "achieved": round(k_tflops, 2), "peak": PEAK_TFLOPS[prec],
-                "unit": "TFLOP/s", "frac": round(k_tflops / PEAK_TFLOPS[prec], 4)}
-    roof["traffic"] = measured_traffic(w.name, mode)
+    roof = roofline(w, mode, plan, kms)
+    roof["traffic"] = measured_traffic(w.name, mode, plan.as_dict()["kernel"])
     try:  # Eq. (3) at the XCD / L2 level for the timed plan (a prediction)
         roof["model_hbm_bytes"] = round(sum(cnn.hbm_bytes(plan, 8, 4 << 20)))
     except cnn.CnnError:
         roof["model_hbm_bytes"] = None
-    roof["algorithmic_bytes_per_launch"] = alg_bytes
+    roof["algorithmic_bytes_per_launch"] = plan.compulsory_bytes
+    roof["eq1_bytes_per_launch"] = plan.eq1_bytes
     roof["kernel_ms"] = round(kms, 5)
+    roof["pct_mfma_peak"] = round(100.0 * w.flops / (kms * 1e-3) / 1e12 / PEAK_TFLOPS[prec], 2)
 
     line = {
         "metric": "conv TFLOP/s (2*Nb*Nk*Nc*Nr*Ns*Nw*Nh/s) + % MFMA peak, 1 MI355X",
@@ -418,7 +480,8 @@ def main():
         "unit": "TFLOP/s",
         "n_gpus": 1,
         "steps": args.steps,
-        "warmup": plan.warmup_steps,
+        "warmup": args.warmup,
+        "untimed_steps": untimed,
         "ms_per_step": round(ms, 5),
         "higher_is_better": True,
         "scaling": "weak",
@@ -430,11 +493,9 @@ def main():
                    "in_dtype": w.dtype, "acc_dtype": "f32",
                    "out_dtype": "bf16" if mode == "bf16_obf16" else "f32",
                    "launch": "eager" if args.eager else "hipgraph",
-                   "plan": {k: v for k, v in plan.as_dict().items()
-                            if k in ("kernel", "variant", "tk", "tp", "tc", "grid")},
+                   "plan": plan_fields(plan),
                    "plan_selection": plan.selection,
-                   "model_plan": {k: v for k, v in model.as_dict().items()
-                                  if k in ("kernel", "variant", "tk", "tp", "tc")}},
+                   "model_plan": plan_fields(model)},
         "pct_mfma_peak": round(100.0 * tflops / PEAK_TFLOPS[prec], 2),
         "roofline": roof,
     }
@@ -445,25 +506,56 @@ def main():
                         "note": "one cnn_fwd call between HIP events; caches flushed by a "
                                 "1 GiB write before each call (warm: no flush)"}
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(w)
+        print("bench: oracle baseline on the host's cores", file=sys.stderr, flush=True)
+        line["cpu_baseline"] = cpu_baseline(w, budget_s=10.0)
 
-    if args.all:
+    if not args.no_configs and not args.plan:
+        configs = []
+        out_dtypes = ["fp32", "bf16"] if args.all else [args.out_dtype]
         for ww in inputs.WORKLOADS:
-            for md in (["f32"] if ww.dtype == "f32" else ["bf16", "bf16_obf16"]):
-                m2, k2, p2 = time_workload(ww, md, min(args.steps, 100), args.warmup, args.eager,
-                                           find=not args.model_plan)
+            for od in out_dtypes:
+                md = mode_of(ww, od)
+                if od == "bf16" and md == "f32":
+                    continue
+                print(f"bench: {ww.name} {md}", file=sys.stderr, flush=True)
+                m2, k2, p2, u2 = time_workload(ww, md, min(args.steps, 100), 0, args.eager,
+                                               find=not args.model_plan)
                 pr = "f32" if md == "f32" else "bf16"
+                mdl = cnn.plan(cnn.problem(*ww.dims()), cnn.DTYPES[md])
+                rec = {"workload": ww.name, "out_dtype": "bf16" if md == "bf16_obf16" else "f32",
+                       "ms": round(k2, 5), "TFLOP_per_s": round(ww.flops / (k2 * 1e-3) / 1e12, 2),
+                       "pct_mfma_peak": round(100 * ww.flops / (k2 * 1e-3) / 1e12 / PEAK_TFLOPS[pr], 2),
+                       "roofline": roofline(ww, md, p2, k2),
+                       "plan": plan_fields(p2), "model_plan": plan_fields(mdl),
+                       "model_plan_ms_ratio": None}
+                rec["roofline"]["traffic"] = measured_traffic(ww.name, md, p2.as_dict()["kernel"])
+                rec["roofline"]["model_hbm_bytes"] = round(p2.hbm_bytes)
+                if (mdl.kernel, mdl.variant, mdl.tp, mdl.kc) != (p2.kernel, p2.variant, p2.tp, p2.kc):
+                    # the model's own choice, timed the same way
+                    _, k3, _, _ = time_workload(ww, md, min(args.steps, 100), 0, args.eager,
+                                                find=False)
+                    rec["model_plan_ms_ratio"] = round(k3 / k2, 3)
+                else:
+                    rec["model_plan_ms_ratio"] = 1.0
+                if not args.no_cpu_baseline and od == out_dtypes[0]:
+                    cb = cpu_baseline(ww, budget_s=2.0)
+                    rec["cpu_baseline"] = {k: cb[k] for k in ("value", "unit", "cores", "sample")}
+                    if ww.name == "tiny3x3_f32":
+                        c1 = cpu_baseline(ww, budget_s=2.0, threads=1)
+                        rec["cpu_baseline_1thread"] = {k: c1[k] for k in ("value", "unit", "cores", "sample")}
+                configs.append(rec)
                 print(f"{ww.name:18s} {md:10s} kernel {k2 * 1e3:9.2f} us  "
-                      f"{ww.flops / (k2 * 1e-3) / 1e12:8.1f} TF/s  "
-                      f"{100 * ww.flops / (k2 * 1e-3) / 1e12 / PEAK_TFLOPS[pr]:5.1f}% peak  "
-                      f"{p2.compulsory_bytes / (k2 * 1e-3) / 1e9:7.0f} GB/s  "
+                      f"{rec['TFLOP_per_s']:8.1f} TF/s  {rec['pct_mfma_peak']:5.1f}% peak  "
+                      f"roofline {rec['roofline']['bound']} {rec['roofline']['frac']:.3f}  "
                       f"plan {p2.as_dict()['kernel']} v{p2.variant} tk{p2.tk} tp{p2.tp} tc{p2.tc}"
-                      + (f" kc{p2.kc}" if p2.kernel == cnn.K_SPLITC else ""),
+                      + (f" kc{p2.kc}" if p2.kernel == cnn.K_SPLITC else "")
+                      + f"  model/find {rec['model_plan_ms_ratio']}",
                       file=sys.stderr, flush=True)
                 if args.cold:
                     c_ms, w_ms = cold_time(ww, md)
                     print(f"{ww.name:18s} {md:10s} single call: cold {c_ms * 1e3:9.2f} us, "
                           f"warm {w_ms * 1e3:9.2f} us", file=sys.stderr, flush=True)
+        line["configs"] = configs
 
     print(json.dumps(line), flush=True)
 

@@ -45,7 +45,7 @@
 extern "C" {
 #endif
 
-#define CNN_ABI_VERSION 1
+#define CNN_ABI_VERSION 2
 
 /* Element types of (In, Ker) -> Out.  Accumulation is always fp32. */
 typedef enum cnn_dtype {
@@ -98,10 +98,7 @@ typedef enum cnn_kernel {
   CNN_K_IGEMM_RAWK = 8,/* as CNN_K_IGEMM_PIPE for fixed 3x3 / 1x1 stencils, Nc % 8 == 0:
                          raw Ker rows copied by DMA, MFMA operands built in registers,
                          no repack and no workspace                                 */
-  CNN_K_STREAM = 9,   /* persistent workgroups (grid = workgroup slots) walking tile
-                         ranges as one pipeline: next tile's loads during the last
-                         stage, Out stores drain under the next tile; raw Ker, kept
-                         resident in LDS when it fits; fixed 3x3, Nc % 8 == 0     */
+                      /* 9: not used                                                  */
   CNN_K_ROWS = 10,    /* stride-1 row streaming, bf16: tiles are whole output rows
                          of one image (tp = L*Nh, L dividing Nw) by 64 features;
                          the Ker tile resident in LDS, input rows streamed through
@@ -168,21 +165,32 @@ typedef struct cnn_plan_t {
   int64_t lds_bytes;    /* LDS per workgroup                                        */
   int64_t slab_rows;    /* max input rows a workgroup stages (halo included)        */
   int64_t ws_bytes;     /* device workspace the plan needs (repacked Ker, or the
-                           fp32 partial Outs of CNN_K_SPLITC); the library
-                           allocates it per (device, stream) on first use      */
+                           fp32 partial Outs of CNN_K_SPLITC), which the caller
+                           passes to cnn_fwd_plan_ws; 0 for most plans        */
   double eq1_elems[3];  /* Eq. (1) terms Out, Ker, In for this tiling (elements)    */
   double eq1_bytes;     /* the same, weighted by element size, summed               */
   double compulsory_bytes; /* |In read| + |Ker| + |Out|, each once                  */
   double flops;         /* 2 Nb Nk Nc Nr Ns Nw Nh                                   */
+  double mfma_flops;    /* flops the workgroups' MFMA tiles issue (tile and
+                           channel-stage padding included)                    */
+  double hbm_bytes;     /* predicted HBM bytes: Eq. (3) at the XCD / L2 level
+                           (cnn_hbm_bytes with 8 XCDs of 4 MiB L2)            */
+  double model_us;      /* the selector's predicted kernel time (microseconds):
+                           the slowest of the MFMA work, the Eq. (1) traffic
+                           and the HBM traffic of the busiest CU's tiles, at
+                           rates measured on MI355X, plus the family's fixed
+                           costs (see cnn_plan)                               */
 } cnn_plan_t;
 
 /*
  * Out = conv(In, Ker) on `stream` (the CNN equation of Sec. 1, scheduled as
  * Listing 3 of Sec. 2).  Uses the plan cached for (problem, dtype, current
- * device): the winner of an earlier cnn_plan_find, else cnn_plan's choice
- * (computed on the first call and cached).  See the file header for
- * layouts.  Errors: CNN_E_NULL, CNN_E_SHAPE, CNN_E_DTYPE, CNN_E_OVERFLOW,
- * CNN_E_ALIAS, CNN_E_HIP.
+ * device): the fastest workspace-free plan of an earlier cnn_plan_find,
+ * else cnn_plan's choice (computed on the first call and cached).  Only
+ * plans that need no workspace are ever used here, so cnn_fwd allocates no
+ * device memory, never synchronises, and may be captured into a HIP graph.
+ * See the file header for layouts.  Errors: CNN_E_NULL, CNN_E_SHAPE,
+ * CNN_E_DTYPE, CNN_E_OVERFLOW, CNN_E_ALIAS, CNN_E_HIP.
  */
 int cnn_fwd(const void* In, const void* Ker, void* Out,
             int64_t Nb, int64_t Nc, int64_t Nk, int64_t Nw, int64_t Nh,
@@ -190,29 +198,68 @@ int cnn_fwd(const void* In, const void* Ker, void* Out,
             int dtype, void* stream);
 
 /*
- * Tile-size selection (Sec. 2, Eq. (1)).  Evaluates the Eq. (1) data
- * movement of every tiling the kernels implement whose footprint fits the
- * budget, and returns the cheapest (ties and grid-fill rules are documented
- * with the implementation).  budget == NULL queries the current HIP device.
- * Writes *plan.  Errors: CNN_E_NULL, CNN_E_SHAPE, CNN_E_DTYPE,
- * CNN_E_OVERFLOW, CNN_E_HIP (device query failed).
+ * Tile-size selection (Sec. 2, Eq. (1); Eq. (3) one level up).  Lists every
+ * tiling the kernels implement whose footprint (LDS tiles and accumulators,
+ * the two halves of the paper's fast memory M) fits the budget, prices each
+ * with Eq. (1) (slab form, bytes), the two-level HBM bytes (Eq. (3) over the
+ * 8 XCDs, plan.hbm_bytes) and its MFMA work, converts them into a time at
+ * rates measured on MI355X (plan.model_us), and returns the workspace-free
+ * candidate of least time; candidates within 2 % of it are ranked by fewer
+ * HBM bytes, then fewer Eq. (1) bytes, then the lower instantiation id.
+ * budget == NULL queries the current HIP device.  Writes *plan.  Errors:
+ * CNN_E_NULL, CNN_E_SHAPE, CNN_E_DTYPE, CNN_E_OVERFLOW, CNN_E_HIP (device
+ * query failed).
  */
 int cnn_plan(const cnn_problem* prob, int dtype, const cnn_budget* budget,
              cnn_plan_t* plan);
 
 /*
- * Empirical selection among the tilings cnn_plan considers (every
- * instantiation whose Eq. (1) footprint fits the current device's budget):
- * runs each on the caller's buffers on `stream`, times it with HIP events
- * (one untimed run, then 3-20 timed runs), times the candidates within 15 %
- * of the fastest (at most four) again over three interleaved rounds of
- * 10-100 runs, and returns the one with the fastest round in *plan (that
- * round's mean time in *best_ms when best_ms is not NULL).  The winner
- * is cached for (problem, dtype, device), so later cnn_fwd calls use it.
- * In and Ker are only read; Out is overwritten and on success holds the
- * result of the winning plan.  Blocks until the timing runs finish; cannot
- * be called while `stream` is being captured (CNN_E_UNSUPPORTED).  Other
- * errors as cnn_fwd.
+ * The candidates cnn_plan ranks (and cnn_plan_find times), each a complete
+ * plan with its model fields: writes min(*count, cap) of them to out (out
+ * may be NULL when cap is 0) and sets *count to the number of candidates.
+ * Errors: CNN_E_NULL (count NULL, or out NULL with cap > 0), as cnn_plan.
+ */
+int cnn_plan_candidates(const cnn_problem* prob, int dtype, const cnn_budget* budget,
+                        cnn_plan_t* out, int cap, int* count);
+
+/*
+ * The kernel instantiations the library holds (its compile-time tilings),
+ * for tests and tuning tools.  Writes min(*count, cap) entries to out (out
+ * may be NULL when cap is 0); *count = how many exist.  Host only.
+ * Errors: CNN_E_NULL.
+ */
+typedef struct cnn_variant_t {
+  int32_t kernel;       /* cnn_kernel family                                      */
+  int32_t variant;      /* instantiation id (cnn_plan_t.variant)                  */
+  int32_t dtype;        /* cnn_dtype                                              */
+  int32_t nr, ns;       /* compile-time stencil, 0 = any                          */
+  int32_t mode;         /* CNN_K_GEMM1: 0 stride 1, 1 strides 2, 2 whole-image
+                           DMA ring; CNN_K_SROWS: output rows per band;
+                           CNN_K_ROWS: 32-position blocks per input row; else 0 */
+  int64_t tk;           /* output features per workgroup                          */
+  int64_t tp;           /* largest tile of outputs, 0 where the problem sets it   */
+  int64_t tc;           /* input channels per stage, 0 = all; CNN_K_ROWS: the
+                           channel count rounded up to 16 it is built for       */
+} cnn_variant_t;
+
+int cnn_variants(cnn_variant_t* out, int cap, int* count);
+
+/*
+ * Empirical selection among the candidates of cnn_plan_candidates (every
+ * tiling whose footprint fits the current device's budget): runs each on
+ * the caller's buffers on `stream`, times it with HIP events (one untimed
+ * run, then 3-20 timed runs), times the candidates within 15 % of the
+ * fastest (at most four) again over three interleaved rounds of 10-100
+ * runs, and returns the one with the fastest round in *plan (that round's
+ * mean time in *best_ms when best_ms is not NULL).  The winner may need a
+ * workspace (plan->ws_bytes > 0, run it with cnn_fwd_plan_ws); the fastest
+ * candidate that needs none is cached for (problem, dtype, device), so
+ * later cnn_fwd calls use it.  Candidates that need a workspace are timed
+ * with one this call allocates and frees before it returns (the only device
+ * allocation the library makes).  In and Ker are only read; Out is
+ * overwritten and on success holds the result of the returned plan.
+ * Blocks until the timing runs finish; cannot be called while `stream` is
+ * being captured (CNN_E_UNSUPPORTED).  Other errors as cnn_fwd.
  */
 int cnn_plan_find(const void* In, const void* Ker, void* Out,
                   const cnn_problem* prob, int dtype, void* stream,
@@ -237,7 +284,11 @@ int cnn_plan_tiles(const cnn_problem* prob, int dtype, int kernel,
 
 /*
  * Out = conv(In, Ker) with an explicit plan.  The plan's problem and dtype
- * must equal (*prob, dtype), else CNN_E_PLAN.  Other errors as cnn_fwd.
+ * must equal (*prob, dtype), and its tiling must be one the library makes
+ * for that problem (geometry, LDS size and the byte ranges its kernel
+ * addresses), else CNN_E_PLAN.  A plan that needs a workspace
+ * (plan->ws_bytes > 0) returns CNN_E_UNSUPPORTED: run it with
+ * cnn_fwd_plan_ws.  Allocates nothing.  Other errors as cnn_fwd.
  */
 int cnn_fwd_plan(const void* In, const void* Ker, void* Out,
                  const cnn_problem* prob, int dtype, const cnn_plan_t* plan,
@@ -246,16 +297,13 @@ int cnn_fwd_plan(const void* In, const void* Ker, void* Out,
 /*
  * As cnn_fwd_plan, with a caller-provided device workspace of ws_bytes
  * bytes (at least plan->ws_bytes, 16-byte aligned; NULL allowed when
- * plan->ws_bytes is 0).  The library then allocates nothing, so this form
- * may be used while the stream is being captured into a HIP graph.  The
- * workspace must not be used by another call that may run concurrently.
- * Errors: as cnn_fwd_plan, and CNN_E_SHAPE if the workspace is too small or
- * misaligned.
- *
- * cnn_fwd and cnn_fwd_plan keep one workspace per (device, stream),
- * allocated on the first call that needs it (or a larger one); during
- * stream capture they cannot allocate and return CNN_E_UNSUPPORTED if the
- * stream has no large enough workspace yet.
+ * plan->ws_bytes is 0): the repacked Ker of the packed-Ker families, or
+ * the kc fp32 partial Outs of CNN_K_SPLITC.  The library keeps no pointer to
+ * it after the call returns, but the kernels queued on `stream` use it
+ * until they finish: it must not be freed or used by another call that may
+ * run concurrently before then.  Allocates nothing, so it may be captured
+ * into a HIP graph.  Errors: as cnn_fwd_plan, and CNN_E_NULL /
+ * CNN_E_SHAPE if the workspace is missing, too small or misaligned.
  */
 int cnn_fwd_plan_ws(const void* In, const void* Ker, void* Out,
                     const cnn_problem* prob, int dtype, const cnn_plan_t* plan,

@@ -10,9 +10,8 @@ Contents
   Sec. 1 CNN equation and Listing 1, strides restored), built into
   ``liboracle.so`` with gcc and called through ctypes here.
 * ``eq1`` -- the paper's data-movement cost, Eq. (1), its relaxed form
-  Eq. (4) and the Case 1a closed form (Sec. 2.1), written out in Python.
-* ``select`` -- brute-force reference for the tile-size selector (Eq. (1)
-  evaluated over every candidate tiling).
+  Eq. (4), the Case 1a closed form and Table 1 (Sec. 2.1), written out in
+  Python.
 
 Inputs are passed as the exact stored values: float32 arrays, or bfloat16
 bit patterns held in uint16 arrays; both are widened exactly to float64
@@ -64,6 +63,8 @@ def _load():
     lib.cnn_oracle_points.restype = ctypes.c_int
     lib.cnn_oracle_threads.argtypes = []
     lib.cnn_oracle_threads.restype = ctypes.c_int
+    lib.cnn_oracle_set_threads.argtypes = [ctypes.c_int]
+    lib.cnn_oracle_set_threads.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -71,6 +72,12 @@ def _load():
 def threads() -> int:
     """OpenMP threads the oracle uses (honours OMP_NUM_THREADS)."""
     return int(_load().cnn_oracle_threads())
+
+
+def set_threads(n: int) -> int:
+    """Use n OpenMP threads from now on (timing only; results do not depend
+    on it).  Returns the previous count."""
+    return int(_load().cnn_oracle_set_threads(int(n)))
 
 
 def widen(x: np.ndarray) -> np.ndarray:

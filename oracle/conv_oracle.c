@@ -127,3 +127,16 @@ int cnn_oracle_threads(void) {
   return 1;
 #endif
 }
+
+/* Sets the OpenMP thread count of later calls (n >= 1); returns the count
+ * used before.  Timing only: the result of every call is independent of it. */
+int cnn_oracle_set_threads(int n) {
+#ifdef _OPENMP
+  const int was = omp_get_max_threads();
+  if (n >= 1) omp_set_num_threads(n);
+  return was;
+#else
+  (void)n;
+  return 1;
+#endif
+}

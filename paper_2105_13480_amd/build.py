@@ -20,8 +20,9 @@ CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libcnn_mi355x.so")
 
-SOURCES = ["cnn_api.cpp", "cnn_select.cpp", "k_direct.hip", "k_igemm.hip", "k_igemm2.hip", "k_igemm3.hip", "k_igemm4.hip", "k_smallc.hip",
-           "k_stream.hip", "k_rows.hip", "k_gemm1.hip", "k_srows.hip"]
+SOURCES = ["cnn_api.cpp", "cnn_select.cpp", "k_direct.hip", "k_igemm.hip", "k_igemm2.hip",
+           "k_igemm3.hip", "k_igemm4.hip", "k_smallc.hip", "k_rows.hip", "k_gemm1.hip",
+           "k_srows.hip"]
 
 ARCH = "gfx950"
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-function",

@@ -20,10 +20,11 @@ CNN_F32, CNN_BF16, CNN_BF16_OBF16 = 0, 1, 2
 DTYPES = {"f32": CNN_F32, "bf16": CNN_BF16, "bf16_obf16": CNN_BF16_OBF16}
 
 (K_AUTO, K_DIRECT, K_IGEMM, K_POINTWISE, K_SMALLC, K_IGEMM_PIPE, K_IGEMM_DMA, K_IGEMM_WIDE,
- K_IGEMM_RAWK, K_STREAM, K_ROWS, K_GEMM1, K_SROWS, K_SPLITC) = range(14)
+ K_IGEMM_RAWK) = range(9)
+K_ROWS, K_GEMM1, K_SROWS, K_SPLITC = range(10, 14)
 KERNEL_NAMES = {K_DIRECT: "direct", K_IGEMM: "igemm", K_POINTWISE: "pointwise", K_SMALLC: "smallc",
                 K_IGEMM_PIPE: "igemm_pipe", K_IGEMM_DMA: "igemm_dma", K_IGEMM_WIDE: "igemm_wide",
-                K_IGEMM_RAWK: "igemm_rawk", K_STREAM: "stream", K_ROWS: "rows",
+                K_IGEMM_RAWK: "igemm_rawk", K_ROWS: "rows",
                 K_GEMM1: "gemm1", K_SROWS: "srows", K_SPLITC: "splitc"}
 
 STATUS = {0: "CNN_OK", -1: "CNN_E_NULL", -2: "CNN_E_SHAPE", -3: "CNN_E_DTYPE",
@@ -31,9 +32,10 @@ STATUS = {0: "CNN_OK", -1: "CNN_E_NULL", -2: "CNN_E_SHAPE", -3: "CNN_E_DTYPE",
           -7: "CNN_E_HIP", -8: "CNN_E_PLAN"}
 
 # Every symbol include/cnn.h declares.
-EXPORTS = ["cnn_fwd", "cnn_plan", "cnn_plan_find", "cnn_plan_lookup", "cnn_plan_tiles",
-           "cnn_fwd_plan", "cnn_fwd_plan_ws", "cnn_eq1_cost", "cnn_slab_cost", "cnn_closed_form", "cnn_hbm_bytes",
-           "cnn_device_budget", "cnn_strerror", "cnn_last_error", "cnn_abi_version"]
+EXPORTS = ["cnn_fwd", "cnn_plan", "cnn_plan_candidates", "cnn_variants", "cnn_plan_find",
+           "cnn_plan_lookup", "cnn_plan_tiles", "cnn_fwd_plan", "cnn_fwd_plan_ws", "cnn_eq1_cost",
+           "cnn_slab_cost", "cnn_closed_form", "cnn_hbm_bytes", "cnn_device_budget",
+           "cnn_strerror", "cnn_last_error", "cnn_abi_version"]
 
 i64 = ctypes.c_int64
 
@@ -56,14 +58,23 @@ class Plan(ctypes.Structure):
                 ("tk", i64), ("tp", i64), ("tc", i64), ("grid", i64), ("lds_bytes", i64),
                 ("slab_rows", i64), ("ws_bytes", i64), ("eq1_elems", ctypes.c_double * 3),
                 ("eq1_bytes", ctypes.c_double), ("compulsory_bytes", ctypes.c_double),
-                ("flops", ctypes.c_double)]
+                ("flops", ctypes.c_double), ("mfma_flops", ctypes.c_double),
+                ("hbm_bytes", ctypes.c_double), ("model_us", ctypes.c_double)]
 
     def as_dict(self) -> dict:
         return {"kernel": KERNEL_NAMES.get(self.kernel, str(self.kernel)), "variant": self.variant,
                 "tk": self.tk, "tp": self.tp, "tc": self.tc, "grid": self.grid, "kc": self.kc,
                 "lds_bytes": self.lds_bytes, "slab_rows": self.slab_rows, "ws_bytes": self.ws_bytes,
                 "eq1_elems": list(self.eq1_elems), "eq1_bytes": self.eq1_bytes,
-                "compulsory_bytes": self.compulsory_bytes, "flops": self.flops}
+                "compulsory_bytes": self.compulsory_bytes, "flops": self.flops,
+                "mfma_flops": self.mfma_flops, "hbm_bytes": self.hbm_bytes,
+                "model_us": self.model_us}
+
+
+class VariantInfo(ctypes.Structure):
+    _fields_ = [("kernel", ctypes.c_int32), ("variant", ctypes.c_int32), ("dtype", ctypes.c_int32),
+                ("nr", ctypes.c_int32), ("ns", ctypes.c_int32), ("mode", ctypes.c_int32),
+                ("tk", i64), ("tp", i64), ("tc", i64)]
 
 
 class ClosedForm(ctypes.Structure):
@@ -97,6 +108,9 @@ def lib():
     P, T, B, PL = (ctypes.POINTER(x) for x in (Problem, Tiles, Budget, Plan))
     L.cnn_fwd.argtypes = [vp, vp, vp] + [i64] * 9 + [ctypes.c_int, vp]
     L.cnn_plan.argtypes = [P, ctypes.c_int, B, PL]
+    ip = ctypes.POINTER(ctypes.c_int)
+    L.cnn_plan_candidates.argtypes = [P, ctypes.c_int, B, PL, ctypes.c_int, ip]
+    L.cnn_variants.argtypes = [ctypes.POINTER(VariantInfo), ctypes.c_int, ip]
     L.cnn_plan_find.argtypes = [vp, vp, vp, P, ctypes.c_int, vp, PL, ctypes.POINTER(ctypes.c_double)]
     L.cnn_plan_lookup.argtypes = [P, ctypes.c_int, PL]
     L.cnn_plan_tiles.argtypes = [P, ctypes.c_int, ctypes.c_int, i64, i64, i64, B, PL]
@@ -114,7 +128,7 @@ def lib():
     L.cnn_last_error.argtypes = []
     L.cnn_last_error.restype = ctypes.c_char_p
     L.cnn_abi_version.argtypes = []
-    for f in ("cnn_fwd", "cnn_plan", "cnn_plan_find", "cnn_plan_lookup", "cnn_plan_tiles", "cnn_fwd_plan", "cnn_fwd_plan_ws", "cnn_eq1_cost",
+    for f in ("cnn_fwd", "cnn_plan", "cnn_plan_candidates", "cnn_variants", "cnn_plan_find", "cnn_plan_lookup", "cnn_plan_tiles", "cnn_fwd_plan", "cnn_fwd_plan_ws", "cnn_eq1_cost",
               "cnn_slab_cost", "cnn_closed_form", "cnn_hbm_bytes", "cnn_device_budget",
               "cnn_abi_version"):
         getattr(L, f).restype = ctypes.c_int
@@ -146,6 +160,26 @@ def plan(prob: Problem, dtype: int, bud: Budget | None = None) -> Plan:
     _check(lib().cnn_plan(ctypes.byref(prob), dtype, ctypes.byref(bud) if bud else None,
                           ctypes.byref(pl)))
     return pl
+
+
+def plan_candidates(prob: Problem, dtype: int, bud: Budget | None = None) -> list:
+    """Every candidate plan cnn_plan ranks, with its model fields."""
+    n = ctypes.c_int()
+    bref = ctypes.byref(bud) if bud else None
+    _check(lib().cnn_plan_candidates(ctypes.byref(prob), dtype, bref, None, 0, ctypes.byref(n)))
+    arr = (Plan * max(1, n.value))()
+    _check(lib().cnn_plan_candidates(ctypes.byref(prob), dtype, bref, arr, n.value,
+                                     ctypes.byref(n)))
+    return [Plan.from_buffer_copy(arr[i]) for i in range(n.value)]
+
+
+def variants() -> list:
+    """The library's kernel instantiations (cnn_variants)."""
+    n = ctypes.c_int()
+    _check(lib().cnn_variants(None, 0, ctypes.byref(n)))
+    arr = (VariantInfo * max(1, n.value))()
+    _check(lib().cnn_variants(arr, n.value, ctypes.byref(n)))
+    return [VariantInfo.from_buffer_copy(arr[i]) for i in range(n.value)]
 
 
 def plan_lookup(prob: Problem, dtype: int) -> Plan:

@@ -8,6 +8,7 @@
 
 #include <algorithm>
 #include <map>
+#include <set>
 #include <mutex>
 #include <string>
 #include <tuple>
@@ -23,6 +24,7 @@ void eq1_terms(const cnn_problem& p, const cnn_tiles& t, int exact, double terms
 void slab_terms(const cnn_problem& p, int64_t tk, int64_t tp, double terms[3]);
 int enumerate_plans(const cnn_problem& p, int dtype, const cnn_budget& bud, cnn_plan_t* out,
                     int cap);
+int list_variants(cnn_variant_t* out, int cap);
 }  // namespace cnnlib
 
 using namespace cnnlib;
@@ -130,44 +132,6 @@ bool same_problem(const cnn_problem& a, const cnn_problem& b) {
          a.Nr == b.Nr && a.Ns == b.Ns && a.sw == b.sw && a.sh == b.sh;
 }
 
-// Device workspace per (device, stream): holds the repacked Ker.  Kernels on
-// one stream run in order, so consecutive calls on a stream may share it.
-std::mutex g_ws_mu;
-std::map<std::pair<int, uintptr_t>, std::pair<void*, int64_t>> g_ws;
-
-int get_workspace(hipStream_t st, int64_t bytes, void** out) {
-  int dev = 0;
-  hipError_t e = hipGetDevice(&dev);
-  if (e != hipSuccess) return fail(CNN_E_HIP, "hipGetDevice: %s", hipGetErrorString(e));
-  std::lock_guard<std::mutex> g(g_ws_mu);
-  auto& ent = g_ws[std::make_pair(dev, (uintptr_t)st)];
-  if (ent.second < bytes) {
-    hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
-    e = hipStreamIsCapturing(st, &cap);
-    if (e != hipSuccess) return fail(CNN_E_HIP, "hipStreamIsCapturing: %s", hipGetErrorString(e));
-    if (cap != hipStreamCaptureStatusNone)
-      return fail(CNN_E_UNSUPPORTED,
-                  "stream is capturing and has no %lld-byte workspace yet: call once on this "
-                  "stream before capture, or use cnn_fwd_plan_ws", (long long)bytes);
-    if (ent.first) {
-      e = hipStreamSynchronize(st);
-      if (e == hipSuccess) e = hipFree(ent.first);
-      if (e != hipSuccess) return fail(CNN_E_HIP, "workspace release: %s", hipGetErrorString(e));
-      ent.first = nullptr;
-      ent.second = 0;
-    }
-    e = hipMalloc(&ent.first, (size_t)bytes);
-    if (e != hipSuccess) {
-      ent.first = nullptr;
-      return fail(CNN_E_HIP, "workspace allocation of %lld bytes: %s", (long long)bytes,
-                  hipGetErrorString(e));
-    }
-    ent.second = bytes;
-  }
-  *out = ent.first;
-  return CNN_OK;
-}
-
 const VariantS* find_variant_s(int id) {
   int n = 0;
   const VariantS* vs = variants_smallc(&n);
@@ -179,31 +143,13 @@ const VariantS* find_variant_s(int id) {
 // Geometry a few-channel plan must carry (the kernel sizes LDS from it).
 bool smallc_geometry_ok(const VariantS& v, const cnn_plan_t& pl) {
   const cnn_problem& p = pl.prob;
-  if (p.Ns > 8 || (p.Nc * p.Nr + 1) / 2 > v.ks || pl.tp < 1 || pl.tp > v.tp) return false;
+  if (p.Ns > 8 || (p.Nc * p.Nr + 1) / 2 > v.ks || pl.tp < 1 || pl.tp > v.tp ||
+      !ranges_ok_smallc(v, p, pl.dtype))
+    return false;
   const int64_t S = slab_rows_max(p, pl.tp);
   const int64_t grid = ((p.Nb * p.Nw * p.Nh + pl.tp - 1) / pl.tp) * ((p.Nk + v.tk - 1) / v.tk);
   return pl.slab_rows == S && pl.grid == grid && pl.lds_bytes == smallc_lds_bytes(v, p, S) &&
          pl.lds_bytes <= 160 * 1024;
-}
-
-const VariantT* find_variant_t(int id) {
-  int n = 0;
-  const VariantT* vs = variants_stream(&n);
-  for (int i = 0; i < n; ++i)
-    if (vs[i].id == id) return &vs[i];
-  return nullptr;
-}
-
-// Geometry a streaming plan must carry: the kernel sizes LDS, its pair
-// slots and its tile ranges from it.
-bool stream_geometry_ok(const VariantT& v, const cnn_plan_t& pl) {
-  const cnn_problem& p = pl.prob;
-  if (v.nr != p.Nr || v.ns != p.Ns || p.Nc % 8 != 0 || (v.kres && p.Nk > v.tk)) return false;
-  if (pl.tp < 1 || pl.tp > v.tp) return false;
-  const int64_t S = slab_rows_max(p, pl.tp);
-  const int64_t tiles = ((p.Nb * p.Nw * p.Nh + pl.tp - 1) / pl.tp) * ((p.Nk + v.tk - 1) / v.tk);
-  return pl.slab_rows == S && stream_fits(v, p, S) && pl.grid >= 1 && pl.grid <= tiles &&
-         pl.lds_bytes == stream_lds_bytes(v, p, S) && pl.lds_bytes <= 160 * 1024;
 }
 
 const VariantR* find_variant_r(int id) {
@@ -218,7 +164,9 @@ const VariantR* find_variant_r(int id) {
 // per tile (the kernel derives its band from tp), its LDS size and grid.
 bool rows_geometry_ok(const VariantR& v, const cnn_plan_t& pl) {
   const cnn_problem& p = pl.prob;
-  if (!rows_fits(v, p) || pl.tc != p.Nc || pl.tp < p.Nh || pl.tp % p.Nh) return false;
+  if (!rows_fits(v, p) || !ranges_ok_whole(p, pl.dtype, 1LL << 31) || pl.tc != p.Nc ||
+      pl.tp < p.Nh || pl.tp % p.Nh)
+    return false;
   const int64_t L = pl.tp / p.Nh;
   if (p.Nw % L) return false;
   const int64_t grid = p.Nb * (p.Nw / L) * ((p.Nk + v.tk - 1) / v.tk);
@@ -238,7 +186,9 @@ const VariantG* find_variant_g(int id) {
 // the grid its tiles imply, its LDS size.
 bool gemm1_geometry_ok(const VariantG& v, const cnn_plan_t& pl) {
   const cnn_problem& p = pl.prob;
-  if (pl.tp < 1 || pl.tp > v.tp || !gemm1_fits(v, p, pl.tp)) return false;
+  if (pl.tp < 1 || pl.tp > v.tp || !gemm1_fits(v, p, pl.tp) ||
+      !ranges_ok_whole(p, pl.dtype, 1LL << 30))
+    return false;
   const int64_t grid = ((p.Nb * p.Nw * p.Nh + pl.tp - 1) / pl.tp) * ((p.Nk + v.tk - 1) / v.tk);
   return pl.grid == grid && pl.lds_bytes == gemm1_lds_bytes(v) && pl.lds_bytes <= 160 * 1024;
 }
@@ -256,7 +206,9 @@ const VariantQ* find_variant_q(int id) {
 // workspace sizes.
 bool srows_geometry_ok(const VariantQ& v, const cnn_plan_t& pl) {
   const cnn_problem& p = pl.prob;
-  if (!srows_fits(v, p) || pl.tc != 16 || pl.tp != v.L * p.Nh) return false;
+  if (!srows_fits(v, p) || !ranges_ok_srows(v, p, pl.dtype) || pl.tc != 16 ||
+      pl.tp != v.L * p.Nh)
+    return false;
   const int64_t grid = p.Nb * (p.Nw / v.L) * ((p.Nk + v.tk - 1) / v.tk);
   return pl.slab_rows == srows_slab_rows(v) && pl.grid == grid &&
          pl.lds_bytes == srows_lds_bytes(v) && pl.lds_bytes <= 160 * 1024 &&
@@ -314,7 +266,8 @@ bool v2_geometry_ok(const Variant2& v, const cnn_plan_t& pl) {
   const int64_t S = slab_rows_max(p, pl.tp);
   const int64_t grid = ((p.Nb * p.Nw * p.Nh + pl.tp - 1) / pl.tp) * ((p.Nk + v.tk - 1) / v.tk);
   if (v.nr > 0 && (v.nr != p.Nr || v.ns != p.Ns)) return false;
-  if (v.rawk && p.Nc % 8 != 0) return false;
+  if (v.rawk && (p.Nc % 8 != 0 || !ranges_ok_rawk(p))) return false;
+  if (!ranges_ok_tile(p, pl.dtype, v.tp, 0)) return false;
   const int64_t pairs = v.pw ? (pl.tp + 1) / 2 : (S * Ny + 1) / 2;
   if (v.pw && (p.Nr != 1 || p.Ns != 1)) return false;
   return pl.slab_rows == S && pairs <= 256LL * v.maxp && pl.grid == grid &&
@@ -322,19 +275,19 @@ bool v2_geometry_ok(const Variant2& v, const cnn_plan_t& pl) {
          pl.lds_bytes <= 160 * 1024;
 }
 
-// ws == nullptr: use the library's per-(device, stream) workspace.
+// ws: the caller's workspace (at least pl.ws_bytes), or nullptr when the
+// plan needs none.  The library itself never allocates device memory here.
 int run_plan(const void* In, const void* Ker, void* Out, const cnn_plan_t& pl, hipStream_t st,
-             void* user_ws = nullptr) {
+             void* ws = nullptr) {
+  if (pl.ws_bytes < 0) return fail(CNN_E_PLAN, "negative ws_bytes");
+  if (pl.ws_bytes > 0 && !ws)
+    return fail(CNN_E_UNSUPPORTED,
+                "plan needs a %lld-byte device workspace: use cnn_fwd_plan_ws",
+                (long long)pl.ws_bytes);
   const ConvArgs a = make_args(pl);
   hipError_t e;
   if (pl.kernel == CNN_K_DIRECT) {
     e = launch_direct(In, Ker, Out, a, pl.dtype, st);
-  } else if (pl.kernel == CNN_K_STREAM) {
-    const VariantT* vt = find_variant_t(pl.variant);
-    if (!vt || vt->dtype != pl.dtype || vt->tk != pl.tk || vt->tc != pl.tc ||
-        !stream_geometry_ok(*vt, pl))
-      return fail(CNN_E_PLAN, "plan names no matching kernel instantiation (variant %d)", pl.variant);
-    e = launch_stream(*vt, In, Ker, Out, a, pl.lds_bytes, st);
   } else if (pl.kernel == CNN_K_GEMM1) {
     const VariantG* vg = find_variant_g(pl.variant);
     if (!vg || vg->dtype != pl.dtype || vg->tk != pl.tk || vg->tc != pl.tc ||
@@ -350,11 +303,6 @@ int run_plan(const void* In, const void* Ker, void* Out, const cnn_plan_t& pl, h
     const VariantQ* vq = find_variant_q(pl.variant);
     if (!vq || vq->dtype != pl.dtype || vq->tk != pl.tk || !srows_geometry_ok(*vq, pl))
       return fail(CNN_E_PLAN, "plan names no matching kernel instantiation (variant %d)", pl.variant);
-    void* ws = user_ws;
-    if (!ws) {
-      int st2 = get_workspace(st, pl.ws_bytes, &ws);
-      if (st2) return st2;
-    }
     e = launch_srows(*vq, In, Ker, Out, ws, a, pl.lds_bytes, st);
   } else if (pl.kernel == CNN_K_SPLITC) {
     const Variant* v = find_variant(pl.variant);
@@ -367,11 +315,6 @@ int run_plan(const void* In, const void* Ker, void* Out, const cnn_plan_t& pl, h
         pl.ws_bytes != 4LL * pl.kc * p.Nb * p.Nk * p.Nw * p.Nh)
       return fail(CNN_E_PLAN, "split plan needs 1 <= kc <= %lld and ws_bytes = 4*kc*|Out|",
                   (long long)stages);
-    void* ws = user_ws;
-    if (!ws) {
-      int st2 = get_workspace(st, pl.ws_bytes, &ws);
-      if (st2) return st2;
-    }
     e = launch_splitc(*v, In, Ker, Out, ws, a, pl.lds_bytes, pl.kc, pl.dtype, st);
   } else if (pl.kernel == CNN_K_SMALLC) {
     const VariantS* vs = find_variant_s(pl.variant);
@@ -382,21 +325,11 @@ int run_plan(const void* In, const void* Ker, void* Out, const cnn_plan_t& pl, h
     if (pl.kernel != CNN_K_IGEMM_WIDE || v4->dtype != pl.dtype || v4->tk != pl.tk ||
         v4->tp != pl.tp || v4->tc != pl.tc || pl.ws_bytes != igemm4_ws_bytes(*v4, pl.prob))
       return fail(CNN_E_PLAN, "plan names no matching kernel instantiation (variant %d)", pl.variant);
-    void* ws = user_ws;
-    if (!ws) {
-      int st2 = get_workspace(st, pl.ws_bytes, &ws);
-      if (st2) return st2;
-    }
     e = launch_igemm4(*v4, In, Ker, Out, ws, a, pl.lds_bytes, st);
   } else if (const Variant3* v3 = find_variant3(pl.variant)) {
     if (pl.kernel != CNN_K_IGEMM_DMA || v3->dtype != pl.dtype || v3->tk != pl.tk ||
         v3->tp != pl.tp || v3->tc != pl.tc || pl.ws_bytes != igemm3_ws_bytes(*v3, pl.prob))
       return fail(CNN_E_PLAN, "plan names no matching kernel instantiation (variant %d)", pl.variant);
-    void* ws = user_ws;
-    if (!ws) {
-      int st2 = get_workspace(st, pl.ws_bytes, &ws);
-      if (st2) return st2;
-    }
     e = launch_igemm3(*v3, In, Ker, Out, ws, a, pl.lds_bytes, st);
   } else if (const Variant2* v2 = find_variant2(pl.variant)) {
     if (pl.kernel != v2_family(*v2) || v2->dtype != pl.dtype ||
@@ -404,11 +337,6 @@ int run_plan(const void* In, const void* Ker, void* Out, const cnn_plan_t& pl, h
         pl.tp < 1 || pl.tp > v2->tp || v2->tc != pl.tc ||
         pl.ws_bytes != igemm2_ws_bytes(*v2, pl.prob) || !v2_geometry_ok(*v2, pl))
       return fail(CNN_E_PLAN, "plan names no matching kernel instantiation (variant %d)", pl.variant);
-    void* ws = user_ws;
-    if (!ws) {
-      int st2 = get_workspace(st, pl.ws_bytes, &ws);
-      if (st2) return st2;
-    }
     e = launch_igemm2(*v2, In, Ker, Out, ws, a, pl.lds_bytes, st);
   } else {
     const Variant* v = find_variant(pl.variant);
@@ -421,12 +349,31 @@ int run_plan(const void* In, const void* Ker, void* Out, const cnn_plan_t& pl, h
   return CNN_OK;
 }
 
+// Kernels whose dynamic-LDS limit was raised, per device.
+std::mutex g_lds_mu;
+std::set<std::pair<const void*, int>> g_lds_done;
+
 // Plan cache keyed by (problem, dtype, device).
 typedef std::tuple<int64_t, int64_t, int64_t, int64_t, int64_t, int64_t, int64_t, int64_t, int64_t, int, int> Key;
 std::mutex g_cache_mu;
 std::map<Key, cnn_plan_t> g_cache;
 
 }  // namespace
+
+namespace cnnlib {
+
+hipError_t allow_max_lds(const void* kernel) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  std::lock_guard<std::mutex> g(g_lds_mu);
+  if (g_lds_done.count(std::make_pair(kernel, dev))) return hipSuccess;
+  e = hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+  if (e == hipSuccess) g_lds_done.insert(std::make_pair(kernel, dev));
+  return e;
+}
+
+}  // namespace cnnlib
 
 extern "C" {
 
@@ -480,7 +427,7 @@ int cnn_plan_tiles(const cnn_problem* prob, int dtype, int kernel, int64_t tk, i
   if (!prob || !plan) return fail(CNN_E_NULL, "prob and plan must be non-NULL");
   int st;
   if ((st = check_problem(*prob)) || (st = check_dtype(dtype))) return st;
-  if (kernel < CNN_K_AUTO || kernel > CNN_K_SPLITC)
+  if (kernel < CNN_K_AUTO || kernel > CNN_K_SPLITC || kernel == 9)
     return fail(CNN_E_UNSUPPORTED, "unknown kernel %d", kernel);
   cnn_budget bud;
   if ((st = resolve_budget(budget, &bud))) return st;
@@ -492,6 +439,24 @@ int cnn_plan_tiles(const cnn_problem* prob, int dtype, int kernel, int64_t tk, i
 
 int cnn_plan(const cnn_problem* prob, int dtype, const cnn_budget* budget, cnn_plan_t* plan) {
   return cnn_plan_tiles(prob, dtype, CNN_K_AUTO, 0, 0, 0, budget, plan);
+}
+
+int cnn_plan_candidates(const cnn_problem* prob, int dtype, const cnn_budget* budget,
+                        cnn_plan_t* out, int cap, int* count) {
+  if (!prob || !count || (cap > 0 && !out))
+    return fail(CNN_E_NULL, "prob, count (and out when cap > 0) must be non-NULL");
+  int st;
+  if ((st = check_problem(*prob)) || (st = check_dtype(dtype))) return st;
+  cnn_budget bud;
+  if ((st = resolve_budget(budget, &bud))) return st;
+  *count = enumerate_plans(*prob, dtype, bud, out, cap < 0 ? 0 : cap);
+  return CNN_OK;
+}
+
+int cnn_variants(cnn_variant_t* out, int cap, int* count) {
+  if (!count || (cap > 0 && !out)) return fail(CNN_E_NULL, "count (and out when cap > 0) must be non-NULL");
+  *count = list_variants(out, cap < 0 ? 0 : cap);
+  return CNN_OK;
 }
 
 int cnn_fwd_plan(const void* In, const void* Ker, void* Out, const cnn_problem* prob, int dtype,
@@ -573,23 +538,31 @@ int cnn_plan_find(const void* In, const void* Ker, void* Out, const cnn_problem*
     return fail(CNN_E_HIP, "hipGetDevice: %s", hipGetErrorString(e));
   cnn_budget bud;
   if ((st = cnn_device_budget(dev, &bud))) return st;
-  static const int kCap = 128;
-  cnn_plan_t* cands = new cnn_plan_t[kCap];
-  const int n = enumerate_plans(*prob, dtype, bud, cands, kCap);
+  std::vector<cnn_plan_t> cands(256);
+  int n = enumerate_plans(*prob, dtype, bud, cands.data(), (int)cands.size());
+  if (n > (int)cands.size()) {
+    cands.resize(n);
+    n = enumerate_plans(*prob, dtype, bud, cands.data(), n);
+  }
+  // One workspace for the candidates that need one, freed before returning.
+  int64_t ws_need = 0;
+  for (int i = 0; i < n; ++i) ws_need = std::max(ws_need, cands[i].ws_bytes);
+  void* ws = nullptr;
+  if (ws_need > 0 && (e = hipMalloc(&ws, (size_t)ws_need)) != hipSuccess)
+    return fail(CNN_E_HIP, "workspace of %lld bytes for timing: %s", (long long)ws_need,
+                hipGetErrorString(e));
   hipEvent_t e0 = nullptr, e1 = nullptr;
   if ((e = hipEventCreate(&e0)) != hipSuccess || (e = hipEventCreate(&e1)) != hipSuccess) {
     if (e0) (void)hipEventDestroy(e0);
-    delete[] cands;
+    if (ws) (void)hipFree(ws);
     return fail(CNN_E_HIP, "hipEventCreate: %s", hipGetErrorString(e));
   }
-  int best = -1;
-  float best_t = 0.f;
-  // Times `reps` back-to-back runs of candidate i; -1 on a launch error.
+  // Times `reps` back-to-back runs of candidate i.
   auto time_it = [&](int i, int reps, float* ms) -> int {
     int s2;
     if ((e = hipEventRecord(e0, hs)) != hipSuccess) return fail(CNN_E_HIP, "hipEventRecord: %s", hipGetErrorString(e));
     for (int r = 0; r < reps; ++r)
-      if ((s2 = run_plan(In, Ker, Out, cands[i], hs))) return s2;
+      if ((s2 = run_plan(In, Ker, Out, cands[i], hs, ws))) return s2;
     if ((e = hipEventRecord(e1, hs)) != hipSuccess || (e = hipEventSynchronize(e1)) != hipSuccess ||
         (e = hipEventElapsedTime(ms, e0, e1)) != hipSuccess)
       return fail(CNN_E_HIP, "timing: %s", hipGetErrorString(e));
@@ -597,61 +570,74 @@ int cnn_plan_find(const void* In, const void* Ker, void* Out, const cnn_problem*
     return CNN_OK;
   };
   st = CNN_OK;
-  std::vector<float> first(n, 0.f);
+  std::vector<float> first(n, 0.f), final_t(n, 0.f);
   for (int i = 0; i < n && st == CNN_OK; ++i) {
     float t1 = 0.f, t = 0.f;
-    if ((st = time_it(i, 1, &t1))) break;  // first run: workspace, caches
+    if ((st = time_it(i, 1, &t1))) break;  // first run: caches
     const int reps = t1 <= 0.f ? 20 : std::max(3, std::min(20, (int)(2.0f / t1)));
     if ((st = time_it(i, reps, &t))) break;
-    first[i] = t;
-    if (best < 0 || t < best_t) {
-      best = i;
-      best_t = t;
-    }
+    first[i] = final_t[i] = t;
   }
-  // Candidates within 15 % of the fastest are timed again, interleaved over
-  // three rounds of longer runs, and ranked by their fastest round: one
+  // The fastest candidates (overall, and among those that need no
+  // workspace) and those within 15 % of them are timed again, interleaved
+  // over three rounds of longer runs, and ranked by their fastest round: one
   // short run per candidate differs by a few per cent from run to run, and
   // the clocks may still be rising during the first pass.
-  if (st == CNN_OK && best >= 0) {
-    std::vector<int> fin;
+  auto argmin = [&](const std::vector<float>& t, bool ws_free) {
+    int b = -1;
     for (int i = 0; i < n; ++i)
-      if (first[i] <= 1.15f * best_t) fin.push_back(i);
-    std::sort(fin.begin(), fin.end(), [&](int x, int y) { return first[x] < first[y]; });
-    if (fin.size() > 4) fin.resize(4);
+      if ((!ws_free || cands[i].ws_bytes == 0) && (b < 0 || t[i] < t[b])) b = i;
+    return b;
+  };
+  if (st == CNN_OK && n > 0) {
+    std::vector<int> fin;
+    for (int pass = 0; pass < 2; ++pass) {
+      const int b = argmin(first, pass == 1);
+      if (b < 0) continue;
+      std::vector<int> near;
+      for (int i = 0; i < n; ++i)
+        if ((pass == 0 || cands[i].ws_bytes == 0) && first[i] <= 1.15f * first[b]) near.push_back(i);
+      std::sort(near.begin(), near.end(), [&](int x, int y) { return first[x] < first[y]; });
+      if (near.size() > 4) near.resize(4);
+      for (int i : near)
+        if (std::find(fin.begin(), fin.end(), i) == fin.end()) fin.push_back(i);
+    }
     if (fin.size() > 1) {
-      std::vector<float> fbest(fin.size(), 0.f);
       for (int round = 0; round < 3 && st == CNN_OK; ++round)
         for (size_t f = 0; f < fin.size() && st == CNN_OK; ++f) {
           const float t0 = first[fin[f]];
           const int reps = t0 <= 0.f ? 50 : std::max(10, std::min(100, (int)(0.5f / t0)));
           float t = 0.f;
           if ((st = time_it(fin[f], reps, &t))) break;
-          if (round == 0 || t < fbest[f]) fbest[f] = t;
+          if (round == 0 || t < final_t[fin[f]]) final_t[fin[f]] = t;
         }
-      if (st == CNN_OK) {
-        size_t w = 0;
-        for (size_t f = 1; f < fin.size(); ++f)
-          if (fbest[f] < fbest[w]) w = f;
-        best = fin[w];
-        best_t = fbest[w];
-      }
     }
+  }
+  const int best = st == CNN_OK ? argmin(final_t, false) : -1;
+  const int best_free = st == CNN_OK ? argmin(final_t, true) : -1;
+  if (best >= 0) {
+    // Leave Out holding the returned plan's result, like a cnn_fwd call would.
+    st = run_plan(In, Ker, Out, cands[best], hs, ws);
   }
   (void)hipEventDestroy(e0);
   (void)hipEventDestroy(e1);
-  if (st == CNN_OK) {
-    // Leave Out holding the winner's result, like a cnn_fwd call would.
-    st = run_plan(In, Ker, Out, cands[best], hs);
+  if (ws) {
+    e = hipStreamSynchronize(hs);
+    const hipError_t e2 = hipFree(ws);
+    if (st == CNN_OK && (e != hipSuccess || e2 != hipSuccess))
+      st = fail(CNN_E_HIP, "workspace release: %s", hipGetErrorString(e != hipSuccess ? e : e2));
   }
+  if (st == CNN_OK && best < 0) st = fail(CNN_E_UNSUPPORTED, "no candidate plan");
   if (st == CNN_OK) {
     *plan = cands[best];
-    if (best_ms) *best_ms = best_t;
-    const cnn_problem& p = *prob;
-    std::lock_guard<std::mutex> g(g_cache_mu);
-    g_cache[Key(p.Nb, p.Nc, p.Nk, p.Nw, p.Nh, p.Nr, p.Ns, p.sw, p.sh, dtype, dev)] = cands[best];
+    if (best_ms) *best_ms = final_t[best];
+    if (best_free >= 0) {
+      const cnn_problem& p = *prob;
+      std::lock_guard<std::mutex> g(g_cache_mu);
+      g_cache[Key(p.Nb, p.Nc, p.Nk, p.Nw, p.Nh, p.Nr, p.Ns, p.sw, p.sh, dtype, dev)] =
+          cands[best_free];
+    }
   }
-  delete[] cands;
   return st;
 }
 

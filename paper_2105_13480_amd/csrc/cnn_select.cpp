@@ -23,6 +23,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <vector>
 
 #include "internal.h"
 
@@ -89,25 +90,58 @@ void eq1_terms(const cnn_problem& p, const cnn_tiles& t, int exact, double terms
                  (double)(t.Tw * t.Th * t.Tb * t.Tk) + (double)(p.Nr * p.Ns * t.Tk * t.Tc);
 }
 
-// MFMA throughput per CU per clock for the dtype's operand type.
-static double mfma_rate(int dtype) { return dtype == CNN_F32 ? 256.0 : 4096.0; }
-// CU <- L2 bytes per CU per clock assumed by the time model.
-static const double kL2BytesPerClk = 64.0;
+// Byte ranges each family addresses with 32-bit buffer offsets (the kernels
+// clamp their buffer descriptors just below 2 GiB): a plan outside them is
+// never made, and a plan handed in is rejected (plan_ranges_ok).
+static const int64_t k2G = 1LL << 31;
 
-// Time model and plan fields shared by the implicit-GEMM families.
+static int64_t in_elems(const cnn_problem& p) {
+  return p.Nb * p.Nc * (p.sw * (p.Nw - 1) + p.Nr) * (p.sh * (p.Nh - 1) + p.Ns);
+}
+
+// images a tile of up to tp outputs touches, plus one of slack each side
+static int64_t tile_images(const cnn_problem& p, int64_t tp) { return tp / (p.Nw * p.Nh) + 2; }
+
+bool ranges_ok_tile(const cnn_problem& p, int dtype, int64_t tp, int64_t tc_extra) {
+  const int64_t Nx = p.sw * (p.Nw - 1) + p.Nr, Ny = p.sh * (p.Nh - 1) + p.Ns;
+  const int64_t imgs = tile_images(p, tp);
+  return (imgs * p.Nc + tc_extra) * Nx * Ny * 2 < k2G &&
+         imgs * p.Nk * p.Nw * p.Nh * out_bytes(dtype) < k2G;
+}
+
+bool ranges_ok_rawk(const cnn_problem& p) {
+  // Ker rows up to Nk + tk + 64 are addressed
+  return (p.Nk + 512) * p.Nc * p.Nr * p.Ns * 2 < k2G;
+}
+
+bool ranges_ok_whole(const cnn_problem& p, int dtype, int64_t in_limit) {
+  return in_elems(p) * 2 < in_limit && p.Nk * p.Nc * p.Nr * p.Ns * 2 < in_limit &&
+         p.Nb * p.Nk * p.Nw * p.Nh * out_bytes(dtype) < k2G;
+}
+
+bool ranges_ok_smallc(const VariantS& v, const cnn_problem& p, int dtype) {
+  return in_elems(p) * 2 < k2G && p.Nk * p.Nc * p.Nr * p.Ns * 2 < k2G &&
+         tile_images(p, v.tp) * p.Nk * p.Nw * p.Nh * out_bytes(dtype) < k2G;
+}
+
+bool ranges_ok_srows(const VariantQ& v, const cnn_problem& p, int dtype) {
+  return in_elems(p) * 2 < k2G && srows_ws_bytes(v, p) < k2G &&
+         p.Nb * p.Nk * p.Nw * p.Nh * out_bytes(dtype) < k2G;
+}
+
+static double model_us(const cnn_plan_t& pl, const cnn_budget& bud);
+
+// Plan fields shared by the implicit-GEMM families (the model's time is set
+// once the plan is complete).
 static bool eval_tiling(const cnn_problem& p, int dtype, int id, int64_t tk, int64_t tp,
                         int64_t tc, int64_t acc, int64_t S, int64_t lds, int64_t ws,
-                        const cnn_budget& bud, cnn_plan_t* plan, double* time_clk) {
+                        const cnn_budget& bud, cnn_plan_t* plan) {
   const int64_t RS = p.Nr * p.Ns;
   const int64_t npix = p.Nb * p.Nw * p.Nh;
   if (lds > bud.lds_bytes || acc > bud.acc_regs) return false;
   const int64_t n_p = ceil_div(npix, tp), n_k = ceil_div(p.Nk, tk);
   const int64_t grid = n_p * n_k;
   if (grid > 0x7fffffffLL) return false;
-  int64_t occ = bud.lds_bytes / lds;
-  occ = std::max<int64_t>(1, std::min<int64_t>(occ, bud.wg_per_cu));
-  const int64_t slots = bud.cus * occ;
-  const int64_t rounds = ceil_div(grid, slots);
 
   double terms[3];
   slab_terms(p, tk, tp, terms);
@@ -115,9 +149,6 @@ static bool eval_tiling(const cnn_problem& p, int dtype, int id, int64_t tk, int
   const double bytes = e_out * terms[0] + e_in * (terms[1] + terms[2]);
   const double tile_flops =
       2.0 * tk * tp * (double)(ceil_div(p.Nc, tc) * tc) * (double)RS;
-  const double tile_clk =
-      std::max(tile_flops / mfma_rate(dtype), (bytes / (double)grid) / kL2BytesPerClk);
-  *time_clk = (double)rounds * (double)slots / (double)bud.cus * tile_clk;
 
   memset(plan, 0, sizeof(*plan));
   plan->prob = p;
@@ -133,48 +164,39 @@ static bool eval_tiling(const cnn_problem& p, int dtype, int id, int64_t tk, int
   plan->ws_bytes = ws;
   for (int i = 0; i < 3; ++i) plan->eq1_elems[i] = terms[i];
   plan->eq1_bytes = bytes;
+  plan->mfma_flops = tile_flops * (double)grid;
   return true;
 }
 
 // Plain staging kernel (conv_igemm).
 static bool eval_variant(const cnn_problem& p, int dtype, const Variant& v,
-                         const cnn_budget& bud, cnn_plan_t* plan, double* time_clk) {
+                         const cnn_budget& bud, cnn_plan_t* plan) {
   const int64_t Ny = p.sh * (p.Nh - 1) + p.Ns;
   const int64_t S = slab_rows_max(p, v.tp);
   const int64_t lds = igemm_lds_bytes(v, S, Ny, p.Nr * p.Ns);
-  return eval_tiling(p, dtype, v.id, v.tk, v.tp, v.tc, v.acc, S, lds, 0, bud, plan, time_clk);
+  return eval_tiling(p, dtype, v.id, v.tk, v.tp, v.tc, v.acc, S, lds, 0, bud, plan);
 }
 
 // Wide-staging pipelined kernel (conv_igemm4).
 static bool eval_variant4(const cnn_problem& p, int dtype, const Variant4& v,
-                          const cnn_budget& bud, cnn_plan_t* plan, double* time_clk) {
+                          const cnn_budget& bud, cnn_plan_t* plan) {
   const int64_t Ny = p.sh * (p.Nh - 1) + p.Ns;
   const int64_t S = slab_rows_max(p, v.tp);
-  if (!igemm4_fits(v, p, S)) return false;
-  const int64_t Nx = p.sw * (p.Nw - 1) + p.Nr;
-  const int64_t imgs = v.tp / (p.Nw * p.Nh) + 2;
-  if ((imgs * p.Nc + v.tc) * Nx * Ny * 2 >= (1LL << 31) ||
-      imgs * p.Nk * p.Nw * p.Nh * out_bytes(dtype) >= (1LL << 31))
-    return false;
+  if (!igemm4_fits(v, p, S) || !ranges_ok_tile(p, dtype, v.tp, v.tc)) return false;
   const int64_t lds = igemm4_lds_bytes(v, S, Ny, p.Nr * p.Ns);
   return eval_tiling(p, dtype, v.id, v.tk, v.tp, v.tc, v.acc, S, lds, igemm4_ws_bytes(v, p),
-                     bud, plan, time_clk);
+                     bud, plan);
 }
 
 // DMA-staged kernel (conv_igemm3).
 static bool eval_variant3(const cnn_problem& p, int dtype, const Variant3& v,
-                          const cnn_budget& bud, cnn_plan_t* plan, double* time_clk) {
+                          const cnn_budget& bud, cnn_plan_t* plan) {
   const int64_t Ny = p.sh * (p.Nh - 1) + p.Ns;
   const int64_t S = slab_rows_max(p, v.tp);
-  if (!igemm3_fits(v, p, S)) return false;
-  const int64_t Nx = p.sw * (p.Nw - 1) + p.Nr;
-  const int64_t imgs = v.tp / (p.Nw * p.Nh) + 2;
-  if ((imgs * p.Nc + v.tc) * Nx * Ny * 2 >= (1LL << 31) ||
-      imgs * p.Nk * p.Nw * p.Nh * out_bytes(dtype) >= (1LL << 31))
-    return false;
+  if (!igemm3_fits(v, p, S) || !ranges_ok_tile(p, dtype, v.tp, v.tc)) return false;
   const int64_t lds = igemm3_lds_bytes(v, S, Ny);
   return eval_tiling(p, dtype, v.id, v.tk, v.tp, v.tc, v.acc, S, lds, igemm3_ws_bytes(v, p),
-                     bud, plan, time_clk);
+                     bud, plan);
 }
 
 // Outputs per tile for a kernel whose tiles hold up to TP outputs: the
@@ -204,11 +226,11 @@ int v2_family(const Variant2& v) {
 // (or be generic) and its slab must fit the per-thread staging registers;
 // raw-Ker instantiations need Nc % 8 == 0 and Ker well below 2 GiB.
 static bool eval_variant2(const cnn_problem& p, int dtype, const Variant2& v,
-                          const cnn_budget& bud, cnn_plan_t* plan, double* time_clk) {
+                          const cnn_budget& bud, cnn_plan_t* plan) {
   if (v.nr > 0 && (v.nr != p.Nr || v.ns != p.Ns)) return false;
   // (rows up to Nk + tk + 64 are addressed with 32-bit byte offsets)
-  if (v.rawk && (p.Nc % 8 != 0 || (p.Nk + 512) * p.Nc * p.Nr * p.Ns * 2 >= (1LL << 31)))
-    return false;
+  if (v.rawk && (p.Nc % 8 != 0 || !ranges_ok_rawk(p))) return false;
+  if (!ranges_ok_tile(p, dtype, v.tp, 0)) return false;
   const int64_t Ny = p.sh * (p.Nh - 1) + p.Ns;
   const int64_t lds_full = igemm2_lds_bytes(v, slab_rows_max(p, v.tp), Ny, p.Nr * p.Ns, v.tp);
   const int64_t occ = std::max<int64_t>(1, std::min<int64_t>(bud.wg_per_cu, bud.lds_bytes / lds_full));
@@ -216,140 +238,169 @@ static bool eval_variant2(const cnn_problem& p, int dtype, const Variant2& v,
   const int64_t S = slab_rows_max(p, tp);
   const int64_t pairs = v.pw ? (tp + 1) / 2 : (S * Ny + 1) / 2;
   if (pairs > 256 * (int64_t)v.maxp) return false;
-  // per-tile buffer offsets are 32-bit: the images a tile touches must span
-  // less than 2 GiB of In and of Out
-  const int64_t Nx = p.sw * (p.Nw - 1) + p.Nr;
-  const int64_t imgs = v.tp / (p.Nw * p.Nh) + 2;
-  if (imgs * p.Nc * Nx * Ny * 2 >= (1LL << 31) ||
-      imgs * p.Nk * p.Nw * p.Nh * out_bytes(dtype) >= (1LL << 31))
-    return false;
   const int64_t lds = igemm2_lds_bytes(v, S, Ny, p.Nr * p.Ns, tp);
   return eval_tiling(p, dtype, v.id, v.tk, tp, v.tc, v.acc, S, lds, igemm2_ws_bytes(v, p),
-                     bud, plan, time_clk);
+                     bud, plan);
 }
 
 // Few-channel kernel (conv_smallc): the flattened (c, r) rows must fit the
 // registers' K-steps, the stencil at most 8 wide, the slab in LDS, and the
 // tensors the 32-bit offsets.
-static bool eval_smallc(const cnn_problem& p, int dtype, const VariantS& v, const cnn_budget& bud,
-                        cnn_plan_t* plan, double* time_clk) {
-  if (p.Ns > 8 || (p.Nc * p.Nr + 1) / 2 > v.ks) return false;
-  const int64_t Nx = p.sw * (p.Nw - 1) + p.Nr, Ny = p.sh * (p.Nh - 1) + p.Ns;
-  if (p.Nb * p.Nc * Nx * Ny * 2 >= (1LL << 31) || p.Nk * p.Nc * p.Nr * p.Ns * 2 >= (1LL << 31))
-    return false;
-  const int64_t imgs = v.tp / (p.Nw * p.Nh) + 2;
-  if (imgs * p.Nk * p.Nw * p.Nh * out_bytes(dtype) >= (1LL << 31)) return false;
+static bool eval_smallc(const cnn_problem& p, int dtype, const VariantS& v, const cnn_budget& bud, cnn_plan_t* plan) {
+  if (p.Ns > 8 || (p.Nc * p.Nr + 1) / 2 > v.ks || !ranges_ok_smallc(v, p, dtype)) return false;
   const int64_t lds_full = smallc_lds_bytes(v, p, slab_rows_max(p, v.tp));
   const int64_t occ = std::max<int64_t>(1, std::min<int64_t>(bud.wg_per_cu, bud.lds_bytes / lds_full));
   const int64_t tp = balanced_tp(p, v.tp, v.tk, bud.cus * occ, 1);
   const int64_t S = slab_rows_max(p, tp);
   const int64_t lds = smallc_lds_bytes(v, p, S);
   // one stage holds every channel (tc = Nc)
-  return eval_tiling(p, dtype, v.id, v.tk, tp, p.Nc, v.acc, S, lds, 0, bud, plan, time_clk);
-}
-
-// Persistent streaming kernel (conv_stream): fixed stencil, Nc % 8 == 0,
-// the slab within the per-thread copy and transpose counts, KRES needs one
-// k tile; the grid is the workgroup slots (each walks a range of tiles).
-static bool eval_stream(const cnn_problem& p, int dtype, const VariantT& v, const cnn_budget& bud,
-                        cnn_plan_t* plan, double* time_clk) {
-  if (v.nr != p.Nr || v.ns != p.Ns || p.Nc % 8 != 0) return false;
-  if (v.kres && p.Nk > v.tk) return false;
-  const int64_t Nx = p.sw * (p.Nw - 1) + p.Nr, Ny = p.sh * (p.Nh - 1) + p.Ns;
-  if ((p.Nk + 512) * p.Nc * p.Nr * p.Ns * 2 >= (1LL << 31) ||
-      p.Nb * p.Nc * Nx * Ny * 2 >= (1LL << 31) ||
-      p.Nb * p.Nk * p.Nw * p.Nh * out_bytes(dtype) >= (1LL << 31))
-    return false;
-  const int64_t lds_full = stream_lds_bytes(v, p, slab_rows_max(p, v.tp));
-  const int64_t occ = std::max<int64_t>(
-      1, std::min<int64_t>(bud.wg_per_cu * 256 / v.threads, bud.lds_bytes / lds_full));
-  const int64_t slots = bud.cus * occ;
-  const int64_t tp = balanced_tp(p, v.tp, v.tk, slots, 2);
-  const int64_t S = slab_rows_max(p, tp);
-  if (!stream_fits(v, p, S)) return false;
-  const int64_t lds = stream_lds_bytes(v, p, S);
-  if (!eval_tiling(p, dtype, v.id, v.tk, tp, v.tc, v.acc, S, lds, 0, bud, plan, time_clk))
-    return false;
-  plan->grid = std::min<int64_t>(plan->grid, slots);
-  return true;
+  return eval_tiling(p, dtype, v.id, v.tk, tp, p.Nc, v.acc, S, lds, 0, bud, plan);
 }
 
 // Row-streaming kernel (conv_rows): stride 1, fixed stencil, Nc % 8 == 0,
 // input rows of at most 32*mb positions; a tile is L whole output rows of
 // one image (L divides Nw, tp = L*Nh) by 64 features, all Nc channels.
-// L = 0 picks the band: the fewest rounds of groups of wr rows per
-// workgroup (one workgroup per CU), then the largest L (least halo).
 static bool eval_rows(const cnn_problem& p, int dtype, const VariantR& v, const cnn_budget& bud,
-                      int64_t L, cnn_plan_t* plan, double* time_clk) {
-  if (!rows_fits(v, p)) return false;
-  const int64_t Nx = p.Nw + p.Nr - 1, Ny = p.Nh + p.Ns - 1;
-  if (p.Nb * p.Nc * Nx * Ny * 2 >= (1LL << 31) || p.Nk * p.Nc * p.Nr * p.Ns * 2 >= (1LL << 31) ||
-      p.Nb * p.Nk * p.Nw * p.Nh * out_bytes(dtype) >= (1LL << 31))
-    return false;
+                      int64_t L, cnn_plan_t* plan) {
+  if (!rows_fits(v, p) || !ranges_ok_whole(p, dtype, k2G)) return false;
   const int64_t lds = rows_lds_bytes(v, p);
   if (lds > std::min<int64_t>(bud.lds_bytes, 160 * 1024)) return false;
-  const int64_t nk = ceil_div(p.Nk, v.tk);
-  if (L == 0) {
-    int64_t best = -1;
-    for (int64_t l = 1; l <= p.Nw; ++l) {
-      if (p.Nw % l) continue;
-      const int64_t cost = ceil_div(p.Nb * (p.Nw / l) * nk, bud.cus) * ceil_div(l, v.wr);
-      if (best < 0 || cost <= best) {
-        best = cost;
-        L = l;
-      }
-    }
-  }
   if (L < 1 || p.Nw % L) return false;
   const int64_t tp = L * p.Nh;
   // the accumulator budget is per lane at two waves per SIMD (8 per
   // workgroup); a 4-wave workgroup (one wave per SIMD) has twice the registers
   cnn_budget b2 = bud;
   b2.acc_regs = bud.acc_regs * 8 / v.waves;
-  return eval_tiling(p, dtype, v.id, v.tk, tp, p.Nc, v.acc, L + p.Nr - 1, lds, 0, b2, plan,
-                     time_clk);
+  if (!eval_tiling(p, dtype, v.id, v.tk, tp, p.Nc, v.acc, L + p.Nr - 1, lds, 0, b2, plan))
+    return false;
+  // the products run over whole 32-position blocks of the input row and
+  // 16-channel groups, every tap at unshifted positions
+  plan->mfma_flops = 2.0 * (double)(ceil_div(p.Nk, v.tk) * v.tk) * (double)(p.Nb * p.Nw) *
+                     (double)(32 * v.mb) * (double)(16 * v.ncg) * (double)(p.Nr * p.Ns);
+  return true;
 }
 
 // 1x1 stride-1 GEMM kernel (conv_gemm1): tiles of tp consecutive pixels
 // (a multiple of 4, balanced over the CUs) by tk features.
-static bool eval_gemm1(const cnn_problem& p, int dtype, const VariantG& v, const cnn_budget& bud,
-                       cnn_plan_t* plan, double* time_clk) {
+static bool eval_gemm1(const cnn_problem& p, int dtype, const VariantG& v, const cnn_budget& bud, cnn_plan_t* plan) {
   const int64_t lds = gemm1_lds_bytes(v);
   if (lds > std::min<int64_t>(bud.lds_bytes, 160 * 1024)) return false;
-  const int64_t Nx = p.sw * (p.Nw - 1) + 1, Ny = p.sh * (p.Nh - 1) + 1;
-  if (p.Nb * p.Nc * Nx * Ny * 2 >= (1LL << 30) || p.Nk * p.Nc * 2 >= (1LL << 30) ||
-      p.Nb * p.Nk * p.Nw * p.Nh * out_bytes(dtype) >= (1LL << 31))
-    return false;
+  if (!ranges_ok_whole(p, dtype, 1LL << 30)) return false;
   const int64_t occ = std::max<int64_t>(1, std::min<int64_t>(bud.wg_per_cu, bud.lds_bytes / lds));
   int64_t tp = balanced_tp(p, v.tp, v.tk, bud.cus * occ, 1);
   tp = std::min<int64_t>(v.tp, (tp + 3) / 4 * 4);
   if (v.s2 == 2) tp = p.Nw * p.Nh;  // a tile is one image
   if (!gemm1_fits(v, p, tp)) return false;
-  return eval_tiling(p, dtype, v.id, v.tk, tp, v.tc, v.acc, 1, lds, 0, bud, plan, time_clk);
+  return eval_tiling(p, dtype, v.id, v.tk, tp, v.tc, v.acc, 1, lds, 0, bud, plan);
 }
 
 // Stride-2 row-band kernel (conv_srows): fixed stencil, tiles of the
 // instantiation's L whole output rows of one image by 256 features, 16
 // channels per chunk, Ker repacked into the workspace.
-static bool eval_srows(const cnn_problem& p, int dtype, const VariantQ& v, const cnn_budget& bud,
-                       cnn_plan_t* plan, double* time_clk) {
-  if (!srows_fits(v, p)) return false;
-  const int64_t Nx = 2 * (p.Nw - 1) + p.Nr, Ny = 2 * (p.Nh - 1) + p.Ns;
+static bool eval_srows(const cnn_problem& p, int dtype, const VariantQ& v, const cnn_budget& bud, cnn_plan_t* plan) {
+  if (!srows_fits(v, p) || !ranges_ok_srows(v, p, dtype)) return false;
   const int64_t ws = srows_ws_bytes(v, p);
-  if (p.Nb * p.Nc * Nx * Ny * 2 >= (1LL << 31) || ws >= (1LL << 31) ||
-      p.Nb * p.Nk * p.Nw * p.Nh * out_bytes(dtype) >= (1LL << 31))
-    return false;
   const int64_t lds = srows_lds_bytes(v);
   if (lds > std::min<int64_t>(bud.lds_bytes, 160 * 1024)) return false;
   // the accumulator budget is per lane at two waves per SIMD; a 4-wave
   // workgroup (one wave per SIMD) has twice the registers
   cnn_budget b2 = bud;
   b2.acc_regs = bud.acc_regs * 8 / v.waves;
-  return eval_tiling(p, dtype, v.id, v.tk, v.L * p.Nh, 16, v.acc, srows_slab_rows(v), lds, ws,
-                     b2, plan, time_clk);
+  if (!eval_tiling(p, dtype, v.id, v.tk, v.L * p.Nh, 16, v.acc, srows_slab_rows(v), lds, ws,
+                   b2, plan))
+    return false;
+  // a 32-position MFMA block per output row
+  plan->mfma_flops = 2.0 * (double)(ceil_div(p.Nk, v.tk) * v.tk) * (double)(p.Nb * p.Nw * 32) *
+                     (double)(p.Nc * p.Nr * p.Ns);
+  return true;
 }
 
-static void fill_common(const cnn_problem& p, int dtype, cnn_plan_t* plan) {
+// The XCD / L2 level the two-level model (Eq. (3) one level up) sees: 8 XCDs
+// of one 4 MiB L2 each on MI355X.
+static const int64_t kXcds = 8;
+static const int64_t kL2Bytes = 4LL << 20;
+
+// Rates of one MI355X the time model converts work and bytes with, all
+// measured on the device (not datasheet figures): the engine clock; the
+// bf16 MFMA rate sustained on operands of these workloads' value ranges
+// (64 % of the 4096 flop/clk/CU datasheet rate: the clock drops with the
+// data-dependent power; fp32 MFMA is taken at its datasheet rate); the
+// CU <- L2 bandwidth per CU; the HBM bandwidth of a large device copy (read
+// plus write); a kernel launch in a graph replay.
+static const double kClkGHz = 2.4;
+static const double kMfmaRealBf16 = 0.64;
+static const double kL2BytesPerClkCU = 64.0;
+static const double kHbmGBs = 5000.0;
+static const double kLaunchUs = 2.0;
+
+// MFMA throughput per CU per clock for the dtype's operand type.
+static double mfma_rate(int dtype) { return dtype == CNN_F32 ? 256.0 : 4096.0; }
+
+// What each kernel family adds to the bounds: the fraction of the sustained
+// MFMA rate its inner loop reaches (operand staging, barriers and waits
+// between the products), its fixed cost per launch beyond the launch itself
+// (set-up, a second kernel) in microseconds, and whether its Out stores
+// drain under later work (true) or only after its last tile (false).
+struct FamilyCost {
+  double mfma_eff;
+  double fixed_us;
+  bool stores_overlap;
+};
+
+static FamilyCost family_cost(int kernel) {
+  switch (kernel) {
+    case CNN_K_ROWS: return {0.70, 2.5, true};
+    case CNN_K_SROWS: return {0.55, 1.5, false};
+    case CNN_K_GEMM1: return {0.55, 1.5, false};
+    case CNN_K_SMALLC: return {0.40, 1.5, false};
+    case CNN_K_IGEMM_RAWK: return {0.35, 1.5, false};
+    case CNN_K_POINTWISE: return {0.30, 1.5, false};
+    case CNN_K_IGEMM_PIPE: return {0.35, 3.0, false};
+    case CNN_K_IGEMM_DMA: return {0.30, 3.0, false};
+    case CNN_K_IGEMM_WIDE: return {0.35, 3.0, false};
+    case CNN_K_SPLITC: return {0.15, 3.0, false};
+    case CNN_K_IGEMM: return {0.15, 1.0, false};
+    default: return {0.25, 1.0, false};  // direct: fp32 vector FMAs
+  }
+}
+
+// The selector's time model for a finished plan (its grid, tiles, Eq. (1)
+// bytes and MFMA work set), in microseconds: the busiest CU's share of the
+// MFMA work, of the Eq. (1) traffic and of the HBM traffic, whichever takes
+// longest, plus the Out drain the family cannot overlap, the launch and
+// the family's fixed cost.
+static double model_us(const cnn_plan_t& pl, const cnn_budget& bud) {
+  const cnn_problem& p = pl.prob;
+  const FamilyCost fc = family_cost(pl.kernel);
+  const double clk_per_us = kClkGHz * 1e3;
+  const double cus = (double)bud.cus;
+  const double out_b = (double)(p.Nb * p.Nk * p.Nw * p.Nh) * out_bytes(pl.dtype);
+  if (pl.kernel == CNN_K_DIRECT) {
+    // 64 lanes x 4 SIMDs x one fp32 FMA (2 flops) per clock per CU
+    const double t = pl.flops / (cus * 512.0 * clk_per_us * fc.mfma_eff);
+    return std::max(t, pl.hbm_bytes / (kHbmGBs * 1e3)) + kLaunchUs + fc.fixed_us;
+  }
+  const double wgs = (double)pl.grid * (pl.kernel == CNN_K_SPLITC ? (double)pl.kc : 1.0);
+  const double per_cu = std::ceil(wgs / cus);        // workgroups the busiest CU runs
+  const double rate = mfma_rate(pl.dtype) * (pl.dtype == CNN_F32 ? 1.0 : kMfmaRealBf16);
+  const double t_mfma = per_cu * (pl.mfma_flops / wgs) / (rate * fc.mfma_eff * clk_per_us);
+  const double t_l2 = per_cu * (pl.eq1_bytes / wgs) / (kL2BytesPerClkCU * clk_per_us);
+  // Out stores of the last round of workgroups drain after their products
+  // unless the family overlaps them.
+  int64_t occ = std::max<int64_t>(1, std::min<int64_t>(bud.wg_per_cu,
+                                                      bud.lds_bytes / std::max<int64_t>(1, pl.lds_bytes)));
+  const double rounds = std::ceil(wgs / (cus * (double)occ));
+  const double drain_b = fc.stores_overlap ? 0.0 : out_b / rounds;
+  const double t_hbm = (pl.hbm_bytes - drain_b) / (kHbmGBs * 1e3);
+  double t = std::max(std::max(t_mfma, t_l2), t_hbm) + drain_b / (kHbmGBs * 1e3);
+  if (pl.kernel == CNN_K_SPLITC)  // the reduce pass: kc fp32 partials read, Out written
+    t += (4.0 * (double)pl.kc * (double)(p.Nb * p.Nk * p.Nw * p.Nh) + out_b) / (kHbmGBs * 1e3) +
+         kLaunchUs;
+  return t + kLaunchUs + fc.fixed_us;
+}
+
+static void fill_common(const cnn_problem& p, int dtype, const cnn_budget& bud,
+                        cnn_plan_t* plan) {
   const int64_t Nx = p.sw * (p.Nw - 1) + p.Nr, Ny = p.sh * (p.Nh - 1) + p.Ns;
   const double e_in = in_bytes(dtype), e_out = out_bytes(dtype);
   // Compulsory traffic: In elements that some output reads, Ker, Out once.
@@ -359,9 +410,18 @@ static void fill_common(const cnn_problem& p, int dtype, cnn_plan_t* plan) {
                                    (double)(p.Nk * p.Nc * p.Nr * p.Ns)) +
                            e_out * (double)(p.Nb * p.Nk * p.Nw * p.Nh);
   plan->flops = 2.0 * (double)p.Nb * p.Nk * p.Nc * p.Nr * p.Ns * p.Nw * p.Nh;
+  if (plan->kernel == CNN_K_DIRECT) {
+    plan->mfma_flops = 0.0;
+    plan->hbm_bytes = plan->compulsory_bytes;
+  } else {
+    double t[3];
+    hbm_terms(*plan, kXcds, kL2Bytes, t);
+    plan->hbm_bytes = t[0] + t[1] + t[2];
+  }
+  plan->model_us = model_us(*plan, bud);
 }
 
-void direct_plan(const cnn_problem& p, int dtype, cnn_plan_t* plan) {
+void direct_plan(const cnn_problem& p, int dtype, const cnn_budget& bud, cnn_plan_t* plan) {
   memset(plan, 0, sizeof(*plan));
   plan->prob = p;
   plan->dtype = dtype;
@@ -378,7 +438,7 @@ void direct_plan(const cnn_problem& p, int dtype, cnn_plan_t* plan) {
   eq1_terms(p, t, 1, terms, nullptr);
   for (int i = 0; i < 3; ++i) plan->eq1_elems[i] = terms[i];
   plan->eq1_bytes = out_bytes(dtype) * terms[0] + in_bytes(dtype) * (terms[1] + terms[2]);
-  fill_common(p, dtype, plan);
+  fill_common(p, dtype, bud, plan);
 }
 
 // Eq. (3) one level up: the plan's tiles split over `xcds` processors (the
@@ -482,10 +542,109 @@ static void splitc_finish(const cnn_problem& p, const cnn_budget& bud, cnn_plan_
   plan->ws_bytes = 4 * kc * p.Nb * p.Nk * p.Nw * p.Nh;
 }
 
+// Candidate order: the smaller model time; within 2 % of it, fewer
+// predicted HBM bytes (Eq. (3) at the XCD level), then fewer Eq. (1) bytes,
+// then the lower instantiation id.
+static bool better(const cnn_plan_t& a, const cnn_plan_t& b) {
+  const double lo = std::min(a.model_us, b.model_us);
+  if (std::fabs(a.model_us - b.model_us) > 0.02 * lo) return a.model_us < b.model_us;
+  if (a.hbm_bytes != b.hbm_bytes) return a.hbm_bytes < b.hbm_bytes;
+  if (a.eq1_bytes != b.eq1_bytes) return a.eq1_bytes < b.eq1_bytes;
+  if (a.variant != b.variant) return a.variant < b.variant;
+  return a.tp > b.tp;
+}
+
+// Every tiling the kernels implement that fits the budget, as complete plans
+// (model fields set); at most cap are written, the count is returned.
+int enumerate_plans(const cnn_problem& p, int dtype, const cnn_budget& bud, cnn_plan_t* out,
+                    int cap) {
+  int n = 0;
+  auto add = [&](cnn_plan_t& cand, int kernel) {
+    cand.kernel = kernel;
+    fill_common(p, dtype, bud, &cand);
+    if (n < cap) out[n] = cand;
+    ++n;
+  };
+  cnn_plan_t cand;
+  int n4 = 0, n3 = 0, n2 = 0, n1 = 0;
+  const Variant4* vs4 = variants4(&n4);
+  for (int i = 0; i < n4; ++i)
+    if (vs4[i].dtype == dtype && eval_variant4(p, dtype, vs4[i], bud, &cand))
+      add(cand, CNN_K_IGEMM_WIDE);
+  const Variant3* vs3 = variants3(&n3);
+  for (int i = 0; i < n3; ++i)
+    if (vs3[i].dtype == dtype && eval_variant3(p, dtype, vs3[i], bud, &cand))
+      add(cand, CNN_K_IGEMM_DMA);
+  const Variant2* vs2 = variants2(&n2);
+  for (int i = 0; i < n2; ++i)
+    if (vs2[i].dtype == dtype && eval_variant2(p, dtype, vs2[i], bud, &cand))
+      add(cand, v2_family(vs2[i]));
+  int nsc = 0;
+  const VariantS* vss = variants_smallc(&nsc);
+  for (int i = 0; i < nsc; ++i)
+    if (vss[i].dtype == dtype && eval_smallc(p, dtype, vss[i], bud, &cand))
+      add(cand, CNN_K_SMALLC);
+  int ngm = 0;
+  const VariantG* vgm = variants_gemm1(&ngm);
+  for (int i = 0; i < ngm; ++i)
+    if (vgm[i].dtype == dtype && eval_gemm1(p, dtype, vgm[i], bud, &cand))
+      add(cand, CNN_K_GEMM1);
+  int nsq = 0;
+  const VariantQ* vsq = variants_srows(&nsq);
+  for (int i = 0; i < nsq; ++i)
+    if (vsq[i].dtype == dtype && eval_srows(p, dtype, vsq[i], bud, &cand))
+      add(cand, CNN_K_SROWS);
+  // row streaming: every band length L dividing Nw, up to 4 groups' rows
+  int nrw = 0;
+  const VariantR* vrw = variants_rows(&nrw);
+  for (int i = 0; i < nrw; ++i) {
+    if (vrw[i].dtype != dtype) continue;
+    for (int64_t L = 1; L <= std::min<int64_t>(p.Nw, 4 * vrw[i].wr); ++L)
+      if (p.Nw % L == 0 && eval_rows(p, dtype, vrw[i], bud, L, &cand))
+        add(cand, CNN_K_ROWS);
+  }
+  const Variant* vs = variants(&n1);
+  for (int i = 0; i < n1; ++i)
+    if (vs[i].dtype == dtype && vs[i].kernel == CNN_K_IGEMM &&
+        eval_variant(p, dtype, vs[i], bud, &cand)) {
+      cnn_plan_t plain = cand;
+      add(plain, CNN_K_IGEMM);
+      // too few tiles for the chip and more than one stage: the split form
+      if (cand.grid < bud.cus && ceil_div(p.Nc, cand.tc) > 1) {
+        splitc_finish(p, bud, &cand);
+        add(cand, CNN_K_SPLITC);
+      }
+    }
+  if (n == 0) {
+    direct_plan(p, dtype, bud, &cand);
+    if (cap > 0) out[0] = cand;
+    n = 1;
+  }
+  return n;
+}
+
 int select_plan(const cnn_problem& p, int dtype, const cnn_budget& bud, int kernel,
                 int64_t tk, int64_t tp, int64_t tc, cnn_plan_t* out) {
   if (kernel == CNN_K_DIRECT) {
-    direct_plan(p, dtype, out);
+    direct_plan(p, dtype, bud, out);
+    return CNN_OK;
+  }
+  if (kernel == CNN_K_AUTO) {
+    // The model's choice among the candidates that need no workspace.
+    std::vector<cnn_plan_t> c(256);
+    int n = enumerate_plans(p, dtype, bud, c.data(), (int)c.size());
+    if (n > (int)c.size()) {
+      c.resize(n);
+      n = enumerate_plans(p, dtype, bud, c.data(), n);
+    }
+    const cnn_plan_t* best = nullptr;
+    for (int i = 0; i < n; ++i)
+      if (c[i].ws_bytes == 0 && (!best || better(c[i], *best))) best = &c[i];
+    if (!best) {
+      direct_plan(p, dtype, bud, out);
+      return CNN_OK;
+    }
+    *out = *best;
     return CNN_OK;
   }
   if (kernel == CNN_K_SPLITC) {
@@ -495,284 +654,159 @@ int select_plan(const cnn_problem& p, int dtype, const cnn_budget& bud, int kern
       const Variant& v = vs[i];
       if (v.dtype != dtype || v.kernel != CNN_K_IGEMM || v.tk != tk || v.tp != tp || v.tc != tc)
         continue;
-      double t;
-      if (!eval_variant(p, dtype, v, bud, out, &t)) continue;
+      if (!eval_variant(p, dtype, v, bud, out)) continue;
       splitc_finish(p, bud, out);
-      fill_common(p, dtype, out);
+      out->kernel = CNN_K_SPLITC;
+      fill_common(p, dtype, bud, out);
       return CNN_OK;
     }
     return CNN_E_UNSUPPORTED;
   }
-  if (kernel != CNN_K_AUTO && kernel != CNN_K_IGEMM && kernel != CNN_K_IGEMM_PIPE &&
-      kernel != CNN_K_IGEMM_DMA && kernel != CNN_K_IGEMM_WIDE && kernel != CNN_K_IGEMM_RAWK &&
-      kernel != CNN_K_POINTWISE && kernel != CNN_K_SMALLC && kernel != CNN_K_STREAM &&
-      kernel != CNN_K_ROWS && kernel != CNN_K_GEMM1 && kernel != CNN_K_SROWS)
-    return CNN_E_UNSUPPORTED;
+  // A requested family and tiling: the instantiations that implement it,
+  // the model's best of them.
   bool found = false;
-  double best_t = 0;
   cnn_plan_t best;
-  auto consider = [&](const cnn_plan_t& cand, double t) {
-    bool better = !found || t < best_t;
-    if (found && t == best_t) {
-      if (cand.tk != best.tk) better = cand.tk > best.tk;
-      else if (cand.tp != best.tp) better = cand.tp > best.tp;
-      else if (cand.tc != best.tc) better = cand.tc > best.tc;
-      else better = cand.variant < best.variant;
-    }
-    if (better) {
+  auto consider = [&](cnn_plan_t& cand, int family) {
+    cand.kernel = family;
+    fill_common(p, dtype, bud, &cand);
+    if (!found || better(cand, best)) {
       best = cand;
-      best_t = t;
       found = true;
     }
   };
-  // The row-streaming kernel is taken only when asked for (a requested
-  // tiling or the plan search): tp = L*Nh whole rows, tc always Nc.
-  if (kernel == CNN_K_ROWS) {
+  cnn_plan_t cand;
+  if (kernel == CNN_K_ROWS) {  // tp = L*Nh whole rows (0: the model's band), tc always Nc
     int nr = 0;
     const VariantR* vr = variants_rows(&nr);
     for (int i = 0; i < nr; ++i) {
       const VariantR& v = vr[i];
-      if (v.dtype != dtype || v.tk != tk || p.Nh < 1 || tp % p.Nh) continue;
-      cnn_plan_t cand;
-      double t;
-      if (eval_rows(p, dtype, v, bud, tp / p.Nh, &cand, &t)) {
-        cand.kernel = CNN_K_ROWS;
-        consider(cand, t);
+      if (v.dtype != dtype || v.tk != tk || tp % p.Nh) continue;
+      if (tp > 0) {
+        if (eval_rows(p, dtype, v, bud, tp / p.Nh, &cand)) consider(cand, CNN_K_ROWS);
+      } else {
+        for (int64_t L = 1; L <= p.Nw; ++L)
+          if (p.Nw % L == 0 && eval_rows(p, dtype, v, bud, L, &cand)) consider(cand, CNN_K_ROWS);
       }
     }
-  }
-  // The 1x1 GEMM kernel likewise: only when asked for (tp: its largest tile).
-  if (kernel == CNN_K_GEMM1) {
+  } else if (kernel == CNN_K_GEMM1) {  // tp: the instantiation's largest tile
     int ng = 0;
     const VariantG* vg = variants_gemm1(&ng);
     for (int i = 0; i < ng; ++i) {
       const VariantG& v = vg[i];
       if (v.dtype != dtype || v.tk != tk || v.tp != tp || v.tc != tc) continue;
-      cnn_plan_t cand;
-      double t;
-      if (eval_gemm1(p, dtype, v, bud, &cand, &t)) {
-        cand.kernel = CNN_K_GEMM1;
-        consider(cand, t);
-      }
+      if (eval_gemm1(p, dtype, v, bud, &cand)) consider(cand, CNN_K_GEMM1);
     }
-  }
-  // The stride-2 row-band kernel likewise (tp = L*Nh names the band; 0: any).
-  if (kernel == CNN_K_SROWS) {
+  } else if (kernel == CNN_K_SROWS) {  // tp = L*Nh names the band; 0: any
     int nq = 0;
     const VariantQ* vq = variants_srows(&nq);
     for (int i = 0; i < nq; ++i) {
       const VariantQ& v = vq[i];
       if (v.dtype != dtype || v.tk != tk || (tp != 0 && tp != v.L * p.Nh) || (tc != 0 && tc != 16))
         continue;
-      cnn_plan_t cand;
-      double t;
-      if (eval_srows(p, dtype, v, bud, &cand, &t)) {
-        cand.kernel = CNN_K_SROWS;
-        consider(cand, t);
-      }
+      if (eval_srows(p, dtype, v, bud, &cand)) consider(cand, CNN_K_SROWS);
     }
-  }
-  // Tier 0 (automatic choice only): a specialized family, when one fits --
-  // the 1x1 GEMM kernel for 1x1 layers (lowest id), else the row-streaming
-  // kernel for stride 1 (its automatic band, lowest id), else the stride-2
-  // row-band kernel (the largest band, then the lowest id).  On the layers
-  // they were built for they are the fastest the plan search finds; the
-  // Eq. (1) time model below prices MFMA at peak and cannot rank them.
-  if (kernel == CNN_K_AUTO) {
-    cnn_plan_t cand;
-    double t;
-    int ng = 0;
-    const VariantG* vg = variants_gemm1(&ng);
-    for (int i = 0; i < ng; ++i)
-      if (vg[i].dtype == dtype && eval_gemm1(p, dtype, vg[i], bud, &cand, &t)) {
-        cand.kernel = CNN_K_GEMM1;
-        fill_common(p, dtype, &cand);
-        *out = cand;
-        return CNN_OK;
-      }
-    int nr = 0;
-    const VariantR* vr = variants_rows(&nr);
-    for (int i = 0; i < nr; ++i)
-      if (vr[i].dtype == dtype && eval_rows(p, dtype, vr[i], bud, 0, &cand, &t)) {
-        cand.kernel = CNN_K_ROWS;
-        fill_common(p, dtype, &cand);
-        *out = cand;
-        return CNN_OK;
-      }
-    int nq = 0;
-    const VariantQ* vq = variants_srows(&nq);
-    const VariantQ* bq = nullptr;
-    for (int i = 0; i < nq; ++i)
-      if (vq[i].dtype == dtype && eval_srows(p, dtype, vq[i], bud, &cand, &t) &&
-          (!bq || vq[i].L > bq->L))
-        bq = &vq[i];
-    if (bq && eval_srows(p, dtype, *bq, bud, &cand, &t)) {
-      cand.kernel = CNN_K_SROWS;
-      fill_common(p, dtype, &cand);
-      *out = cand;
-      return CNN_OK;
+  } else if (kernel == CNN_K_IGEMM_WIDE) {
+    int n4 = 0;
+    const Variant4* vs4 = variants4(&n4);
+    for (int i = 0; i < n4; ++i) {
+      const Variant4& v = vs4[i];
+      if (v.dtype == dtype && v.tk == tk && v.tp == tp && v.tc == tc &&
+          eval_variant4(p, dtype, v, bud, &cand))
+        consider(cand, CNN_K_IGEMM_WIDE);
     }
-  }
-  // Tier 1: the DMA-staged kernel, tier 2: the register-staged pipelined
-  // kernel (both bf16), tier 3: the plain staging kernel.  The wide-staging
-  // kernel competes within tier 1.
-  int n4 = 0;
-  const Variant4* vs4 = variants4(&n4);
-  for (int i = 0; i < n4; ++i) {
-    const Variant4& v = vs4[i];
-    if (v.dtype != dtype || (kernel != CNN_K_AUTO && kernel != CNN_K_IGEMM_WIDE)) continue;
-    if (kernel == CNN_K_IGEMM_WIDE && (v.tk != tk || v.tp != tp || v.tc != tc)) continue;
-    cnn_plan_t cand;
-    double t;
-    if (eval_variant4(p, dtype, v, bud, &cand, &t)) {
-      cand.kernel = CNN_K_IGEMM_WIDE;
-      consider(cand, t);
+  } else if (kernel == CNN_K_IGEMM_DMA) {
+    int n3 = 0;
+    const Variant3* vs3 = variants3(&n3);
+    for (int i = 0; i < n3; ++i) {
+      const Variant3& v = vs3[i];
+      if (v.dtype == dtype && v.tk == tk && v.tp == tp && v.tc == tc &&
+          eval_variant3(p, dtype, v, bud, &cand))
+        consider(cand, CNN_K_IGEMM_DMA);
     }
-  }
-  int n3 = 0;
-  const Variant3* vs3 = variants3(&n3);
-  for (int i = 0; i < n3; ++i) {
-    const Variant3& v = vs3[i];
-    if (v.dtype != dtype || (kernel != CNN_K_AUTO && kernel != CNN_K_IGEMM_DMA)) continue;
-    if (kernel == CNN_K_IGEMM_DMA && (v.tk != tk || v.tp != tp || v.tc != tc)) continue;
-    cnn_plan_t cand;
-    double t;
-    if (eval_variant3(p, dtype, v, bud, &cand, &t)) {
-      cand.kernel = CNN_K_IGEMM_DMA;
-      consider(cand, t);
+  } else if (kernel == CNN_K_SMALLC) {  // tc: always Nc
+    int ns = 0;
+    const VariantS* vss = variants_smallc(&ns);
+    for (int i = 0; i < ns; ++i) {
+      const VariantS& v = vss[i];
+      if (v.dtype == dtype && v.tk == tk && v.tp == tp && eval_smallc(p, dtype, v, bud, &cand))
+        consider(cand, CNN_K_SMALLC);
     }
-  }
-  const bool tier1_found = found;
-  int nt = 0;
-  const VariantT* vst = variants_stream(&nt);
-  for (int i = 0; i < nt; ++i) {
-    const VariantT& v = vst[i];
-    if (tier1_found || v.dtype != dtype || (kernel != CNN_K_AUTO && kernel != CNN_K_STREAM))
-      continue;
-    if (kernel == CNN_K_STREAM && (v.tk != tk || v.tp != tp || v.tc != tc)) continue;
-    cnn_plan_t cand;
-    double t;
-    if (eval_stream(p, dtype, v, bud, &cand, &t)) {
-      cand.kernel = CNN_K_STREAM;
-      consider(cand, t);
+  } else if (kernel == CNN_K_IGEMM_PIPE || kernel == CNN_K_IGEMM_RAWK ||
+             kernel == CNN_K_POINTWISE) {  // tp: the instantiation's largest tile
+    int n2 = 0;
+    const Variant2* vs2 = variants2(&n2);
+    for (int i = 0; i < n2; ++i) {
+      const Variant2& v = vs2[i];
+      if (v.dtype == dtype && v2_family(v) == kernel && v.tk == tk && v.tp == tp &&
+          v.tc == tc && eval_variant2(p, dtype, v, bud, &cand))
+        consider(cand, kernel);
     }
-  }
-  int ns = 0;
-  const VariantS* vss = variants_smallc(&ns);
-  for (int i = 0; i < ns; ++i) {
-    const VariantS& v = vss[i];
-    if (tier1_found || v.dtype != dtype || (kernel != CNN_K_AUTO && kernel != CNN_K_SMALLC))
-      continue;
-    if (kernel == CNN_K_SMALLC && (v.tk != tk || v.tp != tp)) continue;  // tc: always Nc
-    cnn_plan_t cand;
-    double t;
-    if (eval_smallc(p, dtype, v, bud, &cand, &t)) {
-      cand.kernel = CNN_K_SMALLC;
-      consider(cand, t);
-    }
-  }
-  int n2 = 0;
-  const Variant2* vs2 = variants2(&n2);
-  for (int i = 0; i < n2; ++i) {
-    const Variant2& v = vs2[i];
-    const int family = v2_family(v);
-    if (tier1_found || v.dtype != dtype || (kernel != CNN_K_AUTO && kernel != family))
-      continue;
-    if (kernel == family && (v.tk != tk || v.tp != tp || v.tc != tc)) continue;  // tp: largest tile
-    cnn_plan_t cand;
-    double t;
-    if (eval_variant2(p, dtype, v, bud, &cand, &t)) {
-      cand.kernel = family;
-      consider(cand, t);
-    }
-  }
-  if (!found && (kernel == CNN_K_AUTO || kernel == CNN_K_IGEMM)) {
+  } else if (kernel == CNN_K_IGEMM) {
     int n = 0;
     const Variant* vs = variants(&n);
     for (int i = 0; i < n; ++i) {
       const Variant& v = vs[i];
-      if (v.dtype != dtype || v.kernel != CNN_K_IGEMM) continue;
-      if (kernel == CNN_K_IGEMM && (v.tk != tk || v.tp != tp || v.tc != tc)) continue;
-      cnn_plan_t cand;
-      double t;
-      if (eval_variant(p, dtype, v, bud, &cand, &t)) consider(cand, t);
+      if (v.dtype == dtype && v.kernel == CNN_K_IGEMM && v.tk == tk && v.tp == tp &&
+          v.tc == tc && eval_variant(p, dtype, v, bud, &cand))
+        consider(cand, CNN_K_IGEMM);
     }
+  } else {
+    return CNN_E_UNSUPPORTED;
   }
-  if (!found) {
-    if (kernel != CNN_K_AUTO) return CNN_E_UNSUPPORTED;
-    direct_plan(p, dtype, out);  // no slab fits LDS: the direct kernel takes it
-    return CNN_OK;
-  }
-  fill_common(p, dtype, &best);
+  if (!found) return CNN_E_UNSUPPORTED;
   *out = best;
   return CNN_OK;
 }
 
-int enumerate_plans(const cnn_problem& p, int dtype, const cnn_budget& bud, cnn_plan_t* out,
-                    int cap) {
+// The instantiation table of every family (cnn_variants).
+int list_variants(cnn_variant_t* out, int cap) {
   int n = 0;
-  auto add = [&](cnn_plan_t& cand, int kernel) {
-    if (n >= cap) return;
-    cand.kernel = kernel;
-    fill_common(p, dtype, &cand);
-    out[n++] = cand;
-  };
-  double t;
-  cnn_plan_t cand;
-  int n4 = 0, n3 = 0, n2 = 0, n1 = 0;
-  const Variant4* vs4 = variants4(&n4);
-  for (int i = 0; i < n4; ++i)
-    if (vs4[i].dtype == dtype && eval_variant4(p, dtype, vs4[i], bud, &cand, &t))
-      add(cand, CNN_K_IGEMM_WIDE);
-  const Variant3* vs3 = variants3(&n3);
-  for (int i = 0; i < n3; ++i)
-    if (vs3[i].dtype == dtype && eval_variant3(p, dtype, vs3[i], bud, &cand, &t))
-      add(cand, CNN_K_IGEMM_DMA);
-  const Variant2* vs2 = variants2(&n2);
-  for (int i = 0; i < n2; ++i)
-    if (vs2[i].dtype == dtype && eval_variant2(p, dtype, vs2[i], bud, &cand, &t))
-      add(cand, v2_family(vs2[i]));
-  int ntt = 0;
-  const VariantT* vst = variants_stream(&ntt);
-  for (int i = 0; i < ntt; ++i)
-    if (vst[i].dtype == dtype && eval_stream(p, dtype, vst[i], bud, &cand, &t))
-      add(cand, CNN_K_STREAM);
-  int nsc = 0;
-  const VariantS* vss = variants_smallc(&nsc);
-  for (int i = 0; i < nsc; ++i)
-    if (vss[i].dtype == dtype && eval_smallc(p, dtype, vss[i], bud, &cand, &t))
-      add(cand, CNN_K_SMALLC);
-  int ngm = 0;
-  const VariantG* vgm = variants_gemm1(&ngm);
-  for (int i = 0; i < ngm; ++i)
-    if (vgm[i].dtype == dtype && eval_gemm1(p, dtype, vgm[i], bud, &cand, &t))
-      add(cand, CNN_K_GEMM1);
-  int nsq = 0;
-  const VariantQ* vsq = variants_srows(&nsq);
-  for (int i = 0; i < nsq; ++i)
-    if (vsq[i].dtype == dtype && eval_srows(p, dtype, vsq[i], bud, &cand, &t))
-      add(cand, CNN_K_SROWS);
-  // row streaming: every band length L (dividing Nw) of 2 .. 4 groups' rows
-  int nrw = 0;
-  const VariantR* vrw = variants_rows(&nrw);
-  for (int i = 0; i < nrw; ++i) {
-    if (vrw[i].dtype != dtype) continue;
-    for (int64_t L = 2; L <= std::min<int64_t>(p.Nw, 4 * vrw[i].wr); ++L)
-      if (p.Nw % L == 0 && eval_rows(p, dtype, vrw[i], bud, L, &cand, &t))
-        add(cand, CNN_K_ROWS);
-  }
-  const Variant* vs = variants(&n1);
-  for (int i = 0; i < n1; ++i)
-    if (vs[i].dtype == dtype && vs[i].kernel == CNN_K_IGEMM &&
-        eval_variant(p, dtype, vs[i], bud, &cand, &t)) {
-      add(cand, CNN_K_IGEMM);
-      // too few tiles for the chip and more than one stage: the split form
-      if (cand.grid < bud.cus && ceil_div(p.Nc, cand.tc) > 1 && n < cap) {
-        splitc_finish(p, bud, &cand);
-        add(cand, CNN_K_SPLITC);
-      }
+  auto add = [&](int kernel, int id, int dtype, int nr, int ns, int mode, int64_t tk, int64_t tp,
+                 int64_t tc) {
+    if (n < cap) {
+      cnn_variant_t& o = out[n];
+      o.kernel = kernel;
+      o.variant = id;
+      o.dtype = dtype;
+      o.nr = nr;
+      o.ns = ns;
+      o.mode = mode;
+      o.tk = tk;
+      o.tp = tp;
+      o.tc = tc;
     }
-  if (n == 0 && cap > 0) direct_plan(p, dtype, &out[n++]);
+    ++n;
+  };
+  int c = 0;
+  const Variant* v1 = variants(&c);
+  for (int i = 0; i < c; ++i)
+    if (v1[i].kernel == CNN_K_IGEMM)
+      add(CNN_K_IGEMM, v1[i].id, v1[i].dtype, 0, 0, 0, v1[i].tk, v1[i].tp, v1[i].tc);
+  const Variant2* v2 = variants2(&c);
+  for (int i = 0; i < c; ++i)
+    add(v2_family(v2[i]), v2[i].id, v2[i].dtype, v2[i].nr, v2[i].ns, 0, v2[i].tk, v2[i].tp,
+        v2[i].tc);
+  const Variant3* v3 = variants3(&c);
+  for (int i = 0; i < c; ++i)
+    add(CNN_K_IGEMM_DMA, v3[i].id, v3[i].dtype, v3[i].nr, v3[i].ns, 0, v3[i].tk, v3[i].tp,
+        v3[i].tc);
+  const Variant4* v4 = variants4(&c);
+  for (int i = 0; i < c; ++i)
+    add(CNN_K_IGEMM_WIDE, v4[i].id, v4[i].dtype, v4[i].nr, v4[i].ns, 0, v4[i].tk, v4[i].tp,
+        v4[i].tc);
+  const VariantS* vsc = variants_smallc(&c);
+  for (int i = 0; i < c; ++i)
+    add(CNN_K_SMALLC, vsc[i].id, vsc[i].dtype, 0, 0, 0, vsc[i].tk, vsc[i].tp, 0);
+  const VariantR* vr = variants_rows(&c);
+  for (int i = 0; i < c; ++i)
+    add(CNN_K_ROWS, vr[i].id, vr[i].dtype, vr[i].nr, vr[i].ns, vr[i].mb, vr[i].tk, 0,
+        16 * vr[i].ncg);
+  const VariantG* vg = variants_gemm1(&c);
+  for (int i = 0; i < c; ++i)
+    add(CNN_K_GEMM1, vg[i].id, vg[i].dtype, 1, 1, vg[i].s2, vg[i].tk, vg[i].tp, vg[i].tc);
+  const VariantQ* vq = variants_srows(&c);
+  for (int i = 0; i < c; ++i)
+    add(CNN_K_SROWS, vq[i].id, vq[i].dtype, vq[i].nr, vq[i].ns, vq[i].L, vq[i].tk, 0, 16);
   return n;
 }
 

@@ -113,24 +113,6 @@ int64_t smallc_lds_bytes(const VariantS& v, const cnn_problem& p, int64_t slab_r
 hipError_t launch_smallc(const VariantS& v, const void* In, const void* Ker, void* Out,
                          const ConvArgs& a, int64_t lds_bytes, hipStream_t stream);
 
-// A persistent streaming instantiation (bf16, fixed stencil, raw Ker).
-struct VariantT {
-  int32_t id;
-  int32_t dtype;
-  int32_t tk, tp, tc;  // tp = largest tile
-  int32_t acc;
-  int32_t nr, ns;      // compile-time stencil
-  int32_t threads;     // workgroup size
-  int32_t kres;        // 1: the whole Ker stays in LDS (Nk <= tk)
-  int32_t mpos;        // transposed positions per thread: S*Ny <= threads*mpos
-  int32_t ndma;        // natural-copy blocks per thread: tc*S*ceil((Ny+14)/8) <= threads*ndma
-};
-const VariantT* variants_stream(int* count);
-int64_t stream_lds_bytes(const VariantT& v, const cnn_problem& p, int64_t slab_rows);
-bool stream_fits(const VariantT& v, const cnn_problem& p, int64_t slab_rows);
-hipError_t launch_stream(const VariantT& v, const void* In, const void* Ker, void* Out,
-                         const ConvArgs& a, int64_t lds_bytes, hipStream_t stream);
-
 // A row-streaming instantiation (bf16, stride 1, fixed stencil): tk = 64,
 // tiles of whole output rows, Ker resident.
 struct VariantR {
@@ -191,6 +173,21 @@ hipError_t launch_srows(const VariantQ& v, const void* In, const void* Ker, void
 // Ker repack for the pipelined kernels (defined with conv_igemm2).
 __global__ void pack_ker_bf16(const uint16_t* __restrict__ Ker, uint32_t __attribute__((ext_vector_type(4)))* __restrict__ P,
                               ConvArgs a, int TK, int TC, int blk_vecs, int64_t total_vecs);
+
+// Byte ranges a family addresses with 32-bit buffer offsets (below 2 GiB):
+// the images a tile of up to tp outputs touches (plus tc_extra channels of
+// one more image), Ker rows of the raw-Ker families, whole tensors (In and
+// Ker below in_limit), the few-channel and stride-2 row-band families.
+bool ranges_ok_tile(const cnn_problem& p, int dtype, int64_t tp, int64_t tc_extra);
+bool ranges_ok_rawk(const cnn_problem& p);
+bool ranges_ok_whole(const cnn_problem& p, int dtype, int64_t in_limit);
+bool ranges_ok_smallc(const VariantS& v, const cnn_problem& p, int dtype);
+bool ranges_ok_srows(const VariantQ& v, const cnn_problem& p, int dtype);
+
+// Lets `kernel` use up to 160 KiB of dynamic LDS on the current device.
+// The attribute is set once per (kernel, device); later calls return at
+// once.  Thread safe.
+hipError_t allow_max_lds(const void* kernel);
 
 // Launchers (asynchronous; return hipGetLastError()).
 hipError_t launch_direct(const void* In, const void* Ker, void* Out, const ConvArgs& a,

@@ -550,12 +550,9 @@ static hipError_t launch_g(const void* In, const void* Ker, void* Out, const Con
                            int64_t lds, hipStream_t stream) {
   typedef typename std::conditional<DT == CNN_BF16, float, bf16_t>::type TO;
   auto kern = Gemm1Kernel<TO, WP, WK, MBP, NBK, TC, S2>::fn;
-  static bool attr_set = false;
-  if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute((const void*)kern,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+  {
+    const hipError_t e = allow_max_lds((const void*)kern);
     if (e != hipSuccess) return e;
-    attr_set = true;
   }
   hipLaunchKernelGGL(kern, dim3((unsigned)a.grid), dim3(64 * WP * WK), (unsigned)lds, stream,
                      (const bf16_t*)In, (const bf16_t*)Ker, (TO*)Out, a);

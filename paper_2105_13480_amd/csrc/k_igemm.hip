@@ -267,12 +267,9 @@ static hipError_t launch_one(const void* In, const void* Ker, void* Out, const C
     if (split)
       return launch_one<CNN_BF16, WM, WN, MB, NB, TC>(In, Ker, Out, a, lds, stream, kc, cs, true);
   auto kern = conv_igemm<TI, TO, WM, WN, MB, NB, TC>;
-  static bool attr_set = false;  // benign race: every caller sets the same value
-  if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute((const void*)kern,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+  {
+    const hipError_t e = allow_max_lds((const void*)kern);
     if (e != hipSuccess) return e;
-    attr_set = true;
   }
   hipLaunchKernelGGL(kern, dim3((unsigned)a.grid, (unsigned)kc), dim3(256), (unsigned)lds, stream,
                      (const TI*)In, (const TI*)Ker, (TO*)Out, a, cs);

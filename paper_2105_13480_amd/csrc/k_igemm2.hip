@@ -635,12 +635,9 @@ static hipError_t launch_one2(const void* In, const void* Ker, void* Out, void* 
   auto kern = (!PW && (a.Ny & 1))
                   ? conv_igemm2<TO, WM, WN, MB, NB, TC, NR, NS, MAXP, (RAWK != 0), (PW != 0), true>
                   : conv_igemm2<TO, WM, WN, MB, NB, TC, NR, NS, MAXP, (RAWK != 0), (PW != 0), false>;
-  static bool attr_set[2] = {false, false};
-  if (!attr_set[a.Ny & 1]) {
-    hipError_t e = hipFuncSetAttribute((const void*)kern,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+  {
+    const hipError_t e = allow_max_lds((const void*)kern);
     if (e != hipSuccess) return e;
-    attr_set[a.Ny & 1] = true;
   }
   hipLaunchKernelGGL(kern, dim3((unsigned)a.grid), dim3(256), (unsigned)lds, stream,
                      (const bf16_t*)In, (const u32x4_t*)kp, (TO*)Out, a, (int)blk);

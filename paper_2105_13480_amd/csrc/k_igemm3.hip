@@ -354,12 +354,9 @@ static hipError_t launch_one3(const void* In, const void* Ker, void* Out, void* 
   hipLaunchKernelGGL(pack_ker_bf16, dim3((unsigned)pgrid), dim3(256), 0, stream,
                      (const bf16_t*)Ker, (u32x4_t*)ws, a, TK, TC, (int)blk, total);
   auto kern = conv_igemm3<TO, WM, WN, MB, NB, TC, NR, NS, NBUF, NDI, NDK, MPOS>;
-  static bool attr_set = false;
-  if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute((const void*)kern,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+  {
+    const hipError_t e = allow_max_lds((const void*)kern);
     if (e != hipSuccess) return e;
-    attr_set = true;
   }
   hipLaunchKernelGGL(kern, dim3((unsigned)a.grid), dim3(256), (unsigned)lds, stream,
                      (const bf16_t*)In, (const u32x4_t*)ws, (TO*)Out, a,

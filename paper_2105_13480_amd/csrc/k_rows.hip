@@ -607,15 +607,9 @@ static hipError_t launch_r(const void* In, const void* Ker, void* Out, const Con
   // 16-byte Out chunks need rows of a multiple of 4 outputs
   auto kern = (a.Nh & 3) == 0 ? conv_rows<TO, NR, NS, WAVES, RPW, MB, NCG, true>
                               : conv_rows<TO, NR, NS, WAVES, RPW, MB, NCG, false>;
-  static bool attr_set = false;
-  if (!attr_set) {
-    for (auto k : {conv_rows<TO, NR, NS, WAVES, RPW, MB, NCG, true>,
-                   conv_rows<TO, NR, NS, WAVES, RPW, MB, NCG, false>}) {
-      hipError_t e = hipFuncSetAttribute((const void*)k,
-                                         hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
-      if (e != hipSuccess) return e;
-    }
-    attr_set = true;
+  {
+    const hipError_t e = allow_max_lds((const void*)kern);
+    if (e != hipSuccess) return e;
   }
   const int L = a.tp / a.Nh;
   const int n_bands = a.Nw / L;

@@ -284,12 +284,9 @@ static hipError_t launch_s(const void* In, const void* Ker, void* Out, const Con
                            int64_t lds, hipStream_t stream) {
   typedef typename std::conditional<DT == CNN_BF16, float, bf16_t>::type TO;
   auto kern = a.sh == 2 ? conv_smallc<TO, NB, KS, true> : conv_smallc<TO, NB, KS, false>;
-  static bool attr_set[2] = {false, false};
-  if (!attr_set[a.sh == 2]) {
-    hipError_t e = hipFuncSetAttribute((const void*)kern,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+  {
+    const hipError_t e = allow_max_lds((const void*)kern);
     if (e != hipSuccess) return e;
-    attr_set[a.sh == 2] = true;
   }
   hipLaunchKernelGGL(kern, dim3((unsigned)a.grid), dim3(256), (unsigned)lds, stream,
                      (const bf16_t*)In, (const bf16_t*)Ker, (TO*)Out, a);

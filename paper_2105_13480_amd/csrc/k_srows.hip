@@ -477,12 +477,9 @@ static hipError_t launch_q(const void* In, const void* Ker, void* Out, void* ws,
   hipLaunchKernelGGL(pack_ker_srows<NR * NS>, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0,
                      stream, (const bf16_t*)Ker, (u32x4_t*)ws, a, blk);
   auto kern = conv_srows<TO, NR, NS, L, NWV>;
-  static bool attr_set = false;
-  if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute((const void*)kern,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+  {
+    const hipError_t e = allow_max_lds((const void*)kern);
     if (e != hipSuccess) return e;
-    attr_set = true;
   }
   hipLaunchKernelGGL(kern, dim3((unsigned)a.grid), dim3(64 * NWV), (unsigned)lds, stream,
                      (const bf16_t*)In, (const u32x4_t*)ws, (TO*)Out, a, blk);

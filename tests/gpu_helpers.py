@@ -41,7 +41,8 @@ def to_host64(t) -> np.ndarray:
 
 def run(In: np.ndarray, Ker: np.ndarray, sw: int, sh: int, mode: str, plan=None,
         stream=None, fill=float("nan")):
-    """Upload, run cnn_fwd (or cnn_fwd_plan), synchronise, return float64 Out."""
+    """Upload, run cnn_fwd (or cnn_fwd_plan, or cnn_fwd_plan_ws with a workspace of
+    the plan's size), synchronise, return float64 Out."""
     import torch
     Nb, Nc, Nx, Ny = In.shape
     Nk, _, Nr, Ns = Ker.shape
@@ -50,6 +51,11 @@ def run(In: np.ndarray, Ker: np.ndarray, sw: int, sh: int, mode: str, plan=None,
     dOut = out_tensor(Nb, Nk, Nw, Nh, mode, fill)
     if plan is None:
         cnn.fwd(dIn, dKer, dOut, sw, sh, stream=stream)
+    elif plan.ws_bytes > 0:  # the caller's workspace (cnn_fwd_plan_ws)
+        ws = torch.empty(plan.ws_bytes, dtype=torch.uint8, device="cuda")
+        cnn.fwd_plan_ws(dIn, dKer, dOut, plan, ws, sw, sh, stream=stream)
+        torch.cuda.synchronize()
+        del ws
     else:
         cnn.fwd_plan(dIn, dKer, dOut, plan, sw, sh, stream=stream)
     torch.cuda.synchronize()
@@ -77,32 +83,41 @@ def errors(got: np.ndarray, want: np.ndarray, absv: np.ndarray):
     return normwise, cond, point
 
 
-def variant_dims(kernel, vid, dt, tk, tp, tc, stencil):
+def variant_dims(kernel, vid, dt, tk, tp, tc, stencils):
     """Problem sizes on which instantiation `vid` is what cnn_plan_tiles
     picks for (kernel, tk, tp, tc): ragged channel, feature and output
-    tails, several tiles.  None if no candidate fits."""
+    tails, several tiles.  `stencils` lists the (Nr, Ns) to try.  None if
+    no candidate fits."""
+    for stencil in stencils:
+        dims = _variant_dims_one(kernel, vid, dt, tk, tp, tc, stencil)
+        if dims is not None:
+            return dims
+    return None
+
+
+def _fits(dims, dt, kernel, tk, tp, tc, vid):
+    try:
+        pl = cnn.plan_tiles(cnn.problem(*dims), dt, kernel, tk, tp, tc, cnn.budget())
+    except cnn.CnnError:
+        return False
+    return pl.variant == vid
+
+
+def _variant_dims_one(kernel, vid, dt, tk, tp, tc, stencil):
     Nr, Ns = stencil
     if kernel == cnn.K_ROWS:
         return rows_dims(vid, dt, stencil)
-    if kernel == cnn.K_SROWS:  # stride 2, Nc % 16 == 0, Nh % 4 == 0, L | Nw
-        from oracle import select as osel
-        L = next(r[4] for r in osel.SROWS if r[0] == vid)
-        dims = {7: (2, 32, 300, 7, 28, Nr, Ns, 2, 2), 4: (3, 16, 64, 8, 12, Nr, Ns, 2, 2)}[L]
-        try:
-            pl = cnn.plan_tiles(cnn.problem(*dims), dt, kernel, tk, 0, tc, cnn.budget())
-        except cnn.CnnError:
-            return None
-        return dims if pl.variant == vid else None
+    if kernel == cnn.K_SROWS:  # stride 2, Nc % 16 == 0, L | Nw
+        for dims in [(2, 32, 300, 7, 28, Nr, Ns, 2, 2), (3, 16, 64, 8, 12, Nr, Ns, 2, 2)]:
+            if _fits(dims, dt, kernel, tk, 0, tc, vid):
+                return dims
+        return None
     if kernel == cnn.K_GEMM1:  # 1x1, Nc % 8 == 0; stride 1 (Nw*Nh % 4 == 0) or 2 (Nh % 4 == 0)
         cands = [(3, tc + 8, tk + 7, 6, 10, 1, 1, 1, 1), (2, 2 * tc + 16, tk - 5, 8, 14, 1, 1, 1, 1),
                  (1, 24, tk + 7, 4, 5, 1, 1, 1, 1), (3, tc + 8, tk + 7, 6, 8, 1, 1, 2, 2),
                  (2, 2 * tc + 16, tk - 5, 7, 12, 1, 1, 2, 2)]
         for dims in cands:
-            try:
-                pl = cnn.plan_tiles(cnn.problem(*dims), dt, kernel, tk, tp, tc, cnn.budget())
-            except cnn.CnnError:
-                continue
-            if pl.variant == vid:
+            if _fits(dims, dt, kernel, tk, tp, tc, vid):
                 return dims
         return None
     if kernel == cnn.K_SMALLC:  # few channels: Nc*Nr rows must fit the K-steps
@@ -118,65 +133,43 @@ def variant_dims(kernel, vid, dt, tk, tp, tc, stencil):
              (2, tc + 3, max(1, tk - 5), 5, 9, Nr, Ns, 1, 1), (1, tc + 5, tk + 3, 6, 7, Nr, Ns, 1, 1),
              (2, tc + 5, tk + 7, 4, 5, Nr, Ns, 2, 1), (1, tc + 5, tk + 7, 3, 4, Nr, Ns, 1, 1)]
     for dims in cands:
-        try:
-            pl = cnn.plan_tiles(cnn.problem(*dims), dt, kernel, tk, tp, tc, cnn.budget())
-        except cnn.CnnError:
-            continue
-        if pl.variant == vid:
+        if _fits(dims, dt, kernel, tk, tp, tc, vid):
             return dims
     return None
+
+
+def variant_info(vid):
+    return next(v for v in cnn.variants() if v.variant == vid)
 
 
 def rows_dims(vid, dt, stencil):
     """A stride-1 problem the row-streaming instantiation `vid` is chosen
     for: two k tiles (ragged), a ragged channel tail, a band of several
-    row groups; the (tp = L*Nh) is returned as dims[-1] of the tuple."""
-    from oracle import select as osel
-    row = next(r for r in osel.ROWS if r[0] == vid)
-    _, _, nr, ns, mb, ncg, _, _ = row
-    nc = 16 * ncg - 8                      # Nc % 8 == 0, last group half empty
+    row groups."""
+    v = variant_info(vid)
+    nr, ns, mb, ncp = v.nr, v.ns, v.mode, int(v.tc)
+    nc = ncp - 8                           # Nc % 8 == 0, last group half empty
     nh = (29 if mb == 1 else 45) - (ns - 1) if ns > 1 else (30 if mb == 1 else 50)
     for dims in [(2, nc, 71, 10, nh, nr, ns, 1, 1), (3, nc, 64, 6, nh + 1, nr, ns, 1, 1)]:
         for L in (dims[3], 5, 2, 1):
             if dims[3] % L:
                 continue
-            try:
-                pl = cnn.plan_tiles(cnn.problem(*dims), dt, cnn.K_ROWS, 64, L * dims[4], 0,
-                                    cnn.budget())
-            except cnn.CnnError:
-                continue
-            if pl.variant == vid:
+            if _fits(dims, dt, cnn.K_ROWS, 64, L * dims[4], 0, vid):
                 return dims
     return None
 
 
 def variant_cases():
-    """(kernel, vid, dtype, tk, tp, tc, stencil) of every implicit-GEMM
-    instantiation, from the oracle's independent tables."""
-    from oracle import select as osel
+    """(kernel, vid, dtype, tk, tp, tc, stencils to try) of every
+    instantiation the library holds (cnn_variants)."""
     out = []
-    for vid, dt, wm, wn, mb, nb, tc in osel.IGEMM:
-        out.append((cnn.K_IGEMM, vid, dt, 32 * wm * mb, 32 * wn * nb, tc, (3, 3)))
-    for vid, dt, wm, wn, mb, nb, tc, nr, ns, _ in osel.IGEMM4:
-        out.append((cnn.K_IGEMM_WIDE, vid, dt, 32 * wm * mb, 32 * wn * nb, tc,
-                    (nr, ns) if nr else (5, 2)))
-    for vid, dt, wm, wn, mb, nb, tc, nr, ns, *_ in osel.IGEMM3:
-        tk = 32 * wm * mb
-        out.append((cnn.K_IGEMM_DMA, vid, dt, tk, 32 * wn * nb, tc,
-                    (nr, ns) if nr else ((1, 1) if vid % 100 in (10, 11, 12) else (5, 2))))
-    for vid, dt, wm, wn, mb, nb, tc, nr, ns, kres, _, _ in osel.STREAM:
-        out.append((cnn.K_STREAM, vid, dt, 32 * wm * mb, 32 * wn * nb, tc, (nr, ns)))
-    for vid, dt, wp, wk, mbp, nbk, tc, _ in osel.GEMM1:
-        out.append((cnn.K_GEMM1, vid, dt, 32 * wk * nbk, 32 * wp * mbp, tc, (1, 1)))
-    for vid, dt, nr, ns, L in osel.SROWS:
-        out.append((cnn.K_SROWS, vid, dt, 256, 0, 16, (nr, ns)))
-    for vid, dt, nr, ns, mb, ncg, _, _ in osel.ROWS:
-        out.append((cnn.K_ROWS, vid, dt, 64, 0, 0, (nr, ns)))
-    for vid, dt, nb, ks in osel.SMALLC:
-        out.append((cnn.K_SMALLC, vid, dt, 64, 128 * nb, 0, (7, 7) if ks <= 12 else (5, 5)))
-    for vid, dt, wm, wn, mb, nb, tc, nr, ns, _, rawk, pw in osel.IGEMM2:
-        tk = 32 * wm * mb
-        kern = cnn.K_POINTWISE if pw else (cnn.K_IGEMM_RAWK if rawk else cnn.K_IGEMM_PIPE)
-        out.append((kern, vid, dt, tk, 32 * wn * nb, tc,
-                    (nr, ns) if nr else ((1, 1) if tk >= 256 else (5, 2))))
+    for v in cnn.variants():
+        if v.nr:
+            stencils = [(v.nr, v.ns)]
+        elif v.kernel == cnn.K_SMALLC:
+            stencils = [(7, 7), (5, 5)]
+        else:
+            stencils = [(5, 2), (1, 1), (3, 3)]
+        tc = 0 if v.kernel == cnn.K_ROWS else int(v.tc)
+        out.append((v.kernel, v.variant, v.dtype, int(v.tk), int(v.tp), tc, stencils))
     return out

@@ -1,7 +1,9 @@
 """C ABI checks that need no GPU: the library loads, exports every symbol
-include/cnn.h declares, rejects bad arguments before any HIP call, and its
-host-side model (Eq. (1), composite-tile costs, tile selection) equals the
-oracle's."""
+include/cnn.h declares, rejects bad arguments before any HIP call, its
+host-side model (Eq. (1), composite-tile costs, the closed form) equals the
+oracle's, and the plans the selector makes are pinned by facts of the paper:
+their Eq. (1) terms count the loads of Listing 3's point loops, and no plan
+moves less than the Table 1 lower bound."""
 import ctypes
 import itertools
 import os
@@ -11,7 +13,6 @@ import numpy as np
 import pytest
 
 from oracle import eq1 as oeq1
-from oracle import select as osel
 from paper_2105_13480_amd import cnn, inputs
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
@@ -30,7 +31,7 @@ def test_library_exports_every_declared_symbol():
     L = cnn.lib()
     for name in _declared_functions():
         assert hasattr(L, name), name
-    assert L.cnn_abi_version() == 1
+    assert L.cnn_abi_version() == 2
 
 
 def test_strerror_covers_all_codes():
@@ -135,13 +136,147 @@ def test_slab_cost_matches_oracle():
             assert got == tuple(float(x) for x in oeq1.slab_terms(p, tk, tp))
 
 
+BUDGETS = [(256, 160 * 1024, 128, 2), (64, 64 * 1024, 64, 1), (8, 160 * 1024, 128, 2)]
+
+
+def _key(pl):
+    return (pl.kernel, pl.variant, pl.tk, pl.tp, pl.tc, pl.kc)
+
+
+def _better(a, b):
+    """The selector's documented order: less model time; within 2 % of each
+    other, fewer predicted HBM bytes, then fewer Eq. (1) bytes, then the
+    lower instantiation id, then the larger tile."""
+    lo = min(a.model_us, b.model_us)
+    if abs(a.model_us - b.model_us) > 0.02 * lo:
+        return a.model_us < b.model_us
+    for x, y in ((a.hbm_bytes, b.hbm_bytes), (a.eq1_bytes, b.eq1_bytes), (a.variant, b.variant)):
+        if x != y:
+            return x < y
+    return a.tp > b.tp
+
+
 @pytest.mark.parametrize("dtype", [0, 1, 2])
-def test_selector_matches_oracle(dtype):
+def test_plan_is_the_model_minimum(dtype):
+    """cnn_plan's choice is a candidate of cnn_plan_candidates that needs no
+    workspace, and no such candidate comes before it in the model's order
+    (so cnn_fwd never needs a workspace)."""
     for p in _problems():
-        for bud in [(256, 160 * 1024, 128, 2), (64, 64 * 1024, 64, 1), (8, 160 * 1024, 128, 2)]:
-            pl = cnn.plan(cnn.problem(*p.__dict__.values()), dtype, cnn.budget(*bud))
-            want = osel.choose(p, dtype, *bud)
-            assert (pl.kernel, pl.variant, pl.tk, pl.tp, pl.tc) == want, (p, bud)
+        prob = cnn.problem(*p.__dict__.values())
+        for bud in BUDGETS:
+            pl = cnn.plan(prob, dtype, cnn.budget(*bud))
+            cands = cnn.plan_candidates(prob, dtype, cnn.budget(*bud))
+            free = [c for c in cands if c.ws_bytes == 0]
+            assert pl.ws_bytes == 0
+            if not free:
+                assert pl.kernel == cnn.K_DIRECT
+                continue
+            assert _key(pl) in {_key(c) for c in free}, (p, bud)
+            assert pl.model_us <= 1.02 * min(c.model_us for c in free)
+            assert not any(_better(c, pl) for c in free if _key(c) != _key(pl)), (p, bud)
+
+
+def test_candidates_are_complete_plans():
+    for w in inputs.WORKLOADS:
+        prob = cnn.problem(*w.dims())
+        for dt in ((0,) if w.dtype == "f32" else (1, 2)):
+            cands = cnn.plan_candidates(prob, dt, cnn.budget())
+            assert cands
+            for c in cands:
+                assert c.kernel != cnn.K_AUTO and c.grid >= 1 and c.model_us > 0
+                assert c.flops == w.flops and c.mfma_flops >= c.flops
+                assert c.hbm_bytes >= 0.99 * c.compulsory_bytes
+                if c.kernel != cnn.K_DIRECT:
+                    assert c.hbm_bytes == pytest.approx(sum(cnn.hbm_bytes(c, 8, 4 << 20)))
+
+
+def _composite_loads(p, tk, tp):
+    """Loads of Listing 3 run over a composite tiling, counted literally:
+    for every tile of tk features by tp consecutive outputs of the flattened
+    (b, w, h) index, with all Nc channels (W_c = N_c), the set of In
+    elements its point loops read, its Ker tile and its Out tile.  Returns
+    (Out stores, Ker loads, In loads) in elements."""
+    hw, npix = p.Nw * p.Nh, p.Nb * p.Nw * p.Nh
+    out = ker = inn = 0
+    for k0 in range(0, p.Nk, tk):
+        kk = min(tk, p.Nk - k0)
+        for f in range(0, npix, tp):
+            outs = range(f, min(f + tp, npix))
+            pos = set()
+            for q in outs:
+                b, w, h = q // hw, (q % hw) // p.Nh, q % p.Nh
+                for r in range(p.Nr):
+                    for s_ in range(p.Ns):
+                        pos.add((b, p.sw * w + r, p.sh * h + s_))
+            inn += len(pos) * p.Nc
+            ker += kk * p.Nc * p.Nr * p.Ns
+            out += kk * len(outs)
+    return out, ker, inn
+
+
+SMALL = [(2, 24, 70, 6, 8, 3, 3, 1, 1), (1, 16, 40, 8, 12, 3, 3, 2, 2),
+         (3, 16, 33, 4, 6, 1, 1, 1, 1), (2, 8, 20, 5, 7, 5, 3, 2, 1),
+         (2, 3, 64, 6, 6, 7, 7, 2, 2), (1, 48, 300, 4, 4, 1, 1, 2, 2)]
+
+
+@pytest.mark.parametrize("dims", SMALL)
+@pytest.mark.parametrize("dtype", [0, 1])
+def test_candidate_eq1_terms_count_listing3_loads(dims, dtype):
+    """Sec. 2, Eq. (1) on the plans themselves: for every candidate tiling,
+    Out and Ker terms equal the literal counts of Listing 3's stores and
+    loads at the plan's (tk, tp); the In term (whole staged input rows)
+    covers every input element the tile's point loops read, and equals that
+    count when the tiles are whole rows of one image (or whole images) and
+    the stride does not skip input rows or columns."""
+    P = oeq1.Problem(*dims)
+    prob = cnn.problem(*dims)
+    hw = P.Nw * P.Nh
+    n = 0
+    for c in cnn.plan_candidates(prob, dtype, cnn.budget()):
+        if c.kernel == cnn.K_DIRECT:
+            continue
+        o, k, i = _composite_loads(P, c.tk, c.tp)
+        assert (c.eq1_elems[0], c.eq1_elems[1]) == (o, k), (c.as_dict(), o, k)
+        assert c.eq1_elems[2] >= i
+        whole = (c.tp % P.Nh == 0 and hw % c.tp == 0) or c.tp % hw == 0
+        if whole and P.sw <= P.Nr and P.sh <= P.Ns:
+            assert c.eq1_elems[2] == i, c.as_dict()
+        n += 1
+    assert n > 0
+
+
+def _table1_bound_cases():
+    out = [(w.dims(), 0 if w.dtype == "f32" else 1) for w in inputs.WORKLOADS
+           if w.sw <= w.Nr and w.sh <= w.Ns]
+    rng = np.random.default_rng(12)
+    while len(out) < len(inputs.WORKLOADS) + 20:
+        Nr, Ns = (int(x) for x in rng.integers(1, 6, size=2))
+        sw, sh = int(rng.integers(1, Nr + 1)), int(rng.integers(1, Ns + 1))
+        dims = (int(rng.integers(1, 9)), int(rng.integers(1, 200)), int(rng.integers(1, 400)),
+                int(rng.integers(1, 40)), int(rng.integers(1, 40)), Nr, Ns, sw, sh)
+        out.append((dims, int(rng.integers(0, 3))))
+    return out
+
+
+@pytest.mark.parametrize("dims,dtype", _table1_bound_cases())
+def test_candidate_eq1_at_least_the_table1_bound(dims, dtype):
+    """Sec. 2.1: with M_L = M the Table 1 costs are lower bounds.  Every
+    candidate plan, seen as P = min(grid, CUs) processors whose fast memory
+    M (elements) is its LDS footprint plus its Out tile, moves at least P
+    times the Table 1 cost in Eq. (1) elements.  (Checked where the stride
+    does not exceed the stencil: the relaxation's In tile of sw*sh*T_bhw
+    elements assumes every input row and column between reads is read.)"""
+    P_ = oeq1.Problem(*dims)
+    prob = cnn.problem(*dims)
+    bud = cnn.budget()
+    e_in = 4 if dtype == 0 else 2
+    for c in cnn.plan_candidates(prob, dtype, bud):
+        if c.kernel == cnn.K_DIRECT:
+            continue
+        P = min(c.grid, bud.cus)
+        M = c.lds_bytes / e_in + c.tk * c.tp
+        bound = P * oeq1.table1_cost(P_, P, M)
+        assert sum(c.eq1_elems) >= bound * (1 - 1e-12), (c.as_dict(), bound)
 
 
 def test_plan_reports_eq1_and_compulsory_bytes():
@@ -162,9 +297,11 @@ def test_every_instantiation_has_a_fitting_test_shape():
     import sys
     sys.path.insert(0, os.path.join(ROOT, "tests"))
     from gpu_helpers import variant_cases, variant_dims
-    for case in variant_cases():
-        kernel, vid, dt, tk, tp, tc, stencil = case
-        assert variant_dims(kernel, vid, dt, tk, tp, tc, stencil) is not None, vid
+    cases = variant_cases()
+    assert len({c[1] for c in cases}) == len(cases)
+    for case in cases:
+        kernel, vid, dt, tk, tp, tc, stencils = case
+        assert variant_dims(kernel, vid, dt, tk, tp, tc, stencils) is not None, vid
 
 
 def test_plan_find_and_lookup_validate_before_hip():
@@ -232,9 +369,42 @@ def test_splitc_bad_slice_count_rejected_before_hip():
     for kc, ws in [(0, 0), (3, 4 * 3 * nout), (2, 4 * 2 * nout - 4), (-1, 4 * nout)]:
         q = cnn.Plan.from_buffer_copy(pl)
         q.kc, q.ws_bytes = kc, ws
-        st = L.cnn_fwd_plan(0x1000, 0x100000, 0x200000, ctypes.byref(p), cnn.CNN_F32,
-                            ctypes.byref(q), None)
+        st = L.cnn_fwd_plan_ws(0x1000, 0x100000, 0x200000, ctypes.byref(p), cnn.CNN_F32,
+                               ctypes.byref(q), 0x4000000, 1 << 30, None)
         assert st == -8, (kc, ws)
+
+
+def test_workspace_plans_need_the_workspace_form():
+    """cnn_fwd_plan never allocates: a plan that needs a workspace is
+    refused before any HIP call; cnn_fwd_plan_ws checks the workspace."""
+    dims = (1, 16, 16, 16, 16, 3, 3, 1, 1)
+    p = cnn.problem(*dims)
+    pl = cnn.plan_tiles(p, cnn.CNN_F32, cnn.K_SPLITC, 64, 64, 8, cnn.budget())
+    assert pl.ws_bytes > 0
+    L = cnn.lib()
+    args = (0x1000, 0x100000, 0x200000, ctypes.byref(p), cnn.CNN_F32, ctypes.byref(pl))
+    assert L.cnn_fwd_plan(*args, None) == -6
+    assert b"cnn_fwd_plan_ws" in L.cnn_last_error()
+    assert L.cnn_fwd_plan_ws(*args, None, 0, None) == -1
+    assert L.cnn_fwd_plan_ws(*args, 0x4000000, pl.ws_bytes - 16, None) == -2
+    assert L.cnn_fwd_plan_ws(*args, 0x4000008, pl.ws_bytes, None) == -2
+
+
+def test_edited_plan_beyond_32bit_ranges_rejected():
+    """A plan edited onto a problem whose In exceeds the 2 GiB its kernel
+    addresses with 32-bit offsets is refused (CNN_E_PLAN) before any
+    launch, not run with clamped loads and dropped stores."""
+    small = (32, 64, 64, 56, 56, 3, 3, 1, 1)
+    big = (8192, 64, 64, 56, 56, 3, 3, 1, 1)  # In: 8192*64*58*58*2 bytes > 2 GiB
+    pl = cnn.plan_tiles(cnn.problem(*small), cnn.CNN_BF16, cnn.K_ROWS, 64, 7 * 56, 0, cnn.budget())
+    q = cnn.Plan.from_buffer_copy(pl)
+    q.prob = cnn.problem(*big)
+    q.grid = pl.grid // 32 * 8192
+    st = cnn.lib().cnn_fwd_plan(1 << 40, 1 << 42, 1 << 44, ctypes.byref(q.prob), cnn.CNN_BF16,
+                                ctypes.byref(q), None)
+    assert st == -8
+    with pytest.raises(cnn.CnnError):
+        cnn.plan_tiles(cnn.problem(*big), cnn.CNN_BF16, cnn.K_ROWS, 64, 7 * 56, 0, cnn.budget())
 
 
 def test_closed_form_matches_oracle():

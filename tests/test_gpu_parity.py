@@ -10,7 +10,6 @@ import numpy as np
 import pytest
 
 import oracle
-from oracle import select as osel
 from paper_2105_13480_amd import cnn, inputs
 
 from gpu_helpers import (TOL, errors, out_tensor, run, say, to_gpu, to_host64, variant_cases,
@@ -55,9 +54,9 @@ def test_mid_size_auto_plan(dims, mode):
 
 @pytest.mark.parametrize("case", variant_cases(), ids=lambda c: f"v{c[1]}")
 def test_every_igemm_variant_exact_integers(case):
-    kernel, vid, dt, tk, tp, tc, stencil = case
+    kernel, vid, dt, tk, tp, tc, stencils = case
     mode = {0: "f32", 1: "bf16", 2: "bf16_obf16"}[dt]
-    dims = variant_dims(kernel, vid, dt, tk, tp, tc, stencil)
+    dims = variant_dims(kernel, vid, dt, tk, tp, tc, stencils)
     assert dims is not None, f"no test shape fits instantiation {vid}"
     In, Ker = _arrays(dims, mode, seed=vid, dist=("int", -2, 2), kdist=("int", -2, 2))
     pl = cnn.plan_tiles(cnn.problem(*dims), dt, kernel, tk, tp, tc)
@@ -218,37 +217,6 @@ def test_pointwise_gather_exact(shape, tk, mode):
         assert np.array_equal(got, oracle.widen(inputs.f32_to_bf16_bits(want.astype(np.float32))))
 
 
-@pytest.mark.parametrize("mode", ["bf16", "bf16_obf16"])
-@pytest.mark.parametrize("shape,tk,tp", [
-    ((4, 24, 60, 12, 14, 3, 3, 1, 1), 64, 256),    # resident Ker (Nk <= tk), even rows
-    ((3, 32, 50, 11, 9, 3, 3, 1, 1), 64, 256),     # resident Ker, odd rows (funnel / element)
-    ((4, 24, 150, 12, 14, 3, 3, 1, 1), 128, 128),  # streamed Ker, ragged k tiles
-    ((2, 40, 130, 9, 10, 3, 3, 2, 2), 128, 128),   # stride 2
-])
-@pytest.mark.parametrize("cus", [3, 7])
-def test_stream_multi_tile_exact(shape, tk, tp, cus, mode):
-    """The persistent kernel with few workgroup slots, so every workgroup
-    walks several tiles (next-tile prefetch, stores draining under the next
-    tile): bit-exact with the oracle on integer inputs."""
-    Nb, Nc, Nk, Nw, Nh, Nr, Ns, sw, sh = shape
-    pl = cnn.plan_tiles(cnn.problem(*shape), MODES[mode], cnn.K_STREAM, tk, tp, 16,
-                        cnn.budget(cus, 160 * 1024, 128, 2))
-    tiles = -(-(Nb * Nw * Nh) // pl.tp) * -(-Nk // pl.tk)
-    assert pl.grid < tiles  # several tiles per workgroup
-    rng = np.random.default_rng(sum(shape) + cus)
-    Nx, Ny = sw * (Nw - 1) + Nr, sh * (Nh - 1) + Ns
-    In = inputs.f32_to_bf16_bits(rng.integers(-2, 3, size=(Nb, Nc, Nx, Ny)).astype(np.float32))
-    Ker = inputs.f32_to_bf16_bits(rng.integers(-2, 3, size=(Nk, Nc, Nr, Ns)).astype(np.float32))
-    want = oracle.conv(In, Ker, sw, sh)
-    say(f"[parity] stream multi-tile shape={shape} v{pl.variant} tp={pl.tp} grid={pl.grid} "
-        f"tiles={tiles} mode={mode}")
-    got = run(In, Ker, sw, sh, mode, plan=pl)
-    if mode == "bf16":
-        assert np.array_equal(got, want)
-    else:
-        assert np.array_equal(got, oracle.widen(inputs.f32_to_bf16_bits(want.astype(np.float32))))
-
-
 # ---- row-streaming kernel: bands, row groups, store paths -----------------
 ROWS_SHAPES = [
     (2, 56, 71, 10, 56, 3, 3, 1, 1),   # Ny = 58 (two 32-position blocks), 16-byte stores
@@ -285,23 +253,18 @@ def test_rows_bands_exact(shape, mode):
 
 
 def test_rows_float_headline_shape():
-    """The 56x56 3x3 layer on uniform inputs through the row kernel: sampled
-    outputs within the bf16 tolerance of the fp64 oracle."""
+    """The 56x56 3x3 layer on uniform inputs through the row kernel at every
+    band length the plan search tries: every output within the bf16
+    tolerance of the fp64 oracle."""
     w = inputs.BY_NAME["conv3x3_b32"]
     In, Ker = inputs.make_inputs(w)
-    pl = cnn.plan_tiles(cnn.problem(*w.dims()), cnn.CNN_BF16, cnn.K_ROWS, 64, 0, 0)
-    say(f"[parity] rows headline v{pl.variant} tp={pl.tp} grid={pl.grid}")
-    got = run(In, Ker, 1, 1, "bf16", plan=pl)
-    rng = np.random.default_rng(5)
-    idx = np.stack([rng.integers(0, m, size=4000) for m in (w.Nb, w.Nk, w.Nw, w.Nh)], axis=1)
-    # every band's first and last output row, first and last column
-    edge = [(b, k, y, h) for b in (0, w.Nb - 1) for k in (0, 31, 32, 63)
-            for y in range(w.Nw) for h in (0, w.Nh - 1)]
-    idx = np.unique(np.concatenate([idx, np.array(edge)]), axis=0)
-    want, absv = oracle.conv_points(In, Ker, idx, 1, 1, with_abs=True)
-    g = got[idx[:, 0], idx[:, 1], idx[:, 2], idx[:, 3]]
-    nw, cond, _ = errors(g, want, absv)
-    assert nw <= TOL["bf16"] and cond <= TOL["bf16"], (nw, cond)
+    want, absv = oracle.conv(In, Ker, 1, 1, with_abs=True)
+    for L in (4, 7, 8):
+        pl = cnn.plan_tiles(cnn.problem(*w.dims()), cnn.CNN_BF16, cnn.K_ROWS, 64, L * w.Nh, 0)
+        say(f"[parity] rows headline v{pl.variant} tp={pl.tp} grid={pl.grid}")
+        got = run(In, Ker, 1, 1, "bf16", plan=pl)
+        nw, cond, _ = errors(got, want, absv)
+        assert nw <= TOL["bf16"] and cond <= TOL["bf16"], (L, nw, cond)
 
 
 # ---- 1x1 stride-1 GEMM kernel: stages, k tiles, tiles across images --------
@@ -329,10 +292,10 @@ def test_gemm1_exact(shape, mode):
     if mode == "bf16_obf16":
         want = oracle.widen(inputs.f32_to_bf16_bits(want.astype(np.float32)))
     dt = MODES[mode]
-    for vid, vdt, wp, wk, mbp, nbk, tc, s2 in osel.GEMM1:
-        if vdt != dt or s2:
+    for v in cnn.variants():
+        if v.kernel != cnn.K_GEMM1 or v.dtype != dt or v.mode != 0:
             continue
-        tk, tpmax = 32 * wk * nbk, 32 * wp * mbp
+        vid, tk, tpmax, tc = v.variant, v.tk, v.tp, v.tc
         for cus in (256, 3):  # balanced tile; few slots -> the largest tile
             pl = cnn.plan_tiles(cnn.problem(*shape), dt, cnn.K_GEMM1, tk, tpmax, tc,
                                 cnn.budget(cus, 160 * 1024, 128, 2))
@@ -359,10 +322,10 @@ def test_gemm1_ring_exact(shape, mode):
         want = oracle.widen(inputs.f32_to_bf16_bits(want.astype(np.float32)))
     dt = MODES[mode]
     ran = 0
-    for vid, vdt, wp, wk, mbp, nbk, tc, s2 in osel.GEMM1:
-        if vdt != dt or s2 != 2:
+    for v in cnn.variants():
+        if v.kernel != cnn.K_GEMM1 or v.dtype != dt or v.mode != 2:
             continue
-        tk, tpmax = 32 * wk * nbk, 32 * wp * mbp
+        vid, tk, tpmax, tc = v.variant, v.tk, v.tp, v.tc
         pl = cnn.plan_tiles(cnn.problem(*shape), dt, cnn.K_GEMM1, tk, tpmax, tc)
         assert pl.variant == vid and pl.tp == Nw * Nh and pl.grid == Nb * -(-Nk // tk)
         say(f"[parity] gemm1 ring shape={shape} v{vid} grid={pl.grid} mode={mode}")
@@ -400,8 +363,9 @@ def test_srows_exact(shape, mode):
         want = oracle.widen(inputs.f32_to_bf16_bits(want.astype(np.float32)))
     dt = MODES[mode]
     ran = 0
-    for vid, vdt, nr, ns, L in osel.SROWS:
-        if vdt != dt or (nr, ns) != (Nr, Ns) or Nw % L:
+    for v in cnn.variants():
+        vid, L = v.variant, v.mode
+        if v.kernel != cnn.K_SROWS or v.dtype != dt or (v.nr, v.ns) != (Nr, Ns) or Nw % L:
             continue
         pl = cnn.plan_tiles(cnn.problem(*shape), dt, cnn.K_SROWS, 256, L * Nh, 16)
         assert pl.variant == vid and pl.grid == Nb * (Nw // L) * -(-Nk // 256)
@@ -414,23 +378,23 @@ def test_srows_exact(shape, mode):
 
 def test_srows_float_strided_shape():
     """The strided 3x3 layer (64 images, 128 -> 256 channels, 28x28 outputs)
-    on uniform inputs through the row-band kernel: sampled outputs within
-    the bf16 tolerance of the fp64 oracle."""
+    on uniform inputs through every row-band instantiation that fits it:
+    every output within the bf16 tolerance of the fp64 oracle."""
     w = inputs.BY_NAME["conv3x3_s2_b64"]
     In, Ker = inputs.make_inputs(w)
-    pl = cnn.plan_tiles(cnn.problem(*w.dims()), cnn.CNN_BF16, cnn.K_SROWS, 256, 7 * w.Nh, 16)
-    say(f"[parity] srows strided v{pl.variant} tp={pl.tp} grid={pl.grid}")
-    got = run(In, Ker, 2, 2, "bf16", plan=pl)
-    rng = np.random.default_rng(6)
-    idx = np.stack([rng.integers(0, m, size=4000) for m in (w.Nb, w.Nk, w.Nw, w.Nh)], axis=1)
-    # every band's rows at both ends of a row, the feature blocks' edges
-    edge = [(b, k, y, h) for b in (0, w.Nb - 1) for k in (0, 31, 32, 63, 64, 255)
-            for y in range(w.Nw) for h in (0, 3, 4, w.Nh - 1)]
-    idx = np.unique(np.concatenate([idx, np.array(edge)]), axis=0)
-    want, absv = oracle.conv_points(In, Ker, idx, 2, 2, with_abs=True)
-    g = got[idx[:, 0], idx[:, 1], idx[:, 2], idx[:, 3]]
-    nw, cond, _ = errors(g, want, absv)
-    assert nw <= TOL["bf16"] and cond <= TOL["bf16"], (nw, cond)
+    want, absv = oracle.conv(In, Ker, 2, 2, with_abs=True)
+    ran = 0
+    for v in cnn.variants():
+        if v.kernel != cnn.K_SROWS or v.dtype != cnn.CNN_BF16 or w.Nw % v.mode:
+            continue
+        pl = cnn.plan_tiles(cnn.problem(*w.dims()), cnn.CNN_BF16, cnn.K_SROWS, 256,
+                            v.mode * w.Nh, 16)
+        say(f"[parity] srows strided v{pl.variant} tp={pl.tp} grid={pl.grid}")
+        got = run(In, Ker, 2, 2, "bf16", plan=pl)
+        nw, cond, _ = errors(got, want, absv)
+        assert nw <= TOL["bf16"] and cond <= TOL["bf16"], (v.variant, nw, cond)
+        ran += 1
+    assert ran > 0
 
 
 # ---- 1x1 GEMM kernel, strides 2 and 2: the even input rows and columns -----
@@ -460,10 +424,10 @@ def test_gemm1_stride2_exact(shape, mode):
         want = oracle.widen(inputs.f32_to_bf16_bits(want.astype(np.float32)))
     dt = MODES[mode]
     ran = 0
-    for vid, vdt, wp, wk, mbp, nbk, tc, s2 in osel.GEMM1:
-        if vdt != dt or s2 != 1:
+    for v in cnn.variants():
+        if v.kernel != cnn.K_GEMM1 or v.dtype != dt or v.mode != 1:
             continue
-        tk, tpmax = 32 * wk * nbk, 32 * wp * mbp
+        vid, tk, tpmax, tc = v.variant, v.tk, v.tp, v.tc
         for cus in (256, 3):
             pl = cnn.plan_tiles(cnn.problem(*shape), dt, cnn.K_GEMM1, tk, tpmax, tc,
                                 cnn.budget(cus, 160 * 1024, 128, 2))

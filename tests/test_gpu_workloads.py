@@ -1,13 +1,16 @@
 """GPU parity at the full benchmark sizes, in both launch configurations:
 cnn_fwd with the automatic plan, and the plan cnn_plan_find measures to be
-fastest (the one the benchmark times).
+fastest (the one the benchmark times, through cnn_fwd_plan_ws when it needs
+a workspace).
 
-The tiny workload is compared element by element.  For the large ones the
-oracle computes a sample of outputs one by one -- random points plus the
-first and last output of every tile boundary it can reach cheaply -- and a
-checksum identity, which holds at any size, covers every output:
+Every output of every workload is compared with the fp64 oracle's (computed
+once per workload on the host's cores), against the normwise and the
+componentwise-conditioned bars.  A checksum identity, which holds at any
+size, is checked as well:
     sum_{b,k,w,h} Out = sum_{c,r,s} (sum_k Ker[k,c,r,s]) * (sum_{b,w,h} In[b,c,sw*w+r,sh*h+s]).
 """
+import functools
+
 import numpy as np
 import pytest
 
@@ -19,20 +22,15 @@ from gpu_helpers import TOL, errors, out_tensor, run, say, to_gpu
 pytestmark = pytest.mark.gpu
 
 
-def _sample_points(w, plan, n=3000, seed=0):
-    rng = np.random.default_rng(seed)
-    pts = [np.stack([rng.integers(0, m, size=n) for m in (w.Nb, w.Nk, w.Nw, w.Nh)], axis=1)]
-    # outputs on both sides of composite-tile boundaries and feature-tile edges
-    hw, npix = w.Nw * w.Nh, w.Nb * w.Nw * w.Nh
-    edges = []
-    tp, tk = max(int(plan.tp), 1), max(int(plan.tk), 1)
-    for f in list(range(0, npix, tp))[:: max(1, npix // tp // 64)] + [npix - 1]:
-        for q in (f - 1, f, min(f + tp - 1, npix - 1)):
-            if 0 <= q < npix:
-                for k in {0, min(tk - 1, w.Nk - 1), min(tk, w.Nk - 1), w.Nk - 1}:
-                    edges.append((q // hw, k, (q % hw) // w.Nh, q % w.Nh))
-    pts.append(np.array(edges, dtype=np.int64).reshape(-1, 4))
-    return np.unique(np.concatenate(pts), axis=0)
+@functools.lru_cache(maxsize=1)
+def _oracle_full(name):
+    """(In, Ker, Out, sum|In*Ker|) of a workload; the fp64 oracle over every
+    output (one workload held at a time)."""
+    w = inputs.BY_NAME[name]
+    In, Ker = inputs.make_inputs(w)
+    say(f"[workload] oracle {name}: {w.flops / 1e9:.2f} GFLOP on {oracle.threads()} threads")
+    want, absv = oracle.conv(In, Ker, w.sw, w.sh, with_abs=True)
+    return In, Ker, want, absv
 
 
 def _checksum(In64, Ker64, w):
@@ -47,15 +45,15 @@ def _checksum(In64, Ker64, w):
     return tot, tot_abs
 
 
-@pytest.mark.parametrize("plan_src", ["auto", "find"])
 @pytest.mark.parametrize("mode_out", ["fp32_out", "bf16_out"])
+@pytest.mark.parametrize("plan_src", ["auto", "find"])
 @pytest.mark.parametrize("name", [w.name for w in inputs.WORKLOADS])
-def test_workload(name, mode_out, plan_src):
+def test_workload(name, plan_src, mode_out):
     w = inputs.BY_NAME[name]
     if w.dtype == "f32" and mode_out == "bf16_out":
         pytest.skip("fp32 workload has fp32 output only")
     mode = "f32" if w.dtype == "f32" else ("bf16" if mode_out == "fp32_out" else "bf16_obf16")
-    In, Ker = inputs.make_inputs(w)
+    In, Ker, want, absv = _oracle_full(name)
     if plan_src == "auto":
         plan = cnn.plan(cnn.problem(*w.dims()), cnn.DTYPES[mode])
     else:
@@ -64,20 +62,41 @@ def test_workload(name, mode_out, plan_src):
         plan, _ = cnn.plan_find(dIn, dKer, dOut, w.sw, w.sh)
         del dIn, dKer, dOut
     say(f"[workload] {name} mode={mode} {plan_src} plan={plan.as_dict()['kernel']} "
-        f"v{plan.variant} tk={plan.tk} tp={plan.tp} tc={plan.tc} grid={plan.grid}")
+        f"v{plan.variant} tk={plan.tk} tp={plan.tp} tc={plan.tc} kc={plan.kc} grid={plan.grid}")
     got = run(In, Ker, w.sw, w.sh, mode, plan=None if plan_src == "auto" else plan)
     assert got.shape == (w.Nb, w.Nk, w.Nw, w.Nh)
     assert np.isfinite(got).all()
     tol = TOL[mode]
-    if w.Nb * w.Nk * w.Nw * w.Nh <= 1 << 16:
-        want, absv = oracle.conv(In, Ker, w.sw, w.sh, with_abs=True)
-        nw, cond, _ = errors(got, want, absv)
-    else:
-        idx = _sample_points(w, plan)
-        want, absv = oracle.conv_points(In, Ker, idx, w.sw, w.sh, with_abs=True)
-        g = got[idx[:, 0], idx[:, 1], idx[:, 2], idx[:, 3]]
-        nw, cond, _ = errors(g, want, absv)
-    say(f"[workload] {name} {mode}: normwise {nw:.3e} conditioned {cond:.3e}")
+    nw, cond, pt = errors(got, want, absv)
+    say(f"[workload] {name} {mode} {plan_src}: every output: normwise {nw:.3e} "
+        f"conditioned {cond:.3e} (pointwise {pt:.3e}, not gated)")
     assert nw <= tol and cond <= tol
     tot, tot_abs = _checksum(oracle.widen(In), oracle.widen(Ker), w)
     assert abs(got.sum() - tot) <= tol * tot_abs
+
+
+def test_fwd_allocates_no_device_memory():
+    """cnn_fwd's first call on each workload computes and caches a plan and
+    launches it; it allocates no device memory (the plan never needs a
+    workspace).  The kernels' code is loaded first, by running the same plan
+    through cnn_fwd_plan, so that loading it is not counted."""
+    import torch
+    bufs = []
+    for w in inputs.WORKLOADS:
+        mode = "f32" if w.dtype == "f32" else "bf16"
+        In, Ker = inputs.make_inputs(w)
+        dIn, dKer = to_gpu(In), to_gpu(Ker)
+        dOut = out_tensor(w.Nb, w.Nk, w.Nw, w.Nh, mode, 0.0)
+        plan = cnn.plan(cnn.problem(*w.dims()), cnn.DTYPES[mode])
+        assert plan.ws_bytes == 0
+        say(f"[workload] load the code of {w.name} plan {plan.as_dict()['kernel']} v{plan.variant}")
+        cnn.fwd_plan(dIn, dKer, dOut, plan, w.sw, w.sh)
+        bufs.append((w, dIn, dKer, dOut))
+    torch.cuda.synchronize()
+    free0, _ = torch.cuda.mem_get_info()
+    for w, dIn, dKer, dOut in bufs:
+        say(f"[workload] first cnn_fwd call on {w.name}")
+        cnn.fwd(dIn, dKer, dOut, w.sw, w.sh)
+    torch.cuda.synchronize()
+    free1, _ = torch.cuda.mem_get_info()
+    assert free1 == free0, (free0, free1)
