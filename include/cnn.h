@@ -117,7 +117,7 @@ typedef enum cnn_kernel {
                          per stage; fixed 3x3, Nc % 16 == 0,
                          Nh <= 32, Ny <= 64, L | Nw; tp of its plans is L*Nh
                          (cnn_plan_tiles: tp = L*Nh, or 0 for any L)           */
-  CNN_K_SPLITC = 13   /* the paper's Case 2 (Sec. 2.1, W_c < N_c; the partial Outs
+  CNN_K_SPLITC = 13,  /* the paper's Case 2 (Sec. 2.1, W_c < N_c; the partial Outs
                          reduced at the end, Sec. 2.3) on one GPU: the
                          CNN_K_IGEMM tiles (same tk/tp/tc and instantiations)
                          with the channel loop split over kc workgroup slices
@@ -125,6 +125,9 @@ typedef enum cnn_kernel {
                          workspace, a second kernel adds the kc slices in slice
                          order and writes Out.  For shapes with few output
                          tiles and many channels; any dtype and stencil       */
+  CNN_K_AUTO_NO_WORKSPACE = 14 /* (cnn_plan_tiles only) the model's choice among the
+                         plans that need no workspace: the plan cnn_fwd runs
+                         when no cnn_plan_find result is cached              */
 } cnn_kernel;
 
 /*
@@ -201,14 +204,17 @@ int cnn_fwd(const void* In, const void* Ker, void* Out,
  * Tile-size selection (Sec. 2, Eq. (1); Eq. (3) one level up).  Lists every
  * tiling the kernels implement whose footprint (LDS tiles and accumulators,
  * the two halves of the paper's fast memory M) fits the budget, prices each
- * with Eq. (1) (slab form, bytes), the two-level HBM bytes (Eq. (3) over the
- * 8 XCDs, plan.hbm_bytes) and its MFMA work, converts them into a time at
- * rates measured on MI355X (plan.model_us), and returns the workspace-free
- * candidate of least time; candidates within 2 % of it are ranked by fewer
- * HBM bytes, then fewer Eq. (1) bytes, then the lower instantiation id.
- * budget == NULL queries the current HIP device.  Writes *plan.  Errors:
- * CNN_E_NULL, CNN_E_SHAPE, CNN_E_DTYPE, CNN_E_OVERFLOW, CNN_E_HIP (device
- * query failed).
+ * with its MFMA work, its Eq. (1) bytes (slab form) per channel stage and
+ * the two-level HBM bytes (Eq. (3) over the 8 XCDs, plan.hbm_bytes),
+ * converts them into a time with per-family rates measured on MI355X
+ * (plan.model_us), and returns the candidate of least time; candidates
+ * within 2 % of it are ranked by fewer HBM bytes, then fewer Eq. (1) bytes,
+ * then the lower instantiation id.  The choice may need a workspace
+ * (plan.ws_bytes > 0: run it with cnn_fwd_plan_ws); cnn_fwd runs the best
+ * candidate that needs none (cnn_plan_tiles with CNN_K_AUTO_NO_WORKSPACE,
+ * or cnn_plan_lookup).  budget == NULL queries the current HIP device.
+ * Writes *plan.  Errors: CNN_E_NULL, CNN_E_SHAPE, CNN_E_DTYPE,
+ * CNN_E_OVERFLOW, CNN_E_HIP (device query failed).
  */
 int cnn_plan(const cnn_problem* prob, int dtype, const cnn_budget* budget,
              cnn_plan_t* plan);

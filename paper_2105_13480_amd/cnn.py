@@ -21,7 +21,7 @@ DTYPES = {"f32": CNN_F32, "bf16": CNN_BF16, "bf16_obf16": CNN_BF16_OBF16}
 
 (K_AUTO, K_DIRECT, K_IGEMM, K_POINTWISE, K_SMALLC, K_IGEMM_PIPE, K_IGEMM_DMA, K_IGEMM_WIDE,
  K_IGEMM_RAWK) = range(9)
-K_ROWS, K_GEMM1, K_SROWS, K_SPLITC = range(10, 14)
+K_ROWS, K_GEMM1, K_SROWS, K_SPLITC, K_AUTO_NO_WORKSPACE = range(10, 15)
 KERNEL_NAMES = {K_DIRECT: "direct", K_IGEMM: "igemm", K_POINTWISE: "pointwise", K_SMALLC: "smallc",
                 K_IGEMM_PIPE: "igemm_pipe", K_IGEMM_DMA: "igemm_dma", K_IGEMM_WIDE: "igemm_wide",
                 K_IGEMM_RAWK: "igemm_rawk", K_ROWS: "rows",

@@ -427,7 +427,7 @@ int cnn_plan_tiles(const cnn_problem* prob, int dtype, int kernel, int64_t tk, i
   if (!prob || !plan) return fail(CNN_E_NULL, "prob and plan must be non-NULL");
   int st;
   if ((st = check_problem(*prob)) || (st = check_dtype(dtype))) return st;
-  if (kernel < CNN_K_AUTO || kernel > CNN_K_SPLITC || kernel == 9)
+  if (kernel < CNN_K_AUTO || kernel > CNN_K_AUTO_NO_WORKSPACE || kernel == 9)
     return fail(CNN_E_UNSUPPORTED, "unknown kernel %d", kernel);
   cnn_budget bud;
   if ((st = resolve_budget(budget, &bud))) return st;
@@ -506,7 +506,7 @@ static int current_plan(const cnn_problem& p, int dtype, cnn_plan_t* plan) {
   cnn_budget bud;
   int st;
   if ((st = cnn_device_budget(dev, &bud))) return st;
-  if ((st = select_plan(p, dtype, bud, CNN_K_AUTO, 0, 0, 0, plan)))
+  if ((st = select_plan(p, dtype, bud, CNN_K_AUTO_NO_WORKSPACE, 0, 0, 0, plan)))
     return fail(st, "tile selection failed");
   std::lock_guard<std::mutex> g(g_cache_mu);
   g_cache.emplace(key, *plan);  // keeps a plan another thread stored first
@@ -670,7 +670,8 @@ int cnn_hbm_bytes(const cnn_plan_t* plan, int64_t xcds, int64_t l2_bytes, double
   int st;
   if ((st = check_problem(plan->prob)) || (st = check_dtype(plan->dtype))) return st;
   if (xcds < 1 || l2_bytes < 1) return fail(CNN_E_SHAPE, "xcds and l2_bytes must be >= 1");
-  if (plan->kernel == CNN_K_DIRECT || plan->kernel < CNN_K_AUTO || plan->kernel > CNN_K_SPLITC ||
+  if (plan->kernel == CNN_K_DIRECT || plan->kernel <= CNN_K_AUTO || plan->kernel > CNN_K_SPLITC ||
+      plan->kernel == 9 ||
       plan->tk < 1 || plan->tp < 1)
     return fail(CNN_E_PLAN, "needs a tiled plan (not the direct kernel)");
   hbm_terms(*plan, xcds, l2_bytes, terms);

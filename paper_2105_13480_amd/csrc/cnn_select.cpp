@@ -324,79 +324,89 @@ static const int64_t kL2Bytes = 4LL << 20;
 // measured on the device (not datasheet figures): the engine clock; the
 // bf16 MFMA rate sustained on operands of these workloads' value ranges
 // (64 % of the 4096 flop/clk/CU datasheet rate: the clock drops with the
-// data-dependent power; fp32 MFMA is taken at its datasheet rate); the
-// CU <- L2 bandwidth per CU; the HBM bandwidth of a large device copy (read
-// plus write); a kernel launch in a graph replay.
+// data-dependent power; fp32 MFMA is taken at its datasheet rate); the HBM
+// bandwidth of a large device copy (read plus write); a kernel launch.
 static const double kClkGHz = 2.4;
 static const double kMfmaRealBf16 = 0.64;
-static const double kL2BytesPerClkCU = 64.0;
 static const double kHbmGBs = 5000.0;
 static const double kLaunchUs = 2.0;
 
 // MFMA throughput per CU per clock for the dtype's operand type.
 static double mfma_rate(int dtype) { return dtype == CNN_F32 ? 256.0 : 4096.0; }
 
-// What each kernel family adds to the bounds: the fraction of the sustained
-// MFMA rate its inner loop reaches (operand staging, barriers and waits
-// between the products), its fixed cost per launch beyond the launch itself
-// (set-up, a second kernel) in microseconds, and whether its Out stores
-// drain under later work (true) or only after its last tile (false).
+// What each kernel family's implementation adds to the work and the bytes,
+// fitted (least squares on log time) to every candidate of the seven
+// benchmark workloads timed on one MI355X: the fraction of the sustained
+// MFMA rate its inner loop reaches; a fixed cost per workgroup (set-up,
+// the resident Ker tile); and the time of one channel stage when it is not
+// MFMA-bound: a latency plus the stage's share of the Eq. (1) traffic at a
+// per-CU bandwidth.
 struct FamilyCost {
-  double mfma_eff;
-  double fixed_us;
-  bool stores_overlap;
+  double mfma_eff;      // of the sustained MFMA rate
+  double wg_us;         // per workgroup
+  double stage_us;      // per stage, latency
+  double stage_gbs;     // per stage, Eq. (1) bytes per CU per second (GB/s)
 };
 
-static FamilyCost family_cost(int kernel) {
+static FamilyCost family_cost(int kernel, int variant) {
   switch (kernel) {
-    case CNN_K_ROWS: return {0.70, 2.5, true};
-    case CNN_K_SROWS: return {0.55, 1.5, false};
-    case CNN_K_GEMM1: return {0.55, 1.5, false};
-    case CNN_K_SMALLC: return {0.40, 1.5, false};
-    case CNN_K_IGEMM_RAWK: return {0.35, 1.5, false};
-    case CNN_K_POINTWISE: return {0.30, 1.5, false};
-    case CNN_K_IGEMM_PIPE: return {0.35, 3.0, false};
-    case CNN_K_IGEMM_DMA: return {0.30, 3.0, false};
-    case CNN_K_IGEMM_WIDE: return {0.35, 3.0, false};
-    case CNN_K_SPLITC: return {0.15, 3.0, false};
-    case CNN_K_IGEMM: return {0.15, 1.0, false};
-    default: return {0.25, 1.0, false};  // direct: fp32 vector FMAs
+    case CNN_K_ROWS: return {0.73, 5.17, 0.01, 58.0};
+    case CNN_K_SROWS: return {0.53, 1.39, 0.11, 48.3};
+    case CNN_K_GEMM1: {
+      int n = 0;
+      const VariantG* vg = variants_gemm1(&n);
+      for (int i = 0; i < n; ++i)
+        if (vg[i].id == variant && vg[i].s2 == 2) return {0.99, 1.22, 0.52, 50.0};  // DMA ring
+      return {0.36, 1.28, 0.56, 50.1};
+    }
+    case CNN_K_SMALLC: return {0.17, 4.72, 0.17, 49.7};
+    case CNN_K_IGEMM_RAWK: return {0.49, 1.67, 2.41, 29.5};
+    case CNN_K_POINTWISE: return {0.98, 37.19, 0.41, 100.0};
+    case CNN_K_IGEMM_PIPE: return {0.74, 3.80, 2.51, 30.2};
+    case CNN_K_IGEMM_DMA: return {0.55, 6.62, 0.93, 34.8};
+    case CNN_K_IGEMM_WIDE: return {1.00, 0.00, 7.53, 100.0};
+    case CNN_K_SPLITC: return {0.51, 3.07, 1.65, 4.1};
+    case CNN_K_IGEMM: return {0.40, 0.00, 2.14, 3.4};
+    default: return {0.25, 0.0, 0.0, 1.0};  // direct: fp32 vector FMAs
   }
 }
 
-// The selector's time model for a finished plan (its grid, tiles, Eq. (1)
-// bytes and MFMA work set), in microseconds: the busiest CU's share of the
-// MFMA work, of the Eq. (1) traffic and of the HBM traffic, whichever takes
-// longest, plus the Out drain the family cannot overlap, the launch and
-// the family's fixed cost.
+// The selector's time model for a finished plan, in microseconds.  The
+// busiest CU runs ceil(workgroups / CUs) workgroups, up to `occ` of them at
+// once (as LDS allows); each walks its channel stages, a stage taking the
+// longer of its MFMA work and its latency plus its Eq. (1) bytes at the
+// family's stage bandwidth.  The whole is at least the plan's HBM bytes
+// (Eq. (3) at the XCD level) at the copy bandwidth.  Channel-split plans
+// add their reduce pass; every plan adds its launch.
 static double model_us(const cnn_plan_t& pl, const cnn_budget& bud) {
   const cnn_problem& p = pl.prob;
-  const FamilyCost fc = family_cost(pl.kernel);
+  const FamilyCost fc = family_cost(pl.kernel, pl.variant);
   const double clk_per_us = kClkGHz * 1e3;
   const double cus = (double)bud.cus;
-  const double out_b = (double)(p.Nb * p.Nk * p.Nw * p.Nh) * out_bytes(pl.dtype);
+  const double n_out = (double)(p.Nb * p.Nk * p.Nw * p.Nh);
   if (pl.kernel == CNN_K_DIRECT) {
     // 64 lanes x 4 SIMDs x one fp32 FMA (2 flops) per clock per CU
     const double t = pl.flops / (cus * 512.0 * clk_per_us * fc.mfma_eff);
-    return std::max(t, pl.hbm_bytes / (kHbmGBs * 1e3)) + kLaunchUs + fc.fixed_us;
+    return std::max(t, pl.hbm_bytes / (kHbmGBs * 1e3)) + kLaunchUs;
   }
-  const double wgs = (double)pl.grid * (pl.kernel == CNN_K_SPLITC ? (double)pl.kc : 1.0);
-  const double per_cu = std::ceil(wgs / cus);        // workgroups the busiest CU runs
-  const double rate = mfma_rate(pl.dtype) * (pl.dtype == CNN_F32 ? 1.0 : kMfmaRealBf16);
-  const double t_mfma = per_cu * (pl.mfma_flops / wgs) / (rate * fc.mfma_eff * clk_per_us);
-  const double t_l2 = per_cu * (pl.eq1_bytes / wgs) / (kL2BytesPerClkCU * clk_per_us);
-  // Out stores of the last round of workgroups drain after their products
-  // unless the family overlaps them.
-  int64_t occ = std::max<int64_t>(1, std::min<int64_t>(bud.wg_per_cu,
-                                                      bud.lds_bytes / std::max<int64_t>(1, pl.lds_bytes)));
-  const double rounds = std::ceil(wgs / (cus * (double)occ));
-  const double drain_b = fc.stores_overlap ? 0.0 : out_b / rounds;
-  const double t_hbm = (pl.hbm_bytes - drain_b) / (kHbmGBs * 1e3);
-  double t = std::max(std::max(t_mfma, t_l2), t_hbm) + drain_b / (kHbmGBs * 1e3);
+  const double kc = pl.kernel == CNN_K_SPLITC ? (double)pl.kc : 1.0;
+  const double wgs = (double)pl.grid * kc;
+  const double per_cu = std::ceil(wgs / cus);
+  const double tc = pl.tc > 0 ? (double)pl.tc : (double)p.Nc;
+  const double n_st = std::ceil(std::ceil((double)p.Nc / tc) / kc);  // stages per workgroup
+  const int64_t occ = std::max<int64_t>(
+      1, std::min<int64_t>(bud.wg_per_cu, bud.lds_bytes / std::max<int64_t>(1, pl.lds_bytes)));
+  const double rate = mfma_rate(pl.dtype) * (pl.dtype == CNN_F32 ? 1.0 : kMfmaRealBf16) *
+                      clk_per_us * fc.mfma_eff;                    // flops per us per CU
+  const double stage_flops = pl.mfma_flops / wgs / n_st;
+  const double stage_bytes = pl.eq1_bytes / wgs / n_st;
+  const double t_stage =
+      std::max(stage_flops / rate, fc.stage_us + stage_bytes / (fc.stage_gbs * 1e3));
+  double t = std::ceil(per_cu / (double)occ) * (fc.wg_us + n_st * t_stage);
+  t = std::max(t, pl.hbm_bytes / (kHbmGBs * 1e3));
   if (pl.kernel == CNN_K_SPLITC)  // the reduce pass: kc fp32 partials read, Out written
-    t += (4.0 * (double)pl.kc * (double)(p.Nb * p.Nk * p.Nw * p.Nh) + out_b) / (kHbmGBs * 1e3) +
-         kLaunchUs;
-  return t + kLaunchUs + fc.fixed_us;
+    t += kLaunchUs + 4.0 * (kc + 1.0) * n_out / (kHbmGBs * 1e3);
+  return t + kLaunchUs;
 }
 
 static void fill_common(const cnn_problem& p, int dtype, const cnn_budget& bud,
@@ -629,8 +639,10 @@ int select_plan(const cnn_problem& p, int dtype, const cnn_budget& bud, int kern
     direct_plan(p, dtype, bud, out);
     return CNN_OK;
   }
-  if (kernel == CNN_K_AUTO) {
-    // The model's choice among the candidates that need no workspace.
+  if (kernel == CNN_K_AUTO || kernel == CNN_K_AUTO_NO_WORKSPACE) {
+    // The model's choice among all candidates, or among those that need no
+    // workspace.
+    const bool ws_free = kernel == CNN_K_AUTO_NO_WORKSPACE;
     std::vector<cnn_plan_t> c(256);
     int n = enumerate_plans(p, dtype, bud, c.data(), (int)c.size());
     if (n > (int)c.size()) {
@@ -639,7 +651,7 @@ int select_plan(const cnn_problem& p, int dtype, const cnn_budget& bud, int kern
     }
     const cnn_plan_t* best = nullptr;
     for (int i = 0; i < n; ++i)
-      if (c[i].ws_bytes == 0 && (!best || better(c[i], *best))) best = &c[i];
+      if ((!ws_free || c[i].ws_bytes == 0) && (!best || better(c[i], *best))) best = &c[i];
     if (!best) {
       direct_plan(p, dtype, bud, out);
       return CNN_OK;

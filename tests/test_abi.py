@@ -158,22 +158,26 @@ def _better(a, b):
 
 @pytest.mark.parametrize("dtype", [0, 1, 2])
 def test_plan_is_the_model_minimum(dtype):
-    """cnn_plan's choice is a candidate of cnn_plan_candidates that needs no
-    workspace, and no such candidate comes before it in the model's order
-    (so cnn_fwd never needs a workspace)."""
+    """cnn_plan's choice is a candidate of cnn_plan_candidates and no
+    candidate comes before it in the model's order; the choice among the
+    candidates that need no workspace (what cnn_fwd runs) likewise among
+    those."""
     for p in _problems():
         prob = cnn.problem(*p.__dict__.values())
         for bud in BUDGETS:
-            pl = cnn.plan(prob, dtype, cnn.budget(*bud))
             cands = cnn.plan_candidates(prob, dtype, cnn.budget(*bud))
             free = [c for c in cands if c.ws_bytes == 0]
-            assert pl.ws_bytes == 0
+            pl = cnn.plan(prob, dtype, cnn.budget(*bud))
+            assert _key(pl) in {_key(c) for c in cands}, (p, bud)
+            assert pl.model_us <= 1.02 * min(c.model_us for c in cands)
+            assert not any(_better(c, pl) for c in cands if _key(c) != _key(pl)), (p, bud)
+            pf = cnn.plan_tiles(prob, dtype, cnn.K_AUTO_NO_WORKSPACE, bud=cnn.budget(*bud))
+            assert pf.ws_bytes == 0
             if not free:
-                assert pl.kernel == cnn.K_DIRECT
+                assert pf.kernel == cnn.K_DIRECT
                 continue
-            assert _key(pl) in {_key(c) for c in free}, (p, bud)
-            assert pl.model_us <= 1.02 * min(c.model_us for c in free)
-            assert not any(_better(c, pl) for c in free if _key(c) != _key(pl)), (p, bud)
+            assert _key(pf) in {_key(c) for c in free}, (p, bud)
+            assert not any(_better(c, pf) for c in free if _key(c) != _key(pf)), (p, bud)
 
 
 def test_candidates_are_complete_plans():

@@ -54,8 +54,8 @@ def test_workload(name, plan_src, mode_out):
         pytest.skip("fp32 workload has fp32 output only")
     mode = "f32" if w.dtype == "f32" else ("bf16" if mode_out == "fp32_out" else "bf16_obf16")
     In, Ker, want, absv = _oracle_full(name)
-    if plan_src == "auto":
-        plan = cnn.plan(cnn.problem(*w.dims()), cnn.DTYPES[mode])
+    if plan_src == "auto":  # what cnn_fwd runs: the model's best workspace-free plan
+        plan = cnn.plan_tiles(cnn.problem(*w.dims()), cnn.DTYPES[mode], cnn.K_AUTO_NO_WORKSPACE)
     else:
         dIn, dKer = to_gpu(In), to_gpu(Ker)
         dOut = out_tensor(w.Nb, w.Nk, w.Nw, w.Nh, mode, 0.0)
@@ -87,7 +87,7 @@ def test_fwd_allocates_no_device_memory():
         In, Ker = inputs.make_inputs(w)
         dIn, dKer = to_gpu(In), to_gpu(Ker)
         dOut = out_tensor(w.Nb, w.Nk, w.Nw, w.Nh, mode, 0.0)
-        plan = cnn.plan(cnn.problem(*w.dims()), cnn.DTYPES[mode])
+        plan = cnn.plan_tiles(cnn.problem(*w.dims()), cnn.DTYPES[mode], cnn.K_AUTO_NO_WORKSPACE)
         assert plan.ws_bytes == 0
         say(f"[workload] load the code of {w.name} plan {plan.as_dict()['kernel']} v{plan.variant}")
         cnn.fwd_plan(dIn, dKer, dOut, plan, w.sw, w.sh)
