@@ -316,6 +316,24 @@ int cnn_fwd_plan_ws(const void* In, const void* Ker, void* Out,
                     void* workspace, int64_t ws_bytes, void* stream);
 
 /*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, serving loops that forbid allocation): cnn_fwd_plan_ws with the
+ * library's own device scratch of CNN_STATIC_SCRATCH_BYTES (8 MiB) in place
+ * of a caller workspace.  Allocates nothing: the scratch is a static device
+ * array that each GPU the library runs on holds until the process ends.
+ * All calls on one GPU share it, so calls whose kernels may overlap on that
+ * GPU (on different streams, or from several host threads) race and must
+ * be ordered by the caller; consecutive calls on one stream are safe.  A
+ * plan needing more than the scratch holds returns CNN_E_UNSUPPORTED
+ * before any HIP call (use cnn_fwd_plan_ws).  Other errors as cnn_fwd_plan.
+ */
+#define CNN_STATIC_SCRATCH_BYTES (8LL << 20)
+
+int cnn_fwd_plan_static(const void* In, const void* Ker, void* Out,
+                        const cnn_problem* prob, int dtype, const cnn_plan_t* plan,
+                        void* stream);
+
+/*
  * Eq. (1) of the paper for a box tiling, in elements: terms[0] = Out
  * written once, terms[1] = Ker re-read per (b, w, h) tile, terms[2] = In
  * (with halo) re-read per k tile.  halo_mode 0 = the formula as printed

@@ -33,7 +33,8 @@ STATUS = {0: "CNN_OK", -1: "CNN_E_NULL", -2: "CNN_E_SHAPE", -3: "CNN_E_DTYPE",
 
 # Every symbol include/cnn.h declares.
 EXPORTS = ["cnn_fwd", "cnn_plan", "cnn_plan_candidates", "cnn_variants", "cnn_plan_find",
-           "cnn_plan_lookup", "cnn_plan_tiles", "cnn_fwd_plan", "cnn_fwd_plan_ws", "cnn_eq1_cost",
+           "cnn_plan_lookup", "cnn_plan_tiles", "cnn_fwd_plan", "cnn_fwd_plan_ws",
+           "cnn_fwd_plan_static", "cnn_eq1_cost",
            "cnn_slab_cost", "cnn_closed_form", "cnn_hbm_bytes", "cnn_device_budget",
            "cnn_strerror", "cnn_last_error", "cnn_abi_version"]
 
@@ -116,6 +117,7 @@ def lib():
     L.cnn_plan_tiles.argtypes = [P, ctypes.c_int, ctypes.c_int, i64, i64, i64, B, PL]
     L.cnn_fwd_plan.argtypes = [vp, vp, vp, P, ctypes.c_int, PL, vp]
     L.cnn_fwd_plan_ws.argtypes = [vp, vp, vp, P, ctypes.c_int, PL, vp, i64, vp]
+    L.cnn_fwd_plan_static.argtypes = [vp, vp, vp, P, ctypes.c_int, PL, vp]
     L.cnn_eq1_cost.argtypes = [P, T, ctypes.c_int, ctypes.POINTER(ctypes.c_double),
                                ctypes.POINTER(ctypes.c_double)]
     L.cnn_slab_cost.argtypes = [P, i64, i64, ctypes.POINTER(ctypes.c_double)]
@@ -128,8 +130,8 @@ def lib():
     L.cnn_last_error.argtypes = []
     L.cnn_last_error.restype = ctypes.c_char_p
     L.cnn_abi_version.argtypes = []
-    for f in ("cnn_fwd", "cnn_plan", "cnn_plan_candidates", "cnn_variants", "cnn_plan_find", "cnn_plan_lookup", "cnn_plan_tiles", "cnn_fwd_plan", "cnn_fwd_plan_ws", "cnn_eq1_cost",
-              "cnn_slab_cost", "cnn_closed_form", "cnn_hbm_bytes", "cnn_device_budget",
+    for f in ("cnn_fwd", "cnn_plan", "cnn_plan_candidates", "cnn_variants", "cnn_plan_find", "cnn_plan_lookup", "cnn_plan_tiles", "cnn_fwd_plan", "cnn_fwd_plan_ws", "cnn_fwd_plan_static",
+              "cnn_eq1_cost", "cnn_slab_cost", "cnn_closed_form", "cnn_hbm_bytes", "cnn_device_budget",
               "cnn_abi_version"):
         getattr(L, f).restype = ctypes.c_int
     _lib = L
@@ -245,6 +247,15 @@ def fwd_plan_ws_ptr(In: int, Ker: int, Out: int, prob: Problem, dtype: int, pl: 
                                  ws, ws_bytes, stream))
 
 
+STATIC_SCRATCH_BYTES = 8 << 20
+
+
+def fwd_plan_static_ptr(In: int, Ker: int, Out: int, prob: Problem, dtype: int, pl: Plan,
+                        stream: int = 0):
+    _check(lib().cnn_fwd_plan_static(In, Ker, Out, ctypes.byref(prob), dtype, ctypes.byref(pl),
+                                     stream))
+
+
 def _tensor_dims(In, Ker, Out, sw, sh):
     import torch
     for name, t in (("In", In), ("Ker", Ker), ("Out", Out)):
@@ -314,4 +325,13 @@ def fwd_plan_ws(In, Ker, Out, pl: Plan, workspace, sw: int = 1, sh: int = 1, str
     ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
     fwd_plan_ws_ptr(In.data_ptr(), Ker.data_ptr(), Out.data_ptr(), problem(*dims), dt, pl,
                     ws_ptr, ws_bytes, _stream(stream))
+    return Out
+
+
+def fwd_plan_static(In, Ker, Out, pl: Plan, sw: int = 1, sh: int = 1, stream=None):
+    """cnn_fwd_plan_static: the plan's workspace is the library's static
+    device scratch (no allocation; calls that overlap on one GPU race)."""
+    dims, dt = _tensor_dims(In, Ker, Out, sw, sh)
+    fwd_plan_static_ptr(In.data_ptr(), Ker.data_ptr(), Out.data_ptr(), problem(*dims), dt, pl,
+                        _stream(stream))
     return Out

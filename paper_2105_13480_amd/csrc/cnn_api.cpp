@@ -277,32 +277,37 @@ bool v2_geometry_ok(const Variant2& v, const cnn_plan_t& pl) {
 
 // ws: the caller's workspace (at least pl.ws_bytes), or nullptr when the
 // plan needs none.  The library itself never allocates device memory here.
+// dry: check the plan only (no HIP call), return the status a run would.
 int run_plan(const void* In, const void* Ker, void* Out, const cnn_plan_t& pl, hipStream_t st,
-             void* ws = nullptr) {
+             void* ws = nullptr, bool dry = false) {
   if (pl.ws_bytes < 0) return fail(CNN_E_PLAN, "negative ws_bytes");
-  if (pl.ws_bytes > 0 && !ws)
+  if (pl.ws_bytes > 0 && !ws && !dry)
     return fail(CNN_E_UNSUPPORTED,
                 "plan needs a %lld-byte device workspace: use cnn_fwd_plan_ws",
                 (long long)pl.ws_bytes);
   const ConvArgs a = make_args(pl);
   hipError_t e;
   if (pl.kernel == CNN_K_DIRECT) {
+    if (dry) return CNN_OK;
     e = launch_direct(In, Ker, Out, a, pl.dtype, st);
   } else if (pl.kernel == CNN_K_GEMM1) {
     const VariantG* vg = find_variant_g(pl.variant);
     if (!vg || vg->dtype != pl.dtype || vg->tk != pl.tk || vg->tc != pl.tc ||
         !gemm1_geometry_ok(*vg, pl))
       return fail(CNN_E_PLAN, "plan names no matching kernel instantiation (variant %d)", pl.variant);
+    if (dry) return CNN_OK;
     e = launch_gemm1(*vg, In, Ker, Out, a, pl.lds_bytes, st);
   } else if (pl.kernel == CNN_K_ROWS) {
     const VariantR* vr = find_variant_r(pl.variant);
     if (!vr || vr->dtype != pl.dtype || vr->tk != pl.tk || !rows_geometry_ok(*vr, pl))
       return fail(CNN_E_PLAN, "plan names no matching kernel instantiation (variant %d)", pl.variant);
+    if (dry) return CNN_OK;
     e = launch_rows(*vr, In, Ker, Out, a, pl.lds_bytes, st);
   } else if (pl.kernel == CNN_K_SROWS) {
     const VariantQ* vq = find_variant_q(pl.variant);
     if (!vq || vq->dtype != pl.dtype || vq->tk != pl.tk || !srows_geometry_ok(*vq, pl))
       return fail(CNN_E_PLAN, "plan names no matching kernel instantiation (variant %d)", pl.variant);
+    if (dry) return CNN_OK;
     e = launch_srows(*vq, In, Ker, Out, ws, a, pl.lds_bytes, st);
   } else if (pl.kernel == CNN_K_SPLITC) {
     const Variant* v = find_variant(pl.variant);
@@ -315,21 +320,25 @@ int run_plan(const void* In, const void* Ker, void* Out, const cnn_plan_t& pl, h
         pl.ws_bytes != 4LL * pl.kc * p.Nb * p.Nk * p.Nw * p.Nh)
       return fail(CNN_E_PLAN, "split plan needs 1 <= kc <= %lld and ws_bytes = 4*kc*|Out|",
                   (long long)stages);
+    if (dry) return CNN_OK;
     e = launch_splitc(*v, In, Ker, Out, ws, a, pl.lds_bytes, pl.kc, pl.dtype, st);
   } else if (pl.kernel == CNN_K_SMALLC) {
     const VariantS* vs = find_variant_s(pl.variant);
     if (!vs || vs->dtype != pl.dtype || vs->tk != pl.tk || !smallc_geometry_ok(*vs, pl))
       return fail(CNN_E_PLAN, "plan names no matching kernel instantiation (variant %d)", pl.variant);
+    if (dry) return CNN_OK;
     e = launch_smallc(*vs, In, Ker, Out, a, pl.lds_bytes, st);
   } else if (const Variant4* v4 = find_variant4(pl.variant)) {
     if (pl.kernel != CNN_K_IGEMM_WIDE || v4->dtype != pl.dtype || v4->tk != pl.tk ||
         v4->tp != pl.tp || v4->tc != pl.tc || pl.ws_bytes != igemm4_ws_bytes(*v4, pl.prob))
       return fail(CNN_E_PLAN, "plan names no matching kernel instantiation (variant %d)", pl.variant);
+    if (dry) return CNN_OK;
     e = launch_igemm4(*v4, In, Ker, Out, ws, a, pl.lds_bytes, st);
   } else if (const Variant3* v3 = find_variant3(pl.variant)) {
     if (pl.kernel != CNN_K_IGEMM_DMA || v3->dtype != pl.dtype || v3->tk != pl.tk ||
         v3->tp != pl.tp || v3->tc != pl.tc || pl.ws_bytes != igemm3_ws_bytes(*v3, pl.prob))
       return fail(CNN_E_PLAN, "plan names no matching kernel instantiation (variant %d)", pl.variant);
+    if (dry) return CNN_OK;
     e = launch_igemm3(*v3, In, Ker, Out, ws, a, pl.lds_bytes, st);
   } else if (const Variant2* v2 = find_variant2(pl.variant)) {
     if (pl.kernel != v2_family(*v2) || v2->dtype != pl.dtype ||
@@ -337,12 +346,14 @@ int run_plan(const void* In, const void* Ker, void* Out, const cnn_plan_t& pl, h
         pl.tp < 1 || pl.tp > v2->tp || v2->tc != pl.tc ||
         pl.ws_bytes != igemm2_ws_bytes(*v2, pl.prob) || !v2_geometry_ok(*v2, pl))
       return fail(CNN_E_PLAN, "plan names no matching kernel instantiation (variant %d)", pl.variant);
+    if (dry) return CNN_OK;
     e = launch_igemm2(*v2, In, Ker, Out, ws, a, pl.lds_bytes, st);
   } else {
     const Variant* v = find_variant(pl.variant);
     if (!v || v->kernel != pl.kernel || v->dtype != pl.dtype || v->tk != pl.tk ||
         v->tp != pl.tp || v->tc != pl.tc || !igemm_geometry_ok(*v, pl))
       return fail(CNN_E_PLAN, "plan names no matching kernel instantiation (variant %d)", pl.variant);
+    if (dry) return CNN_OK;
     e = launch_igemm(*v, In, Ker, Out, a, pl.lds_bytes, st);
   }
   if (e != hipSuccess) return fail(CNN_E_HIP, "kernel launch failed: %s", hipGetErrorString(e));
@@ -473,6 +484,19 @@ int cnn_fwd_plan(const void* In, const void* Ker, void* Out, const cnn_problem* 
 int cnn_fwd_plan_ws(const void* In, const void* Ker, void* Out, const cnn_problem* prob,
                     int dtype, const cnn_plan_t* plan, void* workspace, int64_t ws_bytes,
                     void* stream) {
+  return cnnlib::fwd_plan_checked(In, Ker, Out, prob, dtype, plan, workspace, ws_bytes, stream,
+                                  false);
+}
+
+}  // extern "C"
+
+namespace cnnlib {
+
+int set_error(int status, const char* msg) { return fail(status, "%s", msg); }
+
+int fwd_plan_checked(const void* In, const void* Ker, void* Out, const cnn_problem* prob,
+                     int dtype, const cnn_plan_t* plan, void* workspace, int64_t ws_bytes,
+                     void* stream, bool dry) {
   if (!prob || !plan) return fail(CNN_E_NULL, "prob and plan must be non-NULL");
   int st;
   if ((st = check_problem(*prob)) || (st = check_dtype(dtype))) return st;
@@ -480,13 +504,18 @@ int cnn_fwd_plan_ws(const void* In, const void* Ker, void* Out, const cnn_proble
   if (!same_problem(plan->prob, *prob) || plan->dtype != dtype)
     return fail(CNN_E_PLAN, "plan was made for another problem or dtype");
   if (plan->ws_bytes > 0) {
-    if (!workspace) return fail(CNN_E_NULL, "plan needs a %lld-byte workspace", (long long)plan->ws_bytes);
+    if (!workspace && !dry)
+      return fail(CNN_E_NULL, "plan needs a %lld-byte workspace", (long long)plan->ws_bytes);
     if (ws_bytes < plan->ws_bytes || ((uintptr_t)workspace & 15))
       return fail(CNN_E_SHAPE, "workspace must be >= %lld bytes and 16-byte aligned",
                   (long long)plan->ws_bytes);
   }
-  return run_plan(In, Ker, Out, *plan, (hipStream_t)stream, workspace);
+  return run_plan(In, Ker, Out, *plan, (hipStream_t)stream, workspace, dry);
 }
+
+}  // namespace cnnlib
+
+extern "C" {
 
 // The plan cnn_fwd uses on the current device: the cached one (the model's
 // choice, or the winner of cnn_plan_find), else the model's choice, cached.

@@ -184,6 +184,15 @@ bool ranges_ok_whole(const cnn_problem& p, int dtype, int64_t in_limit);
 bool ranges_ok_smallc(const VariantS& v, const cnn_problem& p, int dtype);
 bool ranges_ok_srows(const VariantQ& v, const cnn_problem& p, int dtype);
 
+// Records a failure message for cnn_last_error(); returns status.
+int set_error(int status, const char* msg);
+
+// cnn_fwd_plan_ws; with `dry` = true every argument and plan check and no
+// HIP call (a NULL workspace then stands for one of ws_bytes bytes).
+int fwd_plan_checked(const void* In, const void* Ker, void* Out, const cnn_problem* prob,
+                     int dtype, const cnn_plan_t* plan, void* workspace, int64_t ws_bytes,
+                     void* stream, bool dry);
+
 // Lets `kernel` use up to 160 KiB of dynamic LDS on the current device.
 // The attribute is set once per (kernel, device); later calls return at
 // once.  Thread safe.

@@ -516,3 +516,27 @@ def test_hbm_bytes_rejects_bad_arguments():
     d = cnn.plan_tiles(cnn.problem(1, 16, 16, 16, 16, 3, 3, 1, 1), cnn.CNN_F32, cnn.K_DIRECT,
                        bud=cnn.budget())
     assert L.cnn_hbm_bytes(ctypes.byref(d), 8, 1 << 22, terms) == -8
+
+
+def test_static_scratch_entry_validates_before_hip():
+    """cnn_fwd_plan_static refuses, before any HIP call, a plan needing more
+    than CNN_STATIC_SCRATCH_BYTES of workspace, and bad arguments."""
+    L = cnn.lib()
+    dims = (1, 512, 512, 56, 56, 3, 3, 1, 1)
+    p = cnn.problem(*dims)
+    big = cnn.plan_tiles(p, cnn.CNN_BF16, cnn.K_SPLITC, 64, 64, 32, cnn.budget())
+    assert big.ws_bytes > cnn.STATIC_SCRATCH_BYTES
+    ptrs = (1 << 40, 1 << 42, 1 << 44)
+    assert L.cnn_fwd_plan_static(*ptrs, ctypes.byref(p), cnn.CNN_BF16, ctypes.byref(big), None) == -6
+    assert b"CNN_STATIC_SCRATCH_BYTES" in L.cnn_last_error()
+    small = cnn.problem(1, 16, 16, 16, 16, 3, 3, 1, 1)
+    pl = cnn.plan_tiles(small, cnn.CNN_F32, cnn.K_SPLITC, 64, 64, 8, cnn.budget())
+    assert L.cnn_fwd_plan_static(0, 0x100000, 0x200000, ctypes.byref(small), cnn.CNN_F32,
+                                 ctypes.byref(pl), None) == -1
+    assert L.cnn_fwd_plan_static(*ptrs, ctypes.byref(p), cnn.CNN_F32, ctypes.byref(pl),
+                                 None) == -8
+    q = cnn.Plan.from_buffer_copy(pl)
+    q.kc = 3
+    assert L.cnn_fwd_plan_static(0x1000, 0x100000, 0x200000, ctypes.byref(small), cnn.CNN_F32,
+                                 ctypes.byref(q), None) == -8
+
