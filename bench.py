@@ -106,6 +106,10 @@ def forced_plan(spec: str, w, mode: str):
             continue
         if pl.variant == want:
             return pl
+    # several instantiations may implement one tiling: the candidate itself
+    for pl in cnn.plan_candidates(prob, cnn.DTYPES[mode]):
+        if pl.kernel == kern and pl.variant == want and (tp in (0, pl.tp)):
+            return pl
     raise SystemExit(f"--plan {spec}: no tiling resolves to variant {want}")
 
 

@@ -125,8 +125,12 @@ bool ranges_ok_smallc(const VariantS& v, const cnn_problem& p, int dtype) {
 }
 
 bool ranges_ok_srows(const VariantQ& v, const cnn_problem& p, int dtype) {
-  return in_elems(p) * 2 < k2G && srows_ws_bytes(v, p) < k2G &&
-         p.Nb * p.Nk * p.Nw * p.Nh * out_bytes(dtype) < k2G;
+  // (the raw-Ker form addresses Ker up to the end of the last 256-feature
+  // range, and puts Out offsets up to 288 features past the end in the
+  // scalar offset beside an out-of-range lane offset)
+  const int64_t ker_end = (p.Nk + 255) / 256 * 256 * p.Nc * p.Nr * p.Ns * 2;
+  return in_elems(p) * 2 < k2G && srows_ws_bytes(v, p) < k2G && ker_end < k2G &&
+         (p.Nb * p.Nk + 288) * p.Nw * p.Nh * out_bytes(dtype) < k2G;
 }
 
 static double model_us(const cnn_plan_t& pl, const cnn_budget& bud);
@@ -351,7 +355,13 @@ struct FamilyCost {
 static FamilyCost family_cost(int kernel, int variant) {
   switch (kernel) {
     case CNN_K_ROWS: return {0.73, 5.17, 0.01, 58.0};
-    case CNN_K_SROWS: return {0.53, 1.39, 0.11, 48.3};
+    case CNN_K_SROWS: {
+      int n = 0;
+      const VariantQ* vq = variants_srows(&n);
+      for (int i = 0; i < n; ++i)  // Ker repacked on chip, one wave per SIMD
+        if (vq[i].id == variant && vq[i].form == 2) return {0.42, 4.30, 0.11, 48.3};
+      return {0.53, 1.39, 0.11, 48.3};
+    }
     case CNN_K_GEMM1: {
       int n = 0;
       const VariantG* vg = variants_gemm1(&n);

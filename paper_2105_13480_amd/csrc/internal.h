@@ -159,8 +159,9 @@ struct VariantQ {
   int32_t tk;
   int32_t nr, ns;  // compile-time stencil
   int32_t L;       // output rows per band
-  int32_t waves;   // 4 (one per feature pair) or 8 (two, rows split)
+  int32_t waves;   // 4 or 8
   int32_t acc;     // fp32 accumulators per lane
+  int32_t form;    // 1: packed Ker in a workspace; 2: raw Ker repacked on chip
 };
 const VariantQ* variants_srows(int* count);
 int64_t srows_slab_rows(const VariantQ& v);

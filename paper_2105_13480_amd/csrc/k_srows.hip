@@ -378,6 +378,379 @@ __global__ __launch_bounds__(64 * NWV) void conv_srows(const bf16_t* __restrict_
   }
 }
 
+// ---- raw-Ker form -------------------------------------------------------------
+// conv_srows2: the same bands, In staging and operand layout, with two
+// differences.  Ker is read in its raw layout ([k][c][r][s]: a feature's 16
+// channels x RS taps of a chunk are one 32*RS-byte run) and repacked on
+// chip, so no workspace is needed; and the workgroup's 256 features are two
+// tiles of 128 taken one after the other, with two accumulator sets, so the
+// first tile's Out rows are stored while the second tile is multiplied (one
+// row per chunk) and only the second tile's drain remains after the last
+// product.  Four waves (one per SIMD): wave w takes features 32w .. 32w+31
+// of the tile for all L rows of the band.
+// * Ker, per chunk: the raw runs of the tile's 128 features are copied by
+//   16-byte buffer->LDS DMA into a raw buffer (one contiguous kilobyte per
+//   wave instruction); thread (k, g) = (tid/2, tid%2) reads its feature's
+//   8-channel run (RS units, conflict free) back into registers and, one
+//   stage ahead of its use (two stages before it is read), writes the three
+//   B-operand units of a stencil row -- [s][g][k] planes of 136 units, so
+//   the writes of a half wave hit distinct banks -- into that row's slot.
+// * Schedule of chunk x (global over both tiles; stage r = stencil row r):
+//   stage 0 writes In(x+1) from registers and packs slot 2 for (x, 2);
+//   stage 1 reads back raw(x+1), loads In(x+2) into registers and packs
+//   slot 0 for (x+1, 0); stage 2 copies raw(x+2) by DMA, packs slot 1 for
+//   (x+1, 1) and issues 16 Out stores (a row of the first tile's
+//   accumulators during the second tile, out-of-range no-ops otherwise, so
+//   every chunk issues the same memory instructions and the wait counts are
+//   fixed).  One barrier per stage.
+template <typename TO, int NR, int NS, int L>
+__global__ __launch_bounds__(256) void conv_srows2(const bf16_t* __restrict__ In,
+                                                   const bf16_t* __restrict__ Ker,
+                                                   TO* __restrict__ Out, ConvArgs a) {
+  constexpr int NT = 256;
+  constexpr int TKT = 128;                 // features per tile
+  constexpr int RS = NR * NS;
+  constexpr int SR = 2 * (L - 1) + NR;     // slab rows held per chunk
+  constexpr int NI = 2 * SR * 8 * 2;       // In items per chunk
+  constexpr int NIPT = (NI + NT - 1) / NT; // items per thread
+  constexpr int IN_UNITS = 2 * SR * 64;    // 16-byte units per In buffer
+  constexpr int RAW_UNITS = TKT * 2 * RS;  // raw Ker of a chunk: 128 x 16 channels x RS
+  constexpr int NDMA = RAW_UNITS / NT;     // raw copies per thread per chunk
+  constexpr int PST = TKT + 8;             // B-operand plane stride (units)
+  constexpr int SLOT = NS * 2 * PST;       // units per stage slot
+  constexpr int NSTO = 16;                 // Out stores per thread per chunk
+  static_assert(RAW_UNITS % NT == 0, "whole copies");
+  static_assert(NR == 3 && NS <= 3, "one slot per stencil row, taps within one 64-unit row");
+  static_assert(L >= 1 && L <= 7, "rows per band (two accumulator sets)");
+  static_assert(NDMA + NSTO <= 63, "wait counts");
+
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  u32x4_t* kslot = reinterpret_cast<u32x4_t*>(smem);  // [NR][NS][2][PST]
+  u32x4_t* raw = kslot + NR * SLOT;                    // [RAW_UNITS]
+  u32x4_t* ibuf = raw + RAW_UNITS;                     // [2][2][SR][64]
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // (wave-uniform)
+  const int l32 = lane & 31, half = lane >> 5;
+
+  const int n_bands = a.Nw / L;
+  const int tile = xcd_remap(blockIdx.x, gridDim.x);
+  const int band = tile / a.n_ktiles;
+  const int kt = tile - band * a.n_ktiles;  // 256-feature range
+  const int b = band / n_bands;
+  const int w0 = (band - b * n_bands) * L;
+  const int n_cc = a.Nc / 16;
+  const int nt = a.Nk - kt * 256 > TKT ? 2 : 1;  // tiles of 128 features in the range
+  const int n_gc = nt * n_cc;                    // chunks the workgroup walks
+
+  const __amdgpu_buffer_rsrc_t in_rsrc = rsrc_q(In, a.in_total * 2);
+  const __amdgpu_buffer_rsrc_t ker_rsrc = rsrc_q(Ker, (int64_t)a.Nk * a.Nc * RS * 2);
+  const __amdgpu_buffer_rsrc_t out_rsrc = rsrc_q(Out, a.out_total * (int64_t)sizeof(TO));
+
+  // ---- In items and layout: as conv_srows (slot rotation swz below).
+  const uint32_t in_last =
+      __builtin_amdgcn_raw_buffer_load_b16(in_rsrc, (uint32_t)((a.in_total - 1) * 2), 0, 0);
+  int in_e[NIPT];    // element offset of the item's channel 8g + 4hc of chunk 0
+  int in_dst[NIPT];  // unit of its first even column (+ 8 bytes for hc = 1)
+  int in_hc[NIPT];
+  int in_rot[NIPT];  // the block's slot rotation
+  bool in_ok[NIPT];
+#pragma unroll
+  for (int j = 0; j < NIPT; ++j) {
+    const int t = tid + NT * j;
+    const int tt = t < NI ? t : NI - 1;
+    const int hc = tt & 1, b8 = (tt >> 1) & 7, gj = tt >> 4;
+    const int g = gj / SR, jr = gj - g * SR;
+    const int x = 2 * w0 + jr;
+    in_e[j] = (int)((int64_t)b * a.in_img) + (8 * g + 4 * hc) * a.nxny + x * a.Ny + 8 * b8;
+    in_dst[j] = (g * SR + jr) * 64 + 4 * b8;
+    in_hc[j] = hc;
+    in_rot[j] = 2 * ((b8 >> 2) & 1) + (jr & 1);
+    in_ok[j] = t < NI;
+  }
+  u32x4_t vin[NIPT][4];
+  auto load_in = [&](int cc) __attribute__((always_inline)) {
+#pragma unroll
+    for (int j = 0; j < NIPT; ++j)
+#pragma unroll
+      for (int k = 0; k < 4; ++k)
+        vin[j][k] = __builtin_bit_cast(
+            u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(
+                         in_rsrc, (uint32_t)((in_e[j] + (16 * cc + k) * a.nxny) * 2), 0, 0));
+  };
+  auto write_in_part = [&](int cc, u32x4_t* dstb, int i0_, int i1_) __attribute__((always_inline)) {
+    char* base = reinterpret_cast<char*>(dstb);
+#pragma unroll
+    for (int j = 0; j < NIPT; ++j) {
+      if (!in_ok[j]) continue;
+      u32x4_t v[4] = {vin[j][0], vin[j][1], vin[j][2], vin[j][3]};
+      const int d0 = (int)(a.in_total - 1) - (in_e[j] + 16 * cc * a.nxny);
+      if (d0 >= 0 && d0 < 3 * a.nxny + 8) {
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const int d = d0 - k * a.nxny;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const uint32_t lo = d == 2 * i ? ((v[k][i] & 0xffff0000u) | in_last) : v[k][i];
+            v[k][i] = d == 2 * i + 1 ? ((lo & 0xffffu) | (in_last << 16)) : lo;
+          }
+        }
+      }
+      char* p = base + in_dst[j] * 16 + 8 * in_hc[j];
+#pragma unroll
+      for (int i = i0_; i < i1_; ++i) {
+        const int slot = 16 * ((i + in_rot[j]) & 3);
+        const u32x2_t ev = {__builtin_amdgcn_perm(v[1][i], v[0][i], 0x05040100u),
+                            __builtin_amdgcn_perm(v[3][i], v[2][i], 0x05040100u)};
+        *reinterpret_cast<u32x2_t*>(p + slot) = ev;
+        if (NS > 1) {
+          const u32x2_t od = {__builtin_amdgcn_perm(v[1][i], v[0][i], 0x07060302u),
+                              __builtin_amdgcn_perm(v[3][i], v[2][i], 0x07060302u)};
+          *reinterpret_cast<u32x2_t*>(p + 16 * 32 + slot) = od;
+        }
+      }
+    }
+  };
+  auto cc_of = [&](int x) { return x < n_cc ? x : x - n_cc; };
+
+  // ---- Ker: raw copies, read-back, repack.
+  uint32_t raw_src[NDMA];  // byte offset of this thread's pieces, feature base 0, chunk 0
+#pragma unroll
+  for (int j = 0; j < NDMA; ++j) {
+    const int p = j * NT + tid;
+    const int k = p / (2 * RS), q = p - k * 2 * RS;
+    raw_src[j] = (uint32_t)(k * a.Nc * RS * 2 + 16 * q);
+  }
+  auto copy_raw = [&](int x) __attribute__((always_inline)) {
+    const int kb = kt * 256 + (x < n_cc ? 0 : TKT);
+    const uint32_t base = (uint32_t)((kb * a.Nc + 16 * cc_of(x)) * RS * 2);
+#pragma unroll
+    for (int j = 0; j < NDMA; ++j) dma16_q(ker_rsrc, raw + j * NT + 64 * wave, base + raw_src[j]);
+  };
+  u32x4_t run[RS];
+  auto read_run = [&]() __attribute__((always_inline)) {
+#pragma unroll
+    for (int q = 0; q < RS; ++q) run[q] = raw[tid * RS + q];
+  };
+  const int pk = tid >> 1, pg = tid & 1;
+  // Slot of stencil row R: unit (s, g, k) = channels 8g .. 8g+7 of feature k
+  // at tap (R, s), from the run's elements (8g + i) * RS + R NS + s.
+  auto pack = [&](auto RC) __attribute__((always_inline)) {
+    constexpr int R = decltype(RC)::value;
+#pragma unroll
+    for (int s_ = 0; s_ < NS; ++s_) {
+      const int tap = R * NS + s_;
+      u32x4_t v;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int e0 = (2 * i) * RS + tap, e1 = e0 + RS;
+        const uint32_t sel =
+            ((e0 & 1) ? 0x0302u : 0x0100u) | ((e1 & 1) ? 0x07060000u : 0x05040000u);
+        v[i] = __builtin_amdgcn_perm(run[(e1 >> 1) >> 2][(e1 >> 1) & 3],
+                                     run[(e0 >> 1) >> 2][(e0 >> 1) & 3], sel);
+      }
+      kslot[R * SLOT + (s_ * 2 + pg) * PST + pk] = v;
+    }
+  };
+
+  // ---- operands: A = Ker unit (s, half, feature 32 wave + l32) of a slot;
+  // B = In unit of band row i for stencil row r, tap s (as conv_srows).
+  auto swz = [](int u, int par) { return (u & ~3) | (((u & 3) + 2 * ((u >> 4) & 1) + par) & 3); };
+  int a_sw[NS][2];
+#pragma unroll
+  for (int s_ = 0; s_ < NS; ++s_)
+#pragma unroll
+    for (int par = 0; par < 2; ++par)
+      a_sw[s_][par] = swz(((s_ & 1) ? 32 + (s_ >> 1) : (s_ >> 1)) + l32, par);
+  const int ka_off = half * PST + 32 * wave + l32;
+  const int ib_off = half * SR * 64;
+  auto read_ka = [&](int r, int s_) __attribute__((always_inline)) {
+    return kslot[r * SLOT + s_ * 2 * PST + ka_off];
+  };
+  auto read_ib = [&](const u32x4_t* ib, int r, int s_, int i) __attribute__((always_inline)) {
+    const int jr = 2 * i + r;
+    return ib[ib_off + jr * 64 + a_sw[s_][jr & 1]];
+  };
+
+  f32x16_t acc[2][L];
+#pragma unroll
+  for (int t = 0; t < 2; ++t)
+#pragma unroll
+    for (int i = 0; i < L; ++i)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[t][i][e] = 0.f;
+
+  // ---- Out: register j of (tile t, row i) is position l32 of output row
+  // w0 + i, feature kt*256 + 128 t + 32 wave + 4 half + 8 (j/4) + j%4.  The
+  // lane's part of the offset is one register; the rest (tile, row,
+  // register) is wave-uniform and goes in the scalar offset.  Stores of
+  // features past Nk or positions past Nh, and the no-op stores, get an
+  // out-of-range lane offset.
+  const int nhw = a.Nw * a.Nh;
+  const uint32_t lane_off = (uint32_t)((4 * half * nhw + l32) * (int)sizeof(TO));
+  const int feat_lane = kt * 256 + 32 * wave + 4 * half;  // + 128 t + 8 (j/4) + j%4
+  const bool pos_ok = l32 < a.Nh;
+  auto store_regs = [&](const f32x16_t& v, int t, int i, bool valid, int j0, int j1)
+      __attribute__((always_inline)) {
+    // (b, first feature of the wave's block, row w0 + i) -- wave-uniform
+    // (computed where the stores are issued: the empty asm keeps the
+    // compiler from hoisting every row's and register's offsets out of the
+    // chunk loop into registers)
+    // (no-op stores take a zero row offset: their lane offset is out of
+    // range, and lane plus scalar offset then stays within 2^31 .. 2^32)
+    uint32_t row_off = valid ? (uint32_t)(((((int64_t)b * a.Nk + kt * 256 + TKT * t + 32 * wave) *
+                                               a.Nw + w0 + i) * a.Nh) * (int64_t)sizeof(TO))
+                             : 0u;
+    asm volatile("" : "+s"(row_off));
+    // (the lane offset with the validity folded in is made a vector value
+    // here, so the compiler selects it per lane instead of branching on the
+    // wave-uniform part, which would leave its wait counts imprecise)
+    uint32_t lo = (valid && pos_ok) ? lane_off : 0x80000000u;
+    asm volatile("" : "+v"(lo));
+    const int n_room = a.Nk - (feat_lane + TKT * t);  // features of this lane still in range
+#pragma unroll
+    for (int j = j0; j < j1; ++j) {
+      const int dj = 8 * (j >> 2) + (j & 3);
+      const uint32_t vo = dj < n_room ? lo : 0x80000000u;
+      const uint32_t so = row_off + (uint32_t)(dj * nhw * (int)sizeof(TO));
+      if constexpr (sizeof(TO) == 4)
+        __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v[j]), out_rsrc, vo, so, 0);
+      else
+        __builtin_amdgcn_raw_buffer_store_b16(from_f32<bf16_t>(v[j]), out_rsrc, vo, so, 0);
+    }
+  };
+  // The stores chunk x issues (registers j0 .. j1-1 of one row): in the
+  // second tile, row x - n_cc of the first tile while rows remain -- always
+  // from acc[0][0], the rows being shifted down after each chunk's stores,
+  // so the code is the same in every chunk -- else out-of-range no-ops
+  // from registers no product writes at that time.
+  auto chunk_stores = [&](auto TC, int x, int j0, int j1) __attribute__((always_inline)) {
+    constexpr int TL = decltype(TC)::value;
+    if constexpr (TL == 0) {
+      store_regs(acc[1][0], 1, 0, false, j0, j1);
+    } else {
+      const int row = x - n_cc;
+      store_regs(acc[0][0], 0, row, row < L, j0, j1);
+    }
+  };
+  auto shift_rows = [&]() __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i + 1 < L; ++i) acc[0][i] = acc[0][i + 1];
+  };
+  u32x4_t KA[2], IB[2][L];
+  // One stage (stencil row r of the chunk in ib) into accumulator set TL:
+  // NS K-steps from operand parity P, whose step-0 operands are in
+  // registers; each next step's operands -- in the last step, those of the
+  // next stage (slot nr, buffer nib) -- are read between the products.
+  // mem(slot): this stage's memory work, slot 0 first, slot s + 1 after
+  // K-step s's products.
+  auto stage = [&](auto PC, auto TC, int r, const u32x4_t* ib, int nr_, const u32x4_t* nib,
+                   auto mem) __attribute__((always_inline)) {
+    constexpr int P = decltype(PC)::value;
+    constexpr int TL = decltype(TC)::value;
+    mem(0);
+    __builtin_amdgcn_sched_barrier(0);
+    static_for<0, NS>([&](auto SC) {
+      constexpr int st = decltype(SC)::value;
+      constexpr int cu = (P + st) & 1, nx = cu ^ 1;
+#pragma unroll
+      for (int i = 0; i < L; ++i) {
+        acc[TL][i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+            __builtin_bit_cast(bf16x8_t, KA[cu]), __builtin_bit_cast(bf16x8_t, IB[cu][i]),
+            acc[TL][i], 0, 0, 0);
+        if (i == 0) KA[nx] = st + 1 < NS ? read_ka(r, st + 1) : read_ka(nr_, 0);
+        IB[nx][i] = st + 1 < NS ? read_ib(ib, r, st + 1, i) : read_ib(nib, nr_, 0, i);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      mem(st + 1);
+      __builtin_amdgcn_sched_barrier(0);
+    });
+  };
+
+  // One chunk x into accumulator set TL (the three stages and their memory
+  // work; see the schedule above).
+  auto chunk = [&](auto TC, int x) __attribute__((always_inline)) {
+    const int x1 = min(x + 1, n_gc - 1), x2 = min(x + 2, n_gc - 1);
+    const u32x4_t* ib = ibuf + (x & 1) * IN_UNITS;
+    u32x4_t* ibn = ibuf + ((x + 1) & 1) * IN_UNITS;
+    stage(std::integral_constant<int, 0>(), TC, 0, ib, 1, ib, [&](int slot) __attribute__((always_inline)) {
+      if (slot == 0) write_in_part(cc_of(x1), ibn, 0, 2);
+      if (slot == 1) write_in_part(cc_of(x1), ibn, 2, 4);
+      if (slot == 2) pack(std::integral_constant<int, 2>());
+    });
+    __builtin_amdgcn_sched_barrier(0);
+    // raw(x + 1), copied during the previous chunk's stage 2, has landed
+    // (only that stage's stores may remain in flight)
+    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(NSTO) : "memory");
+    stage(std::integral_constant<int, (NS & 1)>(), TC, 1, ib, 2, ib, [&](int slot) __attribute__((always_inline)) {
+      if (slot == 0) {
+        read_run();
+        load_in(cc_of(x2));
+      }
+      if (slot == 2) pack(std::integral_constant<int, 0>());
+    });
+    __builtin_amdgcn_sched_barrier(0);
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    stage(std::integral_constant<int, ((2 * NS) & 1)>(), TC, 2, ib, 0, ibn, [&](int slot) __attribute__((always_inline)) {
+      if (slot == 0) copy_raw(x2);
+      if (slot == 1) {
+        pack(std::integral_constant<int, 1>());
+        chunk_stores(TC, x, 0, NSTO / 2);
+      }
+      if (slot == 2) chunk_stores(TC, x, NSTO / 2, NSTO);
+      if constexpr (decltype(TC)::value == 1)
+        if (slot == 3) shift_rows();
+    });
+    __builtin_amdgcn_sched_barrier(0);
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    if constexpr (((NR * NS) & 1) != 0) {
+      // a chunk has an odd number of K-steps: the next chunk's first
+      // operands were read into parity 1
+      KA[0] = KA[1];
+#pragma unroll
+      for (int i = 0; i < L; ++i) IB[0][i] = IB[1][i];
+    }
+  };
+
+  // ---- prologue: In(0) and raw(0) in, slots 0 and 1 packed, In(1) loads
+  // and raw(1) in flight (then the 16 no-op stores every chunk's stage 2
+  // issues, so the first chunk's wait counts are those of every chunk).
+  load_in(0);
+  copy_raw(0);
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  write_in_part(0, ibuf, 0, 4);
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  read_run();
+  pack(std::integral_constant<int, 0>());
+  pack(std::integral_constant<int, 1>());
+  load_in(cc_of(min(1, n_gc - 1)));
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  copy_raw(min(1, n_gc - 1));
+  chunk_stores(std::integral_constant<int, 0>(), 0, 0, NSTO);
+  KA[0] = read_ka(0, 0);
+#pragma unroll
+  for (int i = 0; i < L; ++i) IB[0][i] = read_ib(ibuf, 0, 0, i);
+
+  for (int x = 0; x < n_cc; ++x) chunk(std::integral_constant<int, 0>(), x);
+  for (int x = n_cc; x < n_gc; ++x) chunk(std::integral_constant<int, 1>(), x);
+
+  // ---- epilogue: the last tile's rows (and any first-tile rows the second
+  // tile's chunks did not reach)
+  if (nt == 2) {
+    // first-tile rows n_cc .. L-1 (the second tile had fewer chunks than
+    // rows) sit in acc[0][0 .. L-1-n_cc] after n_cc shifts
+#pragma unroll
+    for (int i = 0; i < L; ++i)
+      if (i < L - n_cc) store_regs(acc[0][i], 0, n_cc + i, true, 0, 16);
+#pragma unroll
+    for (int i = 0; i < L; ++i) store_regs(acc[1][i], 1, i, true, 0, 16);
+  } else {
+#pragma unroll
+    for (int i = 0; i < L; ++i) store_regs(acc[0][i], 0, i, true, 0, 16);
+  }
+}
+
 // ---- Ker repack --------------------------------------------------------------
 // Slice image of every (k tile, 16-channel chunk): unit
 // ((kt*n_cc + cc)*blk_vecs + (tap*2 + g)*TK + kk) holds channels
@@ -421,21 +794,28 @@ __global__ __launch_bounds__(256) void pack_ker_srows(const bf16_t* __restrict__
 }
 
 // ---- instantiation table ----------------------------------------------------
-// (id, dtype, NR, NS, L, waves): tk = 256, tc = 16, bands of L output rows.
+// (id, dtype, NR, NS, L, waves, form): tk = 256, tc = 16, bands of L output
+// rows; form 1 = conv_srows (Ker repacked into a workspace by a second
+// kernel), form 2 = conv_srows2 (raw Ker, repacked on chip, no workspace).
 // (Four waves -- one per feature pair, all L rows, accumulators in AGPRs --
-// time the same as eight on the 3x3 stride-2 layer, so only eight are built.)
-#define CNN_SROWS_VARIANTS(X)          \
-  X(1900, CNN_BF16, 3, 3, 7, 8)        \
-  X(1901, CNN_BF16, 3, 3, 4, 8)        \
-  X(2000, CNN_BF16_OBF16, 3, 3, 7, 8)  \
-  X(2001, CNN_BF16_OBF16, 3, 3, 4, 8)
+// time the same as eight for conv_srows on the 3x3 stride-2 layer, so only
+// eight are built of that form.)
+#define CNN_SROWS_VARIANTS(X)             \
+  X(1900, CNN_BF16, 3, 3, 7, 8, 1)        \
+  X(1901, CNN_BF16, 3, 3, 4, 8, 1)        \
+  X(2000, CNN_BF16_OBF16, 3, 3, 7, 8, 1)  \
+  X(2001, CNN_BF16_OBF16, 3, 3, 4, 8, 1)  \
+  X(2100, CNN_BF16, 3, 3, 7, 4, 2)        \
+  X(2101, CNN_BF16, 3, 3, 4, 4, 2)        \
+  X(2200, CNN_BF16_OBF16, 3, 3, 7, 4, 2)  \
+  X(2201, CNN_BF16_OBF16, 3, 3, 4, 4, 2)
 
-// acc: fp32 accumulators per lane (8 waves: 2 RW - 1 blocks for odd L, else
-// 2 RW; 4 waves: 2 L blocks, of 16 each)
+// acc: fp32 accumulators per lane (form 1, 8 waves: 2 RW - 1 blocks for
+// odd L, else 2 RW; form 2, 4 waves: two sets of L blocks; 16 each)
 static const VariantQ kVariantsQ[] = {
-#define CNN_QV(id, dt, nr, ns, l, nw)                                                  \
+#define CNN_QV(id, dt, nr, ns, l, nw, form)                                            \
   {id, dt, 256, nr, ns, l, nw,                                                         \
-   nw == 8 ? 32 * ((l + 1) / 2) - 16 * (l & 1) : 32 * l},
+   form == 2 ? 32 * l : (nw == 8 ? 32 * ((l + 1) / 2) - 16 * (l & 1) : 32 * l), form},
     CNN_SROWS_VARIANTS(CNN_QV)
 #undef CNN_QV
 };
@@ -450,6 +830,9 @@ int64_t srows_slab_rows(const VariantQ& v) {
 }
 
 int64_t srows_lds_bytes(const VariantQ& v) {
+  if (v.form == 2)  // stencil-row slots, the raw chunk, two In buffers
+    return ((int64_t)v.nr * v.ns * 2 * (128 + 8) + 128 * 2 * v.nr * v.ns +
+            2 * 2 * srows_slab_rows(v) * 64) * 16;
   return (4 * (int64_t)v.ns * 2 * v.tk + 2 * 2 * srows_slab_rows(v) * 64) * 16;
 }
 
@@ -459,6 +842,7 @@ int64_t srows_blk_vecs(const VariantQ& v) {
 }
 
 int64_t srows_ws_bytes(const VariantQ& v, const cnn_problem& p) {
+  if (v.form == 2) return 0;
   return ((p.Nk + v.tk - 1) / v.tk) * (p.Nc / 16) * srows_blk_vecs(v) * 16;
 }
 
@@ -468,30 +852,41 @@ bool srows_fits(const VariantQ& v, const cnn_problem& p) {
          p.Nh <= 32 && Ny <= 64 && p.Nw % v.L == 0;
 }
 
-template <int DT, int NR, int NS, int L, int NWV>
+template <int DT, int NR, int NS, int L, int NWV, int FORM>
 static hipError_t launch_q(const void* In, const void* Ker, void* Out, void* ws, const ConvArgs& a,
                            int64_t lds, hipStream_t stream, const VariantQ& v) {
   typedef typename std::conditional<DT == CNN_BF16, float, bf16_t>::type TO;
-  const int blk = (int)srows_blk_vecs(v);
-  const int64_t threads = (int64_t)a.n_ktiles * (a.Nc / 16) * 2 * 256;
-  hipLaunchKernelGGL(pack_ker_srows<NR * NS>, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0,
-                     stream, (const bf16_t*)Ker, (u32x4_t*)ws, a, blk);
-  auto kern = conv_srows<TO, NR, NS, L, NWV>;
-  {
+  if constexpr (FORM == 2) {
+    (void)ws;
+    (void)v;
+    auto kern = conv_srows2<TO, NR, NS, L>;
     const hipError_t e = allow_max_lds((const void*)kern);
     if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(kern, dim3((unsigned)a.grid), dim3(256), (unsigned)lds, stream,
+                       (const bf16_t*)In, (const bf16_t*)Ker, (TO*)Out, a);
+    return hipGetLastError();
+  } else {
+    const int blk = (int)srows_blk_vecs(v);
+    const int64_t threads = (int64_t)a.n_ktiles * (a.Nc / 16) * 2 * 256;
+    hipLaunchKernelGGL(pack_ker_srows<NR * NS>, dim3((unsigned)((threads + 255) / 256)), dim3(256),
+                       0, stream, (const bf16_t*)Ker, (u32x4_t*)ws, a, blk);
+    auto kern = conv_srows<TO, NR, NS, L, NWV>;
+    {
+      const hipError_t e = allow_max_lds((const void*)kern);
+      if (e != hipSuccess) return e;
+    }
+    hipLaunchKernelGGL(kern, dim3((unsigned)a.grid), dim3(64 * NWV), (unsigned)lds, stream,
+                       (const bf16_t*)In, (const u32x4_t*)ws, (TO*)Out, a, blk);
+    return hipGetLastError();
   }
-  hipLaunchKernelGGL(kern, dim3((unsigned)a.grid), dim3(64 * NWV), (unsigned)lds, stream,
-                     (const bf16_t*)In, (const u32x4_t*)ws, (TO*)Out, a, blk);
-  return hipGetLastError();
 }
 
 hipError_t launch_srows(const VariantQ& v, const void* In, const void* Ker, void* Out, void* ws,
                         const ConvArgs& a, int64_t lds_bytes, hipStream_t stream) {
   switch (v.id) {
-#define CNN_CASEQ(id, dt, nr, ns, l, nw) \
-  case id:                              \
-    return launch_q<dt, nr, ns, l, nw>(In, Ker, Out, ws, a, lds_bytes, stream, v);
+#define CNN_CASEQ(id, dt, nr, ns, l, nw, form) \
+  case id:                                    \
+    return launch_q<dt, nr, ns, l, nw, form>(In, Ker, Out, ws, a, lds_bytes, stream, v);
     CNN_SROWS_VARIANTS(CNN_CASEQ)
 #undef CNN_CASEQ
     default:

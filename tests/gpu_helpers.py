@@ -95,12 +95,28 @@ def variant_dims(kernel, vid, dt, tk, tp, tc, stencils):
     return None
 
 
-def _fits(dims, dt, kernel, tk, tp, tc, vid):
+def variant_plan(dims, dt, kernel, tk, tp, tc, vid, bud=None):
+    """The plan of instantiation `vid` for (kernel, tk, tp, tc) on problem
+    dims: cnn_plan_tiles' choice if it is `vid`, else the candidate of that
+    instantiation (several instantiations may implement one tiling); None
+    if it does not fit."""
+    prob = cnn.problem(*dims)
     try:
-        pl = cnn.plan_tiles(cnn.problem(*dims), dt, kernel, tk, tp, tc, cnn.budget())
+        pl = cnn.plan_tiles(prob, dt, kernel, tk, tp, tc, bud)
+        if pl.variant == vid:
+            return pl
     except cnn.CnnError:
-        return False
-    return pl.variant == vid
+        pl = None
+    for c in cnn.plan_candidates(prob, dt, bud):
+        if c.variant == vid and c.kernel == kernel and c.tk == tk and (tp == 0 or c.tp == tp or
+                                                                       kernel != cnn.K_SROWS):
+            if pl is None or c.tp == pl.tp:
+                return c
+    return None
+
+
+def _fits(dims, dt, kernel, tk, tp, tc, vid):
+    return variant_plan(dims, dt, kernel, tk, tp, tc, vid, cnn.budget()) is not None
 
 
 def _variant_dims_one(kernel, vid, dt, tk, tp, tc, stencil):

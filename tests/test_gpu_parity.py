@@ -13,7 +13,7 @@ import oracle
 from paper_2105_13480_amd import cnn, inputs
 
 from gpu_helpers import (TOL, errors, out_tensor, run, say, to_gpu, to_host64, variant_cases,
-                         variant_dims)
+                         variant_dims, variant_plan)
 
 pytestmark = pytest.mark.gpu
 
@@ -59,8 +59,8 @@ def test_every_igemm_variant_exact_integers(case):
     dims = variant_dims(kernel, vid, dt, tk, tp, tc, stencils)
     assert dims is not None, f"no test shape fits instantiation {vid}"
     In, Ker = _arrays(dims, mode, seed=vid, dist=("int", -2, 2), kdist=("int", -2, 2))
-    pl = cnn.plan_tiles(cnn.problem(*dims), dt, kernel, tk, tp, tc)
-    assert pl.variant == vid
+    pl = variant_plan(dims, dt, kernel, tk, tp, tc, vid)
+    assert pl is not None and pl.variant == vid
     say(f"[parity] variant {vid} tk={tk} tp={tp} tc={tc} dims={dims} grid={pl.grid}")
     got = run(In, Ker, dims[7], dims[8], mode, plan=pl)
     want = oracle.conv(In, Ker, dims[7], dims[8])
@@ -346,6 +346,8 @@ SROWS_SHAPES = [
     (2, 16, 40, 28, 4, 3, 3, 2, 2),     # Nh = 4: short rows, 4 or 7 bands
     (2, 16, 40, 7, 27, 3, 3, 2, 2),     # Nh = 27 (Ny = 55): a ragged row end
     (1, 32, 70, 8, 13, 3, 3, 2, 2),     # Nh = 13, two bands of 4, features past Nk
+    (2, 16, 200, 7, 28, 3, 3, 2, 2),    # one chunk: first-tile rows left for the end
+    (1, 128, 160, 4, 28, 3, 3, 2, 2),   # eight chunks, a second tile of 32 features
 ]
 
 
@@ -370,8 +372,8 @@ def test_srows_exact(shape, mode):
         vid, L = v.variant, v.mode
         if v.kernel != cnn.K_SROWS or v.dtype != dt or (v.nr, v.ns) != (Nr, Ns) or Nw % L:
             continue
-        pl = cnn.plan_tiles(cnn.problem(*shape), dt, cnn.K_SROWS, 256, L * Nh, 16)
-        assert pl.variant == vid and pl.grid == Nb * (Nw // L) * -(-Nk // 256)
+        pl = variant_plan(shape, dt, cnn.K_SROWS, 256, L * Nh, 16, vid)
+        assert pl is not None and pl.variant == vid and pl.grid == Nb * (Nw // L) * -(-Nk // 256)
         say(f"[parity] srows shape={shape} v{vid} L={L} grid={pl.grid} mode={mode}")
         got = run(In, Ker, 2, 2, mode, plan=pl)
         assert np.array_equal(got, want), (vid, L)
@@ -390,8 +392,7 @@ def test_srows_float_strided_shape():
     for v in cnn.variants():
         if v.kernel != cnn.K_SROWS or v.dtype != cnn.CNN_BF16 or w.Nw % v.mode:
             continue
-        pl = cnn.plan_tiles(cnn.problem(*w.dims()), cnn.CNN_BF16, cnn.K_SROWS, 256,
-                            v.mode * w.Nh, 16)
+        pl = variant_plan(w.dims(), cnn.CNN_BF16, cnn.K_SROWS, 256, v.mode * w.Nh, 16, v.variant)
         say(f"[parity] srows strided v{pl.variant} tp={pl.tp} grid={pl.grid}")
         got = run(In, Ker, 2, 2, "bf16", plan=pl)
         nw, cond, _ = errors(got, want, absv)
