@@ -9,6 +9,10 @@ Contents
 * ``conv_oracle.c`` -- plain fp64 seven-loop direct convolution (paper,
   Sec. 1 CNN equation and Listing 1, strides restored), built into
   ``liboracle.so`` with gcc and called through ctypes here.
+* ``conv_lib`` -- the same definition evaluated by a library routine
+  (PyTorch's CPU convolution in fp64), for comparing every output of the
+  full-size workloads in seconds; pinned element by element to the loop nest
+  above by the CPU tests.
 * ``eq1`` -- the paper's data-movement cost, Eq. (1), its relaxed form
   Eq. (4), the Case 1a closed form and Table 1 (Sec. 2.1), written out in
   Python.
@@ -151,3 +155,24 @@ def conv_points(In: np.ndarray, Ker: np.ndarray, idx: np.ndarray,
     if rc != 0:
         raise ValueError(f"oracle: cnn_oracle_points returned {rc}")
     return (out, absv) if with_abs else out
+
+
+def conv_lib(In: np.ndarray, Ker: np.ndarray, sw: int = 1, sh: int = 1,
+             with_abs: bool = False):
+    """The Sec. 1 CNN equation (valid convolution, strides sw, sh) through
+    PyTorch's fp64 CPU convolution, which computes the same cross-correlation
+    sum Out[b][k][w][h] = sum_{c,r,s} In[b][c][sw*w+r][sh*h+s] Ker[k][c][r][s]
+    (no kernel flip).  The optional second result is sum |In * Ker|, the same
+    routine on |In| and |Ker|.  Only the summation order differs from
+    ``conv``; the CPU tests hold the two equal output by output."""
+    import torch
+    In64 = np.ascontiguousarray(widen(In))
+    Ker64 = np.ascontiguousarray(widen(Ker))
+    _dims(In64, Ker64, sw, sh)
+    ti, tk = torch.from_numpy(In64), torch.from_numpy(Ker64)
+    with torch.no_grad():
+        out = torch.nn.functional.conv2d(ti, tk, stride=(sw, sh)).numpy()
+        if not with_abs:
+            return out
+        absv = torch.nn.functional.conv2d(ti.abs(), tk.abs(), stride=(sw, sh)).numpy()
+    return out, absv

@@ -3,8 +3,9 @@ cnn_fwd with the automatic plan, and the plan cnn_plan_find measures to be
 fastest (the one the benchmark times, through cnn_fwd_plan_ws when it needs
 a workspace).
 
-Every output of every workload is compared with the fp64 oracle's (computed
-once per workload on the host's cores), against the normwise and the
+Every output of every workload is compared with the fp64 oracle's (its
+library-convolution route, computed once per workload on the host's cores
+and pinned to the loop nest by the CPU tests), against the normwise and the
 componentwise-conditioned bars.  A checksum identity, which holds at any
 size, is checked as well:
     sum_{b,k,w,h} Out = sum_{c,r,s} (sum_k Ker[k,c,r,s]) * (sum_{b,w,h} In[b,c,sw*w+r,sh*h+s]).
@@ -28,8 +29,8 @@ def _oracle_full(name):
     output (one workload held at a time)."""
     w = inputs.BY_NAME[name]
     In, Ker = inputs.make_inputs(w)
-    say(f"[workload] oracle {name}: {w.flops / 1e9:.2f} GFLOP on {oracle.threads()} threads")
-    want, absv = oracle.conv(In, Ker, w.sw, w.sh, with_abs=True)
+    say(f"[workload] oracle {name}: {w.flops / 1e9:.2f} GFLOP")
+    want, absv = oracle.conv_lib(In, Ker, w.sw, w.sh, with_abs=True)
     return In, Ker, want, absv
 
 

@@ -230,3 +230,35 @@ def test_bad_extent_rejected():
     with pytest.raises(ValueError):
         oracle.conv_points(np.zeros((1, 1, 4, 4)), np.zeros((1, 1, 3, 3)),
                            np.array([[0, 0, 2, 0]]), 1, 1)
+
+
+@pytest.mark.parametrize("case", _shape_cases())
+def test_library_route_matches_loop_nest(case):
+    """conv_lib (a library convolution, used for every output of the
+    full-size workloads) equals the loop nest output by output, Abs too."""
+    Nb, Nc, Nk, Nw, Nh, Nr, Ns, sw, sh, Nx, Ny = _dims_of(case)
+    rng = np.random.default_rng(7 + hash(case) % 2**31)
+    In = _rand((Nb, Nc, Nx, Ny), rng, "int")
+    Ker = _rand((Nk, Nc, Nr, Ns), rng, "int")
+    got, got_abs = oracle.conv_lib(In, Ker, sw, sh, with_abs=True)
+    want, want_abs = oracle.conv(In, Ker, sw, sh, with_abs=True)
+    assert np.array_equal(got, want) and np.array_equal(got_abs, want_abs)
+
+
+@pytest.mark.parametrize("name", [w.name for w in inputs.WORKLOADS])
+def test_library_route_at_full_size(name):
+    """At every benchmark workload's full size, conv_lib agrees with the loop
+    nest's single-point route on a sample of outputs (corners included) to
+    fp64 rounding of sum |In * Ker|."""
+    w = inputs.BY_NAME[name]
+    In, Ker = inputs.make_inputs(w)
+    got, got_abs = oracle.conv_lib(In, Ker, w.sw, w.sh, with_abs=True)
+    rng = np.random.default_rng(11)
+    idx = np.stack([rng.integers(0, m, size=300) for m in (w.Nb, w.Nk, w.Nw, w.Nh)], axis=1)
+    corners = np.array(list(itertools.product((0, w.Nb - 1), (0, w.Nk - 1),
+                                              (0, w.Nw - 1), (0, w.Nh - 1))))
+    idx = np.concatenate([idx, corners])
+    want, want_abs = oracle.conv_points(In, Ker, idx, w.sw, w.sh, with_abs=True)
+    sel = (idx[:, 0], idx[:, 1], idx[:, 2], idx[:, 3])
+    assert np.all(np.abs(got[sel] - want) <= 1e-13 * want_abs)
+    assert np.allclose(got_abs[sel], want_abs, rtol=1e-13, atol=0)
