@@ -67,9 +67,10 @@ def kernel_source_hash(family: str) -> str:
     return h.hexdigest()[:16]
 
 
-def measured_traffic(workload: str, mode: str, family: str):
+def measured_traffic(workload: str, mode: str, family: str, variant: int):
     """HBM bytes per launch from the committed rocprofv3 counter summary,
-    if it was taken on the current sources of the plan's kernel (else None)."""
+    if it was taken on the same instantiation and the current sources of
+    the plan's kernel (else None)."""
     path = os.path.join(ROOT, "profiles", "hbm_traffic.json")
     try:
         with open(path) as fh:
@@ -77,7 +78,8 @@ def measured_traffic(workload: str, mode: str, family: str):
     except (OSError, ValueError):
         return None
     rec = data.get(f"{workload}/{mode}")
-    if not rec or rec.get("source_hash") != kernel_source_hash(family):
+    if not rec or rec.get("source_hash") != kernel_source_hash(family) or \
+            rec.get("family") != family or rec.get("variant") != variant:
         return None
     return rec.get("hbm_bytes_per_launch")
 
@@ -154,7 +156,7 @@ def _counter_medians(csv_dir: str, counter: str):
 
 
 def summarize_counters(pmc_dir: str, workload: str, mode: str, copy_bytes: int, commands,
-                       family: str):
+                       family: str, variant: int):
     """Write profiles/hbm_traffic.json from four rocprofv3 --pmc passes under
     pmc_dir: conv_fetch / conv_write (FETCH_SIZE / WRITE_SIZE of this bench
     with a forced plan) and copy_fetch / copy_write (the same counters on a
@@ -185,7 +187,8 @@ def summarize_counters(pmc_dir: str, workload: str, mode: str, copy_bytes: int, 
         "fetch_scale": round(f_scale, 4), "write_scale": round(w_scale, 4),
         "hbm_fetch_bytes": round(fetch), "hbm_write_bytes": round(write),
         "hbm_bytes_per_launch": round(fetch + write),
-        "family": family, "source_hash": kernel_source_hash(family), "commands": commands}
+        "family": family, "variant": variant, "source_hash": kernel_source_hash(family),
+        "commands": commands}
     with open(path, "w") as fh:
         json.dump(data, fh, indent=1, sort_keys=True)
     print(json.dumps(data[f"{workload}/{mode}"]))
@@ -409,8 +412,6 @@ def main():
     ap.add_argument("--summarize-counters", default="",
                     help="write profiles/hbm_traffic.json from rocprofv3 --pmc passes in this "
                          "directory (conv_fetch, conv_write, copy_fetch, copy_write); no GPU")
-    ap.add_argument("--family", default="",
-                    help="with --summarize-counters: the kernel family the passes ran")
     ap.add_argument("--commands", default="",
                     help="with --summarize-counters: the commands that made the passes")
     args = ap.parse_args()
@@ -423,8 +424,12 @@ def main():
         from paper_2105_13480_amd import inputs as _inputs
         w = _inputs.BY_NAME[args.workload]
         mode = "f32" if w.dtype == "f32" else ("bf16" if args.out_dtype == "fp32" else "bf16_obf16")
+        parts = args.plan.split(":")
+        if len(parts) < 5:
+            raise SystemExit("--summarize-counters needs --plan KERNEL:TK:TP:TC:VARIANT "
+                             "(the plan the passes ran)")
         summarize_counters(args.summarize_counters, w.name, mode, args.copy_bytes,
-                           [c for c in args.commands.split(";;") if c], args.family)
+                           [c for c in args.commands.split(";;") if c], parts[0], int(parts[4]))
         return
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -468,7 +473,7 @@ def main():
     prec = "f32" if mode == "f32" else "bf16"
     tflops = w.flops / (ms * 1e-3) / 1e12
     roof = roofline(w, mode, plan, kms)
-    roof["traffic"] = measured_traffic(w.name, mode, plan.as_dict()["kernel"])
+    roof["traffic"] = measured_traffic(w.name, mode, plan.as_dict()["kernel"], plan.variant)
     try:  # Eq. (3) at the XCD / L2 level for the timed plan (a prediction)
         roof["model_hbm_bytes"] = round(sum(cnn.hbm_bytes(plan, 8, 4 << 20)))
     except cnn.CnnError:
@@ -532,7 +537,8 @@ def main():
                        "roofline": roofline(ww, md, p2, k2),
                        "plan": plan_fields(p2), "model_plan": plan_fields(mdl),
                        "model_plan_ms_ratio": None}
-                rec["roofline"]["traffic"] = measured_traffic(ww.name, md, p2.as_dict()["kernel"])
+                rec["roofline"]["traffic"] = measured_traffic(ww.name, md, p2.as_dict()["kernel"],
+                                                              p2.variant)
                 rec["roofline"]["model_hbm_bytes"] = round(p2.hbm_bytes)
                 if (mdl.kernel, mdl.variant, mdl.tp, mdl.kc) != (p2.kernel, p2.variant, p2.tp, p2.kc):
                     # the model's own choice, timed the same way

@@ -354,12 +354,12 @@ struct FamilyCost {
 
 static FamilyCost family_cost(int kernel, int variant) {
   switch (kernel) {
-    case CNN_K_ROWS: return {0.73, 5.17, 0.01, 58.0};
+    case CNN_K_ROWS: return {0.73, 6.37, 0.01, 58.0};
     case CNN_K_SROWS: {
       int n = 0;
       const VariantQ* vq = variants_srows(&n);
       for (int i = 0; i < n; ++i)  // Ker repacked on chip, one wave per SIMD
-        if (vq[i].id == variant && vq[i].form == 2) return {0.42, 4.30, 0.11, 48.3};
+        if (vq[i].id == variant && vq[i].form == 2) return {0.50, 4.30, 0.11, 48.3};
       return {0.53, 1.39, 0.11, 48.3};
     }
     case CNN_K_GEMM1: {

@@ -213,8 +213,9 @@ __global__ __launch_bounds__(64 * WAVES) void conv_rows(const bf16_t* __restrict
     int fix0[NINIT];
 #pragma unroll
     for (int j = 0; j < NINIT; ++j) v0[j] = load_block(y0, min(tid + NT * j, nb0 - 1), fix0[j]);
-    // the copies (issued first) have landed in every wave
-    asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(NINIT) : "memory");
+    // the copies have landed in every wave (copies into LDS are not
+    // counted in issue order with loads into registers: wait for all)
+    asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
     // Repack: item (octet j, feature kk), j fastest, so a 16-lane group
     // reads 8 octets of 2 features (runs 144 bytes / a feature apart: distinct
     // banks) and writes 8 consecutive planes at 2 features (plane stride PST

@@ -335,9 +335,11 @@ __global__ __launch_bounds__(64 * NWV) void conv_srows(const bf16_t* __restrict_
             (r + 1) % NR, mem);
       __builtin_amdgcn_sched_barrier(0);
       // the copy issued a stage ago (for stage + 2) has landed; this stage's
-      // copies and loads may stay in flight
+      // copies may stay in flight.  (Copies into LDS are counted in issue
+      // order among themselves but not with loads into registers, so the
+      // stage that issues In loads waits for everything.)
       if (r == 0)
-        asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(NDK + 4 * NIPT) : "memory");
+        asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
       else
         asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(NDK) : "memory");
       kcur = k1;
@@ -385,9 +387,10 @@ __global__ __launch_bounds__(64 * NWV) void conv_srows(const bf16_t* __restrict_
 // chip, so no workspace is needed; and the workgroup's 256 features are two
 // tiles of 128 taken one after the other, with two accumulator sets, so the
 // first tile's Out rows are stored while the second tile is multiplied (one
-// row per chunk) and only the second tile's drain remains after the last
-// product.  Four waves (one per SIMD): wave w takes features 32w .. 32w+31
-// of the tile for all L rows of the band.
+// row per chunk over the second tile's first L chunks, which needs at least
+// L chunks: Nc >= 16 L) and only the second tile's drain remains after the
+// last product.  Four waves (one per SIMD): wave w takes features
+// 32w .. 32w+31 of the tile for all L rows of the band.
 // * Ker, per chunk: the raw runs of the tile's 128 features are copied by
 //   16-byte buffer->LDS DMA into a raw buffer (one contiguous kilobyte per
 //   wave instruction); thread (k, g) = (tid/2, tid%2) reads its feature's
@@ -396,13 +399,21 @@ __global__ __launch_bounds__(64 * NWV) void conv_srows(const bf16_t* __restrict_
 //   B-operand units of a stencil row -- [s][g][k] planes of 136 units, so
 //   the writes of a half wave hit distinct banks -- into that row's slot.
 // * Schedule of chunk x (global over both tiles; stage r = stencil row r):
-//   stage 0 writes In(x+1) from registers and packs slot 2 for (x, 2);
-//   stage 1 reads back raw(x+1), loads In(x+2) into registers and packs
-//   slot 0 for (x+1, 0); stage 2 copies raw(x+2) by DMA, packs slot 1 for
-//   (x+1, 1) and issues 16 Out stores (a row of the first tile's
-//   accumulators during the second tile, out-of-range no-ops otherwise, so
-//   every chunk issues the same memory instructions and the wait counts are
-//   fixed).  One barrier per stage.
+//   stage 0 packs slot 2 for (x, 2) and writes In(x+1) from registers;
+//   stage 1 loads In(x+2) into them, reads back raw(x+1) and packs slot 0
+//   for (x+1, 0); stage 2 copies raw(x+2) by DMA and packs slot 1 for
+//   (x+1, 1).  In the second tile's first L chunks, stages 1 and 2 also
+//   store one row of the first tile.  One barrier per stage; the one ending
+//   stage 0 waits for all the wave's vector-memory work (the raw copies into
+//   LDS are not ordered with the In loads in the wait counter).
+// * With one wave per SIMD, a wave stalled on issue leaves its SIMD's MFMA
+//   idle: every piece of this memory work is issued singly between two of
+//   the stage's products (a stage's pieces spread evenly over its NS*L
+//   products), so the vector-memory and LDS queues never hold a burst.
+// * The range check drops a whole dword that straddles the end of In, and
+//   the loads start at any element: In's last element, loaded once, is
+//   written into its LDS unit after the item holding it (a masked 2-byte
+//   write per item and chunk; the other lanes write a scratch area).
 template <typename TO, int NR, int NS, int L>
 __global__ __launch_bounds__(256) void conv_srows2(const bf16_t* __restrict__ In,
                                                    const bf16_t* __restrict__ Ker,
@@ -418,16 +429,19 @@ __global__ __launch_bounds__(256) void conv_srows2(const bf16_t* __restrict__ In
   constexpr int NDMA = RAW_UNITS / NT;     // raw copies per thread per chunk
   constexpr int PST = TKT + 8;             // B-operand plane stride (units)
   constexpr int SLOT = NS * 2 * PST;       // units per stage slot
-  constexpr int NSTO = 16;                 // Out stores per thread per chunk
+  constexpr int NQ = NS * L;               // products per wave per stage
+  constexpr int NSTO = 16;                 // Out stores per row
+  constexpr int NSH = NSTO / 2;            // of them in each of stages 1 and 2
+  constexpr int SCRATCH_OFF = (NR * SLOT + RAW_UNITS + 2 * IN_UNITS) * 16;  // bytes
   static_assert(RAW_UNITS % NT == 0, "whole copies");
   static_assert(NR == 3 && NS <= 3, "one slot per stencil row, taps within one 64-unit row");
   static_assert(L >= 1 && L <= 7, "rows per band (two accumulator sets)");
-  static_assert(NDMA + NSTO <= 63, "wait counts");
 
   extern __shared__ __attribute__((aligned(16))) char smem[];
   u32x4_t* kslot = reinterpret_cast<u32x4_t*>(smem);  // [NR][NS][2][PST]
   u32x4_t* raw = kslot + NR * SLOT;                    // [RAW_UNITS]
   u32x4_t* ibuf = raw + RAW_UNITS;                     // [2][2][SR][64]
+  // (then a 2 KiB scratch area: writes of lanes without an item)
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -448,69 +462,63 @@ __global__ __launch_bounds__(256) void conv_srows2(const bf16_t* __restrict__ In
   const __amdgpu_buffer_rsrc_t ker_rsrc = rsrc_q(Ker, (int64_t)a.Nk * a.Nc * RS * 2);
   const __amdgpu_buffer_rsrc_t out_rsrc = rsrc_q(Out, a.out_total * (int64_t)sizeof(TO));
 
-  // ---- In items and layout: as conv_srows (slot rotation swz below).
+  // ---- In items and layout: as conv_srows (slot rotation swz below).  An
+  // item is (g, slab row j, 8-column block b8, channel half hc): four 16-byte
+  // loads (channels 8g + 4hc + 0..3 of the chunk); lanes past the last item
+  // load a duplicate and write it to the scratch area.
   const uint32_t in_last =
       __builtin_amdgcn_raw_buffer_load_b16(in_rsrc, (uint32_t)((a.in_total - 1) * 2), 0, 0);
   int in_e[NIPT];    // element offset of the item's channel 8g + 4hc of chunk 0
-  int in_dst[NIPT];  // unit of its first even column (+ 8 bytes for hc = 1)
-  int in_hc[NIPT];
+  int in_lds[NIPT];  // LDS byte offset in buffer 0 of its first even column (+ 8 for hc = 1)
+  int in_buf[NIPT];  // bytes from buffer 0 to buffer 1 (0 for scratch writes)
   int in_rot[NIPT];  // the block's slot rotation
-  bool in_ok[NIPT];
+  int last_c[NIPT];  // channel index (within the item, + 16 cc) of In's last element, or -1000
+  int last_o[NIPT];  // its LDS byte offset from the item's channel-0 position
 #pragma unroll
   for (int j = 0; j < NIPT; ++j) {
     const int t = tid + NT * j;
-    const int tt = t < NI ? t : NI - 1;
+    const bool ok = t < NI;
+    const int tt = ok ? t : NI - 1;
     const int hc = tt & 1, b8 = (tt >> 1) & 7, gj = tt >> 4;
     const int g = gj / SR, jr = gj - g * SR;
     const int x = 2 * w0 + jr;
     in_e[j] = (int)((int64_t)b * a.in_img) + (8 * g + 4 * hc) * a.nxny + x * a.Ny + 8 * b8;
-    in_dst[j] = (g * SR + jr) * 64 + 4 * b8;
-    in_hc[j] = hc;
     in_rot[j] = 2 * ((b8 >> 2) & 1) + (jr & 1);
-    in_ok[j] = t < NI;
+    in_lds[j] = ok ? (int)((ibuf - kslot) * 16) + ((g * SR + jr) * 64 + 4 * b8) * 16 + 8 * hc
+                   : SCRATCH_OFF + 16 * lane;
+    in_buf[j] = ok ? IN_UNITS * 16 : 0;
+    const int col = a.Ny - 1 - 8 * b8;
+    const bool holds = ok && b == a.Nb - 1 && x == a.Nx - 1 && col >= 0 && col < 8;
+    last_c[j] = holds ? a.Nc - 1 - 8 * g - 4 * hc : -1000;
+    last_o[j] = ((col & 1) ? 16 * 32 : 0) + 16 * (((col >> 1) + in_rot[j]) & 3);
   }
-  u32x4_t vin[NIPT][4];
-  auto load_in = [&](int cc) __attribute__((always_inline)) {
-#pragma unroll
-    for (int j = 0; j < NIPT; ++j)
-#pragma unroll
-      for (int k = 0; k < 4; ++k)
-        vin[j][k] = __builtin_bit_cast(
-            u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(
-                         in_rsrc, (uint32_t)((in_e[j] + (16 * cc + k) * a.nxny) * 2), 0, 0));
+  u32x4_t vin[NIPT][4];  // the In chunk the next stage 0 writes
+  auto load_in_one = [&](int cc, int j, int k) __attribute__((always_inline)) {
+    vin[j][k] = __builtin_bit_cast(
+        u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(
+                     in_rsrc, (uint32_t)((in_e[j] + (16 * cc + k) * a.nxny) * 2), 0, 0));
   };
-  auto write_in_part = [&](int cc, u32x4_t* dstb, int i0_, int i1_) __attribute__((always_inline)) {
-    char* base = reinterpret_cast<char*>(dstb);
-#pragma unroll
-    for (int j = 0; j < NIPT; ++j) {
-      if (!in_ok[j]) continue;
-      u32x4_t v[4] = {vin[j][0], vin[j][1], vin[j][2], vin[j][3]};
-      const int d0 = (int)(a.in_total - 1) - (in_e[j] + 16 * cc * a.nxny);
-      if (d0 >= 0 && d0 < 3 * a.nxny + 8) {
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-          const int d = d0 - k * a.nxny;
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const uint32_t lo = d == 2 * i ? ((v[k][i] & 0xffff0000u) | in_last) : v[k][i];
-            v[k][i] = d == 2 * i + 1 ? ((lo & 0xffffu) | (in_last << 16)) : lo;
-          }
-        }
-      }
-      char* p = base + in_dst[j] * 16 + 8 * in_hc[j];
-#pragma unroll
-      for (int i = i0_; i < i1_; ++i) {
-        const int slot = 16 * ((i + in_rot[j]) & 3);
-        const u32x2_t ev = {__builtin_amdgcn_perm(v[1][i], v[0][i], 0x05040100u),
-                            __builtin_amdgcn_perm(v[3][i], v[2][i], 0x05040100u)};
-        *reinterpret_cast<u32x2_t*>(p + slot) = ev;
-        if (NS > 1) {
-          const u32x2_t od = {__builtin_amdgcn_perm(v[1][i], v[0][i], 0x07060302u),
-                              __builtin_amdgcn_perm(v[3][i], v[2][i], 0x07060302u)};
-          *reinterpret_cast<u32x2_t*>(p + 16 * 32 + slot) = od;
-        }
-      }
+  // Step i of item j: column pair i of its block, units 4 b8 + i (even
+  // column) and 32 + 4 b8 + i (odd column), 8 bytes each, at their
+  // swizzled slots.
+  auto write_in_step = [&](int par, int j, int i) __attribute__((always_inline)) {
+    char* p = smem + in_lds[j] + par * in_buf[j];
+    const int slot = 16 * ((i + in_rot[j]) & 3);
+    const u32x4_t* v = vin[j];
+    const u32x2_t ev = {__builtin_amdgcn_perm(v[1][i], v[0][i], 0x05040100u),
+                        __builtin_amdgcn_perm(v[3][i], v[2][i], 0x05040100u)};
+    *reinterpret_cast<u32x2_t*>(p + slot) = ev;
+    if (NS > 1) {
+      const u32x2_t od = {__builtin_amdgcn_perm(v[1][i], v[0][i], 0x07060302u),
+                          __builtin_amdgcn_perm(v[3][i], v[2][i], 0x07060302u)};
+      *reinterpret_cast<u32x2_t*>(p + 16 * 32 + slot) = od;
     }
+  };
+  auto write_last = [&](int par, int cc, int j) __attribute__((always_inline)) {
+    const int ch = last_c[j] - 16 * cc;  // 0..3 when this item holds the element
+    const int off = (unsigned)ch < 4u ? in_lds[j] + par * in_buf[j] + last_o[j] + 2 * ch
+                                      : SCRATCH_OFF + 2 * lane;
+    *reinterpret_cast<uint16_t*>(smem + off) = (uint16_t)in_last;
   };
   auto cc_of = [&](int x) { return x < n_cc ? x : x - n_cc; };
 
@@ -522,36 +530,30 @@ __global__ __launch_bounds__(256) void conv_srows2(const bf16_t* __restrict__ In
     const int k = p / (2 * RS), q = p - k * 2 * RS;
     raw_src[j] = (uint32_t)(k * a.Nc * RS * 2 + 16 * q);
   }
-  auto copy_raw = [&](int x) __attribute__((always_inline)) {
+  auto raw_base = [&](int x) {
     const int kb = kt * 256 + (x < n_cc ? 0 : TKT);
-    const uint32_t base = (uint32_t)((kb * a.Nc + 16 * cc_of(x)) * RS * 2);
-#pragma unroll
-    for (int j = 0; j < NDMA; ++j) dma16_q(ker_rsrc, raw + j * NT + 64 * wave, base + raw_src[j]);
+    return (uint32_t)((kb * a.Nc + 16 * cc_of(x)) * RS * 2);
+  };
+  auto copy_raw_one = [&](uint32_t base, int j) __attribute__((always_inline)) {
+    dma16_q(ker_rsrc, raw + j * NT + 64 * wave, base + raw_src[j]);
   };
   u32x4_t run[RS];
-  auto read_run = [&]() __attribute__((always_inline)) {
-#pragma unroll
-    for (int q = 0; q < RS; ++q) run[q] = raw[tid * RS + q];
-  };
+  auto read_run_one = [&](int q) __attribute__((always_inline)) { run[q] = raw[tid * RS + q]; };
   const int pk = tid >> 1, pg = tid & 1;
-  // Slot of stencil row R: unit (s, g, k) = channels 8g .. 8g+7 of feature k
-  // at tap (R, s), from the run's elements (8g + i) * RS + R NS + s.
-  auto pack = [&](auto RC) __attribute__((always_inline)) {
-    constexpr int R = decltype(RC)::value;
+  // Slot of stencil row R, tap s: unit (s, g, k) = channels 8g .. 8g+7 of
+  // feature k at tap (R, s), from the run's elements (8g + i) * RS + R NS + s.
+  auto pack_tap = [&](int R, int s_) __attribute__((always_inline)) {
+    const int tap = R * NS + s_;
+    u32x4_t v;
 #pragma unroll
-    for (int s_ = 0; s_ < NS; ++s_) {
-      const int tap = R * NS + s_;
-      u32x4_t v;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int e0 = (2 * i) * RS + tap, e1 = e0 + RS;
-        const uint32_t sel =
-            ((e0 & 1) ? 0x0302u : 0x0100u) | ((e1 & 1) ? 0x07060000u : 0x05040000u);
-        v[i] = __builtin_amdgcn_perm(run[(e1 >> 1) >> 2][(e1 >> 1) & 3],
-                                     run[(e0 >> 1) >> 2][(e0 >> 1) & 3], sel);
-      }
-      kslot[R * SLOT + (s_ * 2 + pg) * PST + pk] = v;
+    for (int i = 0; i < 4; ++i) {
+      const int e0 = (2 * i) * RS + tap, e1 = e0 + RS;
+      const uint32_t sel =
+          ((e0 & 1) ? 0x0302u : 0x0100u) | ((e1 & 1) ? 0x07060000u : 0x05040000u);
+      v[i] = __builtin_amdgcn_perm(run[(e1 >> 1) >> 2][(e1 >> 1) & 3],
+                                   run[(e0 >> 1) >> 2][(e0 >> 1) & 3], sel);
     }
+    kslot[R * SLOT + (s_ * 2 + pg) * PST + pk] = v;
   };
 
   // ---- operands: A = Ker unit (s, half, feature 32 wave + l32) of a slot;
@@ -585,124 +587,128 @@ __global__ __launch_bounds__(256) void conv_srows2(const bf16_t* __restrict__ In
   // w0 + i, feature kt*256 + 128 t + 32 wave + 4 half + 8 (j/4) + j%4.  The
   // lane's part of the offset is one register; the rest (tile, row,
   // register) is wave-uniform and goes in the scalar offset.  Stores of
-  // features past Nk or positions past Nh, and the no-op stores, get an
-  // out-of-range lane offset.
+  // features past Nk or positions past Nh get an out-of-range lane offset.
   const int nhw = a.Nw * a.Nh;
   const uint32_t lane_off = (uint32_t)((4 * half * nhw + l32) * (int)sizeof(TO));
   const int feat_lane = kt * 256 + 32 * wave + 4 * half;  // + 128 t + 8 (j/4) + j%4
-  const bool pos_ok = l32 < a.Nh;
-  auto store_regs = [&](const f32x16_t& v, int t, int i, bool valid, int j0, int j1)
-      __attribute__((always_inline)) {
-    // (b, first feature of the wave's block, row w0 + i) -- wave-uniform
-    // (computed where the stores are issued: the empty asm keeps the
-    // compiler from hoisting every row's and register's offsets out of the
-    // chunk loop into registers)
-    // (no-op stores take a zero row offset: their lane offset is out of
-    // range, and lane plus scalar offset then stays within 2^31 .. 2^32)
-    uint32_t row_off = valid ? (uint32_t)(((((int64_t)b * a.Nk + kt * 256 + TKT * t + 32 * wave) *
-                                               a.Nw + w0 + i) * a.Nh) * (int64_t)sizeof(TO))
-                             : 0u;
+  const uint32_t lo = l32 < a.Nh ? lane_off : 0x80000000u;
+  auto store_one = [&](const f32x16_t& v, int t, int i, int j) __attribute__((always_inline)) {
+    // (b, first feature of the wave's block, row w0 + i): wave-uniform,
+    // computed at the store (the empty asm keeps the compiler from hoisting
+    // every row's and register's offset out of the loop into registers)
+    uint32_t row_off = (uint32_t)(((((int64_t)b * a.Nk + kt * 256 + TKT * t + 32 * wave) * a.Nw +
+                                    w0 + i) * a.Nh) * (int64_t)sizeof(TO));
     asm volatile("" : "+s"(row_off));
-    // (the lane offset with the validity folded in is made a vector value
-    // here, so the compiler selects it per lane instead of branching on the
-    // wave-uniform part, which would leave its wait counts imprecise)
-    uint32_t lo = (valid && pos_ok) ? lane_off : 0x80000000u;
-    asm volatile("" : "+v"(lo));
-    const int n_room = a.Nk - (feat_lane + TKT * t);  // features of this lane still in range
-#pragma unroll
-    for (int j = j0; j < j1; ++j) {
-      const int dj = 8 * (j >> 2) + (j & 3);
-      const uint32_t vo = dj < n_room ? lo : 0x80000000u;
-      const uint32_t so = row_off + (uint32_t)(dj * nhw * (int)sizeof(TO));
-      if constexpr (sizeof(TO) == 4)
-        __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v[j]), out_rsrc, vo, so, 0);
-      else
-        __builtin_amdgcn_raw_buffer_store_b16(from_f32<bf16_t>(v[j]), out_rsrc, vo, so, 0);
-    }
+    const int dj = 8 * (j >> 2) + (j & 3);
+    const uint32_t vo = dj < a.Nk - (feat_lane + TKT * t) ? lo : 0x80000000u;
+    const uint32_t so = row_off + (uint32_t)(dj * nhw * (int)sizeof(TO));
+    if constexpr (sizeof(TO) == 4)
+      __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v[j]), out_rsrc, vo, so, 0);
+    else
+      __builtin_amdgcn_raw_buffer_store_b16(from_f32<bf16_t>(v[j]), out_rsrc, vo, so, 0);
   };
-  // The stores chunk x issues (registers j0 .. j1-1 of one row): in the
-  // second tile, row x - n_cc of the first tile while rows remain -- always
-  // from acc[0][0], the rows being shifted down after each chunk's stores,
-  // so the code is the same in every chunk -- else out-of-range no-ops
-  // from registers no product writes at that time.
-  auto chunk_stores = [&](auto TC, int x, int j0, int j1) __attribute__((always_inline)) {
-    constexpr int TL = decltype(TC)::value;
-    if constexpr (TL == 0) {
-      store_regs(acc[1][0], 1, 0, false, j0, j1);
-    } else {
-      const int row = x - n_cc;
-      store_regs(acc[0][0], 0, row, row < L, j0, j1);
-    }
-  };
-  auto shift_rows = [&]() __attribute__((always_inline)) {
-#pragma unroll
-    for (int i = 0; i + 1 < L; ++i) acc[0][i] = acc[0][i + 1];
-  };
+
   u32x4_t KA[2], IB[2][L];
   // One stage (stencil row r of the chunk in ib) into accumulator set TL:
   // NS K-steps from operand parity P, whose step-0 operands are in
   // registers; each next step's operands -- in the last step, those of the
-  // next stage (slot nr, buffer nib) -- are read between the products.
-  // mem(slot): this stage's memory work, slot 0 first, slot s + 1 after
-  // K-step s's products.
+  // next stage (slot nr_, buffer nib) -- are read between the products.
+  // mem(q) (q = 1 .. NQ, compile-time) issues the memory work placed after
+  // product q.
   auto stage = [&](auto PC, auto TC, int r, const u32x4_t* ib, int nr_, const u32x4_t* nib,
                    auto mem) __attribute__((always_inline)) {
     constexpr int P = decltype(PC)::value;
     constexpr int TL = decltype(TC)::value;
-    mem(0);
-    __builtin_amdgcn_sched_barrier(0);
     static_for<0, NS>([&](auto SC) {
       constexpr int st = decltype(SC)::value;
       constexpr int cu = (P + st) & 1, nx = cu ^ 1;
-#pragma unroll
-      for (int i = 0; i < L; ++i) {
+      static_for<0, L>([&](auto IC) {
+        constexpr int i = decltype(IC)::value;
         acc[TL][i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
             __builtin_bit_cast(bf16x8_t, KA[cu]), __builtin_bit_cast(bf16x8_t, IB[cu][i]),
             acc[TL][i], 0, 0, 0);
         if (i == 0) KA[nx] = st + 1 < NS ? read_ka(r, st + 1) : read_ka(nr_, 0);
         IB[nx][i] = st + 1 < NS ? read_ib(ib, r, st + 1, i) : read_ib(nib, nr_, 0, i);
+        mem(std::integral_constant<int, st * L + i + 1>());
         __builtin_amdgcn_sched_barrier(0);
-      }
-      mem(st + 1);
-      __builtin_amdgcn_sched_barrier(0);
+      });
     });
   };
+  // The pieces of a stage's memory work, numbered 0 .. W-1 in issue order,
+  // go after products 1 + floor(w NQ / W): product q takes pieces
+  // [ceil((q-1) W / NQ), ceil(q W / NQ)).
+  auto spread = [&](auto QC, auto WC, auto piece) __attribute__((always_inline)) {
+    constexpr int q = decltype(QC)::value, W = decltype(WC)::value;
+    static_for<((q - 1) * W + NQ - 1) / NQ, (q * W + NQ - 1) / NQ>(piece);
+  };
 
-  // One chunk x into accumulator set TL (the three stages and their memory
-  // work; see the schedule above).
-  auto chunk = [&](auto TC, int x) __attribute__((always_inline)) {
+  // One chunk x into accumulator set TL; SROW >= 0: also store row SROW of
+  // the first tile (acc[0][SROW]) during stages 1 and 2.
+  auto chunk = [&](auto TC, auto SC, int x) __attribute__((always_inline)) {
+    constexpr int SROW = decltype(SC)::value;
+    constexpr int NST = SROW >= 0 ? NSH : 0;  // stores per stage (1 and 2)
     const int x1 = min(x + 1, n_gc - 1), x2 = min(x + 2, n_gc - 1);
+    const int c1 = cc_of(x1), c2 = cc_of(x2);
+    const int par = (x + 1) & 1;  // In buffer of chunk x + 1
     const u32x4_t* ib = ibuf + (x & 1) * IN_UNITS;
-    u32x4_t* ibn = ibuf + ((x + 1) & 1) * IN_UNITS;
-    stage(std::integral_constant<int, 0>(), TC, 0, ib, 1, ib, [&](int slot) __attribute__((always_inline)) {
-      if (slot == 0) write_in_part(cc_of(x1), ibn, 0, 2);
-      if (slot == 1) write_in_part(cc_of(x1), ibn, 2, 4);
-      if (slot == 2) pack(std::integral_constant<int, 2>());
+    const u32x4_t* ibn = ibuf + par * IN_UNITS;
+    // stage 0: the three taps of slot 2, then the item steps and
+    // last-element writes of In(x+1) (5 per item), late in the stage (their
+    // registers were loaded in the previous chunk's stage 1)
+    stage(std::integral_constant<int, 0>(), TC, 0, ib, 1, ib, [&](auto QC) __attribute__((always_inline)) {
+      spread(QC, std::integral_constant<int, 5 * NIPT + NS>(), [&](auto WC) __attribute__((always_inline)) {
+        constexpr int w = decltype(WC)::value;
+        if constexpr (w < NS) {
+          pack_tap(2, w);
+        } else {
+          constexpr int v = w - NS;
+          if constexpr (v % 5 < 4) write_in_step(par, v / 5, v % 5);
+          else write_last(par, c1, v / 5);
+        }
+      });
     });
-    __builtin_amdgcn_sched_barrier(0);
-    // raw(x + 1), copied during the previous chunk's stage 2, has landed
-    // (only that stage's stores may remain in flight)
-    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(NSTO) : "memory");
-    stage(std::integral_constant<int, (NS & 1)>(), TC, 1, ib, 2, ib, [&](int slot) __attribute__((always_inline)) {
-      if (slot == 0) {
-        read_run();
-        load_in(cc_of(x2));
-      }
-      if (slot == 2) pack(std::integral_constant<int, 0>());
+    // raw(x+1), copied during the previous chunk's stage 2, has landed.
+    // (The copies into LDS are not counted in issue order with loads into
+    // registers: waiting for fewer than all would not cover them.)
+    asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    // stage 1: In(x+2) loads, raw(x+1) read-backs and stores 0 .. NST-1 in
+    // turn (the loads first: they have until the next chunk's stage 0);
+    // then the taps of slot 0 for (x+1, 0)
+    stage(std::integral_constant<int, (NS & 1)>(), TC, 1, ib, 2, ib, [&](auto QC) __attribute__((always_inline)) {
+      constexpr int NL = 4 * NIPT;        // In loads
+      static_assert(NL <= RS && (NST == 0 || NST == NL), "stage-1 groups");
+      constexpr int G = NST > 0 ? 3 : 2;  // group g: load g, read-back g (, store g)
+      spread(QC, std::integral_constant<int, RS + NL + NST + NS>(), [&](auto WC) __attribute__((always_inline)) {
+        constexpr int w = decltype(WC)::value;
+        if constexpr (w < G * NL) {
+          constexpr int g = w / G, e = w % G;
+          if constexpr (e == 0) load_in_one(c2, g / 4, g % 4);
+          else if constexpr (e == 1) read_run_one(g);
+          else store_one(acc[0][SROW < 0 ? 0 : SROW], 0, SROW, g);
+        } else if constexpr (w < G * NL + RS - NL) {
+          read_run_one(NL + w - G * NL);
+        } else {
+          pack_tap(0, w - G * NL - (RS - NL));
+        }
+      });
     });
-    __builtin_amdgcn_sched_barrier(0);
     asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-    stage(std::integral_constant<int, ((2 * NS) & 1)>(), TC, 2, ib, 0, ibn, [&](int slot) __attribute__((always_inline)) {
-      if (slot == 0) copy_raw(x2);
-      if (slot == 1) {
-        pack(std::integral_constant<int, 1>());
-        chunk_stores(TC, x, 0, NSTO / 2);
-      }
-      if (slot == 2) chunk_stores(TC, x, NSTO / 2, NSTO);
-      if constexpr (decltype(TC)::value == 1)
-        if (slot == 3) shift_rows();
+    // stage 2: raw(x+2) copies interleaved with stores NST .. 2 NST-1, then
+    // the taps of slot 1 for (x+1, 1)
+    const uint32_t rb = raw_base(x2);
+    stage(std::integral_constant<int, ((2 * NS) & 1)>(), TC, 2, ib, 0, ibn, [&](auto QC) __attribute__((always_inline)) {
+      spread(QC, std::integral_constant<int, NDMA + NST + NS>(), [&](auto WC) __attribute__((always_inline)) {
+        constexpr int w = decltype(WC)::value;
+        if constexpr (w < 2 * NST) {
+          if constexpr (w % 2 == 0) copy_raw_one(rb, w / 2);
+          else store_one(acc[0][SROW < 0 ? 0 : SROW], 0, SROW, NST + w / 2);
+        } else if constexpr (w < NDMA + NST) {
+          copy_raw_one(rb, w - NST);
+        } else {
+          pack_tap(1, w - NDMA - NST);
+        }
+      });
     });
-    __builtin_amdgcn_sched_barrier(0);
     asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
     if constexpr (((NR * NS) & 1) != 0) {
       // a chunk has an odd number of K-steps: the next chunk's first
@@ -714,40 +720,62 @@ __global__ __launch_bounds__(256) void conv_srows2(const bf16_t* __restrict__ In
   };
 
   // ---- prologue: In(0) and raw(0) in, slots 0 and 1 packed, In(1) loads
-  // and raw(1) in flight (then the 16 no-op stores every chunk's stage 2
-  // issues, so the first chunk's wait counts are those of every chunk).
-  load_in(0);
-  copy_raw(0);
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  write_in_part(0, ibuf, 0, 4);
-  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-  read_run();
-  pack(std::integral_constant<int, 0>());
-  pack(std::integral_constant<int, 1>());
-  load_in(cc_of(min(1, n_gc - 1)));
-  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-  copy_raw(min(1, n_gc - 1));
-  chunk_stores(std::integral_constant<int, 0>(), 0, 0, NSTO);
-  KA[0] = read_ka(0, 0);
+  // and raw(1) copies in flight.
+  {
 #pragma unroll
-  for (int i = 0; i < L; ++i) IB[0][i] = read_ib(ibuf, 0, 0, i);
+    for (int j = 0; j < NIPT; ++j)
+#pragma unroll
+      for (int k = 0; k < 4; ++k) load_in_one(0, j, k);
+    const uint32_t rb0 = raw_base(0);
+#pragma unroll
+    for (int j = 0; j < NDMA; ++j) copy_raw_one(rb0, j);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+#pragma unroll
+    for (int j = 0; j < NIPT; ++j) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) write_in_step(0, j, i);
+      write_last(0, 0, j);
+    }
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+#pragma unroll
+    for (int q = 0; q < RS; ++q) read_run_one(q);
+#pragma unroll
+    for (int s_ = 0; s_ < NS; ++s_) pack_tap(0, s_);
+#pragma unroll
+    for (int s_ = 0; s_ < NS; ++s_) pack_tap(1, s_);
+    const int c1 = cc_of(min(1, n_gc - 1));
+#pragma unroll
+    for (int j = 0; j < NIPT; ++j)
+#pragma unroll
+      for (int k = 0; k < 4; ++k) load_in_one(c1, j, k);
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    const uint32_t rb1 = raw_base(min(1, n_gc - 1));
+#pragma unroll
+    for (int j = 0; j < NDMA; ++j) copy_raw_one(rb1, j);
+    KA[0] = read_ka(0, 0);
+#pragma unroll
+    for (int i = 0; i < L; ++i) IB[0][i] = read_ib(ibuf, 0, 0, i);
+  }
 
-  for (int x = 0; x < n_cc; ++x) chunk(std::integral_constant<int, 0>(), x);
-  for (int x = n_cc; x < n_gc; ++x) chunk(std::integral_constant<int, 1>(), x);
-
-  // ---- epilogue: the last tile's rows (and any first-tile rows the second
-  // tile's chunks did not reach)
+  using NOSTORE = std::integral_constant<int, -1>;
+  for (int x = 0; x < n_cc; ++x) chunk(std::integral_constant<int, 0>(), NOSTORE(), x);
   if (nt == 2) {
-    // first-tile rows n_cc .. L-1 (the second tile had fewer chunks than
-    // rows) sit in acc[0][0 .. L-1-n_cc] after n_cc shifts
+    // the second tile: its first L chunks store the first tile's rows
+    // (Nc >= 16 L), the rest store nothing
+    static_for<0, L>([&](auto JC) {
+      chunk(std::integral_constant<int, 1>(), JC, n_cc + decltype(JC)::value);
+    });
+    for (int x = n_cc + L; x < n_gc; ++x) chunk(std::integral_constant<int, 1>(), NOSTORE(), x);
+    // ---- epilogue: the second tile's rows
 #pragma unroll
     for (int i = 0; i < L; ++i)
-      if (i < L - n_cc) store_regs(acc[0][i], 0, n_cc + i, true, 0, 16);
 #pragma unroll
-    for (int i = 0; i < L; ++i) store_regs(acc[1][i], 1, i, true, 0, 16);
+      for (int j = 0; j < NSTO; ++j) store_one(acc[1][i], 1, i, j);
   } else {
 #pragma unroll
-    for (int i = 0; i < L; ++i) store_regs(acc[0][i], 0, i, true, 0, 16);
+    for (int i = 0; i < L; ++i)
+#pragma unroll
+      for (int j = 0; j < NSTO; ++j) store_one(acc[0][i], 0, i, j);
   }
 }
 
@@ -830,9 +858,9 @@ int64_t srows_slab_rows(const VariantQ& v) {
 }
 
 int64_t srows_lds_bytes(const VariantQ& v) {
-  if (v.form == 2)  // stencil-row slots, the raw chunk, two In buffers
+  if (v.form == 2)  // stencil-row slots, the raw chunk, two In buffers, scratch
     return ((int64_t)v.nr * v.ns * 2 * (128 + 8) + 128 * 2 * v.nr * v.ns +
-            2 * 2 * srows_slab_rows(v) * 64) * 16;
+            2 * 2 * srows_slab_rows(v) * 64) * 16 + 2048;
   return (4 * (int64_t)v.ns * 2 * v.tk + 2 * 2 * srows_slab_rows(v) * 64) * 16;
 }
 
@@ -848,8 +876,10 @@ int64_t srows_ws_bytes(const VariantQ& v, const cnn_problem& p) {
 
 bool srows_fits(const VariantQ& v, const cnn_problem& p) {
   const int64_t Ny = 2 * (p.Nh - 1) + p.Ns;
+  // (the raw-Ker form stores the first tile's L rows during the second
+  // tile's first L chunks: Nc >= 16 L)
   return p.sw == 2 && p.sh == 2 && p.Nr == v.nr && p.Ns == v.ns && p.Nc % 16 == 0 &&
-         p.Nh <= 32 && Ny <= 64 && p.Nw % v.L == 0;
+         p.Nh <= 32 && Ny <= 64 && p.Nw % v.L == 0 && (v.form != 2 || p.Nc >= 16 * v.L);
 }
 
 template <int DT, int NR, int NS, int L, int NWV, int FORM>

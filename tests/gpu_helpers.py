@@ -107,12 +107,11 @@ def variant_plan(dims, dt, kernel, tk, tp, tc, vid, bud=None):
             return pl
     except cnn.CnnError:
         pl = None
-    for c in cnn.plan_candidates(prob, dt, bud):
-        if c.variant == vid and c.kernel == kernel and c.tk == tk and (tp == 0 or c.tp == tp or
-                                                                       kernel != cnn.K_SROWS):
-            if pl is None or c.tp == pl.tp:
-                return c
-    return None
+    match = [c for c in cnn.plan_candidates(prob, dt, bud)
+             if c.variant == vid and c.kernel == kernel and c.tk == tk and
+             (tp == 0 or c.tp == tp or kernel != cnn.K_SROWS)]
+    same = [c for c in match if pl is not None and c.tp == pl.tp]
+    return (same or match or [None])[0]
 
 
 def _fits(dims, dt, kernel, tk, tp, tc, vid):
@@ -123,8 +122,9 @@ def _variant_dims_one(kernel, vid, dt, tk, tp, tc, stencil):
     Nr, Ns = stencil
     if kernel == cnn.K_ROWS:
         return rows_dims(vid, dt, stencil)
-    if kernel == cnn.K_SROWS:  # stride 2, Nc % 16 == 0, L | Nw
-        for dims in [(2, 32, 300, 7, 28, Nr, Ns, 2, 2), (3, 16, 64, 8, 12, Nr, Ns, 2, 2)]:
+    if kernel == cnn.K_SROWS:  # stride 2, Nc % 16 == 0, L | Nw (raw-Ker form: Nc >= 16 L)
+        for dims in [(2, 32, 300, 7, 28, Nr, Ns, 2, 2), (3, 16, 64, 8, 12, Nr, Ns, 2, 2),
+                     (2, 128, 300, 28, 14, Nr, Ns, 2, 2)]:
             if _fits(dims, dt, kernel, tk, 0, tc, vid):
                 return dims
         return None
