@@ -316,6 +316,16 @@ static bool eval_srows(const cnn_problem& p, int dtype, const VariantQ& v, const
   // a 32-position MFMA block per output row
   plan->mfma_flops = 2.0 * (double)(ceil_div(p.Nk, v.tk) * v.tk) * (double)(p.Nb * p.Nw * 32) *
                      (double)(p.Nc * p.Nr * p.Ns);
+  if (v.form == 2) {
+    // the raw-Ker form walks its 256 features as two 128-feature tiles in
+    // turn, each streaming the band's In again: Eq. (1)'s In term is that
+    // of 128-feature tiles
+    double t[3];
+    slab_terms(p, 128, v.L * p.Nh, t);
+    plan->eq1_elems[2] = t[2];
+    plan->eq1_bytes = out_bytes(dtype) * plan->eq1_elems[0] +
+                      in_bytes(dtype) * (plan->eq1_elems[1] + plan->eq1_elems[2]);
+  }
   return true;
 }
 
@@ -517,6 +527,16 @@ void hbm_terms(const cnn_plan_t& pl, int64_t xcds, int64_t l2, double terms[3]) 
   terms[0] = e_out * out + (pl.kernel == CNN_K_SPLITC ? 8.0 * pl.kc * out : 0.0);
   terms[1] = ker_b;
   terms[2] = in_b;
+  if (pl.kernel == CNN_K_SROWS) {
+    // the raw-Ker form streams a band's In once per 128-feature tile, the
+    // tiles one after the other: its XCD's bands (tens of 100-KiB-scale
+    // slabs) do not stay in the L2 from one tile to the next
+    int n = 0;
+    const VariantQ* vq = variants_srows(&n);
+    for (int i = 0; i < n; ++i)
+      if (vq[i].id == pl.variant && vq[i].form == 2)
+        terms[2] *= (double)ceil_div(p.Nk, 128) / (double)ceil_div(p.Nk, 256);
+  }
 }
 
 // Table 1 of Sec. 2.1: the closed-form optimum of Eq. (4).  The relaxed
