@@ -396,8 +396,9 @@ __global__ __launch_bounds__(64 * NWV) void conv_srows(const bf16_t* __restrict_
 //   wave instruction); thread (k, g) = (tid/2, tid%2) reads its feature's
 //   8-channel run (RS units, conflict free) back into registers and, one
 //   stage ahead of its use (two stages before it is read), writes the three
-//   B-operand units of a stencil row -- [s][g][k] planes of 136 units, so
-//   the writes of a half wave hit distinct banks -- into that row's slot.
+//   B-operand units of a stencil row -- [s][g][k] planes of 132 units, so
+//   the two g planes of 8 consecutive lanes' writes start 16 banks apart
+//   (measured faster than 136) -- into that row's slot.
 // * Schedule of chunk x (global over both tiles; stage r = stencil row r):
 //   stage 0 packs slot 2 for (x, 2) and writes In(x+1) from registers;
 //   stage 1 loads In(x+2) into them, reads back raw(x+1) and packs slot 0
@@ -427,7 +428,7 @@ __global__ __launch_bounds__(256) void conv_srows2(const bf16_t* __restrict__ In
   constexpr int IN_UNITS = 2 * SR * 64;    // 16-byte units per In buffer
   constexpr int RAW_UNITS = TKT * 2 * RS;  // raw Ker of a chunk: 128 x 16 channels x RS
   constexpr int NDMA = RAW_UNITS / NT;     // raw copies per thread per chunk
-  constexpr int PST = TKT + 8;             // B-operand plane stride (units)
+  constexpr int PST = TKT + 4;             // B-operand plane stride (units)
   constexpr int SLOT = NS * 2 * PST;       // units per stage slot
   constexpr int NQ = NS * L;               // products per wave per stage
   constexpr int NSTO = 16;                 // Out stores per row
@@ -520,7 +521,9 @@ __global__ __launch_bounds__(256) void conv_srows2(const bf16_t* __restrict__ In
                                       : SCRATCH_OFF + 2 * lane;
     *reinterpret_cast<uint16_t*>(smem + off) = (uint16_t)in_last;
   };
-  auto cc_of = [&](int x) { return x < n_cc ? x : x - n_cc; };
+  // the second tile walks the chunks in reverse: its first chunks are the
+  // ones the first tile read last, still in the L2
+  auto cc_of = [&](int x) { return x < n_cc ? x : 2 * n_cc - 1 - x; };
 
   // ---- Ker: raw copies, read-back, repack.
   uint32_t raw_src[NDMA];  // byte offset of this thread's pieces, feature base 0, chunk 0
@@ -859,7 +862,7 @@ int64_t srows_slab_rows(const VariantQ& v) {
 
 int64_t srows_lds_bytes(const VariantQ& v) {
   if (v.form == 2)  // stencil-row slots, the raw chunk, two In buffers, scratch
-    return ((int64_t)v.nr * v.ns * 2 * (128 + 8) + 128 * 2 * v.nr * v.ns +
+    return ((int64_t)v.nr * v.ns * 2 * (128 + 4) + 128 * 2 * v.nr * v.ns +
             2 * 2 * srows_slab_rows(v) * 64) * 16 + 2048;
   return (4 * (int64_t)v.ns * 2 * v.tk + 2 * 2 * srows_slab_rows(v) * 64) * 16;
 }
