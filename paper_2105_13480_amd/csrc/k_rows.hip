@@ -199,8 +199,7 @@ __global__ __launch_bounds__(64 * WAVES) void conv_rows(const bf16_t* __restrict
   if constexpr (RAWST) {
     // The tile's raw rows Ker[k0 .. k0+63][Nc][RS] are one contiguous run
     // of 16-byte chunks: copied into the ring by DMA, one kilobyte per wave
-    // instruction (features past Nk read as zeros).  The first group's rows
-    // are loaded into registers meanwhile.
+    // instruction (features past Nk read as zeros).
     {
       char* raw = reinterpret_cast<char*>(rows);
       const int nch = TK * a.Nc * RS / 8;
@@ -208,14 +207,16 @@ __global__ __launch_bounds__(64 * WAVES) void conv_rows(const bf16_t* __restrict
       for (int q = 0; q * NT < nch; ++q)
         dma16_r(ker_rsrc, raw + (NT * q + 64 * wave) * 16, kbase + (uint32_t)(NT * q + tid) * 16u);
     }
+    // the copies have landed in every wave; the first group's rows are
+    // requested only then (a wait covering the copies would otherwise
+    // cover them too: copies into LDS are not counted in issue order with
+    // loads into registers), and arrive while the tile is repacked
+    asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
     const int nb0 = (min(WR, Lb) + NR - 1) * row_blocks;
     u32x4_t v0[NINIT];
     int fix0[NINIT];
 #pragma unroll
     for (int j = 0; j < NINIT; ++j) v0[j] = load_block(y0, min(tid + NT * j, nb0 - 1), fix0[j]);
-    // the copies have landed in every wave (copies into LDS are not
-    // counted in issue order with loads into registers: wait for all)
-    asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
     // Repack: item (octet j, feature kk), j fastest, so a 16-lane group
     // reads 8 octets of 2 features (runs 144 bytes / a feature apart: distinct
     // banks) and writes 8 consecutive planes at 2 features (plane stride PST
