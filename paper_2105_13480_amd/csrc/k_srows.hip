@@ -335,13 +335,14 @@ __global__ __launch_bounds__(64 * NWV) void conv_srows(const bf16_t* __restrict_
             (r + 1) % NR, mem);
       __builtin_amdgcn_sched_barrier(0);
       // the copy issued a stage ago (for stage + 2) has landed; this stage's
-      // copies may stay in flight.  (Copies into LDS are counted in issue
-      // order among themselves but not with loads into registers, so the
-      // stage that issues In loads waits for everything.)
-      if (r == 0)
-        asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
-      else
-        asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(NDK) : "memory");
+      // copies may stay in flight.  Copies into LDS complete in issue order
+      // among themselves, but a load into registers issued after a copy may
+      // complete before it.  So the wait is stated over copies alone: each
+      // wave issued NDK copies after the ones waited for, and while any
+      // earlier copy is outstanding, so are those NDK, so vmcnt <= NDK
+      // implies the earlier copies are done, whatever In loads (issued in
+      // stage 0 of each chunk) are still in flight.
+      asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(NDK) : "memory");
       kcur = k1;
     });
     if constexpr (((NR * NS) & 1) != 0) {
@@ -791,12 +792,12 @@ __global__ __launch_bounds__(256) void conv_srows2(const bf16_t* __restrict__ In
 // RS taps are one 16-byte-aligned run of RS 16-byte blocks, transposed in
 // registers (v_perm) into RS units.
 template <int RS>
-__global__ __launch_bounds__(256) void pack_ker_srows(const bf16_t* __restrict__ Ker,
+__global__ __launch_bounds__(64) void pack_ker_srows(const bf16_t* __restrict__ Ker,
                                                       u32x4_t* __restrict__ P, ConvArgs a,
                                                       int blk_vecs) {
   constexpr int TK = 256;
   const int n_cc = a.Nc / 16;
-  const int t = blockIdx.x * 256 + threadIdx.x;
+  const int t = blockIdx.x * 64 + threadIdx.x;
   if (t >= a.n_ktiles * n_cc * 2 * TK) return;
   const int kk = t % TK, g = (t / TK) & 1, blk = t / (2 * TK);
   const int kt = blk / n_cc, cc = blk - kt * n_cc;
@@ -901,7 +902,7 @@ static hipError_t launch_q(const void* In, const void* Ker, void* Out, void* ws,
   } else {
     const int blk = (int)srows_blk_vecs(v);
     const int64_t threads = (int64_t)a.n_ktiles * (a.Nc / 16) * 2 * 256;
-    hipLaunchKernelGGL(pack_ker_srows<NR * NS>, dim3((unsigned)((threads + 255) / 256)), dim3(256),
+    hipLaunchKernelGGL(pack_ker_srows<NR * NS>, dim3((unsigned)((threads + 63) / 64)), dim3(64),
                        0, stream, (const bf16_t*)Ker, (u32x4_t*)ws, a, blk);
     auto kern = conv_srows<TO, NR, NS, L, NWV>;
     {
