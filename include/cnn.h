@@ -113,13 +113,16 @@ typedef enum cnn_kernel {
   CNN_K_SROWS = 12,   /* stride-2 layers over bands of whole output rows, bf16:
                          256 features x L rows per workgroup, In rows split by
                          column parity into MFMA-ready LDS units, one stencil
-                         row of Ker per stage.  Two forms (cnn_variants):
+                         row of Ker per stage.  Three forms (cnn_variants):
                          Ker repacked per call into the workspace and copied
-                         by DMA (8 waves, one tile of 256 features); or raw
-                         Ker rows copied by DMA and repacked in registers on
-                         chip, no workspace (4 waves, two tiles of 128
-                         features in turn, the first tile's Out written while
-                         the second computes); fixed 3x3, Nc % 16 == 0,
+                         by DMA (8 waves, one tile of 256 features); the same
+                         workspace read straight into the B-operand
+                         registers (4 waves, one tile of 256 features, LDS
+                         for In only); or raw Ker rows copied by DMA and
+                         repacked in registers on chip, no workspace (4
+                         waves, two tiles of 128 features in turn, the first
+                         tile's Out written while the second computes); fixed
+                         3x3, Nc % 16 == 0,
                          Nh <= 32, Ny <= 64, L | Nw; tp of its plans is L*Nh
                          (cnn_plan_tiles: tp = L*Nh, or 0 for any L)           */
   CNN_K_SPLITC = 13,  /* the paper's Case 2 (Sec. 2.1, W_c < N_c; the partial Outs

@@ -161,7 +161,8 @@ struct VariantQ {
   int32_t L;       // output rows per band
   int32_t waves;   // 4 or 8
   int32_t acc;     // fp32 accumulators per lane
-  int32_t form;    // 1: packed Ker in a workspace; 2: raw Ker repacked on chip
+  int32_t form;    // 1: packed Ker in a workspace, via LDS; 2: raw Ker repacked on chip;
+                   // 3: packed Ker in a workspace, B operands in registers
 };
 const VariantQ* variants_srows(int* count);
 int64_t srows_slab_rows(const VariantQ& v);

@@ -783,6 +783,287 @@ __global__ __launch_bounds__(256) void conv_srows2(const bf16_t* __restrict__ In
   }
 }
 
+// ---- register-Ker form ---------------------------------------------------------
+// conv_srows3: the same bands, In staging and operand layout as conv_srows,
+// with Ker's B operands loaded from the packed image (the workspace, read
+// through the L2) straight into registers instead of through LDS.  Every
+// global access is then a load into registers or a store: no copy into LDS
+// has to be waited for, so no stage ends on a wait for vector memory, and
+// the In loads of a chunk, issued a whole chunk before their rows are
+// written into LDS, stay in flight across stage boundaries.  LDS holds only
+// the two In buffers.
+// * Waves: four, one per SIMD; wave w takes features 64w .. 64w+63 (two
+//   32-feature blocks) for all L rows of the band, accumulators in AGPRs.
+// * Ker: stencil row r's three B-operand units of a block (one per tap, 16
+//   bytes per lane, a wave's load of one unit reads 512 contiguous bytes
+//   per channel group) live in register set r; after the products of tap s
+//   of (chunk, r), the set's tap-s units are reloaded for (chunk + 1, r),
+//   three stages ahead.
+// * In: the next chunk's rows are written item by item in stages 0 (item
+//   0) and 1 (item 1); each item's loads for the chunk after follow its
+//   writes.  Barriers after stage 1 (the next chunk's rows are complete)
+//   and after stage 2 (this chunk's rows are no longer read).
+template <typename TO, int NR, int NS, int L>
+__global__ __launch_bounds__(256) void conv_srows3(const bf16_t* __restrict__ In,
+                                                   const u32x4_t* __restrict__ Kp,
+                                                   TO* __restrict__ Out, ConvArgs a,
+                                                   int blk_vecs) {
+  constexpr int NT = 256;
+  constexpr int TK = 256;
+  constexpr int SR = 2 * (L - 1) + NR;      // slab rows held per chunk
+  constexpr int NI = 2 * SR * 8 * 2;        // In items per chunk
+  constexpr int NIPT = (NI + NT - 1) / NT;  // items per thread
+  constexpr int IN_UNITS = 2 * SR * 64;     // 16-byte units per In buffer
+  constexpr int KER_UNITS = NS * 2 * TK;    // units of one stencil row's slice
+  constexpr int NQ = NS * L;                // product pairs per wave per stage
+  constexpr int SCRATCH_OFF = 2 * IN_UNITS * 16;  // bytes
+  static_assert(NR == 3 && NS <= 3, "one register set per stencil row, taps within one 64-unit row");
+  static_assert(NIPT == 2, "two In items per thread: one written in stage 0, one in stage 1");
+  static_assert(L >= 1 && L <= 7, "rows per band");
+
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  u32x4_t* ibuf = reinterpret_cast<u32x4_t*>(smem);  // [2][2][SR][64]
+  // (then a 2 KiB scratch area: writes of lanes without an item)
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // (wave-uniform)
+  const int l32 = lane & 31, half = lane >> 5;
+
+  const int n_bands = a.Nw / L;
+  const int tile = xcd_remap(blockIdx.x, gridDim.x);
+  const int band = tile / a.n_ktiles;
+  const int kt = tile - band * a.n_ktiles;
+  const int b = band / n_bands;
+  const int w0 = (band - b * n_bands) * L;
+  const int k0 = kt * TK;
+  const int n_cc = a.Nc / 16;
+
+  const __amdgpu_buffer_rsrc_t in_rsrc = rsrc_q(In, a.in_total * 2);
+  const __amdgpu_buffer_rsrc_t kp_rsrc =
+      rsrc_q(Kp, (int64_t)a.n_ktiles * n_cc * blk_vecs * 16);
+  const __amdgpu_buffer_rsrc_t out_rsrc = rsrc_q(Out, a.out_total * (int64_t)sizeof(TO));
+
+  // ---- In items and layout: as conv_srows2 (lanes past the last item load
+  // a duplicate and write it to the scratch area).
+  const uint32_t in_last =
+      __builtin_amdgcn_raw_buffer_load_b16(in_rsrc, (uint32_t)((a.in_total - 1) * 2), 0, 0);
+  int in_e[NIPT];    // element offset of the item's channel 8g + 4hc of chunk 0
+  int in_lds[NIPT];  // LDS byte offset in buffer 0 of its first even column (+ 8 for hc = 1)
+  int in_buf[NIPT];  // bytes from buffer 0 to buffer 1 (0 for scratch writes)
+  int in_rot[NIPT];  // the block's slot rotation
+  int last_c[NIPT];  // channel index (within the item, + 16 cc) of In's last element, or -1000
+  int last_o[NIPT];  // its LDS byte offset from the item's channel-0 position
+#pragma unroll
+  for (int j = 0; j < NIPT; ++j) {
+    const int t = tid + NT * j;
+    const bool ok = t < NI;
+    const int tt = ok ? t : NI - 1;
+    const int hc = tt & 1, b8 = (tt >> 1) & 7, gj = tt >> 4;
+    const int g = gj / SR, jr = gj - g * SR;
+    const int x = 2 * w0 + jr;
+    in_e[j] = (int)((int64_t)b * a.in_img) + (8 * g + 4 * hc) * a.nxny + x * a.Ny + 8 * b8;
+    in_rot[j] = 2 * ((b8 >> 2) & 1) + (jr & 1);
+    in_lds[j] = ok ? ((g * SR + jr) * 64 + 4 * b8) * 16 + 8 * hc : SCRATCH_OFF + 16 * lane;
+    in_buf[j] = ok ? IN_UNITS * 16 : 0;
+    const int col = a.Ny - 1 - 8 * b8;
+    const bool holds = ok && b == a.Nb - 1 && x == a.Nx - 1 && col >= 0 && col < 8;
+    last_c[j] = holds ? a.Nc - 1 - 8 * g - 4 * hc : -1000;
+    last_o[j] = ((col & 1) ? 16 * 32 : 0) + 16 * (((col >> 1) + in_rot[j]) & 3);
+  }
+  u32x4_t vin[NIPT][4];  // In rows of the chunk after the next, until written
+  auto load_in_one = [&](int cc, int j, int k) __attribute__((always_inline)) {
+    vin[j][k] = __builtin_bit_cast(
+        u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(
+                     in_rsrc, (uint32_t)((in_e[j] + (16 * cc + k) * a.nxny) * 2), 0, 0));
+  };
+  auto write_in_step = [&](int par, int j, int i) __attribute__((always_inline)) {
+    char* p = smem + in_lds[j] + par * in_buf[j];
+    const int slot = 16 * ((i + in_rot[j]) & 3);
+    const u32x4_t* v = vin[j];
+    const u32x2_t ev = {__builtin_amdgcn_perm(v[1][i], v[0][i], 0x05040100u),
+                        __builtin_amdgcn_perm(v[3][i], v[2][i], 0x05040100u)};
+    *reinterpret_cast<u32x2_t*>(p + slot) = ev;
+    if (NS > 1) {
+      const u32x2_t od = {__builtin_amdgcn_perm(v[1][i], v[0][i], 0x07060302u),
+                          __builtin_amdgcn_perm(v[3][i], v[2][i], 0x07060302u)};
+      *reinterpret_cast<u32x2_t*>(p + 16 * 32 + slot) = od;
+    }
+  };
+  auto write_last = [&](int par, int cc, int j) __attribute__((always_inline)) {
+    const int ch = last_c[j] - 16 * cc;  // 0..3 when this item holds the element
+    const int off = (unsigned)ch < 4u ? in_lds[j] + par * in_buf[j] + last_o[j] + 2 * ch
+                                      : SCRATCH_OFF + 2 * lane;
+    *reinterpret_cast<uint16_t*>(smem + off) = (uint16_t)in_last;
+  };
+
+  // ---- operands: A = Ker unit (tap s, channel group half, feature
+  // 64 wave + 32 nb + l32) from the packed image; B = In unit of band row i
+  // for stencil row r, tap s (as conv_srows).
+  auto swz = [](int u, int par) { return (u & ~3) | (((u & 3) + 2 * ((u >> 4) & 1) + par) & 3); };
+  int a_sw[NS][2];
+#pragma unroll
+  for (int s_ = 0; s_ < NS; ++s_)
+#pragma unroll
+    for (int par = 0; par < 2; ++par)
+      a_sw[s_][par] = swz(((s_ & 1) ? 32 + (s_ >> 1) : (s_ >> 1)) + l32, par);
+  const int ib_off = half * SR * 64;
+  auto read_ib = [&](const u32x4_t* ib, int r, int s_, int i) __attribute__((always_inline)) {
+    const int jr = 2 * i + r;
+    return ib[ib_off + jr * 64 + a_sw[s_][jr & 1]];
+  };
+  const uint32_t kb_lane = (uint32_t)((half * TK + 64 * wave + l32) * 16);
+  auto load_k = [&](int cc, int r, int s_, int nb) __attribute__((always_inline)) {
+    const uint32_t base = (uint32_t)(((kt * n_cc + cc) * blk_vecs + r * KER_UNITS + s_ * 2 * TK +
+                                      32 * nb) * 16);
+    return __builtin_bit_cast(u32x4_t,
+                              __builtin_amdgcn_raw_buffer_load_b128(kp_rsrc, kb_lane, base, 0));
+  };
+
+  f32x16_t acc[L][2];
+#pragma unroll
+  for (int i = 0; i < L; ++i)
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][nb][e] = 0.f;
+
+  u32x4_t KB[NR][NS][2];  // B-operand units: set r = stencil row r of the current chunk
+  u32x4_t IB[2][L];       // In operands of two consecutive K-steps
+  // One stage (chunk cc, stencil row R, In buffer ib): NS K-steps from
+  // operand parity P, whose step-0 In operands are in registers; each next
+  // step's In operands -- in the last step, those of the next stage (row
+  // nr_, buffer nib) -- are read between the products; after tap s's
+  // products, set R's tap-s units are reloaded for chunk ccn.  mem(q)
+  // (q = 1 .. NQ, compile-time) issues the memory work placed after
+  // product pair q.
+  auto stage = [&](auto PC, auto RC, const u32x4_t* ib, int nr_, const u32x4_t* nib, int ccn,
+                   auto mem) __attribute__((always_inline)) {
+    constexpr int P = decltype(PC)::value;
+    constexpr int R = decltype(RC)::value;
+    static_for<0, NS>([&](auto SC) {
+      constexpr int st = decltype(SC)::value;
+      constexpr int cu = (P + st) & 1, nx = cu ^ 1;
+      static_for<0, L>([&](auto IC) {
+        constexpr int i = decltype(IC)::value;
+#pragma unroll
+        for (int nb = 0; nb < 2; ++nb)
+          acc[i][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+              __builtin_bit_cast(bf16x8_t, KB[R][st][nb]), __builtin_bit_cast(bf16x8_t, IB[cu][i]),
+              acc[i][nb], 0, 0, 0);
+        IB[nx][i] = st + 1 < NS ? read_ib(ib, R, st + 1, i) : read_ib(nib, nr_, 0, i);
+        mem(std::integral_constant<int, st * L + i + 1>());
+        __builtin_amdgcn_sched_barrier(0);
+      });
+      KB[R][st][0] = load_k(ccn, R, st, 0);
+      KB[R][st][1] = load_k(ccn, R, st, 1);
+      __builtin_amdgcn_sched_barrier(0);
+    });
+  };
+  // The pieces of a stage's memory work, numbered 0 .. W-1 in issue order,
+  // go after product pairs 1 + floor(w NQ / W).
+  auto spread = [&](auto QC, auto WC, auto piece) __attribute__((always_inline)) {
+    constexpr int q = decltype(QC)::value, W = decltype(WC)::value;
+    static_for<((q - 1) * W + NQ - 1) / NQ, (q * W + NQ - 1) / NQ>(piece);
+  };
+  // item j of In(c1) into buffer par (four steps and the last element),
+  // then its loads of In(c2)
+  auto in_piece = [&](int j, int w, int par, int c1, int c2) __attribute__((always_inline)) {
+    if (w < 4) write_in_step(par, j, w);
+    else if (w == 4) write_last(par, c1, j);
+    else load_in_one(c2, j, w - 5);
+  };
+
+  // ---- prologue: In(0) written, In(1) loads in flight, the B operands of
+  // chunk 0 loaded.  (Stencil row 0's B loads go before In(1)'s and the
+  // other rows' after, so the loop's first waits match its steady state.)
+#pragma unroll
+  for (int j = 0; j < NIPT; ++j)
+#pragma unroll
+    for (int k = 0; k < 4; ++k) load_in_one(0, j, k);
+#pragma unroll
+  for (int s_ = 0; s_ < NS; ++s_)
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb) KB[0][s_][nb] = load_k(0, 0, s_, nb);
+#pragma unroll
+  for (int j = 0; j < NIPT; ++j) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) write_in_step(0, j, i);
+    write_last(0, 0, j);
+  }
+  {
+    const int c1 = min(1, n_cc - 1);
+#pragma unroll
+    for (int j = 0; j < NIPT; ++j)
+#pragma unroll
+      for (int k = 0; k < 4; ++k) load_in_one(c1, j, k);
+  }
+#pragma unroll
+  for (int r = 1; r < NR; ++r)
+#pragma unroll
+    for (int s_ = 0; s_ < NS; ++s_)
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb) KB[r][s_][nb] = load_k(0, r, s_, nb);
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+#pragma unroll
+  for (int i = 0; i < L; ++i) IB[0][i] = read_ib(ibuf, 0, 0, i);
+
+  for (int cc = 0; cc < n_cc; ++cc) {
+    const int c1 = min(cc + 1, n_cc - 1), c2 = min(cc + 2, n_cc - 1);
+    const int par = (cc + 1) & 1;  // In buffer of chunk cc + 1
+    const u32x4_t* ib = ibuf + (cc & 1) * IN_UNITS;
+    const u32x4_t* ibn = ibuf + par * IN_UNITS;
+    using I0 = std::integral_constant<int, 0>;
+    using I1 = std::integral_constant<int, 1>;
+    using I2 = std::integral_constant<int, 2>;
+    // stage 0: item 0 of In(cc+1), then its loads of In(cc+2)
+    stage(std::integral_constant<int, 0>(), I0(), ib, 1, ib, c1, [&](auto QC) __attribute__((always_inline)) {
+      spread(QC, std::integral_constant<int, 9>(), [&](auto WC) __attribute__((always_inline)) {
+        in_piece(0, decltype(WC)::value, par, c1, c2);
+      });
+    });
+    // stage 1: item 1
+    stage(std::integral_constant<int, (NS & 1)>(), I1(), ib, 2, ib, c1, [&](auto QC) __attribute__((always_inline)) {
+      spread(QC, std::integral_constant<int, 9>(), [&](auto WC) __attribute__((always_inline)) {
+        in_piece(1, decltype(WC)::value, par, c1, c2);
+      });
+    });
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    // stage 2: the next chunk's first In operands come from its buffer
+    stage(std::integral_constant<int, ((2 * NS) & 1)>(), I2(), ib, 0, ibn, c1, [&](auto QC) __attribute__((always_inline)) {
+      (void)QC;
+    });
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    if constexpr (((NR * NS) & 1) != 0) {
+#pragma unroll
+      for (int i = 0; i < L; ++i) IB[0][i] = IB[1][i];
+    }
+  }
+
+  // ---- epilogue: register j of block (i, nb) holds position l32 of output
+  // row w0 + i, feature k0 + 64 wave + 32 nb + 8 (j/4) + 4 half + j%4.
+#pragma unroll
+  for (int nb = 0; nb < 2; ++nb) {
+    const int nblk = k0 + 64 * wave + 32 * nb + 4 * half;
+#pragma unroll
+    for (int i = 0; i < L; ++i) {
+      const int w = w0 + i;
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        const int n = nblk + 8 * (j >> 2) + (j & 3);
+        const uint32_t vo =
+            (n < a.Nk && l32 < a.Nh)
+                ? (uint32_t)(((((int64_t)b * a.Nk + n) * a.Nw + w) * a.Nh + l32) * (int64_t)sizeof(TO))
+                : 0x80000000u;
+        if constexpr (sizeof(TO) == 4)
+          __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc[i][nb][j]), out_rsrc, vo, 0, 0);
+        else
+          __builtin_amdgcn_raw_buffer_store_b16(from_f32<bf16_t>(acc[i][nb][j]), out_rsrc, vo, 0, 0);
+      }
+    }
+  }
+}
+
 // ---- Ker repack --------------------------------------------------------------
 // Slice image of every (k tile, 16-channel chunk): unit
 // ((kt*n_cc + cc)*blk_vecs + (tap*2 + g)*TK + kk) holds channels
@@ -828,7 +1109,9 @@ __global__ __launch_bounds__(64) void pack_ker_srows(const bf16_t* __restrict__ 
 // ---- instantiation table ----------------------------------------------------
 // (id, dtype, NR, NS, L, waves, form): tk = 256, tc = 16, bands of L output
 // rows; form 1 = conv_srows (Ker repacked into a workspace by a second
-// kernel), form 2 = conv_srows2 (raw Ker, repacked on chip, no workspace).
+// kernel, copied into LDS), form 2 = conv_srows2 (raw Ker, repacked on
+// chip, no workspace), form 3 = conv_srows3 (the workspace's B operands
+// loaded into registers).
 // (Four waves -- one per feature pair, all L rows, accumulators in AGPRs --
 // time the same as eight for conv_srows on the 3x3 stride-2 layer, so only
 // eight are built of that form.)
@@ -837,6 +1120,10 @@ __global__ __launch_bounds__(64) void pack_ker_srows(const bf16_t* __restrict__ 
   X(1901, CNN_BF16, 3, 3, 4, 8, 1)        \
   X(2000, CNN_BF16_OBF16, 3, 3, 7, 8, 1)  \
   X(2001, CNN_BF16_OBF16, 3, 3, 4, 8, 1)  \
+  X(2300, CNN_BF16, 3, 3, 7, 4, 3)        \
+  X(2301, CNN_BF16, 3, 3, 4, 4, 3)        \
+  X(2400, CNN_BF16_OBF16, 3, 3, 7, 4, 3)  \
+  X(2401, CNN_BF16_OBF16, 3, 3, 4, 4, 3)  \
   X(2100, CNN_BF16, 3, 3, 7, 4, 2)        \
   X(2101, CNN_BF16, 3, 3, 4, 4, 2)        \
   X(2200, CNN_BF16_OBF16, 3, 3, 7, 4, 2)  \
@@ -862,6 +1149,8 @@ int64_t srows_slab_rows(const VariantQ& v) {
 }
 
 int64_t srows_lds_bytes(const VariantQ& v) {
+  if (v.form == 3)  // two In buffers, scratch
+    return 2 * 2 * srows_slab_rows(v) * 64 * 16 + 2048;
   if (v.form == 2)  // stencil-row slots, the raw chunk, two In buffers, scratch
     return ((int64_t)v.nr * v.ns * 2 * (128 + 4) + 128 * 2 * v.nr * v.ns +
             2 * 2 * srows_slab_rows(v) * 64) * 16 + 2048;
@@ -898,6 +1187,17 @@ static hipError_t launch_q(const void* In, const void* Ker, void* Out, void* ws,
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(kern, dim3((unsigned)a.grid), dim3(256), (unsigned)lds, stream,
                        (const bf16_t*)In, (const bf16_t*)Ker, (TO*)Out, a);
+    return hipGetLastError();
+  } else if constexpr (FORM == 3) {
+    const int blk = (int)srows_blk_vecs(v);
+    const int64_t threads = (int64_t)a.n_ktiles * (a.Nc / 16) * 2 * 256;
+    hipLaunchKernelGGL(pack_ker_srows<NR * NS>, dim3((unsigned)((threads + 63) / 64)), dim3(64),
+                       0, stream, (const bf16_t*)Ker, (u32x4_t*)ws, a, blk);
+    auto kern = conv_srows3<TO, NR, NS, L>;
+    const hipError_t e = allow_max_lds((const void*)kern);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(kern, dim3((unsigned)a.grid), dim3(256), (unsigned)lds, stream,
+                       (const bf16_t*)In, (const u32x4_t*)ws, (TO*)Out, a, blk);
     return hipGetLastError();
   } else {
     const int blk = (int)srows_blk_vecs(v);
