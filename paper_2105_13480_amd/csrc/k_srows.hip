@@ -877,10 +877,9 @@ __global__ __launch_bounds__(256) void conv_srows3(const bf16_t* __restrict__ In
         u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(
                      in_rsrc, (uint32_t)((in_e[j] + (16 * cc + k) * a.nxny) * 2), 0, 0));
   };
-  auto write_in_step = [&](int par, int j, int i) __attribute__((always_inline)) {
+  auto write_in_from = [&](const u32x4_t* v, int par, int j, int i) __attribute__((always_inline)) {
     char* p = smem + in_lds[j] + par * in_buf[j];
     const int slot = 16 * ((i + in_rot[j]) & 3);
-    const u32x4_t* v = vin[j];
     const u32x2_t ev = {__builtin_amdgcn_perm(v[1][i], v[0][i], 0x05040100u),
                         __builtin_amdgcn_perm(v[3][i], v[2][i], 0x05040100u)};
     *reinterpret_cast<u32x2_t*>(p + slot) = ev;
@@ -889,6 +888,9 @@ __global__ __launch_bounds__(256) void conv_srows3(const bf16_t* __restrict__ In
                           __builtin_amdgcn_perm(v[3][i], v[2][i], 0x07060302u)};
       *reinterpret_cast<u32x2_t*>(p + 16 * 32 + slot) = od;
     }
+  };
+  auto write_in_step = [&](int par, int j, int i) __attribute__((always_inline)) {
+    write_in_from(vin[j], par, j, i);
   };
   auto write_last = [&](int par, int cc, int j) __attribute__((always_inline)) {
     const int ch = last_c[j] - 16 * cc;  // 0..3 when this item holds the element
@@ -975,41 +977,46 @@ __global__ __launch_bounds__(256) void conv_srows3(const bf16_t* __restrict__ In
   };
 
   // ---- prologue: In(0) written, In(1) loads in flight, the B operands of
-  // chunk 0 loaded.  (Stencil row 0's B loads go before In(1)'s and the
-  // other rows' after, so the loop's first waits match its steady state.)
-#pragma unroll
-  for (int j = 0; j < NIPT; ++j)
-#pragma unroll
-    for (int k = 0; k < 4; ++k) load_in_one(0, j, k);
-#pragma unroll
-  for (int s_ = 0; s_ < NS; ++s_)
-#pragma unroll
-    for (int nb = 0; nb < 2; ++nb) KB[0][s_][nb] = load_k(0, 0, s_, nb);
-#pragma unroll
-  for (int j = 0; j < NIPT; ++j) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) write_in_step(0, j, i);
-    write_last(0, 0, j);
-  }
+  // chunk 0 loaded.  In(0) goes through registers of its own, so In(1)'s
+  // loads are issued with it; stencil row 0's B loads go before In(1)'s and
+  // the other rows' after, so the loop's first waits match its steady state.
   {
+    u32x4_t v0[NIPT][4];
+#pragma unroll
+    for (int j = 0; j < NIPT; ++j)
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        load_in_one(0, j, k);
+        v0[j][k] = vin[j][k];
+      }
+#pragma unroll
+    for (int s_ = 0; s_ < NS; ++s_)
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb) KB[0][s_][nb] = load_k(0, 0, s_, nb);
     const int c1 = min(1, n_cc - 1);
 #pragma unroll
     for (int j = 0; j < NIPT; ++j)
 #pragma unroll
       for (int k = 0; k < 4; ++k) load_in_one(c1, j, k);
+#pragma unroll
+    for (int r = 1; r < NR; ++r)
+#pragma unroll
+      for (int s_ = 0; s_ < NS; ++s_)
+#pragma unroll
+        for (int nb = 0; nb < 2; ++nb) KB[r][s_][nb] = load_k(0, r, s_, nb);
+#pragma unroll
+    for (int j = 0; j < NIPT; ++j) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) write_in_from(v0[j], 0, j, i);
+      write_last(0, 0, j);
+    }
   }
-#pragma unroll
-  for (int r = 1; r < NR; ++r)
-#pragma unroll
-    for (int s_ = 0; s_ < NS; ++s_)
-#pragma unroll
-      for (int nb = 0; nb < 2; ++nb) KB[r][s_][nb] = load_k(0, r, s_, nb);
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 #pragma unroll
   for (int i = 0; i < L; ++i) IB[0][i] = read_ib(ibuf, 0, 0, i);
 
-  for (int cc = 0; cc < n_cc; ++cc) {
-    const int c1 = min(cc + 1, n_cc - 1), c2 = min(cc + 2, n_cc - 1);
+  for (int cc = 0; cc + 1 < n_cc; ++cc) {
+    const int c1 = cc + 1, c2 = min(cc + 2, n_cc - 1);
     const int par = (cc + 1) & 1;  // In buffer of chunk cc + 1
     const u32x4_t* ib = ibuf + (cc & 1) * IN_UNITS;
     const u32x4_t* ibn = ibuf + par * IN_UNITS;
@@ -1040,27 +1047,50 @@ __global__ __launch_bounds__(256) void conv_srows3(const bf16_t* __restrict__ In
     }
   }
 
-  // ---- epilogue: register j of block (i, nb) holds position l32 of output
+  // ---- the last chunk, band row by band row: all NR x NS taps of row i
+  // (every stencil row's B operands are in registers, the chunk's In in its
+  // buffer), then row i's Out, whose stores drain while the later rows are
+  // multiplied.  Register j of block (i, nb) holds position l32 of output
   // row w0 + i, feature k0 + 64 wave + 32 nb + 8 (j/4) + 4 half + j%4.
+  auto store_row = [&](int i, int q) __attribute__((always_inline)) {
+    const int nb = q >> 4, j = q & 15;
+    const int n = k0 + 64 * wave + 32 * nb + 4 * half + 8 * (j >> 2) + (j & 3);
+    const uint32_t vo =
+        (n < a.Nk && l32 < a.Nh)
+            ? (uint32_t)(((((int64_t)b * a.Nk + n) * a.Nw + w0 + i) * a.Nh + l32) * (int64_t)sizeof(TO))
+            : 0x80000000u;
+    if constexpr (sizeof(TO) == 4)
+      __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc[i][nb][j]), out_rsrc, vo, 0, 0);
+    else
+      __builtin_amdgcn_raw_buffer_store_b16(from_f32<bf16_t>(acc[i][nb][j]), out_rsrc, vo, 0, 0);
+  };
+  {
+    constexpr int T = NR * NS;
+    const u32x4_t* ib = ibuf + ((n_cc - 1) & 1) * IN_UNITS;
+    u32x4_t AT[2][T];  // In operands of a band row's taps
 #pragma unroll
-  for (int nb = 0; nb < 2; ++nb) {
-    const int nblk = k0 + 64 * wave + 32 * nb + 4 * half;
+    for (int t = 0; t < T; ++t) AT[0][t] = read_ib(ib, t / NS, t % NS, 0);
+    static_for<0, L>([&](auto IC) {
+      constexpr int i = decltype(IC)::value;
+      static_for<0, T>([&](auto TC) {
+        constexpr int t = decltype(TC)::value;
 #pragma unroll
-    for (int i = 0; i < L; ++i) {
-      const int w = w0 + i;
+        for (int nb = 0; nb < 2; ++nb)
+          acc[i][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+              __builtin_bit_cast(bf16x8_t, KB[t / NS][t % NS][nb]),
+              __builtin_bit_cast(bf16x8_t, AT[i & 1][t]), acc[i][nb], 0, 0, 0);
+        if constexpr (i + 1 < L) AT[(i + 1) & 1][t] = read_ib(ib, t / NS, t % NS, i + 1);
+        if constexpr (i > 0) {
+          // row i-1's 32 stores, spread over row i's T steps
+          static_for<(t * 32 + T - 1) / T, ((t + 1) * 32 + T - 1) / T>([&](auto QC) {
+            store_row(i - 1, decltype(QC)::value);
+          });
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      });
+    });
 #pragma unroll
-      for (int j = 0; j < 16; ++j) {
-        const int n = nblk + 8 * (j >> 2) + (j & 3);
-        const uint32_t vo =
-            (n < a.Nk && l32 < a.Nh)
-                ? (uint32_t)(((((int64_t)b * a.Nk + n) * a.Nw + w) * a.Nh + l32) * (int64_t)sizeof(TO))
-                : 0x80000000u;
-        if constexpr (sizeof(TO) == 4)
-          __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc[i][nb][j]), out_rsrc, vo, 0, 0);
-        else
-          __builtin_amdgcn_raw_buffer_store_b16(from_f32<bf16_t>(acc[i][nb][j]), out_rsrc, vo, 0, 0);
-      }
-    }
+    for (int q = 0; q < 32; ++q) store_row(L - 1, q);
   }
 }
 
