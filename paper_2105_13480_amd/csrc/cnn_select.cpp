@@ -368,8 +368,11 @@ static FamilyCost family_cost(int kernel, int variant) {
     case CNN_K_SROWS: {
       int n = 0;
       const VariantQ* vq = variants_srows(&n);
-      for (int i = 0; i < n; ++i)  // Ker repacked on chip, one wave per SIMD
-        if (vq[i].id == variant && vq[i].form == 2) return {0.50, 4.30, 0.11, 48.3};
+      for (int i = 0; i < n; ++i) {
+        if (vq[i].id != variant) continue;
+        if (vq[i].form == 2) return {0.50, 4.30, 0.11, 48.3};   // Ker repacked on chip
+        if (vq[i].form == 3) return {0.625, 1.43, 0.11, 48.3};  // B operands in registers
+      }
       return {0.53, 1.39, 0.11, 48.3};
     }
     case CNN_K_GEMM1: {
@@ -414,8 +417,13 @@ static double model_us(const cnn_plan_t& pl, const cnn_budget& bud) {
   const double per_cu = std::ceil(wgs / cus);
   const double tc = pl.tc > 0 ? (double)pl.tc : (double)p.Nc;
   const double n_st = std::ceil(std::ceil((double)p.Nc / tc) / kc);  // stages per workgroup
-  const int64_t occ = std::max<int64_t>(
-      1, std::min<int64_t>(bud.wg_per_cu, bud.lds_bytes / std::max<int64_t>(1, pl.lds_bytes)));
+  // (a stride-2 row-band workgroup fills the register file: one wave per
+  // SIMD with accumulators in AGPRs, or two of about 256 registers each)
+  const int64_t occ =
+      pl.kernel == CNN_K_SROWS
+          ? 1
+          : std::max<int64_t>(1, std::min<int64_t>(bud.wg_per_cu,
+                                                   bud.lds_bytes / std::max<int64_t>(1, pl.lds_bytes)));
   const double rate = mfma_rate(pl.dtype) * (pl.dtype == CNN_F32 ? 1.0 : kMfmaRealBf16) *
                       clk_per_us * fc.mfma_eff;                    // flops per us per CU
   const double stage_flops = pl.mfma_flops / wgs / n_st;
