@@ -261,8 +261,49 @@ __global__ __launch_bounds__(64 * WP * WK) void conv_gemm1(const bf16_t* __restr
 
   // Epilogue: D[feature][pixel] (Ker is the A operand) -- register j of
   // block (mb, nb) holds pixel 32*(wp*MBP + mb) + l32 of the tile, feature
-  // k0 + 32*(wk*NBK + nb) + 8(j/4) + 4*half + j%4.  Each 4-byte store
-  // instruction writes 32 consecutive pixels of two features.
+  // k0 + 32*(wk*NBK + nb) + 8(j/4) + 4*half + j%4.
+  if constexpr (sizeof(TO) == 4 && 32 * NBK * TPMAX * 4 <= (2 * IN_ELEMS + 2 * KER_ELEMS) * 2) {
+    // fp32 Out of a tile inside one image: each feature's tp outputs are one
+    // run of tp/4 16-byte units; the runs go through LDS one wk group
+    // (32*NBK features) at a time and leave as 16-byte stores of
+    // consecutive units.
+    const int bi = p0 / a.hw;
+    if (a.tp % 4 == 0 && a.hw % 4 == 0 && (p0 + tp - 1) / a.hw == bi) {
+      float* stg = reinterpret_cast<float*>(smem);
+      const int upf = tp / 4;  // units per feature
+      const int64_t run0 = (int64_t)bi * a.Nk * a.hw + (p0 - bi * a.hw);
+#pragma unroll
+      for (int rho = 0; rho < WK; ++rho) {
+        if (rho > 0) lds_barrier_g();  // the previous round's reads are done
+        if (wk == rho) {
+#pragma unroll
+          for (int mb = 0; mb < MBP; ++mb) {
+            const int q = 32 * (wp * MBP + mb) + l32;
+            if (q < tp) {
+#pragma unroll
+              for (int nb = 0; nb < NBK; ++nb)
+#pragma unroll
+                for (int j = 0; j < 16; ++j)
+                  stg[(32 * nb + 8 * (j >> 2) + 4 * half + (j & 3)) * tp + q] = acc[mb][nb][j];
+            }
+          }
+        }
+        lds_barrier_g();
+        const int f0 = k0 + 32 * NBK * rho;
+        const int nf = min(32 * NBK, a.Nk - f0);
+        const int units = nf > 0 ? nf * upf : 0;
+        const u32x4_t* src = reinterpret_cast<const u32x4_t*>(stg);
+        for (int u = tid; u < units; u += NT) {
+          const int fl = u / upf, pc = u - fl * upf;
+          const uint32_t off = (uint32_t)((run0 + (int64_t)(f0 + fl) * a.hw) * 4) + 16u * (uint32_t)pc;
+          __builtin_amdgcn_raw_buffer_store_b128(src[fl * upf + pc], out_rsrc, off, 0, 0);
+        }
+      }
+      return;
+    }
+  }
+  // (otherwise each 4-byte store instruction writes 32 consecutive pixels of
+  // two features)
 #pragma unroll
   for (int mb = 0; mb < MBP; ++mb) {
     const int q = 32 * (wp * MBP + mb) + l32;  // pixel within the tile
@@ -466,6 +507,46 @@ __global__ __launch_bounds__(64 * WP * WK) void conv_gemm1d(const bf16_t* __rest
     }
   }
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the trailing (empty) copies
+
+  if constexpr (sizeof(TO) == 4 && 128 * TPMAX * 4 <= DEPTH * STAGE * 16) {
+    // fp32 Out: the tile's Out (image b, features k0 .. k0+TK-1, all hw
+    // pixels) is one contiguous run; it goes through LDS in rounds of 128
+    // features (the waves with wk in {2 rho, 2 rho + 1}) and leaves as
+    // 16-byte stores of consecutive units, whole cache lines but at the
+    // run's two ends.
+    float* stg = reinterpret_cast<float*>(smem);
+    constexpr int WPR = 128 / (32 * NBK);  // wk values per round
+    static_assert(WK % WPR == 0, "whole rounds");
+#pragma unroll
+    for (int rho = 0; rho < WK / WPR; ++rho) {
+      asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");  // LDS free
+      if (wk / WPR == rho) {
+#pragma unroll
+        for (int mb = 0; mb < MBP; ++mb) {
+          const int q = 32 * (wp * MBP + mb) + l32;
+          if (q < hw) {
+#pragma unroll
+            for (int nb = 0; nb < NBK; ++nb)
+#pragma unroll
+              for (int j = 0; j < 16; ++j) {
+                const int fl = 32 * ((wk % WPR) * NBK + nb) + 8 * (j >> 2) + 4 * half + (j & 3);
+                stg[fl * hw + q] = acc[mb][nb][j];
+              }
+          }
+        }
+      }
+      asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+      const int f0 = k0 + 128 * rho;  // first feature of the round
+      const int nf = min(128, a.Nk - f0);
+      const int units = nf > 0 ? nf * hw / 4 : 0;
+      const uint32_t base = (uint32_t)(((int64_t)b * a.Nk + f0) * hw * 4);
+      const u32x4_t* src = reinterpret_cast<const u32x4_t*>(stg);
+      for (int u = tid; u < units; u += NT)
+        __builtin_amdgcn_raw_buffer_store_b128(src[u], out_rsrc,
+                                               base + 16u * (uint32_t)u, 0, 0);
+    }
+    return;
+  }
 
   // Epilogue as in conv_gemm1: a lane holds pixel q of 16 features.
 #pragma unroll
