@@ -373,6 +373,20 @@ std::map<Key, cnn_plan_t> g_cache;
 
 namespace cnnlib {
 
+int device_cus() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return 256;
+  std::lock_guard<std::mutex> g(g_lds_mu);
+  static std::map<int, int> cus;
+  auto it = cus.find(dev);
+  if (it != cus.end()) return it->second;
+  int n = 0;
+  if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n < 1)
+    n = 256;
+  cus.emplace(dev, n);
+  return n;
+}
+
 hipError_t allow_max_lds(const void* kernel) {
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);

@@ -382,7 +382,7 @@ static FamilyCost family_cost(int kernel, int variant) {
         if (vg[i].id == variant && vg[i].s2 == 2) return {0.99, 1.22, 0.52, 50.0};  // DMA ring
       return {0.36, 1.28, 0.56, 50.1};
     }
-    case CNN_K_SMALLC: return {0.17, 4.72, 0.17, 49.7};
+    case CNN_K_SMALLC: return {0.17, 2.64, 0.17, 49.7};
     case CNN_K_IGEMM_RAWK: return {0.49, 1.67, 2.41, 29.5};
     case CNN_K_POINTWISE: return {0.98, 37.19, 0.41, 100.0};
     case CNN_K_IGEMM_PIPE: return {0.74, 3.80, 2.51, 30.2};

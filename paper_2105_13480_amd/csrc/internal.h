@@ -199,6 +199,8 @@ int fwd_plan_checked(const void* In, const void* Ker, void* Out, const cnn_probl
 // The attribute is set once per (kernel, device); later calls return at
 // once.  Thread safe.
 hipError_t allow_max_lds(const void* kernel);
+// Compute units of the current device (cached per device; 256 if the query fails).
+int device_cus();
 
 // Launchers (asynchronous; return hipGetLastError()).
 hipError_t launch_direct(const void* In, const void* Ker, void* Out, const ConvArgs& a,

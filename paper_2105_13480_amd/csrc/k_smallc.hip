@@ -58,24 +58,93 @@ __global__ __launch_bounds__(256) void conv_smallc(const bf16_t* __restrict__ In
   const int wave = tid >> 6;
   const int l32 = lane & 31, half = lane >> 5;
 
-  const int tile = xcd_remap(blockIdx.x, gridDim.x);
-  const int pt = tile / a.n_ktiles;
-  const int kt = tile - pt * a.n_ktiles;
-  const int p0 = pt * a.tp;
-  const int k0 = kt * TK;
-  const int plast = min(p0 + a.tp, a.npix) - 1;
-  const int b0 = p0 / a.hw, w0 = (p0 - b0 * a.hw) / a.Nh;
-  const int b1 = plast / a.hw, w1 = (plast - b1 * a.hw) / a.Nh;
-  const int G0 = b0 * a.Nx + a.sw * w0;                    // first slab row (flattened b, x)
-  const int S = b1 * a.Nx + a.sw * w1 + a.Nr - G0;         // slab rows
+  // ---- a contiguous run of tiles per workgroup: the Ker image is packed
+  // once per run of tiles of one k tile, and each next tile's slab loads
+  // are issued before the current tile's products.
+  const int n_tiles = a.n_ptiles * a.n_ktiles;
+  const int tpw = (n_tiles + (int)gridDim.x - 1) / (int)gridDim.x;
+  const int t_begin = xcd_remap(blockIdx.x, gridDim.x) * tpw;
+  const int t_end = min(t_begin + tpw, n_tiles);
   const int RSTR = (a.Ny + 15) & ~7;                       // LDS row stride (elements)
   const int nq = a.Nc * a.Nr;                              // (c, r) rows of the stencil
   const int nks = (nq + 1) >> 1;                           // K-steps
+  const int cpr = RSTR / 8;                                // 16-byte chunks per slab row
+  const __amdgpu_buffer_rsrc_t ir = rsrc_s(In, a.in_total * 2);
+  const uint32_t in_last =
+      t_begin < t_end ? __builtin_amdgcn_raw_buffer_load_b16(ir, (uint32_t)((a.in_total - 1) * 2), 0, 0)
+                      : 0u;
+
+  // Tile geometry: the first slab row G0 (flattened b, x) and the slab
+  // rows S of tile t (its outputs p0 .. plast).
+  struct Geo {
+    int p0, plast, k0, kt, b0, G0, S;
+  };
+  auto geo = [&](int t) {
+    Geo g;
+    const int pt = t / a.n_ktiles;
+    g.kt = t - pt * a.n_ktiles;
+    g.p0 = pt * a.tp;
+    g.k0 = g.kt * TK;
+    g.plast = min(g.p0 + a.tp, a.npix) - 1;
+    g.b0 = g.p0 / a.hw;
+    const int w0 = (g.p0 - g.b0 * a.hw) / a.Nh;
+    const int b1 = g.plast / a.hw, w1 = (g.plast - b1 * a.hw) / a.Nh;
+    g.G0 = g.b0 * a.Nx + a.sw * w0;
+    g.S = b1 * a.Nx + a.sw * w1 + a.Nr - g.G0;
+    return g;
+  };
+
+  // Slab loads: element (c, row, col) of the LDS image is In[b][c][x][col]
+  // for flattened input row G0 + row = b*Nx + x, zero for col >= Ny.  Chunk
+  // (c, row, k8) = columns 8 k8 .. +7, one unaligned 16-byte load; a thread
+  // holds chunks tid + 256 u (u < U) of the tile in flight, more in batches.
+  constexpr int U = 4;
+  u32x4_t sv[U];
+  int soff[U];
+  auto slab_load = [&](const Geo& g, int e0) __attribute__((always_inline)) {
+    const int n = a.Nc * g.S * cpr;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int e = min(e0 + tid + 256 * u, n - 1);
+      const int crow = e / cpr;
+      const int k8 = e - crow * cpr;
+      const int c = crow / g.S;
+      const int row = crow - c * g.S;
+      const int gr = g.G0 + row;
+      const int b = gr / a.Nx;
+      const int x = gr - b * a.Nx;
+      soff[u] = (int)((int64_t)b * a.in_img + (int64_t)c * a.nxny + (int64_t)x * a.Ny) + 8 * k8;
+      sv[u] = __builtin_bit_cast(
+          u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(ir, (uint32_t)(soff[u] * 2), 0, 0));
+    }
+  };
+  auto slab_write = [&](const Geo& g, int e0) __attribute__((always_inline)) {
+    const int n = a.Nc * g.S * cpr;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int e = e0 + tid + 256 * u;
+      if (e >= n) continue;
+      const int crow = e / cpr;
+      const int k8 = e - crow * cpr;
+      const int d = (int)(a.in_total - 1) - soff[u];
+      u32x4_t vv = sv[u];
+#pragma unroll
+      for (int t = 0; t < 8; t += 2) {
+        uint32_t w = vv[t >> 1];
+        if (d == t) w = (w & 0xffff0000u) | in_last;
+        if (d == t + 1) w = (w & 0xffffu) | (in_last << 16);
+        const int col = 8 * k8 + t;
+        const uint32_t keep = (col < a.Ny ? 0xffffu : 0u) | (col + 1 < a.Ny ? 0xffff0000u : 0u);
+        vv[t >> 1] = w & keep;
+      }
+      *reinterpret_cast<u32x4_t*>(slab + crow * RSTR + 8 * k8) = vv;
+    }
+  };
 
   // Ker image: vector (j, h, kk) holds Ker[k0+kk][c][r][0..7] for the
   // (c, r) row q = 2j + h, zero past Ns, nq or Nk.  All of a thread's
   // loads are issued before any is used.
-  {
+  auto load_kimg = [&](int k0) __attribute__((always_inline)) {
     const int64_t ker_total = (int64_t)a.Nk * a.Nc * a.Nr * a.Ns;
     const __amdgpu_buffer_rsrc_t kr = rsrc_s(Ker, ker_total * 2);
     const uint32_t ker_last =
@@ -114,137 +183,105 @@ __global__ __launch_bounds__(256) void conv_smallc(const bf16_t* __restrict__ In
       }
       kimg[tid + 256 * u] = vv;
     }
-  }
+  };
 
-  // Stage the slab: element (c, row, col) of the LDS image is
-  // In[b][c][x][col] for flattened input row G0 + row = b*Nx + x, zero for
-  // col >= Ny.  Chunk (c, row, k8) = columns 8 k8 .. +7, one unaligned
-  // 16-byte load; batches of U independent loads per thread.
-  {
-    const __amdgpu_buffer_rsrc_t ir = rsrc_s(In, a.in_total * 2);
-    const uint32_t in_last =
-        __builtin_amdgcn_raw_buffer_load_b16(ir, (uint32_t)((a.in_total - 1) * 2), 0, 0);
-    const int cpr = RSTR / 8;  // chunks per slab row
-    const int n = a.Nc * S * cpr;
-    constexpr int U = 4;
-    for (int e0 = 0; e0 < n; e0 += 256 * U) {
-      u32x4_t v[U];
-      int off[U];
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int e = min(e0 + tid + 256 * u, n - 1);
-        const int crow = e / cpr;
-        const int k8 = e - crow * cpr;
-        const int c = crow / S;
-        const int row = crow - c * S;
-        const int gr = G0 + row;
-        const int b = gr / a.Nx;
-        const int x = gr - b * a.Nx;
-        off[u] = (int)((int64_t)b * a.in_img + (int64_t)c * a.nxny + (int64_t)x * a.Ny) + 8 * k8;
-        v[u] = __builtin_bit_cast(
-            u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(ir, (uint32_t)(off[u] * 2), 0, 0));
-      }
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int e = e0 + tid + 256 * u;
-        if (e >= n) continue;
-        const int crow = e / cpr;
-        const int k8 = e - crow * cpr;
-        const int d = (int)(a.in_total - 1) - off[u];
-        u32x4_t vv = v[u];
-#pragma unroll
-        for (int t = 0; t < 8; t += 2) {
-          uint32_t w = vv[t >> 1];
-          if (d == t) w = (w & 0xffff0000u) | in_last;
-          if (d == t + 1) w = (w & 0xffffu) | (in_last << 16);
-          const int col = 8 * k8 + t;
-          const uint32_t keep = (col < a.Ny ? 0xffffu : 0u) | (col + 1 < a.Ny ? 0xffff0000u : 0u);
-          vv[t >> 1] = w & keep;
-        }
-        *reinterpret_cast<u32x4_t*>(slab + crow * RSTR + 8 * k8) = vv;
-      }
-    }
-  }
-  __syncthreads();
-
-  // Output side: each lane's slab position and Out offset; lanes past the
-  // tile's last output recompute and rewrite it (no store masks).
-  int pbase[NB];
-  uint32_t obyte[NB];
-#pragma unroll
-  for (int nb = 0; nb < NB; ++nb) {
-    const int p = p0 + (wave * NB + nb) * 32 + l32;
-    const int pc = p <= plast ? p : plast;
-    const int b = pc / a.hw;
-    const int q = pc - b * a.hw;
-    const int w = q / a.Nh;
-    const int h = q - w * a.Nh;
-    pbase[nb] = (b * a.Nx + a.sw * w - G0) * RSTR + a.sh * h;
-    obyte[nb] = (uint32_t)(((int64_t)(b - b0) * a.Nk * a.hw + q) * (int64_t)sizeof(TO));
-  }
-
-  f32x16_t acc[MB][NB];
-#pragma unroll
-  for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-      for (int j = 0; j < 16; ++j) acc[mb][nb][j] = 0.f;
-
-#pragma unroll
-  for (int j = 0; j < KS; ++j) {
-    if (j < nks) {
-      const int q = min(2 * j + half, nq - 1);  // past nq: weights are zero
-      const int c = q / a.Nr, r = q - (q / a.Nr) * a.Nr;
-      const int qoff = (c * S + r) * RSTR;
-      u32x4_t bv[NB];
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb) {
-        const bf16_t* src = slab + qoff + pbase[nb];
-        if constexpr (SH2) {
-          // the position's first column is even: 4-byte-aligned words
-#pragma unroll
-          for (int d = 0; d < 4; ++d) bv[nb][d] = reinterpret_cast<const uint32_t*>(src)[d];
-        } else {
-#pragma unroll
-          for (int d = 0; d < 4; ++d)
-            bv[nb][d] = (uint32_t)src[2 * d] | ((uint32_t)src[2 * d + 1] << 16);
-        }
-      }
-#pragma unroll
-      for (int mb = 0; mb < MB; ++mb) {
-        const u32x4_t av = kimg[(2 * j + half) * TK + mb * 32 + l32];
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb)
-          acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-              __builtin_bit_cast(bf16x8_t, av), __builtin_bit_cast(bf16x8_t, bv[nb]),
-              acc[mb][nb], 0, 0, 0);
-      }
-    }
-  }
-
-  // Epilogue: register j of a 32x32 accumulator holds feature
-  // 8*(j/4) + 4*half + j%4 of output l32.
-  const __amdgpu_buffer_rsrc_t out_rsrc =
-      rsrc_s(Out + (int64_t)b0 * a.Nk * a.hw,
-             (a.out_total - (int64_t)b0 * a.Nk * a.hw) * (int64_t)sizeof(TO));
   const uint32_t half_off = (uint32_t)(4 * half * a.hw * (int)sizeof(TO));
-  const bool k_full = k0 + TK <= a.Nk;
+  int kt_img = -1;  // k tile of the Ker image in LDS
+  if (t_begin < t_end) slab_load(geo(t_begin), 0);
+  for (int t = t_begin; t < t_end; ++t) {
+    const Geo g = geo(t);
+    const int n_chunks = a.Nc * g.S * cpr;
+    __syncthreads();  // the previous tile's operand reads are done
+    if (g.kt != kt_img) {
+      load_kimg(g.k0);
+      kt_img = g.kt;
+    }
+    // this tile's slab: the first batch is in flight (issued a tile ago)
+    for (int e0 = 0; e0 < n_chunks; e0 += 256 * U) {
+      if (e0 > 0) slab_load(g, e0);
+      slab_write(g, e0);
+    }
+    __syncthreads();
+    if (t + 1 < t_end) slab_load(geo(t + 1), 0);  // lands during this tile's products
+
+    // Output side: each lane's slab position and Out offset; lanes past the
+    // tile's last output recompute and rewrite it (no store masks).
+    int pbase[NB];
+    uint32_t obyte[NB];
 #pragma unroll
-  for (int mb = 0; mb < MB; ++mb) {
+    for (int nb = 0; nb < NB; ++nb) {
+      const int p = g.p0 + (wave * NB + nb) * 32 + l32;
+      const int pc = p <= g.plast ? p : g.plast;
+      const int b = pc / a.hw;
+      const int q = pc - b * a.hw;
+      const int w = q / a.Nh;
+      const int h = q - w * a.Nh;
+      pbase[nb] = (b * a.Nx + a.sw * w - g.G0) * RSTR + a.sh * h;
+      obyte[nb] = (uint32_t)(((int64_t)(b - g.b0) * a.Nk * a.hw + q) * (int64_t)sizeof(TO));
+    }
+
+    f32x16_t acc[MB][NB];
 #pragma unroll
-    for (int j = 0; j < 16; ++j) {
-      const int kw = k0 + mb * 32 + 8 * (j >> 2) + (j & 3);
-      const uint32_t so = (uint32_t)kw * (uint32_t)a.hw * (uint32_t)sizeof(TO);
-      if (k_full || kw + 4 * half < a.Nk) {
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+        for (int j = 0; j < 16; ++j) acc[mb][nb][j] = 0.f;
+
+#pragma unroll
+    for (int j = 0; j < KS; ++j) {
+      if (j < nks) {
+        const int q = min(2 * j + half, nq - 1);  // past nq: weights are zero
+        const int c = q / a.Nr, r = q - (q / a.Nr) * a.Nr;
+        const int qoff = (c * g.S + r) * RSTR;
+        u32x4_t bv[NB];
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) {
-          if constexpr (sizeof(TO) == 4) {
-            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc[mb][nb][j]), out_rsrc,
-                                                  obyte[nb] + half_off, so, 0);
+          const bf16_t* src = slab + qoff + pbase[nb];
+          if constexpr (SH2) {
+            // the position's first column is even: 4-byte-aligned words
+#pragma unroll
+            for (int d = 0; d < 4; ++d) bv[nb][d] = reinterpret_cast<const uint32_t*>(src)[d];
           } else {
-            __builtin_amdgcn_raw_buffer_store_b16(from_f32<bf16_t>(acc[mb][nb][j]), out_rsrc,
-                                                  obyte[nb] + half_off, so, 0);
+#pragma unroll
+            for (int d = 0; d < 4; ++d)
+              bv[nb][d] = (uint32_t)src[2 * d] | ((uint32_t)src[2 * d + 1] << 16);
+          }
+        }
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) {
+          const u32x4_t av = kimg[(2 * j + half) * TK + mb * 32 + l32];
+#pragma unroll
+          for (int nb = 0; nb < NB; ++nb)
+            acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                __builtin_bit_cast(bf16x8_t, av), __builtin_bit_cast(bf16x8_t, bv[nb]),
+                acc[mb][nb], 0, 0, 0);
+        }
+      }
+    }
+
+    // Epilogue: register j of a 32x32 accumulator holds feature
+    // 8*(j/4) + 4*half + j%4 of output l32.
+    const __amdgpu_buffer_rsrc_t out_rsrc =
+        rsrc_s(Out + (int64_t)g.b0 * a.Nk * a.hw,
+               (a.out_total - (int64_t)g.b0 * a.Nk * a.hw) * (int64_t)sizeof(TO));
+    const bool k_full = g.k0 + TK <= a.Nk;
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) {
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        const int kw = g.k0 + mb * 32 + 8 * (j >> 2) + (j & 3);
+        const uint32_t so = (uint32_t)kw * (uint32_t)a.hw * (uint32_t)sizeof(TO);
+        if (k_full || kw + 4 * half < a.Nk) {
+#pragma unroll
+          for (int nb = 0; nb < NB; ++nb) {
+            if constexpr (sizeof(TO) == 4) {
+              __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc[mb][nb][j]), out_rsrc,
+                                                    obyte[nb] + half_off, so, 0);
+            } else {
+              __builtin_amdgcn_raw_buffer_store_b16(from_f32<bf16_t>(acc[mb][nb][j]), out_rsrc,
+                                                    obyte[nb] + half_off, so, 0);
+            }
           }
         }
       }
@@ -288,7 +325,9 @@ static hipError_t launch_s(const void* In, const void* Ker, void* Out, const Con
     const hipError_t e = allow_max_lds((const void*)kern);
     if (e != hipSuccess) return e;
   }
-  hipLaunchKernelGGL(kern, dim3((unsigned)a.grid), dim3(256), (unsigned)lds, stream,
+  // two workgroups per CU fill the registers; each walks a run of tiles
+  const int64_t wgs = std::min<int64_t>(a.grid, 2 * (int64_t)device_cus());
+  hipLaunchKernelGGL(kern, dim3((unsigned)wgs), dim3(256), (unsigned)lds, stream,
                      (const bf16_t*)In, (const bf16_t*)Ker, (TO*)Out, a);
   return hipGetLastError();
 }

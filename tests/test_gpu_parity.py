@@ -69,6 +69,26 @@ def test_every_igemm_variant_exact_integers(case):
     assert np.array_equal(got, want)
 
 
+@pytest.mark.parametrize("mode", ["bf16", "bf16_obf16"])
+def test_smallc_runs_of_tiles_exact(mode):
+    """The few-channel kernel walks a run of tiles per workgroup (two
+    workgroups per CU): 896 tiles of two 64-feature k tiles, so each
+    workgroup takes several tiles and repacks its Ker image when the k tile
+    changes; every output compared exactly on integer inputs."""
+    dims = (32, 3, 128, 56, 56, 7, 7, 2, 2)
+    dt = cnn.DTYPES[mode]
+    In, Ker = _arrays(dims, mode, seed=77, dist=("int", -2, 2), kdist=("int", -2, 2))
+    pl = min((c for c in cnn.plan_candidates(cnn.problem(*dims), dt)
+              if c.kernel == cnn.K_SMALLC and c.tk == 64), key=lambda c: c.model_us)
+    assert pl.grid > 2 * cnn.device_budget(0).cus, "more tiles than resident workgroups"
+    say(f"[parity] smallc runs v{pl.variant} tp={pl.tp} grid={pl.grid} mode={mode}")
+    got = run(In, Ker, dims[7], dims[8], mode, plan=pl)
+    want = oracle.conv_lib(In, Ker, dims[7], dims[8], False)
+    if mode == "bf16_obf16":
+        want = inputs.bf16_bits_to_f32(inputs.f32_to_bf16_bits(want.astype(np.float32))).astype(np.float64)
+    assert np.array_equal(got, want)
+
+
 @pytest.mark.parametrize("mode", list(MODES))
 def test_direct_kernel_exact_integers(mode):
     dims = (2, 7, 9, 11, 6, 3, 2, 2, 1)
