@@ -58,21 +58,22 @@ __global__ __launch_bounds__(256) void conv_smallc(const bf16_t* __restrict__ In
   const int wave = tid >> 6;
   const int l32 = lane & 31, half = lane >> 5;
 
-  // ---- a contiguous run of tiles per workgroup: the Ker image is packed
-  // once per run of tiles of one k tile, and each next tile's slab loads
-  // are issued before the current tile's products.
+  // ---- several tiles per workgroup, strided by the grid: at any time the
+  // workgroups of an XCD work on neighbouring tiles, whose slabs share halo
+  // rows in its L2.  The Ker image is packed again only when the k tile
+  // changes, and each next tile's slab loads are issued before the current
+  // tile's products.
   const int n_tiles = a.n_ptiles * a.n_ktiles;
-  const int tpw = (n_tiles + (int)gridDim.x - 1) / (int)gridDim.x;
-  const int t_begin = xcd_remap(blockIdx.x, gridDim.x) * tpw;
-  const int t_end = min(t_begin + tpw, n_tiles);
+  const int G = (int)gridDim.x;
+  const int t_first = xcd_remap(blockIdx.x, gridDim.x);
   const int RSTR = (a.Ny + 15) & ~7;                       // LDS row stride (elements)
   const int nq = a.Nc * a.Nr;                              // (c, r) rows of the stencil
   const int nks = (nq + 1) >> 1;                           // K-steps
   const int cpr = RSTR / 8;                                // 16-byte chunks per slab row
   const __amdgpu_buffer_rsrc_t ir = rsrc_s(In, a.in_total * 2);
   const uint32_t in_last =
-      t_begin < t_end ? __builtin_amdgcn_raw_buffer_load_b16(ir, (uint32_t)((a.in_total - 1) * 2), 0, 0)
-                      : 0u;
+      t_first < n_tiles ? __builtin_amdgcn_raw_buffer_load_b16(ir, (uint32_t)((a.in_total - 1) * 2), 0, 0)
+                        : 0u;
 
   // Tile geometry: the first slab row G0 (flattened b, x) and the slab
   // rows S of tile t (its outputs p0 .. plast).
@@ -187,8 +188,8 @@ __global__ __launch_bounds__(256) void conv_smallc(const bf16_t* __restrict__ In
 
   const uint32_t half_off = (uint32_t)(4 * half * a.hw * (int)sizeof(TO));
   int kt_img = -1;  // k tile of the Ker image in LDS
-  if (t_begin < t_end) slab_load(geo(t_begin), 0);
-  for (int t = t_begin; t < t_end; ++t) {
+  if (t_first < n_tiles) slab_load(geo(t_first), 0);
+  for (int t = t_first; t < n_tiles; t += G) {
     const Geo g = geo(t);
     const int n_chunks = a.Nc * g.S * cpr;
     __syncthreads();  // the previous tile's operand reads are done
@@ -202,7 +203,7 @@ __global__ __launch_bounds__(256) void conv_smallc(const bf16_t* __restrict__ In
       slab_write(g, e0);
     }
     __syncthreads();
-    if (t + 1 < t_end) slab_load(geo(t + 1), 0);  // lands during this tile's products
+    if (t + G < n_tiles) slab_load(geo(t + G), 0);  // lands during this tile's products
 
     // Output side: each lane's slab position and Out offset; lanes past the
     // tile's last output recompute and rewrite it (no store masks).
@@ -325,7 +326,7 @@ static hipError_t launch_s(const void* In, const void* Ker, void* Out, const Con
     const hipError_t e = allow_max_lds((const void*)kern);
     if (e != hipSuccess) return e;
   }
-  // two workgroups per CU fill the registers; each walks a run of tiles
+  // two workgroups per CU fill the registers; each takes every grid-th tile
   const int64_t wgs = std::min<int64_t>(a.grid, 2 * (int64_t)device_cus());
   hipLaunchKernelGGL(kern, dim3((unsigned)wgs), dim3(256), (unsigned)lds, stream,
                      (const bf16_t*)In, (const bf16_t*)Ker, (TO*)Out, a);
