@@ -344,6 +344,9 @@ static const double kClkGHz = 2.4;
 static const double kMfmaRealBf16 = 0.64;
 static const double kHbmGBs = 5000.0;
 static const double kLaunchUs = 2.0;
+// HBM writes per byte of Out of the stride-2 row-band kernels (row-piece
+// stores, partial lines), measured with WRITE_SIZE.
+static const double kSrowsWriteRate = 1.18;
 
 // MFMA throughput per CU per clock for the dtype's operand type.
 static double mfma_rate(int dtype) { return dtype == CNN_F32 ? 256.0 : 4096.0; }
@@ -507,7 +510,10 @@ void hbm_terms(const cnn_plan_t& pl, int64_t xcds, int64_t l2, double terms[3]) 
     const int64_t t0 = x * q + std::min(x, rem), t1 = t0 + cnt;
     // input rows read: output row (b, w) reads rows b*Nx + sw*w .. + Nr - 1;
     // the output rows are visited in increasing order, so a running end
-    // counts each row once (rows between strided reads are not counted)
+    // counts each row once.  Rows between strided reads are not read, but
+    // a gap shorter than a 128-byte line shares its lines with the rows
+    // around it, which HBM delivers whole: such gaps count as read.
+    const int64_t gap_max = (int64_t)((128.0 - 1.0) / (e_in * (double)Ny));  // rows
     int64_t rows = 0, end = -1, max_slab = 0;
     for (int64_t pt = t0 / n_k; pt <= (t1 - 1) / n_k; ++pt) {
       const int64_t f = pt * tp, last = std::min(f + tp, npix) - 1;
@@ -516,7 +522,7 @@ void hbm_terms(const cnn_plan_t& pl, int64_t xcds, int64_t l2, double terms[3]) 
                                         ((r0 / p.Nw) * Nx + p.sw * (r0 % p.Nw)));
       for (int64_t r = r0; r <= r1; ++r) {
         const int64_t g0 = (r / p.Nw) * Nx + p.sw * (r % p.Nw), g1 = g0 + p.Nr;
-        const int64_t from = std::max(g0, end);
+        const int64_t from = (end >= 0 && g0 > end && g0 - end <= gap_max) ? end : std::max(g0, end);
         if (g1 > from) rows += g1 - from;
         end = std::max(end, g1);
       }
@@ -533,6 +539,11 @@ void hbm_terms(const cnn_plan_t& pl, int64_t xcds, int64_t l2, double terms[3]) 
   }
   const double out = (double)npix * (double)p.Nk;
   terms[0] = e_out * out + (pl.kernel == CNN_K_SPLITC ? 8.0 * pl.kc * out : 0.0);
+  // The stride-2 row-band kernels store Out as row pieces (Nh values per
+  // feature row) that rarely fill a 128-byte line; the L2 merges most
+  // neighbouring pieces but writes some lines twice: measured WRITE_SIZE is
+  // 17-20 % above Out on the 3x3 stride-2 layer (fp32 Out).
+  if (pl.kernel == CNN_K_SROWS) terms[0] *= kSrowsWriteRate;
   terms[1] = ker_b;
   terms[2] = in_b;
   if (pl.kernel == CNN_K_SROWS) {

@@ -454,8 +454,11 @@ def _hbm_brute(pl, xcds, l2):
     """cnn_hbm_bytes by enumeration: XCD x runs the x-th contiguous run of
     the tile index; its In traffic is every (b, x) input row that any output
     of its tiles reads with any stencil row, each once (all channels and
-    columns); its Ker traffic is each k tile it meets once (l2 large) or once
-    per tile (l2 = 1)."""
+    columns), plus the rows of every gap between two such rows (in the
+    flattened b*Nx + x order) that is shorter than a 128-byte line; its Ker
+    traffic is each k tile it meets once (l2 large) or once per tile (l2 =
+    1).  The stride-2 row-band kernels write Out at the measured rate of
+    1.18 bytes per byte."""
     p = pl.prob
     hw, npix = p.Nw * p.Nh, p.Nb * p.Nw * p.Nh
     Ny = p.sh * (p.Nh - 1) + p.Ns
@@ -477,11 +480,16 @@ def _hbm_brute(pl, xcds, l2):
             for f in range(pt * pl.tp, min((pt + 1) * pl.tp, npix)):
                 b, w = f // hw, (f % hw) // p.Nh
                 rows.update((b, p.sw * w + r) for r in range(p.Nr))
-        in_b += len(rows) * p.Nc * Ny * e_in
+        Nx = p.sw * (p.Nw - 1) + p.Nr
+        flat = sorted(b * Nx + x for b, x in rows)
+        gaps = sum(n - m - 1 for m, n in zip(flat, flat[1:])
+                   if 0 < (n - m - 1) * Ny * e_in < 128)
+        in_b += (len(rows) + gaps) * p.Nc * Ny * e_in
         ker_b += sum(ker(k) for k in kts) if l2 > 1 else per_tile
     out = npix * p.Nk
     extra = 8 * pl.kc * out if pl.kernel == cnn.K_SPLITC else 0
-    return e_out * out + extra, ker_b, in_b
+    rate = 1.18 if pl.kernel == cnn.K_SROWS else 1.0
+    return e_out * out * rate + extra, ker_b, in_b
 
 
 @pytest.mark.parametrize("dims,dt,kernel,tk,tp,tc", [
