@@ -382,7 +382,7 @@ static FamilyCost family_cost(int kernel, int variant) {
       int n = 0;
       const VariantG* vg = variants_gemm1(&n);
       for (int i = 0; i < n; ++i)
-        if (vg[i].id == variant && vg[i].s2 == 2) return {0.99, 1.22, 0.52, 50.0};  // DMA ring
+        if (vg[i].id == variant && vg[i].s2 == 2) return {0.99, 1.22, 0.40, 50.0};  // DMA ring
       return {0.36, 1.28, 0.56, 50.1};
     }
     case CNN_K_SMALLC: return {0.17, 2.64, 0.17, 49.7};

@@ -481,6 +481,10 @@ __global__ __launch_bounds__(64 * WP * WK) void conv_gemm1d(const bf16_t* __rest
     for (int nb = 0; nb < NBK; ++nb)
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[mb][nb][e] = 0.f;
+  // whether this wave's last pixel block holds a pixel of the image (the
+  // one that whole images of fewer than TPMAX - 32 pixels leave empty); if
+  // not, its products (padding, never stored) are skipped
+  const bool last_live = __builtin_amdgcn_readfirstlane(32 * (wp * MBP + MBP - 1) < hw ? 1 : 0) != 0;
 
 #pragma unroll
   for (int s = 0; s < DEPTH - 1; ++s) issue(s);
@@ -501,9 +505,10 @@ __global__ __launch_bounds__(64 * WP * WK) void conv_gemm1d(const bf16_t* __rest
       for (int mb = 0; mb < MBP; ++mb)
 #pragma unroll
         for (int nb = 0; nb < NBK; ++nb)
-          acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-              __builtin_bit_cast(bf16x8_t, B[nb]), __builtin_bit_cast(bf16x8_t, A[mb]),
-              acc[mb][nb], 0, 0, 0);
+          if (mb + 1 < MBP || last_live)
+            acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                __builtin_bit_cast(bf16x8_t, B[nb]), __builtin_bit_cast(bf16x8_t, A[mb]),
+                acc[mb][nb], 0, 0, 0);
     }
   }
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the trailing (empty) copies
