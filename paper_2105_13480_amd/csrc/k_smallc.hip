@@ -41,10 +41,18 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc_s(const void* base, int64
 
 // KS: largest number of K-steps (ceil(Nc*Nr/2)) the registers hold.  SH2:
 // sh == 2 (operands gathered with 32-bit LDS reads).
+// Dividers for the launch's runtime divisors (made on the host).
+struct SmallcDiv {
+  FastDiv cpr, nx, hw, nh, nr, kt;
+  FastDiv s0;  // slab rows of the first tile (most tiles have as many)
+  int S0;
+};
+
 template <typename TO, int NB, int KS, bool SH2>
-__global__ __launch_bounds__(256) void conv_smallc(const bf16_t* __restrict__ In,
+__global__ __launch_bounds__(256, 2) void conv_smallc(const bf16_t* __restrict__ In,
                                                    const bf16_t* __restrict__ Ker,
-                                                   TO* __restrict__ Out, ConvArgs a) {
+                                                   TO* __restrict__ Out, ConvArgs a,
+                                                   SmallcDiv dv) {
   constexpr int MB = 2;         // 64 features per tile, shared by the 4 waves
   constexpr int TK = 32 * MB;
   constexpr int KVEC = KS * 2 * TK;  // Ker image vectors
@@ -79,19 +87,21 @@ __global__ __launch_bounds__(256) void conv_smallc(const bf16_t* __restrict__ In
   // rows S of tile t (its outputs p0 .. plast).
   struct Geo {
     int p0, plast, k0, kt, b0, G0, S;
+    FastDiv fs;  // divider for S
   };
   auto geo = [&](int t) {
     Geo g;
-    const int pt = t / a.n_ktiles;
+    const int pt = fdiv(t, dv.kt);
     g.kt = t - pt * a.n_ktiles;
     g.p0 = pt * a.tp;
     g.k0 = g.kt * TK;
     g.plast = min(g.p0 + a.tp, a.npix) - 1;
-    g.b0 = g.p0 / a.hw;
-    const int w0 = (g.p0 - g.b0 * a.hw) / a.Nh;
-    const int b1 = g.plast / a.hw, w1 = (g.plast - b1 * a.hw) / a.Nh;
+    g.b0 = fdiv(g.p0, dv.hw);
+    const int w0 = fdiv(g.p0 - g.b0 * a.hw, dv.nh);
+    const int b1 = fdiv(g.plast, dv.hw), w1 = fdiv(g.plast - b1 * a.hw, dv.nh);
     g.G0 = g.b0 * a.Nx + a.sw * w0;
     g.S = b1 * a.Nx + a.sw * w1 + a.Nr - g.G0;
+    g.fs = g.S == dv.S0 ? dv.s0 : make_fastdiv((uint32_t)g.S);
     return g;
   };
 
@@ -107,12 +117,12 @@ __global__ __launch_bounds__(256) void conv_smallc(const bf16_t* __restrict__ In
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int e = min(e0 + tid + 256 * u, n - 1);
-      const int crow = e / cpr;
+      const int crow = fdiv(e, dv.cpr);
       const int k8 = e - crow * cpr;
-      const int c = crow / g.S;
+      const int c = fdiv(crow, g.fs);
       const int row = crow - c * g.S;
       const int gr = g.G0 + row;
-      const int b = gr / a.Nx;
+      const int b = fdiv(gr, dv.nx);
       const int x = gr - b * a.Nx;
       soff[u] = (int)((int64_t)b * a.in_img + (int64_t)c * a.nxny + (int64_t)x * a.Ny) + 8 * k8;
       sv[u] = __builtin_bit_cast(
@@ -125,7 +135,7 @@ __global__ __launch_bounds__(256) void conv_smallc(const bf16_t* __restrict__ In
     for (int u = 0; u < U; ++u) {
       const int e = e0 + tid + 256 * u;
       if (e >= n) continue;
-      const int crow = e / cpr;
+      const int crow = fdiv(e, dv.cpr);
       const int k8 = e - crow * cpr;
       const int d = (int)(a.in_total - 1) - soff[u];
       u32x4_t vv = sv[u];
@@ -162,7 +172,7 @@ __global__ __launch_bounds__(256) void conv_smallc(const bf16_t* __restrict__ In
       const int k = k0 + kk;
       eok[u] = k < a.Nk && jh < nq;
       const int q = eok[u] ? jh : 0;
-      const int c = q / a.Nr, r = q - (q / a.Nr) * a.Nr;
+      const int c = fdiv(q, dv.nr), r = q - c * a.Nr;
       ebase[u] = (((eok[u] ? k : 0) * a.Nc + c) * a.Nr + r) * a.Ns;
       e[u] = __builtin_bit_cast(
           u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(kr, (uint32_t)(ebase[u] * 2), 0, 0));
@@ -213,9 +223,9 @@ __global__ __launch_bounds__(256) void conv_smallc(const bf16_t* __restrict__ In
     for (int nb = 0; nb < NB; ++nb) {
       const int p = g.p0 + (wave * NB + nb) * 32 + l32;
       const int pc = p <= g.plast ? p : g.plast;
-      const int b = pc / a.hw;
+      const int b = fdiv(pc, dv.hw);
       const int q = pc - b * a.hw;
-      const int w = q / a.Nh;
+      const int w = fdiv(q, dv.nh);
       const int h = q - w * a.Nh;
       pbase[nb] = (b * a.Nx + a.sw * w - g.G0) * RSTR + a.sh * h;
       obyte[nb] = (uint32_t)(((int64_t)(b - g.b0) * a.Nk * a.hw + q) * (int64_t)sizeof(TO));
@@ -233,7 +243,7 @@ __global__ __launch_bounds__(256) void conv_smallc(const bf16_t* __restrict__ In
     for (int j = 0; j < KS; ++j) {
       if (j < nks) {
         const int q = min(2 * j + half, nq - 1);  // past nq: weights are zero
-        const int c = q / a.Nr, r = q - (q / a.Nr) * a.Nr;
+        const int c = fdiv(q, dv.nr), r = q - c * a.Nr;
         const int qoff = (c * g.S + r) * RSTR;
         u32x4_t bv[NB];
 #pragma unroll
@@ -328,8 +338,22 @@ static hipError_t launch_s(const void* In, const void* Ker, void* Out, const Con
   }
   // two workgroups per CU fill the registers; each takes every grid-th tile
   const int64_t wgs = std::min<int64_t>(a.grid, 2 * (int64_t)device_cus());
+  SmallcDiv dv;
+  dv.cpr = make_fastdiv((uint32_t)(((a.Ny + 15) & ~7) / 8));
+  dv.nx = make_fastdiv((uint32_t)a.Nx);
+  dv.hw = make_fastdiv((uint32_t)a.hw);
+  dv.nh = make_fastdiv((uint32_t)a.Nh);
+  dv.nr = make_fastdiv((uint32_t)a.Nr);
+  dv.kt = make_fastdiv((uint32_t)a.n_ktiles);
+  {
+    // the first tile's slab rows, as the kernel's geometry computes them
+    const int plast = (int)std::min<int64_t>(a.tp, a.npix) - 1;
+    const int b1 = plast / a.hw, w1 = (plast - b1 * a.hw) / a.Nh;
+    dv.S0 = b1 * a.Nx + a.sw * w1 + a.Nr;
+    dv.s0 = make_fastdiv((uint32_t)dv.S0);
+  }
   hipLaunchKernelGGL(kern, dim3((unsigned)wgs), dim3(256), (unsigned)lds, stream,
-                     (const bf16_t*)In, (const bf16_t*)Ker, (TO*)Out, a);
+                     (const bf16_t*)In, (const bf16_t*)Ker, (TO*)Out, a, dv);
   return hipGetLastError();
 }
 
