@@ -271,6 +271,7 @@ __global__ __launch_bounds__(64 * WP * WK) void conv_gemm1(const bf16_t* __restr
     if (a.tp % 4 == 0 && a.hw % 4 == 0 && (p0 + tp - 1) / a.hw == bi) {
       float* stg = reinterpret_cast<float*>(smem);
       const int upf = tp / 4;  // units per feature
+      const int nt_q = NT / upf, nt_r = NT - (NT / upf) * upf;
       const int64_t run0 = (int64_t)bi * a.Nk * a.hw + (p0 - bi * a.hw);
 #pragma unroll
       for (int rho = 0; rho < WK; ++rho) {
@@ -293,10 +294,17 @@ __global__ __launch_bounds__(64 * WP * WK) void conv_gemm1(const bf16_t* __restr
         const int nf = min(32 * NBK, a.Nk - f0);
         const int units = nf > 0 ? nf * upf : 0;
         const u32x4_t* src = reinterpret_cast<const u32x4_t*>(stg);
+        // unit u = fl * upf + pc, stepped by NT without a division per unit
+        int fl = tid / upf, pc = tid - (tid / upf) * upf;
         for (int u = tid; u < units; u += NT) {
-          const int fl = u / upf, pc = u - fl * upf;
           const uint32_t off = (uint32_t)((run0 + (int64_t)(f0 + fl) * a.hw) * 4) + 16u * (uint32_t)pc;
-          __builtin_amdgcn_raw_buffer_store_b128(src[fl * upf + pc], out_rsrc, off, 0, 0);
+          __builtin_amdgcn_raw_buffer_store_b128(src[u], out_rsrc, off, 0, 0);
+          fl += nt_q;
+          pc += nt_r;
+          if (pc >= upf) {
+            pc -= upf;
+            ++fl;
+          }
         }
       }
       return;
