@@ -358,20 +358,24 @@ __global__ __launch_bounds__(64 * NWV) void conv_srows(const bf16_t* __restrict_
   // ---- epilogue: register j of block (i, q) holds position l32 of output
   // row w0 + row0 + rdir*i, feature k0 + 64 fp + 32 (q ? 1 - nbf : nbf) +
   // 8 (j/4) + 4 half + j%4.
+  // (byte offsets: the lane's part once per block, plus the wave-uniform
+  // steps of feature and row; lanes past Nh or Nk store out of range)
+  const int kl = l32 < a.Nh ? a.Nk - 4 * half : -1;  // valid: first feature + step < kl
+  const uint32_t hw_b = (uint32_t)(a.Nw * a.Nh * (int)sizeof(TO)), nh_b = (uint32_t)(a.Nh * (int)sizeof(TO));
 #pragma unroll
   for (int q = 0; q < 2; ++q) {
-    const int nblk = k0 + 64 * fp + 32 * (q ? 1 - nbf : nbf) + 4 * half;
+    const int fb = k0 + 64 * fp + 32 * (q ? 1 - nbf : nbf);  // the block's first feature (half 0)
+    const uint32_t vo_q =
+        (uint32_t)(((((int64_t)b * a.Nk + fb + 4 * half) * a.Nw + w0 + row0) * a.Nh + l32) *
+                   (int64_t)sizeof(TO));
 #pragma unroll
     for (int i = 0; i < RW; ++i) {
       if (q == 1 && !has_second(i)) continue;
-      const int w = w0 + row0 + rdir * i;
 #pragma unroll
       for (int j = 0; j < 16; ++j) {
-        const int n = nblk + 8 * (j >> 2) + (j & 3);
-        const uint32_t vo =
-            (n < a.Nk && l32 < a.Nh)
-                ? (uint32_t)(((((int64_t)b * a.Nk + n) * a.Nw + w) * a.Nh + l32) * (int64_t)sizeof(TO))
-                : 0x80000000u;
+        const int f = 8 * (j >> 2) + (j & 3);
+        const uint32_t vo = fb + f < kl ? vo_q + (uint32_t)f * hw_b + (uint32_t)(rdir * i) * nh_b
+                                        : 0x80000000u;
         if constexpr (sizeof(TO) == 4)
           __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc[i][q][j]), out_rsrc, vo, 0, 0);
         else
@@ -1052,13 +1056,20 @@ __global__ __launch_bounds__(256) void conv_srows3(const bf16_t* __restrict__ In
   // buffer), then row i's Out, whose stores drain while the later rows are
   // multiplied.  Register j of block (i, nb) holds position l32 of output
   // row w0 + i, feature k0 + 64 wave + 32 nb + 8 (j/4) + 4 half + j%4.
+  // Out byte offsets: this lane's part (feature k0 + 64 wave + 4 half, band
+  // row 0, position l32) is formed once; a store adds the wave-uniform part
+  // of its feature step f = 32 nb + 8 (j/4) + j%4 and band row i.  Lanes past
+  // Nh or Nk store out of range (dropped).
+  // valid feature steps of this lane: f < kl (none past Nh)
+  const int kl = l32 < a.Nh ? a.Nk - (k0 + 64 * wave) - 4 * half : -1;
+  const uint32_t vo_lane =
+      (uint32_t)(((((int64_t)b * a.Nk + k0 + 64 * wave + 4 * half) * a.Nw + w0) * a.Nh + l32) *
+                 (int64_t)sizeof(TO));
+  const uint32_t hw_b = (uint32_t)(a.Nw * a.Nh * (int)sizeof(TO)), nh_b = (uint32_t)(a.Nh * (int)sizeof(TO));
   auto store_row = [&](int i, int q) __attribute__((always_inline)) {
     const int nb = q >> 4, j = q & 15;
-    const int n = k0 + 64 * wave + 32 * nb + 4 * half + 8 * (j >> 2) + (j & 3);
-    const uint32_t vo =
-        (n < a.Nk && l32 < a.Nh)
-            ? (uint32_t)(((((int64_t)b * a.Nk + n) * a.Nw + w0 + i) * a.Nh + l32) * (int64_t)sizeof(TO))
-            : 0x80000000u;
+    const int f = 32 * nb + 8 * (j >> 2) + (j & 3);
+    const uint32_t vo = f < kl ? vo_lane + (uint32_t)f * hw_b + (uint32_t)i * nh_b : 0x80000000u;
     if constexpr (sizeof(TO) == 4)
       __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc[i][nb][j]), out_rsrc, vo, 0, 0);
     else
