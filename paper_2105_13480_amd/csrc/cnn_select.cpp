@@ -339,10 +339,12 @@ static const int64_t kL2Bytes = 4LL << 20;
 // bf16 MFMA rate sustained on operands of these workloads' value ranges
 // (64 % of the 4096 flop/clk/CU datasheet rate: the clock drops with the
 // data-dependent power; fp32 MFMA is taken at its datasheet rate); the HBM
-// bandwidth of a large device copy (read plus write); a kernel launch.
+// bandwidth of a large device copy (read plus write) and of a large fill
+// (writes only); a kernel launch.
 static const double kClkGHz = 2.4;
 static const double kMfmaRealBf16 = 0.64;
 static const double kHbmGBs = 5000.0;
+static const double kFillGBs = 6900.0;
 static const double kLaunchUs = 2.0;
 // HBM writes per byte of Out of the stride-2 row-band kernels (row-piece
 // stores, partial lines), measured with WRITE_SIZE.
@@ -385,7 +387,7 @@ static FamilyCost family_cost(int kernel, int variant) {
         if (vg[i].id == variant && vg[i].s2 == 2) return {0.99, 1.22, 0.40, 50.0};  // DMA ring
       return {0.36, 1.28, 0.56, 50.1};
     }
-    case CNN_K_SMALLC: return {0.17, 2.64, 0.17, 49.7};
+    case CNN_K_SMALLC: return {0.17, 1.66, 0.17, 49.7};
     case CNN_K_IGEMM_RAWK: return {0.49, 1.67, 2.41, 29.5};
     case CNN_K_POINTWISE: return {0.98, 37.19, 0.41, 100.0};
     case CNN_K_IGEMM_PIPE: return {0.74, 3.80, 2.51, 30.2};
@@ -404,6 +406,19 @@ static FamilyCost family_cost(int kernel, int variant) {
 // family's stage bandwidth.  The whole is at least the plan's HBM bytes
 // (Eq. (3) at the XCD level) at the copy bandwidth.  Channel-split plans
 // add their reduce pass; every plan adds its launch.
+// The time the plan's HBM bytes (Eq. (3) at the XCD level) take at least: at
+// the bandwidth of their mix of reads and writes, from a copy's (half of
+// each, or more reads) to a fill's (writes only), linear in the write share.
+static double hbm_floor_us(const cnn_plan_t& pl) {
+  double t[3];
+  hbm_terms(pl, kXcds, kL2Bytes, t);
+  const double total = t[0] + t[1] + t[2];
+  if (total <= 0.0) return 0.0;
+  const double w = t[0] / total;
+  const double gbs = w <= 0.5 ? kHbmGBs : kHbmGBs + (kFillGBs - kHbmGBs) * (w - 0.5) / 0.5;
+  return total / (gbs * 1e3);
+}
+
 static double model_us(const cnn_plan_t& pl, const cnn_budget& bud) {
   const cnn_problem& p = pl.prob;
   const FamilyCost fc = family_cost(pl.kernel, pl.variant);
@@ -413,7 +428,7 @@ static double model_us(const cnn_plan_t& pl, const cnn_budget& bud) {
   if (pl.kernel == CNN_K_DIRECT) {
     // 64 lanes x 4 SIMDs x one fp32 FMA (2 flops) per clock per CU
     const double t = pl.flops / (cus * 512.0 * clk_per_us * fc.mfma_eff);
-    return std::max(t, pl.hbm_bytes / (kHbmGBs * 1e3)) + kLaunchUs;
+    return std::max(t, hbm_floor_us(pl)) + kLaunchUs;
   }
   const double kc = pl.kernel == CNN_K_SPLITC ? (double)pl.kc : 1.0;
   const double wgs = (double)pl.grid * kc;
@@ -434,7 +449,7 @@ static double model_us(const cnn_plan_t& pl, const cnn_budget& bud) {
   const double t_stage =
       std::max(stage_flops / rate, fc.stage_us + stage_bytes / (fc.stage_gbs * 1e3));
   double t = std::ceil(per_cu / (double)occ) * (fc.wg_us + n_st * t_stage);
-  t = std::max(t, pl.hbm_bytes / (kHbmGBs * 1e3));
+  t = std::max(t, hbm_floor_us(pl));
   if (pl.kernel == CNN_K_SPLITC)  // the reduce pass: kc fp32 partials read, Out written
     t += kLaunchUs + 4.0 * (kc + 1.0) * n_out / (kHbmGBs * 1e3);
   return t + kLaunchUs;
