@@ -39,8 +39,6 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc_s(const void* base, int64
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, n, 0x00020000);
 }
 
-// KS: largest number of K-steps (ceil(Nc*Nr/2)) the registers hold.  SH2:
-// sh == 2 (operands gathered with 32-bit LDS reads).
 // Dividers for the launch's runtime divisors (made on the host).
 struct SmallcDiv {
   FastDiv cpr, nx, hw, nh, nr, kt;
@@ -48,6 +46,9 @@ struct SmallcDiv {
   int S0;
 };
 
+// KS: largest number of K-steps (ceil(Nc*Nr/2)) the registers hold.  SH2:
+// sh == 2 (operands gathered with 32-bit LDS reads).  Two workgroups per CU
+// (two waves per SIMD) run at once, so a wave keeps to 256 registers.
 template <typename TO, int NB, int KS, bool SH2>
 __global__ __launch_bounds__(256, 2) void conv_smallc(const bf16_t* __restrict__ In,
                                                    const bf16_t* __restrict__ Ker,
