@@ -133,7 +133,7 @@ bool ranges_ok_srows(const VariantQ& v, const cnn_problem& p, int dtype) {
          (p.Nb * p.Nk + 288) * p.Nw * p.Nh * out_bytes(dtype) < k2G;
 }
 
-static double model_us(const cnn_plan_t& pl, const cnn_budget& bud);
+static double model_us(const cnn_plan_t& pl, const cnn_budget& bud, double w_out);
 
 // Plan fields shared by the implicit-GEMM families (the model's time is set
 // once the plan is complete).
@@ -399,27 +399,22 @@ static FamilyCost family_cost(int kernel, int variant) {
   }
 }
 
+// The bandwidth HBM sustains for a mix of reads and writes with write share
+// w: a device copy's (half of each, or more reads) up to a fill's (writes
+// only), linear in w.
+static double hbm_gbs(double w) {
+  return w <= 0.5 ? kHbmGBs : kHbmGBs + (kFillGBs - kHbmGBs) * (w - 0.5) / 0.5;
+}
+
 // The selector's time model for a finished plan, in microseconds.  The
 // busiest CU runs ceil(workgroups / CUs) workgroups, up to `occ` of them at
 // once (as LDS allows); each walks its channel stages, a stage taking the
 // longer of its MFMA work and its latency plus its Eq. (1) bytes at the
 // family's stage bandwidth.  The whole is at least the plan's HBM bytes
-// (Eq. (3) at the XCD level) at the copy bandwidth.  Channel-split plans
-// add their reduce pass; every plan adds its launch.
-// The time the plan's HBM bytes (Eq. (3) at the XCD level) take at least: at
-// the bandwidth of their mix of reads and writes, from a copy's (half of
-// each, or more reads) to a fill's (writes only), linear in the write share.
-static double hbm_floor_us(const cnn_plan_t& pl) {
-  double t[3];
-  hbm_terms(pl, kXcds, kL2Bytes, t);
-  const double total = t[0] + t[1] + t[2];
-  if (total <= 0.0) return 0.0;
-  const double w = t[0] / total;
-  const double gbs = w <= 0.5 ? kHbmGBs : kHbmGBs + (kFillGBs - kHbmGBs) * (w - 0.5) / 0.5;
-  return total / (gbs * 1e3);
-}
-
-static double model_us(const cnn_plan_t& pl, const cnn_budget& bud) {
+// (Eq. (3) at the XCD level), of which the share w_out is written, at the
+// bandwidth of that mix.  Channel-split plans add their reduce pass; every
+// plan adds its launch.
+static double model_us(const cnn_plan_t& pl, const cnn_budget& bud, double w_out) {
   const cnn_problem& p = pl.prob;
   const FamilyCost fc = family_cost(pl.kernel, pl.variant);
   const double clk_per_us = kClkGHz * 1e3;
@@ -428,7 +423,7 @@ static double model_us(const cnn_plan_t& pl, const cnn_budget& bud) {
   if (pl.kernel == CNN_K_DIRECT) {
     // 64 lanes x 4 SIMDs x one fp32 FMA (2 flops) per clock per CU
     const double t = pl.flops / (cus * 512.0 * clk_per_us * fc.mfma_eff);
-    return std::max(t, hbm_floor_us(pl)) + kLaunchUs;
+    return std::max(t, pl.hbm_bytes / (hbm_gbs(w_out) * 1e3)) + kLaunchUs;
   }
   const double kc = pl.kernel == CNN_K_SPLITC ? (double)pl.kc : 1.0;
   const double wgs = (double)pl.grid * kc;
@@ -449,7 +444,7 @@ static double model_us(const cnn_plan_t& pl, const cnn_budget& bud) {
   const double t_stage =
       std::max(stage_flops / rate, fc.stage_us + stage_bytes / (fc.stage_gbs * 1e3));
   double t = std::ceil(per_cu / (double)occ) * (fc.wg_us + n_st * t_stage);
-  t = std::max(t, hbm_floor_us(pl));
+  t = std::max(t, pl.hbm_bytes / (hbm_gbs(w_out) * 1e3));
   if (pl.kernel == CNN_K_SPLITC)  // the reduce pass: kc fp32 partials read, Out written
     t += kLaunchUs + 4.0 * (kc + 1.0) * n_out / (kHbmGBs * 1e3);
   return t + kLaunchUs;
@@ -466,15 +461,18 @@ static void fill_common(const cnn_problem& p, int dtype, const cnn_budget& bud,
                                    (double)(p.Nk * p.Nc * p.Nr * p.Ns)) +
                            e_out * (double)(p.Nb * p.Nk * p.Nw * p.Nh);
   plan->flops = 2.0 * (double)p.Nb * p.Nk * p.Nc * p.Nr * p.Ns * p.Nw * p.Nh;
+  double w_out;  // share of the HBM bytes that are writes
   if (plan->kernel == CNN_K_DIRECT) {
     plan->mfma_flops = 0.0;
     plan->hbm_bytes = plan->compulsory_bytes;
+    w_out = e_out * (double)(p.Nb * p.Nk * p.Nw * p.Nh) / plan->compulsory_bytes;
   } else {
     double t[3];
     hbm_terms(*plan, kXcds, kL2Bytes, t);
     plan->hbm_bytes = t[0] + t[1] + t[2];
+    w_out = plan->hbm_bytes > 0.0 ? t[0] / plan->hbm_bytes : 0.0;
   }
-  plan->model_us = model_us(*plan, bud);
+  plan->model_us = model_us(*plan, bud, w_out);
 }
 
 void direct_plan(const cnn_problem& p, int dtype, const cnn_budget& bud, cnn_plan_t* plan) {
