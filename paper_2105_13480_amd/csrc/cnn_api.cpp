@@ -144,7 +144,7 @@ const VariantS* find_variant_s(int id) {
 bool smallc_geometry_ok(const VariantS& v, const cnn_plan_t& pl) {
   const cnn_problem& p = pl.prob;
   if (p.Ns > 8 || (p.Nc * p.Nr + 1) / 2 > v.ks || pl.tp < 1 || pl.tp > v.tp ||
-      !ranges_ok_smallc(v, p, pl.dtype))
+      !smallc_stencil_ok(v, p) || !ranges_ok_smallc(v, p, pl.dtype))
     return false;
   const int64_t S = slab_rows_max(p, pl.tp);
   const int64_t grid = ((p.Nb * p.Nw * p.Nh + pl.tp - 1) / pl.tp) * ((p.Nk + v.tk - 1) / v.tk);

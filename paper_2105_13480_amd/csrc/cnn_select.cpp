@@ -251,7 +251,9 @@ static bool eval_variant2(const cnn_problem& p, int dtype, const Variant2& v,
 // registers' K-steps, the stencil at most 8 wide, the slab in LDS, and the
 // tensors the 32-bit offsets.
 static bool eval_smallc(const cnn_problem& p, int dtype, const VariantS& v, const cnn_budget& bud, cnn_plan_t* plan) {
-  if (p.Ns > 8 || (p.Nc * p.Nr + 1) / 2 > v.ks || !ranges_ok_smallc(v, p, dtype)) return false;
+  if (p.Ns > 8 || (p.Nc * p.Nr + 1) / 2 > v.ks || !smallc_stencil_ok(v, p) ||
+      !ranges_ok_smallc(v, p, dtype))
+    return false;
   const int64_t lds_full = smallc_lds_bytes(v, p, slab_rows_max(p, v.tp));
   const int64_t occ = std::max<int64_t>(1, std::min<int64_t>(bud.wg_per_cu, bud.lds_bytes / lds_full));
   const int64_t tp = balanced_tp(p, v.tp, v.tk, bud.cus * occ, 1);
@@ -387,7 +389,13 @@ static FamilyCost family_cost(int kernel, int variant) {
         if (vg[i].id == variant && vg[i].s2 == 2) return {0.99, 1.22, 0.40, 50.0};  // DMA ring
       return {0.36, 1.28, 0.56, 50.1};
     }
-    case CNN_K_SMALLC: return {0.17, 1.66, 0.17, 49.7};
+    case CNN_K_SMALLC: {
+      int n = 0;
+      const VariantS* vs = variants_smallc(&n);
+      for (int i = 0; i < n; ++i)
+        if (vs[i].id == variant && vs[i].nc) return {0.17, 1.52, 0.17, 49.7};  // stencil compiled in
+      return {0.17, 1.66, 0.17, 49.7};
+    }
     case CNN_K_IGEMM_RAWK: return {0.49, 1.67, 2.41, 29.5};
     case CNN_K_POINTWISE: return {0.98, 37.19, 0.41, 100.0};
     case CNN_K_IGEMM_PIPE: return {0.74, 3.80, 2.51, 30.2};
@@ -870,7 +878,7 @@ int list_variants(cnn_variant_t* out, int cap) {
         v4[i].tc);
   const VariantS* vsc = variants_smallc(&c);
   for (int i = 0; i < c; ++i)
-    add(CNN_K_SMALLC, vsc[i].id, vsc[i].dtype, 0, 0, 0, vsc[i].tk, vsc[i].tp, 0);
+    add(CNN_K_SMALLC, vsc[i].id, vsc[i].dtype, vsc[i].nr, vsc[i].ns, 0, vsc[i].tk, vsc[i].tp, 0);
   const VariantR* vr = variants_rows(&c);
   for (int i = 0; i < c; ++i)
     add(CNN_K_ROWS, vr[i].id, vr[i].dtype, vr[i].nr, vr[i].ns, vr[i].mb, vr[i].tk, 0,

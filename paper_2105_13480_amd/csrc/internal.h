@@ -107,8 +107,10 @@ struct VariantS {
   int32_t tk, tp;   // tk = 64; tp = largest tile
   int32_t ks;       // K-steps held in registers: ceil(Nc*Nr/2) <= ks
   int32_t acc;
+  int32_t nc, nr, ns, st;  // stencil compiled in (Nc, Nr, Ns, both strides), 0 for any
 };
 const VariantS* variants_smallc(int* count);
+bool smallc_stencil_ok(const VariantS& v, const cnn_problem& p);  // the problem fits a fixed stencil
 int64_t smallc_lds_bytes(const VariantS& v, const cnn_problem& p, int64_t slab_rows);
 hipError_t launch_smallc(const VariantS& v, const void* In, const void* Ker, void* Out,
                          const ConvArgs& a, int64_t lds_bytes, hipStream_t stream);

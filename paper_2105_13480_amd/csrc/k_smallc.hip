@@ -47,13 +47,22 @@ struct SmallcDiv {
 };
 
 // KS: largest number of K-steps (ceil(Nc*Nr/2)) the registers hold.  SH2:
-// sh == 2 (operands gathered with 32-bit LDS reads).  Two workgroups per CU
-// (two waves per SIMD) run at once, so a wave keeps to 256 registers.
-template <typename TO, int NB, int KS, bool SH2>
+// sh == 2 (operands gathered with 32-bit LDS reads).  FC, FR, FS, FST: a
+// fixed stencil (Nc, Nr, Ns and both strides) compiled in, 0 for any: the
+// address arithmetic and the K-step count then fold at compile time (the
+// 3-channel 7x7 stride-2 input layer).  Two workgroups per CU (two waves per
+// SIMD) run at once, so a wave keeps to 256 registers.
+template <typename TO, int NB, int KS, bool SH2, int FC = 0, int FR = 0, int FS = 0, int FST = 0>
 __global__ __launch_bounds__(256, 2) void conv_smallc(const bf16_t* __restrict__ In,
                                                    const bf16_t* __restrict__ Ker,
                                                    TO* __restrict__ Out, ConvArgs a,
                                                    SmallcDiv dv) {
+  const int Nc = FC ? FC : a.Nc, Nr = FR ? FR : a.Nr, Ns = FS ? FS : a.Ns;
+  const int sw = FST ? FST : a.sw, sh = FST ? FST : a.sh;
+  auto div_nr = [&](int q) -> int {
+    if constexpr (FR != 0) return q / FR;
+    else return fdiv(q, dv.nr);
+  };
   constexpr int MB = 2;         // 64 features per tile, shared by the 4 waves
   constexpr int TK = 32 * MB;
   constexpr int KVEC = KS * 2 * TK;  // Ker image vectors
@@ -76,7 +85,7 @@ __global__ __launch_bounds__(256, 2) void conv_smallc(const bf16_t* __restrict__
   const int G = (int)gridDim.x;
   const int t_first = xcd_remap(blockIdx.x, gridDim.x);
   const int RSTR = (a.Ny + 15) & ~7;                       // LDS row stride (elements)
-  const int nq = a.Nc * a.Nr;                              // (c, r) rows of the stencil
+  const int nq = Nc * Nr;                              // (c, r) rows of the stencil
   const int nks = (nq + 1) >> 1;                           // K-steps
   const int cpr = RSTR / 8;                                // 16-byte chunks per slab row
   const __amdgpu_buffer_rsrc_t ir = rsrc_s(In, a.in_total * 2);
@@ -100,8 +109,8 @@ __global__ __launch_bounds__(256, 2) void conv_smallc(const bf16_t* __restrict__
     g.b0 = fdiv(g.p0, dv.hw);
     const int w0 = fdiv(g.p0 - g.b0 * a.hw, dv.nh);
     const int b1 = fdiv(g.plast, dv.hw), w1 = fdiv(g.plast - b1 * a.hw, dv.nh);
-    g.G0 = g.b0 * a.Nx + a.sw * w0;
-    g.S = b1 * a.Nx + a.sw * w1 + a.Nr - g.G0;
+    g.G0 = g.b0 * a.Nx + sw * w0;
+    g.S = b1 * a.Nx + sw * w1 + Nr - g.G0;
     g.fs = g.S == dv.S0 ? dv.s0 : make_fastdiv((uint32_t)g.S);
     return g;
   };
@@ -114,7 +123,7 @@ __global__ __launch_bounds__(256, 2) void conv_smallc(const bf16_t* __restrict__
   u32x4_t sv[U];
   int soff[U];
   auto slab_load = [&](const Geo& g, int e0) __attribute__((always_inline)) {
-    const int n = a.Nc * g.S * cpr;
+    const int n = Nc * g.S * cpr;
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int e = min(e0 + tid + 256 * u, n - 1);
@@ -131,7 +140,7 @@ __global__ __launch_bounds__(256, 2) void conv_smallc(const bf16_t* __restrict__
     }
   };
   auto slab_write = [&](const Geo& g, int e0) __attribute__((always_inline)) {
-    const int n = a.Nc * g.S * cpr;
+    const int n = Nc * g.S * cpr;
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int e = e0 + tid + 256 * u;
@@ -157,7 +166,7 @@ __global__ __launch_bounds__(256, 2) void conv_smallc(const bf16_t* __restrict__
   // (c, r) row q = 2j + h, zero past Ns, nq or Nk.  All of a thread's
   // loads are issued before any is used.
   auto load_kimg = [&](int k0) __attribute__((always_inline)) {
-    const int64_t ker_total = (int64_t)a.Nk * a.Nc * a.Nr * a.Ns;
+    const int64_t ker_total = (int64_t)a.Nk * Nc * Nr * Ns;
     const __amdgpu_buffer_rsrc_t kr = rsrc_s(Ker, ker_total * 2);
     const uint32_t ker_last =
         __builtin_amdgcn_raw_buffer_load_b16(kr, (uint32_t)((ker_total - 1) * 2), 0, 0);
@@ -173,8 +182,8 @@ __global__ __launch_bounds__(256, 2) void conv_smallc(const bf16_t* __restrict__
       const int k = k0 + kk;
       eok[u] = k < a.Nk && jh < nq;
       const int q = eok[u] ? jh : 0;
-      const int c = fdiv(q, dv.nr), r = q - c * a.Nr;
-      ebase[u] = (((eok[u] ? k : 0) * a.Nc + c) * a.Nr + r) * a.Ns;
+      const int c = div_nr(q), r = q - c * Nr;
+      ebase[u] = (((eok[u] ? k : 0) * Nc + c) * Nr + r) * Ns;
       e[u] = __builtin_bit_cast(
           u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(kr, (uint32_t)(ebase[u] * 2), 0, 0));
     }
@@ -189,7 +198,7 @@ __global__ __launch_bounds__(256, 2) void conv_smallc(const bf16_t* __restrict__
         uint32_t w = vv[t >> 1];
         if (d == t) w = (w & 0xffff0000u) | ker_last;
         if (d == t + 1) w = (w & 0xffffu) | (ker_last << 16);
-        const uint32_t keep = (eok[u] ? (t < a.Ns ? 0xffffu : 0u) | (t + 1 < a.Ns ? 0xffff0000u : 0u)
+        const uint32_t keep = (eok[u] ? (t < Ns ? 0xffffu : 0u) | (t + 1 < Ns ? 0xffff0000u : 0u)
                                       : 0u);
         vv[t >> 1] = w & keep;
       }
@@ -202,7 +211,7 @@ __global__ __launch_bounds__(256, 2) void conv_smallc(const bf16_t* __restrict__
   if (t_first < n_tiles) slab_load(geo(t_first), 0);
   for (int t = t_first; t < n_tiles; t += G) {
     const Geo g = geo(t);
-    const int n_chunks = a.Nc * g.S * cpr;
+    const int n_chunks = Nc * g.S * cpr;
     __syncthreads();  // the previous tile's operand reads are done
     if (g.kt != kt_img) {
       load_kimg(g.k0);
@@ -228,7 +237,7 @@ __global__ __launch_bounds__(256, 2) void conv_smallc(const bf16_t* __restrict__
       const int q = pc - b * a.hw;
       const int w = fdiv(q, dv.nh);
       const int h = q - w * a.Nh;
-      pbase[nb] = (b * a.Nx + a.sw * w - g.G0) * RSTR + a.sh * h;
+      pbase[nb] = (b * a.Nx + sw * w - g.G0) * RSTR + sh * h;
       obyte[nb] = (uint32_t)(((int64_t)(b - g.b0) * a.Nk * a.hw + q) * (int64_t)sizeof(TO));
     }
 
@@ -244,7 +253,7 @@ __global__ __launch_bounds__(256, 2) void conv_smallc(const bf16_t* __restrict__
     for (int j = 0; j < KS; ++j) {
       if (j < nks) {
         const int q = min(2 * j + half, nq - 1);  // past nq: weights are zero
-        const int c = fdiv(q, dv.nr), r = q - c * a.Nr;
+        const int c = div_nr(q), r = q - c * Nr;
         const int qoff = (c * g.S + r) * RSTR;
         u32x4_t bv[NB];
 #pragma unroll
@@ -302,21 +311,29 @@ __global__ __launch_bounds__(256, 2) void conv_smallc(const bf16_t* __restrict__
 }
 
 // ---- instantiation table ----------------------------------------------------
-// (id, dtype, NB, KS): tk = 64, tp = 128*NB (largest tile); KS = most
-// K-steps, ceil(Nc*Nr/2) <= KS; any Ns <= 8, any stride.
-#define CNN_SMALLC_VARIANTS(X)             \
-  X(1000, CNN_BF16, 2, 12)                 \
-  X(1001, CNN_BF16, 1, 12)                 \
-  X(1002, CNN_BF16, 2, 24)                 \
-  X(1100, CNN_BF16_OBF16, 2, 12)           \
-  X(1101, CNN_BF16_OBF16, 1, 12)           \
-  X(1102, CNN_BF16_OBF16, 2, 24)
+// (id, dtype, NB, KS, FC, FR, FS, FST): tk = 64, tp = 128*NB (largest tile);
+// KS = most K-steps, ceil(Nc*Nr/2) <= KS; any Ns <= 8, any stride, unless
+// FC..FST fix the stencil (1003, 1103: 3 channels, 7x7, stride 2).
+#define CNN_SMALLC_VARIANTS(X)                   \
+  X(1000, CNN_BF16, 2, 12, 0, 0, 0, 0)           \
+  X(1001, CNN_BF16, 1, 12, 0, 0, 0, 0)           \
+  X(1002, CNN_BF16, 2, 24, 0, 0, 0, 0)           \
+  X(1003, CNN_BF16, 2, 12, 3, 7, 7, 2)           \
+  X(1100, CNN_BF16_OBF16, 2, 12, 0, 0, 0, 0)     \
+  X(1101, CNN_BF16_OBF16, 1, 12, 0, 0, 0, 0)     \
+  X(1102, CNN_BF16_OBF16, 2, 24, 0, 0, 0, 0)     \
+  X(1103, CNN_BF16_OBF16, 2, 12, 3, 7, 7, 2)
 
 static const VariantS kVariantsS[] = {
-#define CNN_ROWS(id, dt, nb, ks) {id, dt, 64, 128 * (nb), ks, 16 * 2 * (nb)},
+#define CNN_ROWS(id, dt, nb, ks, fc, fr, fs, fst) \
+  {id, dt, 64, 128 * (nb), ks, 16 * 2 * (nb), fc, fr, fs, fst},
     CNN_SMALLC_VARIANTS(CNN_ROWS)
 #undef CNN_ROWS
 };
+
+bool smallc_stencil_ok(const VariantS& v, const cnn_problem& p) {
+  return v.nc == 0 || (p.Nc == v.nc && p.Nr == v.nr && p.Ns == v.ns && p.sw == v.st && p.sh == v.st);
+}
 
 const VariantS* variants_smallc(int* count) {
   *count = (int)(sizeof(kVariantsS) / sizeof(kVariantsS[0]));
@@ -328,11 +345,12 @@ int64_t smallc_lds_bytes(const VariantS& v, const cnn_problem& p, int64_t slab_r
   return (int64_t)v.ks * 2 * v.tk * 16 + p.Nc * slab_rows * ((Ny + 15) & ~(int64_t)7) * 2;
 }
 
-template <int DT, int NB, int KS>
+template <int DT, int NB, int KS, int FC, int FR, int FS, int FST>
 static hipError_t launch_s(const void* In, const void* Ker, void* Out, const ConvArgs& a,
                            int64_t lds, hipStream_t stream) {
   typedef typename std::conditional<DT == CNN_BF16, float, bf16_t>::type TO;
-  auto kern = a.sh == 2 ? conv_smallc<TO, NB, KS, true> : conv_smallc<TO, NB, KS, false>;
+  auto kern = FST ? conv_smallc<TO, NB, KS, FST == 2, FC, FR, FS, FST>
+                  : a.sh == 2 ? conv_smallc<TO, NB, KS, true> : conv_smallc<TO, NB, KS, false>;
   {
     const hipError_t e = allow_max_lds((const void*)kern);
     if (e != hipSuccess) return e;
@@ -361,9 +379,9 @@ static hipError_t launch_s(const void* In, const void* Ker, void* Out, const Con
 hipError_t launch_smallc(const VariantS& v, const void* In, const void* Ker, void* Out,
                          const ConvArgs& a, int64_t lds_bytes, hipStream_t stream) {
   switch (v.id) {
-#define CNN_CASES(id, dt, nb, ks) \
-  case id:                        \
-    return launch_s<dt, nb, ks>(In, Ker, Out, a, lds_bytes, stream);
+#define CNN_CASES(id, dt, nb, ks, fc, fr, fs, fst) \
+  case id:                                        \
+    return launch_s<dt, nb, ks, fc, fr, fs, fst>(In, Ker, Out, a, lds_bytes, stream);
     CNN_SMALLC_VARIANTS(CNN_CASES)
 #undef CNN_CASES
     default:
