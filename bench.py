@@ -21,7 +21,9 @@ bracketed by torch.cuda.synchronize().
 
 Prints ONE JSON line: the metric (conv TFLOP/s = 2 Nb Nk Nc Nr Ns Nw Nh /
 seconds per step), the roofline of the convolution kernel (HIP events on
-the stream it runs on, algorithmic bytes or flops per launch), the fp64
+the stream it runs on, algorithmic bytes or flops per launch; HBM-bound
+kernels also against the bandwidth of a 256 MiB device copy measured in
+the same run, "frac_of_copy"), the fp64
 CPU oracle timed on this host as a baseline, and under "configs" the same
 figures for every workload (each with its own oracle baseline on a bounded
 sample).
@@ -138,6 +140,30 @@ def copy_calibration(nbytes: int, steps: int):
     print(json.dumps({"copy_bytes": n * 4, "ms_per_copy": round(ms, 5),
                       "GB_per_s_read_plus_write": round(2 * n * 4 / (ms * 1e-3) / 1e9, 1)}),
           flush=True)
+
+
+def copy_gbs(nbytes: int = 1 << 28, steps: int = 20) -> float:
+    """HBM bandwidth of a large device copy (bytes read plus written per
+    second, HIP events, after half a second of untimed copies): the
+    attainable side of the roofline beside the 8 TB/s datasheet figure."""
+    import torch
+    a = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda")
+    b = torch.empty_like(a)
+    t_w = time.perf_counter()
+    while time.perf_counter() - t_w < 0.5:
+        for _ in range(8):
+            b.copy_(a)
+        torch.cuda.synchronize()
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    ev0.record()
+    for _ in range(steps):
+        b.copy_(a)
+    ev1.record()
+    torch.cuda.synchronize()
+    ms = ev0.elapsed_time(ev1) / steps
+    del a, b
+    return 2.0 * nbytes / (ms * 1e-3) / 1e9
 
 
 def _counter_medians(csv_dir: str, counter: str):
@@ -482,6 +508,11 @@ def main():
     roof["eq1_bytes_per_launch"] = plan.eq1_bytes
     roof["kernel_ms"] = round(kms, 5)
     roof["pct_mfma_peak"] = round(100.0 * w.flops / (kms * 1e-3) / 1e12 / PEAK_TFLOPS[prec], 2)
+    # the same algorithmic rate against the measured copy bandwidth
+    copy_bw = copy_gbs()
+    roof["copy_gbs"] = round(copy_bw, 1)
+    if roof["bound"] == "hbm":
+        roof["frac_of_copy"] = round(roof["achieved"] / copy_bw, 4)
 
     line = {
         "metric": "conv TFLOP/s (2*Nb*Nk*Nc*Nr*Ns*Nw*Nh/s) + % MFMA peak, 1 MI355X",
@@ -540,6 +571,8 @@ def main():
                 rec["roofline"]["traffic"] = measured_traffic(ww.name, md, p2.as_dict()["kernel"],
                                                               p2.variant)
                 rec["roofline"]["model_hbm_bytes"] = round(p2.hbm_bytes)
+                if rec["roofline"]["bound"] == "hbm":
+                    rec["roofline"]["frac_of_copy"] = round(rec["roofline"]["achieved"] / copy_bw, 4)
                 if (mdl.kernel, mdl.variant, mdl.tp, mdl.kc) != (p2.kernel, p2.variant, p2.tp, p2.kc):
                     # the model's own choice, timed the same way
                     _, k3, _, _ = time_workload(ww, md, min(args.steps, 100), 0, args.eager,
