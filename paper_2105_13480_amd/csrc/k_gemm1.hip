@@ -528,46 +528,53 @@ __global__ __launch_bounds__(64 * WP * WK) void conv_gemm1d(const bf16_t* __rest
   }
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the trailing (empty) copies
 
-  if constexpr (sizeof(TO) == 4 && 128 * TPMAX * 4 <= DEPTH * STAGE * 16) {
-    // fp32 Out: the tile's Out (image b, features k0 .. k0+TK-1, all hw
-    // pixels) is one contiguous run; it goes through LDS in rounds of 128
-    // features (the waves with wk in {2 rho, 2 rho + 1}) and leaves as
-    // 16-byte stores of consecutive units, whole cache lines but at the
-    // run's two ends.
-    float* stg = reinterpret_cast<float*>(smem);
-    constexpr int WPR = 128 / (32 * NBK);  // wk values per round
-    static_assert(WK % WPR == 0, "whole rounds");
+  // The tile's Out (image b, features k0 .. k0+TK-1, all hw pixels) is one
+  // contiguous run; it goes through LDS in rounds of 128 features (the
+  // waves with wk in {2 rho, 2 rho + 1}) and leaves as 16-byte stores of
+  // consecutive units (4 fp32 or 8 bf16 values), whole cache lines but at
+  // the run's two ends -- when the run starts and ends on 16-byte
+  // boundaries (always for fp32; for bf16 unless hw and the feature count
+  // are odd multiples of 4 and 2), else through the stores below.
+  constexpr int EPU = 16 / (int)sizeof(TO);  // Out values per 16-byte unit
+  if constexpr (128 * TPMAX * (int)sizeof(TO) <= DEPTH * STAGE * 16) {
+    const bool whole_units = ((int64_t)b * a.Nk + k0) * hw % EPU == 0 &&
+                             (a.Nk - k0 >= TK || (int64_t)(a.Nk - k0) * hw % EPU == 0);
+    if (whole_units) {
+      TO* stg = reinterpret_cast<TO*>(smem);
+      constexpr int WPR = 128 / (32 * NBK);  // wk values per round
+      static_assert(WK % WPR == 0, "whole rounds");
 #pragma unroll
-    for (int rho = 0; rho < WK / WPR; ++rho) {
-      asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");  // LDS free
-      if (wk / WPR == rho) {
+      for (int rho = 0; rho < WK / WPR; ++rho) {
+        asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");  // LDS free
+        if (wk / WPR == rho) {
 #pragma unroll
-        for (int mb = 0; mb < MBP; ++mb) {
-          const int q = 32 * (wp * MBP + mb) + l32;
-          if (q < hw) {
+          for (int mb = 0; mb < MBP; ++mb) {
+            const int q = 32 * (wp * MBP + mb) + l32;
+            if (q < hw) {
 #pragma unroll
-            for (int nb = 0; nb < NBK; ++nb)
+              for (int nb = 0; nb < NBK; ++nb)
 #pragma unroll
-              for (int j = 0; j < 16; ++j) {
-                const int fl = 32 * ((wk % WPR) * NBK + nb) + 8 * (j >> 2) + 4 * half + (j & 3);
-                stg[fl * hw + q] = acc[mb][nb][j];
-              }
+                for (int j = 0; j < 16; ++j) {
+                  const int fl = 32 * ((wk % WPR) * NBK + nb) + 8 * (j >> 2) + 4 * half + (j & 3);
+                  stg[fl * hw + q] = from_f32<TO>(acc[mb][nb][j]);
+                }
+            }
           }
         }
+        asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+        const int f0 = k0 + 128 * rho;  // first feature of the round
+        const int nf = min(128, a.Nk - f0);
+        const int units = nf > 0 ? nf * hw / EPU : 0;
+        const uint32_t base = (uint32_t)(((int64_t)b * a.Nk + f0) * hw * (int64_t)sizeof(TO));
+        const u32x4_t* src = reinterpret_cast<const u32x4_t*>(stg);
+        // whole lines, stored through to memory (sc1): they drain during the
+        // kernel instead of waiting, dirty in the L2, for its end
+        for (int u = tid; u < units; u += NT)
+          __builtin_amdgcn_raw_buffer_store_b128(src[u], out_rsrc,
+                                                 base + 16u * (uint32_t)u, 0, kStoreThrough);
       }
-      asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-      const int f0 = k0 + 128 * rho;  // first feature of the round
-      const int nf = min(128, a.Nk - f0);
-      const int units = nf > 0 ? nf * hw / 4 : 0;
-      const uint32_t base = (uint32_t)(((int64_t)b * a.Nk + f0) * hw * 4);
-      const u32x4_t* src = reinterpret_cast<const u32x4_t*>(stg);
-      // whole lines, stored through to memory (sc1): they drain during the
-      // kernel instead of waiting, dirty in the L2, for its end
-      for (int u = tid; u < units; u += NT)
-        __builtin_amdgcn_raw_buffer_store_b128(src[u], out_rsrc,
-                                               base + 16u * (uint32_t)u, 0, kStoreThrough);
+      return;
     }
-    return;
   }
 
   // Epilogue as in conv_gemm1: a lane holds pixel q of 16 features.
