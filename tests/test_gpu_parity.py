@@ -330,12 +330,16 @@ def test_gemm1_exact(shape, mode):
 
 @pytest.mark.parametrize("mode", ["bf16", "bf16_obf16"])
 @pytest.mark.parametrize("shape", GEMM1_SHAPES + [(1, 1000, 33, 12, 20, 1, 1, 1, 1),
-                                                  (4, 8, 256, 2, 2, 1, 1, 1, 1)])
+                                                  (4, 8, 256, 2, 2, 1, 1, 1, 1),
+                                                  (3, 16, 257, 6, 10, 1, 1, 1, 1)])
 def test_gemm1_ring_exact(shape, mode):
     """The 1x1 GEMM kernel with whole-image tiles and both operands copied
     by DMA into a four-stage ring: bit-exact with the oracle on integer
     inputs (ragged last stage, a 240-pixel image, k tiles past Nk, 4-pixel
-    images)."""
+    images).  With bf16 Out a tile's run leaves as whole 16-byte units only
+    when it starts and ends on 16-byte boundaries: Nk = 71 with 60-pixel
+    images never does, Nk = 257 does for images 0 and 2 and not for image 1
+    of the first k tile, so both store paths run side by side."""
     Nb, Nc, Nk, Nw, Nh, Nr, Ns, sw, sh = shape
     rng = np.random.default_rng(sum(shape) + 13)
     In = inputs.f32_to_bf16_bits(rng.integers(-3, 4, size=(Nb, Nc, Nw, Nh)).astype(np.float32))
