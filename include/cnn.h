@@ -86,8 +86,10 @@ typedef enum cnn_kernel {
                          tile's outputs gathered (no halo, no unused rows), 64 channels
                          per stage, raw Ker rows as in CNN_K_IGEMM_RAWK              */
   CNN_K_SMALLC = 4,   /* few input channels, wide stencils (Ns <= 8, ceil(Nc*Nr/2) <= 24),
-                         bf16: K = flattened (c, r, s), Ker in registers, the whole
-                         halo'd slab in LDS; tc of its plans is Nc                    */
+                         bf16: K = flattened (c, r, s), the Ker image and the tile's
+                         halo'd slab in LDS, workgroups walking runs of tiles; tc of
+                         its plans is Nc; variants 1003 and 1103 have the 3-channel
+                         7x7 stride-2 stencil compiled in                            */
   CNN_K_IGEMM_PIPE = 5,/* implicit GEMM, bf16: repacked Ker streamed by DMA, In staged
                          through registers, both double-buffered in LDS               */
   CNN_K_IGEMM_DMA = 6,/* implicit GEMM, bf16: Ker and the natural In rows both copied
