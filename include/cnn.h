@@ -109,9 +109,11 @@ typedef enum cnn_kernel {
                          its plans is Nc                                          */
   CNN_K_GEMM1 = 11,   /* 1x1 layers as a per-pixel GEMM, bf16: In channel rows
                          read by transposing LDS reads, Ker rows as they lie,
-                         both double-buffered in LDS; Nc % 8 == 0, tp a multiple
-                         of 4; strides 1 (Nw*Nh % 4 == 0) or 2 and 2 (Nh % 4 ==
-                         0: 4 output pixels = the even half of 8 input columns) */
+                         both double-buffered in LDS (or, for whole-image tiles
+                         at stride 1, copied by DMA into a four-stage ring);
+                         Nc % 8 == 0, tp a multiple of 4; strides 1 (Nw*Nh % 4
+                         == 0) or 2 and 2 (Nh % 4 == 0: 4 output pixels = the
+                         even half of 8 input columns)                         */
   CNN_K_SROWS = 12,   /* stride-2 layers over bands of whole output rows, bf16:
                          256 features x L rows per workgroup, In rows split by
                          column parity into MFMA-ready LDS units, one stencil
