@@ -180,6 +180,31 @@ def test_plan_is_the_model_minimum(dtype):
             assert not any(_better(c, pf) for c in free if _key(c) != _key(pf)), (p, bud)
 
 
+def test_model_time_is_at_least_the_hbm_floor():
+    """Every candidate's predicted time is at least its HBM bytes (Eq. (3)
+    at the XCD level) at the bandwidth of their read/write mix -- a device
+    copy's 5.0 TB/s for half writes or fewer, rising linearly with the write
+    share to a fill's 6.9 TB/s -- plus the 2 us launch; the stem's traffic
+    is write-dominated (its Out is nine tenths), so it takes the floor's
+    upper end."""
+    def floor_us(pl):
+        out, ker, inp = cnn.hbm_bytes(pl)
+        total = out + ker + inp
+        w = out / total
+        gbs = 5000.0 if w <= 0.5 else 5000.0 + (6900.0 - 5000.0) * (w - 0.5) / 0.5
+        return total / (gbs * 1e3) + 2.0
+    for w in inputs.WORKLOADS:
+        prob = cnn.problem(*w.dims())
+        for c in cnn.plan_candidates(prob, cnn.DTYPES["f32" if w.dtype == "f32" else "bf16"],
+                                     cnn.budget()):
+            if c.kernel in (cnn.K_DIRECT, cnn.K_SPLITC):
+                continue  # direct plans price compulsory bytes; split plans add a reduce
+            assert c.model_us >= floor_us(c) * (1 - 1e-9), (w.name, c.variant, c.model_us)
+    stem = inputs.BY_NAME["stem7x7_s2_b64"]
+    out, ker, inp = cnn.hbm_bytes(cnn.plan(cnn.problem(*stem.dims()), cnn.DTYPES["bf16"], cnn.budget()))
+    assert out / (out + ker + inp) > 0.85
+
+
 def test_candidates_are_complete_plans():
     for w in inputs.WORKLOADS:
         prob = cnn.problem(*w.dims())
