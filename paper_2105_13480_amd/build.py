@@ -22,7 +22,7 @@ LIB = os.path.join(PKG, "libcnn_mi355x.so")
 
 SOURCES = ["cnn_api.cpp", "cnn_select.cpp", "k_direct.hip", "k_igemm.hip", "k_igemm2.hip",
            "k_igemm3.hip", "k_igemm4.hip", "k_smallc.hip", "k_rows.hip", "k_gemm1.hip",
-           "k_srows.hip", "cnn_static.hip"]
+           "k_srows.hip", "k_cslice.hip", "cnn_static.hip"]
 
 ARCH = "gfx950"
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-function",

@@ -247,6 +247,25 @@ const Variant* find_variant(int id) {
   return nullptr;
 }
 
+const VariantC* find_variant_c(int id) {
+  int n = 0;
+  const VariantC* vs = variants_cslice(&n);
+  for (int i = 0; i < n; ++i)
+    if (vs[i].id == id) return &vs[i];
+  return nullptr;
+}
+
+// Geometry a channel-slice plan must carry: the slab, grid and LDS size its
+// tile implies, on a problem the instantiation serves.
+bool cslice_geometry_ok(const VariantC& v, const cnn_plan_t& pl) {
+  const cnn_problem& p = pl.prob;
+  const int64_t Ny = p.sh * (p.Nh - 1) + p.Ns;
+  const int64_t S = slab_rows_max(p, pl.tp);
+  const int64_t grid = ((p.Nb * p.Nw * p.Nh + pl.tp - 1) / pl.tp) * ((p.Nk + v.tk - 1) / v.tk);
+  return cslice_fits(v, p) && pl.slab_rows == S && pl.grid == grid &&
+         pl.lds_bytes == cslice_lds_bytes(v, S, Ny) && pl.lds_bytes <= 160 * 1024;
+}
+
 // Geometry a plain staging plan (and its split form) must carry: the slab,
 // grid and LDS size its tile implies.
 bool igemm_geometry_ok(const Variant& v, const cnn_plan_t& pl) {
@@ -310,18 +329,25 @@ int run_plan(const void* In, const void* Ker, void* Out, const cnn_plan_t& pl, h
     if (dry) return CNN_OK;
     e = launch_srows(*vq, In, Ker, Out, ws, a, pl.lds_bytes, st);
   } else if (pl.kernel == CNN_K_SPLITC) {
-    const Variant* v = find_variant(pl.variant);
+    // the CNN_K_IGEMM tiles split over slices, or the channel-slice kernel
+    const VariantC* vc = find_variant_c(pl.variant);
+    const Variant* v = vc ? nullptr : find_variant(pl.variant);
     const cnn_problem& p = pl.prob;
     const int64_t stages = (p.Nc + pl.tc - 1) / (pl.tc > 0 ? pl.tc : 1);
-    if (!v || v->kernel != CNN_K_IGEMM || v->dtype != pl.dtype || v->tk != pl.tk ||
-        v->tp != pl.tp || v->tc != pl.tc || !igemm_geometry_ok(*v, pl))
+    const bool match =
+        vc ? vc->dtype == pl.dtype && vc->tk == pl.tk && vc->tp == pl.tp && vc->tc == pl.tc &&
+                 cslice_geometry_ok(*vc, pl)
+           : v && v->kernel == CNN_K_IGEMM && v->dtype == pl.dtype && v->tk == pl.tk &&
+                 v->tp == pl.tp && v->tc == pl.tc && igemm_geometry_ok(*v, pl);
+    if (!match)
       return fail(CNN_E_PLAN, "plan names no matching kernel instantiation (variant %d)", pl.variant);
     if (pl.kc < 1 || pl.kc > stages || pl.kc > 65535 ||
         pl.ws_bytes != 4LL * pl.kc * p.Nb * p.Nk * p.Nw * p.Nh)
       return fail(CNN_E_PLAN, "split plan needs 1 <= kc <= %lld and ws_bytes = 4*kc*|Out|",
                   (long long)stages);
     if (dry) return CNN_OK;
-    e = launch_splitc(*v, In, Ker, Out, ws, a, pl.lds_bytes, pl.kc, pl.dtype, st);
+    e = vc ? launch_cslice(*vc, In, Ker, Out, ws, a, pl.lds_bytes, pl.kc, pl.dtype, st)
+           : launch_splitc(*v, In, Ker, Out, ws, a, pl.lds_bytes, pl.kc, pl.dtype, st);
   } else if (pl.kernel == CNN_K_SMALLC) {
     const VariantS* vs = find_variant_s(pl.variant);
     if (!vs || vs->dtype != pl.dtype || vs->tk != pl.tk || !smallc_geometry_ok(*vs, pl))

@@ -401,7 +401,13 @@ static FamilyCost family_cost(int kernel, int variant) {
     case CNN_K_IGEMM_PIPE: return {0.74, 3.80, 2.51, 30.2};
     case CNN_K_IGEMM_DMA: return {0.55, 6.62, 0.93, 34.8};
     case CNN_K_IGEMM_WIDE: return {1.00, 0.00, 7.53, 100.0};
-    case CNN_K_SPLITC: return {0.51, 3.07, 1.65, 4.1};
+    case CNN_K_SPLITC: {
+      int n = 0;
+      const VariantC* vc = variants_cslice(&n);
+      for (int i = 0; i < n; ++i)
+        if (vc[i].id == variant) return {0.50, 1.00, 1.50, 50.0};  // a stage's loads at once
+      return {0.51, 3.07, 1.65, 4.1};
+    }
     case CNN_K_IGEMM: return {0.40, 0.00, 2.14, 3.4};
     default: return {0.25, 0.0, 0.0, 1.0};  // direct: fp32 vector FMAs
   }
@@ -622,6 +628,18 @@ static void splitc_finish(const cnn_problem& p, const cnn_budget& bud, cnn_plan_
   plan->ws_bytes = 4 * kc * p.Nb * p.Nk * p.Nw * p.Nh;
 }
 
+// Channel-slice kernel (conv_cslice): a split form only.
+static bool eval_cslice(const cnn_problem& p, int dtype, const VariantC& v,
+                        const cnn_budget& bud, cnn_plan_t* plan) {
+  if (!cslice_fits(v, p)) return false;
+  const int64_t Ny = p.sh * (p.Nh - 1) + p.Ns;
+  const int64_t S = slab_rows_max(p, v.tp);
+  const int64_t lds = cslice_lds_bytes(v, S, Ny);
+  if (!eval_tiling(p, dtype, v.id, v.tk, v.tp, v.tc, 16, S, lds, 0, bud, plan)) return false;
+  splitc_finish(p, bud, plan);
+  return true;
+}
+
 // Candidate order: the smaller model time; within 2 % of it, fewer
 // predicted HBM bytes (Eq. (3) at the XCD level), then fewer Eq. (1) bytes,
 // then the lower instantiation id.
@@ -695,6 +713,12 @@ int enumerate_plans(const cnn_problem& p, int dtype, const cnn_budget& bud, cnn_
         add(cand, CNN_K_SPLITC);
       }
     }
+  int ncs = 0;
+  const VariantC* vcs = variants_cslice(&ncs);
+  for (int i = 0; i < ncs; ++i)
+    if (vcs[i].dtype == dtype && eval_cslice(p, dtype, vcs[i], bud, &cand) &&
+        cand.grid < bud.cus && ceil_div(p.Nc, cand.tc) > 1)
+      add(cand, CNN_K_SPLITC);
   if (n == 0) {
     direct_plan(p, dtype, bud, &cand);
     if (cap > 0) out[0] = cand;
@@ -738,6 +762,15 @@ int select_plan(const cnn_problem& p, int dtype, const cnn_budget& bud, int kern
         continue;
       if (!eval_variant(p, dtype, v, bud, out)) continue;
       splitc_finish(p, bud, out);
+      out->kernel = CNN_K_SPLITC;
+      fill_common(p, dtype, bud, out);
+      return CNN_OK;
+    }
+    const VariantC* vc = variants_cslice(&n);
+    for (int i = 0; i < n; ++i) {
+      const VariantC& v = vc[i];
+      if (v.dtype != dtype || v.tk != tk || v.tp != tp || v.tc != tc) continue;
+      if (!eval_cslice(p, dtype, v, bud, out)) continue;
       out->kernel = CNN_K_SPLITC;
       fill_common(p, dtype, bud, out);
       return CNN_OK;
@@ -889,6 +922,9 @@ int list_variants(cnn_variant_t* out, int cap) {
   const VariantQ* vq = variants_srows(&c);
   for (int i = 0; i < c; ++i)
     add(CNN_K_SROWS, vq[i].id, vq[i].dtype, vq[i].nr, vq[i].ns, vq[i].L, vq[i].tk, 0, 16);
+  const VariantC* vc = variants_cslice(&c);
+  for (int i = 0; i < c; ++i)
+    add(CNN_K_SPLITC, vc[i].id, vc[i].dtype, vc[i].nr, vc[i].ns, 0, vc[i].tk, vc[i].tp, vc[i].tc);
   return n;
 }
 

@@ -223,6 +223,28 @@ int64_t splitc_slice_channels(int64_t Nc, int64_t tc, int64_t kc);
 hipError_t launch_splitc(const Variant& v, const void* In, const void* Ker, void* Out,
                          void* ws, const ConvArgs& a, int64_t lds_bytes, int kc, int dtype,
                          hipStream_t stream);
+// Out[o] = the sum over the kc fp32 partial Outs Part[z][o], z in order,
+// converted to the Out type of `dtype` (n = |Out| elements).
+hipError_t launch_splitc_reduce(const float* Part, void* Out, int kc, int64_t n, int dtype,
+                                hipStream_t stream);
+
+// A channel-slice instantiation (bf16, fixed stencil): tiles of tk = 32
+// features x tp = 64 outputs over one slice of the channels, tc = 32
+// channels per stage, every load of a stage in flight at once; fp32 partial
+// tiles in the workspace, then the ordered reduce.  A CNN_K_SPLITC family
+// member beside the CNN_K_IGEMM split form.
+struct VariantC {
+  int32_t id;
+  int32_t dtype;
+  int32_t tk, tp, tc;
+  int32_t nr, ns;  // compile-time stencil
+};
+const VariantC* variants_cslice(int* count);
+int64_t cslice_lds_bytes(const VariantC& v, int64_t slab_rows, int64_t Ny);
+bool cslice_fits(const VariantC& v, const cnn_problem& p);  // stencil, Nc % 16, index range
+hipError_t launch_cslice(const VariantC& v, const void* In, const void* Ker, void* Out, void* ws,
+                         const ConvArgs& a, int64_t lds_bytes, int kc, int dtype,
+                         hipStream_t stream);
 hipError_t launch_igemm3(const Variant3& v, const void* In, const void* Ker, void* Out,
                          void* ws, const ConvArgs& a, int64_t lds_bytes, hipStream_t stream);
 // Runs the pipelined kernel; non-raw-Ker variants first pack Ker into `ws`

@@ -342,21 +342,26 @@ int64_t splitc_slice_channels(int64_t Nc, int64_t tc, int64_t kc) {
   return (stages + kc - 1) / kc * tc;
 }
 
+hipError_t launch_splitc_reduce(const float* Part, void* Out, int kc, int64_t n, int dtype,
+                                hipStream_t stream) {
+  int64_t blocks = (n + 255) / 256;
+  if (blocks > 2048) blocks = 2048;  // grid-stride loop covers the rest
+  if (dtype == CNN_BF16_OBF16)
+    hipLaunchKernelGGL(splitc_reduce<bf16_t>, dim3((unsigned)blocks), dim3(256), 0, stream,
+                       Part, (bf16_t*)Out, kc, n);
+  else
+    hipLaunchKernelGGL(splitc_reduce<float>, dim3((unsigned)blocks), dim3(256), 0, stream,
+                       Part, (float*)Out, kc, n);
+  return hipGetLastError();
+}
+
 hipError_t launch_splitc(const Variant& v, const void* In, const void* Ker, void* Out,
                          void* ws, const ConvArgs& a, int64_t lds_bytes, int kc, int dtype,
                          hipStream_t stream) {
   const int cs = (int)splitc_slice_channels(a.Nc, v.tc, kc);
   hipError_t e = launch_igemm_kc(v, In, Ker, ws, a, lds_bytes, stream, kc, cs, true);
   if (e != hipSuccess) return e;
-  int64_t blocks = (a.out_total + 255) / 256;
-  if (blocks > 2048) blocks = 2048;  // grid-stride loop covers the rest
-  if (dtype == CNN_BF16_OBF16)
-    hipLaunchKernelGGL(splitc_reduce<bf16_t>, dim3((unsigned)blocks), dim3(256), 0, stream,
-                       (const float*)ws, (bf16_t*)Out, kc, a.out_total);
-  else
-    hipLaunchKernelGGL(splitc_reduce<float>, dim3((unsigned)blocks), dim3(256), 0, stream,
-                       (const float*)ws, (float*)Out, kc, a.out_total);
-  return hipGetLastError();
+  return launch_splitc_reduce((const float*)ws, Out, kc, a.out_total, dtype, stream);
 }
 
 }  // namespace cnnlib

@@ -136,6 +136,12 @@ def _variant_dims_one(kernel, vid, dt, tk, tp, tc, stencil):
             if _fits(dims, dt, kernel, tk, tp, tc, vid):
                 return dims
         return None
+    if kernel == cnn.K_SPLITC and Nr == Ns and Nr in (1, 3) and tk == 32:
+        # channel-slice kernel: Nc % 16 == 0 (the last stage 16 channels), ragged Nk
+        for dims in [(1, 48, 39, 7, 7, Nr, Ns, 1, 1), (2, 96, 45, 5, 9, Nr, Ns, 2, 1)]:
+            if _fits(dims, dt, kernel, tk, tp, tc, vid):
+                return dims
+        return None
     if kernel == cnn.K_SMALLC:  # few channels: Nc*Nr rows must fit the K-steps
         nc = 3 if Nr == 7 else 9
         cands = [(3, nc, tk + 7, 9, 13, Nr, Ns, 2, 2), (2, nc, tk + 7, 7, 13, Nr, Ns, 1, 1),

@@ -519,14 +519,49 @@ def test_splitc_exact(case):
         assert np.array_equal(got, want), kc
 
 
+# channel-slice kernel (tk 32, tp 64, tc 32): Nc % 16 == 0; the cases span a
+# ragged 16-channel last stage, ragged Nk, tiles across images, strides,
+# 1x1, several stages per slice and empty slices
+CSLICE_CASES = [
+    (1, 512, 512, 7, 7, 3, 3, 1, 1),   # the batch-1 deep layer
+    (1, 48, 39, 7, 7, 3, 3, 1, 1),     # stages of 32 and 16 channels, 39 features
+    (2, 96, 45, 5, 9, 3, 3, 2, 1),     # strides (2, 1), tiles across two images
+    (3, 80, 70, 6, 7, 3, 3, 1, 2),     # strides (1, 2), three k tiles
+    (4, 256, 100, 5, 5, 3, 3, 2, 2),   # stride 2, two p tiles over four images
+    (2, 64, 33, 9, 13, 1, 1, 1, 1),    # 1x1
+]
+
+
+@pytest.mark.parametrize("dims", CSLICE_CASES)
 @pytest.mark.parametrize("mode", ["bf16", "bf16_obf16"])
-def test_splitc_float_late_layer(mode):
+def test_cslice_exact(dims, mode):
+    """Channel-slice kernel: bit-exact with the oracle on integer inputs for
+    kc = 1, 2, stages - 1, stages and the plan's own kc (integer partial sums
+    are exact in fp32)."""
+    Nb, Nc, Nk, Nw, Nh, Nr, Ns, sw, sh = dims
+    In, Ker = _arrays(dims, mode, seed=sum(dims) + 57, dist=("int", -3, 3), kdist=("int", -3, 3))
+    want = oracle.conv(In, Ker, sw, sh)
+    if mode == "bf16_obf16":
+        want = inputs.bf16_bits_to_f32(inputs.f32_to_bf16_bits(want.astype(np.float32))).astype(np.float64)
+    pl = cnn.plan_tiles(cnn.problem(*dims), MODES[mode], cnn.K_SPLITC, 32, 64, 32)
+    assert pl.kernel == cnn.K_SPLITC and pl.variant in (2500, 2501, 2502, 2503)
+    for kc in _splitc_kcs(Nc, 32, pl.kc):
+        pl.kc, pl.ws_bytes = kc, 4 * kc * Nb * Nk * Nw * Nh
+        say(f"[parity] cslice dims={dims} mode={mode} v{pl.variant} grid={pl.grid} kc={kc}")
+        got = run(In, Ker, sw, sh, mode, plan=pl)
+        assert np.array_equal(got, want), kc
+
+
+@pytest.mark.parametrize("tiles", [(64, 64, 32), (32, 64, 32)])
+@pytest.mark.parametrize("mode", ["bf16", "bf16_obf16"])
+def test_splitc_float_late_layer(mode, tiles):
     """The batch-1 deep layer (512 -> 512 channels, 7x7 outputs) on uniform
-    inputs with its split plan (16 slices): every output within the bf16
-    tolerance of the fp64 oracle."""
+    inputs with its split plans (16 slices; the CNN_K_IGEMM tiles and the
+    channel-slice kernel): every output within the bf16 tolerance of the
+    fp64 oracle."""
     w = inputs.BY_NAME["late3x3_b1"]
     In, Ker = inputs.make_inputs(w)
-    pl = cnn.plan_tiles(cnn.problem(*w.dims()), MODES[mode], cnn.K_SPLITC, 64, 64, 32)
+    pl = cnn.plan_tiles(cnn.problem(*w.dims()), MODES[mode], cnn.K_SPLITC, *tiles)
     assert pl.kc > 1
     say(f"[parity] splitc late3x3_b1 mode={mode} v{pl.variant} grid={pl.grid} kc={pl.kc}")
     got = run(In, Ker, 1, 1, mode, plan=pl)
