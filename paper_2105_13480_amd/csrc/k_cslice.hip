@@ -6,11 +6,11 @@
 //
 // Workgroup (tile, z) owns 32 output features x 64 consecutive outputs of the
 // flattened (b, w, h) index (the paper's composite T_bhw) and the channels
-// [z*cs, z*cs + cs) of slice z, in stages of 32 channels.  A stage issues all
-// of its global loads before it waits on any: the tile's Ker rows (32
-// features x 32 channels x all taps, 16-byte loads of the rows as they lie,
-// one feature's 8 channels per thread) and the halo'd In slab of the tile
-// (one position's 8-channel groups per thread).  The stage therefore costs
+// [z*cs, z*cs + cs) of slice z, in stages of TC = 16, 32 or 64 channels.  A
+// stage issues all of its global loads before it waits on any: the tile's
+// Ker rows (32 features x TC channels x all taps, 16-byte loads of the rows
+// as they lie, one feature's 8 channels per thread) and the halo'd In slab
+// of the tile (one position's 8-channel groups per thread).  The stage therefore costs
 // one memory latency rather than one per tap or channel group.  Both then go
 // to LDS in (tap, channel) order:
 //   Ker [tap][c/8][k][8]         an A operand (8 channels of one feature at
@@ -23,10 +23,13 @@
 //
 // GEMM view of a stage: D[k][p] += sum over (tap, c) of Ker[k][c][tap] *
 // In[c][pos(p) + off(tap)] on v_mfma_f32_32x32x16_bf16, a K-step being one
-// tap x 16 channels.  Waves 0 and 1 take outputs 0-31 and 32-63 over half of
-// the K-steps, waves 2 and 3 the same outputs over the other half; the two
-// halves are added through LDS (always in that order), and the slice's fp32
-// partial tile goes to slice z of the workspace.  The ordered reduce of the
+// tap x 16 channels.  The workgroup has two waves per K group -- outputs
+// 0-31 and 32-63 -- and TC / 16 K groups (two for TC = 16), each taking
+// every (TC/16)-th K-step; the groups' accumulators are added through LDS
+// (always in group order), and the slice's fp32 partial tile goes to slice
+// z of the workspace.  On the batch-1 512-channel 3x3 layer TC = 32 (256
+// workgroups) measured fastest: TC = 16 doubles the partials, TC = 64
+// halves the workgroups.  The ordered reduce of the
 // kc slices (splitc_reduce) then writes Out, so the result does not depend
 // on which workgroup finishes first.
 #include "internal.h"
@@ -38,9 +41,6 @@ namespace {
 
 constexpr int kTK = 32;          // output features per tile (one MFMA block of rows)
 constexpr int kTP = 64;          // outputs per tile (two MFMA blocks of columns)
-constexpr int kTC = 32;          // channels per stage
-constexpr int kCG = kTC / 8;     // 8-channel groups per stage
-constexpr int kIPV = kCG + 1;    // 16-byte vectors per In position in LDS (one pad)
 
 __device__ __forceinline__ f32x16_t mfma_bf16(const u32x4_t& a, const u32x4_t& b,
                                               const f32x16_t& c) {
@@ -58,18 +58,29 @@ __device__ __forceinline__ uint32_t half_at(const u32x4_t (&v)[N], int e) {
 
 }  // namespace
 
-template <int NR, int NS>
-__global__ __launch_bounds__(256) void conv_cslice(const bf16_t* __restrict__ In,
+// Waves of a workgroup with stages of TC channels: two per K group, TC / 16
+// K groups (two for TC = 16, whose groups alternate taps).
+template <int TC> struct CsliceShape {
+  static constexpr int NK = TC >= 32 ? TC / 16 : 2;  // K groups
+  static constexpr int NT = 128 * NK;                // threads
+};
+
+template <int NR, int NS, int TC>
+__global__ __launch_bounds__(CsliceShape<TC>::NT) void conv_cslice(const bf16_t* __restrict__ In,
                                                    const bf16_t* __restrict__ Ker,
                                                    float* __restrict__ Part, ConvArgs a, int cs,
                                                    FastDiv dv_nxny) {
   constexpr int T = NR * NS;
+  constexpr int kTC = TC;          // channels per stage (16, 32 or 64)
+  constexpr int kCG = kTC / 8;     // 8-channel groups per stage
+  constexpr int kIPV = kCG + 1;    // 16-byte vectors per In position in LDS (one pad)
+  constexpr int NK = CsliceShape<TC>::NK, NT = CsliceShape<TC>::NT;
   extern __shared__ __attribute__((aligned(16))) char smem[];
   u32x4_t* kl = reinterpret_cast<u32x4_t*>(smem);  // [T][kCG][kTK]
   u32x4_t* il = kl + T * kCG * kTK;                 // [position][kIPV]
 
   const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
+  const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l32 = lane & 31, half = lane >> 5;
   const int pb = wave & 1, kh = wave >> 1;
 
@@ -101,7 +112,7 @@ __global__ __launch_bounds__(256) void conv_cslice(const bf16_t* __restrict__ In
     obase = (int64_t)b * a.Nk * a.hw + q;
   }
 
-  // Ker task of this thread (threads 0 .. 127): feature k0 + kk, its channel
+  // Ker task of this thread (threads 0 .. 4*TC - 1): feature k0 + kk, its channel
   // group kcg of every stage.  Features past Nk stage nothing; their LDS rows
   // feed accumulator rows that are not stored.
   const int kk = tid / kCG, kcg = tid % kCG;
@@ -115,7 +126,8 @@ __global__ __launch_bounds__(256) void conv_cslice(const bf16_t* __restrict__ In
   const int c_begin = (int)blockIdx.y * cs;
   const int c_end = min(a.Nc, c_begin + cs);
   for (int c0 = c_begin; c0 < c_end; c0 += kTC) {
-    const int ncg = min(kTC, c_end - c0) >> 3;  // 2 or 4 (Nc and cs are multiples of 16)
+    const int ncg = min(kTC, c_end - c0) >> 3;  // even (Nc and cs are multiples of 16)
+    static_assert(kTC == 16 || kTC == 32 || kTC == 64, "stages of 16, 32 or 64 channels");
     // Every global load of the stage, Ker first.
     u32x4_t kr[T];
     const bool kload = ktask && kcg < ncg;
@@ -124,7 +136,7 @@ __global__ __launch_bounds__(256) void conv_cslice(const bf16_t* __restrict__ In
 #pragma unroll
       for (int t = 0; t < T; ++t) kr[t] = src[t];
     }
-    for (int base = 0; base < SNt; base += 256) {
+    for (int base = 0; base < SNt; base += NT) {
       const int pos = base + tid;
       if (pos < SNt) {
         const int gp = gpos0 + pos;
@@ -162,14 +174,16 @@ __global__ __launch_bounds__(256) void conv_cslice(const bf16_t* __restrict__ In
     }
     __syncthreads();
 
-    // K-steps (tap t, 16-channel block cb): with 32 channels the waves of
-    // K half kh take cb == kh; with 16, alternate taps.
+    // K-steps j = (tap t, 16-channel block cb), t-major over the stage's
+    // nb blocks; K group kh takes the steps with j % NK == kh (with full
+    // stages: cb == kh).
+    const int nb = ncg >> 1;
 #pragma unroll
     for (int t = 0; t < T; ++t) {
       const int toff = (t / NS) * a.Ny + (t % NS);
 #pragma unroll
-      for (int cb = 0; cb < 2; ++cb) {
-        const bool mine = ncg == 4 ? cb == kh : (cb == 0 && (t & 1) == kh);
+      for (int cb = 0; cb < kCG / 2; ++cb) {
+        const bool mine = cb < nb && (t * nb + cb) % NK == kh;
         if (mine) {
           const u32x4_t av = kl[(t * kCG + 2 * cb + half) * kTK + l32];
           const u32x4_t bv = il[(pix + toff) * kIPV + 2 * cb + half];
@@ -180,13 +194,16 @@ __global__ __launch_bounds__(256) void conv_cslice(const bf16_t* __restrict__ In
     __syncthreads();  // the stage's LDS fully read before the next overwrites it
   }
 
-  // The two K halves' sum (waves 2 and 3 hand theirs to waves 0 and 1), then
-  // the slice's partial tile.  Register j of a 32x32 accumulator holds row
-  // 8*(j/4) + 4*half + j%4 (the feature) of column l32 (the output).
-  float* red = reinterpret_cast<float*>(smem);  // [2][16][64]
-  if (kh == 1) {
+  // The K groups' sum (groups 1 .. NK-1 hand theirs to group 0, which adds
+  // them in group order), then the slice's partial tile.  Register j of a
+  // 32x32 accumulator holds row 8*(j/4) + 4*half + j%4 (the feature) of
+  // column l32 (the output).  (Staging the tile's block in LDS to store
+  // whole lines, written through or not, measured slower than these direct
+  // stores, which overlap other workgroups' work.)
+  float* red = reinterpret_cast<float*>(smem);  // [NK - 1][2][16][64]
+  if (kh > 0) {
 #pragma unroll
-    for (int j = 0; j < 16; ++j) red[(pb * 16 + j) * 64 + lane] = acc[j];
+    for (int j = 0; j < 16; ++j) red[(((kh - 1) * 2 + pb) * 16 + j) * 64 + lane] = acc[j];
   }
   __syncthreads();
   if (kh == 0) {
@@ -194,23 +211,29 @@ __global__ __launch_bounds__(256) void conv_cslice(const bf16_t* __restrict__ In
 #pragma unroll
     for (int j = 0; j < 16; ++j) {
       const int k = k0 + 8 * (j >> 2) + 4 * half + (j & 3);
-      const float v = acc[j] + red[(pb * 16 + j) * 64 + lane];
+      float v = acc[j];
+#pragma unroll
+      for (int g = 1; g < NK; ++g) v += red[(((g - 1) * 2 + pb) * 16 + j) * 64 + lane];
       if (pval && k < a.Nk) dst[obase + (int64_t)k * a.hw] = v;
     }
   }
 }
 
 // ---- instantiation table ------------------------------------------------
-// X(id, dtype, Nr, Ns): the kernel is the same for both bf16 dtypes (the
-// partials are fp32; the reduce writes the Out type).
-#define CNN_CSLICE_VARIANTS(X)    \
-  X(2500, CNN_BF16, 3, 3)         \
-  X(2501, CNN_BF16_OBF16, 3, 3)   \
-  X(2502, CNN_BF16, 1, 1)         \
-  X(2503, CNN_BF16_OBF16, 1, 1)
+// X(id, dtype, Nr, Ns, tc): the kernel is the same for both bf16 dtypes
+// (the partials are fp32; the reduce writes the Out type).
+#define CNN_CSLICE_VARIANTS(X)        \
+  X(2500, CNN_BF16, 3, 3, 32)         \
+  X(2501, CNN_BF16_OBF16, 3, 3, 32)   \
+  X(2502, CNN_BF16, 1, 1, 32)         \
+  X(2503, CNN_BF16_OBF16, 1, 1, 32)   \
+  X(2504, CNN_BF16, 3, 3, 16)         \
+  X(2505, CNN_BF16_OBF16, 3, 3, 16)   \
+  X(2506, CNN_BF16, 3, 3, 64)         \
+  X(2507, CNN_BF16_OBF16, 3, 3, 64)
 
 static const VariantC kVariantsC[] = {
-#define CNN_ROW(id, dt, nr, ns) {id, dt, kTK, kTP, kTC, nr, ns},
+#define CNN_ROW(id, dt, nr, ns, tc) {id, dt, kTK, kTP, tc, nr, ns},
     CNN_CSLICE_VARIANTS(CNN_ROW)
 #undef CNN_ROW
 };
@@ -221,8 +244,10 @@ const VariantC* variants_cslice(int* count) {
 }
 
 int64_t cslice_lds_bytes(const VariantC& v, int64_t slab_rows, int64_t Ny) {
-  const int64_t b = 16 * ((int64_t)v.nr * v.ns * kCG * kTK + slab_rows * Ny * kIPV);
-  return b > 2 * 16 * 64 * 4 ? b : 2 * 16 * 64 * 4;  // at least the K halves' exchange
+  const int64_t cg = v.tc / 8;  // Ker [tap][cg][tk] and In [position][cg + 1] vectors
+  const int64_t b = 16 * ((int64_t)v.nr * v.ns * cg * kTK + slab_rows * Ny * (cg + 1));
+  const int64_t red = 4 * ((v.tc >= 32 ? v.tc / 16 : 2) - 1) * 2 * 16 * 64;  // K groups' exchange
+  return b > red ? b : red;
 }
 
 bool cslice_fits(const VariantC& v, const cnn_problem& p) {
@@ -231,15 +256,16 @@ bool cslice_fits(const VariantC& v, const cnn_problem& p) {
          p.Nb * Nx * Ny < (1LL << 31);  // flattened (b, x, y) positions divided by fdiv
 }
 
-template <int NR, int NS>
+template <int NR, int NS, int TC>
 static hipError_t launch_one_c(const void* In, const void* Ker, void* ws, const ConvArgs& a,
                                int64_t lds, int kc, int cs, hipStream_t stream) {
-  auto kern = conv_cslice<NR, NS>;
+  auto kern = conv_cslice<NR, NS, TC>;
   if (lds > 64 * 1024) {
     const hipError_t e = allow_max_lds((const void*)kern);
     if (e != hipSuccess) return e;
   }
-  hipLaunchKernelGGL(kern, dim3((unsigned)a.grid, (unsigned)kc), dim3(256), (unsigned)lds,
+  hipLaunchKernelGGL(kern, dim3((unsigned)a.grid, (unsigned)kc), dim3(CsliceShape<TC>::NT),
+                     (unsigned)lds,
                      stream, (const bf16_t*)In, (const bf16_t*)Ker, (float*)ws, a, cs,
                      make_fastdiv((uint32_t)a.nxny));
   return hipGetLastError();
@@ -251,9 +277,9 @@ hipError_t launch_cslice(const VariantC& v, const void* In, const void* Ker, voi
   const int cs = (int)splitc_slice_channels(a.Nc, v.tc, kc);
   hipError_t e;
   switch (v.id) {
-#define CNN_CASE(id, dt, nr, ns)                                                 \
+#define CNN_CASE(id, dt, nr, ns, tc)                                            \
   case id:                                                                       \
-    e = launch_one_c<nr, ns>(In, Ker, ws, a, lds_bytes, kc, cs, stream);         \
+    e = launch_one_c<nr, ns, tc>(In, Ker, ws, a, lds_bytes, kc, cs, stream);     \
     break;
     CNN_CSLICE_VARIANTS(CNN_CASE)
 #undef CNN_CASE

@@ -532,27 +532,28 @@ CSLICE_CASES = [
 ]
 
 
-@pytest.mark.parametrize("dims", CSLICE_CASES)
+@pytest.mark.parametrize("dims,tc", [(d, tc) for tc in (32, 16, 64) for d in CSLICE_CASES
+                                     if tc == 32 or d[5] == 3])
 @pytest.mark.parametrize("mode", ["bf16", "bf16_obf16"])
-def test_cslice_exact(dims, mode):
-    """Channel-slice kernel: bit-exact with the oracle on integer inputs for
-    kc = 1, 2, stages - 1, stages and the plan's own kc (integer partial sums
-    are exact in fp32)."""
+def test_cslice_exact(dims, tc, mode):
+    """Channel-slice kernel (stages of 32, 16 or 64 channels): bit-exact with the
+    oracle on integer inputs for kc = 1, 2, stages - 1, stages and the plan's
+    own kc (integer partial sums are exact in fp32)."""
     Nb, Nc, Nk, Nw, Nh, Nr, Ns, sw, sh = dims
     In, Ker = _arrays(dims, mode, seed=sum(dims) + 57, dist=("int", -3, 3), kdist=("int", -3, 3))
     want = oracle.conv(In, Ker, sw, sh)
     if mode == "bf16_obf16":
         want = inputs.bf16_bits_to_f32(inputs.f32_to_bf16_bits(want.astype(np.float32))).astype(np.float64)
-    pl = cnn.plan_tiles(cnn.problem(*dims), MODES[mode], cnn.K_SPLITC, 32, 64, 32)
-    assert pl.kernel == cnn.K_SPLITC and pl.variant in (2500, 2501, 2502, 2503)
-    for kc in _splitc_kcs(Nc, 32, pl.kc):
+    pl = cnn.plan_tiles(cnn.problem(*dims), MODES[mode], cnn.K_SPLITC, 32, 64, tc)
+    assert pl.kernel == cnn.K_SPLITC and 2500 <= pl.variant <= 2507
+    for kc in _splitc_kcs(Nc, tc, pl.kc):
         pl.kc, pl.ws_bytes = kc, 4 * kc * Nb * Nk * Nw * Nh
         say(f"[parity] cslice dims={dims} mode={mode} v{pl.variant} grid={pl.grid} kc={kc}")
         got = run(In, Ker, sw, sh, mode, plan=pl)
         assert np.array_equal(got, want), kc
 
 
-@pytest.mark.parametrize("tiles", [(64, 64, 32), (32, 64, 32)])
+@pytest.mark.parametrize("tiles", [(64, 64, 32), (32, 64, 32), (32, 64, 16), (32, 64, 64)])
 @pytest.mark.parametrize("mode", ["bf16", "bf16_obf16"])
 def test_splitc_float_late_layer(mode, tiles):
     """The batch-1 deep layer (512 -> 512 channels, 7x7 outputs) on uniform
