@@ -131,12 +131,21 @@ typedef enum cnn_kernel {
                          (cnn_plan_tiles: tp = L*Nh, or 0 for any L)           */
   CNN_K_SPLITC = 13,  /* the paper's Case 2 (Sec. 2.1, W_c < N_c; the partial Outs
                          reduced at the end, Sec. 2.3) on one GPU: the
-                         CNN_K_IGEMM tiles (same tk/tp/tc and instantiations)
-                         with the channel loop split over kc workgroup slices
+                         channel loop split over kc workgroup slices
                          (plan.kc); each slice writes fp32 partial sums to the
                          workspace, a second kernel adds the kc slices in slice
                          order and writes Out.  For shapes with few output
-                         tiles and many channels; any dtype and stencil       */
+                         tiles and many channels.  Two kernels: the
+                         CNN_K_IGEMM tiles (same tk/tp/tc and instantiations;
+                         any dtype and stencil), and the channel-slice kernel
+                         (tk 32, tp 64, tc 16/32/64 channels per stage, bf16,
+                         3x3 or 1x1, Nc % 16 == 0), which issues a stage's
+                         loads all at once.  Its atomic-sum instantiations
+                         (cnn_variant_t.mode = 1; fp32 Out) need no
+                         workspace: Out is zeroed, then every slice adds its
+                         partial tile into Out with fp32 atomic adds, so the
+                         summation order -- and the last bits of Out -- may
+                         vary from call to call                               */
   CNN_K_AUTO_NO_WORKSPACE = 14 /* (cnn_plan_tiles only) the model's choice among the
                          plans that need no workspace: the plan cnn_fwd runs
                          when no cnn_plan_find result is cached              */
@@ -169,7 +178,8 @@ typedef struct cnn_plan_t {
   int32_t kc;           /* CNN_K_SPLITC: channel slices (the paper's P_c), 1 ..
                            ceil(Nc/tc); slice z takes channels [z*cs, z*cs + cs),
                            cs = ceil(ceil(Nc/tc)/kc)*tc; a caller may change it
-                           and must then set ws_bytes = 4*kc*Nb*Nk*Nw*Nh.
+                           and must then set ws_bytes = 4*kc*Nb*Nk*Nw*Nh (0
+                           for the atomic-sum instantiations).
                            cnn_plan_tiles picks the smallest kc with no empty
                            slice that gives at least two workgroups per CU,
                            else ceil(Nc/tc).  0 for the other kernels.        */
@@ -204,6 +214,10 @@ typedef struct cnn_plan_t {
  * else cnn_plan's choice (computed on the first call and cached).  Only
  * plans that need no workspace are ever used here, so cnn_fwd allocates no
  * device memory, never synchronises, and may be captured into a HIP graph.
+ * For layers with few outputs and many channels that plan may be the
+ * atomic-sum channel split (CNN_K_SPLITC, fp32 Out), whose summation order
+ * and hence last bits vary between calls; run a CNN_K_SPLITC plan with a
+ * workspace (cnn_fwd_plan_ws) for a fixed order.
  * See the file header for layouts.  Errors: CNN_E_NULL, CNN_E_SHAPE,
  * CNN_E_DTYPE, CNN_E_OVERFLOW, CNN_E_ALIAS, CNN_E_HIP.
  */
@@ -253,7 +267,9 @@ typedef struct cnn_variant_t {
   int32_t nr, ns;       /* compile-time stencil, 0 = any                          */
   int32_t mode;         /* CNN_K_GEMM1: 0 stride 1, 1 strides 2, 2 whole-image
                            DMA ring; CNN_K_SROWS: output rows per band;
-                           CNN_K_ROWS: 32-position blocks per input row; else 0 */
+                           CNN_K_ROWS: 32-position blocks per input row;
+                           CNN_K_SPLITC: 1 for the atomic-sum (workspace-free)
+                           channel-slice instantiations; else 0          */
   int64_t tk;           /* output features per workgroup                          */
   int64_t tp;           /* largest tile of outputs, 0 where the problem sets it   */
   int64_t tc;           /* input channels per stage, 0 = all; CNN_K_ROWS: the

@@ -29,9 +29,15 @@
 // (always in group order), and the slice's fp32 partial tile goes to slice
 // z of the workspace.  On the batch-1 512-channel 3x3 layer TC = 32 (256
 // workgroups) measured fastest: TC = 16 doubles the partials, TC = 64
-// halves the workgroups.  The ordered reduce of the
-// kc slices (splitc_reduce) then writes Out, so the result does not depend
-// on which workgroup finishes first.
+// halves the workgroups.  The ordered reduce of the kc slices
+// (splitc_reduce) then writes Out, so the result does not depend on which
+// workgroup finishes first.
+//
+// Workspace-free instantiations (ATOM, fp32 Out): a fill kernel zeroes Out,
+// then every slice adds its partial tile into Out with fp32 atomic adds.
+// The sum is then formed in the order the workgroups arrive, so the last
+// bits of Out may differ from call to call (integer-valued sums excepted:
+// they are exact in any order).
 #include "internal.h"
 #include "common.h"
 
@@ -65,7 +71,7 @@ template <int TC> struct CsliceShape {
   static constexpr int NT = 128 * NK;                // threads
 };
 
-template <int NR, int NS, int TC>
+template <int NR, int NS, int TC, bool ATOM>
 __global__ __launch_bounds__(CsliceShape<TC>::NT) void conv_cslice(const bf16_t* __restrict__ In,
                                                    const bf16_t* __restrict__ Ker,
                                                    float* __restrict__ Part, ConvArgs a, int cs,
@@ -207,33 +213,41 @@ __global__ __launch_bounds__(CsliceShape<TC>::NT) void conv_cslice(const bf16_t*
   }
   __syncthreads();
   if (kh == 0) {
-    float* dst = Part + (int64_t)blockIdx.y * a.out_total;
+    float* dst = ATOM ? Part : Part + (int64_t)blockIdx.y * a.out_total;
 #pragma unroll
     for (int j = 0; j < 16; ++j) {
       const int k = k0 + 8 * (j >> 2) + 4 * half + (j & 3);
       float v = acc[j];
 #pragma unroll
       for (int g = 1; g < NK; ++g) v += red[(((g - 1) * 2 + pb) * 16 + j) * 64 + lane];
-      if (pval && k < a.Nk) dst[obase + (int64_t)k * a.hw] = v;
+      if (pval && k < a.Nk) {
+        if (ATOM)
+          unsafeAtomicAdd(dst + obase + (int64_t)k * a.hw, v);  // hardware fp32 add
+        else
+          dst[obase + (int64_t)k * a.hw] = v;
+      }
     }
   }
 }
 
 // ---- instantiation table ------------------------------------------------
-// X(id, dtype, Nr, Ns, tc): the kernel is the same for both bf16 dtypes
-// (the partials are fp32; the reduce writes the Out type).
-#define CNN_CSLICE_VARIANTS(X)        \
-  X(2500, CNN_BF16, 3, 3, 32)         \
-  X(2501, CNN_BF16_OBF16, 3, 3, 32)   \
-  X(2502, CNN_BF16, 1, 1, 32)         \
-  X(2503, CNN_BF16_OBF16, 1, 1, 32)   \
-  X(2504, CNN_BF16, 3, 3, 16)         \
-  X(2505, CNN_BF16_OBF16, 3, 3, 16)   \
-  X(2506, CNN_BF16, 3, 3, 64)         \
-  X(2507, CNN_BF16_OBF16, 3, 3, 64)
+// X(id, dtype, Nr, Ns, tc, atom): the kernel is the same for both bf16
+// dtypes (the partials are fp32; the reduce writes the Out type); the
+// atomic-sum instantiations need fp32 Out.
+#define CNN_CSLICE_VARIANTS(X)           \
+  X(2500, CNN_BF16, 3, 3, 32, 0)         \
+  X(2501, CNN_BF16_OBF16, 3, 3, 32, 0)   \
+  X(2502, CNN_BF16, 1, 1, 32, 0)         \
+  X(2503, CNN_BF16_OBF16, 1, 1, 32, 0)   \
+  X(2504, CNN_BF16, 3, 3, 16, 0)         \
+  X(2505, CNN_BF16_OBF16, 3, 3, 16, 0)   \
+  X(2506, CNN_BF16, 3, 3, 64, 0)         \
+  X(2507, CNN_BF16_OBF16, 3, 3, 64, 0)   \
+  X(2508, CNN_BF16, 3, 3, 32, 1)         \
+  X(2509, CNN_BF16, 1, 1, 32, 1)
 
 static const VariantC kVariantsC[] = {
-#define CNN_ROW(id, dt, nr, ns, tc) {id, dt, kTK, kTP, tc, nr, ns},
+#define CNN_ROW(id, dt, nr, ns, tc, atom) {id, dt, kTK, kTP, tc, nr, ns, atom},
     CNN_CSLICE_VARIANTS(CNN_ROW)
 #undef CNN_ROW
 };
@@ -256,10 +270,22 @@ bool cslice_fits(const VariantC& v, const cnn_problem& p) {
          p.Nb * Nx * Ny < (1LL << 31);  // flattened (b, x, y) positions divided by fdiv
 }
 
-template <int NR, int NS, int TC>
+__global__ __launch_bounds__(256) void cslice_zero(float* __restrict__ Out, int64_t n) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t o = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; o < n; o += stride) Out[o] = 0.f;
+}
+
+// ws: the partial slices, or (ATOM) Out itself, zeroed first.
+template <int NR, int NS, int TC, bool ATOM>
 static hipError_t launch_one_c(const void* In, const void* Ker, void* ws, const ConvArgs& a,
                                int64_t lds, int kc, int cs, hipStream_t stream) {
-  auto kern = conv_cslice<NR, NS, TC>;
+  auto kern = conv_cslice<NR, NS, TC, ATOM>;
+  if (ATOM) {
+    int64_t blocks = (a.out_total + 255) / 256;
+    if (blocks > 2048) blocks = 2048;  // grid-stride loop covers the rest
+    hipLaunchKernelGGL(cslice_zero, dim3((unsigned)blocks), dim3(256), 0, stream, (float*)ws,
+                       a.out_total);
+  }
   if (lds > 64 * 1024) {
     const hipError_t e = allow_max_lds((const void*)kern);
     if (e != hipSuccess) return e;
@@ -277,16 +303,17 @@ hipError_t launch_cslice(const VariantC& v, const void* In, const void* Ker, voi
   const int cs = (int)splitc_slice_channels(a.Nc, v.tc, kc);
   hipError_t e;
   switch (v.id) {
-#define CNN_CASE(id, dt, nr, ns, tc)                                            \
-  case id:                                                                       \
-    e = launch_one_c<nr, ns, tc>(In, Ker, ws, a, lds_bytes, kc, cs, stream);     \
+#define CNN_CASE(id, dt, nr, ns, tc, atom)                                          \
+  case id:                                                                           \
+    e = launch_one_c<nr, ns, tc, atom>(In, Ker, atom ? Out : ws, a, lds_bytes, kc, cs, \
+                                       stream);                                      \
     break;
     CNN_CSLICE_VARIANTS(CNN_CASE)
 #undef CNN_CASE
     default:
       return hipErrorInvalidValue;
   }
-  if (e != hipSuccess) return e;
+  if (e != hipSuccess || v.atom) return e;
   return launch_splitc_reduce((const float*)ws, Out, kc, a.out_total, dtype, stream);
 }
 

@@ -403,6 +403,32 @@ def test_splitc_bad_slice_count_rejected_before_hip():
         assert st == -8, (kc, ws)
 
 
+def test_channel_slice_plans():
+    """The channel-slice instantiations (CNN_K_SPLITC, tk 32, tp 64): on the
+    batch-1 deep layer the workspace form keeps 16 fp32 partial Outs and is
+    the model's plan; the atomic-sum form needs no workspace and is the
+    workspace-free plan (the one cnn_fwd runs); a workspace size on the
+    atomic form, or none on the ordered form, is refused before HIP."""
+    bud = cnn.budget()
+    p = cnn.problem(1, 512, 512, 7, 7, 3, 3, 1, 1)
+    ws = cnn.plan(p, cnn.CNN_BF16, bud)
+    assert (ws.kernel, ws.variant, ws.kc, ws.grid) == (cnn.K_SPLITC, 2500, 16, 16)
+    assert ws.ws_bytes == 4 * 16 * 512 * 49
+    free = cnn.plan_tiles(p, cnn.CNN_BF16, cnn.K_AUTO_NO_WORKSPACE, 0, 0, 0, bud)
+    assert (free.kernel, free.variant, free.kc, free.ws_bytes) == (cnn.K_SPLITC, 2508, 16, 0)
+    assert free.model_us > ws.model_us
+    # bf16 Out has no atomic form: its workspace-free plan is another family
+    free_b = cnn.plan_tiles(p, cnn.CNN_BF16_OBF16, cnn.K_AUTO_NO_WORKSPACE, 0, 0, 0, bud)
+    assert free_b.kernel != cnn.K_SPLITC
+    L = cnn.lib()
+    for pl, bad_ws in [(free, 4 * 16 * 512 * 49), (ws, 0)]:
+        q = cnn.Plan.from_buffer_copy(pl)
+        q.ws_bytes = bad_ws
+        st = L.cnn_fwd_plan_ws(0x1000, 0x10000000, 0x20000000, ctypes.byref(p), cnn.CNN_BF16,
+                               ctypes.byref(q), 0x40000000, 1 << 30, None)
+        assert st == -8, pl.variant
+
+
 def test_workspace_plans_need_the_workspace_form():
     """cnn_fwd_plan never allocates: a plan that needs a workspace is
     refused before any HIP call; cnn_fwd_plan_ws checks the workspace."""

@@ -553,6 +553,39 @@ def test_cslice_exact(dims, tc, mode):
         assert np.array_equal(got, want), kc
 
 
+@pytest.mark.parametrize("dims", CSLICE_CASES)
+def test_cslice_atomic_exact(dims):
+    """Workspace-free channel slices (atomic adds into a zeroed fp32 Out):
+    bit-exact with the oracle on integer inputs, whose sums are exact in any
+    order, for kc = 1, 2, stages - 1, stages and the plan's own kc; every
+    call overwrites Out (a NaN fill first)."""
+    Nb, Nc, Nk, Nw, Nh, Nr, Ns, sw, sh = dims
+    In, Ker = _arrays(dims, "bf16", seed=sum(dims) + 91, dist=("int", -3, 3), kdist=("int", -3, 3))
+    want = oracle.conv(In, Ker, sw, sh)
+    vid = 2508 if Nr == 3 else 2509
+    pl = variant_plan(dims, cnn.CNN_BF16, cnn.K_SPLITC, 32, 64, 32, vid)
+    assert pl is not None and pl.variant == vid and pl.ws_bytes == 0
+    for kc in _splitc_kcs(Nc, 32, pl.kc):
+        pl.kc = kc
+        say(f"[parity] cslice atomic dims={dims} v{vid} grid={pl.grid} kc={kc}")
+        got = run(In, Ker, sw, sh, "bf16", plan=pl)
+        assert np.array_equal(got, want), kc
+
+
+def test_cslice_atomic_is_the_workspace_free_late_layer_plan():
+    """cnn_fwd's plan for the batch-1 deep layer (no workspace) is the atomic
+    channel-slice one, within the bf16 tolerance of the fp64 oracle."""
+    w = inputs.BY_NAME["late3x3_b1"]
+    In, Ker = inputs.make_inputs(w)
+    pl = cnn.plan_tiles(cnn.problem(*w.dims()), cnn.CNN_BF16, cnn.K_AUTO_NO_WORKSPACE)
+    assert pl.kernel == cnn.K_SPLITC and pl.variant == 2508 and pl.ws_bytes == 0
+    say("[parity] cnn_fwd late3x3_b1 (atomic channel slices)")
+    got = run(In, Ker, 1, 1, "bf16")
+    want, absv = oracle.conv(In, Ker, 1, 1, with_abs=True)
+    nw, cond, _ = errors(got, want, absv)
+    assert nw < TOL["bf16"] and cond < TOL["bf16"], (nw, cond)
+
+
 @pytest.mark.parametrize("tiles", [(64, 64, 32), (32, 64, 32), (32, 64, 16), (32, 64, 64)])
 @pytest.mark.parametrize("mode", ["bf16", "bf16_obf16"])
 def test_splitc_float_late_layer(mode, tiles):
