@@ -49,7 +49,8 @@ DEFAULT_WORKLOAD = "conv3x3_s2_b64"
 # code comes from its family's source, the shared headers and the launch
 # path, not from the other families' sources or the plan selector.
 FAMILY_SOURCE = {"rows": "k_rows.hip", "srows": "k_srows.hip", "gemm1": "k_gemm1.hip",
-                 "smallc": "k_smallc.hip", "igemm": "k_igemm.hip", "splitc": "k_igemm.hip",
+                 "smallc": "k_smallc.hip", "igemm": "k_igemm.hip",
+                 "splitc": ("k_igemm.hip", "k_cslice.hip"),
                  "pointwise": "k_igemm2.hip", "igemm_pipe": "k_igemm2.hip",
                  "igemm_rawk": "k_igemm2.hip", "igemm_dma": "k_igemm3.hip",
                  "igemm_wide": "k_igemm4.hip", "direct": "k_direct.hip"}
@@ -60,7 +61,9 @@ def kernel_source_hash(family: str) -> str:
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2105_13480_amd", "csrc")
     for f in sorted(os.listdir(csrc)):
-        if (f.startswith("k_") and f != FAMILY_SOURCE.get(family)) or f in NOT_COUNTED:
+        own = FAMILY_SOURCE.get(family, ())
+        own = (own,) if isinstance(own, str) else own
+        if (f.startswith("k_") and f not in own) or f in NOT_COUNTED:
             continue
         with open(os.path.join(csrc, f), "rb") as fh:
             h.update(f.encode() + b"\0" + fh.read())

@@ -13,8 +13,11 @@
 // of the tile (one position's 8-channel groups per thread).  The stage therefore costs
 // one memory latency rather than one per tap or channel group.  Both then go
 // to LDS in (tap, channel) order:
-//   Ker [tap][c/8][k][8]         an A operand (8 channels of one feature at
-//                                one tap) is one 16-byte read;
+//   Ker [tap][c/8][k (+1)][8]    an A operand (8 channels of one feature at
+//                                one tap) is one 16-byte read; one pad
+//                                vector per 32 features keeps the four
+//                                channel groups a thread quad writes off
+//                                one bank;
 //   In  [position][c/8 (+1)][8]  a B operand (8 channels of one position) is
 //                                one 16-byte read; one pad vector per
 //                                position spreads 32 lanes over the banks.
@@ -47,6 +50,7 @@ namespace {
 
 constexpr int kTK = 32;          // output features per tile (one MFMA block of rows)
 constexpr int kTP = 64;          // outputs per tile (two MFMA blocks of columns)
+constexpr int kKS = kTK + 1;     // LDS vectors per (tap, channel group) of Ker (one pad)
 
 __device__ __forceinline__ f32x16_t mfma_bf16(const u32x4_t& a, const u32x4_t& b,
                                               const f32x16_t& c) {
@@ -82,8 +86,8 @@ __global__ __launch_bounds__(CsliceShape<TC>::NT) void conv_cslice(const bf16_t*
   constexpr int kIPV = kCG + 1;    // 16-byte vectors per In position in LDS (one pad)
   constexpr int NK = CsliceShape<TC>::NK, NT = CsliceShape<TC>::NT;
   extern __shared__ __attribute__((aligned(16))) char smem[];
-  u32x4_t* kl = reinterpret_cast<u32x4_t*>(smem);  // [T][kCG][kTK]
-  u32x4_t* il = kl + T * kCG * kTK;                 // [position][kIPV]
+  u32x4_t* kl = reinterpret_cast<u32x4_t*>(smem);  // [T][kCG][kKS]
+  u32x4_t* il = kl + T * kCG * kKS;                 // [position][kIPV]
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -175,7 +179,7 @@ __global__ __launch_bounds__(CsliceShape<TC>::NT) void conv_cslice(const bf16_t*
 #pragma unroll
         for (int m = 0; m < 4; ++m)
           v[m] = half_at(kr, 2 * m * T + t) | (half_at(kr, (2 * m + 1) * T + t) << 16);
-        kl[(t * kCG + kcg) * kTK + kk] = v;
+        kl[(t * kCG + kcg) * kKS + kk] = v;
       }
     }
     __syncthreads();
@@ -191,7 +195,7 @@ __global__ __launch_bounds__(CsliceShape<TC>::NT) void conv_cslice(const bf16_t*
       for (int cb = 0; cb < kCG / 2; ++cb) {
         const bool mine = cb < nb && (t * nb + cb) % NK == kh;
         if (mine) {
-          const u32x4_t av = kl[(t * kCG + 2 * cb + half) * kTK + l32];
+          const u32x4_t av = kl[(t * kCG + 2 * cb + half) * kKS + l32];
           const u32x4_t bv = il[(pix + toff) * kIPV + 2 * cb + half];
           acc = mfma_bf16(av, bv, acc);
         }
@@ -258,8 +262,8 @@ const VariantC* variants_cslice(int* count) {
 }
 
 int64_t cslice_lds_bytes(const VariantC& v, int64_t slab_rows, int64_t Ny) {
-  const int64_t cg = v.tc / 8;  // Ker [tap][cg][tk] and In [position][cg + 1] vectors
-  const int64_t b = 16 * ((int64_t)v.nr * v.ns * cg * kTK + slab_rows * Ny * (cg + 1));
+  const int64_t cg = v.tc / 8;  // Ker [tap][cg][tk + 1] and In [position][cg + 1] vectors
+  const int64_t b = 16 * ((int64_t)v.nr * v.ns * cg * kKS + slab_rows * Ny * (cg + 1));
   const int64_t red = 4 * ((v.tc >= 32 ? v.tc / 16 : 2) - 1) * 2 * 16 * 64;  // K groups' exchange
   return b > red ? b : red;
 }
