@@ -280,12 +280,15 @@ int cnn_variants(cnn_variant_t* out, int cap, int* count);
 
 /*
  * Empirical selection among the candidates of cnn_plan_candidates (every
- * tiling whose footprint fits the current device's budget): runs each on
- * the caller's buffers on `stream`, times it with HIP events (one untimed
- * run, then 3-20 timed runs), times the candidates within 15 % of the
- * fastest (at most four) again over three interleaved rounds of 10-100
- * runs, and returns the one with the fastest round in *plan (that round's
- * mean time in *best_ms when best_ms is not NULL).  The winner may need a
+ * tiling whose footprint fits the current device's budget): after about
+ * 0.2 s of warm-up runs (clocks up from idle), runs each on the caller's
+ * buffers on `stream`, times it with HIP events (one untimed run, then 3-20
+ * timed runs; a candidate faster than 50 us a run is timed again as a
+ * replay of those runs captured into a HIP graph on a private stream, so
+ * that launch overhead does not rank short kernels), times the candidates
+ * within 25 % of the fastest (at most six) again over three interleaved
+ * rounds of 10-100 runs, and returns the one with the fastest round in
+ * *plan (that round's mean time in *best_ms when best_ms is not NULL).  The winner may need a
  * workspace (plan->ws_bytes > 0, run it with cnn_fwd_plan_ws); the fastest
  * candidate that needs none is cached for (problem, dtype, device), so
  * later cnn_fwd calls use it.  Candidates that need a workspace are timed

@@ -7,6 +7,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <chrono>
 #include <map>
 #include <set>
 #include <mutex>
@@ -628,32 +629,85 @@ int cnn_plan_find(const void* In, const void* Ker, void* Out, const cnn_problem*
     if (ws) (void)hipFree(ws);
     return fail(CNN_E_HIP, "hipEventCreate: %s", hipGetErrorString(e));
   }
-  // Times `reps` back-to-back runs of candidate i.
-  auto time_it = [&](int i, int reps, float* ms) -> int {
+  // Times `reps` back-to-back runs of candidate i: launched one by one, or
+  // (graph) captured on a private stream into a HIP graph replayed on the
+  // caller's stream.  Eager launches of kernels shorter than a few
+  // microseconds time the host's launch rate rather than the kernels; a
+  // graph replay times the kernels, as a captured caller runs them.
+  auto time_it = [&](int i, int reps, float* ms, bool graph) -> int {
     int s2;
-    if ((e = hipEventRecord(e0, hs)) != hipSuccess) return fail(CNN_E_HIP, "hipEventRecord: %s", hipGetErrorString(e));
-    for (int r = 0; r < reps; ++r)
-      if ((s2 = run_plan(In, Ker, Out, cands[i], hs, ws))) return s2;
+    hipGraphExec_t exec = nullptr;
+    if (graph) {
+      hipStream_t cs = nullptr;
+      hipGraph_t g = nullptr;
+      if ((e = hipStreamCreateWithFlags(&cs, hipStreamNonBlocking)) != hipSuccess)
+        return fail(CNN_E_HIP, "hipStreamCreate: %s", hipGetErrorString(e));
+      s2 = CNN_OK;
+      if ((e = hipStreamBeginCapture(cs, hipStreamCaptureModeThreadLocal)) == hipSuccess) {
+        for (int r = 0; r < reps && s2 == CNN_OK; ++r) s2 = run_plan(In, Ker, Out, cands[i], cs, ws);
+        const hipError_t e2 = hipStreamEndCapture(cs, &g);
+        if (e == hipSuccess) e = e2;
+      }
+      if (e == hipSuccess && s2 == CNN_OK) e = hipGraphInstantiate(&exec, g, nullptr, nullptr, 0);
+      if (g) (void)hipGraphDestroy(g);
+      (void)hipStreamDestroy(cs);
+      if (s2 != CNN_OK) return s2;
+      if (e != hipSuccess) return fail(CNN_E_HIP, "graph capture: %s", hipGetErrorString(e));
+      if ((e = hipGraphLaunch(exec, hs)) != hipSuccess) {  // first replay: untimed
+        (void)hipGraphExecDestroy(exec);
+        return fail(CNN_E_HIP, "hipGraphLaunch: %s", hipGetErrorString(e));
+      }
+    }
+    if ((e = hipEventRecord(e0, hs)) != hipSuccess) {
+      if (exec) (void)hipGraphExecDestroy(exec);
+      return fail(CNN_E_HIP, "hipEventRecord: %s", hipGetErrorString(e));
+    }
+    if (exec) {
+      e = hipGraphLaunch(exec, hs);
+      if (e != hipSuccess) {
+        (void)hipGraphExecDestroy(exec);
+        return fail(CNN_E_HIP, "hipGraphLaunch: %s", hipGetErrorString(e));
+      }
+    } else {
+      for (int r = 0; r < reps; ++r)
+        if ((s2 = run_plan(In, Ker, Out, cands[i], hs, ws))) return s2;
+    }
     if ((e = hipEventRecord(e1, hs)) != hipSuccess || (e = hipEventSynchronize(e1)) != hipSuccess ||
-        (e = hipEventElapsedTime(ms, e0, e1)) != hipSuccess)
+        (e = hipEventElapsedTime(ms, e0, e1)) != hipSuccess) {
+      if (exec) (void)hipGraphExecDestroy(exec);
       return fail(CNN_E_HIP, "timing: %s", hipGetErrorString(e));
+    }
+    if (exec) (void)hipGraphExecDestroy(exec);
     *ms /= (float)reps;
     return CNN_OK;
   };
+  const float kGraphBelowMs = 0.05f;  // candidates faster than this are timed by graph replay
   st = CNN_OK;
+  // Warm-up: about 0.2 s of the first candidate, so that the first pass does
+  // not time kernels while the clocks are still rising from idle.
+  if (n > 0) {
+    const auto t_start = std::chrono::steady_clock::now();
+    for (int round = 0; round < 100000 && st == CNN_OK; ++round) {
+      for (int r = 0; r < 8 && st == CNN_OK; ++r) st = run_plan(In, Ker, Out, cands[0], hs, ws);
+      if (st == CNN_OK && (e = hipStreamSynchronize(hs)) != hipSuccess)
+        st = fail(CNN_E_HIP, "warm-up: %s", hipGetErrorString(e));
+      if (std::chrono::steady_clock::now() - t_start > std::chrono::milliseconds(200)) break;
+    }
+  }
   std::vector<float> first(n, 0.f), final_t(n, 0.f);
   for (int i = 0; i < n && st == CNN_OK; ++i) {
     float t1 = 0.f, t = 0.f;
-    if ((st = time_it(i, 1, &t1))) break;  // first run: caches
+    if ((st = time_it(i, 1, &t1, false))) break;  // first run: caches
     const int reps = t1 <= 0.f ? 20 : std::max(3, std::min(20, (int)(2.0f / t1)));
-    if ((st = time_it(i, reps, &t))) break;
+    if ((st = time_it(i, reps, &t, false))) break;
+    if (t < kGraphBelowMs && (st = time_it(i, reps, &t, true))) break;
     first[i] = final_t[i] = t;
   }
   // The fastest candidates (overall, and among those that need no
-  // workspace) and those within 15 % of them are timed again, interleaved
-  // over three rounds of longer runs, and ranked by their fastest round: one
-  // short run per candidate differs by a few per cent from run to run, and
-  // the clocks may still be rising during the first pass.
+  // workspace) and those within 25 % of them (at most six of each) are
+  // timed again, interleaved over three rounds of longer runs, and ranked
+  // by their fastest round: one short run per candidate differs by a few
+  // per cent from run to run.
   auto argmin = [&](const std::vector<float>& t, bool ws_free) {
     int b = -1;
     for (int i = 0; i < n; ++i)
@@ -667,9 +721,9 @@ int cnn_plan_find(const void* In, const void* Ker, void* Out, const cnn_problem*
       if (b < 0) continue;
       std::vector<int> near;
       for (int i = 0; i < n; ++i)
-        if ((pass == 0 || cands[i].ws_bytes == 0) && first[i] <= 1.15f * first[b]) near.push_back(i);
+        if ((pass == 0 || cands[i].ws_bytes == 0) && first[i] <= 1.25f * first[b]) near.push_back(i);
       std::sort(near.begin(), near.end(), [&](int x, int y) { return first[x] < first[y]; });
-      if (near.size() > 4) near.resize(4);
+      if (near.size() > 6) near.resize(6);
       for (int i : near)
         if (std::find(fin.begin(), fin.end(), i) == fin.end()) fin.push_back(i);
     }
@@ -679,7 +733,7 @@ int cnn_plan_find(const void* In, const void* Ker, void* Out, const cnn_problem*
           const float t0 = first[fin[f]];
           const int reps = t0 <= 0.f ? 50 : std::max(10, std::min(100, (int)(0.5f / t0)));
           float t = 0.f;
-          if ((st = time_it(fin[f], reps, &t))) break;
+          if ((st = time_it(fin[f], reps, &t, t0 < kGraphBelowMs))) break;
           if (round == 0 || t < final_t[fin[f]]) final_t[fin[f]] = t;
         }
     }
