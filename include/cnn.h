@@ -19,8 +19,9 @@
  *
  * Ownership: the caller owns all three buffers, which are device pointers
  * on the current HIP device.  The library keeps no pointer after a call,
- * never writes In or Ker, and fully overwrites Out (Out is never read, so
- * its prior contents do not matter).  Out must not overlap In or Ker.
+ * never writes In or Ker, and fully overwrites Out (its prior contents do
+ * not matter; only the atomic-sum channel split reads it, after zeroing
+ * it).  Out must not overlap In or Ker.
  *
  * Streams: every compute call is asynchronous on `stream` (a hipStream_t
  * passed as void*; NULL is the null stream).  There is no implicit
