@@ -572,6 +572,33 @@ def test_cslice_atomic_exact(dims):
         assert np.array_equal(got, want), kc
 
 
+def test_cslice_atomic_in_graph():
+    """The atomic-sum channel split (zero fill, then atomic adds into Out)
+    captured into a HIP graph and replayed several times, with eager work
+    and a NaN fill of Out between replays: every replay equals the oracle
+    exactly on integer inputs (exact in any summation order)."""
+    import torch
+    dims = (1, 96, 70, 7, 7, 3, 3, 1, 1)
+    In, Ker = _arrays(dims, "bf16", seed=123, dist=("int", -3, 3), kdist=("int", -3, 3))
+    want = oracle.conv(In, Ker, 1, 1)
+    pl = variant_plan(dims, cnn.CNN_BF16, cnn.K_SPLITC, 32, 64, 32, 2508)
+    assert pl is not None and pl.ws_bytes == 0 and pl.kc > 1
+    dIn, dKer = to_gpu(In), to_gpu(Ker)
+    out = out_tensor(1, 70, 7, 7, "bf16")
+    s = torch.cuda.Stream()
+    g = torch.cuda.CUDAGraph()
+    say(f"[parity] cslice atomic graph capture kc={pl.kc}")
+    with torch.cuda.graph(g, stream=s):
+        cnn.fwd_plan(dIn, dKer, out, pl)
+    for i in range(4):
+        out.fill_(float("nan"))
+        torch.cuda.synchronize()
+        say(f"[parity] cslice atomic graph replay {i}")
+        g.replay()
+        torch.cuda.synchronize()
+        assert np.array_equal(to_host64(out), want), i
+
+
 def test_cslice_atomic_is_the_workspace_free_late_layer_plan():
     """cnn_fwd's plan for the batch-1 deep layer (no workspace) is the atomic
     channel-slice one, within the bf16 tolerance of the fp64 oracle."""
