@@ -146,7 +146,10 @@ typedef enum cnn_kernel {
                          workspace: Out is zeroed, then every slice adds its
                          partial tile into Out with fp32 atomic adds, so the
                          summation order -- and the last bits of Out -- may
-                         vary from call to call                               */
+                         vary from call to call.  Its direct instantiations
+                         (mode = 2; 3x3, either Out type; kc = 1) need none
+                         either: one slice of 128-channel stages per
+                         1024-thread workgroup writes Out in a fixed order */
   CNN_K_AUTO_NO_WORKSPACE = 14 /* (cnn_plan_tiles only) the model's choice among the
                          plans that need no workspace: the plan cnn_fwd runs
                          when no cnn_plan_find result is cached              */
@@ -180,7 +183,8 @@ typedef struct cnn_plan_t {
                            ceil(Nc/tc); slice z takes channels [z*cs, z*cs + cs),
                            cs = ceil(ceil(Nc/tc)/kc)*tc; a caller may change it
                            and must then set ws_bytes = 4*kc*Nb*Nk*Nw*Nh (0
-                           for the atomic-sum instantiations).
+                           for the atomic-sum instantiations; the direct ones
+                           take kc = 1 and no workspace only).
                            cnn_plan_tiles picks the smallest kc with no empty
                            slice that gives at least two workgroups per CU,
                            else ceil(Nc/tc).  0 for the other kernels.        */
@@ -269,8 +273,9 @@ typedef struct cnn_variant_t {
   int32_t mode;         /* CNN_K_GEMM1: 0 stride 1, 1 strides 2, 2 whole-image
                            DMA ring; CNN_K_SROWS: output rows per band;
                            CNN_K_ROWS: 32-position blocks per input row;
-                           CNN_K_SPLITC: 1 for the atomic-sum (workspace-free)
-                           channel-slice instantiations; else 0          */
+                           CNN_K_SPLITC: 1 for the atomic-sum and 2 for the
+                           direct (both workspace-free) channel-slice
+                           instantiations; else 0                        */
   int64_t tk;           /* output features per workgroup                          */
   int64_t tp;           /* largest tile of outputs, 0 where the problem sets it   */
   int64_t tc;           /* input channels per stage, 0 = all; CNN_K_ROWS: the

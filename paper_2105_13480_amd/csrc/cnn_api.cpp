@@ -342,11 +342,12 @@ int run_plan(const void* In, const void* Ker, void* Out, const cnn_plan_t& pl, h
                  v->tp == pl.tp && v->tc == pl.tc && igemm_geometry_ok(*v, pl);
     if (!match)
       return fail(CNN_E_PLAN, "plan names no matching kernel instantiation (variant %d)", pl.variant);
-    const int64_t ws_want = vc && vc->atom ? 0 : 4LL * pl.kc * p.Nb * p.Nk * p.Nw * p.Nh;
-    if (pl.kc < 1 || pl.kc > stages || pl.kc > 65535 || pl.ws_bytes != ws_want)
+    const int64_t ws_want = vc && vc->mode ? 0 : 4LL * pl.kc * p.Nb * p.Nk * p.Nw * p.Nh;
+    if (pl.kc < 1 || pl.kc > stages || pl.kc > 65535 || pl.ws_bytes != ws_want ||
+        (vc && vc->mode == 2 && pl.kc != 1))
       return fail(CNN_E_PLAN,
                   "split plan needs 1 <= kc <= %lld and ws_bytes = 4*kc*|Out| "
-                  "(0 for the atomic-sum instantiations)",
+                  "(0 for the atomic-sum and direct instantiations; kc = 1 for the direct ones)",
                   (long long)stages);
     if (dry) return CNN_OK;
     e = vc ? launch_cslice(*vc, In, Ker, Out, ws, a, pl.lds_bytes, pl.kc, pl.dtype, st)

@@ -404,8 +404,12 @@ static FamilyCost family_cost(int kernel, int variant) {
     case CNN_K_SPLITC: {
       int n = 0;
       const VariantC* vc = variants_cslice(&n);
-      for (int i = 0; i < n; ++i)  // a stage's loads at once; atomic sums cost 1.3 us more
-        if (vc[i].id == variant) return {0.50, vc[i].atom ? 2.30 : 1.00, 1.50, 50.0};
+      // a stage's loads at once; atomic sums cost 1.3 us more; the direct
+      // form's 128-channel stages (one 1024-thread workgroup per CU) run
+      // about 5 us each, bound by one CU's outstanding requests
+      for (int i = 0; i < n; ++i)
+        if (vc[i].id == variant)
+          return {0.50, vc[i].mode == 1 ? 2.30 : 1.00, vc[i].mode == 2 ? 2.90 : 1.50, 50.0};
       return {0.51, 3.07, 1.65, 4.1};
     }
     case CNN_K_IGEMM: return {0.40, 0.00, 2.14, 3.4};
@@ -459,9 +463,9 @@ static double model_us(const cnn_plan_t& pl, const cnn_budget& bud, double w_out
       std::max(stage_flops / rate, fc.stage_us + stage_bytes / (fc.stage_gbs * 1e3));
   double t = std::ceil(per_cu / (double)occ) * (fc.wg_us + n_st * t_stage);
   t = std::max(t, pl.hbm_bytes / (hbm_gbs(w_out) * 1e3));
-  if (pl.kernel == CNN_K_SPLITC && pl.ws_bytes == 0)  // atomic sums: the zero fill of Out
+  if (pl.kernel == CNN_K_SPLITC && pl.ws_bytes == 0 && pl.kc > 1)  // atomic sums: zero fill
     t += kLaunchUs + 4.0 * n_out / (kFillGBs * 1e3);
-  else if (pl.kernel == CNN_K_SPLITC)  // the reduce pass: kc fp32 partials read, Out written
+  else if (pl.kernel == CNN_K_SPLITC && pl.ws_bytes > 0)  // the reduce: kc partials read, Out written
     t += kLaunchUs + 4.0 * (kc + 1.0) * n_out / (kHbmGBs * 1e3);
   return t + kLaunchUs;
 }
@@ -639,7 +643,11 @@ static bool eval_cslice(const cnn_problem& p, int dtype, const VariantC& v,
   const int64_t lds = cslice_lds_bytes(v, S, Ny);
   if (!eval_tiling(p, dtype, v.id, v.tk, v.tp, v.tc, 16, S, lds, 0, bud, plan)) return false;
   splitc_finish(p, bud, plan);
-  if (v.atom) plan->ws_bytes = 0;  // the slices add into Out
+  if (v.mode == 1) plan->ws_bytes = 0;  // the slices add into Out
+  if (v.mode == 2) {                     // one slice writing Out
+    plan->kc = 1;
+    plan->ws_bytes = 0;
+  }
   return true;
 }
 
@@ -927,7 +935,7 @@ int list_variants(cnn_variant_t* out, int cap) {
     add(CNN_K_SROWS, vq[i].id, vq[i].dtype, vq[i].nr, vq[i].ns, vq[i].L, vq[i].tk, 0, 16);
   const VariantC* vc = variants_cslice(&c);
   for (int i = 0; i < c; ++i)
-    add(CNN_K_SPLITC, vc[i].id, vc[i].dtype, vc[i].nr, vc[i].ns, vc[i].atom, vc[i].tk, vc[i].tp,
+    add(CNN_K_SPLITC, vc[i].id, vc[i].dtype, vc[i].nr, vc[i].ns, vc[i].mode, vc[i].tk, vc[i].tp,
         vc[i].tc);
   return n;
 }

@@ -231,15 +231,17 @@ hipError_t launch_splitc_reduce(const float* Part, void* Out, int kc, int64_t n,
 // A channel-slice instantiation (bf16, fixed stencil): tiles of tk = 32
 // features x tp = 64 outputs over one slice of the channels, tc = 32
 // channels per stage, every load of a stage in flight at once; fp32 partial
-// tiles in the workspace, then the ordered reduce (or, atom = 1, fp32 atomic
-// adds into Out after a zero fill: no workspace, fp32 Out only).  A
-// CNN_K_SPLITC family member beside the CNN_K_IGEMM split form.
+// tiles in the workspace, then the ordered reduce (mode 0); fp32 atomic
+// adds into Out after a zero fill (mode 1: no workspace, fp32 Out only); or
+// one slice (kc = 1) of 128-channel stages writing Out directly (mode 2: no
+// workspace, any Out type).  A CNN_K_SPLITC family member beside the
+// CNN_K_IGEMM split form.
 struct VariantC {
   int32_t id;
   int32_t dtype;
   int32_t tk, tp, tc;
   int32_t nr, ns;  // compile-time stencil
-  int32_t atom;    // 1: slices add into Out atomically (summation order varies)
+  int32_t mode;    // 0 partials + reduce; 1 atomic sums into Out (order varies); 2 direct, kc = 1
 };
 const VariantC* variants_cslice(int* count);
 int64_t cslice_lds_bytes(const VariantC& v, int64_t slab_rows, int64_t Ny);

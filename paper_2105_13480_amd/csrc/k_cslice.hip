@@ -36,11 +36,17 @@
 // (splitc_reduce) then writes Out, so the result does not depend on which
 // workgroup finishes first.
 //
-// Workspace-free instantiations (ATOM, fp32 Out): a fill kernel zeroes Out,
-// then every slice adds its partial tile into Out with fp32 atomic adds.
-// The sum is then formed in the order the workgroups arrive, so the last
-// bits of Out may differ from call to call (integer-valued sums excepted:
-// they are exact in any order).
+// Workspace-free instantiations:
+//   atomic (MODE 1, fp32 Out): a fill kernel zeroes Out, then every slice
+//     adds its partial tile into Out with fp32 atomic adds.  The sum is then
+//     formed in the order the workgroups arrive, so the last bits of Out may
+//     differ from call to call (integer-valued sums excepted: they are exact
+//     in any order);
+//   direct (MODE 2, any Out type): one slice (kc = 1) of 128-channel stages
+//     on 1024-thread workgroups (eight K groups), each workgroup walking all
+//     channels of its tile and writing Out itself, in a fixed order.  With
+//     128 channels the In staging spreads (position, 8-channel group) tasks
+//     over the threads instead of one position's groups per thread.
 #include "internal.h"
 #include "common.h"
 
@@ -75,10 +81,12 @@ template <int TC> struct CsliceShape {
   static constexpr int NT = 128 * NK;                // threads
 };
 
-template <int NR, int NS, int TC, bool ATOM>
+// MODE 0: fp32 partial tiles to slice z of Dst (the workspace); 1: fp32
+// atomic adds into Dst (Out, zeroed); 2: TO values into Dst (Out), kc = 1.
+template <int NR, int NS, int TC, int MODE, typename TO>
 __global__ __launch_bounds__(CsliceShape<TC>::NT) void conv_cslice(const bf16_t* __restrict__ In,
                                                    const bf16_t* __restrict__ Ker,
-                                                   float* __restrict__ Part, ConvArgs a, int cs,
+                                                   void* __restrict__ Dst, ConvArgs a, int cs,
                                                    FastDiv dv_nxny) {
   constexpr int T = NR * NS;
   constexpr int kTC = TC;          // channels per stage (16, 32 or 64)
@@ -137,7 +145,8 @@ __global__ __launch_bounds__(CsliceShape<TC>::NT) void conv_cslice(const bf16_t*
   const int c_end = min(a.Nc, c_begin + cs);
   for (int c0 = c_begin; c0 < c_end; c0 += kTC) {
     const int ncg = min(kTC, c_end - c0) >> 3;  // even (Nc and cs are multiples of 16)
-    static_assert(kTC == 16 || kTC == 32 || kTC == 64, "stages of 16, 32 or 64 channels");
+    static_assert(kTC == 16 || kTC == 32 || kTC == 64 || kTC == 128,
+                  "stages of 16, 32, 64 or 128 channels");
     // Every global load of the stage, Ker first.
     u32x4_t kr[T];
     const bool kload = ktask && kcg < ncg;
@@ -146,6 +155,36 @@ __global__ __launch_bounds__(CsliceShape<TC>::NT) void conv_cslice(const bf16_t*
 #pragma unroll
       for (int t = 0; t < T; ++t) kr[t] = src[t];
     }
+    if constexpr (kCG > 8) {
+      // (position, group) tasks, positions fastest: idx = g * SNt + pos.
+      const int ntask = SNt * kCG;
+      for (int base = 0; base < ntask; base += 2 * NT) {
+        uint32_t iv[2][8];
+        int tpos[2], tg[2];
+#pragma unroll
+        for (int m = 0; m < 2; ++m) {
+          const int idx = base + m * NT + tid;
+          tg[m] = idx / SNt;
+          tpos[m] = idx - tg[m] * SNt;
+          if (idx < ntask && tg[m] < ncg) {
+            const int gp = gpos0 + tpos[m];
+            const int b = fdiv(gp, dv_nxny);
+            const bf16_t* src = In + (int64_t)b * a.in_img + (int64_t)(c0 + 8 * tg[m]) * a.nxny +
+                                (gp - b * a.nxny);
+#pragma unroll
+            for (int i = 0; i < 8; ++i) iv[m][i] = src[(int64_t)i * a.nxny];
+          }
+        }
+#pragma unroll
+        for (int m = 0; m < 2; ++m)
+          if (base + m * NT + tid < ntask && tg[m] < ncg) {
+            u32x4_t v;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) v[q] = iv[m][2 * q] | (iv[m][2 * q + 1] << 16);
+            il[tpos[m] * kIPV + tg[m]] = v;
+          }
+      }
+    } else
     for (int base = 0; base < SNt; base += NT) {
       const int pos = base + tid;
       if (pos < SNt) {
@@ -217,7 +256,7 @@ __global__ __launch_bounds__(CsliceShape<TC>::NT) void conv_cslice(const bf16_t*
   }
   __syncthreads();
   if (kh == 0) {
-    float* dst = ATOM ? Part : Part + (int64_t)blockIdx.y * a.out_total;
+    float* dst = static_cast<float*>(Dst) + (MODE == 0 ? (int64_t)blockIdx.y * a.out_total : 0);
 #pragma unroll
     for (int j = 0; j < 16; ++j) {
       const int k = k0 + 8 * (j >> 2) + 4 * half + (j & 3);
@@ -225,8 +264,10 @@ __global__ __launch_bounds__(CsliceShape<TC>::NT) void conv_cslice(const bf16_t*
 #pragma unroll
       for (int g = 1; g < NK; ++g) v += red[(((g - 1) * 2 + pb) * 16 + j) * 64 + lane];
       if (pval && k < a.Nk) {
-        if (ATOM)
+        if constexpr (MODE == 1)
           unsafeAtomicAdd(dst + obase + (int64_t)k * a.hw, v);  // hardware fp32 add
+        else if constexpr (MODE == 2)
+          static_cast<TO*>(Dst)[obase + (int64_t)k * a.hw] = from_f32<TO>(v);
         else
           dst[obase + (int64_t)k * a.hw] = v;
       }
@@ -235,9 +276,10 @@ __global__ __launch_bounds__(CsliceShape<TC>::NT) void conv_cslice(const bf16_t*
 }
 
 // ---- instantiation table ------------------------------------------------
-// X(id, dtype, Nr, Ns, tc, atom): the kernel is the same for both bf16
-// dtypes (the partials are fp32; the reduce writes the Out type); the
-// atomic-sum instantiations need fp32 Out.
+// X(id, dtype, Nr, Ns, tc, mode): mode 0 (partials and the ordered reduce)
+// is the same kernel for both bf16 dtypes (the reduce writes the Out type);
+// mode 1 (atomic sums) needs fp32 Out; mode 2 (direct, kc = 1) writes the
+// dtype's Out type.
 #define CNN_CSLICE_VARIANTS(X)           \
   X(2500, CNN_BF16, 3, 3, 32, 0)         \
   X(2501, CNN_BF16_OBF16, 3, 3, 32, 0)   \
@@ -248,10 +290,12 @@ __global__ __launch_bounds__(CsliceShape<TC>::NT) void conv_cslice(const bf16_t*
   X(2506, CNN_BF16, 3, 3, 64, 0)         \
   X(2507, CNN_BF16_OBF16, 3, 3, 64, 0)   \
   X(2508, CNN_BF16, 3, 3, 32, 1)         \
-  X(2509, CNN_BF16, 1, 1, 32, 1)
+  X(2509, CNN_BF16, 1, 1, 32, 1)         \
+  X(2510, CNN_BF16, 3, 3, 128, 2)        \
+  X(2511, CNN_BF16_OBF16, 3, 3, 128, 2)
 
 static const VariantC kVariantsC[] = {
-#define CNN_ROW(id, dt, nr, ns, tc, atom) {id, dt, kTK, kTP, tc, nr, ns, atom},
+#define CNN_ROW(id, dt, nr, ns, tc, mode) {id, dt, kTK, kTP, tc, nr, ns, mode},
     CNN_CSLICE_VARIANTS(CNN_ROW)
 #undef CNN_ROW
 };
@@ -279,15 +323,20 @@ __global__ __launch_bounds__(256) void cslice_zero(float* __restrict__ Out, int6
   for (int64_t o = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; o < n; o += stride) Out[o] = 0.f;
 }
 
-// ws: the partial slices, or (ATOM) Out itself, zeroed first.
-template <int NR, int NS, int TC, bool ATOM>
-static hipError_t launch_one_c(const void* In, const void* Ker, void* ws, const ConvArgs& a,
+// Out element type of an instantiation: fp32 except the direct form of
+// the bf16-Out dtype.
+template <int DT, int MODE> struct CsliceOut { typedef float T; };
+template <> struct CsliceOut<CNN_BF16_OBF16, 2> { typedef bf16_t T; };
+
+// dst: the partial slices (mode 0), or Out itself (mode 1: zeroed first).
+template <int NR, int NS, int TC, int MODE, typename TO>
+static hipError_t launch_one_c(const void* In, const void* Ker, void* dst, const ConvArgs& a,
                                int64_t lds, int kc, int cs, hipStream_t stream) {
-  auto kern = conv_cslice<NR, NS, TC, ATOM>;
-  if (ATOM) {
+  auto kern = conv_cslice<NR, NS, TC, MODE, TO>;
+  if (MODE == 1) {
     int64_t blocks = (a.out_total + 255) / 256;
     if (blocks > 2048) blocks = 2048;  // grid-stride loop covers the rest
-    hipLaunchKernelGGL(cslice_zero, dim3((unsigned)blocks), dim3(256), 0, stream, (float*)ws,
+    hipLaunchKernelGGL(cslice_zero, dim3((unsigned)blocks), dim3(256), 0, stream, (float*)dst,
                        a.out_total);
   }
   if (lds > 64 * 1024) {
@@ -296,7 +345,7 @@ static hipError_t launch_one_c(const void* In, const void* Ker, void* ws, const 
   }
   hipLaunchKernelGGL(kern, dim3((unsigned)a.grid, (unsigned)kc), dim3(CsliceShape<TC>::NT),
                      (unsigned)lds,
-                     stream, (const bf16_t*)In, (const bf16_t*)Ker, (float*)ws, a, cs,
+                     stream, (const bf16_t*)In, (const bf16_t*)Ker, dst, a, cs,
                      make_fastdiv((uint32_t)a.nxny));
   return hipGetLastError();
 }
@@ -307,17 +356,17 @@ hipError_t launch_cslice(const VariantC& v, const void* In, const void* Ker, voi
   const int cs = (int)splitc_slice_channels(a.Nc, v.tc, kc);
   hipError_t e;
   switch (v.id) {
-#define CNN_CASE(id, dt, nr, ns, tc, atom)                                          \
-  case id:                                                                           \
-    e = launch_one_c<nr, ns, tc, atom>(In, Ker, atom ? Out : ws, a, lds_bytes, kc, cs, \
-                                       stream);                                      \
+#define CNN_CASE(id, dt, nr, ns, tc, mode)                                              \
+  case id:                                                                               \
+    e = launch_one_c<nr, ns, tc, mode, CsliceOut<dt, mode>::T>(In, Ker, mode ? Out : ws, a, \
+                                                               lds_bytes, kc, cs, stream); \
     break;
     CNN_CSLICE_VARIANTS(CNN_CASE)
 #undef CNN_CASE
     default:
       return hipErrorInvalidValue;
   }
-  if (e != hipSuccess || v.atom) return e;
+  if (e != hipSuccess || v.mode) return e;
   return launch_splitc_reduce((const float*)ws, Out, kc, a.out_total, dtype, stream);
 }
 

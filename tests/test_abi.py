@@ -417,9 +417,10 @@ def test_channel_slice_plans():
     free = cnn.plan_tiles(p, cnn.CNN_BF16, cnn.K_AUTO_NO_WORKSPACE, 0, 0, 0, bud)
     assert (free.kernel, free.variant, free.kc, free.ws_bytes) == (cnn.K_SPLITC, 2508, 16, 0)
     assert free.model_us > ws.model_us
-    # bf16 Out has no atomic form: its workspace-free plan is another family
+    # bf16 Out has no atomic form: its workspace-free plan is the direct one
+    # (one slice of 128-channel stages)
     free_b = cnn.plan_tiles(p, cnn.CNN_BF16_OBF16, cnn.K_AUTO_NO_WORKSPACE, 0, 0, 0, bud)
-    assert free_b.kernel != cnn.K_SPLITC
+    assert (free_b.kernel, free_b.variant, free_b.kc, free_b.ws_bytes) == (cnn.K_SPLITC, 2511, 1, 0)
     L = cnn.lib()
     for pl, bad_ws in [(free, 4 * 16 * 512 * 49), (ws, 0)]:
         q = cnn.Plan.from_buffer_copy(pl)

@@ -553,6 +553,45 @@ def test_cslice_exact(dims, tc, mode):
         assert np.array_equal(got, want), kc
 
 
+@pytest.mark.parametrize("dims", [d for d in CSLICE_CASES if d[5] == 3])
+@pytest.mark.parametrize("mode", ["bf16", "bf16_obf16"])
+def test_cslice_direct_exact(dims, mode):
+    """Direct channel-slice form (one slice of 128-channel stages, 1024
+    threads, Out written by the slice itself, no workspace): bit-exact with
+    the oracle on integer inputs, ragged last stages (Nc = 48, 80, 96)
+    included; a slice count other than 1 is refused before HIP."""
+    Nb, Nc, Nk, Nw, Nh, Nr, Ns, sw, sh = dims
+    In, Ker = _arrays(dims, mode, seed=sum(dims) + 13, dist=("int", -3, 3), kdist=("int", -3, 3))
+    want = oracle.conv(In, Ker, sw, sh)
+    if mode == "bf16_obf16":
+        want = inputs.bf16_bits_to_f32(inputs.f32_to_bf16_bits(want.astype(np.float32))).astype(np.float64)
+    pl = cnn.plan_tiles(cnn.problem(*dims), MODES[mode], cnn.K_SPLITC, 32, 64, 128)
+    assert pl.variant in (2510, 2511) and pl.kc == 1 and pl.ws_bytes == 0
+    say(f"[parity] cslice direct dims={dims} mode={mode} v{pl.variant} grid={pl.grid}")
+    got = run(In, Ker, sw, sh, mode, plan=pl)
+    assert np.array_equal(got, want)
+    if -(-Nc // 128) > 1:
+        q = cnn.Plan.from_buffer_copy(pl)
+        q.kc = 2
+        with pytest.raises(cnn.CnnError):
+            run(In, Ker, sw, sh, mode, plan=q)
+
+
+def test_cslice_direct_is_the_workspace_free_bf16_out_late_layer_plan():
+    """cnn_fwd's plan for the batch-1 deep layer with bf16 Out (no fp32
+    atomic target) is the direct channel-slice form, within the bf16-Out
+    tolerance of the fp64 oracle."""
+    w = inputs.BY_NAME["late3x3_b1"]
+    In, Ker = inputs.make_inputs(w)
+    pl = cnn.plan_tiles(cnn.problem(*w.dims()), cnn.CNN_BF16_OBF16, cnn.K_AUTO_NO_WORKSPACE)
+    assert pl.kernel == cnn.K_SPLITC and pl.variant == 2511 and pl.ws_bytes == 0
+    say("[parity] cnn_fwd late3x3_b1 bf16 Out (direct channel slices)")
+    got = run(In, Ker, 1, 1, "bf16_obf16", plan=pl)
+    want, absv = oracle.conv(In, Ker, 1, 1, with_abs=True)
+    nw, cond, _ = errors(got, want, absv)
+    assert nw < TOL["bf16_obf16"] and cond < TOL["bf16_obf16"], (nw, cond)
+
+
 @pytest.mark.parametrize("dims", CSLICE_CASES)
 def test_cslice_atomic_exact(dims):
     """Workspace-free channel slices (atomic adds into a zeroed fp32 Out):
