@@ -638,6 +638,30 @@ def test_cslice_atomic_in_graph():
         assert np.array_equal(to_host64(out), want), i
 
 
+# batch-1 deep layers beyond the benchmark workloads (1x1 2048 -> 512 and
+# 512 -> 2048, 1x1 at 14x14, 3x3 at 14x14, 3x3 at batch 2): the model's plan
+# (channel slices with a workspace) and cnn_fwd's workspace-free plan
+DEEP_B1 = [(1, 2048, 512, 7, 7, 1, 1, 1, 1), (1, 512, 2048, 7, 7, 1, 1, 1, 1),
+           (1, 1024, 256, 14, 14, 1, 1, 1, 1), (1, 256, 256, 14, 14, 3, 3, 1, 1),
+           (2, 512, 512, 7, 7, 3, 3, 1, 1)]
+
+
+@pytest.mark.parametrize("dims", DEEP_B1)
+@pytest.mark.parametrize("mode", ["bf16", "bf16_obf16"])
+def test_batch1_deep_layers(dims, mode):
+    """Every output of the model's plan and of cnn_fwd within the tolerance
+    of the fp64 oracle on uniform inputs and He-normal Ker."""
+    In, Ker = _arrays(dims, mode, seed=sum(dims) + 3)
+    want, absv = oracle.conv(In, Ker, dims[7], dims[8], with_abs=True)
+    pl = cnn.plan(cnn.problem(*dims), MODES[mode])
+    for tag, plan in (("model", pl), ("cnn_fwd", None)):
+        say(f"[parity] deep batch-1 dims={dims} mode={mode} {tag} "
+            f"{'v%d kc=%d' % (pl.variant, pl.kc) if plan else ''}")
+        got = run(In, Ker, dims[7], dims[8], mode, plan=plan)
+        nw, cond, _ = errors(got, want, absv)
+        assert nw < TOL[mode] and cond < TOL[mode], (tag, nw, cond)
+
+
 def test_cslice_atomic_is_the_workspace_free_late_layer_plan():
     """cnn_fwd's plan for the batch-1 deep layer (no workspace) is the atomic
     channel-slice one, within the bf16 tolerance of the fp64 oracle."""
