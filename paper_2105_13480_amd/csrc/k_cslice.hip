@@ -6,13 +6,13 @@
 //
 // Workgroup (tile, z) owns 32 output features x 64 consecutive outputs of the
 // flattened (b, w, h) index (the paper's composite T_bhw) and the channels
-// [z*cs, z*cs + cs) of slice z, in stages of TC = 16, 32 or 64 channels.  A
-// stage issues all of its global loads before it waits on any: the tile's
-// Ker rows (32 features x TC channels x all taps, 16-byte loads of the rows
-// as they lie, one feature's 8 channels per thread) and the halo'd In slab
-// of the tile (one position's 8-channel groups per thread).  The stage therefore costs
-// one memory latency rather than one per tap or channel group.  Both then go
-// to LDS in (tap, channel) order:
+// [z*cs, z*cs + cs) of slice z, in stages of TC = 16, 32, 64 or 128
+// channels.  A stage issues all of its global loads before it waits on any:
+// the tile's Ker rows (32 features x TC channels x all taps, 16-byte loads of
+// the rows as they lie, one feature's 8 channels per thread) and the halo'd
+// In slab of the tile (one position's 8-channel groups per thread).  The
+// stage therefore costs one memory latency rather than one per tap or
+// channel group.  Both then go to LDS in (tap, channel) order:
 //   Ker [tap][c/8][k (+1)][8]    an A operand (8 channels of one feature at
 //                                one tap) is one 16-byte read; one pad
 //                                vector per 32 features keeps the four
@@ -89,7 +89,7 @@ __global__ __launch_bounds__(CsliceShape<TC>::NT) void conv_cslice(const bf16_t*
                                                    void* __restrict__ Dst, ConvArgs a, int cs,
                                                    FastDiv dv_nxny) {
   constexpr int T = NR * NS;
-  constexpr int kTC = TC;          // channels per stage (16, 32 or 64)
+  constexpr int kTC = TC;          // channels per stage (16, 32, 64 or 128)
   constexpr int kCG = kTC / 8;     // 8-channel groups per stage
   constexpr int kIPV = kCG + 1;    // 16-byte vectors per In position in LDS (one pad)
   constexpr int NK = CsliceShape<TC>::NK, NT = CsliceShape<TC>::NT;
@@ -130,9 +130,9 @@ __global__ __launch_bounds__(CsliceShape<TC>::NT) void conv_cslice(const bf16_t*
     obase = (int64_t)b * a.Nk * a.hw + q;
   }
 
-  // Ker task of this thread (threads 0 .. 4*TC - 1): feature k0 + kk, its channel
-  // group kcg of every stage.  Features past Nk stage nothing; their LDS rows
-  // feed accumulator rows that are not stored.
+  // Ker task of this thread (threads 0 .. 4*TC - 1): feature k0 + kk, its
+  // channel group kcg of every stage.  Features past Nk stage nothing; their
+  // LDS rows feed only accumulator rows that are not stored.
   const int kk = tid / kCG, kcg = tid % kCG;
   const bool ktask = tid < kTK * kCG && k0 + kk < a.Nk;
   const bf16_t* krow = Ker + ((int64_t)min(k0 + kk, a.Nk - 1) * a.Nc + 8 * kcg) * T;
@@ -184,29 +184,31 @@ __global__ __launch_bounds__(CsliceShape<TC>::NT) void conv_cslice(const bf16_t*
             il[tpos[m] * kIPV + tg[m]] = v;
           }
       }
-    } else
-    for (int base = 0; base < SNt; base += NT) {
-      const int pos = base + tid;
-      if (pos < SNt) {
-        const int gp = gpos0 + pos;
-        const int b = fdiv(gp, dv_nxny);
-        const bf16_t* src =
-            In + (int64_t)b * a.in_img + (int64_t)c0 * a.nxny + (gp - b * a.nxny);
-        uint32_t iv[kCG][8];
+    } else {
+      // one position's groups per thread, positions fastest
+      for (int base = 0; base < SNt; base += NT) {
+        const int pos = base + tid;
+        if (pos < SNt) {
+          const int gp = gpos0 + pos;
+          const int b = fdiv(gp, dv_nxny);
+          const bf16_t* src =
+              In + (int64_t)b * a.in_img + (int64_t)c0 * a.nxny + (gp - b * a.nxny);
+          uint32_t iv[kCG][8];
 #pragma unroll
-        for (int g = 0; g < kCG; ++g)
-          if (g < ncg) {
+          for (int g = 0; g < kCG; ++g)
+            if (g < ncg) {
 #pragma unroll
-            for (int i = 0; i < 8; ++i) iv[g][i] = src[(int64_t)(8 * g + i) * a.nxny];
-          }
+              for (int i = 0; i < 8; ++i) iv[g][i] = src[(int64_t)(8 * g + i) * a.nxny];
+            }
 #pragma unroll
-        for (int g = 0; g < kCG; ++g)
-          if (g < ncg) {
-            u32x4_t v;
+          for (int g = 0; g < kCG; ++g)
+            if (g < ncg) {
+              u32x4_t v;
 #pragma unroll
-            for (int m = 0; m < 4; ++m) v[m] = iv[g][2 * m] | (iv[g][2 * m + 1] << 16);
-            il[pos * kIPV + g] = v;
-          }
+              for (int m = 0; m < 4; ++m) v[m] = iv[g][2 * m] | (iv[g][2 * m + 1] << 16);
+              il[pos * kIPV + g] = v;
+            }
+        }
       }
     }
     if (kload) {
@@ -328,20 +330,21 @@ __global__ __launch_bounds__(256) void cslice_zero(float* __restrict__ Out, int6
 template <int DT, int MODE> struct CsliceOut { typedef float T; };
 template <> struct CsliceOut<CNN_BF16_OBF16, 2> { typedef bf16_t T; };
 
-// dst: the partial slices (mode 0), or Out itself (mode 1: zeroed first).
+// dst: the partial slices (mode 0), or Out itself (mode 1: zeroed first;
+// mode 2: written once).
 template <int NR, int NS, int TC, int MODE, typename TO>
 static hipError_t launch_one_c(const void* In, const void* Ker, void* dst, const ConvArgs& a,
                                int64_t lds, int kc, int cs, hipStream_t stream) {
   auto kern = conv_cslice<NR, NS, TC, MODE, TO>;
+  if (lds > 64 * 1024) {
+    const hipError_t e = allow_max_lds((const void*)kern);
+    if (e != hipSuccess) return e;
+  }
   if (MODE == 1) {
     int64_t blocks = (a.out_total + 255) / 256;
     if (blocks > 2048) blocks = 2048;  // grid-stride loop covers the rest
     hipLaunchKernelGGL(cslice_zero, dim3((unsigned)blocks), dim3(256), 0, stream, (float*)dst,
                        a.out_total);
-  }
-  if (lds > 64 * 1024) {
-    const hipError_t e = allow_max_lds((const void*)kern);
-    if (e != hipSuccess) return e;
   }
   hipLaunchKernelGGL(kern, dim3((unsigned)a.grid, (unsigned)kc), dim3(CsliceShape<TC>::NT),
                      (unsigned)lds,
