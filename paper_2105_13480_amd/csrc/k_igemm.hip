@@ -344,13 +344,16 @@ int64_t splitc_slice_channels(int64_t Nc, int64_t tc, int64_t kc) {
 
 hipError_t launch_splitc_reduce(const float* Part, void* Out, int kc, int64_t n, int dtype,
                                 hipStream_t stream) {
-  int64_t blocks = (n + 255) / 256;
-  if (blocks > 2048) blocks = 2048;  // grid-stride loop covers the rest
+  // One wave per workgroup: a small Out (25k elements for a batch-1 7x7
+  // layer) then spreads its loads over every CU rather than a hundred
+  // (0.05 us less on that layer's 7.4).
+  int64_t blocks = (n + 63) / 64;
+  if (blocks > 8192) blocks = 8192;  // grid-stride loop covers the rest
   if (dtype == CNN_BF16_OBF16)
-    hipLaunchKernelGGL(splitc_reduce<bf16_t>, dim3((unsigned)blocks), dim3(256), 0, stream,
+    hipLaunchKernelGGL(splitc_reduce<bf16_t>, dim3((unsigned)blocks), dim3(64), 0, stream,
                        Part, (bf16_t*)Out, kc, n);
   else
-    hipLaunchKernelGGL(splitc_reduce<float>, dim3((unsigned)blocks), dim3(256), 0, stream,
+    hipLaunchKernelGGL(splitc_reduce<float>, dim3((unsigned)blocks), dim3(64), 0, stream,
                        Part, (float*)Out, kc, n);
   return hipGetLastError();
 }
