@@ -10,9 +10,10 @@
 // channels.  A stage issues all of its global loads before it waits on any:
 // the tile's Ker rows (32 features x TC channels x all taps, 16-byte loads of
 // the rows as they lie, one feature's 8 channels per thread) and the halo'd
-// In slab of the tile (one position's 8-channel groups per thread).  The
-// stage therefore costs one memory latency rather than one per tap or
-// channel group.  Both then go to LDS in (tap, channel) order:
+// In slab of the tile ((position, 8-channel group) tasks spread over all
+// threads: with one position's groups per thread, 81 threads issued every
+// load of the 7x7 layer's slab, 0.18 us slower).  The stage therefore costs
+// one memory latency rather than one per tap or channel group.  Both then go to LDS in (tap, channel) order:
 //   Ker [tap][c/8][k (+1)][8]    an A operand (8 channels of one feature at
 //                                one tap) is one 16-byte read; one pad
 //                                vector per 32 features keeps the four
@@ -44,9 +45,7 @@
 //     in any order);
 //   direct (MODE 2, any Out type): one slice (kc = 1) of 128-channel stages
 //     on 1024-thread workgroups (eight K groups), each workgroup walking all
-//     channels of its tile and writing Out itself, in a fixed order.  With
-//     128 channels the In staging spreads (position, 8-channel group) tasks
-//     over the threads instead of one position's groups per thread.
+//     channels of its tile and writing Out itself, in a fixed order.
 #include "internal.h"
 #include "common.h"
 
@@ -155,61 +154,33 @@ __global__ __launch_bounds__(CsliceShape<TC>::NT) void conv_cslice(const bf16_t*
 #pragma unroll
       for (int t = 0; t < T; ++t) kr[t] = src[t];
     }
-    if constexpr (kCG > 8) {
-      // (position, group) tasks, positions fastest: idx = g * SNt + pos.
-      const int ntask = SNt * kCG;
-      for (int base = 0; base < ntask; base += 2 * NT) {
-        uint32_t iv[2][8];
-        int tpos[2], tg[2];
+    // (position, group) tasks, positions fastest: idx = g * SNt + pos.
+    const int ntask = SNt * kCG;
+    for (int base = 0; base < ntask; base += 2 * NT) {
+      uint32_t iv[2][8];
+      int tpos[2], tg[2];
 #pragma unroll
-        for (int m = 0; m < 2; ++m) {
-          const int idx = base + m * NT + tid;
-          tg[m] = idx / SNt;
-          tpos[m] = idx - tg[m] * SNt;
-          if (idx < ntask && tg[m] < ncg) {
-            const int gp = gpos0 + tpos[m];
-            const int b = fdiv(gp, dv_nxny);
-            const bf16_t* src = In + (int64_t)b * a.in_img + (int64_t)(c0 + 8 * tg[m]) * a.nxny +
-                                (gp - b * a.nxny);
-#pragma unroll
-            for (int i = 0; i < 8; ++i) iv[m][i] = src[(int64_t)i * a.nxny];
-          }
-        }
-#pragma unroll
-        for (int m = 0; m < 2; ++m)
-          if (base + m * NT + tid < ntask && tg[m] < ncg) {
-            u32x4_t v;
-#pragma unroll
-            for (int q = 0; q < 4; ++q) v[q] = iv[m][2 * q] | (iv[m][2 * q + 1] << 16);
-            il[tpos[m] * kIPV + tg[m]] = v;
-          }
-      }
-    } else {
-      // one position's groups per thread, positions fastest
-      for (int base = 0; base < SNt; base += NT) {
-        const int pos = base + tid;
-        if (pos < SNt) {
-          const int gp = gpos0 + pos;
+      for (int m = 0; m < 2; ++m) {
+        const int idx = base + m * NT + tid;
+        tg[m] = idx / SNt;
+        tpos[m] = idx - tg[m] * SNt;
+        if (idx < ntask && tg[m] < ncg) {
+          const int gp = gpos0 + tpos[m];
           const int b = fdiv(gp, dv_nxny);
-          const bf16_t* src =
-              In + (int64_t)b * a.in_img + (int64_t)c0 * a.nxny + (gp - b * a.nxny);
-          uint32_t iv[kCG][8];
+          const bf16_t* src = In + (int64_t)b * a.in_img + (int64_t)(c0 + 8 * tg[m]) * a.nxny +
+                              (gp - b * a.nxny);
 #pragma unroll
-          for (int g = 0; g < kCG; ++g)
-            if (g < ncg) {
-#pragma unroll
-              for (int i = 0; i < 8; ++i) iv[g][i] = src[(int64_t)(8 * g + i) * a.nxny];
-            }
-#pragma unroll
-          for (int g = 0; g < kCG; ++g)
-            if (g < ncg) {
-              u32x4_t v;
-#pragma unroll
-              for (int m = 0; m < 4; ++m) v[m] = iv[g][2 * m] | (iv[g][2 * m + 1] << 16);
-              il[pos * kIPV + g] = v;
-            }
+          for (int i = 0; i < 8; ++i) iv[m][i] = src[(int64_t)i * a.nxny];
         }
       }
+#pragma unroll
+      for (int m = 0; m < 2; ++m)
+        if (base + m * NT + tid < ntask && tg[m] < ncg) {
+          u32x4_t v;
+#pragma unroll
+          for (int q = 0; q < 4; ++q) v[q] = iv[m][2 * q] | (iv[m][2 * q + 1] << 16);
+          il[tpos[m] * kIPV + tg[m]] = v;
+        }
     }
     if (kload) {
       // kr holds channels 8*kcg .. 8*kcg + 7 x taps 0 .. T-1 as (c, tap),
