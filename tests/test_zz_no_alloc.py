@@ -21,6 +21,7 @@ CASES = [
     ((1, 512, 512, 7, 7, 3, 3, 1, 1), (1, 256, 128, 7, 7, 3, 3, 1, 1), "bf16", cnn.K_SPLITC, 32, 256, 32),
     ((1, 16, 16, 16, 16, 3, 3, 1, 1), (1, 16, 8, 9, 5, 3, 3, 1, 1), "f32", cnn.K_SPLITC, 64, 64, 8),
     ((2, 32, 300, 7, 28, 3, 3, 2, 2), (1, 16, 64, 7, 28, 3, 3, 2, 2), "bf16_obf16", cnn.K_SROWS, 256, 7 * 28, 16),
+    ((1, 512, 512, 7, 7, 3, 3, 1, 1), (1, 96, 70, 7, 7, 3, 3, 1, 1), "bf16_obf16", cnn.K_SPLITC, 32, 64, 32),
 ]
 
 
